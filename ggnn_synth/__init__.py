@@ -1,0 +1,13 @@
+"""Seeded synthetic inputs for the banded GGNN propagation path.
+
+This package only draws random graphs, node scrambles and parameter tensors.
+It holds none of the method's arithmetic (no reordering, no packing, no
+propagation): both the GPU path and the CPU oracle take its outputs as inputs.
+"""
+from .graphs import (  # noqa: F401
+    Graph, rng_for, local_window_graph, backbone_graph, scramble_graph,
+    lognormal_batch_sizes, STREAM_SIZES, STREAM_EDGES, STREAM_SCRAMBLE,
+    STREAM_X, STREAM_W, STREAM_GRU, STREAM_G,
+)
+from .params import draw_params, round_bf16, Params  # noqa: F401
+from .configs import CONFIGS, ConfigSpec, make_graphs, sweep_blocks  # noqa: F401
