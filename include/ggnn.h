@@ -1,0 +1,270 @@
+/*
+ * ggnn.h -- C ABI of the banded gated-GNN propagation library for AMD MI355X
+ * (gfx950).
+ *
+ * The library implements one step of gated graph neural network propagation
+ * (Balog et al., "Fast Training of Sparse Graph Neural Networks on Dense
+ * Hardware", arXiv 1906.11786; Eq. 1 and its typed form) on a graph whose
+ * nodes were reordered to low bandwidth (Compilation section, reverse
+ * Cuthill-McKee) and whose per-edge-type adjacency A_e is stored as three
+ * block diagonals of B x B blocks (Eq. 3, Algorithm 1).  A_e M is then three
+ * batched dense block products, cost O(N B H) instead of O(N^2 H).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - An edge is (src j, dst i, type e): node i receives from node j, i.e.
+ *    a_ij = 1 in the transposed adjacency matrix A_e (Background, Eq. 1).
+ *  - All tensors are dense, contiguous, row-major, with no strides, and
+ *    16-byte aligned.  Shapes are written outermost first.
+ *  - Node-major tensors are [n_pad][F]; feature-major tensors are [F][n_pad]
+ *    (feature f of node i at f * n_pad + i).
+ *  - "dt" tensors hold the compute dtype: IEEE float32 (GGNN_F32) or bfloat16
+ *    (GGNN_BF16, round-to-nearest-even on every store).  Accumulation is
+ *    always float32.  Tensors documented as "float" are float32 for both.
+ *  - Ownership: the caller allocates and frees everything.  The library never
+ *    allocates or frees device memory, never synchronises a stream, and never
+ *    keeps a pointer after a call returns.
+ *  - Device entry points are asynchronous: every argument is validated on
+ *    the host before anything is enqueued, then kernels are launched on
+ *    `stream` (a hipStream_t; NULL is the null stream).  They issue no
+ *    hipMemsetAsync and no allocation, so they can be captured into a HIP
+ *    graph.  A launch error reported by hipGetLastError is GGNN_ERR_DEVICE.
+ *  - Errors: a non-OK status leaves a message retrievable with
+ *    ggnn_last_error() on the calling thread.  Nothing throws across the ABI.
+ *  - Supported sizes for device work: B in {32, 64, 128, 256, 512},
+ *    H in {32, 64, 128, 256}, 1 <= E <= 64, n_pad a positive multiple of B
+ *    (and of 32 for the node-wise calls, which take no B).
+ *  - Results are deterministic: no float atomics; cross-block reductions use a
+ *    fixed partition and a fixed summation order.
+ */
+#ifndef GGNN_H
+#define GGNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GGNN_ABI_VERSION 1
+
+typedef enum {
+  GGNN_OK = 0,
+  GGNN_ERR_INVALID_ARG = 1,  /* bad size, NULL pointer, id out of range       */
+  GGNN_ERR_UNSUPPORTED = 2,  /* valid arguments with no kernel for them       */
+  GGNN_ERR_OUT_OF_BAND = 3,  /* strict packing met an edge outside the band   */
+  GGNN_ERR_DEVICE = 4,       /* HIP launch or runtime error                   */
+  GGNN_ERR_HOST_ALLOC = 5,   /* host-side temporary allocation failed         */
+  GGNN_ERR_WORKSPACE = 6     /* workspace missing or smaller than required    */
+} ggnn_status;
+
+typedef enum { GGNN_F32 = 0, GGNN_BF16 = 1 } ggnn_dtype;
+
+/* Version of this ABI (GGNN_ABI_VERSION of the built library). */
+int ggnn_abi_version(void);
+
+/* Text of the last non-OK status raised on the calling thread ("" if none).
+ * The pointer stays valid until the next library call on that thread. */
+const char* ggnn_last_error(void);
+
+/* Short fixed name of a status code. */
+const char* ggnn_status_string(ggnn_status s);
+
+/* ======================================================================
+ * Host-side graph compilation (synchronous, host memory only)
+ * ====================================================================== */
+
+/* Reverse Cuthill-McKee node order (Compilation section: permute the nodes
+ * to expose low bandwidth; the bandwidth is defined in the Background
+ * section).  The graph is the union of all edge types, symmetrised, with
+ * self-loops and repeated pairs ignored.  Components are taken in order of
+ * their smallest label; each starts at a pseudo-peripheral node found by the
+ * George-Liu iteration from its node of smallest (degree, label); the
+ * breadth-first search appends unvisited neighbours by increasing
+ * (degree, label); the whole sequence is reversed.
+ *   n          number of nodes (>= 0); m number of edges (>= 0)
+ *   src, dst   [m] node ids in [0, n)
+ *   order      [n] out: order[p] = old label placed at new position p
+ *   rank       [n] out: rank[v] = new position of old label v
+ *   bandwidth  nullable out: max |rank[src] - rank[dst]| over the edges
+ * Errors: INVALID_ARG for negative sizes, NULL arrays (when n or m > 0) or
+ * ids out of range; HOST_ALLOC if temporaries cannot be allocated. */
+ggnn_status ggnn_rcm_order(int32_t n, int64_t m, const int32_t* src, const int32_t* dst,
+                           int32_t* order, int32_t* rank, int32_t* bandwidth);
+
+/* Bandwidth of an edge list (Background: the smallest b with a_ij = 0 for
+ * |i - j| > b) under an optional relabelling rank[v] (nullable: identity).
+ *   n          number of nodes; src, dst [m] ids in [0, n); rank [n] or NULL
+ *   bandwidth  out (0 for m == 0) */
+ggnn_status ggnn_bandwidth(int32_t n, int64_t m, const int32_t* src, const int32_t* dst,
+                           const int32_t* rank, int32_t* bandwidth);
+
+/* Bytes of a block band: E * (n_pad / B) * 3 * B * B elements of dtype dt.
+ * Returns 0 for invalid arguments. */
+size_t ggnn_band_bytes(int32_t n_pad, int32_t E, int32_t B, ggnn_dtype dt);
+
+/* Pack typed edges into the three block diagonals of Eq. 3 (Algorithm 1's
+ * Cks, Uks, Lks), one band per edge type:
+ *   band[e][k][s][r][c] = 1 for an edge j -> i of type e with
+ *   i = rank(dst) = k*B + r and j = rank(src) = (k - 1 + s)*B + c,
+ * so s = 0 is the sub-diagonal block L_k (block column k-1), s = 1 the
+ * diagonal block C_k and s = 2 the super-diagonal block U_k (block column
+ * k+1).  Slot (k = 0, s = 0) and slot (k = nb-1, s = 2) are always zero.
+ * Edges whose block row and block column differ by more than one are not
+ * covered (the lossy regime described after Eq. 3): they are dropped and
+ * counted, or, with strict != 0, make the call fail with OUT_OF_BAND after
+ * the whole list has been scanned.  A repeated (src, dst, type) is one edge
+ * (A_e has entries in {0,1}) and is counted as a duplicate.
+ *   n_pad      positive multiple of B (B >= 1 here; the device entry points
+ *              need B in {32..512})
+ *   src, dst   [m] ids in [0, n_pad); etype [m] in [0, E)
+ *   rank       [n_pad] relabelling applied to src and dst, or NULL (identity)
+ *   band       host buffer of ggnn_band_bytes(n_pad, E, B, dt) bytes; fully
+ *              overwritten (zeros, then ones at the edges)
+ *   n_packed, n_dropped, n_duplicate   nullable counters (out) */
+ggnn_status ggnn_banded_pack(int32_t n_pad, int32_t E, int32_t B, int64_t m,
+                             const int32_t* src, const int32_t* dst, const int32_t* etype,
+                             const int32_t* rank, ggnn_dtype dt, int strict, void* band,
+                             int64_t* n_packed, int64_t* n_dropped, int64_t* n_duplicate);
+
+/* ======================================================================
+ * Device entry points: one propagation step and its reverse.
+ * All pointers are device memory owned by the caller.
+ * ====================================================================== */
+
+/* Message transform (typed form of Eq. 1; per-type bias of the Appendix's
+ * "Model" paragraph): M_e = X W_e (+ 1 bias_e^T) for every edge type e.
+ *   X     [n_pad][H] dt, node-major node states
+ *   W     [E][H][H] dt, W[e][h_in][h_out]
+ *   bias  [E][H] float, or NULL for no bias
+ *   M     [E][H][n_pad] float, feature-major: M[e][h][i] (written).  The
+ *         messages stay float in both modes: they are summed over many edges
+ *         next, and a bf16 copy would add a rounding as large as that of
+ *         the bf16 state itself. */
+ggnn_status ggnn_msg_transform(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E,
+                               const void* X, const void* W, const float* bias, float* M,
+                               void* stream);
+
+/* Banded propagation (Eq. 3; Algorithm 1's three batched products):
+ *   a[k] = sum_e  band[e][k][0] M_e[k-1] + band[e][k][1] M_e[k] + band[e][k][2] M_e[k+1]
+ * for every block row k (out-of-range blocks are zero), i.e. a = sum_e A_e M_e
+ * on the covered edges, messages summed.  In bf16 mode each message enters
+ * the matrix cores as a bf16 pair (hi + lo), so the products keep about 16
+ * bits of the float message.
+ *   band  [E][n_pad/B][3][B][B] dt (as ggnn_banded_pack writes it)
+ *   M     [E][H][n_pad] float feature-major
+ *   a     [n_pad][H] float node-major (written) */
+ggnn_status ggnn_banded_propagate(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
+                                  const void* band, const float* M, float* a, void* stream);
+
+/* GRU node update (Eq. 1's GRU, Cho et al. 2014 form; gates (r, z, n)):
+ *   r = sigmoid(a Wi_r + h U_r + b_r),  z = sigmoid(a Wi_z + h U_z + b_z)
+ *   n = tanh(a Wi_n + (r*h) U_n + b_n), h_out = z*h + (1-z)*n
+ * In bf16 mode a enters the matrix cores as a bf16 pair (hi + lo) and r*h
+ * is rounded to bf16.
+ *   a      [n_pad][H] float;  h [n_pad][H] dt
+ *   Wi, U  [H][3H] dt (columns r | z | n);  b [3H] float
+ *   h_out  [n_pad][H] dt (written; must not alias h)
+ *   saved  [n_pad][3H] dt (written: r | z | n per node), or NULL */
+ggnn_status ggnn_gru_update(ggnn_dtype dt, int32_t n_pad, int32_t H, const float* a, const void* h,
+                            const void* Wi, const void* U, const float* b, void* h_out, void* saved,
+                            void* stream);
+
+/* Workspace bytes needed by ggnn_gru_update_bwd for these sizes. */
+size_t ggnn_gru_update_bwd_workspace_bytes(ggnn_dtype dt, int32_t n_pad, int32_t H);
+
+/* Reverse of ggnn_gru_update for the upstream gradient dh_out of h_out:
+ *   da   [H][n_pad] dt, feature-major (written)     = dL/da
+ *   dh   [n_pad][H] float (written)                   = dL/dh through the GRU
+ *   dWi, dU [H][3H] float, db [3H] float: += (the caller zeroes them once;
+ *         weights are shared across steps)
+ *   workspace  device buffer of at least the queried size; its contents
+ *         on entry do not matter
+ *   a, h, saved as passed to / written by the forward call. */
+ggnn_status ggnn_gru_update_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, const float* dh_out,
+                                const float* a, const void* h, const void* saved,
+                                const void* Wi, const void* U,
+                                void* da, float* dh, float* dWi, float* dU, float* db,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Reverse of ggnn_banded_propagate: dM_e = A_e^T da on the covered edges,
+ * evaluated with transposed blocks and the sub/super-diagonal roles swapped:
+ *   dM_e[c] = band[e][c-1][2]^T da[c-1] + band[e][c][1]^T da[c] + band[e][c+1][0]^T da[c+1]
+ *   band  as for the forward; da [H][n_pad] dt feature-major
+ *   dM    [E][H][n_pad] dt feature-major (written) */
+ggnn_status ggnn_banded_propagate_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
+                                      const void* band, const void* da, void* dM, void* stream);
+
+/* Workspace bytes needed by ggnn_msg_transform_bwd for these sizes. */
+size_t ggnn_msg_transform_bwd_workspace_bytes(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E);
+
+/* Reverse of ggnn_msg_transform:
+ *   dX_out = dX_in + sum_e dM_e W_e^T   ([n_pad][H] float; dX_in may be NULL
+ *            for zero, and may equal dX_out for an in-place update)
+ *   dW    [E][H][H] float  += X^T dM_e
+ *   dbias [E][H] float     += column sums of dM_e, or NULL to skip
+ *   X     [n_pad][H] dt;  W [E][H][H] dt;  dM [E][H][n_pad] dt */
+ggnn_status ggnn_msg_transform_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E,
+                                   const void* X, const void* W, const void* dM,
+                                   const float* dX_in, float* dX_out, float* dW, float* dbias,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* ======================================================================
+ * T-step orchestration (Eq. 1 for t = 0..T-1, with stored activations, and
+ * the reverse pass).  Each call enqueues 3*T (forward) or 3*T plus a few
+ * reduction launches (backward) kernels on `stream`.
+ * ====================================================================== */
+
+typedef struct ggnn_model {
+  int32_t dtype;        /* ggnn_dtype */
+  int32_t n_pad, B, H, E, T;
+  const void* band;     /* [E][n_pad/B][3][B][B] dt */
+  const void* W;        /* [E][H][H] dt */
+  const float* bias;    /* [E][H] or NULL */
+  const void* Wi;       /* [H][3H] dt */
+  const void* U;        /* [H][3H] dt */
+  const float* b;       /* [3H] */
+} ggnn_model;
+
+typedef struct ggnn_activations {
+  void* X;              /* [T+1][n_pad][H] dt: X[0] is the input, X[1..T] written */
+  float* a;             /* [T][n_pad][H] float, written by the forward */
+  void* saved;          /* [T][n_pad][3H] dt, written by the forward */
+  float* M;             /* [E][H][n_pad] float scratch (contents not kept) */
+} ggnn_activations;
+
+typedef struct ggnn_grads {
+  float* dX;            /* [n_pad][H]: on entry dL/dX_T, on return dL/dX_0 */
+  float* dW;            /* [E][H][H]  += */
+  float* dbias;         /* [E][H]     += (ignored when the model has no bias) */
+  float* dWi;           /* [H][3H]    += */
+  float* dU;            /* [H][3H]    += */
+  float* db;            /* [3H]       += */
+  void* da;             /* [H][n_pad] dt scratch */
+  void* dM;             /* [E][H][n_pad] dt scratch */
+  float* dh;            /* [n_pad][H] float scratch */
+  void* workspace;      /* device scratch of ggnn_backward_workspace_bytes() */
+  size_t workspace_bytes;
+} ggnn_grads;
+
+/* Workspace bytes needed by ggnn_backward for this model. */
+size_t ggnn_backward_workspace_bytes(const ggnn_model* model);
+
+/* Forward over T steps: for t = 0..T-1,
+ *   M = msg_transform(X[t]); a[t] = banded_propagate(M);
+ *   X[t+1], saved[t] = gru_update(a[t], X[t]). */
+ggnn_status ggnn_forward(const ggnn_model* model, const ggnn_activations* act, void* stream);
+
+/* Reverse pass for L with dL/dX_T given in grads->dX: for t = T-1..0,
+ *   da, dh = gru_update_bwd(dX); dM = banded_propagate_bwd(da);
+ *   dX = dh + sum_e dM_e W_e^T;  weight gradients accumulate (+=).
+ * Needs the activations of a preceding ggnn_forward. */
+ggnn_status ggnn_backward(const ggnn_model* model, const ggnn_activations* act,
+                          const ggnn_grads* grads, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GGNN_H */

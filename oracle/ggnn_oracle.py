@@ -229,33 +229,44 @@ def banded_apply(band: np.ndarray, M: np.ndarray) -> np.ndarray:
 def msg_transform(X: np.ndarray, W: np.ndarray, bias=None) -> np.ndarray:
     """Messages M_e = X W_e (+ 1 b_e^T) for every edge type (typed form of
     Eq. 1; the per-type bias of the Appendix's "Model" paragraph)."""
-    M = np.einsum("nh,ehk->enk", X, W)
+    M = np.stack([X @ W[e] for e in range(W.shape[0])])
     if bias is not None:
         M = M + bias[:, None, :]
     return M
 
 
+def _scatter_rows(n: int, rows: np.ndarray, vals: np.ndarray) -> np.ndarray:
+    """out[i] = sum of vals[k] over all k with rows[k] == i (a weighted count
+    per output row, one feature column at a time)."""
+    out = np.zeros((n, vals.shape[1]))
+    for h in range(vals.shape[1]):
+        out[:, h] = np.bincount(rows, weights=vals[:, h], minlength=n)
+    return out
+
+
 def aggregate(n: int, src, dst, etype, M: np.ndarray) -> np.ndarray:
     """a[i] = sum over edges (j -> i, e) of M_e[j]: the sparse product
     sum_e A_e M_e by explicit scatter-add (Eq. 1; messages are summed)."""
-    a = np.zeros((n, M.shape[2]))
-    np.add.at(a, np.asarray(dst, np.int64), M[np.asarray(etype, np.int64), np.asarray(src, np.int64)])
-    return a
+    src, dst, etype = (np.asarray(x, np.int64) for x in (src, dst, etype))
+    return _scatter_rows(n, dst, M[etype, src])
 
 
 def aggregate_transpose(n: int, src, dst, etype, da: np.ndarray, E: int) -> np.ndarray:
     """Adjoint of `aggregate`: dM_e[j] = sum over edges (j -> i, e) of da[i]
     (a gather along reversed edges, i.e. A_e^T da)."""
+    src, dst, etype = (np.asarray(x, np.int64) for x in (src, dst, etype))
     dM = np.zeros((E, n, da.shape[1]))
-    np.add.at(dM, (np.asarray(etype, np.int64), np.asarray(src, np.int64)), da[np.asarray(dst, np.int64)])
+    for e in range(E):
+        sel = etype == e
+        dM[e] = _scatter_rows(n, src[sel], da[dst[sel]])
     return dM
 
 
 def msg_transform_backward(X: np.ndarray, W: np.ndarray, dM: np.ndarray):
     """Reverse of msg_transform: dX = sum_e dM_e W_e^T, dW_e = X^T dM_e,
     db_e = column sums of dM_e."""
-    dX = np.einsum("enk,ehk->nh", dM, W)
-    dW = np.einsum("nh,enk->ehk", X, dM)
+    dX = sum(dM[e] @ W[e].T for e in range(W.shape[0]))
+    dW = np.stack([X.T @ dM[e] for e in range(W.shape[0])])
     dbias = dM.sum(axis=1)
     return dX, dW, dbias
 

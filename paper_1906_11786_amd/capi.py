@@ -1,0 +1,241 @@
+"""ctypes binding of libggnn.so: one Python function per C-ABI entry point,
+with the same name and argument order (see include/ggnn.h).
+
+Only argument marshalling happens here.  Pointers may be given as ints, as
+objects with ``data_ptr()`` (torch tensors) or as numpy arrays (host entry
+points); ``None`` is NULL.  A non-OK status raises GGNNError carrying the
+library's message.  The library must have been built in-tree
+(``python -m paper_1906_11786_amd.build``); there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libggnn.so")
+
+GGNN_F32 = 0
+GGNN_BF16 = 1
+DTYPES = {"f32": GGNN_F32, "bf16": GGNN_BF16}
+
+STATUS = {0: "GGNN_OK", 1: "GGNN_ERR_INVALID_ARG", 2: "GGNN_ERR_UNSUPPORTED", 3: "GGNN_ERR_OUT_OF_BAND",
+          4: "GGNN_ERR_DEVICE", 5: "GGNN_ERR_HOST_ALLOC", 6: "GGNN_ERR_WORKSPACE"}
+
+EXPORTS = [
+    "ggnn_abi_version", "ggnn_last_error", "ggnn_status_string",
+    "ggnn_rcm_order", "ggnn_bandwidth", "ggnn_band_bytes", "ggnn_banded_pack",
+    "ggnn_msg_transform", "ggnn_banded_propagate", "ggnn_gru_update",
+    "ggnn_gru_update_bwd_workspace_bytes", "ggnn_gru_update_bwd",
+    "ggnn_banded_propagate_bwd", "ggnn_msg_transform_bwd_workspace_bytes", "ggnn_msg_transform_bwd",
+    "ggnn_backward_workspace_bytes", "ggnn_forward", "ggnn_backward",
+]
+
+
+class GGNNError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn}: {msg or STATUS.get(status, status)}")
+        self.status = status
+        self.status_name = STATUS.get(status, str(status))
+
+
+class ggnn_model(C.Structure):
+    _fields_ = [("dtype", C.c_int32), ("n_pad", C.c_int32), ("B", C.c_int32), ("H", C.c_int32),
+                ("E", C.c_int32), ("T", C.c_int32), ("band", C.c_void_p), ("W", C.c_void_p),
+                ("bias", C.c_void_p), ("Wi", C.c_void_p), ("U", C.c_void_p), ("b", C.c_void_p)]
+
+
+class ggnn_activations(C.Structure):
+    _fields_ = [("X", C.c_void_p), ("a", C.c_void_p), ("saved", C.c_void_p), ("M", C.c_void_p)]
+
+
+class ggnn_grads(C.Structure):
+    _fields_ = [("dX", C.c_void_p), ("dW", C.c_void_p), ("dbias", C.c_void_p), ("dWi", C.c_void_p),
+                ("dU", C.c_void_p), ("db", C.c_void_p), ("da", C.c_void_p), ("dM", C.c_void_p),
+                ("dh", C.c_void_p), ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t)]
+
+
+_lib = None
+vp, i32, i64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
+I32P = C.POINTER(C.c_int32)
+I64P = C.POINTER(C.c_int64)
+
+_SIGS = {
+    "ggnn_abi_version": (C.c_int, []),
+    "ggnn_last_error": (C.c_char_p, []),
+    "ggnn_status_string": (C.c_char_p, [C.c_int]),
+    "ggnn_rcm_order": (C.c_int, [i32, i64, vp, vp, vp, vp, vp]),
+    "ggnn_bandwidth": (C.c_int, [i32, i64, vp, vp, vp, vp]),
+    "ggnn_band_bytes": (sz, [i32, i32, i32, C.c_int]),
+    "ggnn_banded_pack": (C.c_int, [i32, i32, i32, i64, vp, vp, vp, vp, C.c_int, C.c_int, vp, vp, vp, vp]),
+    "ggnn_msg_transform": (C.c_int, [C.c_int, i32, i32, i32, vp, vp, vp, vp, vp]),
+    "ggnn_banded_propagate": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp]),
+    "ggnn_gru_update": (C.c_int, [C.c_int, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
+    "ggnn_gru_update_bwd_workspace_bytes": (sz, [C.c_int, i32, i32]),
+    "ggnn_gru_update_bwd": (C.c_int, [C.c_int, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+    "ggnn_banded_propagate_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp]),
+    "ggnn_msg_transform_bwd_workspace_bytes": (sz, [C.c_int, i32, i32, i32]),
+    "ggnn_msg_transform_bwd": (C.c_int, [C.c_int, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+    "ggnn_backward_workspace_bytes": (sz, [C.POINTER(ggnn_model)]),
+    "ggnn_forward": (C.c_int, [C.POINTER(ggnn_model), C.POINTER(ggnn_activations), vp]),
+    "ggnn_backward": (C.c_int, [C.POINTER(ggnn_model), C.POINTER(ggnn_activations), C.POINTER(ggnn_grads), vp]),
+}
+
+
+def lib() -> C.CDLL:
+    """Load the in-tree library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_1906_11786_amd.build`")
+        L = C.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    raise TypeError(f"cannot take a pointer of {type(x)}")
+
+
+def _stream(s):
+    if s is not None:
+        return s if isinstance(s, int) else s.cuda_stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _dt(dt):
+    return DTYPES[dt] if isinstance(dt, str) else int(dt)
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise GGNNError(fn, status, lib().ggnn_last_error().decode())
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+# ---------------------------------------------------------------- host calls
+
+def ggnn_abi_version() -> int:
+    return lib().ggnn_abi_version()
+
+
+def ggnn_last_error() -> str:
+    return lib().ggnn_last_error().decode()
+
+
+def ggnn_status_string(status: int) -> str:
+    return lib().ggnn_status_string(status).decode()
+
+
+def ggnn_rcm_order(n: int, src, dst):
+    """Returns (order, rank, bandwidth) as (int32 array, int32 array, int)."""
+    src, dst = _i32(src), _i32(dst)
+    order = np.empty(n, np.int32)
+    rank = np.empty(n, np.int32)
+    bw = C.c_int32(0)
+    _check("ggnn_rcm_order", lib().ggnn_rcm_order(n, len(src), _ptr(src), _ptr(dst), _ptr(order), _ptr(rank),
+                                                  C.addressof(bw)))
+    return order, rank, int(bw.value)
+
+
+def ggnn_bandwidth(n: int, src, dst, rank=None) -> int:
+    src, dst = _i32(src), _i32(dst)
+    rk = None if rank is None else _i32(rank)
+    bw = C.c_int32(0)
+    _check("ggnn_bandwidth", lib().ggnn_bandwidth(n, len(src), _ptr(src), _ptr(dst), _ptr(rk), C.addressof(bw)))
+    return int(bw.value)
+
+
+def ggnn_band_bytes(n_pad: int, E: int, B: int, dt) -> int:
+    return int(lib().ggnn_band_bytes(n_pad, E, B, _dt(dt)))
+
+
+def ggnn_banded_pack(n_pad: int, E: int, B: int, src, dst, etype, rank=None, dt="bf16", strict: bool = False,
+                     band=None):
+    """Packs into a new (or the given) host array.  Returns
+    (band, n_packed, n_dropped, n_duplicate); band has shape
+    [E, n_pad/B, 3, B, B] and dtype float32 (f32) or uint16 (bf16 bits)."""
+    src, dst, etype = _i32(src), _i32(dst), _i32(etype)
+    rk = None if rank is None else _i32(rank)
+    d = _dt(dt)
+    nb = n_pad // B if B > 0 else 0
+    if band is None:
+        band = np.empty((E, nb, 3, B, B), dtype=np.float32 if d == GGNN_F32 else np.uint16)
+    counts = np.zeros(3, np.int64)
+    _check("ggnn_banded_pack", lib().ggnn_banded_pack(
+        n_pad, E, B, len(src), _ptr(src), _ptr(dst), _ptr(etype), _ptr(rk), d, int(bool(strict)), _ptr(band),
+        counts.ctypes.data, counts.ctypes.data + 8, counts.ctypes.data + 16))
+    return band, int(counts[0]), int(counts[1]), int(counts[2])
+
+
+# -------------------------------------------------------------- device calls
+
+def ggnn_msg_transform(dt, n_pad, H, E, X, W, bias, M, stream=None):
+    _check("ggnn_msg_transform", lib().ggnn_msg_transform(_dt(dt), n_pad, H, E, _ptr(X), _ptr(W), _ptr(bias),
+                                                          _ptr(M), _stream(stream)))
+
+
+def ggnn_banded_propagate(dt, n_pad, B, H, E, band, M, a, stream=None):
+    _check("ggnn_banded_propagate", lib().ggnn_banded_propagate(_dt(dt), n_pad, B, H, E, _ptr(band), _ptr(M),
+                                                                _ptr(a), _stream(stream)))
+
+
+def ggnn_gru_update(dt, n_pad, H, a, h, Wi, U, b, h_out, saved, stream=None):
+    _check("ggnn_gru_update", lib().ggnn_gru_update(_dt(dt), n_pad, H, _ptr(a), _ptr(h), _ptr(Wi), _ptr(U), _ptr(b),
+                                                    _ptr(h_out), _ptr(saved), _stream(stream)))
+
+
+def ggnn_gru_update_bwd_workspace_bytes(dt, n_pad, H) -> int:
+    return int(lib().ggnn_gru_update_bwd_workspace_bytes(_dt(dt), n_pad, H))
+
+
+def ggnn_gru_update_bwd(dt, n_pad, H, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, workspace, workspace_bytes,
+                        stream=None):
+    _check("ggnn_gru_update_bwd", lib().ggnn_gru_update_bwd(
+        _dt(dt), n_pad, H, _ptr(dh_out), _ptr(a), _ptr(h), _ptr(saved), _ptr(Wi), _ptr(U), _ptr(da), _ptr(dh),
+        _ptr(dWi), _ptr(dU), _ptr(db), _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def ggnn_banded_propagate_bwd(dt, n_pad, B, H, E, band, da, dM, stream=None):
+    _check("ggnn_banded_propagate_bwd", lib().ggnn_banded_propagate_bwd(_dt(dt), n_pad, B, H, E, _ptr(band),
+                                                                        _ptr(da), _ptr(dM), _stream(stream)))
+
+
+def ggnn_msg_transform_bwd_workspace_bytes(dt, n_pad, H, E) -> int:
+    return int(lib().ggnn_msg_transform_bwd_workspace_bytes(_dt(dt), n_pad, H, E))
+
+
+def ggnn_msg_transform_bwd(dt, n_pad, H, E, X, W, dM, dX_in, dX_out, dW, dbias, workspace, workspace_bytes,
+                           stream=None):
+    _check("ggnn_msg_transform_bwd", lib().ggnn_msg_transform_bwd(
+        _dt(dt), n_pad, H, E, _ptr(X), _ptr(W), _ptr(dM), _ptr(dX_in), _ptr(dX_out), _ptr(dW), _ptr(dbias),
+        _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def ggnn_backward_workspace_bytes(model: ggnn_model) -> int:
+    return int(lib().ggnn_backward_workspace_bytes(C.byref(model)))
+
+
+def ggnn_forward(model: ggnn_model, act: ggnn_activations, stream=None):
+    _check("ggnn_forward", lib().ggnn_forward(C.byref(model), C.byref(act), _stream(stream)))
+
+
+def ggnn_backward(model: ggnn_model, act: ggnn_activations, grads: ggnn_grads, stream=None):
+    _check("ggnn_backward", lib().ggnn_backward(C.byref(model), C.byref(act), C.byref(grads), _stream(stream)))

@@ -1,0 +1,264 @@
+// C-ABI device entry points: argument validation on the host, then the
+// kernel launches on the caller's stream; and the T-step orchestration of
+// Eq. 1 (forward with stored activations, then the reverse pass).
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+#include "kernels.h"
+
+using namespace ggnn;
+
+namespace {
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+ggnn_status device_status(hipError_t err, const char* what) {
+  if (err == hipSuccess) return GGNN_OK;
+  return fail(GGNN_ERR_DEVICE, "%s: %s", what, hipGetErrorString(err));
+}
+
+#define CHECK_PTR(p, name)                                                  \
+  do {                                                                      \
+    GGNN_CHECK_ARG((p) != nullptr, "%s is NULL", name);                     \
+    GGNN_CHECK_ARG(aligned16(p), "%s is not 16-byte aligned", name);        \
+  } while (0)
+#define CHECK_OPT_PTR(p, name)                                              \
+  do {                                                                      \
+    if ((p) != nullptr) GGNN_CHECK_ARG(aligned16(p), "%s is not 16-byte aligned", name); \
+  } while (0)
+
+ggnn_status check_common(int32_t dt, int32_t n_pad, int32_t H) {
+  GGNN_CHECK_ARG(supported_dtype(dt), "unknown dtype %d", dt);
+  GGNN_CHECK_ARG(n_pad > 0 && n_pad % 32 == 0, "n_pad=%d must be a positive multiple of 32", n_pad);
+  GGNN_CHECK_ARG(supported_H(H), "H=%d must be one of 32, 64, 128, 256", H);
+  GGNN_CHECK_ARG((int64_t)n_pad * 3 * H < (int64_t)1 << 31, "n_pad*3H exceeds 2^31 elements");
+  return GGNN_OK;
+}
+
+ggnn_status check_banded(int32_t dt, int32_t n_pad, int32_t B, int32_t H, int32_t E) {
+  ggnn_status st = check_common(dt, n_pad, H);
+  if (st != GGNN_OK) return st;
+  GGNN_CHECK_ARG(supported_B(B), "B=%d must be one of 32, 64, 128, 256, 512", B);
+  GGNN_CHECK_ARG(n_pad % B == 0, "n_pad=%d must be a multiple of B=%d", n_pad, B);
+  GGNN_CHECK_ARG(E >= 1 && E <= 64, "E=%d must be in [1, 64]", E);
+  return GGNN_OK;
+}
+
+inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+}  // namespace
+
+extern "C" {
+
+ggnn_status ggnn_msg_transform(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E, const void* X, const void* W,
+                               const float* bias, float* M, void* stream) {
+  clear_error();
+  ggnn_status st = check_common(dt, n_pad, H);
+  if (st != GGNN_OK) return st;
+  GGNN_CHECK_ARG(E >= 1 && E <= 64, "E=%d must be in [1, 64]", E);
+  CHECK_PTR(X, "X");
+  CHECK_PTR(W, "W");
+  CHECK_OPT_PTR(bias, "bias");
+  CHECK_PTR(M, "M");
+  return device_status(launch_transform_fwd(dt, n_pad, H, E, X, W, bias, M, as_stream(stream)), "msg_transform");
+}
+
+ggnn_status ggnn_banded_propagate(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E, const void* band,
+                                  const float* M, float* a, void* stream) {
+  clear_error();
+  ggnn_status st = check_banded(dt, n_pad, B, H, E);
+  if (st != GGNN_OK) return st;
+  CHECK_PTR(band, "band");
+  CHECK_PTR(M, "M");
+  CHECK_PTR(a, "a");
+  return device_status(launch_banded_fwd(dt, n_pad, B, H, E, band, M, a, as_stream(stream)), "banded_propagate");
+}
+
+ggnn_status ggnn_gru_update(ggnn_dtype dt, int32_t n_pad, int32_t H, const float* a, const void* h, const void* Wi,
+                            const void* U, const float* b, void* h_out, void* saved, void* stream) {
+  clear_error();
+  ggnn_status st = check_common(dt, n_pad, H);
+  if (st != GGNN_OK) return st;
+  CHECK_PTR(a, "a");
+  CHECK_PTR(h, "h");
+  CHECK_PTR(Wi, "Wi");
+  CHECK_PTR(U, "U");
+  CHECK_PTR(b, "b");
+  CHECK_PTR(h_out, "h_out");
+  CHECK_OPT_PTR(saved, "saved");
+  GGNN_CHECK_ARG(h_out != h, "h_out must not alias h");
+  return device_status(launch_gru_fwd(dt, n_pad, H, a, h, Wi, U, b, h_out, saved, as_stream(stream)), "gru_update");
+}
+
+size_t ggnn_gru_update_bwd_workspace_bytes(ggnn_dtype dt, int32_t n_pad, int32_t H) {
+  if (!supported_dtype(dt) || n_pad <= 0 || n_pad % 32 != 0 || !supported_H(H)) return 0;
+  return gru_bwd_workspace(dt, n_pad, H);
+}
+
+ggnn_status ggnn_gru_update_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, const float* dh_out, const float* a,
+                                const void* h, const void* saved, const void* Wi, const void* U, void* da, float* dh,
+                                float* dWi, float* dU, float* db, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  clear_error();
+  ggnn_status st = check_common(dt, n_pad, H);
+  if (st != GGNN_OK) return st;
+  CHECK_PTR(dh_out, "dh_out");
+  CHECK_PTR(a, "a");
+  CHECK_PTR(h, "h");
+  CHECK_PTR(saved, "saved");
+  CHECK_PTR(Wi, "Wi");
+  CHECK_PTR(U, "U");
+  CHECK_PTR(da, "da");
+  CHECK_PTR(dh, "dh");
+  CHECK_PTR(dWi, "dWi");
+  CHECK_PTR(dU, "dU");
+  CHECK_PTR(db, "db");
+  GGNN_CHECK_ARG(dh != dh_out, "dh must not alias dh_out");
+  const size_t need = gru_bwd_workspace(dt, n_pad, H);
+  if (workspace == nullptr || workspace_bytes < need || !aligned16(workspace))
+    return fail(GGNN_ERR_WORKSPACE, "gru_update_bwd needs a 16-byte aligned workspace of %zu bytes (got %zu)", need,
+                workspace ? workspace_bytes : (size_t)0);
+  return device_status(
+      launch_gru_bwd(dt, n_pad, H, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, workspace, as_stream(stream)),
+      "gru_update_bwd");
+}
+
+ggnn_status ggnn_banded_propagate_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
+                                      const void* band, const void* da, void* dM, void* stream) {
+  clear_error();
+  ggnn_status st = check_banded(dt, n_pad, B, H, E);
+  if (st != GGNN_OK) return st;
+  CHECK_PTR(band, "band");
+  CHECK_PTR(da, "da");
+  CHECK_PTR(dM, "dM");
+  return device_status(launch_banded_bwd(dt, n_pad, B, H, E, band, da, dM, as_stream(stream)),
+                       "banded_propagate_bwd");
+}
+
+size_t ggnn_msg_transform_bwd_workspace_bytes(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E) {
+  if (!supported_dtype(dt) || n_pad <= 0 || n_pad % 32 != 0 || !supported_H(H) || E < 1 || E > 64) return 0;
+  return transform_bwd_workspace(dt, n_pad, H, E);
+}
+
+ggnn_status ggnn_msg_transform_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E, const void* X, const void* W,
+                                   const void* dM, const float* dX_in, float* dX_out, float* dW, float* dbias,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  ggnn_status st = check_common(dt, n_pad, H);
+  if (st != GGNN_OK) return st;
+  GGNN_CHECK_ARG(E >= 1 && E <= 64, "E=%d must be in [1, 64]", E);
+  CHECK_PTR(X, "X");
+  CHECK_PTR(W, "W");
+  CHECK_PTR(dM, "dM");
+  CHECK_OPT_PTR(dX_in, "dX_in");
+  CHECK_PTR(dX_out, "dX_out");
+  CHECK_PTR(dW, "dW");
+  CHECK_OPT_PTR(dbias, "dbias");
+  const size_t need = transform_bwd_workspace(dt, n_pad, H, E);
+  if (workspace == nullptr || workspace_bytes < need || !aligned16(workspace))
+    return fail(GGNN_ERR_WORKSPACE, "msg_transform_bwd needs a 16-byte aligned workspace of %zu bytes (got %zu)",
+                need, workspace ? workspace_bytes : (size_t)0);
+  return device_status(launch_transform_bwd(dt, n_pad, H, E, X, W, dM, dX_in, dX_out, dW, dbias, workspace,
+                                            as_stream(stream)),
+                       "msg_transform_bwd");
+}
+
+// ---------------------------------------------------------------------------
+// T-step orchestration
+// ---------------------------------------------------------------------------
+
+static ggnn_status check_model(const ggnn_model* m) {
+  GGNN_CHECK_ARG(m != nullptr, "model is NULL");
+  ggnn_status st = check_banded(m->dtype, m->n_pad, m->B, m->H, m->E);
+  if (st != GGNN_OK) return st;
+  GGNN_CHECK_ARG(m->T >= 1 && m->T <= 1024, "T=%d must be in [1, 1024]", m->T);
+  CHECK_PTR(m->band, "model.band");
+  CHECK_PTR(m->W, "model.W");
+  CHECK_OPT_PTR(m->bias, "model.bias");
+  CHECK_PTR(m->Wi, "model.Wi");
+  CHECK_PTR(m->U, "model.U");
+  CHECK_PTR(m->b, "model.b");
+  return GGNN_OK;
+}
+
+static ggnn_status check_acts(const ggnn_activations* act) {
+  GGNN_CHECK_ARG(act != nullptr, "activations is NULL");
+  CHECK_PTR(act->X, "act.X");
+  CHECK_PTR(act->a, "act.a");
+  CHECK_PTR(act->saved, "act.saved");
+  CHECK_PTR(act->M, "act.M");
+  return GGNN_OK;
+}
+
+size_t ggnn_backward_workspace_bytes(const ggnn_model* m) {
+  if (m == nullptr || check_model(m) != GGNN_OK) {
+    clear_error();
+    return 0;
+  }
+  size_t a = gru_bwd_workspace(m->dtype, m->n_pad, m->H);
+  size_t b = transform_bwd_workspace(m->dtype, m->n_pad, m->H, m->E);
+  return a > b ? a : b;
+}
+
+ggnn_status ggnn_forward(const ggnn_model* m, const ggnn_activations* act, void* stream) {
+  clear_error();
+  ggnn_status st = check_model(m);
+  if (st != GGNN_OK) return st;
+  st = check_acts(act);
+  if (st != GGNN_OK) return st;
+  const size_t es = dtype_bytes(m->dtype);
+  const size_t xs = (size_t)m->n_pad * m->H;
+  hipStream_t s = as_stream(stream);
+  for (int t = 0; t < m->T; ++t) {
+    const char* Xt = static_cast<const char*>(act->X) + t * xs * es;
+    char* Xn = static_cast<char*>(act->X) + (t + 1) * xs * es;
+    float* at = act->a + t * xs;
+    char* sv = static_cast<char*>(act->saved) + t * 3 * xs * es;
+    hipError_t err = launch_transform_fwd(m->dtype, m->n_pad, m->H, m->E, Xt, m->W, m->bias, act->M, s);
+    if (err == hipSuccess) err = launch_banded_fwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, act->M, at, s);
+    if (err == hipSuccess) err = launch_gru_fwd(m->dtype, m->n_pad, m->H, at, Xt, m->Wi, m->U, m->b, Xn, sv, s);
+    if (err != hipSuccess) return device_status(err, "forward");
+  }
+  return GGNN_OK;
+}
+
+ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, const ggnn_grads* gr, void* stream) {
+  clear_error();
+  ggnn_status st = check_model(m);
+  if (st != GGNN_OK) return st;
+  st = check_acts(act);
+  if (st != GGNN_OK) return st;
+  GGNN_CHECK_ARG(gr != nullptr, "grads is NULL");
+  CHECK_PTR(gr->dX, "grads.dX");
+  CHECK_PTR(gr->dW, "grads.dW");
+  CHECK_PTR(gr->dWi, "grads.dWi");
+  CHECK_PTR(gr->dU, "grads.dU");
+  CHECK_PTR(gr->db, "grads.db");
+  CHECK_PTR(gr->da, "grads.da");
+  CHECK_PTR(gr->dM, "grads.dM");
+  CHECK_PTR(gr->dh, "grads.dh");
+  if (m->bias) CHECK_PTR(gr->dbias, "grads.dbias");
+  const size_t need = ggnn_backward_workspace_bytes(m);
+  if (gr->workspace == nullptr || gr->workspace_bytes < need || !aligned16(gr->workspace))
+    return fail(GGNN_ERR_WORKSPACE, "backward needs a 16-byte aligned workspace of %zu bytes (got %zu)", need,
+                gr->workspace ? gr->workspace_bytes : (size_t)0);
+  const size_t es = dtype_bytes(m->dtype);
+  const size_t xs = (size_t)m->n_pad * m->H;
+  hipStream_t s = as_stream(stream);
+  float* dbias = m->bias ? gr->dbias : nullptr;
+  for (int t = m->T - 1; t >= 0; --t) {
+    const char* Xt = static_cast<const char*>(act->X) + t * xs * es;
+    const float* at = act->a + t * xs;
+    const char* sv = static_cast<const char*>(act->saved) + t * 3 * xs * es;
+    hipError_t err = launch_gru_bwd(m->dtype, m->n_pad, m->H, gr->dX, at, Xt, sv, m->Wi, m->U, gr->da, gr->dh,
+                                    gr->dWi, gr->dU, gr->db, gr->workspace, s);
+    if (err == hipSuccess) err = launch_banded_bwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, gr->da, gr->dM, s);
+    if (err == hipSuccess)
+      err = launch_transform_bwd(m->dtype, m->n_pad, m->H, m->E, Xt, m->W, gr->dM, gr->dh, gr->dX, gr->dW, dbias,
+                                 gr->workspace, s);
+    if (err != hipSuccess) return device_status(err, "backward");
+  }
+  return GGNN_OK;
+}
+
+}  // extern "C"

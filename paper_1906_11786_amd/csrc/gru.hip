@@ -1,0 +1,469 @@
+// GRU node update (Eq. 1's GRU, Cho et al. 2014 form) and its reverse on
+// gfx950 matrix cores, with the gate nonlinearities fused into the GEMM
+// epilogues.
+//
+// Layouts: a [n_pad][H] float, h / h_out [n_pad][H] dt, Wi and U [H][3H] dt
+// (columns r | z | n), b [3H] float, saved [n_pad][3H] dt (r | z | n),
+// da [H][n_pad] dt feature-major, dh [n_pad][H] float.
+//
+// k order ("accumulator-compatible"): inside a 32-wide feature step kk, lane
+// group g holds features 32kk + 4g + {0,1,2,3} and 32kk + 16 + 4g + {0,1,2,3}.
+// These are exactly the features a lane holds in the accumulator of the two
+// 16-feature output tiles 2kk and 2kk+1 (rows 4g + j), for the same node
+// (lane % 16).  So a gate computed in registers is already an operand
+// fragment of the next product: (r*h) U_n in the forward and every product of
+// the backward chain without any cross-lane exchange.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace ggnn {
+namespace dev {
+
+// Fragment of a node-major row in accumulator-compatible k order.
+template <typename S>
+__device__ __forceinline__ frag_t<S> rowfrag(const S* row, int kk, int g) {
+  return load4x2(row + 32 * kk + 4 * g, row + 32 * kk + 16 + 4 * g);
+}
+// Stage the transpose of a 32-column slice of a [H][3H] weight into LDS:
+// dst[f * PW + i] = src[i * 3H + col0 + f], f < 32, i < H.
+template <typename S, int H, int PW, int NT>
+__device__ __forceinline__ void stage_wT(S* dst, const S* src, int col0, int tid) {
+  constexpr int V = 16 / sizeof(S);
+  constexpr int UPR = 32 / V;  // 16-byte units per row slice
+  for (int lin = tid; lin < H * UPR; lin += NT) {
+    int i = lin / UPR, f0 = (lin % UPR) * V;
+    u32x4 v = *reinterpret_cast<const u32x4*>(src + (size_t)i * 3 * H + col0 + f0);
+    const S* pv = reinterpret_cast<const S*>(&v);
+#pragma unroll
+    for (int x = 0; x < V; ++x) dst[(f0 + x) * PW + i] = pv[x];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Forward.  Workgroup: 16*WAVES nodes, wave w: 16 nodes (lane % 16), all
+// features.  D[feature][node]: A operand = weight^T rows from LDS, B operand
+// = a / h / r*h fragments held in registers.  Phase A computes the reset
+// gate for all features (needed in full by (r*h) U_n), phase B the update
+// gate, the candidate and the new state, 32 features at a time.
+// ---------------------------------------------------------------------------
+template <typename S, int H, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void gru_fwd_kernel(const float* __restrict__ a, const S* __restrict__ h,
+                                                                 const S* __restrict__ Wi, const S* __restrict__ U,
+                                                                 const float* __restrict__ b, S* __restrict__ h_out,
+                                                                 S* __restrict__ saved, int n_pad) {
+  constexpr int NT = WAVES * kWave;
+  constexpr int V = 16 / sizeof(S);
+  constexpr int PW = H + V;
+  constexpr int KS = H / 32;
+  __shared__ __attribute__((aligned(16))) S wt[4][32 * PW];
+
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int q = lane % 16, g = lane / 16;
+  const int n0 = xcd_swizzle(blockIdx.x, gridDim.x) * (16 * WAVES) + 16 * wave;
+  const bool valid = n0 < n_pad;
+  const int node = n0 + q;
+
+  // a is fp32; in bf16 mode it enters the matrix cores as hi + lo parts
+  // (al holds the lo part), so a Wi keeps fp32-level accuracy.
+  constexpr int NP = sizeof(S) == 2 ? 2 : 1;
+  frag_t<S> af[NP][KS], hf[KS], rh[KS];
+  if (valid) {
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const float* row = a + (size_t)node * H;
+      f32x4 x = *reinterpret_cast<const f32x4*>(row + 32 * kk + 4 * g);
+      f32x4 y = *reinterpret_cast<const f32x4*>(row + 32 * kk + 16 + 4 * g);
+      float v[8] = {x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
+      if constexpr (NP == 2) {
+        split8(v, af[0][kk], af[NP - 1][kk]);
+      } else {
+        af[0][kk] = pack8<S>(v);
+      }
+      hf[kk] = rowfrag<S>(h + (size_t)node * H, kk, g);
+    }
+  }
+  auto afrag = [&](const S* t, int p, int kk) __attribute__((always_inline)) {
+    return load4x2(t + (16 * p + q) * PW + 32 * kk + 4 * g, t + (16 * p + q) * PW + 32 * kk + 16 + 4 * g);
+  };
+
+  // Phase A: r = sigmoid(a Wi_r + h U_r + b_r); keep r*h as operand fragments.
+  for (int c = 0; c < KS; ++c) {
+    __syncthreads();
+    stage_wT<S, H, PW, NT>(wt[0], Wi, 32 * c, tid);
+    stage_wT<S, H, PW, NT>(wt[1], U, 32 * c, tid);
+    __syncthreads();
+    if (!valid) continue;
+    f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        const frag_t<S> w0 = afrag(wt[0], p, kk);
+#pragma unroll
+        for (int part = 0; part < NP; ++part) mma(acc[p], w0, af[part][kk]);
+        mma(acc[p], afrag(wt[1], p, kk), hf[kk]);
+      }
+    float rhv[8];
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const int f = 32 * c + 16 * p + 4 * g;
+      float r[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        r[j] = sigmoidf_(acc[p][j] + b[f + j]);
+        rhv[4 * p + j] = r[j] * static_cast<float>(hf[c][4 * p + j]);
+      }
+      if (saved) store4(saved + (size_t)node * 3 * H + f, r[0], r[1], r[2], r[3]);
+    }
+    rh[c] = pack8<S>(rhv);
+  }
+  // Phase B: z, n and the new state, 32 features at a time.
+  for (int c = 0; c < KS; ++c) {
+    __syncthreads();
+    stage_wT<S, H, PW, NT>(wt[0], Wi, H + 32 * c, tid);
+    stage_wT<S, H, PW, NT>(wt[1], U, H + 32 * c, tid);
+    stage_wT<S, H, PW, NT>(wt[2], Wi, 2 * H + 32 * c, tid);
+    stage_wT<S, H, PW, NT>(wt[3], U, 2 * H + 32 * c, tid);
+    __syncthreads();
+    if (!valid) continue;
+    f32x4 az[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+    f32x4 an[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        const frag_t<S> w0 = afrag(wt[0], p, kk), w2 = afrag(wt[2], p, kk);
+#pragma unroll
+        for (int part = 0; part < NP; ++part) {
+          mma(az[p], w0, af[part][kk]);
+          mma(an[p], w2, af[part][kk]);
+        }
+        mma(az[p], afrag(wt[1], p, kk), hf[kk]);
+        mma(an[p], afrag(wt[3], p, kk), rh[kk]);
+      }
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const int f = 32 * c + 16 * p + 4 * g;
+      float z[4], n[4], o[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        z[j] = sigmoidf_(az[p][j] + b[H + f + j]);
+        n[j] = tanhf_(an[p][j] + b[2 * H + f + j]);
+        const float hv = static_cast<float>(hf[c][4 * p + j]);
+        o[j] = z[j] * hv + (1.f - z[j]) * n[j];
+      }
+      store4(h_out + (size_t)node * H + f, o[0], o[1], o[2], o[3]);
+      if (saved) {
+        store4(saved + (size_t)node * 3 * H + H + f, z[0], z[1], z[2], z[3]);
+        store4(saved + (size_t)node * 3 * H + 2 * H + f, n[0], n[1], n[2], n[3]);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Backward, per node (wave w: 16 nodes, lane % 16 = node).  With
+// g = dL/dh', dn = g(1-z), dz = g(h-n), n^ = dn(1-n^2), z^ = dz z(1-z),
+// q = n^ U_n^T, r^ = q h r(1-r):
+//   dh = g z + q r + r^ U_r^T + z^ U_z^T,   da = [r^ z^ n^] Wi^T.
+// The gate gradients G^ = [r^ z^ n^] go to `ghat` (node-major [n_pad][3H])
+// for the weight-gradient pass; every lane only re-reads values it wrote
+// itself, so the phases need no barrier.  Weight fragments are read from
+// global memory (they are small and stay cached).
+// ---------------------------------------------------------------------------
+template <typename S, int H, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __restrict__ gin, const S* __restrict__ h,
+                                                                 const S* __restrict__ saved, const S* __restrict__ Wi,
+                                                                 const S* __restrict__ U, S* __restrict__ daT,
+                                                                 float* dh, S* ghat, int n_pad) {
+  constexpr int KS = H / 32;
+  constexpr int MTL = H / 16;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int q = lane % 16, g = lane / 16;
+  const int n0 = xcd_swizzle(blockIdx.x, gridDim.x) * (16 * WAVES) + 16 * wave;
+  if (n0 >= n_pad) return;   // no barriers in this kernel
+  const int node = n0 + q;
+  const S* sv = saved + (size_t)node * 3 * H;
+  S* gh = ghat + (size_t)node * 3 * H;
+  float* dhr = dh + (size_t)node * H;
+
+  // Phase 1: elementwise part.
+#pragma unroll
+  for (int m = 0; m < MTL; ++m) {
+    const int f = 16 * m + 4 * g;
+    f32x4 gg = *reinterpret_cast<const f32x4*>(gin + (size_t)node * H + f);
+    f32x4 z4 = load4f(sv + H + f), n4 = load4f(sv + 2 * H + f);
+    f32x4 h4 = load4f(h + (size_t)node * H + f);
+    float G[4] = {gg.x, gg.y, gg.z, gg.w}, Z[4] = {z4.x, z4.y, z4.z, z4.w}, N[4] = {n4.x, n4.y, n4.z, n4.w};
+    float Hh[4] = {h4.x, h4.y, h4.z, h4.w};
+    float zh[4], nh[4], d0[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float dn = G[j] * (1.f - Z[j]);
+      const float dz = G[j] * (Hh[j] - N[j]);
+      d0[j] = G[j] * Z[j];
+      nh[j] = dn * (1.f - N[j] * N[j]);
+      zh[j] = dz * Z[j] * (1.f - Z[j]);
+    }
+    store4(gh + H + f, zh[0], zh[1], zh[2], zh[3]);
+    store4(gh + 2 * H + f, nh[0], nh[1], nh[2], nh[3]);
+    store4(dhr + f, d0[0], d0[1], d0[2], d0[3]);
+  }
+  // Phase 2: q = n^ U_n^T (D[f_in][node]); r^ and the q r term of dh.
+  frag_t<S> nf[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) nf[kk] = rowfrag<S>(gh + 2 * H, kk, g);
+#pragma unroll
+  for (int m = 0; m < MTL; ++m) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    const S* urow = U + (size_t)(16 * m + q) * 3 * H + 2 * H;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) mma(acc, rowfrag<S>(urow, kk, g), nf[kk]);
+    const int f = 16 * m + 4 * g;
+    f32x4 r4 = load4f(sv + f), h4 = load4f(h + (size_t)node * H + f);
+    f32x4 d4 = *reinterpret_cast<const f32x4*>(dhr + f);
+    float R[4] = {r4.x, r4.y, r4.z, r4.w}, Hh[4] = {h4.x, h4.y, h4.z, h4.w}, D[4] = {d4.x, d4.y, d4.z, d4.w};
+    float rh[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      rh[j] = acc[j] * Hh[j] * R[j] * (1.f - R[j]);
+      D[j] += acc[j] * R[j];
+    }
+    store4(gh + f, rh[0], rh[1], rh[2], rh[3]);
+    store4(dhr + f, D[0], D[1], D[2], D[3]);
+  }
+  // Phase 3: da = G^ Wi^T, D[node][f_in]: four consecutive nodes per lane.
+  frag_t<S> gf[3][KS];
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) gf[s][kk] = rowfrag<S>(gh + s * H, kk, g);
+#pragma unroll
+  for (int n = 0; n < MTL; ++n) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    const S* wrow = Wi + (size_t)(16 * n + q) * 3 * H;
+#pragma unroll
+    for (int s = 0; s < 3; ++s)
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) mma(acc, gf[s][kk], rowfrag<S>(wrow + s * H, kk, g));
+    store4(daT + (size_t)(16 * n + q) * n_pad + n0 + 4 * g, acc[0], acc[1], acc[2], acc[3]);
+  }
+  // Phase 4: dh += r^ U_r^T + z^ U_z^T, D[f_in][node].
+#pragma unroll
+  for (int m = 0; m < MTL; ++m) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    const S* urow = U + (size_t)(16 * m + q) * 3 * H;
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) mma(acc, rowfrag<S>(urow + s * H, kk, g), gf[s][kk]);
+    const int f = 16 * m + 4 * g;
+    f32x4 d4 = *reinterpret_cast<const f32x4*>(dhr + f);
+    store4(dhr + f, d4.x + acc[0], d4.y + acc[1], d4.z + acc[2], d4.w + acc[3]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Weight gradients of the GRU over one node split:
+//   P[split][0][i][c] = sum_nodes a[node][i] G^[node][c]          (dWi)
+//   P[split][1][i][c] = sum_nodes x_c[node][i] G^[node][c]        (dU)
+// with x_c = h for the r and z columns and r*h for the n columns, and
+//   Pb[split][c] = sum_nodes G^[node][c]                          (db).
+// Tile TI x TI (TI = min(H, 64)); both operands are node-major, staged in
+// LDS and read with a stride along nodes.
+// ---------------------------------------------------------------------------
+template <typename S, int H>
+__global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kernel(
+    const float* __restrict__ a, const S* __restrict__ h, const S* __restrict__ saved, const S* __restrict__ ghat,
+    float* __restrict__ P, float* __restrict__ Pb, int n_pad, int nodes_per_split) {
+  constexpr int TI = H < 64 ? H : 64;
+  constexpr int WAVES = TI / 16;
+  constexpr int NT = WAVES * kWave;
+  constexpr int KN = 64;
+  constexpr int PX = TI + 4 / sizeof(S);
+  constexpr int NTL = TI / 16;
+  constexpr int TIN = H / TI, TOUT = 3 * H / TI;
+  __shared__ __attribute__((aligned(16))) S ta[KN * PX];
+  __shared__ __attribute__((aligned(16))) S tb[KN * PX];
+
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int q = lane % 16, g = lane / 16;
+  int bid = blockIdx.x;
+  const int to = bid % TOUT; bid /= TOUT;
+  const int ti = bid % TIN; bid /= TIN;
+  const int which = bid % 2;
+  const int split = bid / 2;
+  const int nlo = split * nodes_per_split;
+  const int nhi = min(n_pad, nlo + nodes_per_split);
+  const int col0 = to * TI;                      // gate column of this tile
+  const bool rh_src = (which == 1 && col0 >= 2 * H);
+  const bool do_bias = (which == 0 && ti == 0 && wave == 0);
+
+  f32x4 acc[NTL];
+  float bsum[NTL];
+#pragma unroll
+  for (int n = 0; n < NTL; ++n) {
+    acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    bsum[n] = 0.f;
+  }
+  for (int c0 = nlo; c0 < nhi; c0 += KN) {
+    __syncthreads();
+    for (int lin = tid; lin < KN * TI / 4; lin += NT) {
+      const int r = lin / (TI / 4), c = (lin % (TI / 4)) * 4;
+      const int node = c0 + r;
+      if (node >= nhi) continue;
+      const int fi = ti * TI + c;
+      f32x4 x;
+      if (which == 0) {
+        x = *reinterpret_cast<const f32x4*>(a + (size_t)node * H + fi);
+      } else {
+        x = load4f(h + (size_t)node * H + fi);
+        if (rh_src) {
+          f32x4 r4 = load4f(saved + (size_t)node * 3 * H + fi);
+          x = f32x4{x.x * r4.x, x.y * r4.y, x.z * r4.z, x.w * r4.w};
+        }
+      }
+      S xa[4] = {from_f<S>(x.x), from_f<S>(x.y), from_f<S>(x.z), from_f<S>(x.w)};
+      S* pa = &ta[r * PX + c];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pa[j] = xa[j];
+      const S* gsrc = ghat + (size_t)node * 3 * H + col0 + c;
+      S* pb = &tb[r * PX + c];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pb[j] = gsrc[j];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < KN / 32; ++kk) {
+      if (c0 + 32 * kk >= nhi) break;
+      frag_t<S> afr = load8_strided(&ta[(32 * kk + 8 * g) * PX + 16 * wave + q], PX);
+#pragma unroll
+      for (int n = 0; n < NTL; ++n) {
+        frag_t<S> bf = load8_strided(&tb[(32 * kk + 8 * g) * PX + 16 * n + q], PX);
+        mma(acc[n], afr, bf);
+        if (do_bias) {
+#pragma unroll
+          for (int x = 0; x < 8; ++x) bsum[n] += static_cast<float>(bf[x]);
+        }
+      }
+    }
+  }
+  float* out = P + ((size_t)split * 2 + which) * H * 3 * H;
+#pragma unroll
+  for (int n = 0; n < NTL; ++n) {
+    const int c = col0 + 16 * n + q;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * 3 * H + c] = acc[n][j];
+  }
+  if (do_bias) {
+#pragma unroll
+    for (int n = 0; n < NTL; ++n) {
+      float v = bsum[n];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (g == 0) Pb[(size_t)split * 3 * H + col0 + 16 * n + q] = v;
+    }
+  }
+}
+
+}  // namespace dev
+
+namespace {
+struct Split {
+  int nsplit, per;
+};
+Split gru_split(int n_pad, int H) {
+  int TI = H < 64 ? H : 64;
+  int tiles = 2 * (H / TI) * (3 * H / TI);
+  int want = (1024 + tiles - 1) / tiles;
+  int per = (n_pad + want - 1) / want;
+  per = (per + 63) / 64 * 64;
+  if (per < 512) per = 512;
+  return {(n_pad + per - 1) / per, per};
+}
+size_t ghat_bytes(int dt, int n_pad, int H) {
+  size_t b = (size_t)n_pad * 3 * H * (dt == GGNN_BF16 ? 2 : 4);
+  return (b + 255) / 256 * 256;
+}
+
+template <typename S, int H>
+hipError_t gru_fwd_h(int n_pad, const float* a, const void* h, const void* Wi, const void* U, const float* b,
+                     void* h_out, void* saved, hipStream_t st) {
+  constexpr int WAVES = 4;
+  hipLaunchKernelGGL((dev::gru_fwd_kernel<S, H, WAVES>), dim3((n_pad + 16 * WAVES - 1) / (16 * WAVES)),
+                     dim3(WAVES * 64), 0, st, a, static_cast<const S*>(h), static_cast<const S*>(Wi),
+                     static_cast<const S*>(U), b, static_cast<S*>(h_out), static_cast<S*>(saved), n_pad);
+  return hipGetLastError();
+}
+
+template <typename S, int H>
+hipError_t gru_bwd_h(int n_pad, const float* dh_out, const float* a, const void* h, const void* saved, const void* Wi,
+                     const void* U, void* da, float* dh, float* dWi, float* dU, float* db, void* ws, hipStream_t st) {
+  constexpr int WAVES = 4;
+  S* ghat = static_cast<S*>(ws);
+  float* P = reinterpret_cast<float*>(static_cast<char*>(ws) + ghat_bytes(sizeof(S) == 2 ? GGNN_BF16 : GGNN_F32, n_pad, H));
+  Split sp = gru_split(n_pad, H);
+  float* Pb = P + (size_t)sp.nsplit * 2 * H * 3 * H;
+  hipLaunchKernelGGL((dev::gru_bwd_kernel<S, H, WAVES>), dim3((n_pad + 16 * WAVES - 1) / (16 * WAVES)),
+                     dim3(WAVES * 64), 0, st, dh_out, static_cast<const S*>(h), static_cast<const S*>(saved),
+                     static_cast<const S*>(Wi), static_cast<const S*>(U), static_cast<S*>(da), dh, ghat, n_pad);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  constexpr int TI = H < 64 ? H : 64;
+  const int blocks = sp.nsplit * 2 * (H / TI) * (3 * H / TI);
+  hipLaunchKernelGGL((dev::gru_wgrad_kernel<S, H>), dim3(blocks), dim3(TI / 16 * 64), 0, st, a,
+                     static_cast<const S*>(h), static_cast<const S*>(saved), ghat, P, Pb, n_pad, sp.per);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const long slice = 2L * H * 3 * H;  // partials are [split][which][H][3H]
+  err = launch_reduce_partials(P, dWi, sp.nsplit, H * 3 * H, slice, st);
+  if (err != hipSuccess) return err;
+  err = launch_reduce_partials(P + (size_t)H * 3 * H, dU, sp.nsplit, H * 3 * H, slice, st);
+  if (err != hipSuccess) return err;
+  return launch_reduce_partials(Pb, db, sp.nsplit, 3 * H, 3L * H, st);
+}
+
+template <typename S>
+hipError_t gru_fwd_t(int n_pad, int H, const float* a, const void* h, const void* Wi, const void* U, const float* b,
+                     void* h_out, void* saved, hipStream_t st) {
+  switch (H) {
+    case 32: return gru_fwd_h<S, 32>(n_pad, a, h, Wi, U, b, h_out, saved, st);
+    case 64: return gru_fwd_h<S, 64>(n_pad, a, h, Wi, U, b, h_out, saved, st);
+    case 128: return gru_fwd_h<S, 128>(n_pad, a, h, Wi, U, b, h_out, saved, st);
+    case 256: return gru_fwd_h<S, 256>(n_pad, a, h, Wi, U, b, h_out, saved, st);
+  }
+  return hipErrorInvalidValue;
+}
+template <typename S>
+hipError_t gru_bwd_t(int n_pad, int H, const float* dh_out, const float* a, const void* h, const void* saved,
+                     const void* Wi, const void* U, void* da, float* dh, float* dWi, float* dU, float* db, void* ws,
+                     hipStream_t st) {
+  switch (H) {
+    case 32: return gru_bwd_h<S, 32>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, st);
+    case 64: return gru_bwd_h<S, 64>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, st);
+    case 128: return gru_bwd_h<S, 128>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, st);
+    case 256: return gru_bwd_h<S, 256>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, st);
+  }
+  return hipErrorInvalidValue;
+}
+}  // namespace
+
+size_t gru_bwd_workspace(int dt, int n_pad, int H) {
+  Split sp = gru_split(n_pad, H);
+  return ghat_bytes(dt, n_pad, H) + ((size_t)sp.nsplit * 2 * H * 3 * H + (size_t)sp.nsplit * 3 * H) * sizeof(float);
+}
+
+hipError_t launch_gru_fwd(int dt, int n_pad, int H, const float* a, const void* h, const void* Wi, const void* U,
+                          const float* b, void* h_out, void* saved, hipStream_t st) {
+  return dt == GGNN_BF16 ? gru_fwd_t<dev::bf16s>(n_pad, H, a, h, Wi, U, b, h_out, saved, st)
+                         : gru_fwd_t<float>(n_pad, H, a, h, Wi, U, b, h_out, saved, st);
+}
+
+hipError_t launch_gru_bwd(int dt, int n_pad, int H, const float* dh_out, const float* a, const void* h,
+                          const void* saved, const void* Wi, const void* U, void* da, float* dh, float* dWi,
+                          float* dU, float* db, void* ws, hipStream_t st) {
+  return dt == GGNN_BF16 ? gru_bwd_t<dev::bf16s>(n_pad, H, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, st)
+                         : gru_bwd_t<float>(n_pad, H, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, st);
+}
+
+}  // namespace ggnn

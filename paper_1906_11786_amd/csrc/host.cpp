@@ -1,0 +1,283 @@
+// Host-side graph compilation: reverse Cuthill-McKee ordering, bandwidth and
+// block-band packing (Compilation section and Eq. 3 of arXiv 1906.11786).
+// Plain C++17, no HIP: these run once per graph, before any device work.
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <tuple>
+#include <utility>
+#include <vector>
+
+#include "common.h"
+
+namespace ggnn {
+
+static thread_local std::string g_last_error;
+
+ggnn_status fail(ggnn_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = std::string(ggnn_status_string(st)) + ": " + buf;
+  return st;
+}
+
+void clear_error() { g_last_error.clear(); }
+
+namespace {
+
+// Undirected simple graph in CSR form: the union of all edge types with both
+// directions, self-loops and repeated pairs removed.  Each neighbour list is
+// sorted by (degree, label), the order in which the search visits them.
+struct SymGraph {
+  std::vector<int64_t> off;
+  std::vector<int32_t> adj;
+  std::vector<int32_t> deg;
+};
+
+SymGraph build_sym(int32_t n, int64_t m, const int32_t* src, const int32_t* dst) {
+  SymGraph g;
+  std::vector<std::pair<int32_t, int32_t>> pairs;
+  pairs.reserve(static_cast<size_t>(2 * m));
+  for (int64_t k = 0; k < m; ++k) {
+    if (src[k] == dst[k]) continue;
+    pairs.emplace_back(src[k], dst[k]);
+    pairs.emplace_back(dst[k], src[k]);
+  }
+  std::sort(pairs.begin(), pairs.end());
+  pairs.erase(std::unique(pairs.begin(), pairs.end()), pairs.end());
+  g.off.assign(static_cast<size_t>(n) + 1, 0);
+  for (auto& p : pairs) g.off[p.first + 1]++;
+  for (int32_t v = 0; v < n; ++v) g.off[v + 1] += g.off[v];
+  g.adj.resize(pairs.size());
+  for (size_t k = 0; k < pairs.size(); ++k) g.adj[k] = pairs[k].second;  // already grouped by first
+  g.deg.resize(n);
+  for (int32_t v = 0; v < n; ++v) g.deg[v] = static_cast<int32_t>(g.off[v + 1] - g.off[v]);
+  for (int32_t v = 0; v < n; ++v) {
+    std::sort(g.adj.begin() + g.off[v], g.adj.begin() + g.off[v + 1], [&](int32_t a, int32_t b) {
+      return g.deg[a] != g.deg[b] ? g.deg[a] < g.deg[b] : a < b;
+    });
+  }
+  return g;
+}
+
+inline bool less_deg_label(const SymGraph& g, int32_t a, int32_t b) {
+  return g.deg[a] != g.deg[b] ? g.deg[a] < g.deg[b] : a < b;
+}
+
+// Breadth-first level structure rooted at `root`.  Fills `nodes` with the
+// visit order and returns the number of levels; `last_begin` receives the
+// index in `nodes` where the deepest level starts.  `stamp`/`cur` mark
+// visited nodes without clearing between calls.
+int32_t level_structure(const SymGraph& g, int32_t root, std::vector<int32_t>& stamp, int32_t cur,
+                        std::vector<int32_t>& nodes, size_t& last_begin) {
+  nodes.clear();
+  nodes.push_back(root);
+  stamp[root] = cur;
+  size_t lo = 0, hi = 1;
+  int32_t levels = 1;
+  last_begin = 0;
+  while (true) {
+    for (size_t q = lo; q < hi; ++q) {
+      int32_t v = nodes[q];
+      for (int64_t k = g.off[v]; k < g.off[v + 1]; ++k) {
+        int32_t w = g.adj[k];
+        if (stamp[w] != cur) {
+          stamp[w] = cur;
+          nodes.push_back(w);
+        }
+      }
+    }
+    if (nodes.size() == hi) break;
+    last_begin = hi;
+    lo = hi;
+    hi = nodes.size();
+    ++levels;
+  }
+  return levels;
+}
+
+}  // namespace
+}  // namespace ggnn
+
+using namespace ggnn;
+
+extern "C" {
+
+int ggnn_abi_version(void) { return GGNN_ABI_VERSION; }
+
+const char* ggnn_last_error(void) { return g_last_error.c_str(); }
+
+const char* ggnn_status_string(ggnn_status s) {
+  switch (s) {
+    case GGNN_OK: return "GGNN_OK";
+    case GGNN_ERR_INVALID_ARG: return "GGNN_ERR_INVALID_ARG";
+    case GGNN_ERR_UNSUPPORTED: return "GGNN_ERR_UNSUPPORTED";
+    case GGNN_ERR_OUT_OF_BAND: return "GGNN_ERR_OUT_OF_BAND";
+    case GGNN_ERR_DEVICE: return "GGNN_ERR_DEVICE";
+    case GGNN_ERR_HOST_ALLOC: return "GGNN_ERR_HOST_ALLOC";
+    case GGNN_ERR_WORKSPACE: return "GGNN_ERR_WORKSPACE";
+  }
+  return "GGNN_ERR_UNKNOWN";
+}
+
+ggnn_status ggnn_bandwidth(int32_t n, int64_t m, const int32_t* src, const int32_t* dst, const int32_t* rank,
+                           int32_t* bandwidth) {
+  clear_error();
+  GGNN_CHECK_ARG(n >= 0 && m >= 0, "n=%d m=%lld must be >= 0", n, (long long)m);
+  GGNN_CHECK_ARG(bandwidth != nullptr, "bandwidth is NULL");
+  GGNN_CHECK_ARG(m == 0 || (src && dst), "src/dst is NULL");
+  int32_t bw = 0;
+  for (int64_t k = 0; k < m; ++k) {
+    int32_t s = src[k], d = dst[k];
+    GGNN_CHECK_ARG(s >= 0 && s < n && d >= 0 && d < n, "edge %lld (%d -> %d) out of range [0,%d)", (long long)k, s,
+                   d, n);
+    if (rank) {
+      s = rank[s];
+      d = rank[d];
+    }
+    int32_t span = s > d ? s - d : d - s;
+    bw = std::max(bw, span);
+  }
+  *bandwidth = bw;
+  return GGNN_OK;
+}
+
+ggnn_status ggnn_rcm_order(int32_t n, int64_t m, const int32_t* src, const int32_t* dst, int32_t* order,
+                           int32_t* rank, int32_t* bandwidth) {
+  clear_error();
+  GGNN_CHECK_ARG(n >= 0 && m >= 0, "n=%d m=%lld must be >= 0", n, (long long)m);
+  GGNN_CHECK_ARG(m == 0 || (src && dst), "src/dst is NULL");
+  GGNN_CHECK_ARG(n == 0 || (order && rank), "order/rank is NULL");
+  for (int64_t k = 0; k < m; ++k)
+    GGNN_CHECK_ARG(src[k] >= 0 && src[k] < n && dst[k] >= 0 && dst[k] < n,
+                   "edge %lld (%d -> %d) out of range [0,%d)", (long long)k, src[k], dst[k], n);
+  try {
+    SymGraph g = build_sym(n, m, src, dst);
+    std::vector<int32_t> stamp(n, -1), nodes, seq;
+    std::vector<char> visited(n, 0);
+    seq.reserve(n);
+    int32_t cur = 0;
+    for (int32_t v0 = 0; v0 < n; ++v0) {
+      if (visited[v0]) continue;
+      size_t last = 0;
+      level_structure(g, v0, stamp, cur++, nodes, last);
+      int32_t root = nodes[0];
+      for (int32_t v : nodes)
+        if (less_deg_label(g, v, root)) root = v;
+      // George-Liu: move to the smallest (degree, label) node of the deepest
+      // level while that deepens the level structure.
+      int32_t depth = level_structure(g, root, stamp, cur++, nodes, last);
+      while (true) {
+        int32_t cand = nodes[last];
+        for (size_t q = last; q < nodes.size(); ++q)
+          if (less_deg_label(g, nodes[q], cand)) cand = nodes[q];
+        std::vector<int32_t> cnodes;
+        size_t clast = 0;
+        int32_t cdepth = level_structure(g, cand, stamp, cur++, cnodes, clast);
+        if (cdepth > depth) {
+          root = cand;
+          depth = cdepth;
+          nodes.swap(cnodes);
+          last = clast;
+        } else {
+          break;
+        }
+      }
+      // Cuthill-McKee search from the root.
+      size_t head = seq.size();
+      seq.push_back(root);
+      visited[root] = 1;
+      while (head < seq.size()) {
+        int32_t x = seq[head++];
+        for (int64_t k = g.off[x]; k < g.off[x + 1]; ++k) {
+          int32_t w = g.adj[k];
+          if (!visited[w]) {
+            visited[w] = 1;
+            seq.push_back(w);
+          }
+        }
+      }
+    }
+    for (int32_t p = 0; p < n; ++p) order[p] = seq[n - 1 - p];
+    for (int32_t p = 0; p < n; ++p) rank[order[p]] = p;
+  } catch (const std::bad_alloc&) {
+    return fail(GGNN_ERR_HOST_ALLOC, "temporary allocation failed (n=%d, m=%lld)", n, (long long)m);
+  }
+  if (bandwidth) return ggnn_bandwidth(n, m, src, dst, rank, bandwidth);
+  return GGNN_OK;
+}
+
+size_t ggnn_band_bytes(int32_t n_pad, int32_t E, int32_t B, ggnn_dtype dt) {
+  if (n_pad <= 0 || E <= 0 || B <= 0 || n_pad % B != 0 || !supported_dtype(dt)) return 0;
+  size_t nb = static_cast<size_t>(n_pad / B);
+  return static_cast<size_t>(E) * nb * 3 * static_cast<size_t>(B) * static_cast<size_t>(B) * dtype_bytes(dt);
+}
+
+ggnn_status ggnn_banded_pack(int32_t n_pad, int32_t E, int32_t B, int64_t m, const int32_t* src, const int32_t* dst,
+                             const int32_t* etype, const int32_t* rank, ggnn_dtype dt, int strict, void* band,
+                             int64_t* n_packed, int64_t* n_dropped, int64_t* n_duplicate) {
+  clear_error();
+  GGNN_CHECK_ARG(supported_dtype(dt), "unknown dtype %d", (int)dt);
+  GGNN_CHECK_ARG(B >= 1 && n_pad >= B && n_pad % B == 0, "n_pad=%d must be a positive multiple of B=%d", n_pad, B);
+  GGNN_CHECK_ARG(E >= 1 && E <= 64, "E=%d must be in [1, 64]", E);
+  GGNN_CHECK_ARG(m >= 0, "m=%lld must be >= 0", (long long)m);
+  GGNN_CHECK_ARG(m == 0 || (src && dst && etype), "src/dst/etype is NULL");
+  GGNN_CHECK_ARG(band != nullptr, "band is NULL");
+  const int64_t nb = n_pad / B;
+  if (rank)
+    for (int32_t v = 0; v < n_pad; ++v)
+      GGNN_CHECK_ARG(rank[v] >= 0 && rank[v] < n_pad, "rank[%d]=%d out of range [0,%d)", v, rank[v], n_pad);
+  for (int64_t k = 0; k < m; ++k) {
+    GGNN_CHECK_ARG(src[k] >= 0 && src[k] < n_pad && dst[k] >= 0 && dst[k] < n_pad,
+                   "edge %lld (%d -> %d) out of range [0,%d)", (long long)k, src[k], dst[k], n_pad);
+    GGNN_CHECK_ARG(etype[k] >= 0 && etype[k] < E, "edge %lld has type %d outside [0,%d)", (long long)k, etype[k],
+                   E);
+  }
+  const size_t elems = ggnn_band_bytes(n_pad, E, B, dt) / dtype_bytes(dt);
+  std::memset(band, 0, elems * dtype_bytes(dt));
+  int64_t packed = 0, dup = 0;
+  std::vector<std::tuple<int32_t, int64_t, int64_t>> out_of_band;  // distinct dropped edges are counted once
+  const size_t BB = static_cast<size_t>(B) * B;
+  for (int64_t k = 0; k < m; ++k) {
+    int64_t i = rank ? rank[dst[k]] : dst[k];
+    int64_t j = rank ? rank[src[k]] : src[k];
+    int64_t kr = i / B, kc = j / B;
+    int64_t s = kc - kr + 1;
+    if (s < 0 || s > 2) {
+      try {
+        out_of_band.emplace_back(etype[k], i, j);
+      } catch (const std::bad_alloc&) {
+        return fail(GGNN_ERR_HOST_ALLOC, "temporary allocation failed");
+      }
+      continue;
+    }
+    size_t idx = ((static_cast<size_t>(etype[k]) * nb + kr) * 3 + s) * BB + static_cast<size_t>(i % B) * B + (j % B);
+    if (dt == GGNN_F32) {
+      float* p = static_cast<float*>(band) + idx;
+      if (*p != 0.0f) { ++dup; continue; }
+      *p = 1.0f;
+    } else {
+      uint16_t* p = static_cast<uint16_t*>(band) + idx;
+      if (*p != 0) { ++dup; continue; }
+      *p = 0x3F80;  // bf16 bit pattern of 1.0
+    }
+    ++packed;
+  }
+  std::sort(out_of_band.begin(), out_of_band.end());
+  const int64_t n_oob = static_cast<int64_t>(out_of_band.size());
+  const int64_t dropped = static_cast<int64_t>(std::unique(out_of_band.begin(), out_of_band.end()) - out_of_band.begin());
+  dup += n_oob - dropped;
+  if (n_packed) *n_packed = packed;
+  if (n_dropped) *n_dropped = dropped;
+  if (n_duplicate) *n_duplicate = dup;
+  if (strict && dropped > 0)
+    return fail(GGNN_ERR_OUT_OF_BAND, "%lld edge(s) fall outside the three block diagonals (B=%d)",
+                (long long)dropped, B);
+  return GGNN_OK;
+}
+
+}  // extern "C"

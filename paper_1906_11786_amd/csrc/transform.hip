@@ -1,0 +1,358 @@
+// Message transform M_e = X W_e (+ b_e) and its reverse on gfx950 matrix
+// cores (typed form of Eq. 1: one H x H map per edge type).
+//
+// Layouts: X [n_pad][H] node-major, W [E][H][H] (W[e][h_in][h_out]),
+// M [E][H][n_pad] float and dM [E][H][n_pad] dt, both feature-major,
+// dX [n_pad][H] float.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace ggnn {
+namespace dev {
+
+// ---------------------------------------------------------------------------
+// Forward.  A workgroup owns 32*WAVES nodes (wave w: 32 of them) for every
+// edge type.  D[node][h_out]: A operand = X rows (contiguous in h_in, read
+// once from HBM and kept in registers for all E types), B operand = W_e^T
+// rows, staged per (e, 64-column chunk) in LDS with the transpose done on
+// the LDS write.  Lanes then hold four consecutive nodes of one feature, the
+// feature-major store unit of M.  M is kept in fp32 (16-byte stores): it is
+// summed over many edges next, and a bf16 copy would add a rounding of the
+// same size as the bf16 state itself at every step.
+// ---------------------------------------------------------------------------
+template <typename S, int H, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void transform_fwd_kernel(const S* __restrict__ X,
+                                                                       const S* __restrict__ W,
+                                                                       const float* __restrict__ bias,
+                                                                       float* __restrict__ M, int n_pad, int E) {
+  constexpr int NT = WAVES * kWave;
+  constexpr int V = 16 / sizeof(S);
+  constexpr int FC = H < 64 ? H : 64;   // output features per LDS chunk
+  constexpr int PW = H + V;             // W^T tile pitch
+  constexpr int KS = H / 32;
+  constexpr int NTL = FC / 16;
+  __shared__ __attribute__((aligned(16))) S wt[FC * PW];
+
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int q = lane % 16, g = lane / 16;
+  const int node0 = xcd_swizzle(blockIdx.x, gridDim.x) * (32 * WAVES) + 32 * wave;
+  const bool valid = node0 < n_pad;
+
+  frag_t<S> af[2][KS];
+  if (valid) {
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) af[mt][kk] = load8(X + (size_t)(node0 + 16 * mt + q) * H + 32 * kk + 8 * g);
+  }
+  for (int e = 0; e < E; ++e) {
+    for (int oc = 0; oc < H; oc += FC) {
+      __syncthreads();
+      const S* wsrc = W + (size_t)e * H * H + oc;
+      for (int lin = tid; lin < H * FC / V; lin += NT) {
+        int i = lin / (FC / V), o8 = (lin % (FC / V)) * V;
+        u32x4 v = *reinterpret_cast<const u32x4*>(wsrc + (size_t)i * H + o8);
+        const S* pv = reinterpret_cast<const S*>(&v);
+#pragma unroll
+        for (int x = 0; x < V; ++x) wt[(o8 + x) * PW + i] = pv[x];
+      }
+      __syncthreads();
+      if (!valid) continue;
+      f32x4 acc[2][NTL];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NTL; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+        for (int nt = 0; nt < NTL; ++nt) {
+          frag_t<S> bf = load8(&wt[(16 * nt + q) * PW + 32 * kk + 8 * g]);
+          mma(acc[0][nt], af[0][kk], bf);
+          mma(acc[1][nt], af[1][kk], bf);
+        }
+      // D[node = node0 + 16mt + 4g + j][o = oc + 16nt + q]
+#pragma unroll
+      for (int nt = 0; nt < NTL; ++nt) {
+        const int o = oc + 16 * nt + q;
+        const float bb = bias ? bias[e * H + o] : 0.f;
+        float* out = M + ((size_t)e * H + o) * n_pad + node0 + 4 * g;
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+          store4(out + 16 * mt, acc[mt][nt][0] + bb, acc[mt][nt][1] + bb, acc[mt][nt][2] + bb, acc[mt][nt][3] + bb);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Backward, input gradient: dX_out = dX_in + sum_e dM_e W_e^T.
+// A workgroup owns 16*WAVES nodes; wave w: 16 nodes, all H input features.
+// D[h_in][node]: A operand = W_e rows (contiguous in h_out, tiny, cached),
+// B operand = dM_e rows of one node: feature-major dM is staged per type in
+// LDS and read with a stride.  Lanes hold four consecutive features of one
+// node: 16-byte float stores into node-major dX.
+// ---------------------------------------------------------------------------
+template <typename S, int H, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void transform_bwd_dx_kernel(const S* __restrict__ W,
+                                                                          const S* __restrict__ dM,
+                                                                          const float* dX_in, float* dX_out,
+                                                                          int n_pad, int E) {
+  constexpr int NT = WAVES * kWave;
+  constexpr int V = 16 / sizeof(S);
+  constexpr int NW = 16 * WAVES;
+  constexpr int PM = NW + 4 / sizeof(S);
+  constexpr int KS = H / 32;
+  constexpr int MTL = H / 16;
+  __shared__ __attribute__((aligned(16))) S tile[H * PM];
+
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int q = lane % 16, g = lane / 16;
+  const int n0 = xcd_swizzle(blockIdx.x, gridDim.x) * NW;
+  const bool valid = n0 + 16 * wave < n_pad;
+
+  f32x4 acc[MTL];
+#pragma unroll
+  for (int m = 0; m < MTL; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int e = 0; e < E; ++e) {
+    __syncthreads();
+    const S* src = dM + (size_t)e * H * n_pad + n0;
+    for (int lin = tid; lin < H * NW / V; lin += NT) {
+      int h = lin / (NW / V), c = (lin % (NW / V)) * V;
+      if (n0 + c >= n_pad) continue;
+      u32x4 v = *reinterpret_cast<const u32x4*>(src + (size_t)h * n_pad + c);
+      uint32_t* p = reinterpret_cast<uint32_t*>(&tile[h * PM + c]);
+      p[0] = v.x; p[1] = v.y; p[2] = v.z; p[3] = v.w;
+    }
+    __syncthreads();
+    if (!valid) continue;
+    const S* we = W + (size_t)e * H * H;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      frag_t<S> bf = load8_strided(&tile[(32 * kk + 8 * g) * PM + 16 * wave + q], PM);
+#pragma unroll
+      for (int m = 0; m < MTL; ++m) {
+        frag_t<S> afr = load8(we + (size_t)(16 * m + q) * H + 32 * kk + 8 * g);
+        mma(acc[m], afr, bf);
+      }
+    }
+  }
+  if (!valid) return;
+  // D[h_in = 16m + 4g + j][node = n0 + 16*wave + q]
+  const size_t row = (size_t)(n0 + 16 * wave + q) * H + 4 * g;
+#pragma unroll
+  for (int m = 0; m < MTL; ++m) {
+    f32x4 base = dX_in ? *reinterpret_cast<const f32x4*>(dX_in + row + 16 * m) : f32x4{0.f, 0.f, 0.f, 0.f};
+    store4(dX_out + row + 16 * m, base.x + acc[m][0], base.y + acc[m][1], base.z + acc[m][2], base.w + acc[m][3]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Backward, weight gradient, one node split: P[split][e][h_in][h_out] =
+// sum over the split's nodes of X[node][h_in] * dM[e][h_out][node], and the
+// bias partial Pb[split][e][h_out] = sum over nodes of dM[e][h_out][node].
+// Workgroup tile TI x TI (TI = min(H, 64)), TI/16 waves; the contraction
+// over nodes runs in chunks of 64: X (node-major) is staged in LDS and read
+// with a stride, dM (feature-major, contiguous in nodes) is read directly.
+// ---------------------------------------------------------------------------
+template <typename S, int H>
+__global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgrad_kernel(
+    const S* __restrict__ X, const S* __restrict__ dM, float* __restrict__ P, float* __restrict__ Pb, int n_pad,
+    int E, int nodes_per_split) {
+  constexpr int TI = H < 64 ? H : 64;
+  constexpr int WAVES = TI / 16;
+  constexpr int NT = WAVES * kWave;
+  constexpr int V = 16 / sizeof(S);
+  constexpr int KN = 64;                  // nodes per LDS chunk
+  constexpr int PX = TI + 4 / sizeof(S);
+  constexpr int NTL = TI / 16;
+  constexpr int TPD = H / TI;             // tiles per dimension
+  __shared__ __attribute__((aligned(16))) S tile[KN * PX];
+
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int q = lane % 16, g = lane / 16;
+  int bid = blockIdx.x;
+  const int to = bid % TPD; bid /= TPD;
+  const int ti = bid % TPD; bid /= TPD;
+  const int e = bid % E;
+  const int split = bid / E;
+  const int nlo = split * nodes_per_split;
+  const int nhi = min(n_pad, nlo + nodes_per_split);
+
+  f32x4 acc[NTL];
+  float bsum[NTL];
+#pragma unroll
+  for (int n = 0; n < NTL; ++n) {
+    acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    bsum[n] = 0.f;
+  }
+  const bool do_bias = (ti == 0 && wave == 0 && Pb != nullptr);
+  for (int c0 = nlo; c0 < nhi; c0 += KN) {
+    __syncthreads();
+    for (int lin = tid; lin < KN * TI / V; lin += NT) {
+      int r = lin / (TI / V), c = (lin % (TI / V)) * V;
+      if (c0 + r >= nhi) continue;
+      u32x4 v = *reinterpret_cast<const u32x4*>(X + (size_t)(c0 + r) * H + ti * TI + c);
+      uint32_t* p = reinterpret_cast<uint32_t*>(&tile[r * PX + c]);
+      p[0] = v.x; p[1] = v.y; p[2] = v.z; p[3] = v.w;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < KN / 32; ++kk) {
+      if (c0 + 32 * kk >= nhi) break;    // n_pad is a multiple of 32
+      frag_t<S> afr = load8_strided(&tile[(32 * kk + 8 * g) * PX + 16 * wave + q], PX);
+#pragma unroll
+      for (int n = 0; n < NTL; ++n) {
+        const int o = to * TI + 16 * n + q;
+        frag_t<S> bf = load8(dM + ((size_t)e * H + o) * n_pad + c0 + 32 * kk + 8 * g);
+        mma(acc[n], afr, bf);
+        if (do_bias) {
+#pragma unroll
+          for (int x = 0; x < 8; ++x) bsum[n] += static_cast<float>(bf[x]);
+        }
+      }
+    }
+  }
+  // D[h_in = ti*TI + 16*wave + 4g + j][h_out = to*TI + 16n + q]
+  float* out = P + ((size_t)split * E + e) * H * H;
+#pragma unroll
+  for (int n = 0; n < NTL; ++n) {
+    const int o = to * TI + 16 * n + q;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * H + o] = acc[n][j];
+  }
+  if (do_bias) {
+#pragma unroll
+    for (int n = 0; n < NTL; ++n) {
+      float v = bsum[n];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (g == 0) Pb[((size_t)split * E + e) * H + to * TI + 16 * n + q] = v;
+    }
+  }
+}
+
+}  // namespace dev
+
+// out[i] += sum_{s < nsplit} part[s * stride + i] for i < count, summed in
+// split order (fixed, so results do not depend on scheduling).
+__global__ void reduce_partials_kernel(const float* __restrict__ part, float* __restrict__ out, int nsplit,
+                                       int count, long stride) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= count) return;
+  float s = 0.f;
+  for (int k = 0; k < nsplit; ++k) s += part[(size_t)k * stride + i];
+  out[i] += s;
+}
+
+hipError_t launch_reduce_partials(const float* part, float* out, int nsplit, int count, long stride,
+                                  hipStream_t st) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(reduce_partials_kernel, dim3((count + 255) / 256), dim3(256), 0, st, part, out, nsplit, count,
+                     stride);
+  return hipGetLastError();
+}
+
+namespace {
+// Node split of the weight-gradient contraction: enough workgroups to fill
+// the chip, each split a multiple of 64 nodes.
+struct Split {
+  int nsplit, per;
+};
+Split transform_split(int n_pad, int H, int E) {
+  int TI = H < 64 ? H : 64;
+  int tiles = E * (H / TI) * (H / TI);
+  int want = (1024 + tiles - 1) / tiles;
+  int maxs = (n_pad + 63) / 64;
+  int ns = want < maxs ? want : maxs;
+  if (ns < 1) ns = 1;
+  int per = ((n_pad + ns - 1) / ns + 63) / 64 * 64;
+  if (per < 512) per = 512;   // keep the partial traffic well below the node traffic
+  ns = (n_pad + per - 1) / per;
+  return {ns, per};
+}
+
+template <typename S, int H>
+hipError_t transform_fwd_h(int n_pad, int E, const void* X, const void* W, const float* bias, float* M,
+                           hipStream_t st) {
+  const S* xp = static_cast<const S*>(X);
+  const S* wp = static_cast<const S*>(W);
+  float* mp = M;
+  const int tiles4 = (n_pad + 127) / 128;
+  if (tiles4 >= 1024) {
+    hipLaunchKernelGGL((dev::transform_fwd_kernel<S, H, 4>), dim3(tiles4), dim3(256), 0, st, xp, wp, bias, mp, n_pad, E);
+  } else {
+    hipLaunchKernelGGL((dev::transform_fwd_kernel<S, H, 2>), dim3((n_pad + 63) / 64), dim3(128), 0, st, xp, wp, bias,
+                       mp, n_pad, E);
+  }
+  return hipGetLastError();
+}
+
+template <typename S, int H>
+hipError_t transform_bwd_h(int n_pad, int E, const void* X, const void* W, const void* dM, const float* dX_in,
+                           float* dX_out, float* dW, float* dbias, void* ws, hipStream_t st) {
+  const S* xp = static_cast<const S*>(X);
+  const S* wp = static_cast<const S*>(W);
+  const S* dp = static_cast<const S*>(dM);
+  hipLaunchKernelGGL((dev::transform_bwd_dx_kernel<S, H, 4>), dim3((n_pad + 63) / 64), dim3(256), 0, st, wp, dp,
+                     dX_in, dX_out, n_pad, E);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  Split sp = transform_split(n_pad, H, E);
+  constexpr int TI = H < 64 ? H : 64;
+  float* P = static_cast<float*>(ws);
+  float* Pb = dbias ? P + (size_t)sp.nsplit * E * H * H : nullptr;
+  const int blocks = sp.nsplit * E * (H / TI) * (H / TI);
+  hipLaunchKernelGGL((dev::transform_wgrad_kernel<S, H>), dim3(blocks), dim3(TI / 16 * 64), 0, st, xp, dp, P, Pb,
+                     n_pad, E, sp.per);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  err = launch_reduce_partials(P, dW, sp.nsplit, E * H * H, (long)E * H * H, st);
+  if (err != hipSuccess || !dbias) return err;
+  return launch_reduce_partials(Pb, dbias, sp.nsplit, E * H, (long)E * H, st);
+}
+
+template <typename S>
+hipError_t transform_fwd_t(int n_pad, int H, int E, const void* X, const void* W, const float* bias, float* M,
+                           hipStream_t st) {
+  switch (H) {
+    case 32: return transform_fwd_h<S, 32>(n_pad, E, X, W, bias, M, st);
+    case 64: return transform_fwd_h<S, 64>(n_pad, E, X, W, bias, M, st);
+    case 128: return transform_fwd_h<S, 128>(n_pad, E, X, W, bias, M, st);
+    case 256: return transform_fwd_h<S, 256>(n_pad, E, X, W, bias, M, st);
+  }
+  return hipErrorInvalidValue;
+}
+template <typename S>
+hipError_t transform_bwd_t(int n_pad, int H, int E, const void* X, const void* W, const void* dM, const float* dX_in,
+                           float* dX_out, float* dW, float* dbias, void* ws, hipStream_t st) {
+  switch (H) {
+    case 32: return transform_bwd_h<S, 32>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, st);
+    case 64: return transform_bwd_h<S, 64>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, st);
+    case 128: return transform_bwd_h<S, 128>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, st);
+    case 256: return transform_bwd_h<S, 256>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, st);
+  }
+  return hipErrorInvalidValue;
+}
+}  // namespace
+
+size_t transform_bwd_workspace(int dt, int n_pad, int H, int E) {
+  (void)dt;
+  Split sp = transform_split(n_pad, H, E);
+  return ((size_t)sp.nsplit * E * H * H + (size_t)sp.nsplit * E * H) * sizeof(float);
+}
+
+hipError_t launch_transform_fwd(int dt, int n_pad, int H, int E, const void* X, const void* W, const float* bias,
+                                float* M, hipStream_t st) {
+  return dt == GGNN_BF16 ? transform_fwd_t<dev::bf16s>(n_pad, H, E, X, W, bias, M, st)
+                         : transform_fwd_t<float>(n_pad, H, E, X, W, bias, M, st);
+}
+
+hipError_t launch_transform_bwd(int dt, int n_pad, int H, int E, const void* X, const void* W, const void* dM,
+                                const float* dX_in, float* dX_out, float* dW, float* dbias, void* ws,
+                                hipStream_t st) {
+  return dt == GGNN_BF16 ? transform_bwd_t<dev::bf16s>(n_pad, H, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, st)
+                         : transform_bwd_t<float>(n_pad, H, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, st);
+}
+
+}  // namespace ggnn

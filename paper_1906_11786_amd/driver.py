@@ -1,0 +1,155 @@
+"""T-step banded GGNN propagation on one GPU, driven through the C ABI.
+
+`compile_graphs` is the host "compilation" of the paper (Compilation section
+and sparse batching): reverse Cuthill-McKee per graph, labels offset into one
+supergraph, then the block band of Eq. 3.  `BandedGGNN` owns the device
+buffers (allocated with torch, which is only the allocator and stream
+provider here) and runs the forward and reverse passes with ggnn_forward /
+ggnn_backward: every arithmetic step runs in the library's HIP kernels.
+"""
+from __future__ import annotations
+
+import time
+from dataclasses import dataclass, field
+from typing import Optional, Sequence
+
+import numpy as np
+
+from . import capi
+
+
+@dataclass
+class Compiled:
+    n_real: int
+    n_pad: int
+    B: int
+    E: int
+    src: np.ndarray          # final labels (int32)
+    dst: np.ndarray
+    etype: np.ndarray
+    offsets: np.ndarray      # graph g occupies [offsets[g], offsets[g+1])
+    bandwidth: int           # max over graphs after reordering
+    rcm_seconds: float = 0.0
+    stats: dict = field(default_factory=dict)
+
+
+def compile_graphs(graphs: Sequence, B: int, E: int, reorder: bool = True) -> Compiled:
+    """Reorder every graph with reverse Cuthill-McKee (ggnn_rcm_order), then
+    place the graphs one after another (disjoint components of one
+    supergraph) and pad to a multiple of B."""
+    t0 = time.perf_counter()
+    S, D, T, offs = [], [], [], [0]
+    bw = 0
+    for g in graphs:
+        if reorder:
+            _, rank, b = capi.ggnn_rcm_order(g.n, g.src, g.dst)
+            s, d = rank[g.src], rank[g.dst]
+        else:
+            s, d = g.src, g.dst
+            b = capi.ggnn_bandwidth(g.n, s, d)
+        bw = max(bw, b)
+        S.append(s.astype(np.int32) + offs[-1])
+        D.append(d.astype(np.int32) + offs[-1])
+        T.append(g.etype.astype(np.int32))
+        offs.append(offs[-1] + g.n)
+    n_real = offs[-1]
+    n_pad = -(-n_real // B) * B
+    return Compiled(n_real, n_pad, B, E, np.concatenate(S), np.concatenate(D), np.concatenate(T),
+                    np.asarray(offs, np.int64), bw, time.perf_counter() - t0)
+
+
+def torch_dtype(dt: str):
+    import torch
+    return torch.bfloat16 if dt == "bf16" else torch.float32
+
+
+def to_device(x: np.ndarray, dt: str, device="cuda"):
+    """float64 values exactly representable in dt -> device tensor of dt."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(device=device).to(torch_dtype(dt))
+
+
+def band_to_device(band: np.ndarray, dt: str, device="cuda"):
+    import torch
+    if dt == "bf16":
+        return torch.from_numpy(band.view(np.int16)).to(device).view(torch.bfloat16)
+    return torch.from_numpy(band).to(device)
+
+
+class BandedGGNN:
+    """Device state of one workload: band, parameters, stored activations,
+    gradients and workspace, sized for T steps."""
+
+    def __init__(self, comp: Compiled, H: int, T: int, dt: str, params, device="cuda", strict: bool = True):
+        import torch
+        self.torch = torch
+        self.comp, self.H, self.T, self.dt, self.device = comp, H, T, dt, device
+        n_pad, E, B = comp.n_pad, comp.E, comp.B
+        td = torch_dtype(dt)
+        t0 = time.perf_counter()
+        band, packed, dropped, dup = capi.ggnn_banded_pack(n_pad, E, B, comp.src, comp.dst, comp.etype, dt=dt,
+                                                           strict=strict)
+        comp.stats.update(n_packed=packed, n_dropped=dropped, n_duplicate=dup,
+                          pack_seconds=time.perf_counter() - t0)
+        t0 = time.perf_counter()
+        self.band = band_to_device(band, dt, device)
+        del band
+        self.W = to_device(params.W, dt, device)
+        self.bias = None if params.bias is None else torch.from_numpy(params.bias.astype(np.float32)).to(device)
+        self.Wi = to_device(params.Wi, dt, device)
+        self.U = to_device(params.U, dt, device)
+        self.b = torch.from_numpy(params.b.astype(np.float32)).to(device)
+        self.X = torch.empty((T + 1, n_pad, H), dtype=td, device=device)
+        self.X[0].copy_(to_device(params.X, dt, device))
+        self.a = torch.empty((T, n_pad, H), dtype=torch.float32, device=device)
+        self.saved = torch.empty((T, n_pad, 3 * H), dtype=td, device=device)
+        self.M = torch.empty((E, H, n_pad), dtype=torch.float32, device=device)
+        self.G = torch.from_numpy(params.G.astype(np.float32)).to(device)
+        self.dX = torch.empty((n_pad, H), dtype=torch.float32, device=device)
+        self.dW = torch.zeros((E, H, H), dtype=torch.float32, device=device)
+        self.dbias = torch.zeros((E, H), dtype=torch.float32, device=device)
+        self.dWi = torch.zeros((H, 3 * H), dtype=torch.float32, device=device)
+        self.dU = torch.zeros((H, 3 * H), dtype=torch.float32, device=device)
+        self.db = torch.zeros((3 * H,), dtype=torch.float32, device=device)
+        self.da = torch.empty((H, n_pad), dtype=td, device=device)
+        self.dM = torch.empty((E, H, n_pad), dtype=td, device=device)
+        self.dh = torch.empty((n_pad, H), dtype=torch.float32, device=device)
+        self.model = capi.ggnn_model(
+            dtype=capi.DTYPES[dt], n_pad=n_pad, B=B, H=H, E=E, T=T, band=self.band.data_ptr(),
+            W=self.W.data_ptr(), bias=None if self.bias is None else self.bias.data_ptr(), Wi=self.Wi.data_ptr(),
+            U=self.U.data_ptr(), b=self.b.data_ptr())
+        ws = capi.ggnn_backward_workspace_bytes(self.model)
+        self.workspace = torch.empty((max(ws, 16),), dtype=torch.uint8, device=device)
+        self.act = capi.ggnn_activations(X=self.X.data_ptr(), a=self.a.data_ptr(), saved=self.saved.data_ptr(),
+                                         M=self.M.data_ptr())
+        self.grads = capi.ggnn_grads(
+            dX=self.dX.data_ptr(), dW=self.dW.data_ptr(), dbias=self.dbias.data_ptr(), dWi=self.dWi.data_ptr(),
+            dU=self.dU.data_ptr(), db=self.db.data_ptr(), da=self.da.data_ptr(), dM=self.dM.data_ptr(),
+            dh=self.dh.data_ptr(), workspace=self.workspace.data_ptr(), workspace_bytes=self.workspace.numel())
+        comp.stats["upload_seconds"] = time.perf_counter() - t0
+
+    def forward(self, stream=None):
+        capi.ggnn_forward(self.model, self.act, stream)
+
+    def backward(self, stream=None, zero_grads: bool = True):
+        """Reverse pass for L = sum(G * X_T); weight gradients are re-zeroed
+        first unless zero_grads is False (then they accumulate)."""
+        self.dX.copy_(self.G)
+        if zero_grads:
+            for t in (self.dW, self.dbias, self.dWi, self.dU, self.db):
+                t.zero_()
+        capi.ggnn_backward(self.model, self.act, self.grads, stream)
+
+    def step(self, stream=None):
+        """One pass of the hot path: T forward steps then T reverse steps."""
+        self.forward(stream)
+        self.backward(stream)
+
+    def results(self) -> dict:
+        """Host copies (float64) of the outputs compared against the oracle."""
+        f = (lambda t: t.float().cpu().numpy().astype(np.float64))
+        out = dict(XT=f(self.X[self.T]), dX0=f(self.dX), dW=f(self.dW), dWi=f(self.dWi), dU=f(self.dU),
+                   db=f(self.db))
+        if self.bias is not None:
+            out["dbias"] = f(self.dbias)
+        return out

@@ -1,0 +1,207 @@
+"""Per-entry-point parity of the HIP kernels against the CPU oracle, called
+through the C ABI.  Integer-valued cases (every partial sum exact in fp32)
+are compared bitwise, so any indexing slip shows; real-valued cases use the
+fp32 / bf16 tolerances."""
+import numpy as np
+import pytest
+
+import oracle as O
+from gpu_helpers import TOL, relerr, say, dev, host, round_to, torch_dt
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+capi = pytest.importorskip("paper_1906_11786_amd.capi")
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    yield
+    torch.cuda.synchronize()
+
+
+def _edges(rng, n, m, E, span):
+    src = rng.integers(0, n, m)
+    dst = np.clip(src + rng.integers(-span, span + 1, m), 0, n - 1)
+    return src, dst, rng.integers(0, E, m)
+
+
+def _band(dt, n_pad, E, B, src, dst, et):
+    band, packed, dropped, dup = capi.ggnn_banded_pack(n_pad, E, B, src, dst, et, dt=dt)
+    if dt == "bf16":
+        return torch.from_numpy(band.view(np.int16)).cuda().view(torch.bfloat16), dropped
+    return torch.from_numpy(band).cuda(), dropped
+
+
+# (B, H, E, nb): several block rows, each block size and feature width.
+BANDED_CASES = [(32, 32, 2, 7), (64, 64, 3, 5), (128, 64, 2, 4), (128, 128, 2, 3), (256, 128, 1, 3),
+                (512, 32, 2, 2), (128, 256, 2, 3), (256, 256, 1, 2), (64, 32, 1, 1)]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("B,H,E,nb", BANDED_CASES)
+def test_banded_propagate_integer_exact(dt, B, H, E, nb):
+    say(f"banded_propagate int dt={dt} B={B} H={H} E={E} nb={nb}")
+    rng = np.random.default_rng(B * 131 + H + E)
+    n = B * nb
+    src, dst, et = _edges(rng, n, 6 * n, E, 2 * B + 5)
+    band, dropped = _band(dt, n, E, B, src, dst, et)
+    assert nb < 3 or dropped > 0      # with fewer than three blocks nothing can fall outside the band
+    M = rng.integers(-4, 5, (E, n, H)).astype(np.float64)
+    Mt = dev(M.transpose(0, 2, 1))                      # feature-major [E][H][n], float
+    a = torch.full((n, H), float("nan"), device="cuda")
+    capi.ggnn_banded_propagate(dt, n, B, H, E, band, Mt, a)
+    s, d, e, _, _ = O.kept_edges(src, dst, et, B)
+    np.testing.assert_array_equal(host(a), O.aggregate(n, s, d, e, M))
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("B,H,E,nb", BANDED_CASES)
+def test_banded_propagate_bwd_integer_exact(dt, B, H, E, nb):
+    say(f"banded_propagate_bwd int dt={dt} B={B} H={H} E={E} nb={nb}")
+    rng = np.random.default_rng(B * 17 + H + E)
+    n = B * nb
+    src, dst, et = _edges(rng, n, 6 * n, E, 2 * B + 5)
+    band, _ = _band(dt, n, E, B, src, dst, et)
+    da = rng.integers(-4, 5, (n, H)).astype(np.float64)
+    dM = torch.full((E, H, n), float("nan"), device="cuda", dtype=torch_dt(dt))
+    capi.ggnn_banded_propagate_bwd(dt, n, B, H, E, band, dev(da.T, dt), dM)
+    s, d, e, _, _ = O.kept_edges(src, dst, et, B)
+    want = O.aggregate_transpose(n, s, d, e, da, E)
+    np.testing.assert_array_equal(host(dM), want.transpose(0, 2, 1))
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_banded_forward_backward_adjoint(dt):
+    """<A M, D> = <M, A^T D> through the two kernels (real values)."""
+    rng = np.random.default_rng(3)
+    B, H, E, nb = 128, 64, 3, 4
+    n = B * nb
+    src, dst, et = _edges(rng, n, 8 * n, E, 2 * B)
+    band, _ = _band(dt, n, E, B, src, dst, et)
+    M = round_to("f32", rng.standard_normal((E, n, H)))
+    D = round_to(dt, rng.standard_normal((n, H)))
+    a = torch.empty((n, H), device="cuda")
+    capi.ggnn_banded_propagate(dt, n, B, H, E, band, dev(M.transpose(0, 2, 1)), a)
+    dM = torch.empty((E, H, n), device="cuda", dtype=torch_dt(dt))
+    capi.ggnn_banded_propagate_bwd(dt, n, B, H, E, band, dev(D.T, dt), dM)
+    lhs = float(np.sum(host(a) * D))
+    rhs = float(np.sum(M.transpose(0, 2, 1) * host(dM)))
+    assert abs(lhs - rhs) <= TOL[dt] * np.sqrt(np.sum(host(a) ** 2) * np.sum(D ** 2))
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("H", [32, 64, 128, 256])
+@pytest.mark.parametrize("n", [96, 1184])
+def test_msg_transform(dt, H, n):
+    say(f"msg_transform dt={dt} H={H} n={n}")
+    rng = np.random.default_rng(H + n)
+    E = 3
+    # integer-valued: exact in every dtype
+    X = rng.integers(-1, 2, (n, H)).astype(np.float64)
+    W = rng.integers(-1, 2, (E, H, H)).astype(np.float64)
+    M = torch.full((E, H, n), float("nan"), device="cuda")
+    capi.ggnn_msg_transform(dt, n, H, E, dev(X, dt), dev(W, dt), None, M)
+    np.testing.assert_array_equal(host(M), O.msg_transform(X, W).transpose(0, 2, 1))
+    # real-valued with bias
+    X = round_to(dt, rng.standard_normal((n, H)))
+    W = round_to(dt, rng.standard_normal((E, H, H)) / np.sqrt(H))
+    bias = rng.uniform(-0.2, 0.2, (E, H)).astype(np.float32).astype(np.float64)
+    capi.ggnn_msg_transform(dt, n, H, E, dev(X, dt), dev(W, dt), dev(bias), M)
+    assert relerr(host(M), O.msg_transform(X, W, bias).transpose(0, 2, 1)) <= TOL["f32"]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("H", [32, 64, 128, 256])
+@pytest.mark.parametrize("n", [96, 1184])
+def test_msg_transform_bwd(dt, H, n):
+    say(f"msg_transform_bwd dt={dt} H={H} n={n}")
+    rng = np.random.default_rng(7 * H + n)
+    E = 3
+    X = rng.integers(-1, 2, (n, H)).astype(np.float64)
+    W = rng.integers(-1, 2, (E, H, H)).astype(np.float64)
+    dM = rng.integers(-2, 3, (E, n, H)).astype(np.float64)
+    dX_in = rng.integers(-3, 4, (n, H)).astype(np.float64)
+    ws_n = capi.ggnn_msg_transform_bwd_workspace_bytes(dt, n, H, E)
+    ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda")
+    dX = torch.full((n, H), float("nan"), device="cuda")
+    dW = dev(np.ones((E, H, H)))            # += semantics: start from ones
+    dbias = dev(np.ones((E, H)))
+    capi.ggnn_msg_transform_bwd(dt, n, H, E, dev(X, dt), dev(W, dt), dev(dM.transpose(0, 2, 1), dt), dev(dX_in),
+                                dX, dW, dbias, ws, ws_n)
+    wdX, wdW, wdb = O.msg_transform_backward(X, W, dM)
+    np.testing.assert_array_equal(host(dX), dX_in + wdX)
+    np.testing.assert_array_equal(host(dW), 1 + wdW)
+    np.testing.assert_array_equal(host(dbias), 1 + wdb)
+    # in place (dX_in == dX_out), no bias gradient
+    dX2 = dev(dX_in)
+    capi.ggnn_msg_transform_bwd(dt, n, H, E, dev(X, dt), dev(W, dt), dev(dM.transpose(0, 2, 1), dt), dX2, dX2,
+                                dW, None, ws, ws_n)
+    np.testing.assert_array_equal(host(dX2), dX_in + wdX)
+    np.testing.assert_array_equal(host(dW), 1 + 2 * wdW)
+
+
+def _gru_inputs(dt, rng, n, H):
+    a = rng.standard_normal((n, H)).astype(np.float32).astype(np.float64)
+    h = round_to(dt, rng.standard_normal((n, H)))
+    k = 1 / np.sqrt(H)
+    Wi = round_to(dt, rng.uniform(-k, k, (H, 3 * H)))
+    U = round_to(dt, rng.uniform(-k, k, (H, 3 * H)))
+    b = rng.uniform(-k, k, 3 * H).astype(np.float32).astype(np.float64)
+    return a, h, Wi, U, b
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("H", [32, 64, 128, 256])
+@pytest.mark.parametrize("n", [96, 1184])
+def test_gru_update(dt, H, n):
+    say(f"gru_update dt={dt} H={H} n={n}")
+    rng = np.random.default_rng(11 * H + n)
+    a, h, Wi, U, b = _gru_inputs(dt, rng, n, H)
+    h_out = torch.full((n, H), float("nan"), device="cuda", dtype=torch_dt(dt))
+    saved = torch.full((n, 3 * H), float("nan"), device="cuda", dtype=torch_dt(dt))
+    capi.ggnn_gru_update(dt, n, H, dev(a), dev(h, dt), dev(Wi, dt), dev(U, dt), dev(b), h_out, saved)
+    hn, r, z, nn = O.gru_forward(a, h, Wi, U, b)
+    assert relerr(host(h_out), hn) <= TOL[dt]
+    assert relerr(host(saved), np.concatenate([r, z, nn], axis=1)) <= TOL[dt]
+    h_out2 = torch.full((n, H), float("nan"), device="cuda", dtype=torch_dt(dt))
+    capi.ggnn_gru_update(dt, n, H, dev(a), dev(h, dt), dev(Wi, dt), dev(U, dt), dev(b), h_out2, None)
+    assert torch.equal(h_out, h_out2)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("H", [32, 64, 128, 256])
+@pytest.mark.parametrize("n", [96, 1184])
+def test_gru_update_bwd(dt, H, n):
+    say(f"gru_update_bwd dt={dt} H={H} n={n}")
+    rng = np.random.default_rng(13 * H + n)
+    a, h, Wi, U, b = _gru_inputs(dt, rng, n, H)
+    _, r, z, nn = O.gru_forward(a, h, Wi, U, b)
+    saved = round_to(dt, np.concatenate([r, z, nn], axis=1))
+    r, z, nn = saved[:, :H], saved[:, H:2 * H], saved[:, 2 * H:]
+    g = rng.standard_normal((n, H)).astype(np.float32).astype(np.float64)
+    ws_n = capi.ggnn_gru_update_bwd_workspace_bytes(dt, n, H)
+    ws = torch.empty(ws_n, dtype=torch.uint8, device="cuda")
+    da = torch.full((H, n), float("nan"), device="cuda", dtype=torch_dt(dt))
+    dh = torch.full((n, H), float("nan"), device="cuda")
+    dWi, dU, db = dev(np.ones((H, 3 * H))), dev(np.ones((H, 3 * H))), dev(np.ones(3 * H))
+    capi.ggnn_gru_update_bwd(dt, n, H, dev(g), dev(a), dev(h, dt), dev(saved, dt), dev(Wi, dt), dev(U, dt), da, dh,
+                             dWi, dU, db, ws, ws_n)
+    wda, wdh, wdWi, wdU, wdb = O.gru_backward(g, a, h, r, z, nn, Wi, U)
+    assert relerr(host(da).T, wda) <= TOL[dt]
+    assert relerr(host(dh), wdh) <= TOL[dt]
+    assert relerr(host(dWi) - 1, wdWi) <= TOL[dt]
+    assert relerr(host(dU) - 1, wdU) <= TOL[dt]
+    assert relerr(host(db) - 1, wdb) <= TOL[dt]
+
+
+def test_device_errors_are_reported():
+    n, H = 128, 64
+    ws_n = capi.ggnn_gru_update_bwd_workspace_bytes("bf16", n, H)
+    small = torch.empty(ws_n // 2, dtype=torch.uint8, device="cuda")
+    x = [torch.zeros((n, 3 * H), device="cuda") for _ in range(11)]
+    with pytest.raises(capi.GGNNError) as ei:
+        capi.ggnn_gru_update_bwd("bf16", n, H, *x, small, ws_n // 2)
+    assert ei.value.status_name == "GGNN_ERR_WORKSPACE"

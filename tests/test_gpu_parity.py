@@ -1,0 +1,193 @@
+"""T-step forward + reverse parity of the whole hot path (ggnn_forward /
+ggnn_backward through the C ABI) against the CPU oracle, on the synthetic
+workloads at their full sizes and on small cases spanning tiles and ragged
+tails.  Large batches are checked on sampled graphs: graphs in a supergraph
+do not interact, so the oracle runs on a few of them alone, and a second
+reverse pass with the upstream gradient restricted to those graphs gives
+weight gradients comparable with the oracle's."""
+import numpy as np
+import pytest
+
+import oracle as O
+from ggnn_synth import CONFIGS, make_graphs, sweep_blocks, draw_params, backbone_graph, scramble_graph, Graph
+from gpu_helpers import TOL, relerr, say
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+drv = pytest.importorskip("paper_1906_11786_amd.driver")
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _oracle_edges(graphs, B, reorder):
+    """Final labelling computed by the oracle's own reordering."""
+    parts = []
+    for g in graphs:
+        if reorder:
+            _, rank = O.rcm_order(g.n, g.src, g.dst)
+            s, d = O.relabel(rank, g.src, g.dst)
+        else:
+            s, d = g.src, g.dst
+        parts.append((g.n, s, d, g.etype))
+    return O.batch_layout(parts, B)
+
+
+def _compare(res, out, dt, keys=("XT", "dX0", "dW", "dWi", "dU", "db"), rows=None):
+    want = dict(XT=out["X"][-1], dX0=out["dX0"], dW=out["dW"], dWi=out["dWi"], dU=out["dU"], db=out["db"])
+    if "dbias" in res:
+        want["dbias"] = out["dbias"]
+        keys = tuple(keys) + ("dbias",)
+    errs = {}
+    for k in keys:
+        g = res[k] if rows is None or k not in ("XT", "dX0") else res[k][rows]
+        w = want[k]
+        errs[k] = relerr(g, w)
+    say("  errors:", {k: f"{v:.2e}" for k, v in errs.items()})
+    for k, v in errs.items():
+        assert v <= TOL[dt], (k, v)
+    return errs
+
+
+def _run_full(graphs, spec_B, E, H, T, dt, cfg, reorder, with_bias=False):
+    comp = drv.compile_graphs(graphs, spec_B, E, reorder=reorder)
+    n_real, n_pad, s, d, e, offs = _oracle_edges(graphs, spec_B, reorder)
+    assert (n_real, n_pad) == (comp.n_real, comp.n_pad)
+    np.testing.assert_array_equal(comp.src, s)         # the product's reordering equals the oracle's
+    np.testing.assert_array_equal(comp.dst, d)
+    params = draw_params(cfg, n_real, n_pad, H, E, dt, with_bias=with_bias)
+    m = drv.BandedGGNN(comp, H, T, dt, params)
+    m.step()
+    torch.cuda.synchronize()
+    res = m.results()
+    out = O.propagate(n_pad, spec_B, s, d, e, params.X, params.W, params.Wi, params.U, params.b, T, G=params.G,
+                      bias=params.bias)
+    assert comp.stats["n_dropped"] == out["n_dropped"]
+    return m, res, out
+
+
+def test_tiny_fp32_workload():
+    spec = CONFIGS[0]
+    say(f"workload {spec.name}")
+    g = make_graphs(spec)
+    _, res, out = _run_full(g, spec.B, spec.E, spec.H, spec.T, spec.dtype, spec.cfg, reorder=False)
+    assert out["n_dropped"] == 0
+    _compare(res, out, "f32")
+
+
+SMALL = [  # (dt, n_nodes, B, E, H, T, bias)
+    ("f32", 700, 64, 2, 64, 2, True),
+    ("f32", 1000, 128, 3, 128, 2, False),
+    ("f32", 300, 32, 2, 32, 3, True),
+    ("bf16", 1500, 128, 4, 64, 3, True),
+    ("bf16", 900, 32, 3, 32, 4, False),
+    ("bf16", 1300, 256, 2, 256, 2, True),
+    ("bf16", 2000, 512, 2, 128, 2, False),
+    ("bf16", 1100, 64, 5, 128, 3, True),
+]
+
+
+@pytest.mark.parametrize("dt,n,B,E,H,T,bias", SMALL)
+def test_small_cases(dt, n, B, E, H, T, bias):
+    say(f"small dt={dt} n={n} B={B} E={E} H={H} T={T} bias={bias}")
+    g = scramble_graph(50 + n, 0, backbone_graph(50 + n, 0, n, E, span_mean=6.0, max_span=B))[0]
+    _, res, out = _run_full([g], B, E, H, T, dt, 50 + n, reorder=True, with_bias=bias)
+    _compare(res, out, dt)
+
+
+def test_small_lossy_band():
+    """Bandwidth above the block size: edges outside the three block
+    diagonals are dropped identically by both sides."""
+    dt, n, B, E, H, T = "bf16", 1200, 32, 3, 64, 2
+    g = backbone_graph(77, 0, n, E, span_mean=20.0, max_span=90)
+    comp = drv.compile_graphs([g], B, E, reorder=False)
+    params = draw_params(77, comp.n_real, comp.n_pad, H, E, dt)
+    m = drv.BandedGGNN(comp, H, T, dt, params, strict=False)
+    assert comp.stats["n_dropped"] > 0
+    m.step()
+    out = O.propagate(comp.n_pad, B, g.src, g.dst, g.etype, params.X, params.W, params.Wi, params.U, params.b, T,
+                      G=params.G)
+    assert out["n_dropped"] == comp.stats["n_dropped"]
+    _compare(m.results(), out, dt)
+
+
+def test_program_graph_workload():
+    spec = CONFIGS[1]
+    say(f"workload {spec.name}")
+    g = make_graphs(spec)
+    m, res, out = _run_full(g, spec.B, spec.E, spec.H, spec.T, spec.dtype, spec.cfg, reorder=True)
+    assert out["n_dropped"] == 0 and m.comp.bandwidth <= spec.B - 1
+    _compare(res, out, spec.dtype)
+    # determinism: a second pass gives identical bits
+    m.step()
+    torch.cuda.synchronize()
+    res2 = m.results()
+    for k in res:
+        assert np.array_equal(res[k], res2[k]), k
+
+
+@pytest.mark.parametrize("spec", sweep_blocks(), ids=lambda s: f"B{s.B}")
+def test_sweep_workloads(spec):
+    say(f"workload {spec.name}")
+    g = make_graphs(spec)
+    _, res, out = _run_full(g, spec.B, spec.E, spec.H, spec.T, spec.dtype, spec.cfg, reorder=False)
+    assert out["n_dropped"] == 0
+    _compare(res, out, spec.dtype)
+
+
+def _sampled_batch(spec, picks):
+    graphs = make_graphs(spec)
+    say(f"workload {spec.name}: {len(graphs)} graphs, {sum(g.n for g in graphs)} nodes; sampling {picks}")
+    comp = drv.compile_graphs(graphs, spec.B, spec.E, reorder=True)
+    params = draw_params(spec.cfg, comp.n_real, comp.n_pad, spec.H, spec.E, spec.dtype)
+    m = drv.BandedGGNN(comp, spec.H, spec.T, spec.dtype, params)
+    assert comp.stats["n_dropped"] == 0
+    m.forward()
+    m.backward()
+    torch.cuda.synchronize()
+    full = m.results()
+    # restrict the upstream gradient to the sampled graphs and run the reverse pass again
+    mask = np.zeros(comp.n_pad, bool)
+    for gi in picks:
+        mask[comp.offsets[gi]:comp.offsets[gi + 1]] = True
+    m.G.mul_(torch.from_numpy(mask.astype(np.float32)).to(m.G.device)[:, None])
+    m.backward()
+    torch.cuda.synchronize()
+    masked = m.results()
+    acc = {}
+    for gi in picks:
+        g = graphs[gi]
+        o = slice(int(comp.offsets[gi]), int(comp.offsets[gi + 1]))
+        _, rank = O.rcm_order(g.n, g.src, g.dst)
+        s, d = O.relabel(rank, g.src, g.dst)
+        np.testing.assert_array_equal(comp.src[(comp.src >= o.start) & (comp.src < o.stop)].size,
+                                      s.size)
+        out = O.propagate(g.n, g.n, s, d, g.etype, params.X[o], params.W, params.Wi, params.U, params.b, spec.T,
+                          G=params.G[o])
+        # rows of this graph, from the full run (graphs do not interact)
+        rows = slice(o.start, o.stop)
+        e1 = relerr(full["XT"][rows], out["X"][-1])
+        e2 = relerr(full["dX0"][rows], out["dX0"])
+        say(f"  graph {gi} n={g.n}: XT {e1:.2e} dX0 {e2:.2e}")
+        assert e1 <= TOL[spec.dtype] and e2 <= TOL[spec.dtype]
+        for k in ("dW", "dWi", "dU", "db"):
+            acc[k] = acc.get(k, 0) + out[k]
+    for k in ("dW", "dWi", "dU", "db"):
+        e = relerr(masked[k], acc[k])
+        say(f"  {k} (sampled graphs) {e:.2e}")
+        assert e <= TOL[spec.dtype], k
+
+
+def test_batch_100k_workload_sampled():
+    _sampled_batch(CONFIGS[2], picks=[0, 7, 19])
+
+
+def test_stress_1m_workload_sampled():
+    _sampled_batch(CONFIGS[4], picks=[0, 70, 139])

@@ -1,0 +1,161 @@
+"""Host side of the C-ABI, on the CPU: the library loads and exports every
+declared symbol, reverse Cuthill-McKee and block packing are bit-exact
+against the oracle, and argument validation reports errors."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as O
+from ggnn_synth import CONFIGS, make_graphs, backbone_graph, scramble_graph, local_window_graph
+
+capi = pytest.importorskip("paper_1906_11786_amd.capi")
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _need_lib():
+    if not os.path.exists(capi.LIB_PATH):
+        pytest.fail("libggnn.so is not built (python -m paper_1906_11786_amd.build)")
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "ggnn.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ggnn_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    _need_lib()
+    L = capi.lib()
+    declared = _declared_functions()
+    assert len(declared) >= 18
+    for name in declared:
+        assert hasattr(L, name), name
+    assert set(declared) == set(capi.EXPORTS)
+    assert capi.ggnn_abi_version() == 1
+    assert capi.ggnn_status_string(3) == "GGNN_ERR_OUT_OF_BAND"
+
+
+def _graphs():
+    out = []
+    g = backbone_graph(11, 0, 3000, 4, span_mean=8.0)
+    out.append(scramble_graph(11, 0, g)[0])
+    out.append(local_window_graph(12, 0, 700, 3, 40, 0.02))     # several components, isolated nodes likely
+    rng = np.random.default_rng(5)
+    n = 400
+    s = rng.integers(0, n, 600); d = rng.integers(0, n, 600)
+    out.append(type(g)(n, s.astype(np.int32), d.astype(np.int32), np.zeros(600, np.int32)))
+    # path, star, empty, single node, self-loops only
+    p = rng.permutation(50)
+    out.append(type(g)(50, p[:-1].astype(np.int32), p[1:].astype(np.int32), np.zeros(49, np.int32)))
+    out.append(type(g)(9, np.zeros(8, np.int32), np.arange(1, 9, dtype=np.int32), np.zeros(8, np.int32)))
+    out.append(type(g)(7, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32)))
+    out.append(type(g)(1, np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros(0, np.int32)))
+    out.append(type(g)(5, np.arange(5, dtype=np.int32), np.arange(5, dtype=np.int32), np.zeros(5, np.int32)))
+    return out
+
+
+def test_rcm_bit_exact_against_oracle():
+    _need_lib()
+    for g in _graphs():
+        order, rank, bw = capi.ggnn_rcm_order(g.n, g.src, g.dst)
+        o_order, o_rank = O.rcm_order(g.n, g.src, g.dst)
+        np.testing.assert_array_equal(order, o_order)
+        np.testing.assert_array_equal(rank, o_rank)
+        s, d = O.relabel(o_rank, g.src, g.dst)
+        assert bw == O.bandwidth(s, d)
+        assert capi.ggnn_bandwidth(g.n, g.src, g.dst, rank) == bw
+        assert capi.ggnn_bandwidth(g.n, g.src, g.dst) == O.bandwidth(g.src, g.dst)
+
+
+def test_rcm_bit_exact_on_program_graph_workload():
+    _need_lib()
+    g = make_graphs(CONFIGS[1])[0]
+    order, rank, bw = capi.ggnn_rcm_order(g.n, g.src, g.dst)
+    o_order, _ = O.rcm_order(g.n, g.src, g.dst)
+    np.testing.assert_array_equal(order, o_order)
+    assert bw <= CONFIGS[1].B - 1
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("B", [4, 8, 32])
+def test_pack_bit_exact_against_oracle(dt, B):
+    _need_lib()
+    rng = np.random.default_rng(B)
+    nb, E = 9, 3
+    n = nb * B
+    src = rng.integers(0, n, 900)
+    dst = np.clip(src + rng.integers(-3 * B, 3 * B + 1, 900), 0, n - 1)
+    et = rng.integers(0, E, 900)
+    src = np.concatenate([src, src[:50]]); dst = np.concatenate([dst, dst[:50]]); et = np.concatenate([et, et[:50]])
+    band, packed, dropped, dup = capi.ggnn_banded_pack(n, E, B, src, dst, et, dt=dt)
+    ob = O.pack_band(n, E, B, src, dst, et)
+    s, d, e, odrop, odup = O.kept_edges(src, dst, et, B)
+    bits = (band == (1.0 if dt == "f32" else 0x3F80))
+    assert set(np.unique(band).tolist()) <= ({0.0, 1.0} if dt == "f32" else {0, 0x3F80})
+    np.testing.assert_array_equal(bits, ob == 1.0)
+    assert (packed, dropped, dup) == (len(s), odrop, odup)
+    assert dropped > 0 and dup >= 50
+
+
+def test_pack_with_rank_equals_pack_of_relabelled_edges():
+    _need_lib()
+    g = scramble_graph(13, 0, backbone_graph(13, 0, 1000, 2))[0]
+    order, rank, bw = capi.ggnn_rcm_order(g.n, g.src, g.dst)
+    n_pad = 1024
+    rk = np.concatenate([rank, np.arange(g.n, n_pad, dtype=np.int32)])
+    a, *ca = capi.ggnn_banded_pack(n_pad, 2, 32, g.src, g.dst, g.etype, rank=rk, dt="bf16")
+    s, d = O.relabel(rank, g.src, g.dst)
+    b, *cb = capi.ggnn_banded_pack(n_pad, 2, 32, s, d, g.etype, dt="bf16")
+    np.testing.assert_array_equal(a, b)
+    assert ca == cb
+
+
+def test_pack_strict_and_validation_errors():
+    _need_lib()
+    src = np.array([0, 100]); dst = np.array([1, 0]); et = np.array([0, 0])
+    with pytest.raises(capi.GGNNError) as ei:
+        capi.ggnn_banded_pack(128, 1, 32, src, dst, et, strict=True)
+    assert ei.value.status_name == "GGNN_ERR_OUT_OF_BAND"
+    _, p, d, u = capi.ggnn_banded_pack(128, 1, 32, src, dst, et, strict=False)
+    assert (p, d, u) == (1, 1, 0)
+    bad = [
+        dict(n_pad=100, E=1, B=32, src=src, dst=dst, et=et),            # n_pad not a multiple of B
+        dict(n_pad=128, E=1, B=32, src=np.array([128]), dst=np.array([0]), et=np.array([0])),  # id out of range
+        dict(n_pad=128, E=1, B=32, src=src, dst=dst, et=np.array([0, 1])),  # type out of range
+        dict(n_pad=128, E=0, B=32, src=src, dst=dst, et=et),            # no edge types
+    ]
+    for kw in bad:
+        with pytest.raises(capi.GGNNError) as ei:
+            capi.ggnn_banded_pack(kw["n_pad"], kw["E"], kw["B"], kw["src"], kw["dst"], kw["et"])
+        assert ei.value.status_name == "GGNN_ERR_INVALID_ARG"
+        assert capi.ggnn_last_error().startswith("GGNN_ERR_INVALID_ARG")
+    with pytest.raises(capi.GGNNError):
+        capi.ggnn_rcm_order(3, [0, 5], [1, 2])
+    assert capi.ggnn_band_bytes(512, 2, 64, "f32") == 2 * 8 * 3 * 64 * 64 * 4
+    assert capi.ggnn_band_bytes(20096, 10, 128, "bf16") == 10 * 157 * 3 * 128 * 128 * 2
+    assert capi.ggnn_band_bytes(100, 2, 64, "f32") == 0
+
+
+def test_device_entry_points_validate_before_touching_the_gpu():
+    """Invalid sizes are rejected on the host, so this runs without a GPU."""
+    _need_lib()
+    for H in [16, 48, 512]:
+        with pytest.raises(capi.GGNNError) as ei:
+            capi.ggnn_msg_transform("bf16", 128, H, 2, 16, 16, None, 16, stream=0)
+        assert ei.value.status_name == "GGNN_ERR_INVALID_ARG"
+    with pytest.raises(capi.GGNNError):
+        capi.ggnn_banded_propagate("bf16", 96, 64, 64, 2, 16, 16, 16, stream=0)   # 96 % 64 != 0
+    with pytest.raises(capi.GGNNError):
+        capi.ggnn_banded_propagate("bf16", 128, 48, 64, 2, 16, 16, 16, stream=0)  # unsupported B
+    with pytest.raises(capi.GGNNError):
+        capi.ggnn_banded_propagate("bf16", 128, 64, 64, 2, None, 16, 16, stream=0)  # NULL band
+    with pytest.raises(capi.GGNNError):
+        capi.ggnn_banded_propagate("bf16", 128, 64, 64, 2, 8, 16, 16, stream=0)   # misaligned band
+    with pytest.raises(capi.GGNNError) as ei:
+        capi.ggnn_gru_update_bwd("bf16", 128, 64, 16, 16, 16, 16, 16, 16, 16, 32, 16, 16, 16, 16, 0, stream=0)
+    assert ei.value.status_name == "GGNN_ERR_WORKSPACE"
+    assert capi.ggnn_gru_update_bwd_workspace_bytes("bf16", 20096, 64) > 0
+    assert capi.ggnn_msg_transform_bwd_workspace_bytes("bf16", 20096, 64, 10) > 0
+    assert capi.ggnn_msg_transform_bwd_workspace_bytes("bf16", 20096, 48, 10) == 0
