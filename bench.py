@@ -24,6 +24,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix cores
+FP32_PEAK_TFLOPS = 157.3    # MI355X fp32 matrix cores
 
 WORKLOADS = {"program_graph": 1, "tiny": 0, "batch_100k": 2, "stress_1m": 4}
 
@@ -35,6 +36,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--workload", default="program_graph",
                    help="program_graph (default), tiny, batch_100k, stress_1m, or sweep_B<block>")
+    p.add_argument("--band", choices=["bits", "dense"], default="bits",
+                   help="band storage: 1 bit per entry (aggregate-first fused forward) or dense in the compute dtype")
     p.add_argument("--kernel-reps", type=int, default=50, help="launches per kernel for the roofline timing")
     p.add_argument("--no-cpu-baseline", action="store_true")
     return p.parse_args()
@@ -52,15 +55,23 @@ def spec_for(name):
     raise SystemExit(f"unknown workload {name}")
 
 
-def banded_bytes(n_pad, B, E, H, es, fwd: bool):
-    """Algorithmic HBM bytes of one banded launch: the band (three blocks per
-    block row and type, minus the two empty corner blocks), the messages (or
-    gradients) read once and the output written once."""
+def kernel_costs(fmt, n_pad, B, E, H, es):
+    """Algorithmic flops and HBM bytes of one launch of each banded kernel.
+    Three full B x B block products per block row and edge type (the two
+    corner blocks outside the matrix are never read), plus the per-type
+    transform where the kernel fuses it; operands read once, outputs written
+    once."""
     nb = n_pad // B
-    band = (3 * nb - 2) * E * B * B * es
-    if fwd:
-        return band + E * H * n_pad * es + n_pad * H * 4      # M in, a (fp32) out
-    return band + H * n_pad * es + E * H * n_pad * es         # da in, dM out
+    blocks = (3 * nb - 2) * E
+    agg_flops = 2.0 * blocks * B * B * H
+    if fmt == "bits":
+        band = blocks * B * B // 8
+        fwd = (agg_flops + 2.0 * n_pad * E * H * H, band + n_pad * H * es + E * H * H * es + n_pad * H * 4)
+        bwd = (agg_flops, band + H * n_pad * es + E * H * n_pad * es)
+        return {"banded_step_bits": fwd, "banded_propagate_bits_bwd": bwd}
+    band = blocks * B * B * es
+    return {"banded_propagate": (agg_flops, band + E * H * n_pad * 4 + n_pad * H * 4),
+            "banded_propagate_bwd": (agg_flops, band + H * n_pad * es + E * H * n_pad * es)}
 
 
 def time_kernel(fn, reps, torch):
@@ -124,7 +135,7 @@ def main():
     gen_s = time.perf_counter() - t0
     comp = compile_graphs(graphs, spec.B, spec.E, reorder=spec.reorder)
     params = draw_params(spec.cfg, comp.n_real, comp.n_pad, spec.H, spec.E, spec.dtype)
-    m = BandedGGNN(comp, spec.H, spec.T, spec.dtype, params)
+    m = BandedGGNN(comp, spec.H, spec.T, spec.dtype, params, band_format=args.band)
     torch.cuda.synchronize()
 
     for _ in range(args.warmup):
@@ -142,25 +153,38 @@ def main():
     sec_per_step = max(wall, dev_s) / args.steps
     value = comp.n_real * spec.T / sec_per_step
 
-    # Roofline of the banded contractions: each launch timed on the stream it
-    # runs on, in the same launch configuration as inside the step.
+    # Roofline of the banded kernels: each launch timed with HIP events on the
+    # stream it runs on, in the same launch shape as inside the step.
     es = 2 if spec.dtype == "bf16" else 4
     n_pad, B, E, H = comp.n_pad, spec.B, spec.E, spec.H
-    fwd_s = time_kernel(lambda: capi.ggnn_banded_propagate(spec.dtype, n_pad, B, H, E, m.band, m.M, m.a[0]),
-                        args.kernel_reps, torch)
-    bwd_s = time_kernel(lambda: capi.ggnn_banded_propagate_bwd(spec.dtype, n_pad, B, H, E, m.band, m.da, m.dM),
-                        args.kernel_reps, torch)
-    kern = {"banded_propagate": (fwd_s, banded_bytes(n_pad, B, E, H, es, True)),
-            "banded_propagate_bwd": (bwd_s, banded_bytes(n_pad, B, E, H, es, False))}
-    dom = max(kern, key=lambda k: kern[k][0])
-    dur, nbytes = kern[dom]
-    achieved = nbytes / dur / 1e9
-    flops = 6.0 * n_pad * B * H * E
-    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                "avg_launch_us": round(dur * 1e6, 2), "algorithmic_bytes": int(nbytes),
-                "mfma_frac_bf16": round(flops / dur / 1e12 / BF16_PEAK_TFLOPS, 4),
-                "other_banded_us": {k: round(v[0] * 1e6, 2) for k, v in kern.items() if k != dom}}
+    if args.band == "bits":
+        fns = {"banded_step_bits": lambda: capi.ggnn_banded_step_bits(spec.dtype, n_pad, B, H, E, m.band, m.X[0],
+                                                                      m.W, m.bias, m.a[0]),
+               "banded_propagate_bits_bwd": lambda: capi.ggnn_banded_propagate_bits_bwd(spec.dtype, n_pad, B, H, E,
+                                                                                        m.band_t, m.da, m.dM)}
+    else:
+        fns = {"banded_propagate": lambda: capi.ggnn_banded_propagate(spec.dtype, n_pad, B, H, E, m.band, m.M,
+                                                                      m.a[0]),
+               "banded_propagate_bwd": lambda: capi.ggnn_banded_propagate_bwd(spec.dtype, n_pad, B, H, E, m.band,
+                                                                              m.da, m.dM)}
+    costs = kernel_costs(args.band, n_pad, B, E, H, es)
+    times = {k: time_kernel(f, args.kernel_reps, torch) for k, f in fns.items()}
+    dom = max(times, key=times.get)
+    dur = times[dom]
+    flops, nbytes = costs[dom]
+    mfma_peak = BF16_PEAK_TFLOPS if spec.dtype == "bf16" else FP32_PEAK_TFLOPS
+    hbm_bound = nbytes / (HBM_PEAK_GBS * 1e9) >= flops / (mfma_peak * 1e12)
+    gbs, tfs = nbytes / dur / 1e9, flops / dur / 1e12
+    if hbm_bound:
+        roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    else:
+        roofline = {"bound": "mfma", "achieved": round(tfs, 2), "peak": mfma_peak, "unit": "TFLOP/s",
+                    "frac": round(tfs / mfma_peak, 4)}
+    roofline.update({"traffic": None, "kernel": dom, "avg_launch_us": round(dur * 1e6, 2),
+                     "algorithmic_bytes": int(nbytes), "algorithmic_flops": flops,
+                     "hbm_frac": round(gbs / HBM_PEAK_GBS, 4), "mfma_frac": round(tfs / mfma_peak, 4),
+                     "other_kernels_us": {k: round(v * 1e6, 2) for k, v in times.items() if k != dom}})
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -179,7 +203,7 @@ def main():
         "vs_baseline": None,
         "dtype": spec.dtype,
         "data": "synthetic",
-        "config": {"workload": spec.name, "n_nodes": comp.n_real, "n_pad": comp.n_pad, "graphs": len(graphs),
+        "config": {"workload": spec.name, "band": args.band, "n_nodes": comp.n_real, "n_pad": comp.n_pad, "graphs": len(graphs),
                    "B": B, "E": E, "H": H, "T": spec.T, "bandwidth_after_reordering": comp.bandwidth,
                    "edges_packed": comp.stats.get("n_packed"), "edges_dropped": comp.stats.get("n_dropped"),
                    "node_steps_per_s_padded": round(comp.n_pad * spec.T / sec_per_step, 1),

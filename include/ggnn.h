@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define GGNN_ABI_VERSION 1
+#define GGNN_ABI_VERSION 2
 
 typedef enum {
   GGNN_OK = 0,
@@ -60,6 +60,10 @@ typedef enum {
 } ggnn_status;
 
 typedef enum { GGNN_F32 = 0, GGNN_BF16 = 1 } ggnn_dtype;
+
+/* Storage of the block band: dense elements of the compute dtype, or one bit
+ * per entry (lossless, since A_e has entries in {0,1}). */
+typedef enum { GGNN_BAND_DENSE = 0, GGNN_BAND_BITS = 1 } ggnn_band_format;
 
 /* Version of this ABI (GGNN_ABI_VERSION of the built library). */
 int ggnn_abi_version(void);
@@ -128,6 +132,26 @@ ggnn_status ggnn_banded_pack(int32_t n_pad, int32_t E, int32_t B, int64_t m,
                              const int32_t* rank, ggnn_dtype dt, int strict, void* band,
                              int64_t* n_packed, int64_t* n_dropped, int64_t* n_duplicate);
 
+/* Bytes of a 1-bit block band: E * (n_pad / B) * 3 * B * (B / 8).
+ * Returns 0 for invalid arguments (B must be a multiple of 8). */
+size_t ggnn_band_bits_bytes(int32_t n_pad, int32_t E, int32_t B);
+
+/* Pack typed edges into the three block diagonals of Eq. 3 at one bit per
+ * entry, plus (optionally) the transposed blocks used by the reverse pass.
+ *   bits[e][k][s][r][B/8]: row r of block (e, k, s) as in ggnn_banded_pack;
+ *     byte c/8 of the row holds columns c..c+7, bit c%8 is column c.
+ *   bits_t[e][j][s][c][B/8]: the transposed blocks with the sub- and
+ *     super-diagonal roles swapped, bits_t[e][j][s] = band[e][j-1+s][2-s]^T:
+ *     row c of block (e, j, s) holds bit r for every edge from node
+ *     j*B + c to node (j-1+s)*B + r.  Nullable.
+ * Coverage, duplicates, counters, strict and errors are as for
+ * ggnn_banded_pack.  B must be a multiple of 8; both buffers hold
+ * ggnn_band_bits_bytes(...) bytes and are fully overwritten. */
+ggnn_status ggnn_banded_pack_bits(int32_t n_pad, int32_t E, int32_t B, int64_t m,
+                                  const int32_t* src, const int32_t* dst, const int32_t* etype,
+                                  const int32_t* rank, int strict, void* bits, void* bits_t,
+                                  int64_t* n_packed, int64_t* n_dropped, int64_t* n_duplicate);
+
 /* ======================================================================
  * Device entry points: one propagation step and its reverse.
  * All pointers are device memory owned by the caller.
@@ -170,6 +194,26 @@ ggnn_status ggnn_banded_propagate(ggnn_dtype dt, int32_t n_pad, int32_t B, int32
 ggnn_status ggnn_gru_update(ggnn_dtype dt, int32_t n_pad, int32_t H, const float* a, const void* h,
                             const void* Wi, const void* U, const float* b, void* h_out, void* saved,
                             void* stream);
+
+/* Aggregate-first propagation step on a 1-bit band (Algorithm 1's operand
+ * order; Eq. 3's three block products):
+ *   a = sum_e (A_e X) W_e  (+ sum_e (A_e 1) bias_e^T when bias != NULL)
+ * The aggregation A_e X and the transform by W_e run in one kernel; the
+ * per-type aggregates never leave the chip (in bf16 mode they enter the
+ * transform as bf16 hi + lo pairs).  Same result as ggnn_msg_transform
+ * followed by ggnn_banded_propagate, without the messages in memory.
+ *   bits  as written by ggnn_banded_pack_bits (16-byte aligned)
+ *   X     [n_pad][H] dt node-major;  W [E][H][H] dt;  bias [E][H] float or NULL
+ *   a     [n_pad][H] float (written) */
+ggnn_status ggnn_banded_step_bits(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
+                                  const void* bits, const void* X, const void* W, const float* bias,
+                                  float* a, void* stream);
+
+/* Reverse of the banded product on a 1-bit band: dM_e = A_e^T da, read
+ * through the transposed blocks (bits_t of ggnn_banded_pack_bits).
+ *   da [H][n_pad] dt feature-major;  dM [E][H][n_pad] dt feature-major (written) */
+ggnn_status ggnn_banded_propagate_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
+                                           const void* bits_t, const void* da, void* dM, void* stream);
 
 /* Workspace bytes needed by ggnn_gru_update_bwd for these sizes. */
 size_t ggnn_gru_update_bwd_workspace_bytes(ggnn_dtype dt, int32_t n_pad, int32_t H);
@@ -219,19 +263,21 @@ ggnn_status ggnn_msg_transform_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int3
 typedef struct ggnn_model {
   int32_t dtype;        /* ggnn_dtype */
   int32_t n_pad, B, H, E, T;
-  const void* band;     /* [E][n_pad/B][3][B][B] dt */
+  const void* band;     /* dense: [E][n_pad/B][3][B][B] dt; bits: bits of ggnn_banded_pack_bits */
   const void* W;        /* [E][H][H] dt */
   const float* bias;    /* [E][H] or NULL */
   const void* Wi;       /* [H][3H] dt */
   const void* U;        /* [H][3H] dt */
   const float* b;       /* [3H] */
+  int32_t band_format;  /* ggnn_band_format */
+  const void* band_t;   /* bits: the transposed bit band (bits_t); dense: unused */
 } ggnn_model;
 
 typedef struct ggnn_activations {
   void* X;              /* [T+1][n_pad][H] dt: X[0] is the input, X[1..T] written */
   float* a;             /* [T][n_pad][H] float, written by the forward */
   void* saved;          /* [T][n_pad][3H] dt, written by the forward */
-  float* M;             /* [E][H][n_pad] float scratch (contents not kept) */
+  float* M;             /* [E][H][n_pad] float scratch for the dense band (NULL allowed with bits) */
 } ggnn_activations;
 
 typedef struct ggnn_grads {
@@ -252,12 +298,14 @@ typedef struct ggnn_grads {
 size_t ggnn_backward_workspace_bytes(const ggnn_model* model);
 
 /* Forward over T steps: for t = 0..T-1,
- *   M = msg_transform(X[t]); a[t] = banded_propagate(M);
- *   X[t+1], saved[t] = gru_update(a[t], X[t]). */
+ *   dense band: M = msg_transform(X[t]); a[t] = banded_propagate(M);
+ *   bit band:   a[t] = banded_step_bits(X[t]);
+ *   then X[t+1], saved[t] = gru_update(a[t], X[t]). */
 ggnn_status ggnn_forward(const ggnn_model* model, const ggnn_activations* act, void* stream);
 
 /* Reverse pass for L with dL/dX_T given in grads->dX: for t = T-1..0,
- *   da, dh = gru_update_bwd(dX); dM = banded_propagate_bwd(da);
+ *   da, dh = gru_update_bwd(dX); dM = banded_propagate_bwd(da) (dense band)
+ *   or banded_propagate_bits_bwd(da) (bit band);
  *   dX = dh + sum_e dM_e W_e^T;  weight gradients accumulate (+=).
  * Needs the activations of a preceding ggnn_forward. */
 ggnn_status ggnn_backward(const ggnn_model* model, const ggnn_activations* act,

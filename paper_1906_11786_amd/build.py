@@ -25,6 +25,7 @@ SOURCES = [
     ("host.cpp", "c++"),
     ("capi_device.cpp", "hip"),
     ("banded.hip", "hip"),
+    ("banded_bits.hip", "hip"),
     ("transform.hip", "hip"),
     ("gru.hip", "hip"),
 ]

@@ -19,6 +19,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libggnn.so"
 GGNN_F32 = 0
 GGNN_BF16 = 1
 DTYPES = {"f32": GGNN_F32, "bf16": GGNN_BF16}
+GGNN_BAND_DENSE = 0
+GGNN_BAND_BITS = 1
+BAND_FORMATS = {"dense": GGNN_BAND_DENSE, "bits": GGNN_BAND_BITS}
 
 STATUS = {0: "GGNN_OK", 1: "GGNN_ERR_INVALID_ARG", 2: "GGNN_ERR_UNSUPPORTED", 3: "GGNN_ERR_OUT_OF_BAND",
           4: "GGNN_ERR_DEVICE", 5: "GGNN_ERR_HOST_ALLOC", 6: "GGNN_ERR_WORKSPACE"}
@@ -26,6 +29,7 @@ STATUS = {0: "GGNN_OK", 1: "GGNN_ERR_INVALID_ARG", 2: "GGNN_ERR_UNSUPPORTED", 3:
 EXPORTS = [
     "ggnn_abi_version", "ggnn_last_error", "ggnn_status_string",
     "ggnn_rcm_order", "ggnn_bandwidth", "ggnn_band_bytes", "ggnn_banded_pack",
+    "ggnn_band_bits_bytes", "ggnn_banded_pack_bits", "ggnn_banded_step_bits", "ggnn_banded_propagate_bits_bwd",
     "ggnn_msg_transform", "ggnn_banded_propagate", "ggnn_gru_update",
     "ggnn_gru_update_bwd_workspace_bytes", "ggnn_gru_update_bwd",
     "ggnn_banded_propagate_bwd", "ggnn_msg_transform_bwd_workspace_bytes", "ggnn_msg_transform_bwd",
@@ -43,7 +47,8 @@ class GGNNError(RuntimeError):
 class ggnn_model(C.Structure):
     _fields_ = [("dtype", C.c_int32), ("n_pad", C.c_int32), ("B", C.c_int32), ("H", C.c_int32),
                 ("E", C.c_int32), ("T", C.c_int32), ("band", C.c_void_p), ("W", C.c_void_p),
-                ("bias", C.c_void_p), ("Wi", C.c_void_p), ("U", C.c_void_p), ("b", C.c_void_p)]
+                ("bias", C.c_void_p), ("Wi", C.c_void_p), ("U", C.c_void_p), ("b", C.c_void_p),
+                ("band_format", C.c_int32), ("band_t", C.c_void_p)]
 
 
 class ggnn_activations(C.Structure):
@@ -69,6 +74,10 @@ _SIGS = {
     "ggnn_bandwidth": (C.c_int, [i32, i64, vp, vp, vp, vp]),
     "ggnn_band_bytes": (sz, [i32, i32, i32, C.c_int]),
     "ggnn_banded_pack": (C.c_int, [i32, i32, i32, i64, vp, vp, vp, vp, C.c_int, C.c_int, vp, vp, vp, vp]),
+    "ggnn_band_bits_bytes": (sz, [i32, i32, i32]),
+    "ggnn_banded_pack_bits": (C.c_int, [i32, i32, i32, i64, vp, vp, vp, vp, C.c_int, vp, vp, vp, vp, vp]),
+    "ggnn_banded_step_bits": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]),
+    "ggnn_banded_propagate_bits_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp]),
     "ggnn_msg_transform": (C.c_int, [C.c_int, i32, i32, i32, vp, vp, vp, vp, vp]),
     "ggnn_banded_propagate": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp]),
     "ggnn_gru_update": (C.c_int, [C.c_int, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
@@ -185,7 +194,38 @@ def ggnn_banded_pack(n_pad: int, E: int, B: int, src, dst, etype, rank=None, dt=
     return band, int(counts[0]), int(counts[1]), int(counts[2])
 
 
+def ggnn_band_bits_bytes(n_pad: int, E: int, B: int) -> int:
+    return int(lib().ggnn_band_bits_bytes(n_pad, E, B))
+
+
+def ggnn_banded_pack_bits(n_pad: int, E: int, B: int, src, dst, etype, rank=None, strict: bool = False,
+                          with_transpose: bool = True):
+    """Returns (bits, bits_t or None, n_packed, n_dropped, n_duplicate);
+    bits arrays have shape [E, n_pad/B, 3, B, B/8] and dtype uint8."""
+    src, dst, etype = _i32(src), _i32(dst), _i32(etype)
+    rk = None if rank is None else _i32(rank)
+    nb = n_pad // B if B > 0 else 0
+    shape = (E, nb, 3, B, max(B // 8, 0))
+    bits = np.empty(shape, np.uint8)
+    bits_t = np.empty(shape, np.uint8) if with_transpose else None
+    counts = np.zeros(3, np.int64)
+    _check("ggnn_banded_pack_bits", lib().ggnn_banded_pack_bits(
+        n_pad, E, B, len(src), _ptr(src), _ptr(dst), _ptr(etype), _ptr(rk), int(bool(strict)), _ptr(bits),
+        _ptr(bits_t), counts.ctypes.data, counts.ctypes.data + 8, counts.ctypes.data + 16))
+    return bits, bits_t, int(counts[0]), int(counts[1]), int(counts[2])
+
+
 # -------------------------------------------------------------- device calls
+
+def ggnn_banded_step_bits(dt, n_pad, B, H, E, bits, X, W, bias, a, stream=None):
+    _check("ggnn_banded_step_bits", lib().ggnn_banded_step_bits(_dt(dt), n_pad, B, H, E, _ptr(bits), _ptr(X),
+                                                                _ptr(W), _ptr(bias), _ptr(a), _stream(stream)))
+
+
+def ggnn_banded_propagate_bits_bwd(dt, n_pad, B, H, E, bits_t, da, dM, stream=None):
+    _check("ggnn_banded_propagate_bits_bwd", lib().ggnn_banded_propagate_bits_bwd(
+        _dt(dt), n_pad, B, H, E, _ptr(bits_t), _ptr(da), _ptr(dM), _stream(stream)))
+
 
 def ggnn_msg_transform(dt, n_pad, H, E, X, W, bias, M, stream=None):
     _check("ggnn_msg_transform", lib().ggnn_msg_transform(_dt(dt), n_pad, H, E, _ptr(X), _ptr(W), _ptr(bias),

@@ -1,0 +1,489 @@
+// Banded propagation on a 1-bit block band (lossless: A_e has entries in
+// {0,1}), in the operand order of Algorithm 1.
+//
+// Forward (fused): a[k] = sum_e ( sum_s C/U/L_e[k][s] X[k-1+s] ) W_e  (+ deg_e b_e)
+//   the three block products of Eq. 3 aggregate the node states first
+//   (pre_e = A_e X, kept in registers), then the per-type transform follows
+//   in the same workgroup, so the messages never go to HBM.
+// Reverse: dM_e[j] = sum_s bits_t[e][j][s] da[j-1+s] = A_e^T da, where the
+//   transposed bit band holds the transposed blocks with the sub- and
+//   super-diagonal roles swapped (bits_t[e][j][s] = band[e][j-1+s][2-s]^T).
+//
+// Bit layout (both bands): bits[e][k][s][r][B/8]: row r of block (e, k, s),
+// byte c/8 holds columns c..c+7, bit c%8.  A lane expands 8 bits to an
+// 8-element matrix-core fragment in registers.
+//
+// k order of the aggregation: inside a chunk of KC nodes, lane group g owns
+// the contiguous columns [g*KC/4, (g+1)*KC/4), so each lane reads KC/32
+// consecutive bytes of its bit row, and the staged node tile is read with
+// 16-byte LDS loads at the same offsets.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace ggnn {
+namespace dev {
+
+// 8 bits -> 8 elements equal to 0 or 1 (bit i -> element i).
+template <typename S> __device__ __forceinline__ frag_t<S> bits_frag(uint32_t byte);
+template <> __device__ __forceinline__ bf16x8 bits_frag<bf16s>(uint32_t byte) {
+  u32x4 w;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t t = (byte >> (2 * k)) & 3u;           // two bits -> two 16-bit lanes
+    w[k] = ((t * 0x8001u) & 0x10001u) * 0x3F80u;         // 0x3F80 is bf16 1.0
+  }
+  return __builtin_bit_cast(bf16x8, w);
+}
+template <> __device__ __forceinline__ f32x8 bits_frag<float>(uint32_t byte) {
+  f32x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = static_cast<float>((byte >> i) & 1u);
+  return r;
+}
+
+// NB consecutive bytes (NB in {1, 2, 4, 8, 16}, naturally aligned) as words.
+template <int NB> struct RowBytes {
+  static constexpr int NW = NB < 4 ? 1 : NB / 4;
+  uint32_t w[NW];
+  __device__ __forceinline__ void load(const uint8_t* p) {
+    if constexpr (NB == 1) {
+      w[0] = *p;
+    } else if constexpr (NB == 2) {
+      w[0] = *reinterpret_cast<const uint16_t*>(p);
+    } else if constexpr (NB == 4) {
+      w[0] = *reinterpret_cast<const uint32_t*>(p);
+    } else if constexpr (NB == 8) {
+      u32x2 v = *reinterpret_cast<const u32x2*>(p);
+      w[0] = v[0];
+      w[1] = v[1];
+    } else {
+      u32x4 v = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = v[i];
+    }
+  }
+  __device__ __forceinline__ uint32_t byte(int i) const { return (w[i / 4] >> (8 * (i % 4))) & 0xFFu; }
+  __device__ __forceinline__ int popc() const {
+    int c = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) c += __popc(w[i]);
+    return c;
+  }
+};
+
+// Two storage elements at p (p 4-byte aligned for bf16, 8-byte for fp32).
+__device__ __forceinline__ void store_pair(bf16s* p, uint32_t lo16, uint32_t hi16) {
+  *reinterpret_cast<uint32_t*>(p) = (lo16 & 0xFFFFu) | (hi16 << 16);
+}
+
+// Stage nodes [n0, n0 + KC) of a node-major [n][H] array into LDS as
+// dst[h * VP + c] (feature rows).  Each thread moves a pair of consecutive
+// nodes for eight features and writes 2-element words, so consecutive lanes
+// write consecutive words.
+template <typename S, int H, int KC, int VP, int NT>
+__device__ __forceinline__ void stage_nodes_T(S* dst, const S* src, int n0, int tid) {
+  constexpr int PAIRS = KC / 2;
+  for (int lin = tid; lin < PAIRS * (H / 8); lin += NT) {
+    const int cp = lin % PAIRS, f0 = (lin / PAIRS) * 8;
+    const S* p0 = src + (size_t)(n0 + 2 * cp) * H + f0;
+    if constexpr (sizeof(S) == 2) {
+      u32x4 x0 = *reinterpret_cast<const u32x4*>(p0);
+      u32x4 x1 = *reinterpret_cast<const u32x4*>(p0 + H);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        store_pair(&dst[(f0 + 2 * i) * VP + 2 * cp], x0[i] & 0xFFFFu, x1[i] & 0xFFFFu);
+        store_pair(&dst[(f0 + 2 * i + 1) * VP + 2 * cp], x0[i] >> 16, x1[i] >> 16);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        typedef float f32x2 __attribute__((ext_vector_type(2)));
+        *reinterpret_cast<f32x2*>(&dst[(f0 + i) * VP + 2 * cp]) = f32x2{p0[i], p0[H + i]};
+      }
+    }
+  }
+}
+
+// Stage columns [n0, n0 + KC) of a feature-major [H][n_pad] array into LDS
+// as dst[h * VP + c] (plain 16-byte copies).
+template <typename S, int H, int KC, int VP, int NT>
+__device__ __forceinline__ void stage_cols(S* dst, const S* src, int n_pad, int n0, int tid) {
+  constexpr int V = 16 / sizeof(S);
+  for (int lin = tid; lin < H * (KC / V); lin += NT) {
+    const int h = lin / (KC / V), c = (lin % (KC / V)) * V;
+    *reinterpret_cast<u32x4*>(&dst[h * VP + c]) = *reinterpret_cast<const u32x4*>(src + (size_t)h * n_pad + n0 + c);
+  }
+}
+
+template <typename S, int H, int B>
+struct BitsCfg {
+  static constexpr int V = 16 / sizeof(S);
+  // Stage the three neighbouring node blocks once per workgroup when they fit
+  // in 64 KB; otherwise stream KC-node chunks per edge type.
+  static constexpr bool ALL = 3 * H * (B + V) * (int)sizeof(S) <= 65536;
+  static constexpr int KC = ALL ? B : (B < 64 ? B : 64);
+  static constexpr int NBUF = ALL ? 3 : 1;
+  static constexpr int VP = KC + V;
+  static constexpr int RB = KC / 32;        // bit-row bytes per lane per chunk (= k steps per chunk)
+  static constexpr int RPW = H >= 256 ? 16 : 32;   // rows per wave
+  static constexpr int NTW = RPW / 16;      // 16-row tiles per wave
+};
+
+// ---------------------------------------------------------------------------
+// Fused forward.  Workgroup: RPW*WAVES rows of block row k.
+// Aggregation D[h][r]: A operand = staged X^T rows (LDS), B operand = bit
+// rows expanded in registers.  Transform D'[h_out][r]: A operand = W_e^T
+// rows (LDS, transposed on the write), B operand = the aggregation
+// accumulators themselves (accumulator-compatible k order, split hi + lo in
+// bf16 mode).  Lanes then hold four consecutive features of one node:
+// 16-byte stores of the fp32 aggregate a.
+// ---------------------------------------------------------------------------
+template <typename S, int H, int B, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* __restrict__ bits,
+                                                                  const S* __restrict__ X, const S* __restrict__ W,
+                                                                  const float* __restrict__ bias,
+                                                                  float* __restrict__ a, int n_pad, int E) {
+  using C = BitsCfg<S, H, B>;
+  constexpr int NT = WAVES * kWave;
+  constexpr int V = C::V, KC = C::KC, VP = C::VP, RB = C::RB, NTW = C::NTW;
+  constexpr int MT = H / 16, HK = H / 32;
+  constexpr int WC = H < 64 ? H : 64;      // W^T rows staged at a time
+  constexpr int WP = H + V;
+  constexpr int NP = sizeof(S) == 2 ? 2 : 1;
+  constexpr int ROWB = B / 8;
+  __shared__ __attribute__((aligned(16))) S vt[C::NBUF][H * VP];
+  __shared__ __attribute__((aligned(16))) S wt[WC * WP];
+
+  const int nb = n_pad / B;
+  constexpr int NW = C::RPW * WAVES;
+  const int tiles_per_row = B / NW;
+  const int t = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int k = t / tiles_per_row;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int q = lane % 16, g = lane / 16;
+  const int rw = (t % tiles_per_row) * NW + C::RPW * wave;   // first row of this wave
+  const int s_lo = (k == 0) ? 1 : 0;
+  const int s_hi = (k == nb - 1) ? 1 : 2;
+
+  if constexpr (C::ALL) {
+    for (int s = s_lo; s <= s_hi; ++s) stage_nodes_T<S, H, KC, VP, NT>(vt[s], X, (k - 1 + s) * B, tid);
+    __syncthreads();
+  }
+  f32x4 acc[NTW][MT];
+#pragma unroll
+  for (int n = 0; n < NTW; ++n)
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[n][m] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // In ALL mode a chunk is a whole block: the bit rows of the next edge type
+  // are loaded while the current one is computed (the loads would otherwise
+  // sit on the critical path of every type).
+  RowBytes<RB> nxt[3][NTW];
+  auto load_type = [&](int e, RowBytes<RB> (&dst)[3][NTW]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      if (s < s_lo || s > s_hi) continue;
+      const uint8_t* brow = bits + ((((size_t)e * nb + k) * 3 + s) * B + rw + q) * ROWB + g * (KC / 32);
+#pragma unroll
+      for (int n = 0; n < NTW; ++n) dst[s][n].load(brow + (size_t)16 * n * ROWB);
+    }
+  };
+  if constexpr (C::ALL) load_type(0, nxt);
+  for (int e = 0; e < E; ++e) {
+    f32x4 pre[NTW][MT];
+#pragma unroll
+    for (int n = 0; n < NTW; ++n)
+#pragma unroll
+      for (int m = 0; m < MT; ++m) pre[n][m] = f32x4{0.f, 0.f, 0.f, 0.f};
+    int deg[NTW];
+#pragma unroll
+    for (int n = 0; n < NTW; ++n) deg[n] = 0;
+    RowBytes<RB> cur[3][NTW];
+    if constexpr (C::ALL) {
+#pragma unroll
+      for (int s = 0; s < 3; ++s)
+#pragma unroll
+        for (int n = 0; n < NTW; ++n) cur[s][n] = nxt[s][n];
+      if (e + 1 < E) load_type(e + 1, nxt);
+    }
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      if (s < s_lo || s > s_hi) continue;
+      const uint8_t* brow = bits + ((((size_t)e * nb + k) * 3 + s) * B + rw + q) * ROWB;
+      for (int c0 = 0; c0 < B; c0 += KC) {
+        if constexpr (!C::ALL) {
+          __syncthreads();
+          stage_nodes_T<S, H, KC, VP, NT>(vt[0], X, (k - 1 + s) * B + c0, tid);
+          __syncthreads();
+        }
+        const S* v = vt[C::ALL ? s : 0];
+        RowBytes<RB> rb[NTW];
+#pragma unroll
+        for (int n = 0; n < NTW; ++n) {
+          if constexpr (C::ALL) {
+            rb[n] = cur[s][n];
+          } else {
+            rb[n].load(brow + (size_t)16 * n * ROWB + (c0 + g * (KC / 4)) / 8);
+          }
+          if (bias) deg[n] += rb[n].popc();
+        }
+#pragma unroll
+        for (int kk = 0; kk < RB; ++kk) {
+          frag_t<S> bf[NTW];
+#pragma unroll
+          for (int n = 0; n < NTW; ++n) bf[n] = bits_frag<S>(rb[n].byte(kk));
+#pragma unroll
+          for (int m = 0; m < MT; ++m) {
+            const frag_t<S> af = load8(&v[(16 * m + q) * VP + g * (KC / 4) + 8 * kk]);
+#pragma unroll
+            for (int n = 0; n < NTW; ++n) mma(pre[n][m], af, bf[n]);
+          }
+        }
+      }
+    }
+    // pre^T in accumulator layout: lane (node q), features 16m + 4g + j.
+    frag_t<S> pf[NP][NTW][HK];
+#pragma unroll
+    for (int n = 0; n < NTW; ++n)
+#pragma unroll
+      for (int kk = 0; kk < HK; ++kk) {
+        float v8[8];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          v8[j] = pre[n][2 * kk][j];
+          v8[4 + j] = pre[n][2 * kk + 1][j];
+        }
+        if constexpr (NP == 2) {
+          split8(v8, pf[0][n][kk], pf[NP - 1][n][kk]);
+        } else {
+          pf[0][n][kk] = pack8<S>(v8);
+        }
+      }
+    for (int oc = 0; oc < H; oc += WC) {
+      __syncthreads();
+      const S* wsrc = W + (size_t)e * H * H + oc;
+      for (int lin = tid; lin < H * (WC / V); lin += NT) {   // wt[o][h] = W[e][h][oc + o]
+        const int h = lin / (WC / V), o8 = (lin % (WC / V)) * V;
+        u32x4 w = *reinterpret_cast<const u32x4*>(wsrc + (size_t)h * H + o8);
+        const S* pw = reinterpret_cast<const S*>(&w);
+#pragma unroll
+        for (int x = 0; x < V; ++x) wt[(o8 + x) * WP + h] = pw[x];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int mo = 0; mo < WC / 16; ++mo)
+#pragma unroll
+        for (int kk = 0; kk < HK; ++kk) {
+          const S* wr = &wt[(16 * mo + q) * WP + 32 * kk + 4 * g];
+          const frag_t<S> af = load4x2(wr, wr + 16);
+#pragma unroll
+          for (int n = 0; n < NTW; ++n)
+#pragma unroll
+            for (int part = 0; part < NP; ++part) mma(acc[n][oc / 16 + mo], af, pf[part][n][kk]);
+        }
+    }
+    if (bias) {
+#pragma unroll
+      for (int n = 0; n < NTW; ++n) {
+        int d = deg[n];
+        d += __shfl_xor(d, 16);
+        d += __shfl_xor(d, 32);
+        const float fd = static_cast<float>(d);
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[n][m][j] += fd * bias[e * H + 16 * m + 4 * g + j];
+      }
+    }
+  }
+#pragma unroll
+  for (int n = 0; n < NTW; ++n) {
+    float* out = a + (size_t)(k * B + rw + 16 * n + q) * H + 4 * g;
+#pragma unroll
+    for (int m = 0; m < MT; ++m) store4(out + 16 * m, acc[n][m][0], acc[n][m][1], acc[n][m][2], acc[n][m][3]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Reverse: dM[e][h][j*B + c] = sum_s sum_r bits_t[e][j][s][c][r] da[h][(j-1+s)*B + r].
+// Workgroup: RPW*WAVES columns c of block j; wave w: RPW of them.  D[c][h]:
+// A operand = transposed bit rows c expanded in registers, B operand = staged
+// da rows (feature-major, plain copies).  Lanes hold four consecutive nodes
+// of one feature: 8-byte (bf16) stores into feature-major dM.
+// ---------------------------------------------------------------------------
+template <typename S, int H, int B, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* __restrict__ bits_t,
+                                                                  const S* __restrict__ da, S* __restrict__ dM,
+                                                                  int n_pad, int E) {
+  using C = BitsCfg<S, H, B>;
+  constexpr int NT = WAVES * kWave;
+  constexpr int KC = C::KC, VP = C::VP, RB = C::RB, NTW = C::NTW;
+  constexpr int NTL = H / 16;
+  constexpr int ROWB = B / 8;
+  __shared__ __attribute__((aligned(16))) S vt[C::NBUF][H * VP];
+
+  const int nb = n_pad / B;
+  constexpr int NW = C::RPW * WAVES;
+  const int tiles_per_blk = B / NW;
+  const int t = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int j = t / tiles_per_blk;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int q = lane % 16, g = lane / 16;
+  const int cw = (t % tiles_per_blk) * NW + C::RPW * wave;
+  const int s_lo = (j == 0) ? 1 : 0;
+  const int s_hi = (j == nb - 1) ? 1 : 2;
+
+  if constexpr (C::ALL) {
+    for (int s = s_lo; s <= s_hi; ++s) stage_cols<S, H, KC, VP, NT>(vt[s], da, n_pad, (j - 1 + s) * B, tid);
+    __syncthreads();
+  }
+  RowBytes<RB> nxt[3][NTW];
+  auto load_type = [&](int e, RowBytes<RB> (&dst)[3][NTW]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      if (s < s_lo || s > s_hi) continue;
+      const uint8_t* brow = bits_t + ((((size_t)e * nb + j) * 3 + s) * B + cw + q) * ROWB + g * (KC / 32);
+#pragma unroll
+      for (int m = 0; m < NTW; ++m) dst[s][m].load(brow + (size_t)16 * m * ROWB);
+    }
+  };
+  if constexpr (C::ALL) load_type(0, nxt);
+  for (int e = 0; e < E; ++e) {
+    f32x4 acc[NTW][NTL];
+#pragma unroll
+    for (int m = 0; m < NTW; ++m)
+#pragma unroll
+      for (int n = 0; n < NTL; ++n) acc[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    RowBytes<RB> cur[3][NTW];
+    if constexpr (C::ALL) {
+#pragma unroll
+      for (int s = 0; s < 3; ++s)
+#pragma unroll
+        for (int m = 0; m < NTW; ++m) cur[s][m] = nxt[s][m];
+      if (e + 1 < E) load_type(e + 1, nxt);
+    }
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      if (s < s_lo || s > s_hi) continue;
+      const uint8_t* brow = bits_t + ((((size_t)e * nb + j) * 3 + s) * B + cw + q) * ROWB;
+      for (int c0 = 0; c0 < B; c0 += KC) {
+        if constexpr (!C::ALL) {
+          __syncthreads();
+          stage_cols<S, H, KC, VP, NT>(vt[0], da, n_pad, (j - 1 + s) * B + c0, tid);
+          __syncthreads();
+        }
+        const S* v = vt[C::ALL ? s : 0];
+        RowBytes<RB> rb[NTW];
+#pragma unroll
+        for (int m = 0; m < NTW; ++m) {
+          if constexpr (C::ALL) {
+            rb[m] = cur[s][m];
+          } else {
+            rb[m].load(brow + (size_t)16 * m * ROWB + (c0 + g * (KC / 4)) / 8);
+          }
+        }
+#pragma unroll
+        for (int kk = 0; kk < RB; ++kk) {
+          frag_t<S> af[NTW];
+#pragma unroll
+          for (int m = 0; m < NTW; ++m) af[m] = bits_frag<S>(rb[m].byte(kk));
+#pragma unroll
+          for (int n = 0; n < NTL; ++n) {
+            const frag_t<S> bf = load8(&v[(16 * n + q) * VP + g * (KC / 4) + 8 * kk]);
+#pragma unroll
+            for (int m = 0; m < NTW; ++m) mma(acc[m][n], af[m], bf);
+          }
+        }
+      }
+    }
+    S* out = dM + (size_t)e * H * n_pad + (size_t)j * B + cw + 4 * g;
+#pragma unroll
+    for (int m = 0; m < NTW; ++m)
+#pragma unroll
+      for (int n = 0; n < NTL; ++n)
+        store4(out + (size_t)(16 * n + q) * n_pad + 16 * m, acc[m][n][0], acc[m][n][1], acc[m][n][2], acc[m][n][3]);
+  }
+}
+
+}  // namespace dev
+
+// Workgroup size: the largest (up to four waves, never more rows than a block
+// holds) that still gives at least this many workgroups.
+#ifndef GGNN_BITS_FWD_MIN_BLOCKS
+#define GGNN_BITS_FWD_MIN_BLOCKS 64
+#endif
+#ifndef GGNN_BITS_BWD_MIN_BLOCKS
+#define GGNN_BITS_BWD_MIN_BLOCKS 256
+#endif
+
+namespace {
+template <typename S, int H, int B>
+hipError_t bits_launch(bool fwd, const void* bits, const void* V, const void* W, const float* bias, void* out,
+                       int n_pad, int E, hipStream_t st) {
+  using C = dev::BitsCfg<S, H, B>;
+  const int nb = n_pad / B;
+  int waves = B / C::RPW < 4 ? B / C::RPW : 4;
+  const long min_blocks = fwd ? GGNN_BITS_FWD_MIN_BLOCKS : GGNN_BITS_BWD_MIN_BLOCKS;
+  while (waves > 1 && (long)nb * (B / (C::RPW * waves)) < min_blocks) waves /= 2;
+  const int blocks = nb * (B / (C::RPW * waves));
+  const uint8_t* bp = static_cast<const uint8_t*>(bits);
+  const S* vp = static_cast<const S*>(V);
+#define GGNN_BITS_CASE(WV)                                                                                   \
+  case WV:                                                                                                   \
+    if constexpr (B / C::RPW >= WV) {                                                                        \
+      if (fwd)                                                                                               \
+        hipLaunchKernelGGL((dev::step_fwd_kernel<S, H, B, WV>), dim3(blocks), dim3(WV * 64), 0, st, bp, vp,  \
+                           static_cast<const S*>(W), bias, static_cast<float*>(out), n_pad, E);              \
+      else                                                                                                   \
+        hipLaunchKernelGGL((dev::bits_bwd_kernel<S, H, B, WV>), dim3(blocks), dim3(WV * 64), 0, st, bp, vp,  \
+                           static_cast<S*>(out), n_pad, E);                                                  \
+    }                                                                                                        \
+    break;
+  switch (waves) {
+    GGNN_BITS_CASE(4)
+    GGNN_BITS_CASE(2)
+    GGNN_BITS_CASE(1)
+  }
+#undef GGNN_BITS_CASE
+  return hipGetLastError();
+}
+
+template <typename S, int H>
+hipError_t bits_h(int B, bool fwd, const void* bits, const void* V, const void* W, const float* bias, void* out,
+                  int n_pad, int E, hipStream_t st) {
+  switch (B) {
+    case 32: return bits_launch<S, H, 32>(fwd, bits, V, W, bias, out, n_pad, E, st);
+    case 64: return bits_launch<S, H, 64>(fwd, bits, V, W, bias, out, n_pad, E, st);
+    case 128: return bits_launch<S, H, 128>(fwd, bits, V, W, bias, out, n_pad, E, st);
+    case 256: return bits_launch<S, H, 256>(fwd, bits, V, W, bias, out, n_pad, E, st);
+    case 512: return bits_launch<S, H, 512>(fwd, bits, V, W, bias, out, n_pad, E, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename S>
+hipError_t bits_t(int H, int B, bool fwd, const void* bits, const void* V, const void* W, const float* bias,
+                  void* out, int n_pad, int E, hipStream_t st) {
+  switch (H) {
+    case 32: return bits_h<S, 32>(B, fwd, bits, V, W, bias, out, n_pad, E, st);
+    case 64: return bits_h<S, 64>(B, fwd, bits, V, W, bias, out, n_pad, E, st);
+    case 128: return bits_h<S, 128>(B, fwd, bits, V, W, bias, out, n_pad, E, st);
+    case 256: return bits_h<S, 256>(B, fwd, bits, V, W, bias, out, n_pad, E, st);
+  }
+  return hipErrorInvalidValue;
+}
+}  // namespace
+
+hipError_t launch_step_fwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits, const void* X,
+                                const void* W, const float* bias, float* a, hipStream_t st) {
+  return dt == GGNN_BF16 ? bits_t<dev::bf16s>(H, B, true, bits, X, W, bias, a, n_pad, E, st)
+                         : bits_t<float>(H, B, true, bits, X, W, bias, a, n_pad, E, st);
+}
+
+hipError_t launch_banded_bwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits_t_, const void* da,
+                                  void* dM, hipStream_t st) {
+  return dt == GGNN_BF16 ? bits_t<dev::bf16s>(H, B, false, bits_t_, da, nullptr, nullptr, dM, n_pad, E, st)
+                         : bits_t<float>(H, B, false, bits_t_, da, nullptr, nullptr, dM, n_pad, E, st);
+}
+
+}  // namespace ggnn

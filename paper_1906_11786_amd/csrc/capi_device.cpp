@@ -135,6 +135,32 @@ ggnn_status ggnn_banded_propagate_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, i
                        "banded_propagate_bwd");
 }
 
+ggnn_status ggnn_banded_step_bits(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E, const void* bits,
+                                  const void* X, const void* W, const float* bias, float* a, void* stream) {
+  clear_error();
+  ggnn_status st = check_banded(dt, n_pad, B, H, E);
+  if (st != GGNN_OK) return st;
+  CHECK_PTR(bits, "bits");
+  CHECK_PTR(X, "X");
+  CHECK_PTR(W, "W");
+  CHECK_OPT_PTR(bias, "bias");
+  CHECK_PTR(a, "a");
+  return device_status(launch_step_fwd_bits(dt, n_pad, B, H, E, bits, X, W, bias, a, as_stream(stream)),
+                       "banded_step_bits");
+}
+
+ggnn_status ggnn_banded_propagate_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
+                                           const void* bits_t, const void* da, void* dM, void* stream) {
+  clear_error();
+  ggnn_status st = check_banded(dt, n_pad, B, H, E);
+  if (st != GGNN_OK) return st;
+  CHECK_PTR(bits_t, "bits_t");
+  CHECK_PTR(da, "da");
+  CHECK_PTR(dM, "dM");
+  return device_status(launch_banded_bwd_bits(dt, n_pad, B, H, E, bits_t, da, dM, as_stream(stream)),
+                       "banded_propagate_bits_bwd");
+}
+
 size_t ggnn_msg_transform_bwd_workspace_bytes(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E) {
   if (!supported_dtype(dt) || n_pad <= 0 || n_pad % 32 != 0 || !supported_H(H) || E < 1 || E > 64) return 0;
   return transform_bwd_workspace(dt, n_pad, H, E);
@@ -178,15 +204,18 @@ static ggnn_status check_model(const ggnn_model* m) {
   CHECK_PTR(m->Wi, "model.Wi");
   CHECK_PTR(m->U, "model.U");
   CHECK_PTR(m->b, "model.b");
+  GGNN_CHECK_ARG(m->band_format == GGNN_BAND_DENSE || m->band_format == GGNN_BAND_BITS,
+                 "unknown band_format %d", m->band_format);
+  if (m->band_format == GGNN_BAND_BITS) CHECK_PTR(m->band_t, "model.band_t");
   return GGNN_OK;
 }
 
-static ggnn_status check_acts(const ggnn_activations* act) {
+static ggnn_status check_acts(const ggnn_model* m, const ggnn_activations* act) {
   GGNN_CHECK_ARG(act != nullptr, "activations is NULL");
   CHECK_PTR(act->X, "act.X");
   CHECK_PTR(act->a, "act.a");
   CHECK_PTR(act->saved, "act.saved");
-  CHECK_PTR(act->M, "act.M");
+  if (m->band_format == GGNN_BAND_DENSE) CHECK_PTR(act->M, "act.M");
   return GGNN_OK;
 }
 
@@ -195,16 +224,17 @@ size_t ggnn_backward_workspace_bytes(const ggnn_model* m) {
     clear_error();
     return 0;
   }
-  size_t a = gru_bwd_workspace(m->dtype, m->n_pad, m->H);
-  size_t b = transform_bwd_workspace(m->dtype, m->n_pad, m->H, m->E);
-  return a > b ? a : b;
+  // Both partial sets live for the whole reverse pass: GRU part, then the
+  // transform part at a 256-byte aligned offset.
+  size_t a = (gru_bwd_workspace(m->dtype, m->n_pad, m->H) + 255) / 256 * 256;
+  return a + transform_bwd_workspace(m->dtype, m->n_pad, m->H, m->E);
 }
 
 ggnn_status ggnn_forward(const ggnn_model* m, const ggnn_activations* act, void* stream) {
   clear_error();
   ggnn_status st = check_model(m);
   if (st != GGNN_OK) return st;
-  st = check_acts(act);
+  st = check_acts(m, act);
   if (st != GGNN_OK) return st;
   const size_t es = dtype_bytes(m->dtype);
   const size_t xs = (size_t)m->n_pad * m->H;
@@ -214,8 +244,13 @@ ggnn_status ggnn_forward(const ggnn_model* m, const ggnn_activations* act, void*
     char* Xn = static_cast<char*>(act->X) + (t + 1) * xs * es;
     float* at = act->a + t * xs;
     char* sv = static_cast<char*>(act->saved) + t * 3 * xs * es;
-    hipError_t err = launch_transform_fwd(m->dtype, m->n_pad, m->H, m->E, Xt, m->W, m->bias, act->M, s);
-    if (err == hipSuccess) err = launch_banded_fwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, act->M, at, s);
+    hipError_t err;
+    if (m->band_format == GGNN_BAND_BITS) {
+      err = launch_step_fwd_bits(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, Xt, m->W, m->bias, at, s);
+    } else {
+      err = launch_transform_fwd(m->dtype, m->n_pad, m->H, m->E, Xt, m->W, m->bias, act->M, s);
+      if (err == hipSuccess) err = launch_banded_fwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, act->M, at, s);
+    }
     if (err == hipSuccess) err = launch_gru_fwd(m->dtype, m->n_pad, m->H, at, Xt, m->Wi, m->U, m->b, Xn, sv, s);
     if (err != hipSuccess) return device_status(err, "forward");
   }
@@ -226,7 +261,7 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
   clear_error();
   ggnn_status st = check_model(m);
   if (st != GGNN_OK) return st;
-  st = check_acts(act);
+  st = check_acts(m, act);
   if (st != GGNN_OK) return st;
   GGNN_CHECK_ARG(gr != nullptr, "grads is NULL");
   CHECK_PTR(gr->dX, "grads.dX");
@@ -246,19 +281,34 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
   const size_t xs = (size_t)m->n_pad * m->H;
   hipStream_t s = as_stream(stream);
   float* dbias = m->bias ? gr->dbias : nullptr;
+  // Weight-gradient partials accumulate over all T steps and are reduced
+  // once at the end (fixed split partition and order: deterministic).
+  void* ws_gru = gr->workspace;
+  void* ws_tr = static_cast<char*>(gr->workspace) + (gru_bwd_workspace(m->dtype, m->n_pad, m->H) + 255) / 256 * 256;
+  {
+    hipError_t err = launch_gru_bwd_partials_clear(m->dtype, m->n_pad, m->H, ws_gru, s);
+    if (err == hipSuccess) err = launch_transform_bwd_partials_clear(m->dtype, m->n_pad, m->H, m->E, ws_tr, s);
+    if (err != hipSuccess) return device_status(err, "backward");
+  }
   for (int t = m->T - 1; t >= 0; --t) {
     const char* Xt = static_cast<const char*>(act->X) + t * xs * es;
     const float* at = act->a + t * xs;
     const char* sv = static_cast<const char*>(act->saved) + t * 3 * xs * es;
     hipError_t err = launch_gru_bwd(m->dtype, m->n_pad, m->H, gr->dX, at, Xt, sv, m->Wi, m->U, gr->da, gr->dh,
-                                    gr->dWi, gr->dU, gr->db, gr->workspace, s);
-    if (err == hipSuccess) err = launch_banded_bwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, gr->da, gr->dM, s);
+                                    gr->dWi, gr->dU, gr->db, ws_gru, s, 1);
+    if (err == hipSuccess)
+      err = m->band_format == GGNN_BAND_BITS
+                ? launch_banded_bwd_bits(m->dtype, m->n_pad, m->B, m->H, m->E, m->band_t, gr->da, gr->dM, s)
+                : launch_banded_bwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, gr->da, gr->dM, s);
     if (err == hipSuccess)
       err = launch_transform_bwd(m->dtype, m->n_pad, m->H, m->E, Xt, m->W, gr->dM, gr->dh, gr->dX, gr->dW, dbias,
-                                 gr->workspace, s);
+                                 ws_tr, s, 1);
     if (err != hipSuccess) return device_status(err, "backward");
   }
-  return GGNN_OK;
+  hipError_t err = launch_gru_bwd_partials_reduce(m->dtype, m->n_pad, m->H, gr->dWi, gr->dU, gr->db, ws_gru, s);
+  if (err == hipSuccess)
+    err = launch_transform_bwd_partials_reduce(m->dtype, m->n_pad, m->H, m->E, gr->dW, dbias, ws_tr, s);
+  return device_status(err, "backward");
 }
 
 }  // extern "C"

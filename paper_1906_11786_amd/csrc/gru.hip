@@ -275,7 +275,7 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
 template <typename S, int H>
 __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kernel(
     const float* __restrict__ a, const S* __restrict__ h, const S* __restrict__ saved, const S* __restrict__ ghat,
-    float* __restrict__ P, float* __restrict__ Pb, int n_pad, int nodes_per_split) {
+    float* __restrict__ P, float* __restrict__ Pb, int n_pad, int nodes_per_split, int accumulate) {
   constexpr int TI = H < 64 ? H : 64;
   constexpr int WAVES = TI / 16;
   constexpr int NT = WAVES * kWave;
@@ -353,7 +353,10 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kern
   for (int n = 0; n < NTL; ++n) {
     const int c = col0 + 16 * n + q;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * 3 * H + c] = acc[n][j];
+    for (int j = 0; j < 4; ++j) {
+      float* p = &out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * 3 * H + c];
+      *p = accumulate ? *p + acc[n][j] : acc[n][j];
+    }
   }
   if (do_bias) {
 #pragma unroll
@@ -361,7 +364,8 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kern
       float v = bsum[n];
       v += __shfl_xor(v, 16);
       v += __shfl_xor(v, 32);
-      if (g == 0) Pb[(size_t)split * 3 * H + col0 + 16 * n + q] = v;
+      float* p = &Pb[(size_t)split * 3 * H + col0 + 16 * n + q];
+      if (g == 0) *p = accumulate ? *p + v : v;
     }
   }
 }
@@ -398,7 +402,8 @@ hipError_t gru_fwd_h(int n_pad, const float* a, const void* h, const void* Wi, c
 
 template <typename S, int H>
 hipError_t gru_bwd_h(int n_pad, const float* dh_out, const float* a, const void* h, const void* saved, const void* Wi,
-                     const void* U, void* da, float* dh, float* dWi, float* dU, float* db, void* ws, hipStream_t st) {
+                     const void* U, void* da, float* dh, float* dWi, float* dU, float* db, void* ws, int pm,
+                     hipStream_t st) {
   constexpr int WAVES = 4;
   S* ghat = static_cast<S*>(ws);
   float* P = reinterpret_cast<float*>(static_cast<char*>(ws) + ghat_bytes(sizeof(S) == 2 ? GGNN_BF16 : GGNN_F32, n_pad, H));
@@ -412,9 +417,9 @@ hipError_t gru_bwd_h(int n_pad, const float* dh_out, const float* a, const void*
   constexpr int TI = H < 64 ? H : 64;
   const int blocks = sp.nsplit * 2 * (H / TI) * (3 * H / TI);
   hipLaunchKernelGGL((dev::gru_wgrad_kernel<S, H>), dim3(blocks), dim3(TI / 16 * 64), 0, st, a,
-                     static_cast<const S*>(h), static_cast<const S*>(saved), ghat, P, Pb, n_pad, sp.per);
+                     static_cast<const S*>(h), static_cast<const S*>(saved), ghat, P, Pb, n_pad, sp.per, pm);
   err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  if (err != hipSuccess || pm) return err;
   const long slice = 2L * H * 3 * H;  // partials are [split][which][H][3H]
   err = launch_reduce_partials(P, dWi, sp.nsplit, H * 3 * H, slice, st);
   if (err != hipSuccess) return err;
@@ -437,12 +442,12 @@ hipError_t gru_fwd_t(int n_pad, int H, const float* a, const void* h, const void
 template <typename S>
 hipError_t gru_bwd_t(int n_pad, int H, const float* dh_out, const float* a, const void* h, const void* saved,
                      const void* Wi, const void* U, void* da, float* dh, float* dWi, float* dU, float* db, void* ws,
-                     hipStream_t st) {
+                     int pm, hipStream_t st) {
   switch (H) {
-    case 32: return gru_bwd_h<S, 32>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, st);
-    case 64: return gru_bwd_h<S, 64>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, st);
-    case 128: return gru_bwd_h<S, 128>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, st);
-    case 256: return gru_bwd_h<S, 256>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, st);
+    case 32: return gru_bwd_h<S, 32>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, pm, st);
+    case 64: return gru_bwd_h<S, 64>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, pm, st);
+    case 128: return gru_bwd_h<S, 128>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, pm, st);
+    case 256: return gru_bwd_h<S, 256>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, pm, st);
   }
   return hipErrorInvalidValue;
 }
@@ -461,9 +466,29 @@ hipError_t launch_gru_fwd(int dt, int n_pad, int H, const float* a, const void* 
 
 hipError_t launch_gru_bwd(int dt, int n_pad, int H, const float* dh_out, const float* a, const void* h,
                           const void* saved, const void* Wi, const void* U, void* da, float* dh, float* dWi,
-                          float* dU, float* db, void* ws, hipStream_t st) {
-  return dt == GGNN_BF16 ? gru_bwd_t<dev::bf16s>(n_pad, H, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, st)
-                         : gru_bwd_t<float>(n_pad, H, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, st);
+                          float* dU, float* db, void* ws, hipStream_t st, int partial_mode) {
+  return dt == GGNN_BF16
+             ? gru_bwd_t<dev::bf16s>(n_pad, H, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, partial_mode, st)
+             : gru_bwd_t<float>(n_pad, H, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, partial_mode, st);
+}
+
+hipError_t launch_gru_bwd_partials_clear(int dt, int n_pad, int H, void* ws, hipStream_t st) {
+  Split sp = gru_split(n_pad, H);
+  float* P = reinterpret_cast<float*>(static_cast<char*>(ws) + ghat_bytes(dt, n_pad, H));
+  return launch_fill_zero(P, (size_t)sp.nsplit * 2 * H * 3 * H + (size_t)sp.nsplit * 3 * H, st);
+}
+
+hipError_t launch_gru_bwd_partials_reduce(int dt, int n_pad, int H, float* dWi, float* dU, float* db, void* ws,
+                                          hipStream_t st) {
+  Split sp = gru_split(n_pad, H);
+  float* P = reinterpret_cast<float*>(static_cast<char*>(ws) + ghat_bytes(dt, n_pad, H));
+  float* Pb = P + (size_t)sp.nsplit * 2 * H * 3 * H;
+  const long slice = 2L * H * 3 * H;
+  hipError_t err = launch_reduce_partials(P, dWi, sp.nsplit, H * 3 * H, slice, st);
+  if (err != hipSuccess) return err;
+  err = launch_reduce_partials(P + (size_t)H * 3 * H, dU, sp.nsplit, H * 3 * H, slice, st);
+  if (err != hipSuccess) return err;
+  return launch_reduce_partials(Pb, db, sp.nsplit, 3 * H, 3L * H, st);
 }
 
 }  // namespace ggnn

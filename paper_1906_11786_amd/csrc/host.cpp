@@ -280,4 +280,81 @@ ggnn_status ggnn_banded_pack(int32_t n_pad, int32_t E, int32_t B, int64_t m, con
   return GGNN_OK;
 }
 
+size_t ggnn_band_bits_bytes(int32_t n_pad, int32_t E, int32_t B) {
+  if (n_pad <= 0 || E <= 0 || B < 8 || B % 8 != 0 || n_pad % B != 0) return 0;
+  return static_cast<size_t>(E) * static_cast<size_t>(n_pad / B) * 3 * static_cast<size_t>(B) * (B / 8);
+}
+
+ggnn_status ggnn_banded_pack_bits(int32_t n_pad, int32_t E, int32_t B, int64_t m, const int32_t* src,
+                                  const int32_t* dst, const int32_t* etype, const int32_t* rank, int strict,
+                                  void* bits, void* bits_t, int64_t* n_packed, int64_t* n_dropped,
+                                  int64_t* n_duplicate) {
+  clear_error();
+  GGNN_CHECK_ARG(B >= 8 && B % 8 == 0 && n_pad >= B && n_pad % B == 0,
+                 "n_pad=%d must be a positive multiple of B=%d, B a multiple of 8", n_pad, B);
+  GGNN_CHECK_ARG(E >= 1 && E <= 64, "E=%d must be in [1, 64]", E);
+  GGNN_CHECK_ARG(m >= 0, "m=%lld must be >= 0", (long long)m);
+  GGNN_CHECK_ARG(m == 0 || (src && dst && etype), "src/dst/etype is NULL");
+  GGNN_CHECK_ARG(bits != nullptr, "bits is NULL");
+  const int64_t nb = n_pad / B;
+  if (rank)
+    for (int32_t v = 0; v < n_pad; ++v)
+      GGNN_CHECK_ARG(rank[v] >= 0 && rank[v] < n_pad, "rank[%d]=%d out of range [0,%d)", v, rank[v], n_pad);
+  for (int64_t k = 0; k < m; ++k) {
+    GGNN_CHECK_ARG(src[k] >= 0 && src[k] < n_pad && dst[k] >= 0 && dst[k] < n_pad,
+                   "edge %lld (%d -> %d) out of range [0,%d)", (long long)k, src[k], dst[k], n_pad);
+    GGNN_CHECK_ARG(etype[k] >= 0 && etype[k] < E, "edge %lld has type %d outside [0,%d)", (long long)k, etype[k],
+                   E);
+  }
+  const size_t nbytes = ggnn_band_bits_bytes(n_pad, E, B);
+  uint8_t* out = static_cast<uint8_t*>(bits);
+  uint8_t* out_t = static_cast<uint8_t*>(bits_t);
+  std::memset(out, 0, nbytes);
+  if (out_t) std::memset(out_t, 0, nbytes);
+  const size_t row_bytes = static_cast<size_t>(B / 8);
+  const size_t blk = static_cast<size_t>(B) * row_bytes;
+  int64_t packed = 0, dup = 0;
+  std::vector<std::tuple<int32_t, int64_t, int64_t>> out_of_band;
+  for (int64_t k = 0; k < m; ++k) {
+    const int64_t i = rank ? rank[dst[k]] : dst[k];
+    const int64_t j = rank ? rank[src[k]] : src[k];
+    const int64_t ki = i / B, kj = j / B;
+    const int64_t s = kj - ki + 1;
+    if (s < 0 || s > 2) {
+      try {
+        out_of_band.emplace_back(etype[k], i, j);
+      } catch (const std::bad_alloc&) {
+        return fail(GGNN_ERR_HOST_ALLOC, "temporary allocation failed");
+      }
+      continue;
+    }
+    const int64_t r = i % B, c = j % B;
+    // row r of block (e, ki, s), bit c
+    uint8_t* byte = out + ((static_cast<size_t>(etype[k]) * nb + ki) * 3 + s) * blk + r * row_bytes + c / 8;
+    const uint8_t bit = static_cast<uint8_t>(1u << (c % 8));
+    if (*byte & bit) {
+      ++dup;
+      continue;
+    }
+    *byte |= bit;
+    ++packed;
+    if (out_t) {
+      // transposed block: row c of block (e, kj, 2 - s), bit r
+      uint8_t* tb = out_t + ((static_cast<size_t>(etype[k]) * nb + kj) * 3 + (2 - s)) * blk + c * row_bytes + r / 8;
+      *tb |= static_cast<uint8_t>(1u << (r % 8));
+    }
+  }
+  std::sort(out_of_band.begin(), out_of_band.end());
+  const int64_t n_oob = static_cast<int64_t>(out_of_band.size());
+  const int64_t dropped = static_cast<int64_t>(std::unique(out_of_band.begin(), out_of_band.end()) - out_of_band.begin());
+  dup += n_oob - dropped;
+  if (n_packed) *n_packed = packed;
+  if (n_dropped) *n_dropped = dropped;
+  if (n_duplicate) *n_duplicate = dup;
+  if (strict && dropped > 0)
+    return fail(GGNN_ERR_OUT_OF_BAND, "%lld edge(s) fall outside the three block diagonals (B=%d)",
+                (long long)dropped, B);
+  return GGNN_OK;
+}
+
 }  // extern "C"

@@ -158,7 +158,7 @@ __global__ __launch_bounds__(WAVES * kWave) void transform_bwd_dx_kernel(const S
 template <typename S, int H>
 __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgrad_kernel(
     const S* __restrict__ X, const S* __restrict__ dM, float* __restrict__ P, float* __restrict__ Pb, int n_pad,
-    int E, int nodes_per_split) {
+    int E, int nodes_per_split, int accumulate) {
   constexpr int TI = H < 64 ? H : 64;
   constexpr int WAVES = TI / 16;
   constexpr int NT = WAVES * kWave;
@@ -219,7 +219,10 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
   for (int n = 0; n < NTL; ++n) {
     const int o = to * TI + 16 * n + q;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * H + o] = acc[n][j];
+    for (int j = 0; j < 4; ++j) {
+      float* p = &out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * H + o];
+      *p = accumulate ? *p + acc[n][j] : acc[n][j];
+    }
   }
   if (do_bias) {
 #pragma unroll
@@ -227,7 +230,8 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
       float v = bsum[n];
       v += __shfl_xor(v, 16);
       v += __shfl_xor(v, 32);
-      if (g == 0) Pb[((size_t)split * E + e) * H + to * TI + 16 * n + q] = v;
+      float* p = &Pb[((size_t)split * E + e) * H + to * TI + 16 * n + q];
+      if (g == 0) *p = accumulate ? *p + v : v;
     }
   }
 }
@@ -243,6 +247,24 @@ __global__ void reduce_partials_kernel(const float* __restrict__ part, float* __
   float s = 0.f;
   for (int k = 0; k < nsplit; ++k) s += part[(size_t)k * stride + i];
   out[i] += s;
+}
+
+// Zero-fill with a kernel (not hipMemsetAsync, so the launch can sit inside a
+// captured HIP graph).  p is 16-byte aligned.
+__global__ void fill_zero_kernel(float* __restrict__ p, size_t count) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (4 * i + 3 < count) {
+    reinterpret_cast<float4*>(p)[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+  } else {
+    for (size_t k = 4 * i; k < count; ++k) p[k] = 0.f;
+  }
+}
+
+hipError_t launch_fill_zero(float* p, size_t count, hipStream_t st) {
+  if (count == 0) return hipSuccess;
+  const size_t n4 = (count + 3) / 4;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, st, p, count);
+  return hipGetLastError();
 }
 
 hipError_t launch_reduce_partials(const float* part, float* out, int nsplit, int count, long stride,
@@ -290,7 +312,7 @@ hipError_t transform_fwd_h(int n_pad, int E, const void* X, const void* W, const
 
 template <typename S, int H>
 hipError_t transform_bwd_h(int n_pad, int E, const void* X, const void* W, const void* dM, const float* dX_in,
-                           float* dX_out, float* dW, float* dbias, void* ws, hipStream_t st) {
+                           float* dX_out, float* dW, float* dbias, void* ws, int partial_mode, hipStream_t st) {
   const S* xp = static_cast<const S*>(X);
   const S* wp = static_cast<const S*>(W);
   const S* dp = static_cast<const S*>(dM);
@@ -304,9 +326,9 @@ hipError_t transform_bwd_h(int n_pad, int E, const void* X, const void* W, const
   float* Pb = dbias ? P + (size_t)sp.nsplit * E * H * H : nullptr;
   const int blocks = sp.nsplit * E * (H / TI) * (H / TI);
   hipLaunchKernelGGL((dev::transform_wgrad_kernel<S, H>), dim3(blocks), dim3(TI / 16 * 64), 0, st, xp, dp, P, Pb,
-                     n_pad, E, sp.per);
+                     n_pad, E, sp.per, partial_mode);
   err = hipGetLastError();
-  if (err != hipSuccess) return err;
+  if (err != hipSuccess || partial_mode) return err;
   err = launch_reduce_partials(P, dW, sp.nsplit, E * H * H, (long)E * H * H, st);
   if (err != hipSuccess || !dbias) return err;
   return launch_reduce_partials(Pb, dbias, sp.nsplit, E * H, (long)E * H, st);
@@ -325,12 +347,12 @@ hipError_t transform_fwd_t(int n_pad, int H, int E, const void* X, const void* W
 }
 template <typename S>
 hipError_t transform_bwd_t(int n_pad, int H, int E, const void* X, const void* W, const void* dM, const float* dX_in,
-                           float* dX_out, float* dW, float* dbias, void* ws, hipStream_t st) {
+                           float* dX_out, float* dW, float* dbias, void* ws, int pm, hipStream_t st) {
   switch (H) {
-    case 32: return transform_bwd_h<S, 32>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, st);
-    case 64: return transform_bwd_h<S, 64>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, st);
-    case 128: return transform_bwd_h<S, 128>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, st);
-    case 256: return transform_bwd_h<S, 256>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, st);
+    case 32: return transform_bwd_h<S, 32>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, pm, st);
+    case 64: return transform_bwd_h<S, 64>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, pm, st);
+    case 128: return transform_bwd_h<S, 128>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, pm, st);
+    case 256: return transform_bwd_h<S, 256>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, pm, st);
   }
   return hipErrorInvalidValue;
 }
@@ -350,9 +372,24 @@ hipError_t launch_transform_fwd(int dt, int n_pad, int H, int E, const void* X, 
 
 hipError_t launch_transform_bwd(int dt, int n_pad, int H, int E, const void* X, const void* W, const void* dM,
                                 const float* dX_in, float* dX_out, float* dW, float* dbias, void* ws,
-                                hipStream_t st) {
-  return dt == GGNN_BF16 ? transform_bwd_t<dev::bf16s>(n_pad, H, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, st)
-                         : transform_bwd_t<float>(n_pad, H, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, st);
+                                hipStream_t st, int partial_mode) {
+  return dt == GGNN_BF16
+             ? transform_bwd_t<dev::bf16s>(n_pad, H, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, partial_mode, st)
+             : transform_bwd_t<float>(n_pad, H, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, partial_mode, st);
+}
+
+hipError_t launch_transform_bwd_partials_clear(int dt, int n_pad, int H, int E, void* ws, hipStream_t st) {
+  return launch_fill_zero(static_cast<float*>(ws), transform_bwd_workspace(dt, n_pad, H, E) / sizeof(float), st);
+}
+
+hipError_t launch_transform_bwd_partials_reduce(int dt, int n_pad, int H, int E, float* dW, float* dbias, void* ws,
+                                                hipStream_t st) {
+  (void)dt;
+  Split sp = transform_split(n_pad, H, E);
+  float* P = static_cast<float*>(ws);
+  hipError_t err = launch_reduce_partials(P, dW, sp.nsplit, E * H * H, (long)E * H * H, st);
+  if (err != hipSuccess || !dbias) return err;
+  return launch_reduce_partials(P + (size_t)sp.nsplit * E * H * H, dbias, sp.nsplit, E * H, (long)E * H, st);
 }
 
 }  // namespace ggnn

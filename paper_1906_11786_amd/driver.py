@@ -80,20 +80,36 @@ class BandedGGNN:
     """Device state of one workload: band, parameters, stored activations,
     gradients and workspace, sized for T steps."""
 
-    def __init__(self, comp: Compiled, H: int, T: int, dt: str, params, device="cuda", strict: bool = True):
+    def __init__(self, comp: Compiled, H: int, T: int, dt: str, params, device="cuda", strict: bool = True,
+                 band_format: str = "bits"):
+        """band_format: "bits" (1 bit per band entry; aggregate-first fused
+        forward) or "dense" (band entries in the compute dtype; transform-first
+        forward)."""
         import torch
         self.torch = torch
         self.comp, self.H, self.T, self.dt, self.device = comp, H, T, dt, device
+        self.band_format = band_format
         n_pad, E, B = comp.n_pad, comp.E, comp.B
         td = torch_dtype(dt)
         t0 = time.perf_counter()
-        band, packed, dropped, dup = capi.ggnn_banded_pack(n_pad, E, B, comp.src, comp.dst, comp.etype, dt=dt,
-                                                           strict=strict)
-        comp.stats.update(n_packed=packed, n_dropped=dropped, n_duplicate=dup,
-                          pack_seconds=time.perf_counter() - t0)
-        t0 = time.perf_counter()
-        self.band = band_to_device(band, dt, device)
-        del band
+        self.band_t = None
+        if band_format == "bits":
+            bits, bits_t, packed, dropped, dup = capi.ggnn_banded_pack_bits(n_pad, E, B, comp.src, comp.dst,
+                                                                            comp.etype, strict=strict)
+            comp.stats.update(n_packed=packed, n_dropped=dropped, n_duplicate=dup,
+                              pack_seconds=time.perf_counter() - t0)
+            t0 = time.perf_counter()
+            self.band = torch.from_numpy(bits).to(device)
+            self.band_t = torch.from_numpy(bits_t).to(device)
+            del bits, bits_t
+        else:
+            band, packed, dropped, dup = capi.ggnn_banded_pack(n_pad, E, B, comp.src, comp.dst, comp.etype, dt=dt,
+                                                               strict=strict)
+            comp.stats.update(n_packed=packed, n_dropped=dropped, n_duplicate=dup,
+                              pack_seconds=time.perf_counter() - t0)
+            t0 = time.perf_counter()
+            self.band = band_to_device(band, dt, device)
+            del band
         self.W = to_device(params.W, dt, device)
         self.bias = None if params.bias is None else torch.from_numpy(params.bias.astype(np.float32)).to(device)
         self.Wi = to_device(params.Wi, dt, device)
@@ -103,7 +119,8 @@ class BandedGGNN:
         self.X[0].copy_(to_device(params.X, dt, device))
         self.a = torch.empty((T, n_pad, H), dtype=torch.float32, device=device)
         self.saved = torch.empty((T, n_pad, 3 * H), dtype=td, device=device)
-        self.M = torch.empty((E, H, n_pad), dtype=torch.float32, device=device)
+        self.M = (torch.empty((E, H, n_pad), dtype=torch.float32, device=device) if band_format == "dense"
+                  else None)
         self.G = torch.from_numpy(params.G.astype(np.float32)).to(device)
         self.dX = torch.empty((n_pad, H), dtype=torch.float32, device=device)
         self.dW = torch.zeros((E, H, H), dtype=torch.float32, device=device)
@@ -117,11 +134,12 @@ class BandedGGNN:
         self.model = capi.ggnn_model(
             dtype=capi.DTYPES[dt], n_pad=n_pad, B=B, H=H, E=E, T=T, band=self.band.data_ptr(),
             W=self.W.data_ptr(), bias=None if self.bias is None else self.bias.data_ptr(), Wi=self.Wi.data_ptr(),
-            U=self.U.data_ptr(), b=self.b.data_ptr())
+            U=self.U.data_ptr(), b=self.b.data_ptr(), band_format=capi.BAND_FORMATS[band_format],
+            band_t=None if self.band_t is None else self.band_t.data_ptr())
         ws = capi.ggnn_backward_workspace_bytes(self.model)
         self.workspace = torch.empty((max(ws, 16),), dtype=torch.uint8, device=device)
         self.act = capi.ggnn_activations(X=self.X.data_ptr(), a=self.a.data_ptr(), saved=self.saved.data_ptr(),
-                                         M=self.M.data_ptr())
+                                         M=None if self.M is None else self.M.data_ptr())
         self.grads = capi.ggnn_grads(
             dX=self.dX.data_ptr(), dW=self.dW.data_ptr(), dbias=self.dbias.data_ptr(), dWi=self.dWi.data_ptr(),
             dU=self.dU.data_ptr(), db=self.db.data_ptr(), da=self.da.data_ptr(), dM=self.dM.data_ptr(),

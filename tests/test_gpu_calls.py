@@ -197,6 +197,62 @@ def test_gru_update_bwd(dt, H, n):
     assert relerr(host(db) - 1, wdb) <= TOL[dt]
 
 
+def _bits(n_pad, E, B, src, dst, et):
+    bits, bits_t, packed, dropped, dup = capi.ggnn_banded_pack_bits(n_pad, E, B, src, dst, et)
+    return torch.from_numpy(bits).cuda(), torch.from_numpy(bits_t).cuda(), dropped
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("B,H,E,nb", BANDED_CASES)
+def test_banded_step_bits_integer_exact(dt, B, H, E, nb):
+    """a = sum_e (A_e X) W_e on the 1-bit band, small integers: exact."""
+    say(f"banded_step_bits int dt={dt} B={B} H={H} E={E} nb={nb}")
+    rng = np.random.default_rng(B * 7 + H + E)
+    n = B * nb
+    src, dst, et = _edges(rng, n, 6 * n, E, 2 * B + 5)
+    bits, _, dropped = _bits(n, E, B, src, dst, et)
+    X = rng.integers(-2, 3, (n, H)).astype(np.float64)
+    W = rng.integers(-1, 2, (E, H, H)).astype(np.float64)
+    bias = rng.integers(-2, 3, (E, H)).astype(np.float64)
+    a = torch.full((n, H), float("nan"), device="cuda")
+    capi.ggnn_banded_step_bits(dt, n, B, H, E, bits, dev(X, dt), dev(W, dt), dev(bias), a)
+    s, d, e, _, _ = O.kept_edges(src, dst, et, B)
+    np.testing.assert_array_equal(host(a), O.aggregate(n, s, d, e, O.msg_transform(X, W, bias)))
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("B,H,E,nb", [(128, 64, 3, 5), (64, 128, 2, 6), (256, 256, 2, 3), (32, 32, 4, 9)])
+def test_banded_step_bits_real_values(dt, B, H, E, nb):
+    """bf16 inputs, fp32 results: the aggregate enters the transform as a hi +
+    lo pair, so the result is close to fp32 accuracy."""
+    say(f"banded_step_bits real dt={dt} B={B} H={H} E={E} nb={nb}")
+    rng = np.random.default_rng(B + 3 * H + E)
+    n = B * nb
+    src, dst, et = _edges(rng, n, 4 * n, E, B + 3)
+    bits, _, _ = _bits(n, E, B, src, dst, et)
+    X = round_to(dt, rng.standard_normal((n, H)))
+    W = round_to(dt, rng.standard_normal((E, H, H)) / np.sqrt(H))
+    a = torch.empty((n, H), device="cuda")
+    capi.ggnn_banded_step_bits(dt, n, B, H, E, bits, dev(X, dt), dev(W, dt), None, a)
+    s, d, e, _, _ = O.kept_edges(src, dst, et, B)
+    assert relerr(host(a), O.aggregate(n, s, d, e, O.msg_transform(X, W))) <= 1e-4
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("B,H,E,nb", BANDED_CASES)
+def test_banded_propagate_bits_bwd_integer_exact(dt, B, H, E, nb):
+    say(f"banded_propagate_bits_bwd int dt={dt} B={B} H={H} E={E} nb={nb}")
+    rng = np.random.default_rng(B * 19 + H + E)
+    n = B * nb
+    src, dst, et = _edges(rng, n, 6 * n, E, 2 * B + 5)
+    _, bits_t, _ = _bits(n, E, B, src, dst, et)
+    da = rng.integers(-4, 5, (n, H)).astype(np.float64)
+    dM = torch.full((E, H, n), float("nan"), device="cuda", dtype=torch_dt(dt))
+    capi.ggnn_banded_propagate_bits_bwd(dt, n, B, H, E, bits_t, dev(da.T, dt), dM)
+    s, d, e, _, _ = O.kept_edges(src, dst, et, B)
+    np.testing.assert_array_equal(host(dM), O.aggregate_transpose(n, s, d, e, da, E).transpose(0, 2, 1))
+
+
 def test_device_errors_are_reported():
     n, H = 128, 64
     ws_n = capi.ggnn_gru_update_bwd_workspace_bytes("bf16", n, H)

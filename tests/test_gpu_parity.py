@@ -56,14 +56,14 @@ def _compare(res, out, dt, keys=("XT", "dX0", "dW", "dWi", "dU", "db"), rows=Non
     return errs
 
 
-def _run_full(graphs, spec_B, E, H, T, dt, cfg, reorder, with_bias=False):
+def _run_full(graphs, spec_B, E, H, T, dt, cfg, reorder, with_bias=False, band_format="bits"):
     comp = drv.compile_graphs(graphs, spec_B, E, reorder=reorder)
     n_real, n_pad, s, d, e, offs = _oracle_edges(graphs, spec_B, reorder)
     assert (n_real, n_pad) == (comp.n_real, comp.n_pad)
     np.testing.assert_array_equal(comp.src, s)         # the product's reordering equals the oracle's
     np.testing.assert_array_equal(comp.dst, d)
     params = draw_params(cfg, n_real, n_pad, H, E, dt, with_bias=with_bias)
-    m = drv.BandedGGNN(comp, H, T, dt, params)
+    m = drv.BandedGGNN(comp, H, T, dt, params, band_format=band_format)
     m.step()
     torch.cuda.synchronize()
     res = m.results()
@@ -73,11 +73,13 @@ def _run_full(graphs, spec_B, E, H, T, dt, cfg, reorder, with_bias=False):
     return m, res, out
 
 
-def test_tiny_fp32_workload():
+@pytest.mark.parametrize("band_format", ["bits", "dense"])
+def test_tiny_fp32_workload(band_format):
     spec = CONFIGS[0]
-    say(f"workload {spec.name}")
+    say(f"workload {spec.name} band={band_format}")
     g = make_graphs(spec)
-    _, res, out = _run_full(g, spec.B, spec.E, spec.H, spec.T, spec.dtype, spec.cfg, reorder=False)
+    _, res, out = _run_full(g, spec.B, spec.E, spec.H, spec.T, spec.dtype, spec.cfg, reorder=False,
+                            band_format=band_format)
     assert out["n_dropped"] == 0
     _compare(res, out, "f32")
 
@@ -94,22 +96,24 @@ SMALL = [  # (dt, n_nodes, B, E, H, T, bias)
 ]
 
 
+@pytest.mark.parametrize("band_format", ["bits", "dense"])
 @pytest.mark.parametrize("dt,n,B,E,H,T,bias", SMALL)
-def test_small_cases(dt, n, B, E, H, T, bias):
-    say(f"small dt={dt} n={n} B={B} E={E} H={H} T={T} bias={bias}")
+def test_small_cases(dt, n, B, E, H, T, bias, band_format):
+    say(f"small dt={dt} n={n} B={B} E={E} H={H} T={T} bias={bias} band={band_format}")
     g = scramble_graph(50 + n, 0, backbone_graph(50 + n, 0, n, E, span_mean=6.0, max_span=B))[0]
-    _, res, out = _run_full([g], B, E, H, T, dt, 50 + n, reorder=True, with_bias=bias)
+    _, res, out = _run_full([g], B, E, H, T, dt, 50 + n, reorder=True, with_bias=bias, band_format=band_format)
     _compare(res, out, dt)
 
 
-def test_small_lossy_band():
+@pytest.mark.parametrize("band_format", ["bits", "dense"])
+def test_small_lossy_band(band_format):
     """Bandwidth above the block size: edges outside the three block
     diagonals are dropped identically by both sides."""
     dt, n, B, E, H, T = "bf16", 1200, 32, 3, 64, 2
     g = backbone_graph(77, 0, n, E, span_mean=20.0, max_span=90)
     comp = drv.compile_graphs([g], B, E, reorder=False)
     params = draw_params(77, comp.n_real, comp.n_pad, H, E, dt)
-    m = drv.BandedGGNN(comp, H, T, dt, params, strict=False)
+    m = drv.BandedGGNN(comp, H, T, dt, params, strict=False, band_format=band_format)
     assert comp.stats["n_dropped"] > 0
     m.step()
     out = O.propagate(comp.n_pad, B, g.src, g.dst, g.etype, params.X, params.W, params.Wi, params.U, params.b, T,
@@ -118,11 +122,13 @@ def test_small_lossy_band():
     _compare(m.results(), out, dt)
 
 
-def test_program_graph_workload():
+@pytest.mark.parametrize("band_format", ["bits", "dense"])
+def test_program_graph_workload(band_format):
     spec = CONFIGS[1]
-    say(f"workload {spec.name}")
+    say(f"workload {spec.name} band={band_format}")
     g = make_graphs(spec)
-    m, res, out = _run_full(g, spec.B, spec.E, spec.H, spec.T, spec.dtype, spec.cfg, reorder=True)
+    m, res, out = _run_full(g, spec.B, spec.E, spec.H, spec.T, spec.dtype, spec.cfg, reorder=True,
+                            band_format=band_format)
     assert out["n_dropped"] == 0 and m.comp.bandwidth <= spec.B - 1
     _compare(res, out, spec.dtype)
     # determinism: a second pass gives identical bits
@@ -133,11 +139,13 @@ def test_program_graph_workload():
         assert np.array_equal(res[k], res2[k]), k
 
 
+@pytest.mark.parametrize("band_format", ["bits", "dense"])
 @pytest.mark.parametrize("spec", sweep_blocks(), ids=lambda s: f"B{s.B}")
-def test_sweep_workloads(spec):
-    say(f"workload {spec.name}")
+def test_sweep_workloads(spec, band_format):
+    say(f"workload {spec.name} band={band_format}")
     g = make_graphs(spec)
-    _, res, out = _run_full(g, spec.B, spec.E, spec.H, spec.T, spec.dtype, spec.cfg, reorder=False)
+    _, res, out = _run_full(g, spec.B, spec.E, spec.H, spec.T, spec.dtype, spec.cfg, reorder=False,
+                            band_format=band_format)
     assert out["n_dropped"] == 0
     _compare(res, out, spec.dtype)
 

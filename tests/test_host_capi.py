@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
     for name in declared:
         assert hasattr(L, name), name
     assert set(declared) == set(capi.EXPORTS)
-    assert capi.ggnn_abi_version() == 1
+    assert capi.ggnn_abi_version() == 2
     assert capi.ggnn_status_string(3) == "GGNN_ERR_OUT_OF_BAND"
 
 
@@ -159,3 +159,53 @@ def test_device_entry_points_validate_before_touching_the_gpu():
     assert capi.ggnn_gru_update_bwd_workspace_bytes("bf16", 20096, 64) > 0
     assert capi.ggnn_msg_transform_bwd_workspace_bytes("bf16", 20096, 64, 10) > 0
     assert capi.ggnn_msg_transform_bwd_workspace_bytes("bf16", 20096, 48, 10) == 0
+
+
+def _unpack_bits(bits):
+    return np.unpackbits(bits, axis=-1, bitorder="little").astype(np.float64)
+
+
+@pytest.mark.parametrize("B", [8, 32, 64])
+def test_pack_bits_bit_exact_against_oracle(B):
+    _need_lib()
+    rng = np.random.default_rng(300 + B)
+    nb, E = 7, 3
+    n = nb * B
+    src = rng.integers(0, n, 1200)
+    dst = np.clip(src + rng.integers(-3 * B, 3 * B + 1, 1200), 0, n - 1)
+    et = rng.integers(0, E, 1200)
+    src = np.concatenate([src, src[:40]]); dst = np.concatenate([dst, dst[:40]]); et = np.concatenate([et, et[:40]])
+    bits, bits_t, packed, dropped, dup = capi.ggnn_banded_pack_bits(n, E, B, src, dst, et)
+    assert bits.shape == (E, nb, 3, B, B // 8)
+    assert capi.ggnn_band_bits_bytes(n, E, B) == bits.nbytes
+    band = O.pack_band(n, E, B, src, dst, et)
+    np.testing.assert_array_equal(_unpack_bits(bits), band)
+    s, d, e, odrop, odup = O.kept_edges(src, dst, et, B)
+    assert (packed, dropped, dup) == (len(s), odrop, odup)
+    # transposed blocks with roles swapped: bits_t[e][j][s] = band[e][j-1+s][2-s]^T
+    bt = _unpack_bits(bits_t)
+    for j in range(nb):
+        for sl in range(3):
+            kr = j - 1 + sl
+            want = band[:, kr, 2 - sl].transpose(0, 2, 1) if 0 <= kr < nb else np.zeros((E, B, B))
+            np.testing.assert_array_equal(bt[:, j, sl], want)
+    # and, semantically, the transposed band applied to da is the oracle's gather
+    da = rng.integers(-3, 4, (n, 5)).astype(np.float64)
+    dap = np.zeros((nb + 2, B, 5)); dap[1:nb + 1] = da.reshape(nb, B, 5)
+    dM = np.zeros((E, nb, B, 5))
+    for sl in range(3):
+        dM += np.einsum("ejcr,jrh->ejch", bt[:, :, sl], dap[sl:sl + nb])
+    np.testing.assert_array_equal(dM.reshape(E, n, 5), O.aggregate_transpose(n, s, d, e, da, E))
+
+
+def test_pack_bits_strict_and_errors():
+    _need_lib()
+    src = np.array([0, 100]); dst = np.array([1, 0]); et = np.array([0, 0])
+    with pytest.raises(capi.GGNNError) as ei:
+        capi.ggnn_banded_pack_bits(128, 1, 32, src, dst, et, strict=True)
+    assert ei.value.status_name == "GGNN_ERR_OUT_OF_BAND"
+    with pytest.raises(capi.GGNNError) as ei:
+        capi.ggnn_banded_pack_bits(120, 1, 12, src, dst, et)      # B not a multiple of 8
+    assert ei.value.status_name == "GGNN_ERR_INVALID_ARG"
+    bits, bits_t, *_ = capi.ggnn_banded_pack_bits(128, 1, 32, src, dst, et, with_transpose=False)
+    assert bits_t is None and int(np.unpackbits(bits).sum()) == 1
