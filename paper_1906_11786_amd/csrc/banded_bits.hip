@@ -189,7 +189,34 @@ __global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* 
     }
   };
   if constexpr (C::ALL) load_type(0, nxt);
+  // W_e^T chunks: one chunk of WC output rows is H * WC / V 16-byte units.
+  constexpr int WU = (H * (WC / V) + NT - 1) / NT;
+  u32x4 wreg[WU];
+  auto load_w = [&](int e, int oc) __attribute__((always_inline)) {
+    const S* wsrc = W + (size_t)e * H * H + oc;
+#pragma unroll
+    for (int u = 0; u < WU; ++u) {
+      const int lin = u * NT + tid;
+      if ((H * (WC / V)) % NT == 0 || lin < H * (WC / V)) {
+        const int h = lin / (WC / V), o8 = (lin % (WC / V)) * V;
+        wreg[u] = *reinterpret_cast<const u32x4*>(wsrc + (size_t)h * H + o8);
+      }
+    }
+  };
+  auto store_w = [&]() __attribute__((always_inline)) {   // wt[o][h] = W[e][h][oc + o]
+#pragma unroll
+    for (int u = 0; u < WU; ++u) {
+      const int lin = u * NT + tid;
+      if ((H * (WC / V)) % NT == 0 || lin < H * (WC / V)) {
+        const int h = lin / (WC / V), o8 = (lin % (WC / V)) * V;
+        const S* pw = reinterpret_cast<const S*>(&wreg[u]);
+#pragma unroll
+        for (int x = 0; x < V; ++x) wt[(o8 + x) * WP + h] = pw[x];
+      }
+    }
+  };
   for (int e = 0; e < E; ++e) {
+    load_w(e, 0);   // in flight during the aggregation below
     f32x4 pre[NTW][MT];
 #pragma unroll
     for (int n = 0; n < NTW; ++n)
@@ -261,15 +288,9 @@ __global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* 
       }
     for (int oc = 0; oc < H; oc += WC) {
       __syncthreads();
-      const S* wsrc = W + (size_t)e * H * H + oc;
-      for (int lin = tid; lin < H * (WC / V); lin += NT) {   // wt[o][h] = W[e][h][oc + o]
-        const int h = lin / (WC / V), o8 = (lin % (WC / V)) * V;
-        u32x4 w = *reinterpret_cast<const u32x4*>(wsrc + (size_t)h * H + o8);
-        const S* pw = reinterpret_cast<const S*>(&w);
-#pragma unroll
-        for (int x = 0; x < V; ++x) wt[(o8 + x) * WP + h] = pw[x];
-      }
+      store_w();
       __syncthreads();
+      if (oc + WC < H) load_w(e, oc + WC);   // next chunk, in flight during this one
 #pragma unroll
       for (int mo = 0; mo < WC / 16; ++mo)
 #pragma unroll
@@ -314,7 +335,7 @@ __global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* 
 template <typename S, int H, int B, int WAVES>
 __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* __restrict__ bits_t,
                                                                   const S* __restrict__ da, S* __restrict__ dM,
-                                                                  int n_pad, int E) {
+                                                                  int n_pad, int E, int groups) {
   using C = BitsCfg<S, H, B>;
   constexpr int NT = WAVES * kWave;
   constexpr int KC = C::KC, VP = C::VP, RB = C::RB, NTW = C::NTW;
@@ -325,7 +346,11 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
   const int nb = n_pad / B;
   constexpr int NW = C::RPW * WAVES;
   const int tiles_per_blk = B / NW;
-  const int t = xcd_swizzle(blockIdx.x, gridDim.x);
+  // Logical id = (tile, type group), the group fastest: the groups of one
+  // tile share the staged da blocks through one XCD's L2.
+  const int t0 = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int grp = t0 % groups, t = t0 / groups;
+  const int e_lo = grp * E / groups, e_hi = (grp + 1) * E / groups;
   const int j = t / tiles_per_blk;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int q = lane % 16, g = lane / 16;
@@ -347,8 +372,8 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
       for (int m = 0; m < NTW; ++m) dst[s][m].load(brow + (size_t)16 * m * ROWB);
     }
   };
-  if constexpr (C::ALL) load_type(0, nxt);
-  for (int e = 0; e < E; ++e) {
+  if constexpr (C::ALL) load_type(e_lo, nxt);
+  for (int e = e_lo; e < e_hi; ++e) {
     f32x4 acc[NTW][NTL];
 #pragma unroll
     for (int m = 0; m < NTW; ++m)
@@ -360,7 +385,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
       for (int s = 0; s < 3; ++s)
 #pragma unroll
         for (int m = 0; m < NTW; ++m) cur[s][m] = nxt[s][m];
-      if (e + 1 < E) load_type(e + 1, nxt);
+      if (e + 1 < e_hi) load_type(e + 1, nxt);
     }
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
@@ -413,7 +438,10 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
 #define GGNN_BITS_FWD_MIN_BLOCKS 64
 #endif
 #ifndef GGNN_BITS_BWD_MIN_BLOCKS
-#define GGNN_BITS_BWD_MIN_BLOCKS 256
+#define GGNN_BITS_BWD_MIN_BLOCKS 64
+#endif
+#ifndef GGNN_BITS_BWD_WAVES
+#define GGNN_BITS_BWD_WAVES 4096
 #endif
 
 namespace {
@@ -425,7 +453,15 @@ hipError_t bits_launch(bool fwd, const void* bits, const void* V, const void* W,
   int waves = B / C::RPW < 4 ? B / C::RPW : 4;
   const long min_blocks = fwd ? GGNN_BITS_FWD_MIN_BLOCKS : GGNN_BITS_BWD_MIN_BLOCKS;
   while (waves > 1 && (long)nb * (B / (C::RPW * waves)) < min_blocks) waves /= 2;
-  const int blocks = nb * (B / (C::RPW * waves));
+  const int tiles = nb * (B / (C::RPW * waves));
+  // The reverse pass writes one output per edge type, so types can be split
+  // over workgroups freely: enough groups for about GGNN_BITS_BWD_WAVES waves.
+  int groups = 1;
+  if (!fwd) {
+    const long want = (GGNN_BITS_BWD_WAVES + (long)tiles * waves - 1) / ((long)tiles * waves);
+    groups = (int)(want < 1 ? 1 : (want > E ? E : want));
+  }
+  const int blocks = tiles * groups;
   const uint8_t* bp = static_cast<const uint8_t*>(bits);
   const S* vp = static_cast<const S*>(V);
 #define GGNN_BITS_CASE(WV)                                                                                   \
@@ -436,7 +472,7 @@ hipError_t bits_launch(bool fwd, const void* bits, const void* V, const void* W,
                            static_cast<const S*>(W), bias, static_cast<float*>(out), n_pad, E);              \
       else                                                                                                   \
         hipLaunchKernelGGL((dev::bits_bwd_kernel<S, H, B, WV>), dim3(blocks), dim3(WV * 64), 0, st, bp, vp,  \
-                           static_cast<S*>(out), n_pad, E);                                                  \
+                           static_cast<S*>(out), n_pad, E, groups);                                          \
     }                                                                                                        \
     break;
   switch (waves) {

@@ -166,100 +166,122 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_fwd_kernel(const float* __r
 // g = dL/dh', dn = g(1-z), dz = g(h-n), n^ = dn(1-n^2), z^ = dz z(1-z),
 // q = n^ U_n^T, r^ = q h r(1-r):
 //   dh = g z + q r + r^ U_r^T + z^ U_z^T,   da = [r^ z^ n^] Wi^T.
-// The gate gradients G^ = [r^ z^ n^] go to `ghat` (node-major [n_pad][3H])
-// for the weight-gradient pass; every lane only re-reads values it wrote
-// itself, so the phases need no barrier.  Weight fragments are read from
-// global memory (they are small and stay cached).
+// The gate gradients are kept in registers as operand fragments
+// (accumulator-compatible order) and dh as an accumulator across the four
+// phases; G^ = [r^ z^ n^] is also written to `ghat` (node-major
+// [n_pad][3H]) for the weight-gradient pass.  For H <= 64 the weights are
+// staged once per workgroup in LDS (plain copies: the reverse products read
+// rows of Wi and U, contiguous in the gate dimension); larger H reads their
+// fragments from global memory (cached).
 // ---------------------------------------------------------------------------
 template <typename S, int H, int WAVES>
 __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __restrict__ gin, const S* __restrict__ h,
                                                                  const S* __restrict__ saved, const S* __restrict__ Wi,
                                                                  const S* __restrict__ U, S* __restrict__ daT,
-                                                                 float* dh, S* ghat, int n_pad) {
+                                                                 float* __restrict__ dh, S* __restrict__ ghat,
+                                                                 int n_pad) {
   constexpr int KS = H / 32;
   constexpr int MTL = H / 16;
+  constexpr int NT = WAVES * kWave;
+  constexpr int V = 16 / sizeof(S);
+  constexpr bool LDSW = H <= 64;                       // weights fit in LDS
+  constexpr int WROW = 3 * H + V;                       // LDS row pitch of a staged weight
+  __shared__ __attribute__((aligned(16))) S wl[LDSW ? 2 : 1][LDSW ? H * WROW : 1];
+
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int q = lane % 16, g = lane / 16;
   const int n0 = xcd_swizzle(blockIdx.x, gridDim.x) * (16 * WAVES) + 16 * wave;
-  if (n0 >= n_pad) return;   // no barriers in this kernel
+  const bool valid = n0 < n_pad;
   const int node = n0 + q;
-  const S* sv = saved + (size_t)node * 3 * H;
-  S* gh = ghat + (size_t)node * 3 * H;
-  float* dhr = dh + (size_t)node * H;
 
-  // Phase 1: elementwise part.
-#pragma unroll
-  for (int m = 0; m < MTL; ++m) {
-    const int f = 16 * m + 4 * g;
-    f32x4 gg = *reinterpret_cast<const f32x4*>(gin + (size_t)node * H + f);
-    f32x4 z4 = load4f(sv + H + f), n4 = load4f(sv + 2 * H + f);
-    f32x4 h4 = load4f(h + (size_t)node * H + f);
-    float G[4] = {gg.x, gg.y, gg.z, gg.w}, Z[4] = {z4.x, z4.y, z4.z, z4.w}, N[4] = {n4.x, n4.y, n4.z, n4.w};
-    float Hh[4] = {h4.x, h4.y, h4.z, h4.w};
-    float zh[4], nh[4], d0[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float dn = G[j] * (1.f - Z[j]);
-      const float dz = G[j] * (Hh[j] - N[j]);
-      d0[j] = G[j] * Z[j];
-      nh[j] = dn * (1.f - N[j] * N[j]);
-      zh[j] = dz * Z[j] * (1.f - Z[j]);
+  if constexpr (LDSW) {
+    for (int lin = tid; lin < H * (3 * H / V); lin += NT) {
+      const int r = lin / (3 * H / V), c = (lin % (3 * H / V)) * V;
+      *reinterpret_cast<u32x4*>(&wl[0][r * WROW + c]) = *reinterpret_cast<const u32x4*>(Wi + (size_t)r * 3 * H + c);
+      *reinterpret_cast<u32x4*>(&wl[1][r * WROW + c]) = *reinterpret_cast<const u32x4*>(U + (size_t)r * 3 * H + c);
     }
-    store4(gh + H + f, zh[0], zh[1], zh[2], zh[3]);
-    store4(gh + 2 * H + f, nh[0], nh[1], nh[2], nh[3]);
-    store4(dhr + f, d0[0], d0[1], d0[2], d0[3]);
   }
-  // Phase 2: q = n^ U_n^T (D[f_in][node]); r^ and the q r term of dh.
-  frag_t<S> nf[KS];
-#pragma unroll
-  for (int kk = 0; kk < KS; ++kk) nf[kk] = rowfrag<S>(gh + 2 * H, kk, g);
-#pragma unroll
-  for (int m = 0; m < MTL; ++m) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    const S* urow = U + (size_t)(16 * m + q) * 3 * H + 2 * H;
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) mma(acc, rowfrag<S>(urow, kk, g), nf[kk]);
-    const int f = 16 * m + 4 * g;
-    f32x4 r4 = load4f(sv + f), h4 = load4f(h + (size_t)node * H + f);
-    f32x4 d4 = *reinterpret_cast<const f32x4*>(dhr + f);
-    float R[4] = {r4.x, r4.y, r4.z, r4.w}, Hh[4] = {h4.x, h4.y, h4.z, h4.w}, D[4] = {d4.x, d4.y, d4.z, d4.w};
-    float rh[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      rh[j] = acc[j] * Hh[j] * R[j] * (1.f - R[j]);
-      D[j] += acc[j] * R[j];
+  // Weight row fragment (row `row` of Wi or U, gate `gate`, step kk).
+  auto wfrag = [&](int which, int row, int gate, int kk) __attribute__((always_inline)) {
+    if constexpr (LDSW) {
+      const S* p = &wl[which][row * WROW + gate * H];
+      return rowfrag<S>(p, kk, g);
+    } else {
+      const S* p = (which ? U : Wi) + (size_t)row * 3 * H + gate * H;
+      return rowfrag<S>(p, kk, g);
     }
-    store4(gh + f, rh[0], rh[1], rh[2], rh[3]);
-    store4(dhr + f, D[0], D[1], D[2], D[3]);
+  };
+
+  // Phase 1: elementwise part, kept in registers.
+  frag_t<S> gf[3][KS];          // r^, z^, n^ as operand fragments
+  f32x4 dacc[MTL];              // dh accumulator (D layout: features 16m + 4g + j)
+  float zv[8], nv[8];
+  if (valid) {
+    const S* sv = saved + (size_t)node * 3 * H;
+#pragma unroll
+    for (int m = 0; m < MTL; ++m) {
+      const int f = 16 * m + 4 * g;
+      const f32x4 gg = *reinterpret_cast<const f32x4*>(gin + (size_t)node * H + f);
+      const f32x4 z4 = load4f(sv + H + f), n4 = load4f(sv + 2 * H + f);
+      const f32x4 h4 = load4f(h + (size_t)node * H + f);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float dn = gg[j] * (1.f - z4[j]);
+        const float dz = gg[j] * (h4[j] - n4[j]);
+        dacc[m][j] = gg[j] * z4[j];
+        nv[4 * (m % 2) + j] = dn * (1.f - n4[j] * n4[j]);
+        zv[4 * (m % 2) + j] = dz * z4[j] * (1.f - z4[j]);
+      }
+      if (m % 2 == 1) {
+        gf[2][m / 2] = pack8<S>(nv);
+        gf[1][m / 2] = pack8<S>(zv);
+      }
+      S* gh = ghat + (size_t)node * 3 * H;
+      store4(gh + H + f, zv[4 * (m % 2)], zv[4 * (m % 2) + 1], zv[4 * (m % 2) + 2], zv[4 * (m % 2) + 3]);
+      store4(gh + 2 * H + f, nv[4 * (m % 2)], nv[4 * (m % 2) + 1], nv[4 * (m % 2) + 2], nv[4 * (m % 2) + 3]);
+    }
+  }
+  if constexpr (LDSW) __syncthreads();
+  if (!valid) return;   // no barrier follows
+  // Phase 2: q = n^ U_n^T (D[f_in][node]); r^ and the q r term of dh.
+  {
+    const S* sv = saved + (size_t)node * 3 * H;
+    float rv[8];
+#pragma unroll
+    for (int m = 0; m < MTL; ++m) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) mma(acc, wfrag(1, 16 * m + q, 2, kk), gf[2][kk]);
+      const int f = 16 * m + 4 * g;
+      const f32x4 r4 = load4f(sv + f), h4 = load4f(h + (size_t)node * H + f);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        rv[4 * (m % 2) + j] = acc[j] * h4[j] * r4[j] * (1.f - r4[j]);
+        dacc[m][j] += acc[j] * r4[j];
+      }
+      store4(ghat + (size_t)node * 3 * H + f, rv[4 * (m % 2)], rv[4 * (m % 2) + 1], rv[4 * (m % 2) + 2],
+             rv[4 * (m % 2) + 3]);
+      if (m % 2 == 1) gf[0][m / 2] = pack8<S>(rv);
+    }
   }
   // Phase 3: da = G^ Wi^T, D[node][f_in]: four consecutive nodes per lane.
-  frag_t<S> gf[3][KS];
-#pragma unroll
-  for (int s = 0; s < 3; ++s)
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) gf[s][kk] = rowfrag<S>(gh + s * H, kk, g);
 #pragma unroll
   for (int n = 0; n < MTL; ++n) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    const S* wrow = Wi + (size_t)(16 * n + q) * 3 * H;
 #pragma unroll
-    for (int s = 0; s < 3; ++s)
+    for (int gate = 0; gate < 3; ++gate)
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) mma(acc, gf[s][kk], rowfrag<S>(wrow + s * H, kk, g));
+      for (int kk = 0; kk < KS; ++kk) mma(acc, gf[gate][kk], wfrag(0, 16 * n + q, gate, kk));
     store4(daT + (size_t)(16 * n + q) * n_pad + n0 + 4 * g, acc[0], acc[1], acc[2], acc[3]);
   }
-  // Phase 4: dh += r^ U_r^T + z^ U_z^T, D[f_in][node].
+  // Phase 4: dh += r^ U_r^T + z^ U_z^T, D[f_in][node]; one store of dh.
 #pragma unroll
   for (int m = 0; m < MTL; ++m) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    const S* urow = U + (size_t)(16 * m + q) * 3 * H;
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
+    for (int gate = 0; gate < 2; ++gate)
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) mma(acc, rowfrag<S>(urow + s * H, kk, g), gf[s][kk]);
-    const int f = 16 * m + 4 * g;
-    f32x4 d4 = *reinterpret_cast<const f32x4*>(dhr + f);
-    store4(dhr + f, d4.x + acc[0], d4.y + acc[1], d4.z + acc[2], d4.w + acc[3]);
+      for (int kk = 0; kk < KS; ++kk) mma(dacc[m], wfrag(1, 16 * m + q, gate, kk), gf[gate][kk]);
+    store4(dh + (size_t)node * H + 16 * m + 4 * g, dacc[m][0], dacc[m][1], dacc[m][2], dacc[m][3]);
   }
 }
 
@@ -306,33 +328,70 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kern
     acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
     bsum[n] = 0.f;
   }
-  for (int c0 = nlo; c0 < nhi; c0 += KN) {
-    __syncthreads();
-    for (int lin = tid; lin < KN * TI / 4; lin += NT) {
+  // Software pipeline: the next chunk's operands are loaded into registers
+  // (a, h, r*h and G^ as four-element groups) while the current chunk is
+  // multiplied.
+  constexpr int TU = KN * TI / 4;
+  constexpr int UN = (TU + NT - 1) / NT;
+  f32x4 ar[UN];
+  u32x2 gr[UN];     // four G^ elements (8 bytes for bf16; fp32 uses two of these per group below)
+  f32x4 gf32[sizeof(S) == 4 ? UN : 1];
+  auto load_chunk = [&](int c0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+      const int lin = u * NT + tid;
       const int r = lin / (TI / 4), c = (lin % (TI / 4)) * 4;
       const int node = c0 + r;
-      if (node >= nhi) continue;
-      const int fi = ti * TI + c;
-      f32x4 x;
-      if (which == 0) {
-        x = *reinterpret_cast<const f32x4*>(a + (size_t)node * H + fi);
-      } else {
-        x = load4f(h + (size_t)node * H + fi);
-        if (rh_src) {
-          f32x4 r4 = load4f(saved + (size_t)node * 3 * H + fi);
-          x = f32x4{x.x * r4.x, x.y * r4.y, x.z * r4.z, x.w * r4.w};
+      if ((TU % NT == 0 || lin < TU) && node < nhi) {
+        const int fi = ti * TI + c;
+        if (which == 0) {
+          ar[u] = *reinterpret_cast<const f32x4*>(a + (size_t)node * H + fi);
+        } else {
+          f32x4 x = load4f(h + (size_t)node * H + fi);
+          if (rh_src) {
+            const f32x4 r4 = load4f(saved + (size_t)node * 3 * H + fi);
+            x = f32x4{x.x * r4.x, x.y * r4.y, x.z * r4.z, x.w * r4.w};
+          }
+          ar[u] = x;
+        }
+        const S* gsrc = ghat + (size_t)node * 3 * H + col0 + c;
+        if constexpr (sizeof(S) == 2) {
+          gr[u] = *reinterpret_cast<const u32x2*>(gsrc);
+        } else {
+          gf32[u] = *reinterpret_cast<const f32x4*>(gsrc);
         }
       }
-      S xa[4] = {from_f<S>(x.x), from_f<S>(x.y), from_f<S>(x.z), from_f<S>(x.w)};
-      S* pa = &ta[r * PX + c];
+    }
+  };
+  if (nlo < nhi) load_chunk(nlo);
+  for (int c0 = nlo; c0 < nhi; c0 += KN) {
+    __syncthreads();
 #pragma unroll
-      for (int j = 0; j < 4; ++j) pa[j] = xa[j];
-      const S* gsrc = ghat + (size_t)node * 3 * H + col0 + c;
-      S* pb = &tb[r * PX + c];
+    for (int u = 0; u < UN; ++u) {
+      const int lin = u * NT + tid;
+      const int r = lin / (TI / 4), c = (lin % (TI / 4)) * 4;
+      if ((TU % NT == 0 || lin < TU) && c0 + r < nhi) {
+        S* pa = &ta[r * PX + c];
+        S* pb = &tb[r * PX + c];
+        if constexpr (sizeof(S) == 2) {
+          // rows are 4-byte aligned: write as two 32-bit words
+          const uint32_t lo = static_cast<uint32_t>(f2bf(ar[u].x)) | (static_cast<uint32_t>(f2bf(ar[u].y)) << 16);
+          const uint32_t hi = static_cast<uint32_t>(f2bf(ar[u].z)) | (static_cast<uint32_t>(f2bf(ar[u].w)) << 16);
+          reinterpret_cast<uint32_t*>(pa)[0] = lo;
+          reinterpret_cast<uint32_t*>(pa)[1] = hi;
+          reinterpret_cast<uint32_t*>(pb)[0] = gr[u].x;
+          reinterpret_cast<uint32_t*>(pb)[1] = gr[u].y;
+        } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) pb[j] = gsrc[j];
+          for (int j = 0; j < 4; ++j) {
+            pa[j] = from_f<S>(ar[u][j]);
+            pb[j] = from_f<S>(gf32[sizeof(S) == 4 ? u : 0][j]);
+          }
+        }
+      }
     }
     __syncthreads();
+    if (c0 + KN < nhi) load_chunk(c0 + KN);
 #pragma unroll
     for (int kk = 0; kk < KN / 32; ++kk) {
       if (c0 + 32 * kk >= nhi) break;

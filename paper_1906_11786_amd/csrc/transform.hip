@@ -114,17 +114,33 @@ __global__ __launch_bounds__(WAVES * kWave) void transform_bwd_dx_kernel(const S
   f32x4 acc[MTL];
 #pragma unroll
   for (int m = 0; m < MTL; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+  constexpr int TU = H * NW / V;                 // 16-byte units of one dM tile
+  constexpr int UN = (TU + NT - 1) / NT;
+  u32x4 reg[UN];
+  auto load_tile = [&](int e) __attribute__((always_inline)) {
+    const S* src = dM + (size_t)e * H * n_pad + n0;
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+      const int lin = u * NT + tid;
+      const int h = lin / (NW / V), c = (lin % (NW / V)) * V;
+      if ((TU % NT == 0 || lin < TU) && n0 + c < n_pad)
+        reg[u] = *reinterpret_cast<const u32x4*>(src + (size_t)h * n_pad + c);
+    }
+  };
+  load_tile(0);
   for (int e = 0; e < E; ++e) {
     __syncthreads();
-    const S* src = dM + (size_t)e * H * n_pad + n0;
-    for (int lin = tid; lin < H * NW / V; lin += NT) {
-      int h = lin / (NW / V), c = (lin % (NW / V)) * V;
-      if (n0 + c >= n_pad) continue;
-      u32x4 v = *reinterpret_cast<const u32x4*>(src + (size_t)h * n_pad + c);
-      uint32_t* p = reinterpret_cast<uint32_t*>(&tile[h * PM + c]);
-      p[0] = v.x; p[1] = v.y; p[2] = v.z; p[3] = v.w;
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+      const int lin = u * NT + tid;
+      const int h = lin / (NW / V), c = (lin % (NW / V)) * V;
+      if ((TU % NT == 0 || lin < TU) && n0 + c < n_pad) {
+        uint32_t* p = reinterpret_cast<uint32_t*>(&tile[h * PM + c]);
+        p[0] = reg[u].x; p[1] = reg[u].y; p[2] = reg[u].z; p[3] = reg[u].w;
+      }
     }
     __syncthreads();
+    if (e + 1 < E) load_tile(e + 1);    // in flight during this type's products
     if (!valid) continue;
     const S* we = W + (size_t)e * H * H;
 #pragma unroll
@@ -187,28 +203,57 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
     bsum[n] = 0.f;
   }
   const bool do_bias = (ti == 0 && wave == 0 && Pb != nullptr);
+  // Software pipeline: the next chunk's X tile and dM fragments are loaded
+  // into registers while the current chunk is multiplied.
+  constexpr int TU = KN * TI / V;
+  constexpr int UN = (TU + NT - 1) / NT;
+  u32x4 xr[UN];
+  frag_t<S> br[KN / 32][NTL];
+  auto load_chunk = [&](int c0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+      const int lin = u * NT + tid;
+      const int r = lin / (TI / V), c = (lin % (TI / V)) * V;
+      if ((TU % NT == 0 || lin < TU) && c0 + r < nhi)
+        xr[u] = *reinterpret_cast<const u32x4*>(X + (size_t)(c0 + r) * H + ti * TI + c);
+    }
+#pragma unroll
+    for (int kk = 0; kk < KN / 32; ++kk) {
+      if (c0 + 32 * kk >= nhi) break;
+#pragma unroll
+      for (int n = 0; n < NTL; ++n)
+        br[kk][n] = load8(dM + ((size_t)e * H + to * TI + 16 * n + q) * n_pad + c0 + 32 * kk + 8 * g);
+    }
+  };
+  if (nlo < nhi) load_chunk(nlo);
   for (int c0 = nlo; c0 < nhi; c0 += KN) {
     __syncthreads();
-    for (int lin = tid; lin < KN * TI / V; lin += NT) {
-      int r = lin / (TI / V), c = (lin % (TI / V)) * V;
-      if (c0 + r >= nhi) continue;
-      u32x4 v = *reinterpret_cast<const u32x4*>(X + (size_t)(c0 + r) * H + ti * TI + c);
-      uint32_t* p = reinterpret_cast<uint32_t*>(&tile[r * PX + c]);
-      p[0] = v.x; p[1] = v.y; p[2] = v.z; p[3] = v.w;
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+      const int lin = u * NT + tid;
+      const int r = lin / (TI / V), c = (lin % (TI / V)) * V;
+      if ((TU % NT == 0 || lin < TU) && c0 + r < nhi) {
+        uint32_t* p = reinterpret_cast<uint32_t*>(&tile[r * PX + c]);
+        p[0] = xr[u].x; p[1] = xr[u].y; p[2] = xr[u].z; p[3] = xr[u].w;
+      }
     }
+    frag_t<S> bcur[KN / 32][NTL];
+#pragma unroll
+    for (int kk = 0; kk < KN / 32; ++kk)
+#pragma unroll
+      for (int n = 0; n < NTL; ++n) bcur[kk][n] = br[kk][n];
     __syncthreads();
+    if (c0 + KN < nhi) load_chunk(c0 + KN);
 #pragma unroll
     for (int kk = 0; kk < KN / 32; ++kk) {
       if (c0 + 32 * kk >= nhi) break;    // n_pad is a multiple of 32
       frag_t<S> afr = load8_strided(&tile[(32 * kk + 8 * g) * PX + 16 * wave + q], PX);
 #pragma unroll
       for (int n = 0; n < NTL; ++n) {
-        const int o = to * TI + 16 * n + q;
-        frag_t<S> bf = load8(dM + ((size_t)e * H + o) * n_pad + c0 + 32 * kk + 8 * g);
-        mma(acc[n], afr, bf);
+        mma(acc[n], afr, bcur[kk][n]);
         if (do_bias) {
 #pragma unroll
-          for (int x = 0; x < 8; ++x) bsum[n] += static_cast<float>(bf[x]);
+          for (int x = 0; x < 8; ++x) bsum[n] += static_cast<float>(bcur[kk][n][x]);
         }
       }
     }
