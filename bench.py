@@ -6,14 +6,27 @@ A step is one pass of the whole hot path over the workload: T forward steps
 with the band, parameters and activations resident in HBM.  The metric is
 node-steps/s = real nodes * T / seconds per step.
 
-Prints one JSON line.  `--gpus N` with N > 1 is refused: this build runs on
+Prints one JSON line.  `--gpus N` with N > 1 is refused: the path runs on
 one GPU.
+
+The roofline entry times the dominant banded kernel live (HIP events on its
+stream).  Its `traffic` field is the HBM traffic per launch measured with the
+FETCH_SIZE and WRITE_SIZE counters of two rocprofv3 --pmc runs of this same
+command, each scaled by what the counter reads for a plain copy of known size
+(the calibration copy every run makes after the timed region);
+`--traffic-from FETCH.csv WRITE.csv` turns those two counter files into the
+summary kept under profiles/.  The figure is used only while the kernel's
+sources hash to the value recorded with it.
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -28,6 +41,21 @@ FP32_PEAK_TFLOPS = 157.3    # MI355X fp32 matrix cores
 
 WORKLOADS = {"program_graph": 1, "tiny": 0, "batch_100k": 2, "stress_1m": 4}
 
+# C-ABI entry point -> (device kernel name fragment, sources that define it)
+KERNELS = {
+    "banded_step_bits": ("step_fwd_kernel", ["banded_bits.hip", "device_common.h"]),
+    "banded_propagate_bits_bwd": ("bits_bwd_kernel", ["banded_bits.hip", "device_common.h"]),
+    "banded_propagate": ("banded_fwd_kernel", ["banded.hip", "device_common.h"]),
+    "banded_propagate_bwd": ("banded_bwd_kernel", ["banded.hip", "device_common.h"]),
+}
+# Other kernels of the step, listed in the traffic summary.
+OTHER_KERNELS = ["gru_fwd_kernel", "gru_bwd_kernel", "gru_wgrad_kernel", "transform_bwd_dx_kernel",
+                 "transform_wgrad_kernel", "transform_fwd_kernel", "reduce_partials_kernel"]
+CAL_ELEMS = 64 << 20            # calibration copy: 64 Mi fp32 read, 64 Mi fp32 written
+CAL_BYTES = CAL_ELEMS * 4
+CAL_NAME = "neg_kernel"         # torch's elementwise negation: one read and one write per element
+PROFILES = os.path.join(ROOT, "profiles")
+
 
 def parse():
     p = argparse.ArgumentParser()
@@ -40,7 +68,81 @@ def parse():
                    help="band storage: 1 bit per entry (aggregate-first fused forward) or dense in the compute dtype")
     p.add_argument("--kernel-reps", type=int, default=50, help="launches per kernel for the roofline timing")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                   help="summarise two rocprofv3 --pmc counter files (FETCH_SIZE, WRITE_SIZE) of this command "
+                        "and exit")
     return p.parse_args()
+
+
+def source_hash(names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_1906_11786_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(kernel, workload, band):
+    """Bytes per launch recorded under profiles/ for this kernel, workload and
+    band, if the kernel's sources are unchanged since; else None."""
+    want = source_hash(KERNELS[kernel][1])
+    for path in sorted(glob.glob(os.path.join(PROFILES, "*.md"))):
+        with open(path) as f:
+            for line in f:
+                if not line.startswith("traffic-record: "):
+                    continue
+                rec = json.loads(line[len("traffic-record: "):])
+                if (rec.get("kernel"), rec.get("workload"), rec.get("band")) == (kernel, workload, band):
+                    if rec.get("source_hash") == want:
+                        return rec["bytes_per_launch"], os.path.relpath(path, ROOT)
+    return None, None
+
+
+def _counter_rows(path, counter):
+    """Per-dispatch counter totals of a rocprofv3 counter_collection.csv:
+    {dispatch id: (kernel name, value)}."""
+    out = {}
+    with open(path, newline="") as f:
+        for row in csv.DictReader(f):
+            row = {k.lower(): v for k, v in row.items()}
+            if row.get("counter_name") != counter:
+                continue
+            d = row["dispatch_id"]
+            name, v = out.get(d, (row["kernel_name"], 0.0))
+            out[d] = (name, v + float(row["counter_value"]))
+    return out
+
+
+def traffic_summary(fetch_csv, write_csv, cmd_line):
+    """Markdown summary of the calibrated HBM traffic per launch, with one
+    machine-readable record per banded kernel."""
+    fetch, write = _counter_rows(fetch_csv, "FETCH_SIZE"), _counter_rows(write_csv, "WRITE_SIZE")
+
+    def per_kernel(rows, frag):
+        vals = [v for name, v in rows.values() if frag in name]
+        return (statistics.median(vals), len(vals)) if vals else (None, 0)
+
+    cf, _ = per_kernel(fetch, CAL_NAME)
+    cw, _ = per_kernel(write, CAL_NAME)
+    if not cf or not cw:
+        raise SystemExit("calibration copy not found in the counter files")
+    kf, kw = CAL_BYTES / cf, CAL_BYTES / cw
+    lines = ["| kernel | launches | FETCH_SIZE (median) | WRITE_SIZE (median) | calibrated bytes / launch |",
+             "|---|---:|---:|---:|---:|",
+             f"| calibration copy ({CAL_NAME}, {CAL_BYTES} B read + {CAL_BYTES} B written) | 1 | {cf:.0f} | "
+             f"{cw:.0f} | {CAL_BYTES * 2} |"]
+    recs = []
+    for frag in [v[0] for v in KERNELS.values()] + OTHER_KERNELS:
+        f, n = per_kernel(fetch, frag)
+        w, _ = per_kernel(write, frag)
+        if f is None or w is None:
+            continue
+        b = f * kf + w * kw
+        lines.append(f"| `{frag}` | {n} | {f:.0f} | {w:.0f} | {b:.0f} |")
+        for k, (fr, srcs) in KERNELS.items():
+            if fr == frag:
+                recs.append((k, b, srcs))
+    return lines, (kf, kw), recs
 
 
 def spec_for(name):
@@ -117,6 +219,15 @@ def cpu_baseline(spec, graphs, comp, params):
 
 def main():
     args = parse()
+    if args.traffic_from:
+        lines, (kf, kw), recs = traffic_summary(*args.traffic_from, " ".join(sys.argv))
+        print("\n".join(lines))
+        print(f"\nscale factors: FETCH_SIZE x {kf:.2f}, WRITE_SIZE x {kw:.2f} (bytes per counter unit)\n")
+        for k, b, srcs in recs:
+            rec = {"kernel": k, "workload": spec_for(args.workload).name, "band": args.band, "bytes_per_launch": int(round(b)),
+                   "source_hash": source_hash(srcs), "sources": srcs}
+            print("traffic-record: " + json.dumps(rec))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); multi-GPU runs are not part of this build",
               file=sys.stderr)
@@ -181,10 +292,18 @@ def main():
     else:
         roofline = {"bound": "mfma", "achieved": round(tfs, 2), "peak": mfma_peak, "unit": "TFLOP/s",
                     "frac": round(tfs / mfma_peak, 4)}
-    roofline.update({"traffic": None, "kernel": dom, "avg_launch_us": round(dur * 1e6, 2),
+    traffic, traffic_src = recorded_traffic(dom, spec.name, args.band)
+    roofline.update({"traffic": traffic, "traffic_source": traffic_src, "kernel": dom, "avg_launch_us": round(dur * 1e6, 2),
                      "algorithmic_bytes": int(nbytes), "algorithmic_flops": flops,
                      "hbm_frac": round(gbs / HBM_PEAK_GBS, 4), "mfma_frac": round(tfs / mfma_peak, 4),
                      "other_kernels_us": {k: round(v * 1e6, 2) for k, v in times.items() if k != dom}})
+
+    # Calibration copy for the traffic counters (outside every timed region).
+    cal_src = torch.ones(CAL_ELEMS, dtype=torch.float32, device="cuda")
+    cal_dst = torch.empty_like(cal_src)
+    torch.neg(cal_src, out=cal_dst)
+    torch.cuda.synchronize()
+    del cal_src, cal_dst
 
     cpu = None
     if not args.no_cpu_baseline:

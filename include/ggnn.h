@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define GGNN_ABI_VERSION 2
+#define GGNN_ABI_VERSION 3
 
 typedef enum {
   GGNN_OK = 0,
@@ -288,7 +288,8 @@ typedef struct ggnn_grads {
   float* dU;            /* [H][3H]    += */
   float* db;            /* [3H]       += */
   void* da;             /* [H][n_pad] dt scratch */
-  void* dM;             /* [E][H][n_pad] dt scratch */
+  void* dM;             /* [E][H][T*n_pad] dt scratch: step t's message gradient in columns
+                         * [t*n_pad, (t+1)*n_pad) of every (e, h) row */
   float* dh;            /* [n_pad][H] float scratch */
   void* workspace;      /* device scratch of ggnn_backward_workspace_bytes() */
   size_t workspace_bytes;
@@ -304,9 +305,13 @@ size_t ggnn_backward_workspace_bytes(const ggnn_model* model);
 ggnn_status ggnn_forward(const ggnn_model* model, const ggnn_activations* act, void* stream);
 
 /* Reverse pass for L with dL/dX_T given in grads->dX: for t = T-1..0,
- *   da, dh = gru_update_bwd(dX); dM = banded_propagate_bwd(da) (dense band)
- *   or banded_propagate_bits_bwd(da) (bit band);
- *   dX = dh + sum_e dM_e W_e^T;  weight gradients accumulate (+=).
+ *   da, dh, G^_t = gru_update_bwd node pass(dX); dM_t = banded_propagate_bwd(da)
+ *   (dense band) or banded_propagate_bits_bwd(da) (bit band);
+ *   dX = dh + sum_e dM_t,e W_e^T;
+ * then the weight gradients as single contractions over all T * n_pad rows:
+ *   dWi, dU, db += sums over t of the GRU products of (a[t], X[t], saved[t], G^_t),
+ *   dW_e += sum_t X[t]^T dM_t,e, dbias_e += row sums of dM_t,e (accumulate, +=).
+ * G^_t is kept in the workspace, dM_t in grads->dM.
  * Needs the activations of a preceding ggnn_forward. */
 ggnn_status ggnn_backward(const ggnn_model* model, const ggnn_activations* act,
                           const ggnn_grads* grads, void* stream);

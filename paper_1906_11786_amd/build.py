@@ -16,9 +16,12 @@ LIB = os.path.join(HERE, "libggnn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Device code: gfx950 only; packed fp32 instructions are disabled (hipcc
-# emits them from plain float code otherwise).
+# emits them from plain float code otherwise).  Matrix-core results stay in
+# the unified VGPR file (gfx950 needs no separate accumulator registers):
+# otherwise the compiler parks accumulators in AGPRs and spends a VALU move
+# per element on every round trip.
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
-             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-mllvm", "-amdgpu-mfma-vgpr-form"]
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall"]
 
 SOURCES = [

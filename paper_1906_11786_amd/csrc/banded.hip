@@ -168,7 +168,8 @@ __global__ __launch_bounds__(WAVES * kWave) void banded_fwd_kernel(const S* __re
 template <typename S, int H, int WAVES, int KC>
 __global__ __launch_bounds__(WAVES * kWave) void banded_bwd_kernel(const S* __restrict__ band,
                                                                     const S* __restrict__ da,
-                                                                    S* __restrict__ dM, int n_pad, int B, int E) {
+                                                                    S* __restrict__ dM, int n_pad, int B, int E,
+                                                                    long ldm) {
   constexpr int NT = WAVES * kWave;
   constexpr int V = 16 / sizeof(S);
   constexpr int NW = 32 * WAVES;             // sender columns per workgroup
@@ -271,12 +272,12 @@ __global__ __launch_bounds__(WAVES * kWave) void banded_bwd_kernel(const S* __re
     __syncthreads();
   }
   // D[c = cw + 16m + 4g + i][h = 16n + q]
-  S* out = dM + (size_t)e * H * n_pad + (size_t)j * B + c0 + cw + 4 * g;
+  S* out = dM + (size_t)e * H * ldm + (size_t)j * B + c0 + cw + 4 * g;
 #pragma unroll
   for (int m = 0; m < 2; ++m)
 #pragma unroll
     for (int n = 0; n < NTL; ++n)
-      store4(out + (size_t)(16 * n + q) * n_pad + 16 * m, acc[m][n][0], acc[m][n][1], acc[m][n][2], acc[m][n][3]);
+      store4(out + (size_t)(16 * n + q) * ldm + 16 * m, acc[m][n][0], acc[m][n][1], acc[m][n][2], acc[m][n][3]);
 }
 
 // ---------------------------------------------------------------------------
@@ -319,7 +320,8 @@ static hipError_t fwd_dispatch(const void* band, const float* M, float* a, int n
 }
 
 template <typename S, int H>
-static hipError_t bwd_dispatch(const void* band, const void* da, void* dM, int n_pad, int B, int E, hipStream_t st) {
+static hipError_t bwd_dispatch(const void* band, const void* da, void* dM, long ldm, int n_pad, int B, int E,
+                               hipStream_t st) {
   const int nb = n_pad / B;
   const int waves = pick_waves(B, nb, E, GGNN_BWD_MIN_BLOCKS);
   const int blocks = E * nb * (B / (32 * waves));
@@ -328,9 +330,9 @@ static hipError_t bwd_dispatch(const void* band, const void* da, void* dM, int n
   const S* dp = static_cast<const S*>(da);
   S* op = static_cast<S*>(dM);
   switch (waves) {
-    case 4: hipLaunchKernelGGL((banded_bwd_kernel<S, H, 4, KC>), dim3(blocks), dim3(256), 0, st, bp, dp, op, n_pad, B, E); break;
-    case 2: hipLaunchKernelGGL((banded_bwd_kernel<S, H, 2, KC>), dim3(blocks), dim3(128), 0, st, bp, dp, op, n_pad, B, E); break;
-    default: hipLaunchKernelGGL((banded_bwd_kernel<S, H, 1, KC>), dim3(blocks), dim3(64), 0, st, bp, dp, op, n_pad, B, E); break;
+    case 4: hipLaunchKernelGGL((banded_bwd_kernel<S, H, 4, KC>), dim3(blocks), dim3(256), 0, st, bp, dp, op, n_pad, B, E, ldm); break;
+    case 2: hipLaunchKernelGGL((banded_bwd_kernel<S, H, 2, KC>), dim3(blocks), dim3(128), 0, st, bp, dp, op, n_pad, B, E, ldm); break;
+    default: hipLaunchKernelGGL((banded_bwd_kernel<S, H, 1, KC>), dim3(blocks), dim3(64), 0, st, bp, dp, op, n_pad, B, E, ldm); break;
   }
   return hipGetLastError();
 }
@@ -346,12 +348,13 @@ static hipError_t fwd_h(int H, const void* band, const float* M, float* a, int n
   return hipErrorInvalidValue;
 }
 template <typename S>
-static hipError_t bwd_h(int H, const void* band, const void* da, void* dM, int n_pad, int B, int E, hipStream_t st) {
+static hipError_t bwd_h(int H, const void* band, const void* da, void* dM, long ldm, int n_pad, int B, int E,
+                        hipStream_t st) {
   switch (H) {
-    case 32: return bwd_dispatch<S, 32>(band, da, dM, n_pad, B, E, st);
-    case 64: return bwd_dispatch<S, 64>(band, da, dM, n_pad, B, E, st);
-    case 128: return bwd_dispatch<S, 128>(band, da, dM, n_pad, B, E, st);
-    case 256: return bwd_dispatch<S, 256>(band, da, dM, n_pad, B, E, st);
+    case 32: return bwd_dispatch<S, 32>(band, da, dM, ldm, n_pad, B, E, st);
+    case 64: return bwd_dispatch<S, 64>(band, da, dM, ldm, n_pad, B, E, st);
+    case 128: return bwd_dispatch<S, 128>(band, da, dM, ldm, n_pad, B, E, st);
+    case 256: return bwd_dispatch<S, 256>(band, da, dM, ldm, n_pad, B, E, st);
   }
   return hipErrorInvalidValue;
 }
@@ -365,9 +368,9 @@ hipError_t launch_banded_fwd(int dt, int n_pad, int B, int H, int E, const void*
 }
 
 hipError_t launch_banded_bwd(int dt, int n_pad, int B, int H, int E, const void* band, const void* da, void* dM,
-                             hipStream_t st) {
-  return dt == GGNN_BF16 ? dev::bwd_h<dev::bf16s>(H, band, da, dM, n_pad, B, E, st)
-                         : dev::bwd_h<float>(H, band, da, dM, n_pad, B, E, st);
+                             long ldm, hipStream_t st) {
+  return dt == GGNN_BF16 ? dev::bwd_h<dev::bf16s>(H, band, da, dM, ldm, n_pad, B, E, st)
+                         : dev::bwd_h<float>(H, band, da, dM, ldm, n_pad, B, E, st);
 }
 
 }  // namespace ggnn

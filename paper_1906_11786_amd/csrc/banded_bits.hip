@@ -26,12 +26,13 @@ namespace dev {
 // 8 bits -> 8 elements equal to 0 or 1 (bit i -> element i).
 template <typename S> __device__ __forceinline__ frag_t<S> bits_frag(uint32_t byte);
 template <> __device__ __forceinline__ bf16x8 bits_frag<bf16s>(uint32_t byte) {
+  // byte * 0x8001 holds bit i at position i and again at i + 15, so after a
+  // shift by 2k, bit 0 is bit 2k and bit 16 is bit 2k+1; times 0x3F80 (bf16
+  // 1.0) that is the word of elements 2k and 2k+1.
+  const uint32_t x = byte * 0x8001u;
   u32x4 w;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const uint32_t t = (byte >> (2 * k)) & 3u;           // two bits -> two 16-bit lanes
-    w[k] = ((t * 0x8001u) & 0x10001u) * 0x3F80u;         // 0x3F80 is bf16 1.0
-  }
+  for (int k = 0; k < 4; ++k) w[k] = ((x >> (2 * k)) & 0x10001u) * 0x3F80u;
   return __builtin_bit_cast(bf16x8, w);
 }
 template <> __device__ __forceinline__ f32x8 bits_frag<float>(uint32_t byte) {
@@ -326,7 +327,8 @@ __global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* 
 }
 
 // ---------------------------------------------------------------------------
-// Reverse: dM[e][h][j*B + c] = sum_s sum_r bits_t[e][j][s][c][r] da[h][(j-1+s)*B + r].
+// Reverse: dM[e][h][j*B + c] = sum_s sum_r bits_t[e][j][s][c][r] da[h][(j-1+s)*B + r],
+// dM rows of length ldm >= n_pad.
 // Workgroup: RPW*WAVES columns c of block j; wave w: RPW of them.  D[c][h]:
 // A operand = transposed bit rows c expanded in registers, B operand = staged
 // da rows (feature-major, plain copies).  Lanes hold four consecutive nodes
@@ -335,7 +337,7 @@ __global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* 
 template <typename S, int H, int B, int WAVES>
 __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* __restrict__ bits_t,
                                                                   const S* __restrict__ da, S* __restrict__ dM,
-                                                                  int n_pad, int E, int groups) {
+                                                                  int n_pad, int E, int groups, long ldm) {
   using C = BitsCfg<S, H, B>;
   constexpr int NT = WAVES * kWave;
   constexpr int KC = C::KC, VP = C::VP, RB = C::RB, NTW = C::NTW;
@@ -421,12 +423,12 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
         }
       }
     }
-    S* out = dM + (size_t)e * H * n_pad + (size_t)j * B + cw + 4 * g;
+    S* out = dM + (size_t)e * H * ldm + (size_t)j * B + cw + 4 * g;
 #pragma unroll
     for (int m = 0; m < NTW; ++m)
 #pragma unroll
       for (int n = 0; n < NTL; ++n)
-        store4(out + (size_t)(16 * n + q) * n_pad + 16 * m, acc[m][n][0], acc[m][n][1], acc[m][n][2], acc[m][n][3]);
+        store4(out + (size_t)(16 * n + q) * ldm + 16 * m, acc[m][n][0], acc[m][n][1], acc[m][n][2], acc[m][n][3]);
   }
 }
 
@@ -447,7 +449,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
 namespace {
 template <typename S, int H, int B>
 hipError_t bits_launch(bool fwd, const void* bits, const void* V, const void* W, const float* bias, void* out,
-                       int n_pad, int E, hipStream_t st) {
+                       long ldm, int n_pad, int E, hipStream_t st) {
   using C = dev::BitsCfg<S, H, B>;
   const int nb = n_pad / B;
   int waves = B / C::RPW < 4 ? B / C::RPW : 4;
@@ -472,7 +474,7 @@ hipError_t bits_launch(bool fwd, const void* bits, const void* V, const void* W,
                            static_cast<const S*>(W), bias, static_cast<float*>(out), n_pad, E);              \
       else                                                                                                   \
         hipLaunchKernelGGL((dev::bits_bwd_kernel<S, H, B, WV>), dim3(blocks), dim3(WV * 64), 0, st, bp, vp,  \
-                           static_cast<S*>(out), n_pad, E, groups);                                          \
+                           static_cast<S*>(out), n_pad, E, groups, ldm);                                     \
     }                                                                                                        \
     break;
   switch (waves) {
@@ -486,25 +488,25 @@ hipError_t bits_launch(bool fwd, const void* bits, const void* V, const void* W,
 
 template <typename S, int H>
 hipError_t bits_h(int B, bool fwd, const void* bits, const void* V, const void* W, const float* bias, void* out,
-                  int n_pad, int E, hipStream_t st) {
+                  long ldm, int n_pad, int E, hipStream_t st) {
   switch (B) {
-    case 32: return bits_launch<S, H, 32>(fwd, bits, V, W, bias, out, n_pad, E, st);
-    case 64: return bits_launch<S, H, 64>(fwd, bits, V, W, bias, out, n_pad, E, st);
-    case 128: return bits_launch<S, H, 128>(fwd, bits, V, W, bias, out, n_pad, E, st);
-    case 256: return bits_launch<S, H, 256>(fwd, bits, V, W, bias, out, n_pad, E, st);
-    case 512: return bits_launch<S, H, 512>(fwd, bits, V, W, bias, out, n_pad, E, st);
+    case 32: return bits_launch<S, H, 32>(fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
+    case 64: return bits_launch<S, H, 64>(fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
+    case 128: return bits_launch<S, H, 128>(fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
+    case 256: return bits_launch<S, H, 256>(fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
+    case 512: return bits_launch<S, H, 512>(fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
   }
   return hipErrorInvalidValue;
 }
 
 template <typename S>
 hipError_t bits_t(int H, int B, bool fwd, const void* bits, const void* V, const void* W, const float* bias,
-                  void* out, int n_pad, int E, hipStream_t st) {
+                  void* out, long ldm, int n_pad, int E, hipStream_t st) {
   switch (H) {
-    case 32: return bits_h<S, 32>(B, fwd, bits, V, W, bias, out, n_pad, E, st);
-    case 64: return bits_h<S, 64>(B, fwd, bits, V, W, bias, out, n_pad, E, st);
-    case 128: return bits_h<S, 128>(B, fwd, bits, V, W, bias, out, n_pad, E, st);
-    case 256: return bits_h<S, 256>(B, fwd, bits, V, W, bias, out, n_pad, E, st);
+    case 32: return bits_h<S, 32>(B, fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
+    case 64: return bits_h<S, 64>(B, fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
+    case 128: return bits_h<S, 128>(B, fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
+    case 256: return bits_h<S, 256>(B, fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
   }
   return hipErrorInvalidValue;
 }
@@ -512,14 +514,14 @@ hipError_t bits_t(int H, int B, bool fwd, const void* bits, const void* V, const
 
 hipError_t launch_step_fwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits, const void* X,
                                 const void* W, const float* bias, float* a, hipStream_t st) {
-  return dt == GGNN_BF16 ? bits_t<dev::bf16s>(H, B, true, bits, X, W, bias, a, n_pad, E, st)
-                         : bits_t<float>(H, B, true, bits, X, W, bias, a, n_pad, E, st);
+  return dt == GGNN_BF16 ? bits_t<dev::bf16s>(H, B, true, bits, X, W, bias, a, 0, n_pad, E, st)
+                         : bits_t<float>(H, B, true, bits, X, W, bias, a, 0, n_pad, E, st);
 }
 
 hipError_t launch_banded_bwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits_t_, const void* da,
-                                  void* dM, hipStream_t st) {
-  return dt == GGNN_BF16 ? bits_t<dev::bf16s>(H, B, false, bits_t_, da, nullptr, nullptr, dM, n_pad, E, st)
-                         : bits_t<float>(H, B, false, bits_t_, da, nullptr, nullptr, dM, n_pad, E, st);
+                                  void* dM, long ldm, hipStream_t st) {
+  return dt == GGNN_BF16 ? bits_t<dev::bf16s>(H, B, false, bits_t_, da, nullptr, nullptr, dM, ldm, n_pad, E, st)
+                         : bits_t<float>(H, B, false, bits_t_, da, nullptr, nullptr, dM, ldm, n_pad, E, st);
 }
 
 }  // namespace ggnn

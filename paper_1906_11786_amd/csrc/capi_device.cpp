@@ -48,6 +48,26 @@ inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
 }  // namespace
 
+// Reverse-pass workspace: the gate gradients G^ of every step ([T][n_pad][3H],
+// kept for the GRU weight gradients), then the GRU and message-transform
+// weight-gradient partials over K = T * n_pad rows, each at a 256-byte
+// aligned offset.
+namespace {
+struct BwdLayout {
+  size_t ghat, gru_part, tr_part, total;
+};
+BwdLayout bwd_layout(const ggnn_model* m) {
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  const long K = (long)m->T * m->n_pad;
+  BwdLayout l;
+  l.ghat = 0;
+  l.gru_part = up(ghat_bytes(m->dtype, K, m->H));
+  l.tr_part = l.gru_part + up(gru_wgrad_workspace(K, m->H));
+  l.total = l.tr_part + transform_wgrad_workspace(K, m->H, m->E);
+  return l;
+}
+}  // namespace
+
 extern "C" {
 
 ggnn_status ggnn_msg_transform(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E, const void* X, const void* W,
@@ -131,7 +151,7 @@ ggnn_status ggnn_banded_propagate_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, i
   CHECK_PTR(band, "band");
   CHECK_PTR(da, "da");
   CHECK_PTR(dM, "dM");
-  return device_status(launch_banded_bwd(dt, n_pad, B, H, E, band, da, dM, as_stream(stream)),
+  return device_status(launch_banded_bwd(dt, n_pad, B, H, E, band, da, dM, n_pad, as_stream(stream)),
                        "banded_propagate_bwd");
 }
 
@@ -157,13 +177,13 @@ ggnn_status ggnn_banded_propagate_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t
   CHECK_PTR(bits_t, "bits_t");
   CHECK_PTR(da, "da");
   CHECK_PTR(dM, "dM");
-  return device_status(launch_banded_bwd_bits(dt, n_pad, B, H, E, bits_t, da, dM, as_stream(stream)),
+  return device_status(launch_banded_bwd_bits(dt, n_pad, B, H, E, bits_t, da, dM, n_pad, as_stream(stream)),
                        "banded_propagate_bits_bwd");
 }
 
 size_t ggnn_msg_transform_bwd_workspace_bytes(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E) {
   if (!supported_dtype(dt) || n_pad <= 0 || n_pad % 32 != 0 || !supported_H(H) || E < 1 || E > 64) return 0;
-  return transform_bwd_workspace(dt, n_pad, H, E);
+  return transform_wgrad_workspace(n_pad, H, E);
 }
 
 ggnn_status ggnn_msg_transform_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E, const void* X, const void* W,
@@ -180,13 +200,14 @@ ggnn_status ggnn_msg_transform_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int3
   CHECK_PTR(dX_out, "dX_out");
   CHECK_PTR(dW, "dW");
   CHECK_OPT_PTR(dbias, "dbias");
-  const size_t need = transform_bwd_workspace(dt, n_pad, H, E);
+  const size_t need = transform_wgrad_workspace(n_pad, H, E);
   if (workspace == nullptr || workspace_bytes < need || !aligned16(workspace))
     return fail(GGNN_ERR_WORKSPACE, "msg_transform_bwd needs a 16-byte aligned workspace of %zu bytes (got %zu)",
                 need, workspace ? workspace_bytes : (size_t)0);
-  return device_status(launch_transform_bwd(dt, n_pad, H, E, X, W, dM, dX_in, dX_out, dW, dbias, workspace,
-                                            as_stream(stream)),
-                       "msg_transform_bwd");
+  hipStream_t hs = as_stream(stream);
+  hipError_t err = launch_transform_bwd_dx(dt, n_pad, H, E, W, dM, n_pad, dX_in, dX_out, hs);
+  if (err == hipSuccess) err = launch_transform_wgrad(dt, n_pad, H, E, X, dM, n_pad, dW, dbias, workspace, hs);
+  return device_status(err, "msg_transform_bwd");
 }
 
 // ---------------------------------------------------------------------------
@@ -219,15 +240,13 @@ static ggnn_status check_acts(const ggnn_model* m, const ggnn_activations* act) 
   return GGNN_OK;
 }
 
+
 size_t ggnn_backward_workspace_bytes(const ggnn_model* m) {
   if (m == nullptr || check_model(m) != GGNN_OK) {
     clear_error();
     return 0;
   }
-  // Both partial sets live for the whole reverse pass: GRU part, then the
-  // transform part at a 256-byte aligned offset.
-  size_t a = (gru_bwd_workspace(m->dtype, m->n_pad, m->H) + 255) / 256 * 256;
-  return a + transform_bwd_workspace(m->dtype, m->n_pad, m->H, m->E);
+  return bwd_layout(m).total;
 }
 
 ggnn_status ggnn_forward(const ggnn_model* m, const ggnn_activations* act, void* stream) {
@@ -273,41 +292,40 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
   CHECK_PTR(gr->dM, "grads.dM");
   CHECK_PTR(gr->dh, "grads.dh");
   if (m->bias) CHECK_PTR(gr->dbias, "grads.dbias");
-  const size_t need = ggnn_backward_workspace_bytes(m);
-  if (gr->workspace == nullptr || gr->workspace_bytes < need || !aligned16(gr->workspace))
-    return fail(GGNN_ERR_WORKSPACE, "backward needs a 16-byte aligned workspace of %zu bytes (got %zu)", need,
+  const BwdLayout L = bwd_layout(m);
+  if (gr->workspace == nullptr || gr->workspace_bytes < L.total || !aligned16(gr->workspace))
+    return fail(GGNN_ERR_WORKSPACE, "backward needs a 16-byte aligned workspace of %zu bytes (got %zu)", L.total,
                 gr->workspace ? gr->workspace_bytes : (size_t)0);
   const size_t es = dtype_bytes(m->dtype);
   const size_t xs = (size_t)m->n_pad * m->H;
+  const long K = (long)m->T * m->n_pad;   // rows of the weight-gradient contractions; also the dM row length
   hipStream_t s = as_stream(stream);
   float* dbias = m->bias ? gr->dbias : nullptr;
-  // Weight-gradient partials accumulate over all T steps and are reduced
-  // once at the end (fixed split partition and order: deterministic).
-  void* ws_gru = gr->workspace;
-  void* ws_tr = static_cast<char*>(gr->workspace) + (gru_bwd_workspace(m->dtype, m->n_pad, m->H) + 255) / 256 * 256;
-  {
-    hipError_t err = launch_gru_bwd_partials_clear(m->dtype, m->n_pad, m->H, ws_gru, s);
-    if (err == hipSuccess) err = launch_transform_bwd_partials_clear(m->dtype, m->n_pad, m->H, m->E, ws_tr, s);
-    if (err != hipSuccess) return device_status(err, "backward");
-  }
+  char* ws = static_cast<char*>(gr->workspace);
+  char* ghat = ws + L.ghat;
+  // Node passes, t = T-1..0.  The weight gradients are sums over steps and
+  // nodes of products of per-step quantities, so each step only stores its
+  // factors (G^ of step t, dM of step t at column offset t * n_pad) and the
+  // sums run once, over all T * n_pad rows, after the loop.
   for (int t = m->T - 1; t >= 0; --t) {
     const char* Xt = static_cast<const char*>(act->X) + t * xs * es;
-    const float* at = act->a + t * xs;
     const char* sv = static_cast<const char*>(act->saved) + t * 3 * xs * es;
-    hipError_t err = launch_gru_bwd(m->dtype, m->n_pad, m->H, gr->dX, at, Xt, sv, m->Wi, m->U, gr->da, gr->dh,
-                                    gr->dWi, gr->dU, gr->db, ws_gru, s, 1);
+    char* ght = ghat + t * 3 * xs * es;
+    char* dMt = static_cast<char*>(gr->dM) + (size_t)t * m->n_pad * es;
+    hipError_t err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xt, sv, m->Wi, m->U, gr->da, gr->dh,
+                                          ght, s);
     if (err == hipSuccess)
       err = m->band_format == GGNN_BAND_BITS
-                ? launch_banded_bwd_bits(m->dtype, m->n_pad, m->B, m->H, m->E, m->band_t, gr->da, gr->dM, s)
-                : launch_banded_bwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, gr->da, gr->dM, s);
+                ? launch_banded_bwd_bits(m->dtype, m->n_pad, m->B, m->H, m->E, m->band_t, gr->da, dMt, K, s)
+                : launch_banded_bwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, gr->da, dMt, K, s);
     if (err == hipSuccess)
-      err = launch_transform_bwd(m->dtype, m->n_pad, m->H, m->E, Xt, m->W, gr->dM, gr->dh, gr->dX, gr->dW, dbias,
-                                 ws_tr, s, 1);
+      err = launch_transform_bwd_dx(m->dtype, m->n_pad, m->H, m->E, m->W, dMt, K, gr->dh, gr->dX, s);
     if (err != hipSuccess) return device_status(err, "backward");
   }
-  hipError_t err = launch_gru_bwd_partials_reduce(m->dtype, m->n_pad, m->H, gr->dWi, gr->dU, gr->db, ws_gru, s);
+  hipError_t err = launch_gru_wgrad(m->dtype, K, m->H, act->a, act->X, act->saved, ghat, gr->dWi, gr->dU, gr->db,
+                                    ws + L.gru_part, s);
   if (err == hipSuccess)
-    err = launch_transform_bwd_partials_reduce(m->dtype, m->n_pad, m->H, m->E, gr->dW, dbias, ws_tr, s);
+    err = launch_transform_wgrad(m->dtype, K, m->H, m->E, act->X, gr->dM, K, gr->dW, dbias, ws + L.tr_part, s);
   return device_status(err, "backward");
 }
 

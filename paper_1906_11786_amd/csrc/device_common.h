@@ -25,17 +25,22 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint16_t bf16s;  // bf16 storage word
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 
 __device__ __forceinline__ float bf2f(bf16s v) { return __uint_as_float(static_cast<uint32_t>(v) << 16); }
 
-// Round to nearest bf16, ties to even (finite inputs).
-__device__ __forceinline__ bf16s f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return static_cast<bf16s>(u >> 16);
+// Round to nearest bf16, ties to even: gfx950 converts two floats per
+// instruction (v_cvt_pk_bf16_f32), element 0 in the low half.
+__device__ __forceinline__ uint32_t pk2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2_t));
 }
+__device__ __forceinline__ bf16s f2bf(float f) { return __builtin_bit_cast(bf16s, static_cast<__bf16>(f)); }
+// The two bf16 halves of a packed word as floats.
+__device__ __forceinline__ float lo_f(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi_f(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // Storage element -> float and back.
 template <typename S> __device__ __forceinline__ float to_f(S v);
@@ -110,11 +115,7 @@ __device__ __forceinline__ f32x8 load8_strided(const float* p, int stride) {
 // Build a fragment from eight floats, rounding to the storage type.
 template <typename S> __device__ __forceinline__ frag_t<S> pack8(const float* v);
 template <> __device__ __forceinline__ bf16x8 pack8<bf16s>(const float* v) {
-  uint32_t w[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    w[i] = static_cast<uint32_t>(f2bf(v[2 * i])) | (static_cast<uint32_t>(f2bf(v[2 * i + 1])) << 16);
-  u32x4 u = u32x4{w[0], w[1], w[2], w[3]};
+  u32x4 u = u32x4{pk2(v[0], v[1]), pk2(v[2], v[3]), pk2(v[4], v[5]), pk2(v[6], v[7])};
   return __builtin_bit_cast(bf16x8, u);
 }
 template <> __device__ __forceinline__ f32x8 pack8<float>(const float* v) {
@@ -126,9 +127,7 @@ template <> __device__ __forceinline__ f32x8 pack8<float>(const float* v) {
 
 // Store four consecutive elements from floats (8 B for bf16, 16 B for fp32).
 __device__ __forceinline__ void store4(bf16s* p, float a, float b, float c, float d) {
-  u32x2 v = u32x2{static_cast<uint32_t>(f2bf(a)) | (static_cast<uint32_t>(f2bf(b)) << 16),
-                       static_cast<uint32_t>(f2bf(c)) | (static_cast<uint32_t>(f2bf(d)) << 16)};
-  *reinterpret_cast<u32x2*>(p) = v;
+  *reinterpret_cast<u32x2*>(p) = u32x2{pk2(a, b), pk2(c, d)};
 }
 __device__ __forceinline__ void store4(float* p, float a, float b, float c, float d) {
   *reinterpret_cast<f32x4*>(p) = f32x4{a, b, c, d};
@@ -146,39 +145,34 @@ __device__ __forceinline__ f32x4 load4f(const float* p) { return *reinterpret_ca
 // hi = bf16(x) and lo = bf16(x - hi) (hi + lo equals x to about 16 bits);
 // for fp32 only `hi` is written (hi and lo then point to the same place).
 __device__ __forceinline__ void split_store4(bf16s* hi, bf16s* lo, f32x4 v) {
-  bf16s h[4], l[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    h[i] = f2bf(v[i]);
-    l[i] = f2bf(v[i] - bf2f(h[i]));
-  }
-  *reinterpret_cast<u32x2*>(hi) = u32x2{static_cast<uint32_t>(h[0]) | (static_cast<uint32_t>(h[1]) << 16),
-                                        static_cast<uint32_t>(h[2]) | (static_cast<uint32_t>(h[3]) << 16)};
-  *reinterpret_cast<u32x2*>(lo) = u32x2{static_cast<uint32_t>(l[0]) | (static_cast<uint32_t>(l[1]) << 16),
-                                        static_cast<uint32_t>(l[2]) | (static_cast<uint32_t>(l[3]) << 16)};
+  const uint32_t h0 = pk2(v[0], v[1]), h1 = pk2(v[2], v[3]);
+  *reinterpret_cast<u32x2*>(hi) = u32x2{h0, h1};
+  *reinterpret_cast<u32x2*>(lo) =
+      u32x2{pk2(v[0] - lo_f(h0), v[1] - hi_f(h0)), pk2(v[2] - lo_f(h1), v[3] - hi_f(h1))};
 }
 __device__ __forceinline__ void split_store4(float* hi, float*, f32x4 v) { *reinterpret_cast<f32x4*>(hi) = v; }
 
 // Split eight floats into bf16 hi and lo fragments (see split_store4).
 __device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
-  float h[8], l[8];
+  u32x4 h, l;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    h[i] = bf2f(f2bf(v[i]));
-    l[i] = v[i] - h[i];
+  for (int i = 0; i < 4; ++i) {
+    h[i] = pk2(v[2 * i], v[2 * i + 1]);
+    l[i] = pk2(v[2 * i] - lo_f(h[i]), v[2 * i + 1] - hi_f(h[i]));
   }
-  hi = pack8<bf16s>(h);
-  lo = pack8<bf16s>(l);
+  hi = __builtin_bit_cast(bf16x8, h);
+  lo = __builtin_bit_cast(bf16x8, l);
 }
 
 // 16-byte vector copy unit (8 bf16 or 4 fp32 elements).
 template <typename S> struct Vec16 { static constexpr int elems = 16 / sizeof(S); };
 
-__device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + __expf(-x)); }
+// Gate nonlinearities: hardware exp2 and reciprocal (v_exp_f32, v_rcp_f32,
+// each within about 1 ulp) instead of an IEEE division sequence.
+__device__ __forceinline__ float sigmoidf_(float x) { return __builtin_amdgcn_rcpf(1.0f + __expf(-x)); }
 __device__ __forceinline__ float tanhf_(float x) {
   // tanh(x) = 1 - 2 / (exp(2x) + 1), saturating cleanly for large |x|
-  float e = __expf(2.0f * x);
-  return 1.0f - 2.0f / (e + 1.0f);
+  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(__expf(2.0f * x) + 1.0f);
 }
 
 // Logical workgroup index spread so that consecutive logical tiles land on the

@@ -286,18 +286,21 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
 }
 
 // ---------------------------------------------------------------------------
-// Weight gradients of the GRU over one node split:
-//   P[split][0][i][c] = sum_nodes a[node][i] G^[node][c]          (dWi)
-//   P[split][1][i][c] = sum_nodes x_c[node][i] G^[node][c]        (dU)
+// Weight gradients of the GRU over one split of the rows k:
+//   P[split][0][i][c] = sum_k a[k][i] G^[k][c]          (dWi)
+//   P[split][1][i][c] = sum_k x_c[k][i] G^[k][c]        (dU)
 // with x_c = h for the r and z columns and r*h for the n columns, and
-//   Pb[split][c] = sum_nodes G^[node][c]                          (db).
-// Tile TI x TI (TI = min(H, 64)); both operands are node-major, staged in
-// LDS and read with a stride along nodes.
+//   Pb[split][c] = sum_k G^[k][c]                       (db).
+// The rows are the nodes of one step (K = n_pad) or of all T steps at once
+// (K = T * n_pad: a, h, saved and G^ stacked over t).  Tile TI x TI
+// (TI = min(H, 64)); both operands are node-major, staged in LDS and read
+// with a stride along k.  The tile index runs fastest over the logical
+// workgroup index, so the tiles of one split share their rows in one L2.
 // ---------------------------------------------------------------------------
 template <typename S, int H>
 __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kernel(
     const float* __restrict__ a, const S* __restrict__ h, const S* __restrict__ saved, const S* __restrict__ ghat,
-    float* __restrict__ P, float* __restrict__ Pb, int n_pad, int nodes_per_split, int accumulate) {
+    float* __restrict__ P, float* __restrict__ Pb, long K, int rows_per_split) {
   constexpr int TI = H < 64 ? H : 64;
   constexpr int WAVES = TI / 16;
   constexpr int NT = WAVES * kWave;
@@ -310,13 +313,13 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kern
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int q = lane % 16, g = lane / 16;
-  int bid = blockIdx.x;
+  int bid = xcd_swizzle(blockIdx.x, gridDim.x);
   const int to = bid % TOUT; bid /= TOUT;
   const int ti = bid % TIN; bid /= TIN;
   const int which = bid % 2;
   const int split = bid / 2;
-  const int nlo = split * nodes_per_split;
-  const int nhi = min(n_pad, nlo + nodes_per_split);
+  const long nlo = (long)split * rows_per_split;
+  const long nhi = min(K, nlo + rows_per_split);
   const int col0 = to * TI;                      // gate column of this tile
   const bool rh_src = (which == 1 && col0 >= 2 * H);
   const bool do_bias = (which == 0 && ti == 0 && wave == 0);
@@ -336,12 +339,12 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kern
   f32x4 ar[UN];
   u32x2 gr[UN];     // four G^ elements (8 bytes for bf16; fp32 uses two of these per group below)
   f32x4 gf32[sizeof(S) == 4 ? UN : 1];
-  auto load_chunk = [&](int c0) __attribute__((always_inline)) {
+  auto load_chunk = [&](long c0) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < UN; ++u) {
       const int lin = u * NT + tid;
       const int r = lin / (TI / 4), c = (lin % (TI / 4)) * 4;
-      const int node = c0 + r;
+      const long node = c0 + r;
       if ((TU % NT == 0 || lin < TU) && node < nhi) {
         const int fi = ti * TI + c;
         if (which == 0) {
@@ -364,7 +367,7 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kern
     }
   };
   if (nlo < nhi) load_chunk(nlo);
-  for (int c0 = nlo; c0 < nhi; c0 += KN) {
+  for (long c0 = nlo; c0 < nhi; c0 += KN) {
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < UN; ++u) {
@@ -375,8 +378,8 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kern
         S* pb = &tb[r * PX + c];
         if constexpr (sizeof(S) == 2) {
           // rows are 4-byte aligned: write as two 32-bit words
-          const uint32_t lo = static_cast<uint32_t>(f2bf(ar[u].x)) | (static_cast<uint32_t>(f2bf(ar[u].y)) << 16);
-          const uint32_t hi = static_cast<uint32_t>(f2bf(ar[u].z)) | (static_cast<uint32_t>(f2bf(ar[u].w)) << 16);
+          const uint32_t lo = pk2(ar[u].x, ar[u].y);
+          const uint32_t hi = pk2(ar[u].z, ar[u].w);
           reinterpret_cast<uint32_t*>(pa)[0] = lo;
           reinterpret_cast<uint32_t*>(pa)[1] = hi;
           reinterpret_cast<uint32_t*>(pb)[0] = gr[u].x;
@@ -413,8 +416,7 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kern
     const int c = col0 + 16 * n + q;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      float* p = &out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * 3 * H + c];
-      *p = accumulate ? *p + acc[n][j] : acc[n][j];
+      out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * 3 * H + c] = acc[n][j];
     }
   }
   if (do_bias) {
@@ -423,8 +425,7 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kern
       float v = bsum[n];
       v += __shfl_xor(v, 16);
       v += __shfl_xor(v, 32);
-      float* p = &Pb[(size_t)split * 3 * H + col0 + 16 * n + q];
-      if (g == 0) *p = accumulate ? *p + v : v;
+      if (g == 0) Pb[(size_t)split * 3 * H + col0 + 16 * n + q] = v;
     }
   }
 }
@@ -432,21 +433,22 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kern
 }  // namespace dev
 
 namespace {
+// Row split of the weight-gradient contraction (same policy as the message
+// transform's): about 2048 workgroups, splits of at least GGNN_WGRAD_MIN_ROWS
+// rows, a multiple of 64.
+#ifndef GGNN_WGRAD_MIN_ROWS
+#define GGNN_WGRAD_MIN_ROWS 1024
+#endif
 struct Split {
   int nsplit, per;
 };
-Split gru_split(int n_pad, int H) {
-  int TI = H < 64 ? H : 64;
-  int tiles = 2 * (H / TI) * (3 * H / TI);
-  int want = (1024 + tiles - 1) / tiles;
-  int per = (n_pad + want - 1) / want;
-  per = (per + 63) / 64 * 64;
-  if (per < 512) per = 512;
-  return {(n_pad + per - 1) / per, per};
-}
-size_t ghat_bytes(int dt, int n_pad, int H) {
-  size_t b = (size_t)n_pad * 3 * H * (dt == GGNN_BF16 ? 2 : 4);
-  return (b + 255) / 256 * 256;
+Split gru_split(long K, int H) {
+  const long TI = H < 64 ? H : 64;
+  const long tiles = 2 * (H / TI) * (3 * H / TI);
+  const long want = (2048 + tiles - 1) / tiles;
+  long per = ((K + want - 1) / want + 63) / 64 * 64;
+  if (per < GGNN_WGRAD_MIN_ROWS) per = GGNN_WGRAD_MIN_ROWS;
+  return {(int)((K + per - 1) / per), (int)per};
 }
 
 template <typename S, int H>
@@ -460,25 +462,29 @@ hipError_t gru_fwd_h(int n_pad, const float* a, const void* h, const void* Wi, c
 }
 
 template <typename S, int H>
-hipError_t gru_bwd_h(int n_pad, const float* dh_out, const float* a, const void* h, const void* saved, const void* Wi,
-                     const void* U, void* da, float* dh, float* dWi, float* dU, float* db, void* ws, int pm,
-                     hipStream_t st) {
+hipError_t gru_bwd_nodes_h(int n_pad, const float* dh_out, const void* h, const void* saved, const void* Wi,
+                           const void* U, void* da, float* dh, void* ghat, hipStream_t st) {
   constexpr int WAVES = 4;
-  S* ghat = static_cast<S*>(ws);
-  float* P = reinterpret_cast<float*>(static_cast<char*>(ws) + ghat_bytes(sizeof(S) == 2 ? GGNN_BF16 : GGNN_F32, n_pad, H));
-  Split sp = gru_split(n_pad, H);
-  float* Pb = P + (size_t)sp.nsplit * 2 * H * 3 * H;
   hipLaunchKernelGGL((dev::gru_bwd_kernel<S, H, WAVES>), dim3((n_pad + 16 * WAVES - 1) / (16 * WAVES)),
                      dim3(WAVES * 64), 0, st, dh_out, static_cast<const S*>(h), static_cast<const S*>(saved),
-                     static_cast<const S*>(Wi), static_cast<const S*>(U), static_cast<S*>(da), dh, ghat, n_pad);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
+                     static_cast<const S*>(Wi), static_cast<const S*>(U), static_cast<S*>(da), dh,
+                     static_cast<S*>(ghat), n_pad);
+  return hipGetLastError();
+}
+
+template <typename S, int H>
+hipError_t gru_wgrad_h(long K, const float* a, const void* h, const void* saved, const void* ghat, float* dWi,
+                       float* dU, float* db, void* ws, hipStream_t st) {
   constexpr int TI = H < 64 ? H : 64;
+  Split sp = gru_split(K, H);
+  float* P = static_cast<float*>(ws);
+  float* Pb = P + (size_t)sp.nsplit * 2 * H * 3 * H;
   const int blocks = sp.nsplit * 2 * (H / TI) * (3 * H / TI);
   hipLaunchKernelGGL((dev::gru_wgrad_kernel<S, H>), dim3(blocks), dim3(TI / 16 * 64), 0, st, a,
-                     static_cast<const S*>(h), static_cast<const S*>(saved), ghat, P, Pb, n_pad, sp.per, pm);
-  err = hipGetLastError();
-  if (err != hipSuccess || pm) return err;
+                     static_cast<const S*>(h), static_cast<const S*>(saved), static_cast<const S*>(ghat), P, Pb, K,
+                     sp.per);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
   const long slice = 2L * H * 3 * H;  // partials are [split][which][H][3H]
   err = launch_reduce_partials(P, dWi, sp.nsplit, H * 3 * H, slice, st);
   if (err != hipSuccess) return err;
@@ -487,34 +493,45 @@ hipError_t gru_bwd_h(int n_pad, const float* dh_out, const float* a, const void*
   return launch_reduce_partials(Pb, db, sp.nsplit, 3 * H, 3L * H, st);
 }
 
+#define GGNN_GRU_SWITCH(CALL)                  \
+  switch (H) {                                 \
+    case 32: { constexpr int HH = 32; CALL; }  \
+    case 64: { constexpr int HH = 64; CALL; }  \
+    case 128: { constexpr int HH = 128; CALL; } \
+    case 256: { constexpr int HH = 256; CALL; } \
+  }                                            \
+  return hipErrorInvalidValue;
+
 template <typename S>
 hipError_t gru_fwd_t(int n_pad, int H, const float* a, const void* h, const void* Wi, const void* U, const float* b,
                      void* h_out, void* saved, hipStream_t st) {
-  switch (H) {
-    case 32: return gru_fwd_h<S, 32>(n_pad, a, h, Wi, U, b, h_out, saved, st);
-    case 64: return gru_fwd_h<S, 64>(n_pad, a, h, Wi, U, b, h_out, saved, st);
-    case 128: return gru_fwd_h<S, 128>(n_pad, a, h, Wi, U, b, h_out, saved, st);
-    case 256: return gru_fwd_h<S, 256>(n_pad, a, h, Wi, U, b, h_out, saved, st);
-  }
-  return hipErrorInvalidValue;
+  GGNN_GRU_SWITCH(return (gru_fwd_h<S, HH>(n_pad, a, h, Wi, U, b, h_out, saved, st)))
 }
 template <typename S>
-hipError_t gru_bwd_t(int n_pad, int H, const float* dh_out, const float* a, const void* h, const void* saved,
-                     const void* Wi, const void* U, void* da, float* dh, float* dWi, float* dU, float* db, void* ws,
-                     int pm, hipStream_t st) {
-  switch (H) {
-    case 32: return gru_bwd_h<S, 32>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, pm, st);
-    case 64: return gru_bwd_h<S, 64>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, pm, st);
-    case 128: return gru_bwd_h<S, 128>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, pm, st);
-    case 256: return gru_bwd_h<S, 256>(n_pad, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, pm, st);
-  }
-  return hipErrorInvalidValue;
+hipError_t gru_bwd_nodes_t(int n_pad, int H, const float* dh_out, const void* h, const void* saved, const void* Wi,
+                           const void* U, void* da, float* dh, void* ghat, hipStream_t st) {
+  GGNN_GRU_SWITCH(return (gru_bwd_nodes_h<S, HH>(n_pad, dh_out, h, saved, Wi, U, da, dh, ghat, st)))
 }
+template <typename S>
+hipError_t gru_wgrad_t(long K, int H, const float* a, const void* h, const void* saved, const void* ghat, float* dWi,
+                       float* dU, float* db, void* ws, hipStream_t st) {
+  GGNN_GRU_SWITCH(return (gru_wgrad_h<S, HH>(K, a, h, saved, ghat, dWi, dU, db, ws, st)))
+}
+#undef GGNN_GRU_SWITCH
 }  // namespace
 
+size_t ghat_bytes(int dt, long rows, int H) {
+  size_t b = (size_t)rows * 3 * H * (dt == GGNN_BF16 ? 2 : 4);
+  return (b + 255) / 256 * 256;
+}
+
+size_t gru_wgrad_workspace(long K, int H) {
+  Split sp = gru_split(K, H);
+  return ((size_t)sp.nsplit * 2 * H * 3 * H + (size_t)sp.nsplit * 3 * H) * sizeof(float);
+}
+
 size_t gru_bwd_workspace(int dt, int n_pad, int H) {
-  Split sp = gru_split(n_pad, H);
-  return ghat_bytes(dt, n_pad, H) + ((size_t)sp.nsplit * 2 * H * 3 * H + (size_t)sp.nsplit * 3 * H) * sizeof(float);
+  return ghat_bytes(dt, n_pad, H) + gru_wgrad_workspace(n_pad, H);
 }
 
 hipError_t launch_gru_fwd(int dt, int n_pad, int H, const float* a, const void* h, const void* Wi, const void* U,
@@ -523,31 +540,26 @@ hipError_t launch_gru_fwd(int dt, int n_pad, int H, const float* a, const void* 
                          : gru_fwd_t<float>(n_pad, H, a, h, Wi, U, b, h_out, saved, st);
 }
 
+hipError_t launch_gru_bwd_nodes(int dt, int n_pad, int H, const float* dh_out, const void* h, const void* saved,
+                                const void* Wi, const void* U, void* da, float* dh, void* ghat, hipStream_t st) {
+  return dt == GGNN_BF16 ? gru_bwd_nodes_t<dev::bf16s>(n_pad, H, dh_out, h, saved, Wi, U, da, dh, ghat, st)
+                         : gru_bwd_nodes_t<float>(n_pad, H, dh_out, h, saved, Wi, U, da, dh, ghat, st);
+}
+
+hipError_t launch_gru_wgrad(int dt, long K, int H, const float* a, const void* h, const void* saved, const void* ghat,
+                            float* dWi, float* dU, float* db, void* ws, hipStream_t st) {
+  return dt == GGNN_BF16 ? gru_wgrad_t<dev::bf16s>(K, H, a, h, saved, ghat, dWi, dU, db, ws, st)
+                         : gru_wgrad_t<float>(K, H, a, h, saved, ghat, dWi, dU, db, ws, st);
+}
+
 hipError_t launch_gru_bwd(int dt, int n_pad, int H, const float* dh_out, const float* a, const void* h,
                           const void* saved, const void* Wi, const void* U, void* da, float* dh, float* dWi,
-                          float* dU, float* db, void* ws, hipStream_t st, int partial_mode) {
-  return dt == GGNN_BF16
-             ? gru_bwd_t<dev::bf16s>(n_pad, H, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, partial_mode, st)
-             : gru_bwd_t<float>(n_pad, H, dh_out, a, h, saved, Wi, U, da, dh, dWi, dU, db, ws, partial_mode, st);
-}
-
-hipError_t launch_gru_bwd_partials_clear(int dt, int n_pad, int H, void* ws, hipStream_t st) {
-  Split sp = gru_split(n_pad, H);
-  float* P = reinterpret_cast<float*>(static_cast<char*>(ws) + ghat_bytes(dt, n_pad, H));
-  return launch_fill_zero(P, (size_t)sp.nsplit * 2 * H * 3 * H + (size_t)sp.nsplit * 3 * H, st);
-}
-
-hipError_t launch_gru_bwd_partials_reduce(int dt, int n_pad, int H, float* dWi, float* dU, float* db, void* ws,
-                                          hipStream_t st) {
-  Split sp = gru_split(n_pad, H);
-  float* P = reinterpret_cast<float*>(static_cast<char*>(ws) + ghat_bytes(dt, n_pad, H));
-  float* Pb = P + (size_t)sp.nsplit * 2 * H * 3 * H;
-  const long slice = 2L * H * 3 * H;
-  hipError_t err = launch_reduce_partials(P, dWi, sp.nsplit, H * 3 * H, slice, st);
+                          float* dU, float* db, void* ws, hipStream_t st) {
+  void* ghat = ws;
+  void* part = static_cast<char*>(ws) + ghat_bytes(dt, n_pad, H);
+  hipError_t err = launch_gru_bwd_nodes(dt, n_pad, H, dh_out, h, saved, Wi, U, da, dh, ghat, st);
   if (err != hipSuccess) return err;
-  err = launch_reduce_partials(P + (size_t)H * 3 * H, dU, sp.nsplit, H * 3 * H, slice, st);
-  if (err != hipSuccess) return err;
-  return launch_reduce_partials(Pb, db, sp.nsplit, 3 * H, 3L * H, st);
+  return launch_gru_wgrad(dt, n_pad, H, a, h, saved, ghat, dWi, dU, db, part, st);
 }
 
 }  // namespace ggnn

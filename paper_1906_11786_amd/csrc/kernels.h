@@ -12,8 +12,10 @@ namespace ggnn {
 
 hipError_t launch_banded_fwd(int dt, int n_pad, int B, int H, int E, const void* band, const float* M, float* a,
                              hipStream_t st);
+// dM rows have length ldm >= n_pad (ldm = T * n_pad when the reverse pass
+// keeps every step's message gradient for the weight-gradient products).
 hipError_t launch_banded_bwd(int dt, int n_pad, int B, int H, int E, const void* band, const void* da, void* dM,
-                             hipStream_t st);
+                             long ldm, hipStream_t st);
 
 // out[i] += sum_s part[s * stride + i], i < count, fixed summation order.
 hipError_t launch_reduce_partials(const float* part, float* out, int nsplit, int count, long stride,
@@ -23,32 +25,37 @@ hipError_t launch_reduce_partials(const float* part, float* out, int nsplit, int
 hipError_t launch_step_fwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits, const void* X,
                                 const void* W, const float* bias, float* a, hipStream_t st);
 hipError_t launch_banded_bwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits_t, const void* da,
-                                  void* dM, hipStream_t st);
+                                  void* dM, long ldm, hipStream_t st);
 
 hipError_t launch_transform_fwd(int dt, int n_pad, int H, int E, const void* X, const void* W, const float* bias,
                                 float* M, hipStream_t st);
-// Workspace layout of the transform backward (floats): partial dW then
-// partial dbias, one slice per node split.
-size_t transform_bwd_workspace(int dt, int n_pad, int H, int E);
-// partial_mode 0: dW, dbias += this call's gradient (partials written, then
-// reduced); 1: the call only adds its gradient into the partials of `ws`
-// (cleared and reduced by the two functions below), for multi-step loops.
-hipError_t launch_transform_bwd(int dt, int n_pad, int H, int E, const void* X, const void* W, const void* dM,
-                                const float* dX_in, float* dX_out, float* dW, float* dbias, void* ws,
-                                hipStream_t st, int partial_mode = 0);
-hipError_t launch_transform_bwd_partials_clear(int dt, int n_pad, int H, int E, void* ws, hipStream_t st);
-hipError_t launch_transform_bwd_partials_reduce(int dt, int n_pad, int H, int E, float* dW, float* dbias, void* ws,
-                                                hipStream_t st);
+// Input gradient dX_out = dX_in + sum_e dM_e W_e^T (dM rows of length ld).
+hipError_t launch_transform_bwd_dx(int dt, int n_pad, int H, int E, const void* W, const void* dM, long ld,
+                                   const float* dX_in, float* dX_out, hipStream_t st);
+// Weight gradients over K rows: dW += X^T dM, dbias += row sums of dM (NULL
+// to skip), X = K rows [K][H], dM rows of length ld >= K.  The workspace
+// (transform_wgrad_workspace bytes) holds per-split partials, reduced in a
+// fixed order.
+size_t transform_wgrad_workspace(long K, int H, int E);
+hipError_t launch_transform_wgrad(int dt, long K, int H, int E, const void* X, const void* dM, long ld, float* dW,
+                                  float* dbias, void* ws, hipStream_t st);
 hipError_t launch_fill_zero(float* p, size_t count, hipStream_t st);
 
 hipError_t launch_gru_fwd(int dt, int n_pad, int H, const float* a, const void* h, const void* Wi, const void* U,
                           const float* b, void* h_out, void* saved, hipStream_t st);
+// Node pass of the GRU reverse: da, dh and the gate gradients G^ [n_pad][3H].
+hipError_t launch_gru_bwd_nodes(int dt, int n_pad, int H, const float* dh_out, const void* h, const void* saved,
+                                const void* Wi, const void* U, void* da, float* dh, void* ghat, hipStream_t st);
+size_t ghat_bytes(int dt, long rows, int H);
+// GRU weight gradients over K rows of (a, h, saved, G^) stacked node-major:
+// dWi, dU, db += (partials in ws of gru_wgrad_workspace bytes, fixed order).
+size_t gru_wgrad_workspace(long K, int H);
+hipError_t launch_gru_wgrad(int dt, long K, int H, const float* a, const void* h, const void* saved, const void* ghat,
+                            float* dWi, float* dU, float* db, void* ws, hipStream_t st);
+// One step: node pass with G^ in ws, then the weight gradients over n_pad rows.
 size_t gru_bwd_workspace(int dt, int n_pad, int H);
 hipError_t launch_gru_bwd(int dt, int n_pad, int H, const float* dh_out, const float* a, const void* h,
                           const void* saved, const void* Wi, const void* U, void* da, float* dh, float* dWi,
-                          float* dU, float* db, void* ws, hipStream_t st, int partial_mode = 0);
-hipError_t launch_gru_bwd_partials_clear(int dt, int n_pad, int H, void* ws, hipStream_t st);
-hipError_t launch_gru_bwd_partials_reduce(int dt, int n_pad, int H, float* dWi, float* dU, float* db, void* ws,
-                                          hipStream_t st);
+                          float* dU, float* db, void* ws, hipStream_t st);
 
 }  // namespace ggnn

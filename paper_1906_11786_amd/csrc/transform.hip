@@ -2,8 +2,8 @@
 // cores (typed form of Eq. 1: one H x H map per edge type).
 //
 // Layouts: X [n_pad][H] node-major, W [E][H][H] (W[e][h_in][h_out]),
-// M [E][H][n_pad] float and dM [E][H][n_pad] dt, both feature-major,
-// dX [n_pad][H] float.
+// M [E][H][n_pad] float and dM [E][H][ld] dt (ld >= n_pad), both
+// feature-major, dX [n_pad][H] float.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -86,7 +86,8 @@ __global__ __launch_bounds__(WAVES * kWave) void transform_fwd_kernel(const S* _
 }
 
 // ---------------------------------------------------------------------------
-// Backward, input gradient: dX_out = dX_in + sum_e dM_e W_e^T.
+// Backward, input gradient: dX_out = dX_in + sum_e dM_e W_e^T (dM rows of
+// length ld >= n_pad: one step's slice of a multi-step buffer).
 // A workgroup owns 16*WAVES nodes; wave w: 16 nodes, all H input features.
 // D[h_in][node]: A operand = W_e rows (contiguous in h_out, tiny, cached),
 // B operand = dM_e rows of one node: feature-major dM is staged per type in
@@ -97,7 +98,7 @@ template <typename S, int H, int WAVES>
 __global__ __launch_bounds__(WAVES * kWave) void transform_bwd_dx_kernel(const S* __restrict__ W,
                                                                           const S* __restrict__ dM,
                                                                           const float* dX_in, float* dX_out,
-                                                                          int n_pad, int E) {
+                                                                          int n_pad, int E, long ld) {
   constexpr int NT = WAVES * kWave;
   constexpr int V = 16 / sizeof(S);
   constexpr int NW = 16 * WAVES;
@@ -118,13 +119,13 @@ __global__ __launch_bounds__(WAVES * kWave) void transform_bwd_dx_kernel(const S
   constexpr int UN = (TU + NT - 1) / NT;
   u32x4 reg[UN];
   auto load_tile = [&](int e) __attribute__((always_inline)) {
-    const S* src = dM + (size_t)e * H * n_pad + n0;
+    const S* src = dM + (size_t)e * H * ld + n0;
 #pragma unroll
     for (int u = 0; u < UN; ++u) {
       const int lin = u * NT + tid;
       const int h = lin / (NW / V), c = (lin % (NW / V)) * V;
       if ((TU % NT == 0 || lin < TU) && n0 + c < n_pad)
-        reg[u] = *reinterpret_cast<const u32x4*>(src + (size_t)h * n_pad + c);
+        reg[u] = *reinterpret_cast<const u32x4*>(src + (size_t)h * ld + c);
     }
   };
   load_tile(0);
@@ -164,22 +165,26 @@ __global__ __launch_bounds__(WAVES * kWave) void transform_bwd_dx_kernel(const S
 }
 
 // ---------------------------------------------------------------------------
-// Backward, weight gradient, one node split: P[split][e][h_in][h_out] =
-// sum over the split's nodes of X[node][h_in] * dM[e][h_out][node], and the
-// bias partial Pb[split][e][h_out] = sum over nodes of dM[e][h_out][node].
-// Workgroup tile TI x TI (TI = min(H, 64)), TI/16 waves; the contraction
-// over nodes runs in chunks of 64: X (node-major) is staged in LDS and read
-// with a stride, dM (feature-major, contiguous in nodes) is read directly.
+// Backward, weight gradient, one split of the contraction: P[split][e][h_in]
+// [h_out] = sum over the split's rows k of X[k][h_in] * dM[e][h_out][k], and
+// the bias partial Pb[split][e][h_out] = sum over k of dM[e][h_out][k].  The
+// contraction runs over K rows: K = n_pad for one step, or T * n_pad for all
+// steps at once (X[t] stacked, dM rows of length ld = T * n_pad holding step
+// t at offset t * n_pad).  Workgroup tile TI x TI (TI = min(H, 64)), TI/16
+// waves; rows are taken in chunks of 64: X (node-major) is staged in LDS and
+// read with a stride, dM (feature-major, contiguous in k) is read directly.
+// The tile index runs fastest over the logical workgroup index, so the tiles
+// of one split share their X chunks in one XCD's L2.
 // ---------------------------------------------------------------------------
 template <typename S, int H>
 __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgrad_kernel(
-    const S* __restrict__ X, const S* __restrict__ dM, float* __restrict__ P, float* __restrict__ Pb, int n_pad,
-    int E, int nodes_per_split, int accumulate) {
+    const S* __restrict__ X, const S* __restrict__ dM, long ld, float* __restrict__ P, float* __restrict__ Pb,
+    long K, int E, int rows_per_split) {
   constexpr int TI = H < 64 ? H : 64;
   constexpr int WAVES = TI / 16;
   constexpr int NT = WAVES * kWave;
   constexpr int V = 16 / sizeof(S);
-  constexpr int KN = 64;                  // nodes per LDS chunk
+  constexpr int KN = 64;                  // rows per LDS chunk
   constexpr int PX = TI + 4 / sizeof(S);
   constexpr int NTL = TI / 16;
   constexpr int TPD = H / TI;             // tiles per dimension
@@ -187,13 +192,13 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int q = lane % 16, g = lane / 16;
-  int bid = blockIdx.x;
+  int bid = xcd_swizzle(blockIdx.x, gridDim.x);
   const int to = bid % TPD; bid /= TPD;
   const int ti = bid % TPD; bid /= TPD;
   const int e = bid % E;
   const int split = bid / E;
-  const int nlo = split * nodes_per_split;
-  const int nhi = min(n_pad, nlo + nodes_per_split);
+  const long nlo = (long)split * rows_per_split;
+  const long nhi = min(K, nlo + rows_per_split);
 
   f32x4 acc[NTL];
   float bsum[NTL];
@@ -209,7 +214,7 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
   constexpr int UN = (TU + NT - 1) / NT;
   u32x4 xr[UN];
   frag_t<S> br[KN / 32][NTL];
-  auto load_chunk = [&](int c0) __attribute__((always_inline)) {
+  auto load_chunk = [&](long c0) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < UN; ++u) {
       const int lin = u * NT + tid;
@@ -222,11 +227,11 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
       if (c0 + 32 * kk >= nhi) break;
 #pragma unroll
       for (int n = 0; n < NTL; ++n)
-        br[kk][n] = load8(dM + ((size_t)e * H + to * TI + 16 * n + q) * n_pad + c0 + 32 * kk + 8 * g);
+        br[kk][n] = load8(dM + ((size_t)e * H + to * TI + 16 * n + q) * ld + c0 + 32 * kk + 8 * g);
     }
   };
   if (nlo < nhi) load_chunk(nlo);
-  for (int c0 = nlo; c0 < nhi; c0 += KN) {
+  for (long c0 = nlo; c0 < nhi; c0 += KN) {
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < UN; ++u) {
@@ -246,7 +251,7 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
     if (c0 + KN < nhi) load_chunk(c0 + KN);
 #pragma unroll
     for (int kk = 0; kk < KN / 32; ++kk) {
-      if (c0 + 32 * kk >= nhi) break;    // n_pad is a multiple of 32
+      if (c0 + 32 * kk >= nhi) break;    // K and the split length are multiples of 32
       frag_t<S> afr = load8_strided(&tile[(32 * kk + 8 * g) * PX + 16 * wave + q], PX);
 #pragma unroll
       for (int n = 0; n < NTL; ++n) {
@@ -265,8 +270,7 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
     const int o = to * TI + 16 * n + q;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      float* p = &out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * H + o];
-      *p = accumulate ? *p + acc[n][j] : acc[n][j];
+      out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * H + o] = acc[n][j];
     }
   }
   if (do_bias) {
@@ -275,23 +279,46 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
       float v = bsum[n];
       v += __shfl_xor(v, 16);
       v += __shfl_xor(v, 32);
-      float* p = &Pb[((size_t)split * E + e) * H + to * TI + 16 * n + q];
-      if (g == 0) *p = accumulate ? *p + v : v;
+      if (g == 0) Pb[((size_t)split * E + e) * H + to * TI + 16 * n + q] = v;
     }
   }
 }
 
 }  // namespace dev
 
-// out[i] += sum_{s < nsplit} part[s * stride + i] for i < count, summed in
-// split order (fixed, so results do not depend on scheduling).
-__global__ void reduce_partials_kernel(const float* __restrict__ part, float* __restrict__ out, int nsplit,
-                                       int count, long stride) {
-  int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= count) return;
+// out[i] += sum_{s < nsplit} part[s * stride + i] for i < count.  A
+// workgroup of 64 x RW threads owns 64 consecutive outputs: thread (x, y)
+// sums the splits s = y, y + RW, y + 2RW, ... in increasing order (eight
+// loads in flight), then thread (x, 0) adds the RW sums in order y = 0..RW-1.
+// The order depends only on nsplit, so results do not depend on scheduling.
+constexpr int kReduceRW = 16;
+__global__ __launch_bounds__(64 * kReduceRW) void reduce_partials_kernel(const float* __restrict__ part,
+                                                                         float* __restrict__ out, int nsplit,
+                                                                         int count, long stride) {
+  constexpr int RW = kReduceRW;
+  __shared__ float red[RW][64];
+  const int x = threadIdx.x % 64, y = threadIdx.x / 64;
+  const int i = blockIdx.x * 64 + x;
   float s = 0.f;
-  for (int k = 0; k < nsplit; ++k) s += part[(size_t)k * stride + i];
-  out[i] += s;
+  if (i < count) {
+    int k = y;
+    for (; k + 7 * RW < nsplit; k += 8 * RW) {
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = part[(size_t)(k + j * RW) * stride + i];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) s += v[j];
+    }
+    for (; k < nsplit; k += RW) s += part[(size_t)k * stride + i];
+  }
+  red[y][x] = s;
+  __syncthreads();
+  if (y == 0 && i < count) {
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < RW; ++w) t += red[w][x];
+    out[i] += t;
+  }
 }
 
 // Zero-fill with a kernel (not hipMemsetAsync, so the launch can sit inside a
@@ -315,28 +342,29 @@ hipError_t launch_fill_zero(float* p, size_t count, hipStream_t st) {
 hipError_t launch_reduce_partials(const float* part, float* out, int nsplit, int count, long stride,
                                   hipStream_t st) {
   if (count <= 0) return hipSuccess;
-  hipLaunchKernelGGL(reduce_partials_kernel, dim3((count + 255) / 256), dim3(256), 0, st, part, out, nsplit, count,
-                     stride);
+  hipLaunchKernelGGL(reduce_partials_kernel, dim3((count + 63) / 64), dim3(64 * kReduceRW), 0, st, part, out, nsplit,
+                     count, stride);
   return hipGetLastError();
 }
 
 namespace {
-// Node split of the weight-gradient contraction: enough workgroups to fill
-// the chip, each split a multiple of 64 nodes.
+// Row split of the weight-gradient contraction: about 2048 workgroups over
+// all tiles (several waves per SIMD to hide the memory latency of the chunk
+// loop), each split a multiple of 64 rows and at least GGNN_WGRAD_MIN_ROWS,
+// so the partial slices stay small next to the rows they summarise.
+#ifndef GGNN_WGRAD_MIN_ROWS
+#define GGNN_WGRAD_MIN_ROWS 1024
+#endif
 struct Split {
   int nsplit, per;
 };
-Split transform_split(int n_pad, int H, int E) {
-  int TI = H < 64 ? H : 64;
-  int tiles = E * (H / TI) * (H / TI);
-  int want = (1024 + tiles - 1) / tiles;
-  int maxs = (n_pad + 63) / 64;
-  int ns = want < maxs ? want : maxs;
-  if (ns < 1) ns = 1;
-  int per = ((n_pad + ns - 1) / ns + 63) / 64 * 64;
-  if (per < 512) per = 512;   // keep the partial traffic well below the node traffic
-  ns = (n_pad + per - 1) / per;
-  return {ns, per};
+Split transform_split(long K, int H, int E) {
+  const long TI = H < 64 ? H : 64;
+  const long tiles = E * (H / TI) * (H / TI);
+  const long want = (2048 + tiles - 1) / tiles;
+  long per = ((K + want - 1) / want + 63) / 64 * 64;
+  if (per < GGNN_WGRAD_MIN_ROWS) per = GGNN_WGRAD_MIN_ROWS;
+  return {(int)((K + per - 1) / per), (int)per};
 }
 
 template <typename S, int H>
@@ -356,24 +384,25 @@ hipError_t transform_fwd_h(int n_pad, int E, const void* X, const void* W, const
 }
 
 template <typename S, int H>
-hipError_t transform_bwd_h(int n_pad, int E, const void* X, const void* W, const void* dM, const float* dX_in,
-                           float* dX_out, float* dW, float* dbias, void* ws, int partial_mode, hipStream_t st) {
-  const S* xp = static_cast<const S*>(X);
-  const S* wp = static_cast<const S*>(W);
-  const S* dp = static_cast<const S*>(dM);
-  hipLaunchKernelGGL((dev::transform_bwd_dx_kernel<S, H, 4>), dim3((n_pad + 63) / 64), dim3(256), 0, st, wp, dp,
-                     dX_in, dX_out, n_pad, E);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
-  Split sp = transform_split(n_pad, H, E);
+hipError_t transform_dx_h(int n_pad, int E, const void* W, const void* dM, long ld, const float* dX_in,
+                          float* dX_out, hipStream_t st) {
+  hipLaunchKernelGGL((dev::transform_bwd_dx_kernel<S, H, 4>), dim3((n_pad + 63) / 64), dim3(256), 0, st,
+                     static_cast<const S*>(W), static_cast<const S*>(dM), dX_in, dX_out, n_pad, E, ld);
+  return hipGetLastError();
+}
+
+template <typename S, int H>
+hipError_t transform_wgrad_h(long K, int E, const void* X, const void* dM, long ld, float* dW, float* dbias, void* ws,
+                             hipStream_t st) {
+  Split sp = transform_split(K, H, E);
   constexpr int TI = H < 64 ? H : 64;
   float* P = static_cast<float*>(ws);
   float* Pb = dbias ? P + (size_t)sp.nsplit * E * H * H : nullptr;
   const int blocks = sp.nsplit * E * (H / TI) * (H / TI);
-  hipLaunchKernelGGL((dev::transform_wgrad_kernel<S, H>), dim3(blocks), dim3(TI / 16 * 64), 0, st, xp, dp, P, Pb,
-                     n_pad, E, sp.per, partial_mode);
-  err = hipGetLastError();
-  if (err != hipSuccess || partial_mode) return err;
+  hipLaunchKernelGGL((dev::transform_wgrad_kernel<S, H>), dim3(blocks), dim3(TI / 16 * 64), 0, st,
+                     static_cast<const S*>(X), static_cast<const S*>(dM), ld, P, Pb, K, E, sp.per);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
   err = launch_reduce_partials(P, dW, sp.nsplit, E * H * H, (long)E * H * H, st);
   if (err != hipSuccess || !dbias) return err;
   return launch_reduce_partials(Pb, dbias, sp.nsplit, E * H, (long)E * H, st);
@@ -391,21 +420,31 @@ hipError_t transform_fwd_t(int n_pad, int H, int E, const void* X, const void* W
   return hipErrorInvalidValue;
 }
 template <typename S>
-hipError_t transform_bwd_t(int n_pad, int H, int E, const void* X, const void* W, const void* dM, const float* dX_in,
-                           float* dX_out, float* dW, float* dbias, void* ws, int pm, hipStream_t st) {
+hipError_t transform_dx_t(int n_pad, int H, int E, const void* W, const void* dM, long ld, const float* dX_in,
+                          float* dX_out, hipStream_t st) {
   switch (H) {
-    case 32: return transform_bwd_h<S, 32>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, pm, st);
-    case 64: return transform_bwd_h<S, 64>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, pm, st);
-    case 128: return transform_bwd_h<S, 128>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, pm, st);
-    case 256: return transform_bwd_h<S, 256>(n_pad, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, pm, st);
+    case 32: return transform_dx_h<S, 32>(n_pad, E, W, dM, ld, dX_in, dX_out, st);
+    case 64: return transform_dx_h<S, 64>(n_pad, E, W, dM, ld, dX_in, dX_out, st);
+    case 128: return transform_dx_h<S, 128>(n_pad, E, W, dM, ld, dX_in, dX_out, st);
+    case 256: return transform_dx_h<S, 256>(n_pad, E, W, dM, ld, dX_in, dX_out, st);
+  }
+  return hipErrorInvalidValue;
+}
+template <typename S>
+hipError_t transform_wgrad_t(long K, int H, int E, const void* X, const void* dM, long ld, float* dW, float* dbias,
+                             void* ws, hipStream_t st) {
+  switch (H) {
+    case 32: return transform_wgrad_h<S, 32>(K, E, X, dM, ld, dW, dbias, ws, st);
+    case 64: return transform_wgrad_h<S, 64>(K, E, X, dM, ld, dW, dbias, ws, st);
+    case 128: return transform_wgrad_h<S, 128>(K, E, X, dM, ld, dW, dbias, ws, st);
+    case 256: return transform_wgrad_h<S, 256>(K, E, X, dM, ld, dW, dbias, ws, st);
   }
   return hipErrorInvalidValue;
 }
 }  // namespace
 
-size_t transform_bwd_workspace(int dt, int n_pad, int H, int E) {
-  (void)dt;
-  Split sp = transform_split(n_pad, H, E);
+size_t transform_wgrad_workspace(long K, int H, int E) {
+  Split sp = transform_split(K, H, E);
   return ((size_t)sp.nsplit * E * H * H + (size_t)sp.nsplit * E * H) * sizeof(float);
 }
 
@@ -415,26 +454,16 @@ hipError_t launch_transform_fwd(int dt, int n_pad, int H, int E, const void* X, 
                          : transform_fwd_t<float>(n_pad, H, E, X, W, bias, M, st);
 }
 
-hipError_t launch_transform_bwd(int dt, int n_pad, int H, int E, const void* X, const void* W, const void* dM,
-                                const float* dX_in, float* dX_out, float* dW, float* dbias, void* ws,
-                                hipStream_t st, int partial_mode) {
-  return dt == GGNN_BF16
-             ? transform_bwd_t<dev::bf16s>(n_pad, H, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, partial_mode, st)
-             : transform_bwd_t<float>(n_pad, H, E, X, W, dM, dX_in, dX_out, dW, dbias, ws, partial_mode, st);
+hipError_t launch_transform_bwd_dx(int dt, int n_pad, int H, int E, const void* W, const void* dM, long ld,
+                                   const float* dX_in, float* dX_out, hipStream_t st) {
+  return dt == GGNN_BF16 ? transform_dx_t<dev::bf16s>(n_pad, H, E, W, dM, ld, dX_in, dX_out, st)
+                         : transform_dx_t<float>(n_pad, H, E, W, dM, ld, dX_in, dX_out, st);
 }
 
-hipError_t launch_transform_bwd_partials_clear(int dt, int n_pad, int H, int E, void* ws, hipStream_t st) {
-  return launch_fill_zero(static_cast<float*>(ws), transform_bwd_workspace(dt, n_pad, H, E) / sizeof(float), st);
-}
-
-hipError_t launch_transform_bwd_partials_reduce(int dt, int n_pad, int H, int E, float* dW, float* dbias, void* ws,
-                                                hipStream_t st) {
-  (void)dt;
-  Split sp = transform_split(n_pad, H, E);
-  float* P = static_cast<float*>(ws);
-  hipError_t err = launch_reduce_partials(P, dW, sp.nsplit, E * H * H, (long)E * H * H, st);
-  if (err != hipSuccess || !dbias) return err;
-  return launch_reduce_partials(P + (size_t)sp.nsplit * E * H * H, dbias, sp.nsplit, E * H, (long)E * H, st);
+hipError_t launch_transform_wgrad(int dt, long K, int H, int E, const void* X, const void* dM, long ld, float* dW,
+                                  float* dbias, void* ws, hipStream_t st) {
+  return dt == GGNN_BF16 ? transform_wgrad_t<dev::bf16s>(K, H, E, X, dM, ld, dW, dbias, ws, st)
+                         : transform_wgrad_t<float>(K, H, E, X, dM, ld, dW, dbias, ws, st);
 }
 
 }  // namespace ggnn

@@ -129,7 +129,7 @@ class BandedGGNN:
         self.dU = torch.zeros((H, 3 * H), dtype=torch.float32, device=device)
         self.db = torch.zeros((3 * H,), dtype=torch.float32, device=device)
         self.da = torch.empty((H, n_pad), dtype=td, device=device)
-        self.dM = torch.empty((E, H, n_pad), dtype=td, device=device)
+        self.dM = torch.empty((E, H, T * n_pad), dtype=td, device=device)
         self.dh = torch.empty((n_pad, H), dtype=torch.float32, device=device)
         self.model = capi.ggnn_model(
             dtype=capi.DTYPES[dt], n_pad=n_pad, B=B, H=H, E=E, T=T, band=self.band.data_ptr(),
