@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define GGNN_ABI_VERSION 3
+#define GGNN_ABI_VERSION 4
 
 typedef enum {
   GGNN_OK = 0,
@@ -215,6 +215,20 @@ ggnn_status ggnn_banded_step_bits(ggnn_dtype dt, int32_t n_pad, int32_t B, int32
 ggnn_status ggnn_banded_propagate_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
                                            const void* bits_t, const void* da, void* dM, void* stream);
 
+/* Reverse of ggnn_banded_step_bits in the same fused form (Algorithm 1's
+ * operand order run backwards), per edge type e:
+ *   dM_e = A_e^T da                      (through bits_t; stored, rounded to dt)
+ *   dX_out = dX_in + sum_e dM_e W_e^T    (dM_e enters as the stored value)
+ *   bits_t  transposed bit band of ggnn_banded_pack_bits (16-byte aligned)
+ *   da      [H][n_pad] dt feature-major;  W [E][H][H] dt
+ *   dX_in   [n_pad][H] float or NULL (zero); dX_out [n_pad][H] float (written;
+ *           may be the same buffer as dX_in)
+ *   dM      node-major, dt: row r (< n_pad) of type e at dM + (e * ldm + r) * H;
+ *           ldm >= n_pad rows per type (written) */
+ggnn_status ggnn_banded_step_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
+                                      const void* bits_t, const void* da, const void* W, const float* dX_in,
+                                      float* dX_out, void* dM, int64_t ldm, void* stream);
+
 /* Workspace bytes needed by ggnn_gru_update_bwd for these sizes. */
 size_t ggnn_gru_update_bwd_workspace_bytes(ggnn_dtype dt, int32_t n_pad, int32_t H);
 
@@ -288,8 +302,10 @@ typedef struct ggnn_grads {
   float* dU;            /* [H][3H]    += */
   float* db;            /* [3H]       += */
   void* da;             /* [H][n_pad] dt scratch */
-  void* dM;             /* [E][H][T*n_pad] dt scratch: step t's message gradient in columns
-                         * [t*n_pad, (t+1)*n_pad) of every (e, h) row */
+  void* dM;             /* E*H*T*n_pad dt scratch: every step's message gradient.  Dense band:
+                         * feature-major [E][H][T*n_pad], step t in columns [t*n_pad, (t+1)*n_pad)
+                         * of every (e, h) row.  Bit band: node-major [E][T*n_pad][H], step t in
+                         * rows [t*n_pad, (t+1)*n_pad) of every type. */
   float* dh;            /* [n_pad][H] float scratch */
   void* workspace;      /* device scratch of ggnn_backward_workspace_bytes() */
   size_t workspace_bytes;
@@ -305,9 +321,9 @@ size_t ggnn_backward_workspace_bytes(const ggnn_model* model);
 ggnn_status ggnn_forward(const ggnn_model* model, const ggnn_activations* act, void* stream);
 
 /* Reverse pass for L with dL/dX_T given in grads->dX: for t = T-1..0,
- *   da, dh, G^_t = gru_update_bwd node pass(dX); dM_t = banded_propagate_bwd(da)
- *   (dense band) or banded_propagate_bits_bwd(da) (bit band);
- *   dX = dh + sum_e dM_t,e W_e^T;
+ *   da, dh, G^_t = gru_update_bwd node pass(dX);
+ *   dense band: dM_t = banded_propagate_bwd(da); dX = dh + sum_e dM_t,e W_e^T;
+ *   bit band:   dM_t, dX = banded_step_bits_bwd(da, dX_in = dh) (one kernel);
  * then the weight gradients as single contractions over all T * n_pad rows:
  *   dWi, dU, db += sums over t of the GRU products of (a[t], X[t], saved[t], G^_t),
  *   dW_e += sum_t X[t]^T dM_t,e, dbias_e += row sums of dM_t,e (accumulate, +=).

@@ -16,29 +16,29 @@ LIB = os.path.join(HERE, "libggnn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Device code: gfx950 only; packed fp32 instructions are disabled (hipcc
-# emits them from plain float code otherwise).  Matrix-core results stay in
-# the unified VGPR file (gfx950 needs no separate accumulator registers):
-# otherwise the compiler parks accumulators in AGPRs and spends a VALU move
-# per element on every round trip.
+# emits them from plain float code otherwise).
 HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
-             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-mllvm", "-amdgpu-mfma-vgpr-form"]
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Each kernel source is built once per storage dtype.  The bf16 build keeps
+# matrix-core results in the unified VGPR file (gfx950 needs no separate
+# accumulator registers; otherwise the compiler parks accumulators in AGPRs
+# and spends a VALU move per element on every round trip).  The fp32 build
+# keeps the default assignment: its large-H forms do not compile in VGPR-only
+# mode with this toolchain.
+DT_FLAGS = {"bf16": ["-DGGNN_DT_BF16=1", "-mllvm", "-amdgpu-mfma-vgpr-form"], "f32": ["-DGGNN_DT_BF16=0"]}
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall"]
 
-SOURCES = [
-    ("host.cpp", "c++"),
-    ("capi_device.cpp", "hip"),
-    ("banded.hip", "hip"),
-    ("banded_bits.hip", "hip"),
-    ("transform.hip", "hip"),
-    ("gru.hip", "hip"),
-]
+# (source, language, dtype build or None)
+SOURCES = [("host.cpp", "c++", None), ("capi_device.cpp", "hip", None)] + [
+    (src, "hip", dt) for src in ("banded.hip", "banded_bits.hip", "transform.hip", "gru.hip") for dt in ("bf16", "f32")]
 
 
-def _compile(src: str, lang: str) -> str:
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+def _compile(src: str, lang: str, dt) -> str:
+    stem = os.path.splitext(src)[0] + ("" if dt is None else "_" + dt)
+    obj = os.path.join(BUILD, stem + ".o")
     path = os.path.join(CSRC, src)
     if lang == "hip":
-        cmd = [HIPCC, "-x", "hip", *HIP_FLAGS, "-c", path, "-o", obj]
+        cmd = [HIPCC, "-x", "hip", *HIP_FLAGS, *(DT_FLAGS[dt] if dt else []), "-c", path, "-o", obj]
     else:
         cmd = [HIPCC, "-x", "c++", *HOST_FLAGS, "-c", path, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -30,6 +30,7 @@ EXPORTS = [
     "ggnn_abi_version", "ggnn_last_error", "ggnn_status_string",
     "ggnn_rcm_order", "ggnn_bandwidth", "ggnn_band_bytes", "ggnn_banded_pack",
     "ggnn_band_bits_bytes", "ggnn_banded_pack_bits", "ggnn_banded_step_bits", "ggnn_banded_propagate_bits_bwd",
+    "ggnn_banded_step_bits_bwd",
     "ggnn_msg_transform", "ggnn_banded_propagate", "ggnn_gru_update",
     "ggnn_gru_update_bwd_workspace_bytes", "ggnn_gru_update_bwd",
     "ggnn_banded_propagate_bwd", "ggnn_msg_transform_bwd_workspace_bytes", "ggnn_msg_transform_bwd",
@@ -78,6 +79,7 @@ _SIGS = {
     "ggnn_banded_pack_bits": (C.c_int, [i32, i32, i32, i64, vp, vp, vp, vp, C.c_int, vp, vp, vp, vp, vp]),
     "ggnn_banded_step_bits": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]),
     "ggnn_banded_propagate_bits_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp]),
+    "ggnn_banded_step_bits_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i64, vp]),
     "ggnn_msg_transform": (C.c_int, [C.c_int, i32, i32, i32, vp, vp, vp, vp, vp]),
     "ggnn_banded_propagate": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp]),
     "ggnn_gru_update": (C.c_int, [C.c_int, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
@@ -225,6 +227,12 @@ def ggnn_banded_step_bits(dt, n_pad, B, H, E, bits, X, W, bias, a, stream=None):
 def ggnn_banded_propagate_bits_bwd(dt, n_pad, B, H, E, bits_t, da, dM, stream=None):
     _check("ggnn_banded_propagate_bits_bwd", lib().ggnn_banded_propagate_bits_bwd(
         _dt(dt), n_pad, B, H, E, _ptr(bits_t), _ptr(da), _ptr(dM), _stream(stream)))
+
+
+def ggnn_banded_step_bits_bwd(dt, n_pad, B, H, E, bits_t, da, W, dX_in, dX_out, dM, ldm, stream=None):
+    _check("ggnn_banded_step_bits_bwd", lib().ggnn_banded_step_bits_bwd(
+        _dt(dt), n_pad, B, H, E, _ptr(bits_t), _ptr(da), _ptr(W), _ptr(dX_in), _ptr(dX_out), _ptr(dM), ldm,
+        _stream(stream)))
 
 
 def ggnn_msg_transform(dt, n_pad, H, E, X, W, bias, M, stream=None):

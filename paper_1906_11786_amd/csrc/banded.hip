@@ -361,16 +361,16 @@ static hipError_t bwd_h(int H, const void* band, const void* da, void* dM, long 
 
 }  // namespace dev
 
-hipError_t launch_banded_fwd(int dt, int n_pad, int B, int H, int E, const void* band, const float* M, float* a,
+namespace GGNN_IMPL_NS {
+hipError_t launch_banded_fwd(int n_pad, int B, int H, int E, const void* band, const float* M, float* a,
                              hipStream_t st) {
-  return dt == GGNN_BF16 ? dev::fwd_h<dev::bf16s>(H, band, M, a, n_pad, B, E, st)
-                         : dev::fwd_h<float>(H, band, M, a, n_pad, B, E, st);
+  return dev::fwd_h<dev::dt_t>(H, band, M, a, n_pad, B, E, st);
 }
 
-hipError_t launch_banded_bwd(int dt, int n_pad, int B, int H, int E, const void* band, const void* da, void* dM,
-                             long ldm, hipStream_t st) {
-  return dt == GGNN_BF16 ? dev::bwd_h<dev::bf16s>(H, band, da, dM, ldm, n_pad, B, E, st)
-                         : dev::bwd_h<float>(H, band, da, dM, ldm, n_pad, B, E, st);
+hipError_t launch_banded_bwd(int n_pad, int B, int H, int E, const void* band, const void* da, void* dM, long ldm,
+                             hipStream_t st) {
+  return dev::bwd_h<dev::dt_t>(H, band, da, dM, ldm, n_pad, B, E, st);
 }
+}  // namespace GGNN_IMPL_NS
 
 }  // namespace ggnn

@@ -26,13 +26,14 @@ namespace dev {
 // 8 bits -> 8 elements equal to 0 or 1 (bit i -> element i).
 template <typename S> __device__ __forceinline__ frag_t<S> bits_frag(uint32_t byte);
 template <> __device__ __forceinline__ bf16x8 bits_frag<bf16s>(uint32_t byte) {
-  // byte * 0x8001 holds bit i at position i and again at i + 15, so after a
-  // shift by 2k, bit 0 is bit 2k and bit 16 is bit 2k+1; times 0x3F80 (bf16
-  // 1.0) that is the word of elements 2k and 2k+1.
+  // byte * 0x8001 holds bit i at position i and again at i + 15, so bit 2k
+  // sits at 2k and bit 2k+1 at 16 + 2k.  Masking those two and multiplying
+  // by 0x3F80 >> 2k (bf16 1.0 shifted down; exact for 2k <= 6) gives the
+  // word of elements 2k and 2k+1 without a shift.
   const uint32_t x = byte * 0x8001u;
   u32x4 w;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) w[k] = ((x >> (2 * k)) & 0x10001u) * 0x3F80u;
+  for (int k = 0; k < 4; ++k) w[k] = (x & (0x10001u << (2 * k))) * (0x3F80u >> (2 * k));
   return __builtin_bit_cast(bf16x8, w);
 }
 template <> __device__ __forceinline__ f32x8 bits_frag<float>(uint32_t byte) {
@@ -128,58 +129,78 @@ struct BitsCfg {
   static constexpr int RB = KC / 32;        // bit-row bytes per lane per chunk (= k steps per chunk)
   static constexpr int RPW = H >= 256 ? 16 : 32;   // rows per wave
   static constexpr int NTW = RPW / 16;      // 16-row tiles per wave
+  // Smallest workgroup (waves) launched; the fp32 forms with H >= 128 keep
+  // at least two waves (their one-wave forms are not built: the code
+  // generator fails on them in VGPR-only matrix-core mode).
+  static constexpr int MINW = (sizeof(S) == 4 && H >= 128 && B / RPW >= 2) ? 2 : 1;
+  // Forward, H <= 64 with the blocks staged: the transform's weight
+  // fragments are read straight from global memory (L1/L2 resident, issued
+  // at the top of each type and used at its end), so no weight staging sits
+  // in the prologue and the type loop has no barrier.
+  static constexpr bool WDIR = ALL && H <= 64;
+  static constexpr int WP = H + V;          // W^T row pitch (LDS chunks otherwise)
 };
 
 // ---------------------------------------------------------------------------
-// Fused forward.  Workgroup: RPW*WAVES rows of block row k.
-// Aggregation D[h][r]: A operand = staged X^T rows (LDS), B operand = bit
-// rows expanded in registers.  Transform D'[h_out][r]: A operand = W_e^T
-// rows (LDS, transposed on the write), B operand = the aggregation
-// accumulators themselves (accumulator-compatible k order, split hi + lo in
-// bf16 mode).  Lanes then hold four consecutive features of one node:
-// 16-byte stores of the fp32 aggregate a.
+// Fused step on a bit band, forward (REV = false) or reverse (REV = true).
+// Workgroup: RPW*WAVES rows of block row k (columns of block column k in
+// the reverse).
+//   forward:  a[k]  = sum_e (sum_s bits[e][k][s] X[k-1+s]) W_e   (+ deg_e bias_e)
+//   reverse:  dM_e[k] = sum_s bits_t[e][k][s] da[k-1+s]          (stored, dt)
+//             dX[k] = dX_in[k] + sum_e dM_e[k] W_e^T
+// Aggregation D[h][r]: A operand = staged feature rows of X (transposed on
+// the LDS write) or of da (feature-major already: plain copies), B operand =
+// bit rows expanded in registers.  Transform D'[h_out][r]: A operand = rows
+// of W_e^T (forward) or W_e (reverse), B operand = the aggregation
+// accumulators themselves (accumulator-compatible k order; forward: split hi
+// + lo in bf16 mode; reverse: the rounded dM that is stored).  Lanes then
+// hold four consecutive features of one node: 16-byte fp32 stores of a / dX.
+// WDIR: the weight fragments come straight from global memory, requested at
+// the top of type e and consumed after its aggregation; the type loop has no
+// barrier (waves drift freely and hide each other's latencies) and the bit
+// rows of the next two types are in flight while a type is computed.
+// Otherwise the weights are staged per type in LDS in 64-row chunks.
+// TG type groups (WDIR only): the workgroup has TG * WAVES waves; wave w
+// takes rows as wave w % WAVES and the types of group w / WAVES (a
+// contiguous range), so TG waves share a SIMD and overlap one another's VALU,
+// LDS and matrix work.  The groups' partial sums meet in LDS at the end (over
+// the staged blocks), added in group order.
 // ---------------------------------------------------------------------------
-template <typename S, int H, int B, int WAVES>
-__global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* __restrict__ bits,
-                                                                  const S* __restrict__ X, const S* __restrict__ W,
-                                                                  const float* __restrict__ bias,
-                                                                  float* __restrict__ a, int n_pad, int E) {
+template <typename S, int H, int B, int WAVES, bool WDIR, int TG, bool REV>
+__global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
+    const uint8_t* __restrict__ bits, const S* __restrict__ X, const S* __restrict__ W, const float* __restrict__ bias,
+    float* out, int n_pad, int E, const float* dX_in, S* __restrict__ dM, long ldm) {
   using C = BitsCfg<S, H, B>;
-  constexpr int NT = WAVES * kWave;
-  constexpr int V = C::V, KC = C::KC, VP = C::VP, RB = C::RB, NTW = C::NTW;
+  constexpr int NT = TG * WAVES * kWave;
+  constexpr int V = C::V, KC = C::KC, VP = C::VP, RB = C::RB, NTW = C::NTW, WP = C::WP;
   constexpr int MT = H / 16, HK = H / 32;
-  constexpr int WC = H < 64 ? H : 64;      // W^T rows staged at a time
-  constexpr int WP = H + V;
-  constexpr int NP = sizeof(S) == 2 ? 2 : 1;
+  constexpr int WC = WDIR ? H : (H < 64 ? H : 64);   // weight rows per chunk
+  constexpr int NP = (sizeof(S) == 2 && !REV) ? 2 : 1;
   constexpr int ROWB = B / 8;
+  static_assert(!WDIR || C::WDIR, "direct weights need the staged blocks and H <= 64");
+  static_assert(TG == 1 || WDIR, "type groups need the barrier-free loop");
+  static_assert(TG == 1 || (TG - 1) * WAVES * kWave * NTW * MT * 16 <= (int)(C::NBUF * H * VP * sizeof(S)),
+                "partial sums must fit in the staged-block space");
   __shared__ __attribute__((aligned(16))) S vt[C::NBUF][H * VP];
-  __shared__ __attribute__((aligned(16))) S wt[WC * WP];
+  __shared__ __attribute__((aligned(16))) S wt[WDIR ? 8 : WC * WP];
 
   const int nb = n_pad / B;
   constexpr int NW = C::RPW * WAVES;
   const int tiles_per_row = B / NW;
   const int t = xcd_swizzle(blockIdx.x, gridDim.x);
   const int k = t / tiles_per_row;
-  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int tid = threadIdx.x, wave = (tid / kWave) % WAVES, lane = tid % kWave;
+  const int tg = tid / (WAVES * kWave);
   const int q = lane % 16, g = lane / 16;
   const int rw = (t % tiles_per_row) * NW + C::RPW * wave;   // first row of this wave
   const int s_lo = (k == 0) ? 1 : 0;
   const int s_hi = (k == nb - 1) ? 1 : 2;
+  const int e_lo = tg * E / TG, e_hi = (tg + 1) * E / TG;     // this wave's types
 
-  if constexpr (C::ALL) {
-    for (int s = s_lo; s <= s_hi; ++s) stage_nodes_T<S, H, KC, VP, NT>(vt[s], X, (k - 1 + s) * B, tid);
-    __syncthreads();
-  }
-  f32x4 acc[NTW][MT];
-#pragma unroll
-  for (int n = 0; n < NTW; ++n)
-#pragma unroll
-    for (int m = 0; m < MT; ++m) acc[n][m] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // In ALL mode a chunk is a whole block: the bit rows of the next edge type
-  // are loaded while the current one is computed (the loads would otherwise
-  // sit on the critical path of every type).
-  RowBytes<RB> nxt[3][NTW];
+  // The bit rows of the first types are requested before the staging, so
+  // their latency overlaps it; later types' rows are loaded while the current
+  // one is computed (one type ahead, two with WDIR).
+  RowBytes<RB> nx1[3][NTW], nx2[3][NTW];
   auto load_type = [&](int e, RowBytes<RB> (&dst)[3][NTW]) __attribute__((always_inline)) {
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
@@ -189,35 +210,159 @@ __global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* 
       for (int n = 0; n < NTW; ++n) dst[s][n].load(brow + (size_t)16 * n * ROWB);
     }
   };
-  if constexpr (C::ALL) load_type(0, nxt);
-  // W_e^T chunks: one chunk of WC output rows is H * WC / V 16-byte units.
-  constexpr int WU = (H * (WC / V) + NT - 1) / NT;
+  if constexpr (C::ALL) {
+    if (e_lo < e_hi) load_type(e_lo, nx1);
+  }
+  if constexpr (WDIR) {
+    if (e_lo + 1 < e_hi) load_type(e_lo + 1, nx2);
+  }
+
+  // Staging of the three blocks as feature rows, vt[s][f * VP + c] =
+  // node (k-1+s)*B + c, feature f.  Forward: V x V tiles of node-major X,
+  // transposed on the LDS write (consecutive lanes take tiles consecutive
+  // along the destination row: conflict-free 16-byte stores, loads of whole
+  // 128-byte lines).  Reverse: plain 16-byte copies of feature-major da.
+  // Each thread issues the loads of up to PB units before its writes.
+  if constexpr (C::ALL) {
+    if constexpr (!REV) {
+      constexpr int XT = (KC / V) * (H / V);       // tiles per block
+      constexpr int PB = 2;
+      const int total = (s_hi - s_lo + 1) * XT;
+      for (int base = 0; base < total; base += PB * NT) {
+        u32x4 r[PB][V];
+#pragma unroll
+        for (int u = 0; u < PB; ++u) {
+          const int lin = base + u * NT + tid;
+          if (lin < total) {
+            const int slot = s_lo + lin / XT, rem = lin % XT;
+            const int cq = rem % (KC / V), fq = rem / (KC / V);
+            tile_load<S>(r[u], X + (size_t)((k - 1 + slot) * B + V * cq) * H + V * fq, H);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < PB; ++u) {
+          const int lin = base + u * NT + tid;
+          if (lin < total) {
+            const int slot = s_lo + lin / XT, rem = lin % XT;
+            const int cq = rem % (KC / V), fq = rem / (KC / V);
+            tile_store_T<S, VP>(&vt[slot][(V * fq) * VP + V * cq], r[u]);
+          }
+        }
+      }
+    } else {
+      constexpr int UPB = H * (KC / V);            // 16-byte units per block
+      constexpr int PB = 4;
+      const int total = (s_hi - s_lo + 1) * UPB;
+      for (int base = 0; base < total; base += PB * NT) {
+        u32x4 r[PB];
+#pragma unroll
+        for (int u = 0; u < PB; ++u) {
+          const int lin = base + u * NT + tid;
+          if (lin < total) {
+            const int slot = s_lo + lin / UPB, rem = lin % UPB;
+            const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
+            r[u] = *reinterpret_cast<const u32x4*>(X + (size_t)h * n_pad + (k - 1 + slot) * B + c);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < PB; ++u) {
+          const int lin = base + u * NT + tid;
+          if (lin < total) {
+            const int slot = s_lo + lin / UPB, rem = lin % UPB;
+            const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
+            *reinterpret_cast<u32x4*>(&vt[slot][h * VP + c]) = r[u];
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  f32x4 acc[NTW][MT];
+#pragma unroll
+  for (int n = 0; n < NTW; ++n)
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[n][m] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // WDIR weight fragments: A row o = 16 mo + q, k values h in the
+  // accumulator-compatible order 32 kk + 4 g + {0..3}, 32 kk + 16 + 4 g + {0..3}.
+  // Forward: element (o, h) is W[e][h][o] (a column of W: 2-byte gathers);
+  // reverse: it is W[e][o][h] (a row: two 8-byte loads).
+  frag_t<S> wf[WDIR ? H / 16 : 1][WDIR ? HK : 1];
+  auto load_wfrags = [&](int e) __attribute__((always_inline)) {
+    if constexpr (WDIR) {
+      const S* we = W + (size_t)e * H * H;
+#pragma unroll
+      for (int mo = 0; mo < H / 16; ++mo)
+#pragma unroll
+        for (int kk = 0; kk < HK; ++kk) {
+          if constexpr (REV) {
+            const S* p = we + (size_t)(16 * mo + q) * H + 32 * kk + 4 * g;
+            wf[mo][kk] = load4x2(p, p + 16);
+          } else {
+            const S* p = we + (size_t)(32 * kk + 4 * g) * H + 16 * mo + q;
+            if constexpr (sizeof(S) == 2) {
+              u32x4 w;
+#pragma unroll
+              for (int d = 0; d < 4; ++d) {
+                const int h0 = (d < 2 ? 0 : 16) + 2 * (d % 2);
+                w[d] = static_cast<uint32_t>(p[(size_t)h0 * H]) |
+                       (static_cast<uint32_t>(p[(size_t)(h0 + 1) * H]) << 16);
+              }
+              wf[mo][kk] = __builtin_bit_cast(bf16x8, w);
+            } else {
+#pragma unroll
+              for (int x = 0; x < 8; ++x) wf[mo][kk][x] = p[(size_t)((x < 4 ? 0 : 16) + x % 4) * H];
+            }
+          }
+        }
+    }
+  };
+
+  // Per-type weight chunks in LDS (not WDIR): chunk rows o in [oc, oc + WC),
+  // wt[o][h] = W[e][h][oc + o] (forward, transposed on the write) or
+  // W[e][oc + o][h] (reverse, plain copies); H * WC / V 16-byte units,
+  // prefetched into registers during the aggregation.
+  constexpr int WU = WDIR ? 1 : (H * (WC / V) + NT - 1) / NT;
   u32x4 wreg[WU];
   auto load_w = [&](int e, int oc) __attribute__((always_inline)) {
-    const S* wsrc = W + (size_t)e * H * H + oc;
 #pragma unroll
     for (int u = 0; u < WU; ++u) {
       const int lin = u * NT + tid;
       if ((H * (WC / V)) % NT == 0 || lin < H * (WC / V)) {
-        const int h = lin / (WC / V), o8 = (lin % (WC / V)) * V;
-        wreg[u] = *reinterpret_cast<const u32x4*>(wsrc + (size_t)h * H + o8);
+        if constexpr (REV) {
+          const int o = lin / (H / V), h8 = (lin % (H / V)) * V;
+          wreg[u] = *reinterpret_cast<const u32x4*>(W + (size_t)e * H * H + (size_t)(oc + o) * H + h8);
+        } else {
+          const int h = lin / (WC / V), o8 = (lin % (WC / V)) * V;
+          wreg[u] = *reinterpret_cast<const u32x4*>(W + (size_t)e * H * H + (size_t)h * H + oc + o8);
+        }
       }
     }
   };
-  auto store_w = [&]() __attribute__((always_inline)) {   // wt[o][h] = W[e][h][oc + o]
+  auto store_w = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < WU; ++u) {
       const int lin = u * NT + tid;
       if ((H * (WC / V)) % NT == 0 || lin < H * (WC / V)) {
-        const int h = lin / (WC / V), o8 = (lin % (WC / V)) * V;
-        const S* pw = reinterpret_cast<const S*>(&wreg[u]);
+        if constexpr (REV) {
+          const int o = lin / (H / V), h8 = (lin % (H / V)) * V;
+          *reinterpret_cast<u32x4*>(&wt[o * WP + h8]) = wreg[u];
+        } else {
+          const int h = lin / (WC / V), o8 = (lin % (WC / V)) * V;
+          const S* pw = reinterpret_cast<const S*>(&wreg[u]);
 #pragma unroll
-        for (int x = 0; x < V; ++x) wt[(o8 + x) * WP + h] = pw[x];
+          for (int x = 0; x < V; ++x) wt[(o8 + x) * WP + h] = pw[x];
+        }
       }
     }
   };
-  for (int e = 0; e < E; ++e) {
-    load_w(e, 0);   // in flight during the aggregation below
+  for (int e = e_lo; e < e_hi; ++e) {
+    if constexpr (WDIR) {
+      load_wfrags(e);      // consumed after the aggregation below
+    } else {
+      load_w(e, 0);        // in flight during the aggregation below
+    }
     f32x4 pre[NTW][MT];
 #pragma unroll
     for (int n = 0; n < NTW; ++n)
@@ -231,8 +376,15 @@ __global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* 
 #pragma unroll
       for (int s = 0; s < 3; ++s)
 #pragma unroll
-        for (int n = 0; n < NTW; ++n) cur[s][n] = nxt[s][n];
-      if (e + 1 < E) load_type(e + 1, nxt);
+        for (int n = 0; n < NTW; ++n) {
+          cur[s][n] = nx1[s][n];
+          if constexpr (WDIR) nx1[s][n] = nx2[s][n];
+        }
+      if constexpr (WDIR) {
+        if (e + 2 < e_hi) load_type(e + 2, nx2);
+      } else {
+        if (e + 1 < e_hi) load_type(e + 1, nx1);
+      }
     }
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
@@ -241,7 +393,11 @@ __global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* 
       for (int c0 = 0; c0 < B; c0 += KC) {
         if constexpr (!C::ALL) {
           __syncthreads();
-          stage_nodes_T<S, H, KC, VP, NT>(vt[0], X, (k - 1 + s) * B + c0, tid);
+          if constexpr (REV) {
+            stage_cols<S, H, KC, VP, NT>(vt[0], X, n_pad, (k - 1 + s) * B + c0, tid);
+          } else {
+            stage_nodes_T<S, H, KC, VP, NT>(vt[0], X, (k - 1 + s) * B + c0, tid);
+          }
           __syncthreads();
         }
         const S* v = vt[C::ALL ? s : 0];
@@ -253,7 +409,7 @@ __global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* 
           } else {
             rb[n].load(brow + (size_t)16 * n * ROWB + (c0 + g * (KC / 4)) / 8);
           }
-          if (bias) deg[n] += rb[n].popc();
+          if (!REV && bias) deg[n] += rb[n].popc();
         }
 #pragma unroll
         for (int kk = 0; kk < RB; ++kk) {
@@ -287,24 +443,55 @@ __global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* 
           pf[0][n][kk] = pack8<S>(v8);
         }
       }
-    for (int oc = 0; oc < H; oc += WC) {
-      __syncthreads();
-      store_w();
-      __syncthreads();
-      if (oc + WC < H) load_w(e, oc + WC);   // next chunk, in flight during this one
+    if constexpr (REV) {
+      // dM_e rows of this wave's nodes (node-major, rows of type e start at
+      // row e * ldm): features 32kk + 4g + {0..3} and 32kk + 16 + 4g + {0..3}.
 #pragma unroll
-      for (int mo = 0; mo < WC / 16; ++mo)
+      for (int n = 0; n < NTW; ++n) {
+        S* row = dM + ((size_t)e * ldm + k * B + rw + 16 * n + q) * H + 4 * g;
 #pragma unroll
         for (int kk = 0; kk < HK; ++kk) {
-          const S* wr = &wt[(16 * mo + q) * WP + 32 * kk + 4 * g];
-          const frag_t<S> af = load4x2(wr, wr + 16);
+          if constexpr (sizeof(S) == 2) {
+            const u32x4 w = __builtin_bit_cast(u32x4, pf[0][n][kk]);
+            *reinterpret_cast<u32x2*>(row + 32 * kk) = u32x2{w[0], w[1]};
+            *reinterpret_cast<u32x2*>(row + 32 * kk + 16) = u32x2{w[2], w[3]};
+          } else {
+            const f32x8 w = pf[0][n][kk];
+            *reinterpret_cast<f32x4*>(row + 32 * kk) = f32x4{w[0], w[1], w[2], w[3]};
+            *reinterpret_cast<f32x4*>(row + 32 * kk + 16) = f32x4{w[4], w[5], w[6], w[7]};
+          }
+        }
+      }
+    }
+    if constexpr (WDIR) {
+#pragma unroll
+      for (int mo = 0; mo < H / 16; ++mo)
+#pragma unroll
+        for (int kk = 0; kk < HK; ++kk)
 #pragma unroll
           for (int n = 0; n < NTW; ++n)
 #pragma unroll
-            for (int part = 0; part < NP; ++part) mma(acc[n][oc / 16 + mo], af, pf[part][n][kk]);
-        }
+            for (int part = 0; part < NP; ++part) mma(acc[n][mo], wf[mo][kk], pf[part][n][kk]);
+    } else {
+      for (int oc = 0; oc < H; oc += WC) {
+        __syncthreads();
+        store_w();
+        __syncthreads();
+        if (oc + WC < H) load_w(e, oc + WC);   // next chunk, in flight during this one
+#pragma unroll
+        for (int mo = 0; mo < WC / 16; ++mo)
+#pragma unroll
+          for (int kk = 0; kk < HK; ++kk) {
+            const S* wr = &wt[(16 * mo + q) * WP + 32 * kk + 4 * g];
+            const frag_t<S> af = load4x2(wr, wr + 16);
+#pragma unroll
+            for (int n = 0; n < NTW; ++n)
+#pragma unroll
+              for (int part = 0; part < NP; ++part) mma(acc[n][oc / 16 + mo], af, pf[part][n][kk]);
+          }
+      }
     }
-    if (bias) {
+    if (!REV && bias) {
 #pragma unroll
       for (int n = 0; n < NTW; ++n) {
         int d = deg[n];
@@ -318,11 +505,42 @@ __global__ __launch_bounds__(WAVES * kWave) void step_fwd_kernel(const uint8_t* 
       }
     }
   }
+  if constexpr (TG > 1) {
+    // Groups 1.. leave their sums in LDS (over the staged blocks, once every
+    // wave is done reading them); group 0 adds them in group order.
+    f32x4* red = reinterpret_cast<f32x4*>(&vt[0][0]);
+    __syncthreads();
+    if (tg > 0) {
+#pragma unroll
+      for (int n = 0; n < NTW; ++n)
+#pragma unroll
+        for (int m = 0; m < MT; ++m) red[((((tg - 1) * WAVES + wave) * NTW + n) * MT + m) * kWave + lane] = acc[n][m];
+    }
+    __syncthreads();
+    if (tg > 0) return;
+#pragma unroll
+    for (int gi = 1; gi < TG; ++gi)
+#pragma unroll
+      for (int n = 0; n < NTW; ++n)
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+          const f32x4 r = red[((((gi - 1) * WAVES + wave) * NTW + n) * MT + m) * kWave + lane];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[n][m][j] += r[j];
+        }
+  }
 #pragma unroll
   for (int n = 0; n < NTW; ++n) {
-    float* out = a + (size_t)(k * B + rw + 16 * n + q) * H + 4 * g;
+    const size_t row = (size_t)(k * B + rw + 16 * n + q) * H + 4 * g;
 #pragma unroll
-    for (int m = 0; m < MT; ++m) store4(out + 16 * m, acc[n][m][0], acc[n][m][1], acc[n][m][2], acc[n][m][3]);
+    for (int m = 0; m < MT; ++m) {
+      f32x4 v = acc[n][m];
+      if (REV && dX_in) {
+        const f32x4 b = *reinterpret_cast<const f32x4*>(dX_in + row + 16 * m);
+        v = f32x4{b[0] + v[0], b[1] + v[1], b[2] + v[2], b[3] + v[3]};
+      }
+      store4(out + row + 16 * m, v[0], v[1], v[2], v[3]);
+    }
   }
 }
 
@@ -340,7 +558,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
                                                                   int n_pad, int E, int groups, long ldm) {
   using C = BitsCfg<S, H, B>;
   constexpr int NT = WAVES * kWave;
-  constexpr int KC = C::KC, VP = C::VP, RB = C::RB, NTW = C::NTW;
+  constexpr int V = C::V, KC = C::KC, VP = C::VP, RB = C::RB, NTW = C::NTW;
   constexpr int NTL = H / 16;
   constexpr int ROWB = B / 8;
   __shared__ __attribute__((aligned(16))) S vt[C::NBUF][H * VP];
@@ -361,7 +579,32 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
   const int s_hi = (j == nb - 1) ? 1 : 2;
 
   if constexpr (C::ALL) {
-    for (int s = s_lo; s <= s_hi; ++s) stage_cols<S, H, KC, VP, NT>(vt[s], da, n_pad, (j - 1 + s) * B, tid);
+    // The three da blocks, plain 16-byte copies; each thread issues up to
+    // four loads before its LDS writes.
+    constexpr int UPB = H * (KC / V);            // units per block
+    constexpr int PB = 4;
+    const int total = (s_hi - s_lo + 1) * UPB;
+    for (int base = 0; base < total; base += PB * NT) {
+      u32x4 r[PB];
+#pragma unroll
+      for (int u = 0; u < PB; ++u) {
+        const int lin = base + u * NT + tid;
+        if (lin < total) {
+          const int slot = s_lo + lin / UPB, rem = lin % UPB;
+          const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
+          r[u] = *reinterpret_cast<const u32x4*>(da + (size_t)h * n_pad + (j - 1 + slot) * B + c);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < PB; ++u) {
+        const int lin = base + u * NT + tid;
+        if (lin < total) {
+          const int slot = s_lo + lin / UPB, rem = lin % UPB;
+          const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
+          *reinterpret_cast<u32x4*>(&vt[slot][h * VP + c]) = r[u];
+        }
+      }
+    }
     __syncthreads();
   }
   RowBytes<RB> nxt[3][NTW];
@@ -442,39 +685,72 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
 #ifndef GGNN_BITS_BWD_MIN_BLOCKS
 #define GGNN_BITS_BWD_MIN_BLOCKS 64
 #endif
+#ifndef GGNN_BITS_TG2_MAX_BLOCKS
+#define GGNN_BITS_TG2_MAX_BLOCKS 512
+#endif
 #ifndef GGNN_BITS_BWD_WAVES
 #define GGNN_BITS_BWD_WAVES 4096
 #endif
 
 namespace {
+// One launch of a bit-band kernel.  mode 0: fused forward step; 1: fused
+// reverse step (dM node-major, dX); 2: reverse product only (dM feature-major).
+struct BitsArgs {
+  int mode;
+  const void* bits;
+  const void* V;        // X (forward) or da (reverse)
+  const void* W;
+  const float* bias;
+  void* out;            // a, dX_out or dM
+  const float* dX_in;
+  void* dM;             // mode 1
+  long ldm;
+  int n_pad, E;
+};
+
 template <typename S, int H, int B>
-hipError_t bits_launch(bool fwd, const void* bits, const void* V, const void* W, const float* bias, void* out,
-                       long ldm, int n_pad, int E, hipStream_t st) {
+hipError_t bits_launch(const BitsArgs& A, hipStream_t st) {
   using C = dev::BitsCfg<S, H, B>;
-  const int nb = n_pad / B;
+  const int nb = A.n_pad / B;
+  const bool fused = A.mode != 2;
   int waves = B / C::RPW < 4 ? B / C::RPW : 4;
-  const long min_blocks = fwd ? GGNN_BITS_FWD_MIN_BLOCKS : GGNN_BITS_BWD_MIN_BLOCKS;
-  while (waves > 1 && (long)nb * (B / (C::RPW * waves)) < min_blocks) waves /= 2;
+  const long min_blocks = fused ? GGNN_BITS_FWD_MIN_BLOCKS : GGNN_BITS_BWD_MIN_BLOCKS;
+  while (waves > C::MINW && (long)nb * (B / (C::RPW * waves)) < min_blocks) waves /= 2;
   const int tiles = nb * (B / (C::RPW * waves));
-  // The reverse pass writes one output per edge type, so types can be split
-  // over workgroups freely: enough groups for about GGNN_BITS_BWD_WAVES waves.
+  // The plain reverse product writes one output per edge type, so types can
+  // be split over workgroups freely: enough groups for about
+  // GGNN_BITS_BWD_WAVES waves.
   int groups = 1;
-  if (!fwd) {
+  if (!fused) {
     const long want = (GGNN_BITS_BWD_WAVES + (long)tiles * waves - 1) / ((long)tiles * waves);
-    groups = (int)(want < 1 ? 1 : (want > E ? E : want));
+    groups = (int)(want < 1 ? 1 : (want > A.E ? A.E : want));
   }
   const int blocks = tiles * groups;
-  const uint8_t* bp = static_cast<const uint8_t*>(bits);
-  const S* vp = static_cast<const S*>(V);
+  // Fused steps: two type groups per workgroup (two waves per SIMD) when the
+  // grid alone does not give every SIMD several waves.
+  const bool tg2 = C::WDIR && blocks <= GGNN_BITS_TG2_MAX_BLOCKS;
+  const uint8_t* bp = static_cast<const uint8_t*>(A.bits);
+  const S* vp = static_cast<const S*>(A.V);
+  const S* wp = static_cast<const S*>(A.W);
+  float* op = static_cast<float*>(A.out);
+  S* dmp = static_cast<S*>(A.dM);
+#define GGNN_STEP(WV, TGN, REVB)                                                                              \
+  hipLaunchKernelGGL((dev::step_bits_kernel<S, H, B, WV, C::WDIR, TGN, REVB>), dim3(blocks), dim3(TGN * WV * 64), \
+                     0, st, bp, vp, wp, A.bias, op, A.n_pad, A.E, A.dX_in, dmp, A.ldm)
 #define GGNN_BITS_CASE(WV)                                                                                   \
   case WV:                                                                                                   \
-    if constexpr (B / C::RPW >= WV) {                                                                        \
-      if (fwd)                                                                                               \
-        hipLaunchKernelGGL((dev::step_fwd_kernel<S, H, B, WV>), dim3(blocks), dim3(WV * 64), 0, st, bp, vp,  \
-                           static_cast<const S*>(W), bias, static_cast<float*>(out), n_pad, E);              \
+    if constexpr (B / C::RPW >= WV && WV >= C::MINW) {                                                       \
+      if (A.mode == 0 && tg2)                                                                                \
+        GGNN_STEP(WV, (C::WDIR ? 2 : 1), false);                                                             \
+      else if (A.mode == 0)                                                                                  \
+        GGNN_STEP(WV, 1, false);                                                                             \
+      else if (A.mode == 1 && tg2)                                                                           \
+        GGNN_STEP(WV, (C::WDIR ? 2 : 1), true);                                                              \
+      else if (A.mode == 1)                                                                                  \
+        GGNN_STEP(WV, 1, true);                                                                              \
       else                                                                                                   \
         hipLaunchKernelGGL((dev::bits_bwd_kernel<S, H, B, WV>), dim3(blocks), dim3(WV * 64), 0, st, bp, vp,  \
-                           static_cast<S*>(out), n_pad, E, groups, ldm);                                     \
+                           static_cast<S*>(A.out), A.n_pad, A.E, groups, A.ldm);                             \
     }                                                                                                        \
     break;
   switch (waves) {
@@ -483,45 +759,50 @@ hipError_t bits_launch(bool fwd, const void* bits, const void* V, const void* W,
     GGNN_BITS_CASE(1)
   }
 #undef GGNN_BITS_CASE
+#undef GGNN_STEP
   return hipGetLastError();
 }
 
 template <typename S, int H>
-hipError_t bits_h(int B, bool fwd, const void* bits, const void* V, const void* W, const float* bias, void* out,
-                  long ldm, int n_pad, int E, hipStream_t st) {
+hipError_t bits_h(int B, const BitsArgs& A, hipStream_t st) {
   switch (B) {
-    case 32: return bits_launch<S, H, 32>(fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
-    case 64: return bits_launch<S, H, 64>(fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
-    case 128: return bits_launch<S, H, 128>(fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
-    case 256: return bits_launch<S, H, 256>(fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
-    case 512: return bits_launch<S, H, 512>(fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
+    case 32: return bits_launch<S, H, 32>(A, st);
+    case 64: return bits_launch<S, H, 64>(A, st);
+    case 128: return bits_launch<S, H, 128>(A, st);
+    case 256: return bits_launch<S, H, 256>(A, st);
+    case 512: return bits_launch<S, H, 512>(A, st);
   }
   return hipErrorInvalidValue;
 }
 
 template <typename S>
-hipError_t bits_t(int H, int B, bool fwd, const void* bits, const void* V, const void* W, const float* bias,
-                  void* out, long ldm, int n_pad, int E, hipStream_t st) {
+hipError_t bits_t(int H, int B, const BitsArgs& A, hipStream_t st) {
   switch (H) {
-    case 32: return bits_h<S, 32>(B, fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
-    case 64: return bits_h<S, 64>(B, fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
-    case 128: return bits_h<S, 128>(B, fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
-    case 256: return bits_h<S, 256>(B, fwd, bits, V, W, bias, out, ldm, n_pad, E, st);
+    case 32: return bits_h<S, 32>(B, A, st);
+    case 64: return bits_h<S, 64>(B, A, st);
+    case 128: return bits_h<S, 128>(B, A, st);
+    case 256: return bits_h<S, 256>(B, A, st);
   }
   return hipErrorInvalidValue;
 }
 }  // namespace
 
-hipError_t launch_step_fwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits, const void* X,
-                                const void* W, const float* bias, float* a, hipStream_t st) {
-  return dt == GGNN_BF16 ? bits_t<dev::bf16s>(H, B, true, bits, X, W, bias, a, 0, n_pad, E, st)
-                         : bits_t<float>(H, B, true, bits, X, W, bias, a, 0, n_pad, E, st);
+namespace GGNN_IMPL_NS {
+hipError_t launch_step_fwd_bits(int n_pad, int B, int H, int E, const void* bits, const void* X, const void* W,
+                                const float* bias, float* a, hipStream_t st) {
+  return bits_t<dev::dt_t>(H, B, BitsArgs{0, bits, X, W, bias, a, nullptr, nullptr, 0, n_pad, E}, st);
 }
 
-hipError_t launch_banded_bwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits_t_, const void* da,
-                                  void* dM, long ldm, hipStream_t st) {
-  return dt == GGNN_BF16 ? bits_t<dev::bf16s>(H, B, false, bits_t_, da, nullptr, nullptr, dM, ldm, n_pad, E, st)
-                         : bits_t<float>(H, B, false, bits_t_, da, nullptr, nullptr, dM, ldm, n_pad, E, st);
+hipError_t launch_step_bwd_bits(int n_pad, int B, int H, int E, const void* bits_t_, const void* da, const void* W,
+                                const float* dX_in, float* dX_out, void* dM, long ldm, hipStream_t st) {
+  return bits_t<dev::dt_t>(H, B, BitsArgs{1, bits_t_, da, W, nullptr, dX_out, dX_in, dM, ldm, n_pad, E}, st);
 }
+
+hipError_t launch_banded_bwd_bits(int n_pad, int B, int H, int E, const void* bits_t_, const void* da, void* dM,
+                                  long ldm, hipStream_t st) {
+  return bits_t<dev::dt_t>(H, B, BitsArgs{2, bits_t_, da, nullptr, nullptr, dM, nullptr, nullptr, ldm, n_pad, E},
+                           st);
+}
+}  // namespace GGNN_IMPL_NS
 
 }  // namespace ggnn

@@ -181,6 +181,24 @@ ggnn_status ggnn_banded_propagate_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t
                        "banded_propagate_bits_bwd");
 }
 
+ggnn_status ggnn_banded_step_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
+                                      const void* bits_t, const void* da, const void* W, const float* dX_in,
+                                      float* dX_out, void* dM, int64_t ldm, void* stream) {
+  clear_error();
+  ggnn_status st = check_banded(dt, n_pad, B, H, E);
+  if (st != GGNN_OK) return st;
+  CHECK_PTR(bits_t, "bits_t");
+  CHECK_PTR(da, "da");
+  CHECK_PTR(W, "W");
+  CHECK_OPT_PTR(dX_in, "dX_in");
+  CHECK_PTR(dX_out, "dX_out");
+  CHECK_PTR(dM, "dM");
+  GGNN_CHECK_ARG(ldm >= n_pad, "ldm=%lld must be at least n_pad=%d", (long long)ldm, n_pad);
+  return device_status(
+      launch_step_bwd_bits(dt, n_pad, B, H, E, bits_t, da, W, dX_in, dX_out, dM, (long)ldm, as_stream(stream)),
+      "banded_step_bits_bwd");
+}
+
 size_t ggnn_msg_transform_bwd_workspace_bytes(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E) {
   if (!supported_dtype(dt) || n_pad <= 0 || n_pad % 32 != 0 || !supported_H(H) || E < 1 || E > 64) return 0;
   return transform_wgrad_workspace(n_pad, H, E);
@@ -314,18 +332,25 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
     char* dMt = static_cast<char*>(gr->dM) + (size_t)t * m->n_pad * es;
     hipError_t err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xt, sv, m->Wi, m->U, gr->da, gr->dh,
                                           ght, s);
-    if (err == hipSuccess)
-      err = m->band_format == GGNN_BAND_BITS
-                ? launch_banded_bwd_bits(m->dtype, m->n_pad, m->B, m->H, m->E, m->band_t, gr->da, dMt, K, s)
-                : launch_banded_bwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, gr->da, dMt, K, s);
-    if (err == hipSuccess)
-      err = launch_transform_bwd_dx(m->dtype, m->n_pad, m->H, m->E, m->W, dMt, K, gr->dh, gr->dX, s);
+    if (err != hipSuccess) return device_status(err, "backward");
+    if (m->band_format == GGNN_BAND_BITS) {
+      // dM node-major: step t in rows [t*n_pad, (t+1)*n_pad) of each type.
+      char* dMr = static_cast<char*>(gr->dM) + (size_t)t * m->n_pad * m->H * es;
+      err = launch_step_bwd_bits(m->dtype, m->n_pad, m->B, m->H, m->E, m->band_t, gr->da, m->W, gr->dh, gr->dX,
+                                 dMr, K, s);
+    } else {
+      err = launch_banded_bwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, gr->da, dMt, K, s);
+      if (err == hipSuccess)
+        err = launch_transform_bwd_dx(m->dtype, m->n_pad, m->H, m->E, m->W, dMt, K, gr->dh, gr->dX, s);
+    }
     if (err != hipSuccess) return device_status(err, "backward");
   }
   hipError_t err = launch_gru_wgrad(m->dtype, K, m->H, act->a, act->X, act->saved, ghat, gr->dWi, gr->dU, gr->db,
                                     ws + L.gru_part, s);
   if (err == hipSuccess)
-    err = launch_transform_wgrad(m->dtype, K, m->H, m->E, act->X, gr->dM, K, gr->dW, dbias, ws + L.tr_part, s);
+    err = m->band_format == GGNN_BAND_BITS
+              ? launch_transform_wgrad_nm(m->dtype, K, m->H, m->E, act->X, gr->dM, K, gr->dW, dbias, ws + L.tr_part, s)
+              : launch_transform_wgrad(m->dtype, K, m->H, m->E, act->X, gr->dM, K, gr->dW, dbias, ws + L.tr_part, s);
   return device_status(err, "backward");
 }
 

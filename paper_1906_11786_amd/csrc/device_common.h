@@ -16,6 +16,18 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+// Each kernel source is compiled twice: GGNN_DT_BF16=1 builds its bf16
+// kernels (matrix-core results kept in VGPRs), GGNN_DT_BF16=0 its fp32 ones.
+// The launchers of one build live in namespace ggnn::GGNN_IMPL_NS.
+#ifndef GGNN_DT_BF16
+#error "compile with -DGGNN_DT_BF16=1 (bf16 kernels) or -DGGNN_DT_BF16=0 (fp32 kernels)"
+#endif
+#if GGNN_DT_BF16
+#define GGNN_IMPL_NS impl_bf16
+#else
+#define GGNN_IMPL_NS impl_f32
+#endif
+
 namespace ggnn {
 namespace dev {
 
@@ -25,6 +37,11 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint16_t bf16s;  // bf16 storage word
+#if GGNN_DT_BF16
+typedef bf16s dt_t;      // storage type of this build
+#else
+typedef float dt_t;
+#endif
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
@@ -162,6 +179,33 @@ __device__ __forceinline__ void split8(const float* v, bf16x8& hi, bf16x8& lo) {
   }
   hi = __builtin_bit_cast(bf16x8, h);
   lo = __builtin_bit_cast(bf16x8, l);
+}
+
+// A V x V tile (V = 16 / sizeof(S): 8 x 8 bf16 or 4 x 4 fp32) moved from
+// global memory to LDS transposed: V row loads of 16 bytes, a transpose in
+// registers (v_perm_b32 on 16-bit halves for bf16), V 16-byte LDS stores.
+//   tile_load:    r[i] = src[i * ss .. i * ss + V)
+//   tile_store_T: dst[x * P + i] = r[i][x]          (dst, P 16-byte aligned)
+template <typename S>
+__device__ __forceinline__ void tile_load(u32x4 (&r)[16 / sizeof(S)], const S* src, long ss) {
+#pragma unroll
+  for (int i = 0; i < (int)(16 / sizeof(S)); ++i) r[i] = *reinterpret_cast<const u32x4*>(src + i * ss);
+}
+template <typename S, int P>
+__device__ __forceinline__ void tile_store_T(S* dst, const u32x4 (&r)[16 / sizeof(S)]) {
+  if constexpr (sizeof(S) == 2) {
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      const uint32_t sel = (x & 1) ? 0x07060302u : 0x05040100u;   // high or low halves of r[2j], r[2j+1]
+      u32x4 o;
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) o[jj] = __builtin_amdgcn_perm(r[2 * jj + 1][x / 2], r[2 * jj][x / 2], sel);
+      *reinterpret_cast<u32x4*>(dst + x * P) = o;
+    }
+  } else {
+#pragma unroll
+    for (int x = 0; x < 4; ++x) *reinterpret_cast<u32x4*>(dst + x * P) = u32x4{r[0][x], r[1][x], r[2][x], r[3][x]};
+  }
 }
 
 // 16-byte vector copy unit (8 bf16 or 4 fp32 elements).

@@ -520,6 +520,7 @@ hipError_t gru_wgrad_t(long K, int H, const float* a, const void* h, const void*
 #undef GGNN_GRU_SWITCH
 }  // namespace
 
+#if GGNN_DT_BF16   // dtype-independent helpers: built once
 size_t ghat_bytes(int dt, long rows, int H) {
   size_t b = (size_t)rows * 3 * H * (dt == GGNN_BF16 ? 2 : 4);
   return (b + 255) / 256 * 256;
@@ -534,24 +535,6 @@ size_t gru_bwd_workspace(int dt, int n_pad, int H) {
   return ghat_bytes(dt, n_pad, H) + gru_wgrad_workspace(n_pad, H);
 }
 
-hipError_t launch_gru_fwd(int dt, int n_pad, int H, const float* a, const void* h, const void* Wi, const void* U,
-                          const float* b, void* h_out, void* saved, hipStream_t st) {
-  return dt == GGNN_BF16 ? gru_fwd_t<dev::bf16s>(n_pad, H, a, h, Wi, U, b, h_out, saved, st)
-                         : gru_fwd_t<float>(n_pad, H, a, h, Wi, U, b, h_out, saved, st);
-}
-
-hipError_t launch_gru_bwd_nodes(int dt, int n_pad, int H, const float* dh_out, const void* h, const void* saved,
-                                const void* Wi, const void* U, void* da, float* dh, void* ghat, hipStream_t st) {
-  return dt == GGNN_BF16 ? gru_bwd_nodes_t<dev::bf16s>(n_pad, H, dh_out, h, saved, Wi, U, da, dh, ghat, st)
-                         : gru_bwd_nodes_t<float>(n_pad, H, dh_out, h, saved, Wi, U, da, dh, ghat, st);
-}
-
-hipError_t launch_gru_wgrad(int dt, long K, int H, const float* a, const void* h, const void* saved, const void* ghat,
-                            float* dWi, float* dU, float* db, void* ws, hipStream_t st) {
-  return dt == GGNN_BF16 ? gru_wgrad_t<dev::bf16s>(K, H, a, h, saved, ghat, dWi, dU, db, ws, st)
-                         : gru_wgrad_t<float>(K, H, a, h, saved, ghat, dWi, dU, db, ws, st);
-}
-
 hipError_t launch_gru_bwd(int dt, int n_pad, int H, const float* dh_out, const float* a, const void* h,
                           const void* saved, const void* Wi, const void* U, void* da, float* dh, float* dWi,
                           float* dU, float* db, void* ws, hipStream_t st) {
@@ -561,5 +544,23 @@ hipError_t launch_gru_bwd(int dt, int n_pad, int H, const float* dh_out, const f
   if (err != hipSuccess) return err;
   return launch_gru_wgrad(dt, n_pad, H, a, h, saved, ghat, dWi, dU, db, part, st);
 }
+#endif
+
+namespace GGNN_IMPL_NS {
+hipError_t launch_gru_fwd(int n_pad, int H, const float* a, const void* h, const void* Wi, const void* U,
+                          const float* b, void* h_out, void* saved, hipStream_t st) {
+  return gru_fwd_t<dev::dt_t>(n_pad, H, a, h, Wi, U, b, h_out, saved, st);
+}
+
+hipError_t launch_gru_bwd_nodes(int n_pad, int H, const float* dh_out, const void* h, const void* saved,
+                                const void* Wi, const void* U, void* da, float* dh, void* ghat, hipStream_t st) {
+  return gru_bwd_nodes_t<dev::dt_t>(n_pad, H, dh_out, h, saved, Wi, U, da, dh, ghat, st);
+}
+
+hipError_t launch_gru_wgrad(long K, int H, const float* a, const void* h, const void* saved, const void* ghat,
+                            float* dWi, float* dU, float* db, void* ws, hipStream_t st) {
+  return gru_wgrad_t<dev::dt_t>(K, H, a, h, saved, ghat, dWi, dU, db, ws, st);
+}
+}  // namespace GGNN_IMPL_NS
 
 }  // namespace ggnn

@@ -1,6 +1,11 @@
 // Launchers of the gfx950 kernels, one per device operation.  Arguments are
 // validated by the C-ABI layer before these are called; each returns the
 // hipGetLastError() of its launches.
+//
+// Every kernel source is built twice, once per storage dtype (bf16 kernels
+// with matrix-core results kept in VGPRs, fp32 kernels with the compiler's
+// default register assignment); the launchers of each build live in
+// ggnn::impl_bf16 / ggnn::impl_f32, and the functions below pick one by dt.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -10,52 +15,126 @@
 
 namespace ggnn {
 
-hipError_t launch_banded_fwd(int dt, int n_pad, int B, int H, int E, const void* band, const float* M, float* a,
-                             hipStream_t st);
-// dM rows have length ldm >= n_pad (ldm = T * n_pad when the reverse pass
-// keeps every step's message gradient for the weight-gradient products).
-hipError_t launch_banded_bwd(int dt, int n_pad, int B, int H, int E, const void* band, const void* da, void* dM,
-                             long ldm, hipStream_t st);
+#define GGNN_DT_LAUNCHERS                                                                                         \
+  hipError_t launch_banded_fwd(int n_pad, int B, int H, int E, const void* band, const float* M, float* a,        \
+                               hipStream_t st);                                                                   \
+  hipError_t launch_banded_bwd(int n_pad, int B, int H, int E, const void* band, const void* da, void* dM,        \
+                               long ldm, hipStream_t st);                                                         \
+  hipError_t launch_step_fwd_bits(int n_pad, int B, int H, int E, const void* bits, const void* X, const void* W, \
+                                  const float* bias, float* a, hipStream_t st);                                   \
+  hipError_t launch_banded_bwd_bits(int n_pad, int B, int H, int E, const void* bits_t, const void* da, void* dM, \
+                                    long ldm, hipStream_t st);                                                    \
+  hipError_t launch_step_bwd_bits(int n_pad, int B, int H, int E, const void* bits_t, const void* da,             \
+                                  const void* W, const float* dX_in, float* dX_out, void* dM, long ldm,           \
+                                  hipStream_t st);                                                                \
+  hipError_t launch_transform_fwd(int n_pad, int H, int E, const void* X, const void* W, const float* bias,       \
+                                  float* M, hipStream_t st);                                                      \
+  hipError_t launch_transform_bwd_dx(int n_pad, int H, int E, const void* W, const void* dM, long ld,             \
+                                     const float* dX_in, float* dX_out, hipStream_t st);                          \
+  hipError_t launch_transform_wgrad(long K, int H, int E, const void* X, const void* dM, long ld, float* dW,      \
+                                    float* dbias, void* ws, hipStream_t st);                                      \
+  hipError_t launch_transform_wgrad_nm(long K, int H, int E, const void* X, const void* dM, long ldk, float* dW,  \
+                                       float* dbias, void* ws, hipStream_t st);                                   \
+  hipError_t launch_gru_fwd(int n_pad, int H, const float* a, const void* h, const void* Wi, const void* U,       \
+                            const float* b, void* h_out, void* saved, hipStream_t st);                            \
+  hipError_t launch_gru_bwd_nodes(int n_pad, int H, const float* dh_out, const void* h, const void* saved,        \
+                                  const void* Wi, const void* U, void* da, float* dh, void* ghat,                 \
+                                  hipStream_t st);                                                                \
+  hipError_t launch_gru_wgrad(long K, int H, const float* a, const void* h, const void* saved, const void* ghat,  \
+                              float* dWi, float* dU, float* db, void* ws, hipStream_t st);
+
+namespace impl_bf16 {
+GGNN_DT_LAUNCHERS
+}
+namespace impl_f32 {
+GGNN_DT_LAUNCHERS
+}
+#undef GGNN_DT_LAUNCHERS
+
+#define GGNN_DT_PICK(fn, ...) (dt == GGNN_BF16 ? impl_bf16::fn(__VA_ARGS__) : impl_f32::fn(__VA_ARGS__))
+
+// Dense band: transform-first propagation and its reverse.  dM rows have
+// length ldm >= n_pad (ldm = T * n_pad when the reverse pass keeps every
+// step's message gradient for the weight-gradient products).
+inline hipError_t launch_banded_fwd(int dt, int n_pad, int B, int H, int E, const void* band, const float* M,
+                                    float* a, hipStream_t st) {
+  return GGNN_DT_PICK(launch_banded_fwd, n_pad, B, H, E, band, M, a, st);
+}
+inline hipError_t launch_banded_bwd(int dt, int n_pad, int B, int H, int E, const void* band, const void* da,
+                                    void* dM, long ldm, hipStream_t st) {
+  return GGNN_DT_PICK(launch_banded_bwd, n_pad, B, H, E, band, da, dM, ldm, st);
+}
 
 // out[i] += sum_s part[s * stride + i], i < count, fixed summation order.
 hipError_t launch_reduce_partials(const float* part, float* out, int nsplit, int count, long stride,
                                   hipStream_t st);
+hipError_t launch_fill_zero(float* p, size_t count, hipStream_t st);
 
 // 1-bit band: fused aggregate-first forward and transposed-band reverse.
-hipError_t launch_step_fwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits, const void* X,
-                                const void* W, const float* bias, float* a, hipStream_t st);
-hipError_t launch_banded_bwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits_t, const void* da,
-                                  void* dM, long ldm, hipStream_t st);
+inline hipError_t launch_step_fwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits, const void* X,
+                                       const void* W, const float* bias, float* a, hipStream_t st) {
+  return GGNN_DT_PICK(launch_step_fwd_bits, n_pad, B, H, E, bits, X, W, bias, a, st);
+}
+inline hipError_t launch_banded_bwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits_t, const void* da,
+                                         void* dM, long ldm, hipStream_t st) {
+  return GGNN_DT_PICK(launch_banded_bwd_bits, n_pad, B, H, E, bits_t, da, dM, ldm, st);
+}
+// Fused reverse step: dM_e = A_e^T da stored node-major (rows of type e start
+// at row e * ldm of dM), dX_out = dX_in (or 0) + sum_e dM_e W_e^T.
+inline hipError_t launch_step_bwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits_t, const void* da,
+                                       const void* W, const float* dX_in, float* dX_out, void* dM, long ldm,
+                                       hipStream_t st) {
+  return GGNN_DT_PICK(launch_step_bwd_bits, n_pad, B, H, E, bits_t, da, W, dX_in, dX_out, dM, ldm, st);
+}
 
-hipError_t launch_transform_fwd(int dt, int n_pad, int H, int E, const void* X, const void* W, const float* bias,
-                                float* M, hipStream_t st);
+inline hipError_t launch_transform_fwd(int dt, int n_pad, int H, int E, const void* X, const void* W,
+                                       const float* bias, float* M, hipStream_t st) {
+  return GGNN_DT_PICK(launch_transform_fwd, n_pad, H, E, X, W, bias, M, st);
+}
 // Input gradient dX_out = dX_in + sum_e dM_e W_e^T (dM rows of length ld).
-hipError_t launch_transform_bwd_dx(int dt, int n_pad, int H, int E, const void* W, const void* dM, long ld,
-                                   const float* dX_in, float* dX_out, hipStream_t st);
+inline hipError_t launch_transform_bwd_dx(int dt, int n_pad, int H, int E, const void* W, const void* dM, long ld,
+                                          const float* dX_in, float* dX_out, hipStream_t st) {
+  return GGNN_DT_PICK(launch_transform_bwd_dx, n_pad, H, E, W, dM, ld, dX_in, dX_out, st);
+}
 // Weight gradients over K rows: dW += X^T dM, dbias += row sums of dM (NULL
 // to skip), X = K rows [K][H], dM rows of length ld >= K.  The workspace
 // (transform_wgrad_workspace bytes) holds per-split partials, reduced in a
 // fixed order.
 size_t transform_wgrad_workspace(long K, int H, int E);
-hipError_t launch_transform_wgrad(int dt, long K, int H, int E, const void* X, const void* dM, long ld, float* dW,
-                                  float* dbias, void* ws, hipStream_t st);
-hipError_t launch_fill_zero(float* p, size_t count, hipStream_t st);
+inline hipError_t launch_transform_wgrad(int dt, long K, int H, int E, const void* X, const void* dM, long ld,
+                                         float* dW, float* dbias, void* ws, hipStream_t st) {
+  return GGNN_DT_PICK(launch_transform_wgrad, K, H, E, X, dM, ld, dW, dbias, ws, st);
+}
+// The same with node-major dM: row k of type e at dM + (e * ldk + k) * H.
+inline hipError_t launch_transform_wgrad_nm(int dt, long K, int H, int E, const void* X, const void* dM, long ldk,
+                                            float* dW, float* dbias, void* ws, hipStream_t st) {
+  return GGNN_DT_PICK(launch_transform_wgrad_nm, K, H, E, X, dM, ldk, dW, dbias, ws, st);
+}
 
-hipError_t launch_gru_fwd(int dt, int n_pad, int H, const float* a, const void* h, const void* Wi, const void* U,
-                          const float* b, void* h_out, void* saved, hipStream_t st);
+inline hipError_t launch_gru_fwd(int dt, int n_pad, int H, const float* a, const void* h, const void* Wi,
+                                 const void* U, const float* b, void* h_out, void* saved, hipStream_t st) {
+  return GGNN_DT_PICK(launch_gru_fwd, n_pad, H, a, h, Wi, U, b, h_out, saved, st);
+}
 // Node pass of the GRU reverse: da, dh and the gate gradients G^ [n_pad][3H].
-hipError_t launch_gru_bwd_nodes(int dt, int n_pad, int H, const float* dh_out, const void* h, const void* saved,
-                                const void* Wi, const void* U, void* da, float* dh, void* ghat, hipStream_t st);
+inline hipError_t launch_gru_bwd_nodes(int dt, int n_pad, int H, const float* dh_out, const void* h,
+                                       const void* saved, const void* Wi, const void* U, void* da, float* dh,
+                                       void* ghat, hipStream_t st) {
+  return GGNN_DT_PICK(launch_gru_bwd_nodes, n_pad, H, dh_out, h, saved, Wi, U, da, dh, ghat, st);
+}
 size_t ghat_bytes(int dt, long rows, int H);
 // GRU weight gradients over K rows of (a, h, saved, G^) stacked node-major:
 // dWi, dU, db += (partials in ws of gru_wgrad_workspace bytes, fixed order).
 size_t gru_wgrad_workspace(long K, int H);
-hipError_t launch_gru_wgrad(int dt, long K, int H, const float* a, const void* h, const void* saved, const void* ghat,
-                            float* dWi, float* dU, float* db, void* ws, hipStream_t st);
+inline hipError_t launch_gru_wgrad(int dt, long K, int H, const float* a, const void* h, const void* saved,
+                                   const void* ghat, float* dWi, float* dU, float* db, void* ws, hipStream_t st) {
+  return GGNN_DT_PICK(launch_gru_wgrad, K, H, a, h, saved, ghat, dWi, dU, db, ws, st);
+}
 // One step: node pass with G^ in ws, then the weight gradients over n_pad rows.
 size_t gru_bwd_workspace(int dt, int n_pad, int H);
 hipError_t launch_gru_bwd(int dt, int n_pad, int H, const float* dh_out, const float* a, const void* h,
                           const void* saved, const void* Wi, const void* U, void* da, float* dh, float* dWi,
                           float* dU, float* db, void* ws, hipStream_t st);
+
+#undef GGNN_DT_PICK
 
 }  // namespace ggnn

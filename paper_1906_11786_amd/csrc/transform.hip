@@ -284,8 +284,126 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
   }
 }
 
+// ---------------------------------------------------------------------------
+// Backward, weight gradient with node-major dM (the fused bit-band reverse
+// step writes dM_e rows node by node): one split of the rows,
+//   P[split][e][h_in][h_out] = sum_k X[k][h_in] * dM[e][k][h_out],
+//   Pb[split][e][h_out]      = sum_k dM[e][k][h_out],
+// rows k of type e at dM + (e * ldk + k) * H.  Tile TI x TI (TI = min(H, 64)),
+// TI/16 waves.  Rows are taken in chunks of 64: both operands are staged
+// transposed in LDS (V x V register-transposed tiles; consecutive lanes fill
+// consecutive 16-byte pieces of one LDS row, so the stores are conflict-free
+// and every load instruction reads whole lines) and read as contiguous
+// fragments.  The next chunk's tiles are loaded while the current one is
+// multiplied.  The tile index runs fastest over the logical workgroup index,
+// so the tiles of one split share their X rows in one XCD's L2.
+// ---------------------------------------------------------------------------
+template <typename S, int H>
+__global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgrad_nm_kernel(
+    const S* __restrict__ X, const S* __restrict__ dM, long ldk, float* __restrict__ P, float* __restrict__ Pb,
+    long K, int E, int rows_per_split) {
+  constexpr int TI = H < 64 ? H : 64;
+  constexpr int WAVES = TI / 16;
+  constexpr int NT = WAVES * kWave;
+  constexpr int V = 16 / sizeof(S);
+  constexpr int KN = 64;                  // rows per chunk
+  constexpr int PK = KN + V;              // LDS row pitch (16-byte multiple)
+  constexpr int NTL = TI / 16;
+  constexpr int TPD = H / TI;             // tiles per dimension
+  constexpr int TT = (KN / V) * (TI / V); // V x V tiles per operand chunk
+  constexpr int UN = (2 * TT + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) S xs[TI * PK];
+  __shared__ __attribute__((aligned(16))) S ds[TI * PK];
+
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int q = lane % 16, g = lane / 16;
+  int bid = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int to = bid % TPD; bid /= TPD;
+  const int ti = bid % TPD; bid /= TPD;
+  const int e = bid % E;
+  const int split = bid / E;
+  const long nlo = (long)split * rows_per_split;
+  const long nhi = min(K, nlo + rows_per_split);
+  const S* dMe = dM + (size_t)e * ldk * H;
+
+  f32x4 acc[NTL];
+  float bsum[NTL];
+#pragma unroll
+  for (int n = 0; n < NTL; ++n) {
+    acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    bsum[n] = 0.f;
+  }
+  const bool do_bias = (ti == 0 && wave == 0 && Pb != nullptr);
+
+  // Unit u < TT: X tile; TT <= u < 2 TT: dM tile.  Within an operand, the
+  // row-group index kq runs fastest.  Rows past nhi are staged as zeros.
+  u32x4 r[UN][V];
+  auto load_chunk = [&](long c0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+      const int lin = u * NT + tid;
+      if ((2 * TT) % NT == 0 || lin < 2 * TT) {
+        const int w = lin % TT, kq = w % (KN / V), cq = w / (KN / V);
+        const long row = c0 + V * kq;
+        const S* src = lin < TT ? X + (size_t)row * H + ti * TI + V * cq : dMe + (size_t)row * H + to * TI + V * cq;
+#pragma unroll
+        for (int i = 0; i < V; ++i)
+          r[u][i] = (row + i < nhi) ? *reinterpret_cast<const u32x4*>(src + (size_t)i * H) : u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+  };
+  auto store_chunk = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+      const int lin = u * NT + tid;
+      if ((2 * TT) % NT == 0 || lin < 2 * TT) {
+        const int w = lin % TT, kq = w % (KN / V), cq = w / (KN / V);
+        tile_store_T<S, PK>(&(lin < TT ? xs : ds)[(V * cq) * PK + V * kq], r[u]);
+      }
+    }
+  };
+  if (nlo < nhi) load_chunk(nlo);
+  for (long c0 = nlo; c0 < nhi; c0 += KN) {
+    __syncthreads();
+    store_chunk();
+    __syncthreads();
+    if (c0 + KN < nhi) load_chunk(c0 + KN);
+#pragma unroll
+    for (int kk = 0; kk < KN / 32; ++kk) {
+      const frag_t<S> afr = load8(&xs[(16 * wave + q) * PK + 32 * kk + 8 * g]);
+#pragma unroll
+      for (int n = 0; n < NTL; ++n) {
+        const frag_t<S> bf = load8(&ds[(16 * n + q) * PK + 32 * kk + 8 * g]);
+        mma(acc[n], afr, bf);
+        if (do_bias) {
+#pragma unroll
+          for (int x = 0; x < 8; ++x) bsum[n] += static_cast<float>(bf[x]);
+        }
+      }
+    }
+  }
+  // D[h_in = ti*TI + 16*wave + 4g + j][h_out = to*TI + 16n + q]
+  float* out = P + ((size_t)split * E + e) * H * H;
+#pragma unroll
+  for (int n = 0; n < NTL; ++n) {
+    const int o = to * TI + 16 * n + q;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * H + o] = acc[n][j];
+  }
+  if (do_bias) {
+#pragma unroll
+    for (int n = 0; n < NTL; ++n) {
+      float v = bsum[n];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (g == 0) Pb[((size_t)split * E + e) * H + to * TI + 16 * n + q] = v;
+    }
+  }
+}
+
 }  // namespace dev
 
+#if GGNN_DT_BF16   // dtype-independent kernels: built once
 // out[i] += sum_{s < nsplit} part[s * stride + i] for i < count.  A
 // workgroup of 64 x RW threads owns 64 consecutive outputs: thread (x, y)
 // sums the splits s = y, y + RW, y + 2RW, ... in increasing order (eight
@@ -346,6 +464,8 @@ hipError_t launch_reduce_partials(const float* part, float* out, int nsplit, int
                      count, stride);
   return hipGetLastError();
 }
+
+#endif
 
 namespace {
 // Row split of the weight-gradient contraction: about 2048 workgroups over
@@ -408,6 +528,35 @@ hipError_t transform_wgrad_h(long K, int E, const void* X, const void* dM, long 
   return launch_reduce_partials(Pb, dbias, sp.nsplit, E * H, (long)E * H, st);
 }
 
+template <typename S, int H>
+hipError_t transform_wgrad_nm_h(long K, int E, const void* X, const void* dM, long ldk, float* dW, float* dbias,
+                                void* ws, hipStream_t st) {
+  Split sp = transform_split(K, H, E);
+  constexpr int TI = H < 64 ? H : 64;
+  float* P = static_cast<float*>(ws);
+  float* Pb = dbias ? P + (size_t)sp.nsplit * E * H * H : nullptr;
+  const int blocks = sp.nsplit * E * (H / TI) * (H / TI);
+  hipLaunchKernelGGL((dev::transform_wgrad_nm_kernel<S, H>), dim3(blocks), dim3(TI / 16 * 64), 0, st,
+                     static_cast<const S*>(X), static_cast<const S*>(dM), ldk, P, Pb, K, E, sp.per);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  err = launch_reduce_partials(P, dW, sp.nsplit, E * H * H, (long)E * H * H, st);
+  if (err != hipSuccess || !dbias) return err;
+  return launch_reduce_partials(Pb, dbias, sp.nsplit, E * H, (long)E * H, st);
+}
+
+template <typename S>
+hipError_t transform_wgrad_nm_t(long K, int H, int E, const void* X, const void* dM, long ldk, float* dW,
+                                float* dbias, void* ws, hipStream_t st) {
+  switch (H) {
+    case 32: return transform_wgrad_nm_h<S, 32>(K, E, X, dM, ldk, dW, dbias, ws, st);
+    case 64: return transform_wgrad_nm_h<S, 64>(K, E, X, dM, ldk, dW, dbias, ws, st);
+    case 128: return transform_wgrad_nm_h<S, 128>(K, E, X, dM, ldk, dW, dbias, ws, st);
+    case 256: return transform_wgrad_nm_h<S, 256>(K, E, X, dM, ldk, dW, dbias, ws, st);
+  }
+  return hipErrorInvalidValue;
+}
+
 template <typename S>
 hipError_t transform_fwd_t(int n_pad, int H, int E, const void* X, const void* W, const float* bias, float* M,
                            hipStream_t st) {
@@ -443,27 +592,33 @@ hipError_t transform_wgrad_t(long K, int H, int E, const void* X, const void* dM
 }
 }  // namespace
 
+#if GGNN_DT_BF16
 size_t transform_wgrad_workspace(long K, int H, int E) {
   Split sp = transform_split(K, H, E);
   return ((size_t)sp.nsplit * E * H * H + (size_t)sp.nsplit * E * H) * sizeof(float);
 }
+#endif
 
-hipError_t launch_transform_fwd(int dt, int n_pad, int H, int E, const void* X, const void* W, const float* bias,
-                                float* M, hipStream_t st) {
-  return dt == GGNN_BF16 ? transform_fwd_t<dev::bf16s>(n_pad, H, E, X, W, bias, M, st)
-                         : transform_fwd_t<float>(n_pad, H, E, X, W, bias, M, st);
+namespace GGNN_IMPL_NS {
+hipError_t launch_transform_fwd(int n_pad, int H, int E, const void* X, const void* W, const float* bias, float* M,
+                                hipStream_t st) {
+  return transform_fwd_t<dev::dt_t>(n_pad, H, E, X, W, bias, M, st);
 }
 
-hipError_t launch_transform_bwd_dx(int dt, int n_pad, int H, int E, const void* W, const void* dM, long ld,
+hipError_t launch_transform_bwd_dx(int n_pad, int H, int E, const void* W, const void* dM, long ld,
                                    const float* dX_in, float* dX_out, hipStream_t st) {
-  return dt == GGNN_BF16 ? transform_dx_t<dev::bf16s>(n_pad, H, E, W, dM, ld, dX_in, dX_out, st)
-                         : transform_dx_t<float>(n_pad, H, E, W, dM, ld, dX_in, dX_out, st);
+  return transform_dx_t<dev::dt_t>(n_pad, H, E, W, dM, ld, dX_in, dX_out, st);
 }
 
-hipError_t launch_transform_wgrad(int dt, long K, int H, int E, const void* X, const void* dM, long ld, float* dW,
+hipError_t launch_transform_wgrad(long K, int H, int E, const void* X, const void* dM, long ld, float* dW,
                                   float* dbias, void* ws, hipStream_t st) {
-  return dt == GGNN_BF16 ? transform_wgrad_t<dev::bf16s>(K, H, E, X, dM, ld, dW, dbias, ws, st)
-                         : transform_wgrad_t<float>(K, H, E, X, dM, ld, dW, dbias, ws, st);
+  return transform_wgrad_t<dev::dt_t>(K, H, E, X, dM, ld, dW, dbias, ws, st);
 }
+
+hipError_t launch_transform_wgrad_nm(long K, int H, int E, const void* X, const void* dM, long ldk, float* dW,
+                                     float* dbias, void* ws, hipStream_t st) {
+  return transform_wgrad_nm_t<dev::dt_t>(K, H, E, X, dM, ldk, dW, dbias, ws, st);
+}
+}  // namespace GGNN_IMPL_NS
 
 }  // namespace ggnn

@@ -253,6 +253,59 @@ def test_banded_propagate_bits_bwd_integer_exact(dt, B, H, E, nb):
     np.testing.assert_array_equal(host(dM), O.aggregate_transpose(n, s, d, e, da, E).transpose(0, 2, 1))
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("B,H,E,nb", BANDED_CASES)
+def test_banded_step_bits_bwd_integer_exact(dt, B, H, E, nb):
+    """Fused reverse step, small integers: dM_e = A_e^T da (node-major rows,
+    row stride ldm > n_pad: the rows past n_pad stay untouched) and
+    dX = dX_in + sum_e dM_e W_e^T, exact."""
+    say(f"banded_step_bits_bwd int dt={dt} B={B} H={H} E={E} nb={nb}")
+    rng = np.random.default_rng(B * 23 + H + E)
+    n = B * nb
+    src, dst, et = _edges(rng, n, 6 * n, E, 2 * B + 5)
+    _, bits_t, _ = _bits(n, E, B, src, dst, et)
+    da = rng.integers(-4, 5, (n, H)).astype(np.float64)
+    W = rng.integers(-1, 2, (E, H, H)).astype(np.float64)
+    dX_in = rng.integers(-3, 4, (n, H)).astype(np.float64)
+    ldm = n + 32
+    dM = torch.full((E, ldm, H), float("nan"), device="cuda", dtype=torch_dt(dt))
+    dX = torch.full((n, H), float("nan"), device="cuda")
+    capi.ggnn_banded_step_bits_bwd(dt, n, B, H, E, bits_t, dev(da.T, dt), dev(W, dt), dev(dX_in), dX, dM, ldm)
+    s, d, e, _, _ = O.kept_edges(src, dst, et, B)
+    want_dM = O.aggregate_transpose(n, s, d, e, da, E)
+    got = host(dM)
+    np.testing.assert_array_equal(got[:, :n], want_dM)
+    assert np.isnan(got[:, n:]).all()
+    want_dX, _, _ = O.msg_transform_backward(np.zeros((n, H)), W, want_dM)
+    np.testing.assert_array_equal(host(dX), dX_in + want_dX)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("B,H,E,nb", [(128, 64, 10, 5), (64, 128, 2, 6), (256, 256, 2, 3), (32, 32, 4, 9)])
+def test_banded_step_bits_bwd_real_values(dt, B, H, E, nb):
+    """Real values, in place (dX_in is dX_out) and without dX_in: dX agrees
+    with the oracle to the dtype's tolerance (dM enters the transform as its
+    stored, rounded value)."""
+    say(f"banded_step_bits_bwd real dt={dt} B={B} H={H} E={E} nb={nb}")
+    rng = np.random.default_rng(B + 5 * H + E)
+    n = B * nb
+    src, dst, et = _edges(rng, n, 4 * n, E, B + 3)
+    _, bits_t, _ = _bits(n, E, B, src, dst, et)
+    da = round_to(dt, rng.standard_normal((n, H)))
+    W = round_to(dt, rng.standard_normal((E, H, H)) / np.sqrt(H))
+    dX0 = rng.standard_normal((n, H))
+    s, d, e, _, _ = O.kept_edges(src, dst, et, B)
+    want_dM = O.aggregate_transpose(n, s, d, e, da, E)
+    want_dX, _, _ = O.msg_transform_backward(np.zeros((n, H)), W, want_dM)
+    dM = torch.empty((E, n, H), device="cuda", dtype=torch_dt(dt))
+    dX = dev(dX0)
+    capi.ggnn_banded_step_bits_bwd(dt, n, B, H, E, bits_t, dev(da.T, dt), dev(W, dt), dX, dX, dM, n)
+    assert relerr(host(dM), want_dM) <= TOL[dt]
+    assert relerr(host(dX), dX0 + want_dX) <= TOL[dt]
+    capi.ggnn_banded_step_bits_bwd(dt, n, B, H, E, bits_t, dev(da.T, dt), dev(W, dt), None, dX, dM, n)
+    assert relerr(host(dX), want_dX) <= TOL[dt]
+
+
 def test_device_errors_are_reported():
     n, H = 128, 64
     ws_n = capi.ggnn_gru_update_bwd_workspace_bytes("bf16", n, H)
