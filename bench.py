@@ -41,16 +41,17 @@ FP32_PEAK_TFLOPS = 157.3    # MI355X fp32 matrix cores
 
 WORKLOADS = {"program_graph": 1, "tiny": 0, "batch_100k": 2, "stress_1m": 4}
 
-# C-ABI entry point -> (device kernel name fragment, sources that define it)
+# C-ABI entry point -> (device kernel name fragments, sources that define it)
 KERNELS = {
-    "banded_step_bits": ("step_fwd_kernel", ["banded_bits.hip", "device_common.h"]),
-    "banded_propagate_bits_bwd": ("bits_bwd_kernel", ["banded_bits.hip", "device_common.h"]),
-    "banded_propagate": ("banded_fwd_kernel", ["banded.hip", "device_common.h"]),
-    "banded_propagate_bwd": ("banded_bwd_kernel", ["banded.hip", "device_common.h"]),
+    "banded_step_bits": (("step_bits_kernel", ", false>("), ["banded_bits.hip", "device_common.h"]),
+    "banded_step_bits_bwd": (("step_bits_kernel", ", true>("), ["banded_bits.hip", "device_common.h"]),
+    "banded_propagate": (("banded_fwd_kernel",), ["banded.hip", "device_common.h"]),
+    "banded_propagate_bwd": (("banded_bwd_kernel",), ["banded.hip", "device_common.h"]),
 }
 # Other kernels of the step, listed in the traffic summary.
-OTHER_KERNELS = ["gru_fwd_kernel", "gru_bwd_kernel", "gru_wgrad_kernel", "transform_bwd_dx_kernel",
-                 "transform_wgrad_kernel", "transform_fwd_kernel", "reduce_partials_kernel"]
+OTHER_KERNELS = [("gru_fwd_kernel",), ("gru_bwd_kernel",), ("gru_wgrad_kernel",), ("transform_bwd_dx_kernel",),
+                 ("transform_wgrad_kernel",), ("transform_wgrad_nm_kernel",), ("transform_fwd_kernel",),
+                 ("reduce_partials_kernel",)]
 CAL_ELEMS = 64 << 20            # calibration copy: 64 Mi fp32 read, 64 Mi fp32 written
 CAL_BYTES = CAL_ELEMS * 4
 CAL_NAME = "neg_kernel"         # torch's elementwise negation: one read and one write per element
@@ -118,12 +119,12 @@ def traffic_summary(fetch_csv, write_csv, cmd_line):
     machine-readable record per banded kernel."""
     fetch, write = _counter_rows(fetch_csv, "FETCH_SIZE"), _counter_rows(write_csv, "WRITE_SIZE")
 
-    def per_kernel(rows, frag):
-        vals = [v for name, v in rows.values() if frag in name]
+    def per_kernel(rows, frags):
+        vals = [v for name, v in rows.values() if all(f in name for f in frags)]
         return (statistics.median(vals), len(vals)) if vals else (None, 0)
 
-    cf, _ = per_kernel(fetch, CAL_NAME)
-    cw, _ = per_kernel(write, CAL_NAME)
+    cf, _ = per_kernel(fetch, (CAL_NAME,))
+    cw, _ = per_kernel(write, (CAL_NAME,))
     if not cf or not cw:
         raise SystemExit("calibration copy not found in the counter files")
     kf, kw = CAL_BYTES / cf, CAL_BYTES / cw
@@ -138,7 +139,7 @@ def traffic_summary(fetch_csv, write_csv, cmd_line):
         if f is None or w is None:
             continue
         b = f * kf + w * kw
-        lines.append(f"| `{frag}` | {n} | {f:.0f} | {w:.0f} | {b:.0f} |")
+        lines.append(f"| `{' '.join(frag)}` | {n} | {f:.0f} | {w:.0f} | {b:.0f} |")
         for k, (fr, srcs) in KERNELS.items():
             if fr == frag:
                 recs.append((k, b, srcs))
@@ -168,9 +169,11 @@ def kernel_costs(fmt, n_pad, B, E, H, es):
     agg_flops = 2.0 * blocks * B * B * H
     if fmt == "bits":
         band = blocks * B * B // 8
-        fwd = (agg_flops + 2.0 * n_pad * E * H * H, band + n_pad * H * es + E * H * H * es + n_pad * H * 4)
-        bwd = (agg_flops, band + H * n_pad * es + E * H * n_pad * es)
-        return {"banded_step_bits": fwd, "banded_propagate_bits_bwd": bwd}
+        tr_flops = 2.0 * n_pad * E * H * H
+        fwd = (agg_flops + tr_flops, band + n_pad * H * es + E * H * H * es + n_pad * H * 4)
+        # reverse: bits_t, da, W read; dM (all types) written; dX_in read, dX_out written
+        bwd = (agg_flops + tr_flops, band + H * n_pad * es + E * H * H * es + E * n_pad * H * es + 2 * n_pad * H * 4)
+        return {"banded_step_bits": fwd, "banded_step_bits_bwd": bwd}
     band = blocks * B * B * es
     return {"banded_propagate": (agg_flops, band + E * H * n_pad * 4 + n_pad * H * 4),
             "banded_propagate_bwd": (agg_flops, band + H * n_pad * es + E * H * n_pad * es)}
@@ -271,8 +274,9 @@ def main():
     if args.band == "bits":
         fns = {"banded_step_bits": lambda: capi.ggnn_banded_step_bits(spec.dtype, n_pad, B, H, E, m.band, m.X[0],
                                                                       m.W, m.bias, m.a[0]),
-               "banded_propagate_bits_bwd": lambda: capi.ggnn_banded_propagate_bits_bwd(spec.dtype, n_pad, B, H, E,
-                                                                                        m.band_t, m.da, m.dM)}
+               "banded_step_bits_bwd": lambda: capi.ggnn_banded_step_bits_bwd(spec.dtype, n_pad, B, H, E, m.band_t,
+                                                                              m.da, m.W, m.dh, m.dX, m.dM,
+                                                                              spec.T * n_pad)}
     else:
         fns = {"banded_propagate": lambda: capi.ggnn_banded_propagate(spec.dtype, n_pad, B, H, E, m.band, m.M,
                                                                       m.a[0]),

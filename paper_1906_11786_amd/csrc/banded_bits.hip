@@ -164,12 +164,21 @@ struct BitsCfg {
 // takes rows as wave w % WAVES and the types of group w / WAVES (a
 // contiguous range), so TG waves share a SIMD and overlap one another's VALU,
 // LDS and matrix work.  The groups' partial sums meet in LDS at the end (over
-// the staged blocks), added in group order.
+// the staged blocks): with TG = NTW = 2 group g completes row tile g (its own
+// partial plus the other group's), otherwise group 0 completes both; either
+// way a = (group 0 partial) + (group 1 partial).
+// GRU (forward, WDIR): the node update of Eq. 1 runs on the completed
+// aggregate in the same workgroup, so `a` goes to memory only for the
+// reverse pass and the next state X' and the gates (r | z | n) are written
+// here.  Wi^T and U^T are staged in LDS with the blocks; the GRU products
+// take a (hi + lo in bf16 mode), h and r*h as operand fragments straight
+// from registers (accumulator-compatible order).
 // ---------------------------------------------------------------------------
-template <typename S, int H, int B, int WAVES, bool WDIR, int TG, bool REV>
+template <typename S, int H, int B, int WAVES, bool WDIR, int TG, bool REV, bool GRU>
 __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
     const uint8_t* __restrict__ bits, const S* __restrict__ X, const S* __restrict__ W, const float* __restrict__ bias,
-    float* out, int n_pad, int E, const float* dX_in, S* __restrict__ dM, long ldm) {
+    float* out, int n_pad, int E, const float* dX_in, S* __restrict__ dM, long ldm, const S* __restrict__ Wi,
+    const S* __restrict__ U, const float* __restrict__ bg, S* __restrict__ h_out, S* __restrict__ saved) {
   using C = BitsCfg<S, H, B>;
   constexpr int NT = TG * WAVES * kWave;
   constexpr int V = C::V, KC = C::KC, VP = C::VP, RB = C::RB, NTW = C::NTW, WP = C::WP;
@@ -181,8 +190,11 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   static_assert(TG == 1 || WDIR, "type groups need the barrier-free loop");
   static_assert(TG == 1 || (TG - 1) * WAVES * kWave * NTW * MT * 16 <= (int)(C::NBUF * H * VP * sizeof(S)),
                 "partial sums must fit in the staged-block space");
+  static_assert(!GRU || (WDIR && !REV), "the GRU epilogue is a forward, direct-weight form");
+  constexpr int GP = H + V;                  // row pitch of the staged Wi^T, U^T
   __shared__ __attribute__((aligned(16))) S vt[C::NBUF][H * VP];
   __shared__ __attribute__((aligned(16))) S wt[WDIR ? 8 : WC * WP];
+  __shared__ __attribute__((aligned(16))) S gw[GRU ? 2 * 3 * H * GP : 8];
 
   const int nb = n_pad / B;
   constexpr int NW = C::RPW * WAVES;
@@ -225,27 +237,38 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   // Each thread issues the loads of up to PB units before its writes.
   if constexpr (C::ALL) {
     if constexpr (!REV) {
+      // With GRU, the tiles of Wi and U follow (gw[m][c * GP + h] = Wi / U[h][c]).
       constexpr int XT = (KC / V) * (H / V);       // tiles per block
+      constexpr int GT = (H / V) * (3 * H / V);    // tiles per GRU weight
       constexpr int PB = 2;
-      const int total = (s_hi - s_lo + 1) * XT;
+      const int nx = (s_hi - s_lo + 1) * XT;
+      const int total = nx + (GRU ? 2 * GT : 0);
       for (int base = 0; base < total; base += PB * NT) {
         u32x4 r[PB][V];
 #pragma unroll
         for (int u = 0; u < PB; ++u) {
           const int lin = base + u * NT + tid;
-          if (lin < total) {
+          if (lin < nx) {
             const int slot = s_lo + lin / XT, rem = lin % XT;
             const int cq = rem % (KC / V), fq = rem / (KC / V);
             tile_load<S>(r[u], X + (size_t)((k - 1 + slot) * B + V * cq) * H + V * fq, H);
+          } else if (lin < total) {
+            const int w = lin - nx, m = w / GT, rem = w % GT;
+            const int hq = rem % (H / V), cq = rem / (H / V);
+            tile_load<S>(r[u], (m ? U : Wi) + (size_t)(V * hq) * 3 * H + V * cq, 3 * H);
           }
         }
 #pragma unroll
         for (int u = 0; u < PB; ++u) {
           const int lin = base + u * NT + tid;
-          if (lin < total) {
+          if (lin < nx) {
             const int slot = s_lo + lin / XT, rem = lin % XT;
             const int cq = rem % (KC / V), fq = rem / (KC / V);
             tile_store_T<S, VP>(&vt[slot][(V * fq) * VP + V * cq], r[u]);
+          } else if (lin < total) {
+            const int w = lin - nx, m = w / GT, rem = w % GT;
+            const int hq = rem % (H / V), cq = rem / (H / V);
+            tile_store_T<S, GP>(&gw[(size_t)m * 3 * H * GP + (V * cq) * GP + V * hq], r[u]);
           }
         }
       }
@@ -505,32 +528,58 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
       }
     }
   }
+  // Row tiles this wave completes: all of them, or with two groups and two
+  // tiles per wave, tile tg.
+  constexpr bool SPLIT = (TG == 2 && NTW == 2);
   if constexpr (TG > 1) {
-    // Groups 1.. leave their sums in LDS (over the staged blocks, once every
-    // wave is done reading them); group 0 adds them in group order.
     f32x4* red = reinterpret_cast<f32x4*>(&vt[0][0]);
-    __syncthreads();
-    if (tg > 0) {
+    __syncthreads();   // every wave is done reading the staged blocks
+    if constexpr (SPLIT) {
+      // Each group hands the other group's tile over through LDS (static
+      // register indices: the tile is picked by a uniform branch).
 #pragma unroll
-      for (int n = 0; n < NTW; ++n)
+      for (int n = 0; n < NTW; ++n) {
+        if (n == tg) continue;
 #pragma unroll
-        for (int m = 0; m < MT; ++m) red[((((tg - 1) * WAVES + wave) * NTW + n) * MT + m) * kWave + lane] = acc[n][m];
-    }
-    __syncthreads();
-    if (tg > 0) return;
+        for (int m = 0; m < MT; ++m) red[(((tg * WAVES + wave) * MT) + m) * kWave + lane] = acc[n][m];
+      }
+      __syncthreads();
 #pragma unroll
-    for (int gi = 1; gi < TG; ++gi)
-#pragma unroll
-      for (int n = 0; n < NTW; ++n)
+      for (int n = 0; n < NTW; ++n) {
+        if (n != tg) continue;
 #pragma unroll
         for (int m = 0; m < MT; ++m) {
-          const f32x4 r = red[((((gi - 1) * WAVES + wave) * NTW + n) * MT + m) * kWave + lane];
+          const f32x4 r = red[((((1 - tg) * WAVES + wave) * MT) + m) * kWave + lane];
+          // a = (group 0 partial) + (group 1 partial), in that order
 #pragma unroll
-          for (int j = 0; j < 4; ++j) acc[n][m][j] += r[j];
+          for (int j = 0; j < 4; ++j) acc[n][m][j] = n == 0 ? acc[n][m][j] + r[j] : r[j] + acc[n][m][j];
         }
+      }
+    } else {
+      // Groups 1.. leave their sums in LDS; group 0 adds them in group order.
+      if (tg > 0) {
+#pragma unroll
+        for (int n = 0; n < NTW; ++n)
+#pragma unroll
+          for (int m = 0; m < MT; ++m) red[((((tg - 1) * WAVES + wave) * NTW + n) * MT + m) * kWave + lane] = acc[n][m];
+      }
+      __syncthreads();
+      if (tg > 0) return;
+#pragma unroll
+      for (int gi = 1; gi < TG; ++gi)
+#pragma unroll
+        for (int n = 0; n < NTW; ++n)
+#pragma unroll
+          for (int m = 0; m < MT; ++m) {
+            const f32x4 r = red[((((gi - 1) * WAVES + wave) * NTW + n) * MT + m) * kWave + lane];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[n][m][j] += r[j];
+          }
+    }
   }
 #pragma unroll
   for (int n = 0; n < NTW; ++n) {
+    if (SPLIT && n != tg) continue;
     const size_t row = (size_t)(k * B + rw + 16 * n + q) * H + 4 * g;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
@@ -540,6 +589,88 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         v = f32x4{b[0] + v[0], b[1] + v[1], b[2] + v[2], b[3] + v[3]};
       }
       store4(out + row + 16 * m, v[0], v[1], v[2], v[3]);
+    }
+    if constexpr (GRU) {
+      // GRU of Eq. 1 (Cho et al. 2014 form) for this tile's 16 nodes, as in
+      // the stand-alone GRU kernel: D[feature][node] with A = rows of Wi^T /
+      // U^T (LDS) and B = a (hi + lo), h, r*h fragments.
+      constexpr int KS = H / 32;
+      const int node = k * B + rw + 16 * n + q;
+      frag_t<S> af[NP][KS], hf[KS], rh[KS];
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        float v8[8];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          v8[j] = acc[n][2 * kk][j];
+          v8[4 + j] = acc[n][2 * kk + 1][j];
+        }
+        if constexpr (NP == 2) {
+          split8(v8, af[0][kk], af[NP - 1][kk]);
+        } else {
+          af[0][kk] = pack8<S>(v8);
+        }
+        hf[kk] = load4x2(X + (size_t)node * H + 32 * kk + 4 * g, X + (size_t)node * H + 32 * kk + 16 + 4 * g);
+      }
+      auto gfrag = [&](int mat, int col, int kk) __attribute__((always_inline)) {   // rows col..col+15 of Wi^T / U^T
+        const S* base = gw + (size_t)mat * 3 * H * GP + (size_t)(col + q) * GP + 32 * kk + 4 * g;
+        return load4x2(base, base + 16);
+      };
+      // r for all features (r*h is an operand of the candidate product).
+#pragma unroll
+      for (int c = 0; c < KS; ++c) {
+        float rhv[8];
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          f32x4 ar = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) {
+            const frag_t<S> w0 = gfrag(0, 32 * c + 16 * p, kk);
+#pragma unroll
+            for (int part = 0; part < NP; ++part) mma(ar, w0, af[part][kk]);
+            mma(ar, gfrag(1, 32 * c + 16 * p, kk), hf[kk]);
+          }
+          const int f = 32 * c + 16 * p + 4 * g;
+          float r[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            r[j] = sigmoidf_(ar[j] + bg[f + j]);
+            rhv[4 * p + j] = r[j] * static_cast<float>(hf[c][4 * p + j]);
+          }
+          store4(saved + (size_t)node * 3 * H + f, r[0], r[1], r[2], r[3]);
+        }
+        rh[c] = pack8<S>(rhv);
+      }
+      // z, n and the new state.
+#pragma unroll
+      for (int c = 0; c < KS; ++c)
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          f32x4 az = {0.f, 0.f, 0.f, 0.f}, an = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int kk = 0; kk < KS; ++kk) {
+            const frag_t<S> wz = gfrag(0, H + 32 * c + 16 * p, kk), wn = gfrag(0, 2 * H + 32 * c + 16 * p, kk);
+#pragma unroll
+            for (int part = 0; part < NP; ++part) {
+              mma(az, wz, af[part][kk]);
+              mma(an, wn, af[part][kk]);
+            }
+            mma(az, gfrag(1, H + 32 * c + 16 * p, kk), hf[kk]);
+            mma(an, gfrag(1, 2 * H + 32 * c + 16 * p, kk), rh[kk]);
+          }
+          const int f = 32 * c + 16 * p + 4 * g;
+          float z[4], nn[4], o[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            z[j] = sigmoidf_(az[j] + bg[H + f + j]);
+            nn[j] = tanhf_(an[j] + bg[2 * H + f + j]);
+            const float hv = static_cast<float>(hf[c][4 * p + j]);
+            o[j] = z[j] * hv + (1.f - z[j]) * nn[j];
+          }
+          store4(h_out + (size_t)node * H + f, o[0], o[1], o[2], o[3]);
+          store4(saved + (size_t)node * 3 * H + H + f, z[0], z[1], z[2], z[3]);
+          store4(saved + (size_t)node * 3 * H + 2 * H + f, nn[0], nn[1], nn[2], nn[3]);
+        }
     }
   }
 }
@@ -706,6 +837,12 @@ struct BitsArgs {
   void* dM;             // mode 1
   long ldm;
   int n_pad, E;
+  const void* Wi = nullptr;   // mode 0 with the GRU epilogue (when non-NULL and supported)
+  const void* U = nullptr;
+  const float* bg = nullptr;
+  void* h_out = nullptr;
+  void* saved = nullptr;
+  bool* fused_gru = nullptr;  // set to whether the GRU ran in the step
 };
 
 template <typename S, int H, int B>
@@ -734,20 +871,28 @@ hipError_t bits_launch(const BitsArgs& A, hipStream_t st) {
   const S* wp = static_cast<const S*>(A.W);
   float* op = static_cast<float*>(A.out);
   S* dmp = static_cast<S*>(A.dM);
-#define GGNN_STEP(WV, TGN, REVB)                                                                              \
-  hipLaunchKernelGGL((dev::step_bits_kernel<S, H, B, WV, C::WDIR, TGN, REVB>), dim3(blocks), dim3(TGN * WV * 64), \
-                     0, st, bp, vp, wp, A.bias, op, A.n_pad, A.E, A.dX_in, dmp, A.ldm)
+  // The GRU epilogue rides along only in the two-group form (a small grid,
+  // where the separate GRU launch would cost most).
+  const bool gru = A.mode == 0 && A.Wi != nullptr && C::WDIR && tg2;
+  if (A.fused_gru) *A.fused_gru = gru;
+#define GGNN_STEP(WV, TGN, REVB, GRUB)                                                                        \
+  hipLaunchKernelGGL((dev::step_bits_kernel<S, H, B, WV, C::WDIR, TGN, REVB, GRUB>), dim3(blocks),            \
+                     dim3(TGN * WV * 64), 0, st, bp, vp, wp, A.bias, op, A.n_pad, A.E, A.dX_in, dmp, A.ldm,     \
+                     static_cast<const S*>(A.Wi), static_cast<const S*>(A.U), A.bg, static_cast<S*>(A.h_out),  \
+                     static_cast<S*>(A.saved))
 #define GGNN_BITS_CASE(WV)                                                                                   \
   case WV:                                                                                                   \
     if constexpr (B / C::RPW >= WV && WV >= C::MINW) {                                                       \
-      if (A.mode == 0 && tg2)                                                                                \
-        GGNN_STEP(WV, (C::WDIR ? 2 : 1), false);                                                             \
+      if (A.mode == 0 && gru)                                                                                \
+        GGNN_STEP(WV, (C::WDIR ? 2 : 1), false, C::WDIR);                                                    \
+      else if (A.mode == 0 && tg2)                                                                           \
+        GGNN_STEP(WV, (C::WDIR ? 2 : 1), false, false);                                                      \
       else if (A.mode == 0)                                                                                  \
-        GGNN_STEP(WV, 1, false);                                                                             \
+        GGNN_STEP(WV, 1, false, false);                                                                      \
       else if (A.mode == 1 && tg2)                                                                           \
-        GGNN_STEP(WV, (C::WDIR ? 2 : 1), true);                                                              \
+        GGNN_STEP(WV, (C::WDIR ? 2 : 1), true, false);                                                       \
       else if (A.mode == 1)                                                                                  \
-        GGNN_STEP(WV, 1, true);                                                                              \
+        GGNN_STEP(WV, 1, true, false);                                                                       \
       else                                                                                                   \
         hipLaunchKernelGGL((dev::bits_bwd_kernel<S, H, B, WV>), dim3(blocks), dim3(WV * 64), 0, st, bp, vp,  \
                            static_cast<S*>(A.out), A.n_pad, A.E, groups, A.ldm);                             \
@@ -791,6 +936,19 @@ namespace GGNN_IMPL_NS {
 hipError_t launch_step_fwd_bits(int n_pad, int B, int H, int E, const void* bits, const void* X, const void* W,
                                 const float* bias, float* a, hipStream_t st) {
   return bits_t<dev::dt_t>(H, B, BitsArgs{0, bits, X, W, bias, a, nullptr, nullptr, 0, n_pad, E}, st);
+}
+
+hipError_t launch_step_fwd_bits_gru(int n_pad, int B, int H, int E, const void* bits, const void* X, const void* W,
+                                    const float* bias, float* a, const void* Wi, const void* U, const float* bg,
+                                    void* h_out, void* saved, bool* fused, hipStream_t st) {
+  BitsArgs A{0, bits, X, W, bias, a, nullptr, nullptr, 0, n_pad, E};
+  A.Wi = Wi;
+  A.U = U;
+  A.bg = bg;
+  A.h_out = h_out;
+  A.saved = saved;
+  A.fused_gru = fused;
+  return bits_t<dev::dt_t>(H, B, A, st);
 }
 
 hipError_t launch_step_bwd_bits(int n_pad, int B, int H, int E, const void* bits_t_, const void* da, const void* W,

@@ -282,13 +282,16 @@ ggnn_status ggnn_forward(const ggnn_model* m, const ggnn_activations* act, void*
     float* at = act->a + t * xs;
     char* sv = static_cast<char*>(act->saved) + t * 3 * xs * es;
     hipError_t err;
+    bool fused = false;   // the bit-band step also ran the GRU update
     if (m->band_format == GGNN_BAND_BITS) {
-      err = launch_step_fwd_bits(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, Xt, m->W, m->bias, at, s);
+      err = launch_step_fwd_bits_gru(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, Xt, m->W, m->bias, at, m->Wi,
+                                     m->U, m->b, Xn, sv, &fused, s);
     } else {
       err = launch_transform_fwd(m->dtype, m->n_pad, m->H, m->E, Xt, m->W, m->bias, act->M, s);
       if (err == hipSuccess) err = launch_banded_fwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, act->M, at, s);
     }
-    if (err == hipSuccess) err = launch_gru_fwd(m->dtype, m->n_pad, m->H, at, Xt, m->Wi, m->U, m->b, Xn, sv, s);
+    if (err == hipSuccess && !fused)
+      err = launch_gru_fwd(m->dtype, m->n_pad, m->H, at, Xt, m->Wi, m->U, m->b, Xn, sv, s);
     if (err != hipSuccess) return device_status(err, "forward");
   }
   return GGNN_OK;

@@ -24,6 +24,9 @@ namespace ggnn {
                                   const float* bias, float* a, hipStream_t st);                                   \
   hipError_t launch_banded_bwd_bits(int n_pad, int B, int H, int E, const void* bits_t, const void* da, void* dM, \
                                     long ldm, hipStream_t st);                                                    \
+  hipError_t launch_step_fwd_bits_gru(int n_pad, int B, int H, int E, const void* bits, const void* X,           \
+                                      const void* W, const float* bias, float* a, const void* Wi, const void* U,  \
+                                      const float* bg, void* h_out, void* saved, bool* fused, hipStream_t st);    \
   hipError_t launch_step_bwd_bits(int n_pad, int B, int H, int E, const void* bits_t, const void* da,             \
                                   const void* W, const float* dX_in, float* dX_out, void* dM, long ldm,           \
                                   hipStream_t st);                                                                \
@@ -78,6 +81,14 @@ inline hipError_t launch_step_fwd_bits(int dt, int n_pad, int B, int H, int E, c
 inline hipError_t launch_banded_bwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits_t, const void* da,
                                          void* dM, long ldm, hipStream_t st) {
   return GGNN_DT_PICK(launch_banded_bwd_bits, n_pad, B, H, E, bits_t, da, dM, ldm, st);
+}
+// Forward step with the GRU update fused in where the shape allows (sets
+// *fused; otherwise only `a` is written and the caller runs the GRU).
+inline hipError_t launch_step_fwd_bits_gru(int dt, int n_pad, int B, int H, int E, const void* bits, const void* X,
+                                           const void* W, const float* bias, float* a, const void* Wi, const void* U,
+                                           const float* bg, void* h_out, void* saved, bool* fused, hipStream_t st) {
+  return GGNN_DT_PICK(launch_step_fwd_bits_gru, n_pad, B, H, E, bits, X, W, bias, a, Wi, U, bg, h_out, saved, fused,
+                      st);
 }
 // Fused reverse step: dM_e = A_e^T da stored node-major (rows of type e start
 // at row e * ldm of dM), dX_out = dX_in (or 0) + sum_e dM_e W_e^T.
