@@ -18,6 +18,7 @@
 // consecutive bytes of its bit row, and the staged node tile is read with
 // 16-byte LDS loads at the same offsets.
 #include "device_common.h"
+#include "gru_wave.h"
 #include "kernels.h"
 
 namespace ggnn {
@@ -167,18 +168,25 @@ struct BitsCfg {
 // the staged blocks): with TG = NTW = 2 group g completes row tile g (its own
 // partial plus the other group's), otherwise group 0 completes both; either
 // way a = (group 0 partial) + (group 1 partial).
-// GRU (forward, WDIR): the node update of Eq. 1 runs on the completed
+// GRU, forward (WDIR): the node update of Eq. 1 runs on the completed
 // aggregate in the same workgroup, so `a` goes to memory only for the
 // reverse pass and the next state X' and the gates (r | z | n) are written
 // here.  Wi^T and U^T are staged in LDS with the blocks; the GRU products
 // take a (hi + lo in bf16 mode), h and r*h as operand fragments straight
 // from registers (accumulator-compatible order).
+// GRU, reverse (WDIR): the completed dX of these nodes is dL/dh' of the
+// previous step's GRU, whose reverse (gru_bwd_wave) runs right here: it
+// writes that step's da (feature-major), dh and G^, so one launch covers a
+// whole reverse step.  Wi and U are staged in LDS (plain copies) with the
+// blocks; dX itself is written only when `out` is not NULL.
 // ---------------------------------------------------------------------------
 template <typename S, int H, int B, int WAVES, bool WDIR, int TG, bool REV, bool GRU>
 __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
     const uint8_t* __restrict__ bits, const S* __restrict__ X, const S* __restrict__ W, const float* __restrict__ bias,
     float* out, int n_pad, int E, const float* dX_in, S* __restrict__ dM, long ldm, const S* __restrict__ Wi,
-    const S* __restrict__ U, const float* __restrict__ bg, S* __restrict__ h_out, S* __restrict__ saved) {
+    const S* __restrict__ U, const float* __restrict__ bg, S* __restrict__ h_out, S* __restrict__ saved,
+    const S* __restrict__ rh_h, const S* __restrict__ rh_saved, S* __restrict__ rh_da, float* __restrict__ rh_dh,
+    S* __restrict__ rh_ghat) {
   using C = BitsCfg<S, H, B>;
   constexpr int NT = TG * WAVES * kWave;
   constexpr int V = C::V, KC = C::KC, VP = C::VP, RB = C::RB, NTW = C::NTW, WP = C::WP;
@@ -190,11 +198,13 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   static_assert(TG == 1 || WDIR, "type groups need the barrier-free loop");
   static_assert(TG == 1 || (TG - 1) * WAVES * kWave * NTW * MT * 16 <= (int)(C::NBUF * H * VP * sizeof(S)),
                 "partial sums must fit in the staged-block space");
-  static_assert(!GRU || (WDIR && !REV), "the GRU epilogue is a forward, direct-weight form");
-  constexpr int GP = H + V;                  // row pitch of the staged Wi^T, U^T
+  static_assert(!GRU || WDIR, "the GRU epilogues are direct-weight forms");
+  constexpr int GP = H + V;                  // forward: row pitch of the staged Wi^T, U^T ([3H][H] each)
+  constexpr int GR = 3 * H + V;              // reverse: row pitch of the staged Wi, U ([H][3H] each)
+  constexpr int GWN = !GRU ? 8 : (REV ? 2 * H * GR : 2 * 3 * H * GP);
   __shared__ __attribute__((aligned(16))) S vt[C::NBUF][H * VP];
   __shared__ __attribute__((aligned(16))) S wt[WDIR ? 8 : WC * WP];
-  __shared__ __attribute__((aligned(16))) S gw[GRU ? 2 * 3 * H * GP : 8];
+  __shared__ __attribute__((aligned(16))) S gw[GWN];
 
   const int nb = n_pad / B;
   constexpr int NW = C::RPW * WAVES;
@@ -273,27 +283,38 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         }
       }
     } else {
+      // With GRU, plain copies of Wi and U follow (gw[m][h * GR + c]).
       constexpr int UPB = H * (KC / V);            // 16-byte units per block
+      constexpr int UPW = H * (3 * H / V);         // 16-byte units per GRU weight
       constexpr int PB = 4;
-      const int total = (s_hi - s_lo + 1) * UPB;
+      const int nx = (s_hi - s_lo + 1) * UPB;
+      const int total = nx + (GRU ? 2 * UPW : 0);
       for (int base = 0; base < total; base += PB * NT) {
         u32x4 r[PB];
 #pragma unroll
         for (int u = 0; u < PB; ++u) {
           const int lin = base + u * NT + tid;
-          if (lin < total) {
+          if (lin < nx) {
             const int slot = s_lo + lin / UPB, rem = lin % UPB;
             const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
             r[u] = *reinterpret_cast<const u32x4*>(X + (size_t)h * n_pad + (k - 1 + slot) * B + c);
+          } else if (lin < total) {
+            const int w = lin - nx, m = w / UPW, rem = w % UPW;
+            const int h = rem / (3 * H / V), c = (rem % (3 * H / V)) * V;
+            r[u] = *reinterpret_cast<const u32x4*>((m ? U : Wi) + (size_t)h * 3 * H + c);
           }
         }
 #pragma unroll
         for (int u = 0; u < PB; ++u) {
           const int lin = base + u * NT + tid;
-          if (lin < total) {
+          if (lin < nx) {
             const int slot = s_lo + lin / UPB, rem = lin % UPB;
             const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
             *reinterpret_cast<u32x4*>(&vt[slot][h * VP + c]) = r[u];
+          } else if (lin < total) {
+            const int w = lin - nx, m = w / UPW, rem = w % UPW;
+            const int h = rem / (3 * H / V), c = (rem % (3 * H / V)) * V;
+            *reinterpret_cast<u32x4*>(&gw[(size_t)m * H * GR + h * GR + c]) = r[u];
           }
         }
       }
@@ -581,6 +602,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   for (int n = 0; n < NTW; ++n) {
     if (SPLIT && n != tg) continue;
     const size_t row = (size_t)(k * B + rw + 16 * n + q) * H + 4 * g;
+    f32x4 gg[MT];   // reverse: dX of this tile
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       f32x4 v = acc[n][m];
@@ -588,9 +610,14 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         const f32x4 b = *reinterpret_cast<const f32x4*>(dX_in + row + 16 * m);
         v = f32x4{b[0] + v[0], b[1] + v[1], b[2] + v[2], b[3] + v[3]};
       }
-      store4(out + row + 16 * m, v[0], v[1], v[2], v[3]);
+      gg[m] = v;
+      if (!REV || out) store4(out + row + 16 * m, v[0], v[1], v[2], v[3]);
     }
-    if constexpr (GRU) {
+    if constexpr (GRU && REV) {
+      gru_bwd_wave<S, H, GR>(gg, k * B + rw + 16 * n, q, g, rh_h, rh_saved, gw, gw + H * GR, rh_da, n_pad, rh_dh,
+                             rh_ghat);
+    }
+    if constexpr (GRU && !REV) {
       // GRU of Eq. 1 (Cho et al. 2014 form) for this tile's 16 nodes, as in
       // the stand-alone GRU kernel: D[feature][node] with A = rows of Wi^T /
       // U^T (LDS) and B = a (hi + lo), h, r*h fragments.
@@ -843,6 +870,12 @@ struct BitsArgs {
   void* h_out = nullptr;
   void* saved = nullptr;
   bool* fused_gru = nullptr;  // set to whether the GRU ran in the step
+  // mode 1 with the previous step's GRU reverse (when rh_da != NULL and supported)
+  const void* rh_h = nullptr;
+  const void* rh_saved = nullptr;
+  void* rh_da = nullptr;
+  float* rh_dh = nullptr;
+  void* rh_ghat = nullptr;
 };
 
 template <typename S, int H, int B>
@@ -874,12 +907,15 @@ hipError_t bits_launch(const BitsArgs& A, hipStream_t st) {
   // The GRU epilogue rides along only in the two-group form (a small grid,
   // where the separate GRU launch would cost most).
   const bool gru = A.mode == 0 && A.Wi != nullptr && C::WDIR && tg2;
-  if (A.fused_gru) *A.fused_gru = gru;
+  const bool rgru = A.mode == 1 && A.rh_da != nullptr && C::WDIR && tg2;
+  if (A.fused_gru) *A.fused_gru = gru || rgru;
+  if (rgru) op = nullptr;   // dX goes straight into the GRU reverse
 #define GGNN_STEP(WV, TGN, REVB, GRUB)                                                                        \
   hipLaunchKernelGGL((dev::step_bits_kernel<S, H, B, WV, C::WDIR, TGN, REVB, GRUB>), dim3(blocks),            \
                      dim3(TGN * WV * 64), 0, st, bp, vp, wp, A.bias, op, A.n_pad, A.E, A.dX_in, dmp, A.ldm,     \
                      static_cast<const S*>(A.Wi), static_cast<const S*>(A.U), A.bg, static_cast<S*>(A.h_out),  \
-                     static_cast<S*>(A.saved))
+                     static_cast<S*>(A.saved), static_cast<const S*>(A.rh_h), static_cast<const S*>(A.rh_saved), \
+                     static_cast<S*>(A.rh_da), A.rh_dh, static_cast<S*>(A.rh_ghat))
 #define GGNN_BITS_CASE(WV)                                                                                   \
   case WV:                                                                                                   \
     if constexpr (B / C::RPW >= WV && WV >= C::MINW) {                                                       \
@@ -889,6 +925,8 @@ hipError_t bits_launch(const BitsArgs& A, hipStream_t st) {
         GGNN_STEP(WV, (C::WDIR ? 2 : 1), false, false);                                                      \
       else if (A.mode == 0)                                                                                  \
         GGNN_STEP(WV, 1, false, false);                                                                      \
+      else if (A.mode == 1 && rgru)                                                                          \
+        GGNN_STEP(WV, (C::WDIR ? 2 : 1), true, C::WDIR);                                                     \
       else if (A.mode == 1 && tg2)                                                                           \
         GGNN_STEP(WV, (C::WDIR ? 2 : 1), true, false);                                                       \
       else if (A.mode == 1)                                                                                  \
@@ -954,6 +992,22 @@ hipError_t launch_step_fwd_bits_gru(int n_pad, int B, int H, int E, const void* 
 hipError_t launch_step_bwd_bits(int n_pad, int B, int H, int E, const void* bits_t_, const void* da, const void* W,
                                 const float* dX_in, float* dX_out, void* dM, long ldm, hipStream_t st) {
   return bits_t<dev::dt_t>(H, B, BitsArgs{1, bits_t_, da, W, nullptr, dX_out, dX_in, dM, ldm, n_pad, E}, st);
+}
+
+hipError_t launch_step_bwd_bits_gru(int n_pad, int B, int H, int E, const void* bits_t_, const void* da,
+                                    const void* W, const float* dX_in, float* dX_out, void* dM, long ldm,
+                                    const void* Wi, const void* U, const void* h_prev, const void* saved_prev,
+                                    void* da_prev, float* dh_prev, void* ghat_prev, bool* fused, hipStream_t st) {
+  BitsArgs A{1, bits_t_, da, W, nullptr, dX_out, dX_in, dM, ldm, n_pad, E};
+  A.Wi = Wi;
+  A.U = U;
+  A.rh_h = h_prev;
+  A.rh_saved = saved_prev;
+  A.rh_da = da_prev;
+  A.rh_dh = dh_prev;
+  A.rh_ghat = ghat_prev;
+  A.fused_gru = fused;
+  return bits_t<dev::dt_t>(H, B, A, st);
 }
 
 hipError_t launch_banded_bwd_bits(int n_pad, int B, int H, int E, const void* bits_t_, const void* da, void* dM,

@@ -54,16 +54,21 @@ inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 // aligned offset.
 namespace {
 struct BwdLayout {
-  size_t ghat, gru_part, tr_part, total;
+  size_t ghat, gru_part, tr_part, da2, dh2, total;
 };
 BwdLayout bwd_layout(const ggnn_model* m) {
   auto up = [](size_t x) { return (x + 255) / 256 * 256; };
   const long K = (long)m->T * m->n_pad;
+  const size_t es = m->dtype == GGNN_BF16 ? 2 : 4;
   BwdLayout l;
   l.ghat = 0;
   l.gru_part = up(ghat_bytes(m->dtype, K, m->H));
   l.tr_part = l.gru_part + up(gru_wgrad_workspace(K, m->H));
-  l.total = l.tr_part + transform_wgrad_workspace(K, m->H, m->E);
+  // second da / dh buffers: the fused bit-band reverse step reads one step's
+  // and writes the previous step's
+  l.da2 = l.tr_part + up(transform_wgrad_workspace(K, m->H, m->E));
+  l.dh2 = l.da2 + up((size_t)m->H * m->n_pad * es);
+  l.total = l.dh2 + (size_t)m->n_pad * m->H * sizeof(float);
   return l;
 }
 }  // namespace
@@ -326,27 +331,48 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
   char* ghat = ws + L.ghat;
   // Node passes, t = T-1..0.  The weight gradients are sums over steps and
   // nodes of products of per-step quantities, so each step only stores its
-  // factors (G^ of step t, dM of step t at column offset t * n_pad) and the
-  // sums run once, over all T * n_pad rows, after the loop.
-  for (int t = m->T - 1; t >= 0; --t) {
-    const char* Xt = static_cast<const char*>(act->X) + t * xs * es;
-    const char* sv = static_cast<const char*>(act->saved) + t * 3 * xs * es;
-    char* ght = ghat + t * 3 * xs * es;
-    char* dMt = static_cast<char*>(gr->dM) + (size_t)t * m->n_pad * es;
-    hipError_t err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xt, sv, m->Wi, m->U, gr->da, gr->dh,
-                                          ght, s);
+  // factors (G^ of step t; dM of step t at offset t * n_pad) and the sums
+  // run once, over all T * n_pad rows, after the loop.
+  auto Xs = [&](int t) { return static_cast<const char*>(act->X) + t * xs * es; };
+  auto Ss = [&](int t) { return static_cast<const char*>(act->saved) + t * 3 * xs * es; };
+  auto Gs = [&](int t) { return ghat + t * 3 * xs * es; };
+  if (m->band_format == GGNN_BAND_BITS) {
+    // Bit band: the reverse step of t also runs the GRU reverse of t-1 when
+    // the kernel shape allows (one launch per step); da and dh alternate
+    // between two buffers (step t's are read while t-1's are written).
+    void* da_b[2] = {gr->da, ws + L.da2};
+    float* dh_b[2] = {gr->dh, reinterpret_cast<float*>(ws + L.dh2)};
+    int cur = 0;
+    hipError_t err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xs(m->T - 1), Ss(m->T - 1), m->Wi, m->U,
+                                          da_b[0], dh_b[0], Gs(m->T - 1), s);
     if (err != hipSuccess) return device_status(err, "backward");
-    if (m->band_format == GGNN_BAND_BITS) {
-      // dM node-major: step t in rows [t*n_pad, (t+1)*n_pad) of each type.
-      char* dMr = static_cast<char*>(gr->dM) + (size_t)t * m->n_pad * m->H * es;
-      err = launch_step_bwd_bits(m->dtype, m->n_pad, m->B, m->H, m->E, m->band_t, gr->da, m->W, gr->dh, gr->dX,
-                                 dMr, K, s);
-    } else {
-      err = launch_banded_bwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, gr->da, dMt, K, s);
+    for (int t = m->T - 1; t >= 0; --t) {
+      char* dMr = static_cast<char*>(gr->dM) + (size_t)t * m->n_pad * m->H * es;   // node-major rows of step t
+      if (t > 0) {
+        bool fused = false;
+        err = launch_step_bwd_bits_gru(m->dtype, m->n_pad, m->B, m->H, m->E, m->band_t, da_b[cur], m->W, dh_b[cur],
+                                       gr->dX, dMr, K, m->Wi, m->U, Xs(t - 1), Ss(t - 1), da_b[1 - cur],
+                                       dh_b[1 - cur], Gs(t - 1), &fused, s);
+        if (err == hipSuccess && !fused)
+          err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xs(t - 1), Ss(t - 1), m->Wi, m->U,
+                                     da_b[1 - cur], dh_b[1 - cur], Gs(t - 1), s);
+      } else {
+        err = launch_step_bwd_bits(m->dtype, m->n_pad, m->B, m->H, m->E, m->band_t, da_b[cur], m->W, dh_b[cur],
+                                   gr->dX, dMr, K, s);
+      }
+      if (err != hipSuccess) return device_status(err, "backward");
+      cur ^= 1;
+    }
+  } else {
+    for (int t = m->T - 1; t >= 0; --t) {
+      char* dMt = static_cast<char*>(gr->dM) + (size_t)t * m->n_pad * es;   // feature-major columns of step t
+      hipError_t err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xs(t), Ss(t), m->Wi, m->U, gr->da,
+                                            gr->dh, Gs(t), s);
+      if (err == hipSuccess) err = launch_banded_bwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, gr->da, dMt, K, s);
       if (err == hipSuccess)
         err = launch_transform_bwd_dx(m->dtype, m->n_pad, m->H, m->E, m->W, dMt, K, gr->dh, gr->dX, s);
+      if (err != hipSuccess) return device_status(err, "backward");
     }
-    if (err != hipSuccess) return device_status(err, "backward");
   }
   hipError_t err = launch_gru_wgrad(m->dtype, K, m->H, act->a, act->X, act->saved, ghat, gr->dWi, gr->dU, gr->db,
                                     ws + L.gru_part, s);

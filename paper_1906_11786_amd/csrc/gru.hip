@@ -14,16 +14,12 @@
 // fragment of the next product: (r*h) U_n in the forward and every product of
 // the backward chain without any cross-lane exchange.
 #include "device_common.h"
+#include "gru_wave.h"
 #include "kernels.h"
 
 namespace ggnn {
 namespace dev {
 
-// Fragment of a node-major row in accumulator-compatible k order.
-template <typename S>
-__device__ __forceinline__ frag_t<S> rowfrag(const S* row, int kk, int g) {
-  return load4x2(row + 32 * kk + 4 * g, row + 32 * kk + 16 + 4 * g);
-}
 // Stage the transpose of a 32-column slice of a [H][3H] weight into LDS:
 // dst[f * PW + i] = src[i * 3H + col0 + f], f < 32, i < H.
 template <typename S, int H, int PW, int NT>
@@ -162,17 +158,10 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_fwd_kernel(const float* __r
 }
 
 // ---------------------------------------------------------------------------
-// Backward, per node (wave w: 16 nodes, lane % 16 = node).  With
-// g = dL/dh', dn = g(1-z), dz = g(h-n), n^ = dn(1-n^2), z^ = dz z(1-z),
-// q = n^ U_n^T, r^ = q h r(1-r):
-//   dh = g z + q r + r^ U_r^T + z^ U_z^T,   da = [r^ z^ n^] Wi^T.
-// The gate gradients are kept in registers as operand fragments
-// (accumulator-compatible order) and dh as an accumulator across the four
-// phases; G^ = [r^ z^ n^] is also written to `ghat` (node-major
-// [n_pad][3H]) for the weight-gradient pass.  For H <= 64 the weights are
-// staged once per workgroup in LDS (plain copies: the reverse products read
-// rows of Wi and U, contiguous in the gate dimension); larger H reads their
-// fragments from global memory (cached).
+// Backward, per node (wave w: 16 nodes, lane % 16 = node): gru_bwd_wave.
+// For H <= 64 the weights are staged once per workgroup in LDS (plain
+// copies: the reverse products read rows of Wi and U, contiguous in the gate
+// dimension); larger H reads their fragments from global memory (cached).
 // ---------------------------------------------------------------------------
 template <typename S, int H, int WAVES>
 __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __restrict__ gin, const S* __restrict__ h,
@@ -180,7 +169,6 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
                                                                  const S* __restrict__ U, S* __restrict__ daT,
                                                                  float* __restrict__ dh, S* __restrict__ ghat,
                                                                  int n_pad) {
-  constexpr int KS = H / 32;
   constexpr int MTL = H / 16;
   constexpr int NT = WAVES * kWave;
   constexpr int V = 16 / sizeof(S);
@@ -200,88 +188,16 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
       *reinterpret_cast<u32x4*>(&wl[0][r * WROW + c]) = *reinterpret_cast<const u32x4*>(Wi + (size_t)r * 3 * H + c);
       *reinterpret_cast<u32x4*>(&wl[1][r * WROW + c]) = *reinterpret_cast<const u32x4*>(U + (size_t)r * 3 * H + c);
     }
+    __syncthreads();
   }
-  // Weight row fragment (row `row` of Wi or U, gate `gate`, step kk).
-  auto wfrag = [&](int which, int row, int gate, int kk) __attribute__((always_inline)) {
-    if constexpr (LDSW) {
-      const S* p = &wl[which][row * WROW + gate * H];
-      return rowfrag<S>(p, kk, g);
-    } else {
-      const S* p = (which ? U : Wi) + (size_t)row * 3 * H + gate * H;
-      return rowfrag<S>(p, kk, g);
-    }
-  };
-
-  // Phase 1: elementwise part, kept in registers.
-  frag_t<S> gf[3][KS];          // r^, z^, n^ as operand fragments
-  f32x4 dacc[MTL];              // dh accumulator (D layout: features 16m + 4g + j)
-  float zv[8], nv[8];
-  if (valid) {
-    const S* sv = saved + (size_t)node * 3 * H;
-#pragma unroll
-    for (int m = 0; m < MTL; ++m) {
-      const int f = 16 * m + 4 * g;
-      const f32x4 gg = *reinterpret_cast<const f32x4*>(gin + (size_t)node * H + f);
-      const f32x4 z4 = load4f(sv + H + f), n4 = load4f(sv + 2 * H + f);
-      const f32x4 h4 = load4f(h + (size_t)node * H + f);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float dn = gg[j] * (1.f - z4[j]);
-        const float dz = gg[j] * (h4[j] - n4[j]);
-        dacc[m][j] = gg[j] * z4[j];
-        nv[4 * (m % 2) + j] = dn * (1.f - n4[j] * n4[j]);
-        zv[4 * (m % 2) + j] = dz * z4[j] * (1.f - z4[j]);
-      }
-      if (m % 2 == 1) {
-        gf[2][m / 2] = pack8<S>(nv);
-        gf[1][m / 2] = pack8<S>(zv);
-      }
-      S* gh = ghat + (size_t)node * 3 * H;
-      store4(gh + H + f, zv[4 * (m % 2)], zv[4 * (m % 2) + 1], zv[4 * (m % 2) + 2], zv[4 * (m % 2) + 3]);
-      store4(gh + 2 * H + f, nv[4 * (m % 2)], nv[4 * (m % 2) + 1], nv[4 * (m % 2) + 2], nv[4 * (m % 2) + 3]);
-    }
-  }
-  if constexpr (LDSW) __syncthreads();
   if (!valid) return;   // no barrier follows
-  // Phase 2: q = n^ U_n^T (D[f_in][node]); r^ and the q r term of dh.
-  {
-    const S* sv = saved + (size_t)node * 3 * H;
-    float rv[8];
+  f32x4 gg[MTL];
 #pragma unroll
-    for (int m = 0; m < MTL; ++m) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) mma(acc, wfrag(1, 16 * m + q, 2, kk), gf[2][kk]);
-      const int f = 16 * m + 4 * g;
-      const f32x4 r4 = load4f(sv + f), h4 = load4f(h + (size_t)node * H + f);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        rv[4 * (m % 2) + j] = acc[j] * h4[j] * r4[j] * (1.f - r4[j]);
-        dacc[m][j] += acc[j] * r4[j];
-      }
-      store4(ghat + (size_t)node * 3 * H + f, rv[4 * (m % 2)], rv[4 * (m % 2) + 1], rv[4 * (m % 2) + 2],
-             rv[4 * (m % 2) + 3]);
-      if (m % 2 == 1) gf[0][m / 2] = pack8<S>(rv);
-    }
-  }
-  // Phase 3: da = G^ Wi^T, D[node][f_in]: four consecutive nodes per lane.
-#pragma unroll
-  for (int n = 0; n < MTL; ++n) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int gate = 0; gate < 3; ++gate)
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) mma(acc, gf[gate][kk], wfrag(0, 16 * n + q, gate, kk));
-    store4(daT + (size_t)(16 * n + q) * n_pad + n0 + 4 * g, acc[0], acc[1], acc[2], acc[3]);
-  }
-  // Phase 4: dh += r^ U_r^T + z^ U_z^T, D[f_in][node]; one store of dh.
-#pragma unroll
-  for (int m = 0; m < MTL; ++m) {
-#pragma unroll
-    for (int gate = 0; gate < 2; ++gate)
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) mma(dacc[m], wfrag(1, 16 * m + q, gate, kk), gf[gate][kk]);
-    store4(dh + (size_t)node * H + 16 * m + 4 * g, dacc[m][0], dacc[m][1], dacc[m][2], dacc[m][3]);
+  for (int m = 0; m < MTL; ++m) gg[m] = *reinterpret_cast<const f32x4*>(gin + (size_t)node * H + 16 * m + 4 * g);
+  if constexpr (LDSW) {
+    gru_bwd_wave<S, H, WROW>(gg, n0, q, g, h, saved, &wl[0][0], &wl[1][0], daT, n_pad, dh, ghat);
+  } else {
+    gru_bwd_wave<S, H, 3 * H>(gg, n0, q, g, h, saved, Wi, U, daT, n_pad, dh, ghat);
   }
 }
 

@@ -1,0 +1,108 @@
+// Reverse of the GRU node update (Eq. 1's GRU, Cho et al. 2014 form) for
+// the 16 nodes of one wave, shared by the stand-alone GRU reverse kernel and
+// the fused bit-band reverse step.
+//
+// Lanes: q = lane % 16 is the node (n0 + q), g = lane / 16.  With
+// g' = dL/dh', dn = g'(1-z), dz = g'(h-n), n^ = dn(1-n^2), z^ = dz z(1-z),
+// q' = n^ U_n^T, r^ = q' h r(1-r):
+//   dh = g' z + q' r + r^ U_r^T + z^ U_z^T,   da = [r^ z^ n^] Wi^T.
+// The gate gradients are kept in registers as operand fragments
+// (accumulator-compatible order: features 32kk + 4g + {0..3} and
+// 32kk + 16 + 4g + {0..3}) and dh as an accumulator across the phases;
+// G^ = [r^ z^ n^] is also written to `ghat` (node-major [.][3H]) for the
+// weight-gradient pass.
+#pragma once
+
+#include "device_common.h"
+
+namespace ggnn {
+namespace dev {
+
+// Fragment of a node-major row in accumulator-compatible k order.
+template <typename S>
+__device__ __forceinline__ frag_t<S> rowfrag(const S* row, int kk, int g) {
+  return load4x2(row + 32 * kk + 4 * g, row + 32 * kk + 16 + 4 * g);
+}
+
+// gg[m]: dL/dh' for features 16m + 4g + {0..3} of node n0 + q.
+// Wi, U: [H][3H] weights with row pitch WP (LDS copies or global memory).
+// Writes daT[f][n0 + 4g + j] (feature-major, row pitch ld), dh[node][.]
+// (node-major, float) and ghat[node][.] (node-major, 3H).
+template <typename S, int H, int WP>
+__device__ __forceinline__ void gru_bwd_wave(const f32x4 (&gg)[H / 16], int n0, int q, int g, const S* h,
+                                             const S* saved, const S* Wi, const S* U, S* daT, long ld, float* dh,
+                                             S* ghat) {
+  constexpr int KS = H / 32;
+  constexpr int MTL = H / 16;
+  const int node = n0 + q;
+  auto wfrag = [&](int which, int row, int gate, int kk) __attribute__((always_inline)) {
+    return rowfrag<S>((which ? U : Wi) + (size_t)row * WP + gate * H, kk, g);
+  };
+  // Phase 1: elementwise part, kept in registers.
+  frag_t<S> gf[3][KS];          // r^, z^, n^ as operand fragments
+  f32x4 dacc[MTL];              // dh accumulator (D layout: features 16m + 4g + j)
+  float zv[8], nv[8];
+  const S* sv = saved + (size_t)node * 3 * H;
+  S* gh = ghat + (size_t)node * 3 * H;
+#pragma unroll
+  for (int m = 0; m < MTL; ++m) {
+    const int f = 16 * m + 4 * g;
+    const f32x4 z4 = load4f(sv + H + f), n4 = load4f(sv + 2 * H + f);
+    const f32x4 h4 = load4f(h + (size_t)node * H + f);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float dn = gg[m][j] * (1.f - z4[j]);
+      const float dz = gg[m][j] * (h4[j] - n4[j]);
+      dacc[m][j] = gg[m][j] * z4[j];
+      nv[4 * (m % 2) + j] = dn * (1.f - n4[j] * n4[j]);
+      zv[4 * (m % 2) + j] = dz * z4[j] * (1.f - z4[j]);
+    }
+    if (m % 2 == 1) {
+      gf[2][m / 2] = pack8<S>(nv);
+      gf[1][m / 2] = pack8<S>(zv);
+    }
+    store4(gh + H + f, zv[4 * (m % 2)], zv[4 * (m % 2) + 1], zv[4 * (m % 2) + 2], zv[4 * (m % 2) + 3]);
+    store4(gh + 2 * H + f, nv[4 * (m % 2)], nv[4 * (m % 2) + 1], nv[4 * (m % 2) + 2], nv[4 * (m % 2) + 3]);
+  }
+  // Phase 2: q' = n^ U_n^T (D[f_in][node]); r^ and the q' r term of dh.
+  {
+    float rv[8];
+#pragma unroll
+    for (int m = 0; m < MTL; ++m) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) mma(acc, wfrag(1, 16 * m + q, 2, kk), gf[2][kk]);
+      const int f = 16 * m + 4 * g;
+      const f32x4 r4 = load4f(sv + f), h4 = load4f(h + (size_t)node * H + f);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        rv[4 * (m % 2) + j] = acc[j] * h4[j] * r4[j] * (1.f - r4[j]);
+        dacc[m][j] += acc[j] * r4[j];
+      }
+      store4(gh + f, rv[4 * (m % 2)], rv[4 * (m % 2) + 1], rv[4 * (m % 2) + 2], rv[4 * (m % 2) + 3]);
+      if (m % 2 == 1) gf[0][m / 2] = pack8<S>(rv);
+    }
+  }
+  // Phase 3: da = G^ Wi^T, D[node][f_in]: four consecutive nodes per lane.
+#pragma unroll
+  for (int n = 0; n < MTL; ++n) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int gate = 0; gate < 3; ++gate)
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) mma(acc, gf[gate][kk], wfrag(0, 16 * n + q, gate, kk));
+    store4(daT + (size_t)(16 * n + q) * ld + n0 + 4 * g, acc[0], acc[1], acc[2], acc[3]);
+  }
+  // Phase 4: dh += r^ U_r^T + z^ U_z^T, D[f_in][node]; one store of dh.
+#pragma unroll
+  for (int m = 0; m < MTL; ++m) {
+#pragma unroll
+    for (int gate = 0; gate < 2; ++gate)
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) mma(dacc[m], wfrag(1, 16 * m + q, gate, kk), gf[gate][kk]);
+    store4(dh + (size_t)node * H + 16 * m + 4 * g, dacc[m][0], dacc[m][1], dacc[m][2], dacc[m][3]);
+  }
+}
+
+}  // namespace dev
+}  // namespace ggnn

@@ -27,6 +27,11 @@ namespace ggnn {
   hipError_t launch_step_fwd_bits_gru(int n_pad, int B, int H, int E, const void* bits, const void* X,           \
                                       const void* W, const float* bias, float* a, const void* Wi, const void* U,  \
                                       const float* bg, void* h_out, void* saved, bool* fused, hipStream_t st);    \
+  hipError_t launch_step_bwd_bits_gru(int n_pad, int B, int H, int E, const void* bits_t, const void* da,         \
+                                      const void* W, const float* dX_in, float* dX_out, void* dM, long ldm,       \
+                                      const void* Wi, const void* U, const void* h_prev, const void* saved_prev,  \
+                                      void* da_prev, float* dh_prev, void* ghat_prev, bool* fused,                \
+                                      hipStream_t st);                                                            \
   hipError_t launch_step_bwd_bits(int n_pad, int B, int H, int E, const void* bits_t, const void* da,             \
                                   const void* W, const float* dX_in, float* dX_out, void* dM, long ldm,           \
                                   hipStream_t st);                                                                \
@@ -89,6 +94,18 @@ inline hipError_t launch_step_fwd_bits_gru(int dt, int n_pad, int B, int H, int 
                                            const float* bg, void* h_out, void* saved, bool* fused, hipStream_t st) {
   return GGNN_DT_PICK(launch_step_fwd_bits_gru, n_pad, B, H, E, bits, X, W, bias, a, Wi, U, bg, h_out, saved, fused,
                       st);
+}
+// Reverse step that continues, where the shape allows (sets *fused), with
+// the previous step's GRU reverse on the completed dX: writes da_prev
+// (feature-major), dh_prev and ghat_prev; dX_out may then be NULL.  When
+// not fused, dX_out is written and the caller runs the GRU reverse.
+inline hipError_t launch_step_bwd_bits_gru(int dt, int n_pad, int B, int H, int E, const void* bits_t, const void* da,
+                                           const void* W, const float* dX_in, float* dX_out, void* dM, long ldm,
+                                           const void* Wi, const void* U, const void* h_prev, const void* saved_prev,
+                                           void* da_prev, float* dh_prev, void* ghat_prev, bool* fused,
+                                           hipStream_t st) {
+  return GGNN_DT_PICK(launch_step_bwd_bits_gru, n_pad, B, H, E, bits_t, da, W, dX_in, dX_out, dM, ldm, Wi, U, h_prev,
+                      saved_prev, da_prev, dh_prev, ghat_prev, fused, st);
 }
 // Fused reverse step: dM_e = A_e^T da stored node-major (rows of type e start
 // at row e * ldm of dM), dX_out = dX_in (or 0) + sum_e dM_e W_e^T.
