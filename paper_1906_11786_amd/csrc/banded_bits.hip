@@ -15,8 +15,9 @@
 //
 // k order of the aggregation: inside a chunk of KC nodes, lane group g owns
 // the contiguous columns [g*KC/4, (g+1)*KC/4), so each lane reads KC/32
-// consecutive bytes of its bit row, and the staged node tile is read with
-// 16-byte LDS loads at the same offsets.
+// consecutive bytes of its bit row.  The staged node tile is kept in LDS in
+// fragment order (frag_off below), so every fragment read of a wave covers
+// 1 KB of consecutive bytes.
 #include "device_common.h"
 #include "gru_wave.h"
 #include "kernels.h"
@@ -79,11 +80,28 @@ __device__ __forceinline__ void store_pair(bf16s* p, uint32_t lo16, uint32_t hi1
   *reinterpret_cast<uint32_t*>(p) = (lo16 & 0xFFFFu) | (hi16 << 16);
 }
 
-// Stage nodes [n0, n0 + KC) of a node-major [n][H] array into LDS as
-// dst[h * VP + c] (feature rows).  Each thread moves a pair of consecutive
-// nodes for eight features and writes 2-element words, so consecutive lanes
-// write consecutive words.
-template <typename S, int H, int KC, int VP, int NT>
+// Fragment order of a staged chunk (KC nodes x H features) in LDS.  The
+// eight elements a lane feeds to one matrix-core step (feature h, nodes
+// g*KC/4 + 8kk + 0..7 of the chunk) are NV = 8/V 16-byte vectors; for each
+// (k step kk, feature tile h/16, vector) the 64 lanes' vectors are
+// contiguous.  The LDS serves 16 lanes' 16-byte reads per pass from 64
+// four-byte banks, so a fragment read (16 consecutive lanes on 256
+// consecutive bytes) never conflicts; reading feature rows at a padded
+// pitch instead took two passes per read.
+// Staged node chunk: fragment (kk, feature tile h/16).
+template <typename S, int H, int KC>
+__device__ __forceinline__ int frag_off(int h, int c) {
+  const int g = c / (KC / 4), kk = (c % (KC / 4)) / 8;
+  return fo<S>(kk * (H / 16) + h / 16, h % 16 + 16 * g, c % 8);
+}
+template <typename S, int H>
+__device__ __forceinline__ frag_t<S> load_frag(const S* v, int kk, int m, int lane) {
+  return load_fragi<S>(v, kk * (H / 16) + m, lane);
+}
+// Stage nodes [n0, n0 + KC) of a node-major [n][H] array into LDS in
+// fragment order.  Each thread moves a pair of consecutive nodes for eight
+// features and writes 2-element words.
+template <typename S, int H, int KC, int NT>
 __device__ __forceinline__ void stage_nodes_T(S* dst, const S* src, int n0, int tid) {
   constexpr int PAIRS = KC / 2;
   for (int lin = tid; lin < PAIRS * (H / 8); lin += NT) {
@@ -94,27 +112,28 @@ __device__ __forceinline__ void stage_nodes_T(S* dst, const S* src, int n0, int 
       u32x4 x1 = *reinterpret_cast<const u32x4*>(p0 + H);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        store_pair(&dst[(f0 + 2 * i) * VP + 2 * cp], x0[i] & 0xFFFFu, x1[i] & 0xFFFFu);
-        store_pair(&dst[(f0 + 2 * i + 1) * VP + 2 * cp], x0[i] >> 16, x1[i] >> 16);
+        store_pair(&dst[frag_off<S, H, KC>(f0 + 2 * i, 2 * cp)], x0[i] & 0xFFFFu, x1[i] & 0xFFFFu);
+        store_pair(&dst[frag_off<S, H, KC>(f0 + 2 * i + 1, 2 * cp)], x0[i] >> 16, x1[i] >> 16);
       }
     } else {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         typedef float f32x2 __attribute__((ext_vector_type(2)));
-        *reinterpret_cast<f32x2*>(&dst[(f0 + i) * VP + 2 * cp]) = f32x2{p0[i], p0[H + i]};
+        *reinterpret_cast<f32x2*>(&dst[frag_off<S, H, KC>(f0 + i, 2 * cp)]) = f32x2{p0[i], p0[H + i]};
       }
     }
   }
 }
 
 // Stage columns [n0, n0 + KC) of a feature-major [H][n_pad] array into LDS
-// as dst[h * VP + c] (plain 16-byte copies).
-template <typename S, int H, int KC, int VP, int NT>
+// in fragment order (16-byte copies: a unit is one fragment vector).
+template <typename S, int H, int KC, int NT>
 __device__ __forceinline__ void stage_cols(S* dst, const S* src, int n_pad, int n0, int tid) {
   constexpr int V = 16 / sizeof(S);
   for (int lin = tid; lin < H * (KC / V); lin += NT) {
     const int h = lin / (KC / V), c = (lin % (KC / V)) * V;
-    *reinterpret_cast<u32x4*>(&dst[h * VP + c]) = *reinterpret_cast<const u32x4*>(src + (size_t)h * n_pad + n0 + c);
+    *reinterpret_cast<u32x4*>(&dst[frag_off<S, H, KC>(h, c)]) =
+        *reinterpret_cast<const u32x4*>(src + (size_t)h * n_pad + n0 + c);
   }
 }
 
@@ -130,10 +149,10 @@ struct BitsCfg {
   static constexpr int RB = KC / 32;        // bit-row bytes per lane per chunk (= k steps per chunk)
   static constexpr int RPW = H >= 256 ? 16 : 32;   // rows per wave
   static constexpr int NTW = RPW / 16;      // 16-row tiles per wave
-  // Smallest workgroup (waves) launched; the fp32 forms with H >= 128 keep
-  // at least two waves (their one-wave forms are not built: the code
-  // generator fails on them in VGPR-only matrix-core mode).
-  static constexpr int MINW = (sizeof(S) == 4 && H >= 128 && B / RPW >= 2) ? 2 : 1;
+  // Smallest workgroup (waves) launched; the fp32 forms with H >= 128 and
+  // the bf16 forms with H = 256 keep at least two waves (their one-wave
+  // forms are not built: the code generator fails on them).
+  static constexpr int MINW = ((sizeof(S) == 4 && H >= 128) || H >= 256) && B / RPW >= 2 ? 2 : 1;
   // Forward, H <= 64 with the blocks staged: the transform's weight
   // fragments are read straight from global memory (L1/L2 resident, issued
   // at the top of each type and used at its end), so no weight staging sits
@@ -199,9 +218,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   static_assert(TG == 1 || (TG - 1) * WAVES * kWave * NTW * MT * 16 <= (int)(C::NBUF * H * VP * sizeof(S)),
                 "partial sums must fit in the staged-block space");
   static_assert(!GRU || WDIR, "the GRU epilogues are direct-weight forms");
-  constexpr int GP = H + V;                  // forward: row pitch of the staged Wi^T, U^T ([3H][H] each)
-  constexpr int GR = 3 * H + V;              // reverse: row pitch of the staged Wi, U ([H][3H] each)
-  constexpr int GWN = !GRU ? 8 : (REV ? 2 * H * GR : 2 * 3 * H * GP);
+  constexpr int GWN = !GRU ? 8 : 2 * 3 * H * H;   // Wi and U in fragment order
   __shared__ __attribute__((aligned(16))) S vt[C::NBUF][H * VP];
   __shared__ __attribute__((aligned(16))) S wt[WDIR ? 8 : WC * WP];
   __shared__ __attribute__((aligned(16))) S gw[GWN];
@@ -239,15 +256,14 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
     if (e_lo + 1 < e_hi) load_type(e_lo + 1, nx2);
   }
 
-  // Staging of the three blocks as feature rows, vt[s][f * VP + c] =
+  // Staging of the three blocks in fragment order, vt[s][frag_off(f, c)] =
   // node (k-1+s)*B + c, feature f.  Forward: V x V tiles of node-major X,
-  // transposed on the LDS write (consecutive lanes take tiles consecutive
-  // along the destination row: conflict-free 16-byte stores, loads of whole
-  // 128-byte lines).  Reverse: plain 16-byte copies of feature-major da.
+  // transposed in registers (loads of whole 128-byte lines), one 16-byte
+  // store per tile row.  Reverse: plain 16-byte copies of feature-major da.
   // Each thread issues the loads of up to PB units before its writes.
   if constexpr (C::ALL) {
     if constexpr (!REV) {
-      // With GRU, the tiles of Wi and U follow (gw[m][c * GP + h] = Wi / U[h][c]).
+      // With GRU, the tiles of Wi and U follow (fragment order, gru_fwd_idx).
       constexpr int XT = (KC / V) * (H / V);       // tiles per block
       constexpr int GT = (H / V) * (3 * H / V);    // tiles per GRU weight
       constexpr int PB = 2;
@@ -274,16 +290,28 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
           if (lin < nx) {
             const int slot = s_lo + lin / XT, rem = lin % XT;
             const int cq = rem % (KC / V), fq = rem / (KC / V);
-            tile_store_T<S, VP>(&vt[slot][(V * fq) * VP + V * cq], r[u]);
+#pragma unroll
+            for (int x = 0; x < V; ++x)
+              *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(V * fq + x, V * cq)]) = tile_row_T<S>(r[u], x);
           } else if (lin < total) {
             const int w = lin - nx, m = w / GT, rem = w % GT;
             const int hq = rem % (H / V), cq = rem / (H / V);
-            tile_store_T<S, GP>(&gw[(size_t)m * 3 * H * GP + (V * cq) * GP + V * hq], r[u]);
+            // row x of the transposed tile: gate column V*cq + x, input
+            // features V*hq .. V*hq + V - 1 (runs of four)
+#pragma unroll
+            for (int x = 0; x < V; ++x) {
+              const u32x4 o = tile_row_T<S>(r[u], x);
+              const S* po = reinterpret_cast<const S*>(&o);
+              const int col = V * cq + x;
+#pragma unroll
+              for (int i = 0; i < V; i += 4)
+                put4<S>(gw, gru_fwd_idx<S, H>(m, col / 16, (V * hq + i) / 32), col % 16, V * hq + i, po + i);
+            }
           }
         }
       }
     } else {
-      // With GRU, plain copies of Wi and U follow (gw[m][h * GR + c]).
+      // With GRU, Wi and U follow (fragment order, gru_rev_idx).
       constexpr int UPB = H * (KC / V);            // 16-byte units per block
       constexpr int UPW = H * (3 * H / V);         // 16-byte units per GRU weight
       constexpr int PB = 4;
@@ -310,11 +338,16 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
           if (lin < nx) {
             const int slot = s_lo + lin / UPB, rem = lin % UPB;
             const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
-            *reinterpret_cast<u32x4*>(&vt[slot][h * VP + c]) = r[u];
+            *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(h, c)]) = r[u];
           } else if (lin < total) {
             const int w = lin - nx, m = w / UPW, rem = w % UPW;
             const int h = rem / (3 * H / V), c = (rem % (3 * H / V)) * V;
-            *reinterpret_cast<u32x4*>(&gw[(size_t)m * H * GR + h * GR + c]) = r[u];
+            // input feature h, gate columns c .. c + V - 1 (runs of four)
+            const S* po = reinterpret_cast<const S*>(&r[u]);
+#pragma unroll
+            for (int i = 0; i < V; i += 4)
+              put4<S>(gw, gru_rev_idx<S, H>(m, h / 16, (c + i) / H, ((c + i) % H) / 32), h % 16, (c + i) % H,
+                      po + i);
           }
         }
       }
@@ -438,9 +471,9 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         if constexpr (!C::ALL) {
           __syncthreads();
           if constexpr (REV) {
-            stage_cols<S, H, KC, VP, NT>(vt[0], X, n_pad, (k - 1 + s) * B + c0, tid);
+            stage_cols<S, H, KC, NT>(vt[0], X, n_pad, (k - 1 + s) * B + c0, tid);
           } else {
-            stage_nodes_T<S, H, KC, VP, NT>(vt[0], X, (k - 1 + s) * B + c0, tid);
+            stage_nodes_T<S, H, KC, NT>(vt[0], X, (k - 1 + s) * B + c0, tid);
           }
           __syncthreads();
         }
@@ -462,7 +495,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
           for (int n = 0; n < NTW; ++n) bf[n] = bits_frag<S>(rb[n].byte(kk));
 #pragma unroll
           for (int m = 0; m < MT; ++m) {
-            const frag_t<S> af = load8(&v[(16 * m + q) * VP + g * (KC / 4) + 8 * kk]);
+            const frag_t<S> af = load_frag<S, H>(v, kk, m, lane);
 #pragma unroll
             for (int n = 0; n < NTW; ++n) mma(pre[n][m], af, bf[n]);
           }
@@ -614,13 +647,16 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
       if (!REV || out) store4(out + row + 16 * m, v[0], v[1], v[2], v[3]);
     }
     if constexpr (GRU && REV) {
-      gru_bwd_wave<S, H, GR>(gg, k * B + rw + 16 * n, q, g, rh_h, rh_saved, gw, gw + H * GR, rh_da, n_pad, rh_dh,
+      auto wl = [&](int which, int row, int gate, int kk) __attribute__((always_inline)) {
+        return load_fragi<S>(gw, gru_rev_idx<S, H>(which, row / 16, gate, kk), lane);
+      };
+      gru_bwd_wave<S, H>(gg, k * B + rw + 16 * n, q, g, rh_h, rh_saved, wl, rh_da, n_pad, rh_dh,
                              rh_ghat);
     }
     if constexpr (GRU && !REV) {
       // GRU of Eq. 1 (Cho et al. 2014 form) for this tile's 16 nodes, as in
-      // the stand-alone GRU kernel: D[feature][node] with A = rows of Wi^T /
-      // U^T (LDS) and B = a (hi + lo), h, r*h fragments.
+      // the stand-alone GRU kernel: D[feature][node] with A = Wi^T / U^T
+      // fragments (LDS) and B = a (hi + lo), h, r*h fragments.
       constexpr int KS = H / 32;
       const int node = k * B + rw + 16 * n + q;
       frag_t<S> af[NP][KS], hf[KS], rh[KS];
@@ -639,65 +675,76 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         }
         hf[kk] = load4x2(X + (size_t)node * H + 32 * kk + 4 * g, X + (size_t)node * H + 32 * kk + 16 + 4 * g);
       }
-      auto gfrag = [&](int mat, int col, int kk) __attribute__((always_inline)) {   // rows col..col+15 of Wi^T / U^T
-        const S* base = gw + (size_t)mat * 3 * H * GP + (size_t)(col + q) * GP + 32 * kk + 4 * g;
-        return load4x2(base, base + 16);
+      // Weight fragments of gate columns 16*t16 .. 16*t16 + 15 (fragment order).
+      auto gfrag = [&](int mat, int t16, int kk) __attribute__((always_inline)) {
+        return load_fragi<S>(gw, gru_fwd_idx<S, H>(mat, t16, kk), lane);
       };
-      // r for all features (r*h is an operand of the candidate product).
+      constexpr int NC = H / 16;   // 16-feature tiles of one gate
+      // r for all features (r*h is an operand of the candidate product); the
+      // k loops are outermost, so the NC accumulators are independent chains.
+      f32x4 ar[NC];
 #pragma unroll
-      for (int c = 0; c < KS; ++c) {
+      for (int c = 0; c < NC; ++c) ar[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          const frag_t<S> w0 = gfrag(0, c, kk);
+#pragma unroll
+          for (int part = 0; part < NP; ++part) mma(ar[c], w0, af[part][kk]);
+          mma(ar[c], gfrag(1, c, kk), hf[kk]);
+        }
+#pragma unroll
+      for (int c2 = 0; c2 < KS; ++c2) {
         float rhv[8];
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
-          f32x4 ar = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int kk = 0; kk < KS; ++kk) {
-            const frag_t<S> w0 = gfrag(0, 32 * c + 16 * p, kk);
-#pragma unroll
-            for (int part = 0; part < NP; ++part) mma(ar, w0, af[part][kk]);
-            mma(ar, gfrag(1, 32 * c + 16 * p, kk), hf[kk]);
-          }
-          const int f = 32 * c + 16 * p + 4 * g;
+          const int f = 32 * c2 + 16 * p + 4 * g;
           float r[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            r[j] = sigmoidf_(ar[j] + bg[f + j]);
-            rhv[4 * p + j] = r[j] * static_cast<float>(hf[c][4 * p + j]);
+            r[j] = sigmoidf_(ar[2 * c2 + p][j] + bg[f + j]);
+            rhv[4 * p + j] = r[j] * static_cast<float>(hf[c2][4 * p + j]);
           }
           store4(saved + (size_t)node * 3 * H + f, r[0], r[1], r[2], r[3]);
         }
-        rh[c] = pack8<S>(rhv);
+        rh[c2] = pack8<S>(rhv);
       }
-      // z, n and the new state.
+      // z, n and the new state (2 NC independent chains).
+      f32x4 az[NC], an[NC];
 #pragma unroll
-      for (int c = 0; c < KS; ++c)
+      for (int c = 0; c < NC; ++c) {
+        az[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+        an[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
-          f32x4 az = {0.f, 0.f, 0.f, 0.f}, an = {0.f, 0.f, 0.f, 0.f};
+      for (int kk = 0; kk < KS; ++kk)
 #pragma unroll
-          for (int kk = 0; kk < KS; ++kk) {
-            const frag_t<S> wz = gfrag(0, H + 32 * c + 16 * p, kk), wn = gfrag(0, 2 * H + 32 * c + 16 * p, kk);
+        for (int c = 0; c < NC; ++c) {
+          const frag_t<S> wz = gfrag(0, NC + c, kk), wn = gfrag(0, 2 * NC + c, kk);
 #pragma unroll
-            for (int part = 0; part < NP; ++part) {
-              mma(az, wz, af[part][kk]);
-              mma(an, wn, af[part][kk]);
-            }
-            mma(az, gfrag(1, H + 32 * c + 16 * p, kk), hf[kk]);
-            mma(an, gfrag(1, 2 * H + 32 * c + 16 * p, kk), rh[kk]);
+          for (int part = 0; part < NP; ++part) {
+            mma(az[c], wz, af[part][kk]);
+            mma(an[c], wn, af[part][kk]);
           }
-          const int f = 32 * c + 16 * p + 4 * g;
-          float z[4], nn[4], o[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            z[j] = sigmoidf_(az[j] + bg[H + f + j]);
-            nn[j] = tanhf_(an[j] + bg[2 * H + f + j]);
-            const float hv = static_cast<float>(hf[c][4 * p + j]);
-            o[j] = z[j] * hv + (1.f - z[j]) * nn[j];
-          }
-          store4(h_out + (size_t)node * H + f, o[0], o[1], o[2], o[3]);
-          store4(saved + (size_t)node * 3 * H + H + f, z[0], z[1], z[2], z[3]);
-          store4(saved + (size_t)node * 3 * H + 2 * H + f, nn[0], nn[1], nn[2], nn[3]);
+          mma(az[c], gfrag(1, NC + c, kk), hf[kk]);
+          mma(an[c], gfrag(1, 2 * NC + c, kk), rh[kk]);
         }
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int f = 16 * c + 4 * g;
+        float z[4], nn[4], o[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          z[j] = sigmoidf_(az[c][j] + bg[H + f + j]);
+          nn[j] = tanhf_(an[c][j] + bg[2 * H + f + j]);
+          const float hv = static_cast<float>(hf[c / 2][4 * (c % 2) + j]);
+          o[j] = z[j] * hv + (1.f - z[j]) * nn[j];
+        }
+        store4(h_out + (size_t)node * H + f, o[0], o[1], o[2], o[3]);
+        store4(saved + (size_t)node * 3 * H + H + f, z[0], z[1], z[2], z[3]);
+        store4(saved + (size_t)node * 3 * H + 2 * H + f, nn[0], nn[1], nn[2], nn[3]);
+      }
     }
   }
 }
@@ -759,7 +806,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
         if (lin < total) {
           const int slot = s_lo + lin / UPB, rem = lin % UPB;
           const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
-          *reinterpret_cast<u32x4*>(&vt[slot][h * VP + c]) = r[u];
+          *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(h, c)]) = r[u];
         }
       }
     }
@@ -797,7 +844,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
       for (int c0 = 0; c0 < B; c0 += KC) {
         if constexpr (!C::ALL) {
           __syncthreads();
-          stage_cols<S, H, KC, VP, NT>(vt[0], da, n_pad, (j - 1 + s) * B + c0, tid);
+          stage_cols<S, H, KC, NT>(vt[0], da, n_pad, (j - 1 + s) * B + c0, tid);
           __syncthreads();
         }
         const S* v = vt[C::ALL ? s : 0];
@@ -817,7 +864,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
           for (int m = 0; m < NTW; ++m) af[m] = bits_frag<S>(rb[m].byte(kk));
 #pragma unroll
           for (int n = 0; n < NTL; ++n) {
-            const frag_t<S> bf = load8(&v[(16 * n + q) * VP + g * (KC / 4) + 8 * kk]);
+            const frag_t<S> bf = load_frag<S, H>(v, kk, n, lane);
 #pragma unroll
             for (int m = 0; m < NTW; ++m) mma(acc[m][n], af[m], bf);
           }

@@ -191,21 +191,99 @@ __device__ __forceinline__ void tile_load(u32x4 (&r)[16 / sizeof(S)], const S* s
 #pragma unroll
   for (int i = 0; i < (int)(16 / sizeof(S)); ++i) r[i] = *reinterpret_cast<const u32x4*>(src + i * ss);
 }
+//   tile_row_T:   row x of the transposed tile, (r[0][x], ..., r[V-1][x])
+template <typename S>
+__device__ __forceinline__ u32x4 tile_row_T(const u32x4 (&r)[16 / sizeof(S)], int x) {
+  if constexpr (sizeof(S) == 2) {
+    const uint32_t sel = (x & 1) ? 0x07060302u : 0x05040100u;   // high or low halves of r[2j], r[2j+1]
+    u32x4 o;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) o[jj] = __builtin_amdgcn_perm(r[2 * jj + 1][x / 2], r[2 * jj][x / 2], sel);
+    return o;
+  } else {
+    return u32x4{r[0][x], r[1][x], r[2][x], r[3][x]};
+  }
+}
 template <typename S, int P>
 __device__ __forceinline__ void tile_store_T(S* dst, const u32x4 (&r)[16 / sizeof(S)]) {
+#pragma unroll
+  for (int x = 0; x < (int)(16 / sizeof(S)); ++x) *reinterpret_cast<u32x4*>(dst + x * P) = tile_row_T<S>(r, x);
+}
+
+// Fragment order in LDS: operand fragments stored so that, for each
+// fragment, the 64 lanes' copies are contiguous (per 16-byte vector), so a
+// wave's fragment read covers consecutive bytes.  The LDS serves 16 lanes'
+// 16-byte reads per pass from 64 four-byte banks: such a read never
+// conflicts, where rows read at a padded pitch took two passes.
+// fo: element e (0..7) of lane `lane`'s copy of fragment `idx`.
+template <typename S>
+__device__ __forceinline__ int fo(int idx, int lane, int e) {
+  constexpr int V = 16 / (int)sizeof(S), NV = 8 / V;
+  return ((idx * NV + e / V) * 64 + lane) * V + e % V;
+}
+template <typename S>
+__device__ __forceinline__ frag_t<S> load_fragi(const S* v, int idx, int lane) {
   if constexpr (sizeof(S) == 2) {
-#pragma unroll
-    for (int x = 0; x < 8; ++x) {
-      const uint32_t sel = (x & 1) ? 0x07060302u : 0x05040100u;   // high or low halves of r[2j], r[2j+1]
-      u32x4 o;
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) o[jj] = __builtin_amdgcn_perm(r[2 * jj + 1][x / 2], r[2 * jj][x / 2], sel);
-      *reinterpret_cast<u32x4*>(dst + x * P) = o;
-    }
+    return load8(v + fo<S>(idx, lane, 0));
   } else {
-#pragma unroll
-    for (int x = 0; x < 4; ++x) *reinterpret_cast<u32x4*>(dst + x * P) = u32x4{r[0][x], r[1][x], r[2][x], r[3][x]};
+    return load4x2(v + fo<S>(idx, lane, 0), v + fo<S>(idx, lane, 4));
   }
+}
+// GRU weights Wi, U ([H][3H]) staged in LDS in fragment order, each
+// fragment holding eight input features in accumulator-compatible order
+// (32kk + 4g + {0..3}, 32kk + 16 + 4g + {0..3}) of one gate column:
+//   gru_fwd_frag: A operand of D[gate col][node], rows = gate columns
+//                 col..col+15 (mat 0 = Wi, 1 = U);
+//   gru_rev_frag: operand rows = input features row..row+15, k = gate
+//                 columns gate*H + 32kk + ... (the reverse products).
+template <typename S, int H>
+__device__ __forceinline__ int gru_fwd_idx(int mat, int col16, int kk) {
+  return (mat * (3 * H / 16) + col16) * (H / 32) + kk;
+}
+template <typename S, int H>
+__device__ __forceinline__ int gru_rev_idx(int mat, int row16, int gate, int kk) {
+  return ((mat * (H / 16) + row16) * 3 + gate) * (H / 32) + kk;
+}
+// Place four consecutive elements `w` (8 bytes bf16, 16 bytes fp32) of the
+// k run starting at k0 (4-aligned, within a 32-step) of fragment `idx`, row
+// r16 (0..15) of its operand tile.
+template <typename S>
+__device__ __forceinline__ void put4(S* base, int idx, int r16, int k0, const S* w) {
+  const int kk32 = k0 % 32, half = kk32 / 16, g = (kk32 % 16) / 4;
+  S* d = base + fo<S>(idx, r16 + 16 * g, 4 * half);
+  if constexpr (sizeof(S) == 2) {
+    *reinterpret_cast<u32x2*>(d) = *reinterpret_cast<const u32x2*>(w);
+  } else {
+    *reinterpret_cast<u32x4*>(d) = *reinterpret_cast<const u32x4*>(w);
+  }
+}
+
+
+// Fragment of an operand stored k-major in LDS (element (k, n) at
+// base[k * P + n]): lane (q, g) receives elements (k0 + 8g + j, n0 + q),
+// j = 0..7.  For bf16 this is two transposing reads (ds_read_b64_tr_b16: in
+// each group of 16 lanes, lane i receives element i % 4 of the 8-byte runs
+// addressed by lanes i / 4, 4 + i / 4, 8 + i / 4 and 12 + i / 4); lane p of a
+// group addresses row k0 + 8g + p / 4 (+ 4 for the second read) at column
+// n0 + 4 (p % 4).  n0 and P are multiples of 4; the rows of one 16-lane
+// group fall on disjoint banks when P * 2 bytes is 160 mod 256.
+typedef short tr_v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) tr_v4i16 lds_tr_v4i16;
+__device__ __forceinline__ bf16x8 tr_frag(const bf16s* base, int P, int k0, int n0, int lane) {
+  const int p = lane % 16, g = lane / 16;
+  bf16s* a0 = const_cast<bf16s*>(base) + (k0 + 8 * g + p / 4) * P + n0 + 4 * (p % 4);
+  const tr_v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_tr_v4i16*)(a0));
+  const tr_v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_tr_v4i16*)(a0 + 4 * P));
+  typedef short v8i16 __attribute__((ext_vector_type(8)));
+  const v8i16 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+__device__ __forceinline__ f32x8 tr_frag(const float* base, int P, int k0, int n0, int lane) {
+  const int q = lane % 16, g = lane / 16;
+  f32x8 r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = base[(k0 + 8 * g + j) * P + n0 + q];
+  return r;
 }
 
 // 16-byte vector copy unit (8 bf16 or 4 fp32 elements).

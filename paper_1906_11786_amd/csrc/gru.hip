@@ -173,8 +173,7 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
   constexpr int NT = WAVES * kWave;
   constexpr int V = 16 / sizeof(S);
   constexpr bool LDSW = H <= 64;                       // weights fit in LDS
-  constexpr int WROW = 3 * H + V;                       // LDS row pitch of a staged weight
-  __shared__ __attribute__((aligned(16))) S wl[LDSW ? 2 : 1][LDSW ? H * WROW : 1];
+  __shared__ __attribute__((aligned(16))) S wl[LDSW ? 2 * 3 * H * H : 1];   // Wi, U in fragment order
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int q = lane % 16, g = lane / 16;
@@ -183,10 +182,14 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
   const int node = n0 + q;
 
   if constexpr (LDSW) {
-    for (int lin = tid; lin < H * (3 * H / V); lin += NT) {
-      const int r = lin / (3 * H / V), c = (lin % (3 * H / V)) * V;
-      *reinterpret_cast<u32x4*>(&wl[0][r * WROW + c]) = *reinterpret_cast<const u32x4*>(Wi + (size_t)r * 3 * H + c);
-      *reinterpret_cast<u32x4*>(&wl[1][r * WROW + c]) = *reinterpret_cast<const u32x4*>(U + (size_t)r * 3 * H + c);
+    for (int lin = tid; lin < 2 * H * (3 * H / V); lin += NT) {
+      const int mat = lin / (H * (3 * H / V)), rem = lin % (H * (3 * H / V));
+      const int r = rem / (3 * H / V), c = (rem % (3 * H / V)) * V;
+      const u32x4 w = *reinterpret_cast<const u32x4*>((mat ? U : Wi) + (size_t)r * 3 * H + c);
+      const S* pw = reinterpret_cast<const S*>(&w);
+#pragma unroll
+      for (int i = 0; i < V; i += 4)
+        put4<S>(wl, gru_rev_idx<S, H>(mat, r / 16, (c + i) / H, ((c + i) % H) / 32), r % 16, (c + i) % H, pw + i);
     }
     __syncthreads();
   }
@@ -195,9 +198,15 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
 #pragma unroll
   for (int m = 0; m < MTL; ++m) gg[m] = *reinterpret_cast<const f32x4*>(gin + (size_t)node * H + 16 * m + 4 * g);
   if constexpr (LDSW) {
-    gru_bwd_wave<S, H, WROW>(gg, n0, q, g, h, saved, &wl[0][0], &wl[1][0], daT, n_pad, dh, ghat);
+    auto wf = [&](int which, int row, int gate, int kk) __attribute__((always_inline)) {
+      return load_fragi<S>(wl, gru_rev_idx<S, H>(which, row / 16, gate, kk), lane);
+    };
+    gru_bwd_wave<S, H>(gg, n0, q, g, h, saved, wf, daT, n_pad, dh, ghat);
   } else {
-    gru_bwd_wave<S, H, 3 * H>(gg, n0, q, g, h, saved, Wi, U, daT, n_pad, dh, ghat);
+    auto wf = [&](int which, int row, int gate, int kk) __attribute__((always_inline)) {
+      return rowfrag<S>((which ? U : Wi) + (size_t)row * 3 * H + gate * H, kk, g);
+    };
+    gru_bwd_wave<S, H>(gg, n0, q, g, h, saved, wf, daT, n_pad, dh, ghat);
   }
 }
 
@@ -207,141 +216,186 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
 //   P[split][1][i][c] = sum_k x_c[k][i] G^[k][c]        (dU)
 // with x_c = h for the r and z columns and r*h for the n columns, and
 //   Pb[split][c] = sum_k G^[k][c]                       (db).
-// The rows are the nodes of one step (K = n_pad) or of all T steps at once
-// (K = T * n_pad: a, h, saved and G^ stacked over t).  Tile TI x TI
-// (TI = min(H, 64)); both operands are node-major, staged in LDS and read
-// with a stride along k.  The tile index runs fastest over the logical
-// workgroup index, so the tiles of one split share their rows in one L2.
+// The rows are the nodes of all T steps at once (K = T * n_pad: a, h, saved
+// and G^ stacked over t).  A workgroup owns one split of the rows and a
+// slice of IT input features (all of them up to H = 64), every gate column:
+// each input row is read once.  Per chunk of KC rows the operands are
+// staged node-major in LDS (plain 16-byte copies; a rounded to bf16, r*h
+// formed on the way) and read as matrix-core fragments with transposing
+// LDS reads; the next chunk's loads are in flight during the products.
+// Wave w: matrix w / 4 (dWi or dU) and a quarter of that matrix's tiles.
 // ---------------------------------------------------------------------------
+template <typename S, int H> struct GruWgradCfg {
+  static constexpr int IT = H >= 128 ? 4096 / H : H;   // input features per workgroup
+  static constexpr int NI = IT / 16, NCT = 3 * H / 16;  // tiles: input, gate columns
+  static constexpr int KC = (H >= 256 || sizeof(S) == 4) ? 32 : 64;   // rows per chunk
+  static constexpr int IW = H == 32 ? 1 : NI;            // input tiles per wave
+  static constexpr int CW = H == 32 ? 3 : NCT / 4;       // gate-column tiles per wave
+  static constexpr int PA = IT + 16, PG = 3 * H + 16;    // LDS row pitches (elements)
+  // LDS buffers: two (the next chunk is written while the current one is
+  // read) when they fit in 160 KB.
+  static constexpr int NBUF = 2 * KC * (3 * PA + PG) * (int)sizeof(S) <= 160 * 1024 ? 2 : 1;
+};
+
 template <typename S, int H>
-__global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kernel(
-    const float* __restrict__ a, const S* __restrict__ h, const S* __restrict__ saved, const S* __restrict__ ghat,
-    float* __restrict__ P, float* __restrict__ Pb, long K, int rows_per_split) {
-  constexpr int TI = H < 64 ? H : 64;
-  constexpr int WAVES = TI / 16;
-  constexpr int NT = WAVES * kWave;
-  constexpr int KN = 64;
-  constexpr int PX = TI + 4 / sizeof(S);
-  constexpr int NTL = TI / 16;
-  constexpr int TIN = H / TI, TOUT = 3 * H / TI;
-  __shared__ __attribute__((aligned(16))) S ta[KN * PX];
-  __shared__ __attribute__((aligned(16))) S tb[KN * PX];
+__global__ __launch_bounds__(512) void gru_wgrad_kernel(const float* __restrict__ a, const S* __restrict__ h,
+                                                        const S* __restrict__ saved, const S* __restrict__ ghat,
+                                                        float* __restrict__ P, float* __restrict__ Pb, long K,
+                                                        int rows_per_split) {
+  using C = GruWgradCfg<S, H>;
+  constexpr int IT = C::IT, KC = C::KC, IW = C::IW, CW = C::CW, PA = C::PA, PG = C::PG, NBUF = C::NBUF;
+  constexpr int NT = 512;
+  constexpr int V = 16 / sizeof(S);
+  constexpr int NA = KC * IT / V, NG = KC * 3 * H / V;   // 16-byte units per chunk
+  constexpr int UA = (NA + NT - 1) / NT, UG = (NG + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) S sa[NBUF][3][KC * PA];   // a, h, r*h
+  __shared__ __attribute__((aligned(16))) S sg[NBUF][KC * PG];      // G^
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int q = lane % 16, g = lane / 16;
-  int bid = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int to = bid % TOUT; bid /= TOUT;
-  const int ti = bid % TIN; bid /= TIN;
-  const int which = bid % 2;
-  const int split = bid / 2;
+  constexpr int NSL = H / IT;
+  const int bid = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int sl = bid % NSL, split = bid / NSL;
+  const int i0 = sl * IT;
   const long nlo = (long)split * rows_per_split;
   const long nhi = min(K, nlo + rows_per_split);
-  const int col0 = to * TI;                      // gate column of this tile
-  const bool rh_src = (which == 1 && col0 >= 2 * H);
-  const bool do_bias = (which == 0 && ti == 0 && wave == 0);
+  const int mat = wave / 4, sub = wave % 4;
+  const int it0 = H == 32 ? sub % 2 : 0;
+  const int ct0 = H == 32 ? (sub / 2) * 3 : sub * CW;
+  const bool do_bias = mat == 0 && sl == 0 && it0 == 0;
 
-  f32x4 acc[NTL];
-  float bsum[NTL];
+  f32x4 acc[IW][CW];
+  float bsum[CW];
 #pragma unroll
-  for (int n = 0; n < NTL; ++n) {
-    acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-    bsum[n] = 0.f;
-  }
-  // Software pipeline: the next chunk's operands are loaded into registers
-  // (a, h, r*h and G^ as four-element groups) while the current chunk is
-  // multiplied.
-  constexpr int TU = KN * TI / 4;
-  constexpr int UN = (TU + NT - 1) / NT;
-  f32x4 ar[UN];
-  u32x2 gr[UN];     // four G^ elements (8 bytes for bf16; fp32 uses two of these per group below)
-  f32x4 gf32[sizeof(S) == 4 ? UN : 1];
+  for (int i = 0; i < IW; ++i)
+#pragma unroll
+    for (int c = 0; c < CW; ++c) acc[i][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < CW; ++c) bsum[c] = 0.f;
+
+  // Register stage of one chunk: per A unit the fp32 a (V values), h and r;
+  // per G unit the 16 bytes of G^.
+  f32x4 ra[UA][V / 4];
+  u32x4 rh[UA], rr[UA], rg[UG];
   auto load_chunk = [&](long c0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < UN; ++u) {
+    for (int u = 0; u < UA; ++u) {
       const int lin = u * NT + tid;
-      const int r = lin / (TI / 4), c = (lin % (TI / 4)) * 4;
-      const long node = c0 + r;
-      if ((TU % NT == 0 || lin < TU) && node < nhi) {
-        const int fi = ti * TI + c;
-        if (which == 0) {
-          ar[u] = *reinterpret_cast<const f32x4*>(a + (size_t)node * H + fi);
-        } else {
-          f32x4 x = load4f(h + (size_t)node * H + fi);
-          if (rh_src) {
-            const f32x4 r4 = load4f(saved + (size_t)node * 3 * H + fi);
-            x = f32x4{x.x * r4.x, x.y * r4.y, x.z * r4.z, x.w * r4.w};
-          }
-          ar[u] = x;
+      const long row = c0 + lin / (IT / V);
+      const int f = i0 + (lin % (IT / V)) * V;
+      if ((NA % NT == 0 || lin < NA) && row < nhi) {
+#pragma unroll
+        for (int x = 0; x < V / 4; ++x) ra[u][x] = *reinterpret_cast<const f32x4*>(a + (size_t)row * H + f + 4 * x);
+        rh[u] = *reinterpret_cast<const u32x4*>(h + (size_t)row * H + f);
+        rr[u] = *reinterpret_cast<const u32x4*>(saved + (size_t)row * 3 * H + f);
+      } else {   // rows past the split (a ragged last chunk) contribute zeros
+#pragma unroll
+        for (int x = 0; x < V / 4; ++x) ra[u][x] = f32x4{0.f, 0.f, 0.f, 0.f};
+        rh[u] = u32x4{0u, 0u, 0u, 0u};
+        rr[u] = u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UG; ++u) {
+      const int lin = u * NT + tid;
+      const long row = c0 + lin / (3 * H / V);
+      const int c = (lin % (3 * H / V)) * V;
+      rg[u] = ((NG % NT == 0 || lin < NG) && row < nhi)
+                  ? *reinterpret_cast<const u32x4*>(ghat + (size_t)row * 3 * H + c)
+                  : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto store_chunk = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < UA; ++u) {
+      const int lin = u * NT + tid;
+      if (NA % NT == 0 || lin < NA) {
+        const int r = lin / (IT / V), f = (lin % (IT / V)) * V;
+        const S* ph = reinterpret_cast<const S*>(&rh[u]);
+        const S* pr = reinterpret_cast<const S*>(&rr[u]);
+        float av[V], rhv[V];
+#pragma unroll
+        for (int x = 0; x < V; ++x) {
+          av[x] = ra[u][x / 4][x % 4];
+          rhv[x] = to_f<S>(ph[x]) * to_f<S>(pr[x]);
         }
-        const S* gsrc = ghat + (size_t)node * 3 * H + col0 + c;
+        u32x4 wa, wr;
         if constexpr (sizeof(S) == 2) {
-          gr[u] = *reinterpret_cast<const u32x2*>(gsrc);
+#pragma unroll
+          for (int x = 0; x < 4; ++x) {
+            wa[x] = pk2(av[2 * x], av[2 * x + 1]);
+            wr[x] = pk2(rhv[2 * x], rhv[2 * x + 1]);
+          }
         } else {
-          gf32[u] = *reinterpret_cast<const f32x4*>(gsrc);
+#pragma unroll
+          for (int x = 0; x < 4; ++x) {
+            wa[x] = __float_as_uint(av[x]);
+            wr[x] = __float_as_uint(rhv[x]);
+          }
         }
+        *reinterpret_cast<u32x4*>(&sa[buf][0][r * PA + f]) = wa;
+        *reinterpret_cast<u32x4*>(&sa[buf][1][r * PA + f]) = rh[u];
+        *reinterpret_cast<u32x4*>(&sa[buf][2][r * PA + f]) = wr;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UG; ++u) {
+      const int lin = u * NT + tid;
+      if (NG % NT == 0 || lin < NG) {
+        const int r = lin / (3 * H / V), c = (lin % (3 * H / V)) * V;
+        *reinterpret_cast<u32x4*>(&sg[buf][r * PG + c]) = rg[u];
       }
     }
   };
+
+  // Splits start at multiples of 64 rows; a last chunk that runs past the
+  // split is zero-filled.
   if (nlo < nhi) load_chunk(nlo);
-  for (long c0 = nlo; c0 < nhi; c0 += KN) {
+  int buf = 0;
+  for (long c0 = nlo; c0 < nhi; c0 += KC, buf = NBUF == 2 ? buf ^ 1 : 0) {
+    if (NBUF == 1 && c0 > nlo) __syncthreads();   // the previous chunk is fully read
+    store_chunk(buf);
     __syncthreads();
+    if (c0 + KC < nhi) load_chunk(c0 + KC);
 #pragma unroll
-    for (int u = 0; u < UN; ++u) {
-      const int lin = u * NT + tid;
-      const int r = lin / (TI / 4), c = (lin % (TI / 4)) * 4;
-      if ((TU % NT == 0 || lin < TU) && c0 + r < nhi) {
-        S* pa = &ta[r * PX + c];
-        S* pb = &tb[r * PX + c];
-        if constexpr (sizeof(S) == 2) {
-          // rows are 4-byte aligned: write as two 32-bit words
-          const uint32_t lo = pk2(ar[u].x, ar[u].y);
-          const uint32_t hi = pk2(ar[u].z, ar[u].w);
-          reinterpret_cast<uint32_t*>(pa)[0] = lo;
-          reinterpret_cast<uint32_t*>(pa)[1] = hi;
-          reinterpret_cast<uint32_t*>(pb)[0] = gr[u].x;
-          reinterpret_cast<uint32_t*>(pb)[1] = gr[u].y;
-        } else {
+    for (int k0 = 0; k0 < KC; k0 += 32) {
+      frag_t<S> fa[IW][2];   // [.][0]: a (dWi) or h (dU r, z columns); [.][1]: r*h (dU n columns)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            pa[j] = from_f<S>(ar[u][j]);
-            pb[j] = from_f<S>(gf32[sizeof(S) == 4 ? u : 0][j]);
-          }
-        }
+      for (int i = 0; i < IW; ++i) {
+        const int n0 = 16 * (it0 + i);
+        fa[i][0] = tr_frag(sa[buf][mat == 0 ? 0 : 1], PA, k0, n0, lane);
+        if (mat == 1 && (ct0 + CW) * 16 > 2 * H) fa[i][1] = tr_frag(sa[buf][2], PA, k0, n0, lane);
       }
-    }
-    __syncthreads();
-    if (c0 + KN < nhi) load_chunk(c0 + KN);
 #pragma unroll
-    for (int kk = 0; kk < KN / 32; ++kk) {
-      if (c0 + 32 * kk >= nhi) break;
-      frag_t<S> afr = load8_strided(&ta[(32 * kk + 8 * g) * PX + 16 * wave + q], PX);
-#pragma unroll
-      for (int n = 0; n < NTL; ++n) {
-        frag_t<S> bf = load8_strided(&tb[(32 * kk + 8 * g) * PX + 16 * n + q], PX);
-        mma(acc[n], afr, bf);
+      for (int c = 0; c < CW; ++c) {
+        const int ct = ct0 + c;
+        const frag_t<S> fb = tr_frag(sg[buf], PG, k0, 16 * ct, lane);
         if (do_bias) {
 #pragma unroll
-          for (int x = 0; x < 8; ++x) bsum[n] += static_cast<float>(bf[x]);
+          for (int x = 0; x < 8; ++x) bsum[c] += static_cast<float>(fb[x]);
         }
+        const int src = (mat == 1 && 16 * ct >= 2 * H) ? 1 : 0;
+#pragma unroll
+        for (int i = 0; i < IW; ++i) mma(acc[i][c], src ? fa[i][1] : fa[i][0], fb);
       }
     }
   }
-  float* out = P + ((size_t)split * 2 + which) * H * 3 * H;
+  // D[i = i0 + 16 (it0 + i) + 4g + j][c = 16 (ct0 + c) + q]
+  float* out = P + ((size_t)split * 2 + mat) * H * 3 * H;
 #pragma unroll
-  for (int n = 0; n < NTL; ++n) {
-    const int c = col0 + 16 * n + q;
+  for (int i = 0; i < IW; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * 3 * H + c] = acc[n][j];
-    }
-  }
+    for (int c = 0; c < CW; ++c)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        out[(size_t)(i0 + 16 * (it0 + i) + 4 * g + j) * 3 * H + 16 * (ct0 + c) + q] = acc[i][c][j];
   if (do_bias) {
 #pragma unroll
-    for (int n = 0; n < NTL; ++n) {
-      float v = bsum[n];
+    for (int c = 0; c < CW; ++c) {
+      float v = bsum[c];
       v += __shfl_xor(v, 16);
       v += __shfl_xor(v, 32);
-      if (g == 0) Pb[(size_t)split * 3 * H + col0 + 16 * n + q] = v;
+      if (g == 0) Pb[(size_t)split * 3 * H + 16 * (ct0 + c) + q] = v;
     }
   }
 }
@@ -349,21 +403,17 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void gru_wgrad_kern
 }  // namespace dev
 
 namespace {
-// Row split of the weight-gradient contraction (same policy as the message
-// transform's): about 2048 workgroups, splits of at least GGNN_WGRAD_MIN_ROWS
-// rows, a multiple of 64.
-#ifndef GGNN_WGRAD_MIN_ROWS
-#define GGNN_WGRAD_MIN_ROWS 1024
-#endif
+// Row split of the weight-gradient contraction: about 256 workgroups (one
+// per compute unit, 8 waves each) over splits x input-feature slices;
+// splits are multiples of 64 rows.
 struct Split {
   int nsplit, per;
 };
 Split gru_split(long K, int H) {
-  const long TI = H < 64 ? H : 64;
-  const long tiles = 2 * (H / TI) * (3 * H / TI);
-  const long want = (2048 + tiles - 1) / tiles;
+  const long slices = H >= 128 ? H / (4096 / H) : 1;
+  const long want = 256 / slices > 0 ? 256 / slices : 1;
   long per = ((K + want - 1) / want + 63) / 64 * 64;
-  if (per < GGNN_WGRAD_MIN_ROWS) per = GGNN_WGRAD_MIN_ROWS;
+  if (per < 64) per = 64;
   return {(int)((K + per - 1) / per), (int)per};
 }
 
@@ -391,12 +441,11 @@ hipError_t gru_bwd_nodes_h(int n_pad, const float* dh_out, const void* h, const 
 template <typename S, int H>
 hipError_t gru_wgrad_h(long K, const float* a, const void* h, const void* saved, const void* ghat, float* dWi,
                        float* dU, float* db, void* ws, hipStream_t st) {
-  constexpr int TI = H < 64 ? H : 64;
   Split sp = gru_split(K, H);
   float* P = static_cast<float*>(ws);
   float* Pb = P + (size_t)sp.nsplit * 2 * H * 3 * H;
-  const int blocks = sp.nsplit * 2 * (H / TI) * (3 * H / TI);
-  hipLaunchKernelGGL((dev::gru_wgrad_kernel<S, H>), dim3(blocks), dim3(TI / 16 * 64), 0, st, a,
+  const int blocks = sp.nsplit * (H / dev::GruWgradCfg<S, H>::IT);
+  hipLaunchKernelGGL((dev::gru_wgrad_kernel<S, H>), dim3(blocks), dim3(512), 0, st, a,
                      static_cast<const S*>(h), static_cast<const S*>(saved), static_cast<const S*>(ghat), P, Pb, K,
                      sp.per);
   hipError_t err = hipGetLastError();

@@ -25,19 +25,17 @@ __device__ __forceinline__ frag_t<S> rowfrag(const S* row, int kk, int g) {
 }
 
 // gg[m]: dL/dh' for features 16m + 4g + {0..3} of node n0 + q.
-// Wi, U: [H][3H] weights with row pitch WP (LDS copies or global memory).
+// wfrag(which, row, gate, kk): the weight fragment of input feature `row`
+// (row % 16 == q) and gate columns gate*H + 32kk + (accumulator-compatible
+// order) of Wi (which = 0) or U (which = 1), from LDS or global memory.
 // Writes daT[f][n0 + 4g + j] (feature-major, row pitch ld), dh[node][.]
 // (node-major, float) and ghat[node][.] (node-major, 3H).
-template <typename S, int H, int WP>
+template <typename S, int H, typename WF>
 __device__ __forceinline__ void gru_bwd_wave(const f32x4 (&gg)[H / 16], int n0, int q, int g, const S* h,
-                                             const S* saved, const S* Wi, const S* U, S* daT, long ld, float* dh,
-                                             S* ghat) {
+                                             const S* saved, WF wfrag, S* daT, long ld, float* dh, S* ghat) {
   constexpr int KS = H / 32;
   constexpr int MTL = H / 16;
   const int node = n0 + q;
-  auto wfrag = [&](int which, int row, int gate, int kk) __attribute__((always_inline)) {
-    return rowfrag<S>((which ? U : Wi) + (size_t)row * WP + gate * H, kk, g);
-  };
   // Phase 1: elementwise part, kept in registers.
   frag_t<S> gf[3][KS];          // r^, z^, n^ as operand fragments
   f32x4 dacc[MTL];              // dh accumulator (D layout: features 16m + 4g + j)
@@ -67,11 +65,16 @@ __device__ __forceinline__ void gru_bwd_wave(const f32x4 (&gg)[H / 16], int n0, 
   // Phase 2: q' = n^ U_n^T (D[f_in][node]); r^ and the q' r term of dh.
   {
     float rv[8];
+    f32x4 qacc[MTL];
+#pragma unroll
+    for (int m = 0; m < MTL; ++m) qacc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+      for (int m = 0; m < MTL; ++m) mma(qacc[m], wfrag(1, 16 * m + q, 2, kk), gf[2][kk]);
 #pragma unroll
     for (int m = 0; m < MTL; ++m) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) mma(acc, wfrag(1, 16 * m + q, 2, kk), gf[2][kk]);
+      const f32x4 acc = qacc[m];
       const int f = 16 * m + 4 * g;
       const f32x4 r4 = load4f(sv + f), h4 = load4f(h + (size_t)node * H + f);
 #pragma unroll
@@ -83,25 +86,30 @@ __device__ __forceinline__ void gru_bwd_wave(const f32x4 (&gg)[H / 16], int n0, 
       if (m % 2 == 1) gf[0][m / 2] = pack8<S>(rv);
     }
   }
-  // Phase 3: da = G^ Wi^T, D[node][f_in]: four consecutive nodes per lane.
+  // Phase 3: da = G^ Wi^T, D[node][f_in]: four consecutive nodes per lane;
+  // phase 4: dh += r^ U_r^T + z^ U_z^T, D[f_in][node].  The k loops are
+  // outermost so that the MTL accumulators of each form independent chains.
+  f32x4 dacc2[MTL];
 #pragma unroll
-  for (int n = 0; n < MTL; ++n) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int n = 0; n < MTL; ++n) dacc2[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int gate = 0; gate < 3; ++gate)
+  for (int gate = 0; gate < 3; ++gate)
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) mma(acc, gf[gate][kk], wfrag(0, 16 * n + q, gate, kk));
-    store4(daT + (size_t)(16 * n + q) * ld + n0 + 4 * g, acc[0], acc[1], acc[2], acc[3]);
-  }
-  // Phase 4: dh += r^ U_r^T + z^ U_z^T, D[f_in][node]; one store of dh.
+    for (int kk = 0; kk < KS; ++kk)
 #pragma unroll
-  for (int m = 0; m < MTL; ++m) {
+      for (int n = 0; n < MTL; ++n) mma(dacc2[n], gf[gate][kk], wfrag(0, 16 * n + q, gate, kk));
 #pragma unroll
-    for (int gate = 0; gate < 2; ++gate)
+  for (int gate = 0; gate < 2; ++gate)
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) mma(dacc[m], wfrag(1, 16 * m + q, gate, kk), gf[gate][kk]);
+    for (int kk = 0; kk < KS; ++kk)
+#pragma unroll
+      for (int m = 0; m < MTL; ++m) mma(dacc[m], wfrag(1, 16 * m + q, gate, kk), gf[gate][kk]);
+#pragma unroll
+  for (int n = 0; n < MTL; ++n)
+    store4(daT + (size_t)(16 * n + q) * ld + n0 + 4 * g, dacc2[n][0], dacc2[n][1], dacc2[n][2], dacc2[n][3]);
+#pragma unroll
+  for (int m = 0; m < MTL; ++m)
     store4(dh + (size_t)node * H + 16 * m + 4 * g, dacc[m][0], dacc[m][1], dacc[m][2], dacc[m][3]);
-  }
 }
 
 }  // namespace dev
