@@ -6,6 +6,11 @@ A step is one pass of the whole hot path over the workload: T forward steps
 with the band, parameters and activations resident in HBM.  The metric is
 node-steps/s = real nodes * T / seconds per step.
 
+The step is timed twice: launched eagerly, and recorded once as a HIP graph
+and replayed (the same kernels, without host launch overhead between them);
+`value` is the faster of the two (`config.timing` says which; `--eager`
+skips the graph).
+
 Prints one JSON line.  `--gpus N` with N > 1 is refused: the path runs on
 one GPU.
 
@@ -43,8 +48,11 @@ WORKLOADS = {"program_graph": 1, "tiny": 0, "batch_100k": 2, "stress_1m": 4}
 
 # C-ABI entry point -> (device kernel name fragments, sources that define it)
 KERNELS = {
-    "banded_step_bits": (("step_bits_kernel", ", false>("), ["banded_bits.hip", "device_common.h"]),
-    "banded_step_bits_bwd": (("step_bits_kernel", ", true>("), ["banded_bits.hip", "device_common.h"]),
+    "step_bits_gru": (("step_bits_kernel", ", false, true>("), ["banded_bits.hip", "device_common.h"]),
+    "step_bits_gru_bwd": (("step_bits_kernel", ", true, true>("),
+                          ["banded_bits.hip", "device_common.h", "gru_wave.h"]),
+    "banded_step_bits": (("step_bits_kernel", ", false, false>("), ["banded_bits.hip", "device_common.h"]),
+    "banded_step_bits_bwd": (("step_bits_kernel", ", true, false>("), ["banded_bits.hip", "device_common.h"]),
     "banded_propagate": (("banded_fwd_kernel",), ["banded.hip", "device_common.h"]),
     "banded_propagate_bwd": (("banded_bwd_kernel",), ["banded.hip", "device_common.h"]),
 }
@@ -69,6 +77,7 @@ def parse():
                    help="band storage: 1 bit per entry (aggregate-first fused forward) or dense in the compute dtype")
     p.add_argument("--kernel-reps", type=int, default=50, help="launches per kernel for the roofline timing")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--eager", action="store_true", help="time eager launches only (no HIP graph replay)")
     p.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="summarise two rocprofv3 --pmc counter files (FETCH_SIZE, WRITE_SIZE) of this command "
                         "and exit")
@@ -162,18 +171,29 @@ def kernel_costs(fmt, n_pad, B, E, H, es):
     """Algorithmic flops and HBM bytes of one launch of each banded kernel.
     Three full B x B block products per block row and edge type (the two
     corner blocks outside the matrix are never read), plus the per-type
-    transform where the kernel fuses it; operands read once, outputs written
-    once."""
+    transform and the GRU node work where the kernel fuses them; operands
+    read once, outputs written once."""
     nb = n_pad // B
     blocks = (3 * nb - 2) * E
     agg_flops = 2.0 * blocks * B * B * H
     if fmt == "bits":
         band = blocks * B * B // 8
         tr_flops = 2.0 * n_pad * E * H * H
-        fwd = (agg_flops + tr_flops, band + n_pad * H * es + E * H * H * es + n_pad * H * 4)
+        gru_flops = 12.0 * n_pad * H * H          # a Wi, h U_rz, (r*h) U_n; reverse: G^ Wi^T, G^ U^T
+        nh = n_pad * H
+        gru_w = 6 * H * H * es + 3 * H * 4        # Wi, U, b
+        fwd = (agg_flops + tr_flops, band + nh * es + E * H * H * es + nh * 4)
         # reverse: bits_t, da, W read; dM (all types) written; dX_in read, dX_out written
-        bwd = (agg_flops + tr_flops, band + H * n_pad * es + E * H * H * es + E * n_pad * H * es + 2 * n_pad * H * 4)
-        return {"banded_step_bits": fwd, "banded_step_bits_bwd": bwd}
+        bwd = (agg_flops + tr_flops, band + nh * es + E * H * H * es + E * nh * es + 2 * nh * 4)
+        # fused forward step: + GRU (h = X read once; h_out, saved written)
+        fwd_gru = (agg_flops + tr_flops + gru_flops, band + nh * es + E * H * H * es + nh * 4 + gru_w + nh * es
+                   + 3 * nh * es)
+        # fused reverse step: + GRU reverse of the previous step (h_prev, saved_prev read;
+        # da_prev, dh_prev, G^ written); the summed dX is not stored
+        bwd_gru = (agg_flops + tr_flops + gru_flops, band + nh * es + E * H * H * es + E * nh * es + nh * 4 + gru_w
+                   + nh * es + 3 * nh * es + nh * es + nh * 4 + 3 * nh * es)
+        return {"banded_step_bits": fwd, "banded_step_bits_bwd": bwd, "step_bits_gru": fwd_gru,
+                "step_bits_gru_bwd": bwd_gru}
     band = blocks * B * B * es
     return {"banded_propagate": (agg_flops, band + E * H * n_pad * 4 + n_pad * H * 4),
             "banded_propagate_bwd": (agg_flops, band + H * n_pad * es + E * H * n_pad * es)}
@@ -252,19 +272,31 @@ def main():
     m = BandedGGNN(comp, spec.H, spec.T, spec.dtype, params, band_format=args.band)
     torch.cuda.synchronize()
 
-    for _ in range(args.warmup):
-        m.step()
-    torch.cuda.synchronize()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    start.record()
-    for _ in range(args.steps):
-        m.step()
-    end.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    dev_s = start.elapsed_time(end) / 1e3
-    sec_per_step = max(wall, dev_s) / args.steps
+    def timed(fn):
+        """Seconds per step over args.steps calls after args.warmup, the larger
+        of the host clock and the device events around the timed calls."""
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        start.record()
+        for _ in range(args.steps):
+            fn()
+        end.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        return max(wall, start.elapsed_time(end) / 1e3) / args.steps
+
+    eager_s = timed(m.step)
+    graph_s = None
+    if not args.eager:
+        # The same step recorded once as a HIP graph and replayed: no host
+        # launch overhead between the kernels.
+        m.capture()
+        graph_s = timed(m.replay)
+    use_graph = graph_s is not None and graph_s < eager_s
+    sec_per_step = graph_s if use_graph else eager_s
     value = comp.n_real * spec.T / sec_per_step
 
     # Roofline of the banded kernels: each launch timed with HIP events on the
@@ -272,11 +304,19 @@ def main():
     es = 2 if spec.dtype == "bf16" else 4
     n_pad, B, E, H = comp.n_pad, spec.B, spec.E, spec.H
     if args.band == "bits":
-        fns = {"banded_step_bits": lambda: capi.ggnn_banded_step_bits(spec.dtype, n_pad, B, H, E, m.band, m.X[0],
-                                                                      m.W, m.bias, m.a[0]),
-               "banded_step_bits_bwd": lambda: capi.ggnn_banded_step_bits_bwd(spec.dtype, n_pad, B, H, E, m.band_t,
-                                                                              m.da, m.W, m.dh, m.dX, m.dM,
-                                                                              spec.T * n_pad)}
+        # The two launches a step is made of (ggnn_forward runs the first T
+        # times, ggnn_backward the second for t = T-1..1), with the step's own
+        # buffers: state 0 -> 1 and the reverse of step 1 into step 0.
+        td = m.X.dtype
+        da_prev = torch.empty_like(m.da)
+        dh_prev = torch.empty_like(m.dh)
+        ghat = torch.empty((n_pad, 3 * H), dtype=td, device="cuda")
+        fns = {"step_bits_gru": lambda: capi.ggnn_step_bits_gru(spec.dtype, n_pad, B, H, E, m.band, m.X[0], m.W,
+                                                                m.bias, m.Wi, m.U, m.b, m.a[0], m.X[1],
+                                                                m.saved[0]),
+               "step_bits_gru_bwd": lambda: capi.ggnn_step_bits_gru_bwd(
+                   spec.dtype, n_pad, B, H, E, m.band_t, m.da, m.W, m.dh, m.dM, spec.T * n_pad, m.Wi, m.U,
+                   m.X[0], m.saved[0], da_prev, dh_prev, ghat)}
     else:
         fns = {"banded_propagate": lambda: capi.ggnn_banded_propagate(spec.dtype, n_pad, B, H, E, m.band, m.M,
                                                                       m.a[0]),
@@ -330,6 +370,9 @@ def main():
                    "B": B, "E": E, "H": H, "T": spec.T, "bandwidth_after_reordering": comp.bandwidth,
                    "edges_packed": comp.stats.get("n_packed"), "edges_dropped": comp.stats.get("n_dropped"),
                    "node_steps_per_s_padded": round(comp.n_pad * spec.T / sec_per_step, 1),
+                   "timing": "hip_graph_replay" if use_graph else "eager",
+                   "ms_per_step_eager": round(eager_s * 1e3, 4),
+                   "ms_per_step_graph": None if graph_s is None else round(graph_s * 1e3, 4),
                    "host_compile_s": round(comp.rcm_seconds + comp.stats.get("pack_seconds", 0.0), 3),
                    "generate_s": round(gen_s, 3)},
         "roofline": roofline,

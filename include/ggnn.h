@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define GGNN_ABI_VERSION 4
+#define GGNN_ABI_VERSION 5
 
 typedef enum {
   GGNN_OK = 0,
@@ -228,6 +228,35 @@ ggnn_status ggnn_banded_propagate_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t
 ggnn_status ggnn_banded_step_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
                                       const void* bits_t, const void* da, const void* W, const float* dX_in,
                                       float* dX_out, void* dM, int64_t ldm, void* stream);
+
+/* One forward step of Eq. 1 on a 1-bit band: ggnn_banded_step_bits followed
+ * by ggnn_gru_update on its result, run as one kernel where the shape allows
+ * (small grids, H <= 64), as two otherwise.  Same arguments and layouts as
+ * those two calls:
+ *   a      [n_pad][H] float (written: the aggregate, kept for the reverse pass)
+ *   h_out  [n_pad][H] dt (written: the next state);  saved [n_pad][3H] dt (r | z | n)
+ * Wi, U [H][3H] dt; b [3H] float.  X and h_out must not overlap. */
+ggnn_status ggnn_step_bits_gru(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
+                               const void* bits, const void* X, const void* W, const float* bias,
+                               const void* Wi, const void* U, const float* b, float* a, void* h_out,
+                               void* saved, void* stream);
+
+/* One reverse step on a 1-bit band, the form ggnn_backward runs for t > 0:
+ * the reverse of step t's propagation (ggnn_banded_step_bits_bwd: dM_e =
+ * A_e^T da and g = dX_in + sum_e dM_e W_e^T), then the reverse of step t-1's
+ * GRU update with g as the gradient of its output (ggnn_gru_update_bwd's
+ * node part), one kernel where the shape allows.  g itself is not stored.
+ *   da, W, dX_in, dM, ldm    as for ggnn_banded_step_bits_bwd
+ *   h_prev [n_pad][H] dt (X_{t-1});  saved_prev [n_pad][3H] dt (gates of step t-1)
+ *   da_prev [H][n_pad] dt feature-major (written; must not alias da)
+ *   dh_prev [n_pad][H] float (written);  ghat_prev [n_pad][3H] dt (written: the
+ *           gate pre-activation gradients r^ | z^ | n^ of step t-1, the factor of the
+ *           GRU weight gradients) */
+ggnn_status ggnn_step_bits_gru_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
+                                   const void* bits_t, const void* da, const void* W, const float* dX_in,
+                                   void* dM, int64_t ldm, const void* Wi, const void* U, const void* h_prev,
+                                   const void* saved_prev, void* da_prev, float* dh_prev, void* ghat_prev,
+                                   void* stream);
 
 /* Workspace bytes needed by ggnn_gru_update_bwd for these sizes. */
 size_t ggnn_gru_update_bwd_workspace_bytes(ggnn_dtype dt, int32_t n_pad, int32_t H);

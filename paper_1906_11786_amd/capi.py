@@ -30,7 +30,7 @@ EXPORTS = [
     "ggnn_abi_version", "ggnn_last_error", "ggnn_status_string",
     "ggnn_rcm_order", "ggnn_bandwidth", "ggnn_band_bytes", "ggnn_banded_pack",
     "ggnn_band_bits_bytes", "ggnn_banded_pack_bits", "ggnn_banded_step_bits", "ggnn_banded_propagate_bits_bwd",
-    "ggnn_banded_step_bits_bwd",
+    "ggnn_banded_step_bits_bwd", "ggnn_step_bits_gru", "ggnn_step_bits_gru_bwd",
     "ggnn_msg_transform", "ggnn_banded_propagate", "ggnn_gru_update",
     "ggnn_gru_update_bwd_workspace_bytes", "ggnn_gru_update_bwd",
     "ggnn_banded_propagate_bwd", "ggnn_msg_transform_bwd_workspace_bytes", "ggnn_msg_transform_bwd",
@@ -80,6 +80,9 @@ _SIGS = {
     "ggnn_banded_step_bits": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]),
     "ggnn_banded_propagate_bits_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp]),
     "ggnn_banded_step_bits_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i64, vp]),
+    "ggnn_step_bits_gru": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+    "ggnn_step_bits_gru_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp,
+                                         vp, vp, vp]),
     "ggnn_msg_transform": (C.c_int, [C.c_int, i32, i32, i32, vp, vp, vp, vp, vp]),
     "ggnn_banded_propagate": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp]),
     "ggnn_gru_update": (C.c_int, [C.c_int, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
@@ -233,6 +236,19 @@ def ggnn_banded_step_bits_bwd(dt, n_pad, B, H, E, bits_t, da, W, dX_in, dX_out, 
     _check("ggnn_banded_step_bits_bwd", lib().ggnn_banded_step_bits_bwd(
         _dt(dt), n_pad, B, H, E, _ptr(bits_t), _ptr(da), _ptr(W), _ptr(dX_in), _ptr(dX_out), _ptr(dM), ldm,
         _stream(stream)))
+
+
+def ggnn_step_bits_gru(dt, n_pad, B, H, E, bits, X, W, bias, Wi, U, b, a, h_out, saved, stream=None):
+    _check("ggnn_step_bits_gru", lib().ggnn_step_bits_gru(
+        _dt(dt), n_pad, B, H, E, _ptr(bits), _ptr(X), _ptr(W), _ptr(bias), _ptr(Wi), _ptr(U), _ptr(b), _ptr(a),
+        _ptr(h_out), _ptr(saved), _stream(stream)))
+
+
+def ggnn_step_bits_gru_bwd(dt, n_pad, B, H, E, bits_t, da, W, dX_in, dM, ldm, Wi, U, h_prev, saved_prev, da_prev,
+                           dh_prev, ghat_prev, stream=None):
+    _check("ggnn_step_bits_gru_bwd", lib().ggnn_step_bits_gru_bwd(
+        _dt(dt), n_pad, B, H, E, _ptr(bits_t), _ptr(da), _ptr(W), _ptr(dX_in), _ptr(dM), ldm, _ptr(Wi), _ptr(U),
+        _ptr(h_prev), _ptr(saved_prev), _ptr(da_prev), _ptr(dh_prev), _ptr(ghat_prev), _stream(stream)))
 
 
 def ggnn_msg_transform(dt, n_pad, H, E, X, W, bias, M, stream=None):

@@ -204,6 +204,63 @@ ggnn_status ggnn_banded_step_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, i
       "banded_step_bits_bwd");
 }
 
+ggnn_status ggnn_step_bits_gru(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E, const void* bits,
+                               const void* X, const void* W, const float* bias, const void* Wi, const void* U,
+                               const float* b, float* a, void* h_out, void* saved, void* stream) {
+  clear_error();
+  ggnn_status st = check_banded(dt, n_pad, B, H, E);
+  if (st != GGNN_OK) return st;
+  CHECK_PTR(bits, "bits");
+  CHECK_PTR(X, "X");
+  CHECK_PTR(W, "W");
+  CHECK_OPT_PTR(bias, "bias");
+  CHECK_PTR(Wi, "Wi");
+  CHECK_PTR(U, "U");
+  CHECK_PTR(b, "b");
+  CHECK_PTR(a, "a");
+  CHECK_PTR(h_out, "h_out");
+  CHECK_PTR(saved, "saved");
+  hipStream_t s = as_stream(stream);
+  bool fused = false;
+  hipError_t err = launch_step_fwd_bits_gru(dt, n_pad, B, H, E, bits, X, W, bias, a, Wi, U, b, h_out, saved, &fused, s);
+  if (err == hipSuccess && !fused) err = launch_gru_fwd(dt, n_pad, H, a, X, Wi, U, b, h_out, saved, s);
+  return device_status(err, "step_bits_gru");
+}
+
+ggnn_status ggnn_step_bits_gru_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
+                                   const void* bits_t, const void* da, const void* W, const float* dX_in, void* dM,
+                                   int64_t ldm, const void* Wi, const void* U, const void* h_prev,
+                                   const void* saved_prev, void* da_prev, float* dh_prev, void* ghat_prev,
+                                   void* stream) {
+  clear_error();
+  ggnn_status st = check_banded(dt, n_pad, B, H, E);
+  if (st != GGNN_OK) return st;
+  CHECK_PTR(bits_t, "bits_t");
+  CHECK_PTR(da, "da");
+  CHECK_PTR(W, "W");
+  CHECK_OPT_PTR(dX_in, "dX_in");
+  CHECK_PTR(dM, "dM");
+  GGNN_CHECK_ARG(ldm >= n_pad, "ldm=%lld must be at least n_pad=%d", (long long)ldm, n_pad);
+  CHECK_PTR(Wi, "Wi");
+  CHECK_PTR(U, "U");
+  CHECK_PTR(h_prev, "h_prev");
+  CHECK_PTR(saved_prev, "saved_prev");
+  CHECK_PTR(da_prev, "da_prev");
+  CHECK_PTR(dh_prev, "dh_prev");
+  CHECK_PTR(ghat_prev, "ghat_prev");
+  GGNN_CHECK_ARG(da_prev != da, "da_prev must not alias da (da is read by every workgroup)");
+  hipStream_t s = as_stream(stream);
+  bool fused = false;
+  hipError_t err = launch_step_bwd_bits_gru(dt, n_pad, B, H, E, bits_t, da, W, dX_in, dh_prev, dM, (long)ldm, Wi, U,
+                                            h_prev, saved_prev, da_prev, dh_prev, ghat_prev, &fused, s);
+  // Unfused shapes: the summed dX went to dh_prev; the GRU reverse reads it
+  // there and overwrites it node by node with dh (each node's row is read
+  // before it is written, by the same wave).
+  if (err == hipSuccess && !fused)
+    err = launch_gru_bwd_nodes(dt, n_pad, H, dh_prev, h_prev, saved_prev, Wi, U, da_prev, dh_prev, ghat_prev, s);
+  return device_status(err, "step_bits_gru_bwd");
+}
+
 size_t ggnn_msg_transform_bwd_workspace_bytes(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E) {
   if (!supported_dtype(dt) || n_pad <= 0 || n_pad % 32 != 0 || !supported_H(H) || E < 1 || E > 64) return 0;
   return transform_wgrad_workspace(n_pad, H, E);

@@ -228,7 +228,7 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
 template <typename S, int H> struct GruWgradCfg {
   static constexpr int IT = H >= 128 ? 4096 / H : H;   // input features per workgroup
   static constexpr int NI = IT / 16, NCT = 3 * H / 16;  // tiles: input, gate columns
-  static constexpr int KC = (H >= 256 || sizeof(S) == 4) ? 32 : 64;   // rows per chunk
+  static constexpr int KC = (sizeof(S) == 4 || H >= 256) ? 32 : (H >= 128 ? 64 : 128);   // rows per chunk
   static constexpr int IW = H == 32 ? 1 : NI;            // input tiles per wave
   static constexpr int CW = H == 32 ? 3 : NCT / 4;       // gate-column tiles per wave
   static constexpr int PA = IT + 16, PG = 3 * H + 16;    // LDS row pitches (elements)
@@ -348,7 +348,7 @@ __global__ __launch_bounds__(512) void gru_wgrad_kernel(const float* __restrict_
     }
   };
 
-  // Splits start at multiples of 64 rows; a last chunk that runs past the
+  // Splits start at multiples of KC rows; a last chunk that runs past the
   // split is zero-filled.
   if (nlo < nhi) load_chunk(nlo);
   int buf = 0;
@@ -405,15 +405,14 @@ __global__ __launch_bounds__(512) void gru_wgrad_kernel(const float* __restrict_
 namespace {
 // Row split of the weight-gradient contraction: about 256 workgroups (one
 // per compute unit, 8 waves each) over splits x input-feature slices;
-// splits are multiples of 64 rows.
+// splits are multiples of 128 rows.
 struct Split {
   int nsplit, per;
 };
 Split gru_split(long K, int H) {
   const long slices = H >= 128 ? H / (4096 / H) : 1;
   const long want = 256 / slices > 0 ? 256 / slices : 1;
-  long per = ((K + want - 1) / want + 63) / 64 * 64;
-  if (per < 64) per = 64;
+  long per = ((K + want - 1) / want + 127) / 128 * 128;
   return {(int)((K + per - 1) / per), (int)per};
 }
 

@@ -289,114 +289,143 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
 // step writes dM_e rows node by node): one split of the rows,
 //   P[split][e][h_in][h_out] = sum_k X[k][h_in] * dM[e][k][h_out],
 //   Pb[split][e][h_out]      = sum_k dM[e][k][h_out],
-// rows k of type e at dM + (e * ldk + k) * H.  Tile TI x TI (TI = min(H, 64)),
-// TI/16 waves.  Rows are taken in chunks of 64: both operands are staged
-// transposed in LDS (V x V register-transposed tiles; consecutive lanes fill
-// consecutive 16-byte pieces of one LDS row, so the stores are conflict-free
-// and every load instruction reads whole lines) and read as contiguous
-// fragments.  The next chunk's tiles are loaded while the current one is
-// multiplied.  The tile index runs fastest over the logical workgroup index,
-// so the tiles of one split share their X rows in one XCD's L2.
+// rows k of type e at dM + (e * ldk + k) * H.  A workgroup (8 waves) owns one
+// split of the rows, a group of TE edge types and a slice of IT input
+// features: per chunk of KC rows it stages X and the group's dM rows
+// node-major in LDS (plain 16-byte copies) and reads them as matrix-core
+// fragments with transposing LDS reads, the next chunk's loads in flight.
+// Wave w owns the (type, output tile) pairs w, w + 8, ... of its workgroup,
+// each over all IT/16 input tiles.
 // ---------------------------------------------------------------------------
+template <typename S, int H> struct WgradNmCfg {
+  static constexpr int IT = H >= 256 ? 64 : H;                  // input features per workgroup
+  static constexpr int TE = H <= 32 ? 10 : (H == 64 ? 4 : (H == 128 && sizeof(S) == 2 ? 2 : 1));   // types per workgroup
+  static constexpr int KC = sizeof(S) == 4 ? 64 : 128;           // rows per chunk
+  static constexpr int PX = IT + 16, PD = H + 16;                // LDS row pitches (elements)
+  static constexpr int NPAIR = TE * H / 16;                      // (type, output tile) pairs
+  static constexpr int PW = (NPAIR + 7) / 8;                     // pairs per wave (at most)
+  static constexpr int NBUF = 2 * KC * (PX + TE * PD) * (int)sizeof(S) <= 160 * 1024 ? 2 : 1;
+};
+
 template <typename S, int H>
-__global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgrad_nm_kernel(
-    const S* __restrict__ X, const S* __restrict__ dM, long ldk, float* __restrict__ P, float* __restrict__ Pb,
-    long K, int E, int rows_per_split) {
-  constexpr int TI = H < 64 ? H : 64;
-  constexpr int WAVES = TI / 16;
-  constexpr int NT = WAVES * kWave;
+__global__ __launch_bounds__(512) void transform_wgrad_nm_kernel(const S* __restrict__ X, const S* __restrict__ dM,
+                                                                 long ldk, float* __restrict__ P,
+                                                                 float* __restrict__ Pb, long K, int E,
+                                                                 int rows_per_split) {
+  using C = WgradNmCfg<S, H>;
+  constexpr int IT = C::IT, TE = C::TE, KC = C::KC, PX = C::PX, PD = C::PD, PW = C::PW, NBUF = C::NBUF;
+  constexpr int NT = 512, NI = IT / 16;
   constexpr int V = 16 / sizeof(S);
-  constexpr int KN = 64;                  // rows per chunk
-  constexpr int PK = KN + V;              // LDS row pitch (16-byte multiple)
-  constexpr int NTL = TI / 16;
-  constexpr int TPD = H / TI;             // tiles per dimension
-  constexpr int TT = (KN / V) * (TI / V); // V x V tiles per operand chunk
-  constexpr int UN = (2 * TT + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) S xs[TI * PK];
-  __shared__ __attribute__((aligned(16))) S ds[TI * PK];
+  constexpr int NX = KC * IT / V, ND = TE * KC * H / V;   // 16-byte units per chunk
+  constexpr int UX = (NX + NT - 1) / NT, UD = (ND + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) S sx[NBUF][KC * PX];
+  __shared__ __attribute__((aligned(16))) S sd[NBUF][TE * KC * PD];
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int q = lane % 16, g = lane / 16;
+  constexpr int NSL = H / IT;
+  const int ngroups = (E + TE - 1) / TE;
   int bid = xcd_swizzle(blockIdx.x, gridDim.x);
-  const int to = bid % TPD; bid /= TPD;
-  const int ti = bid % TPD; bid /= TPD;
-  const int e = bid % E;
-  const int split = bid / E;
+  const int sl = bid % NSL; bid /= NSL;
+  const int grp = bid % ngroups;
+  const int split = bid / ngroups;
+  const int e0 = grp * TE, ne = min(TE, E - e0);
+  const int i0 = sl * IT;
   const long nlo = (long)split * rows_per_split;
   const long nhi = min(K, nlo + rows_per_split);
-  const S* dMe = dM + (size_t)e * ldk * H;
 
-  f32x4 acc[NTL];
-  float bsum[NTL];
+  f32x4 acc[PW][NI];
+  float bsum[PW];
 #pragma unroll
-  for (int n = 0; n < NTL; ++n) {
-    acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-    bsum[n] = 0.f;
+  for (int p = 0; p < PW; ++p) {
+    bsum[p] = 0.f;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) acc[p][i] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  const bool do_bias = (ti == 0 && wave == 0 && Pb != nullptr);
 
-  // Unit u < TT: X tile; TT <= u < 2 TT: dM tile.  Within an operand, the
-  // row-group index kq runs fastest.  Rows past nhi are staged as zeros.
-  u32x4 r[UN][V];
+  u32x4 rx[UX], rd[UD];
   auto load_chunk = [&](long c0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < UN; ++u) {
+    for (int u = 0; u < UX; ++u) {
       const int lin = u * NT + tid;
-      if ((2 * TT) % NT == 0 || lin < 2 * TT) {
-        const int w = lin % TT, kq = w % (KN / V), cq = w / (KN / V);
-        const long row = c0 + V * kq;
-        const S* src = lin < TT ? X + (size_t)row * H + ti * TI + V * cq : dMe + (size_t)row * H + to * TI + V * cq;
+      const long row = c0 + lin / (IT / V);
+      const int f = i0 + (lin % (IT / V)) * V;
+      rx[u] = ((NX % NT == 0 || lin < NX) && row < nhi) ? *reinterpret_cast<const u32x4*>(X + (size_t)row * H + f)
+                                                        : u32x4{0u, 0u, 0u, 0u};
+    }
 #pragma unroll
-        for (int i = 0; i < V; ++i)
-          r[u][i] = (row + i < nhi) ? *reinterpret_cast<const u32x4*>(src + (size_t)i * H) : u32x4{0u, 0u, 0u, 0u};
+    for (int u = 0; u < UD; ++u) {
+      const int lin = u * NT + tid;
+      const int te = lin / (KC * H / V), rem = lin % (KC * H / V);
+      const long row = c0 + rem / (H / V);
+      const int c = (rem % (H / V)) * V;
+      rd[u] = ((ND % NT == 0 || lin < ND) && te < ne && row < nhi)
+                  ? *reinterpret_cast<const u32x4*>(dM + ((size_t)(e0 + te) * ldk + row) * H + c)
+                  : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+  auto store_chunk = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < UX; ++u) {
+      const int lin = u * NT + tid;
+      if (NX % NT == 0 || lin < NX)
+        *reinterpret_cast<u32x4*>(&sx[buf][(lin / (IT / V)) * PX + (lin % (IT / V)) * V]) = rx[u];
+    }
+#pragma unroll
+    for (int u = 0; u < UD; ++u) {
+      const int lin = u * NT + tid;
+      if (ND % NT == 0 || lin < ND) {
+        const int te = lin / (KC * H / V), rem = lin % (KC * H / V);
+        *reinterpret_cast<u32x4*>(&sd[buf][(te * KC + rem / (H / V)) * PD + (rem % (H / V)) * V]) = rd[u];
       }
     }
   };
-  auto store_chunk = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int u = 0; u < UN; ++u) {
-      const int lin = u * NT + tid;
-      if ((2 * TT) % NT == 0 || lin < 2 * TT) {
-        const int w = lin % TT, kq = w % (KN / V), cq = w / (KN / V);
-        tile_store_T<S, PK>(&(lin < TT ? xs : ds)[(V * cq) * PK + V * kq], r[u]);
-      }
-    }
-  };
+
+  // Splits start at multiples of KC rows; a chunk that runs past the split
+  // (or a type past E) is zero-filled.
   if (nlo < nhi) load_chunk(nlo);
-  for (long c0 = nlo; c0 < nhi; c0 += KN) {
+  int buf = 0;
+  for (long c0 = nlo; c0 < nhi; c0 += KC, buf = NBUF == 2 ? buf ^ 1 : 0) {
+    if (NBUF == 1 && c0 > nlo) __syncthreads();
+    store_chunk(buf);
     __syncthreads();
-    store_chunk();
-    __syncthreads();
-    if (c0 + KN < nhi) load_chunk(c0 + KN);
+    if (c0 + KC < nhi) load_chunk(c0 + KC);
 #pragma unroll
-    for (int kk = 0; kk < KN / 32; ++kk) {
-      const frag_t<S> afr = load8(&xs[(16 * wave + q) * PK + 32 * kk + 8 * g]);
+    for (int k0 = 0; k0 < KC; k0 += 32) {
+      frag_t<S> fa[NI];
 #pragma unroll
-      for (int n = 0; n < NTL; ++n) {
-        const frag_t<S> bf = load8(&ds[(16 * n + q) * PK + 32 * kk + 8 * g]);
-        mma(acc[n], afr, bf);
-        if (do_bias) {
+      for (int i = 0; i < NI; ++i) fa[i] = tr_frag(sx[buf], PX, k0, 16 * i, lane);
 #pragma unroll
-          for (int x = 0; x < 8; ++x) bsum[n] += static_cast<float>(bf[x]);
+      for (int p = 0; p < PW; ++p) {
+        const int pr = wave + 8 * p;
+        if (PW * 8 == C::NPAIR || pr < C::NPAIR) {
+          const int te = pr / (H / 16), ot = pr % (H / 16);
+          const frag_t<S> fb = tr_frag(sd[buf] + te * KC * PD, PD, k0, 16 * ot, lane);
+#pragma unroll
+          for (int x = 0; x < 8; ++x) bsum[p] += static_cast<float>(fb[x]);
+#pragma unroll
+          for (int i = 0; i < NI; ++i) mma(acc[p][i], fa[i], fb);
         }
       }
     }
   }
-  // D[h_in = ti*TI + 16*wave + 4g + j][h_out = to*TI + 16n + q]
-  float* out = P + ((size_t)split * E + e) * H * H;
+  // D[h_in = i0 + 16 i + 4g + j][h_out = 16 ot + q] of type e0 + te
 #pragma unroll
-  for (int n = 0; n < NTL; ++n) {
-    const int o = to * TI + 16 * n + q;
+  for (int p = 0; p < PW; ++p) {
+    const int pr = wave + 8 * p;
+    if (!(PW * 8 == C::NPAIR || pr < C::NPAIR)) continue;
+    const int te = pr / (H / 16), ot = pr % (H / 16);
+    if (te >= ne) continue;
+    float* out = P + ((size_t)split * E + e0 + te) * H * H;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) out[(size_t)(ti * TI + 16 * wave + 4 * g + j) * H + o] = acc[n][j];
-  }
-  if (do_bias) {
+    for (int i = 0; i < NI; ++i)
 #pragma unroll
-    for (int n = 0; n < NTL; ++n) {
-      float v = bsum[n];
+      for (int j = 0; j < 4; ++j) out[(size_t)(i0 + 16 * i + 4 * g + j) * H + 16 * ot + q] = acc[p][i][j];
+    if (Pb != nullptr && sl == 0) {
+      float v = bsum[p];
       v += __shfl_xor(v, 16);
       v += __shfl_xor(v, 32);
-      if (g == 0) Pb[((size_t)split * E + e) * H + to * TI + 16 * n + q] = v;
+      if (g == 0) Pb[((size_t)split * E + e0 + te) * H + 16 * ot + q] = v;
     }
   }
 }
@@ -487,6 +516,17 @@ Split transform_split(long K, int H, int E) {
   return {(int)((K + per - 1) / per), (int)per};
 }
 
+// Node-major form: about 256 workgroups (one per compute unit, 8 waves
+// each) over splits x type groups x input slices; splits are multiples of
+// 128 rows.
+Split transform_nm_split(long K, int H, int E) {
+  const long te = H <= 32 ? 10 : (H == 64 ? 4 : (H == 128 ? 2 : 1));
+  const long per_split = ((E + te - 1) / te) * (H >= 256 ? H / 64 : 1);
+  const long want = 256 / per_split > 0 ? 256 / per_split : 1;
+  long per = ((K + want - 1) / want + 127) / 128 * 128;
+  return {(int)((K + per - 1) / per), (int)per};
+}
+
 template <typename S, int H>
 hipError_t transform_fwd_h(int n_pad, int E, const void* X, const void* W, const float* bias, float* M,
                            hipStream_t st) {
@@ -531,12 +571,12 @@ hipError_t transform_wgrad_h(long K, int E, const void* X, const void* dM, long 
 template <typename S, int H>
 hipError_t transform_wgrad_nm_h(long K, int E, const void* X, const void* dM, long ldk, float* dW, float* dbias,
                                 void* ws, hipStream_t st) {
-  Split sp = transform_split(K, H, E);
-  constexpr int TI = H < 64 ? H : 64;
+  Split sp = transform_nm_split(K, H, E);
+  using C = dev::WgradNmCfg<S, H>;
   float* P = static_cast<float*>(ws);
   float* Pb = dbias ? P + (size_t)sp.nsplit * E * H * H : nullptr;
-  const int blocks = sp.nsplit * E * (H / TI) * (H / TI);
-  hipLaunchKernelGGL((dev::transform_wgrad_nm_kernel<S, H>), dim3(blocks), dim3(TI / 16 * 64), 0, st,
+  const int blocks = sp.nsplit * ((E + C::TE - 1) / C::TE) * (H / C::IT);
+  hipLaunchKernelGGL((dev::transform_wgrad_nm_kernel<S, H>), dim3(blocks), dim3(512), 0, st,
                      static_cast<const S*>(X), static_cast<const S*>(dM), ldk, P, Pb, K, E, sp.per);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
@@ -594,8 +634,10 @@ hipError_t transform_wgrad_t(long K, int H, int E, const void* X, const void* dM
 
 #if GGNN_DT_BF16
 size_t transform_wgrad_workspace(long K, int H, int E) {
-  Split sp = transform_split(K, H, E);
-  return ((size_t)sp.nsplit * E * H * H + (size_t)sp.nsplit * E * H) * sizeof(float);
+  // large enough for both forms (feature-major and node-major dM)
+  const Split a = transform_split(K, H, E), b = transform_nm_split(K, H, E);
+  const size_t n = (size_t)(a.nsplit > b.nsplit ? a.nsplit : b.nsplit);
+  return (n * E * H * H + n * E * H) * sizeof(float);
 }
 #endif
 

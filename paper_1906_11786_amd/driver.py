@@ -123,11 +123,19 @@ class BandedGGNN:
                   else None)
         self.G = torch.from_numpy(params.G.astype(np.float32)).to(device)
         self.dX = torch.empty((n_pad, H), dtype=torch.float32, device=device)
-        self.dW = torch.zeros((E, H, H), dtype=torch.float32, device=device)
-        self.dbias = torch.zeros((E, H), dtype=torch.float32, device=device)
-        self.dWi = torch.zeros((H, 3 * H), dtype=torch.float32, device=device)
-        self.dU = torch.zeros((H, 3 * H), dtype=torch.float32, device=device)
-        self.db = torch.zeros((3 * H,), dtype=torch.float32, device=device)
+        # All weight gradients in one buffer (one fill clears them), each
+        # view starting on a 64-float boundary.
+        sizes = [E * H * H, E * H, H * 3 * H, H * 3 * H, 3 * H]
+        offs = [0]
+        for s_ in sizes:
+            offs.append(offs[-1] + -(-s_ // 64) * 64)
+        self.grad_buf = torch.zeros((offs[-1],), dtype=torch.float32, device=device)
+        views = [self.grad_buf[o:o + s_] for o, s_ in zip(offs, sizes)]
+        self.dW = views[0].view(E, H, H)
+        self.dbias = views[1].view(E, H)
+        self.dWi = views[2].view(H, 3 * H)
+        self.dU = views[3].view(H, 3 * H)
+        self.db = views[4]
         self.da = torch.empty((H, n_pad), dtype=td, device=device)
         self.dM = torch.empty((E, H, T * n_pad), dtype=td, device=device)
         self.dh = torch.empty((n_pad, H), dtype=torch.float32, device=device)
@@ -154,14 +162,37 @@ class BandedGGNN:
         first unless zero_grads is False (then they accumulate)."""
         self.dX.copy_(self.G)
         if zero_grads:
-            for t in (self.dW, self.dbias, self.dWi, self.dU, self.db):
-                t.zero_()
+            self.grad_buf.zero_()
         capi.ggnn_backward(self.model, self.act, self.grads, stream)
 
     def step(self, stream=None):
         """One pass of the hot path: T forward steps then T reverse steps."""
         self.forward(stream)
         self.backward(stream)
+
+    def capture(self):
+        """Record one step() as a HIP graph (torch.cuda.CUDAGraph on a side
+        stream); replay() then runs the same kernels without host launch
+        overhead.  Nothing in the step calls hipMemsetAsync (gradients are
+        cleared by a fill kernel), so the graph holds kernel and copy nodes
+        only."""
+        torch = self.torch
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            self.step()   # warm-up on the capture stream
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            self.step()
+        torch.cuda.synchronize()
+        self.graph = g
+        return g
+
+    def replay(self):
+        """One step() through the captured graph (capture() first)."""
+        self.graph.replay()
 
     def results(self) -> dict:
         """Host copies (float64) of the outputs compared against the oracle."""

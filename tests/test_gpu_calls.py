@@ -306,6 +306,73 @@ def test_banded_step_bits_bwd_real_values(dt, B, H, E, nb):
     assert relerr(host(dX), want_dX) <= TOL[dt]
 
 
+STEP_GRU_CASES = [(128, 64, 10, 5), (64, 128, 2, 6), (32, 32, 4, 9), (256, 256, 2, 3)]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("B,H,E,nb", STEP_GRU_CASES)
+def test_step_bits_gru(dt, B, H, E, nb):
+    """One forward step (propagation + GRU, fused where the shape allows):
+    the aggregate against the oracle's, the GRU outputs against the oracle's
+    GRU of that aggregate."""
+    say(f"step_bits_gru dt={dt} B={B} H={H} E={E} nb={nb}")
+    rng = np.random.default_rng(B + 7 * H + E)
+    n = B * nb
+    src, dst, et = _edges(rng, n, 4 * n, E, B + 3)
+    bits, _, _ = _bits(n, E, B, src, dst, et)
+    X = round_to(dt, rng.standard_normal((n, H)))
+    W = round_to(dt, rng.standard_normal((E, H, H)) / np.sqrt(H))
+    bias = rng.standard_normal((E, H)) * 0.1
+    _, _, Wi, U, b = _gru_inputs(dt, rng, n, H)
+    a = torch.full((n, H), float("nan"), device="cuda")
+    h_out = torch.full((n, H), float("nan"), device="cuda", dtype=torch_dt(dt))
+    saved = torch.full((n, 3 * H), float("nan"), device="cuda", dtype=torch_dt(dt))
+    capi.ggnn_step_bits_gru(dt, n, B, H, E, bits, dev(X, dt), dev(W, dt), dev(bias), dev(Wi, dt), dev(U, dt),
+                            dev(b), a, h_out, saved)
+    s, d, e, _, _ = O.kept_edges(src, dst, et, B)
+    wa = O.aggregate(n, s, d, e, O.msg_transform(X, W, bias))
+    assert relerr(host(a), wa) <= 1e-4
+    # the GRU half consumes the aggregate the kernel produced (fp32)
+    hn, r, z, nn = O.gru_forward(host(a), X, Wi, U, b)
+    assert relerr(host(h_out), hn) <= TOL[dt]
+    assert relerr(host(saved), np.concatenate([r, z, nn], axis=1)) <= TOL[dt]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("B,H,E,nb", STEP_GRU_CASES)
+def test_step_bits_gru_bwd(dt, B, H, E, nb):
+    """One reverse step (propagation reverse of step t + GRU reverse of step
+    t-1, fused where the shape allows) against the oracle."""
+    say(f"step_bits_gru_bwd dt={dt} B={B} H={H} E={E} nb={nb}")
+    rng = np.random.default_rng(B + 11 * H + E)
+    n = B * nb
+    src, dst, et = _edges(rng, n, 4 * n, E, B + 3)
+    _, bits_t, _ = _bits(n, E, B, src, dst, et)
+    da = round_to(dt, rng.standard_normal((n, H)))
+    W = round_to(dt, rng.standard_normal((E, H, H)) / np.sqrt(H))
+    dX_in = rng.standard_normal((n, H))
+    a_prev, h_prev, Wi, U, b = _gru_inputs(dt, rng, n, H)
+    _, r, z, nn = O.gru_forward(a_prev, h_prev, Wi, U, b)
+    saved = round_to(dt, np.concatenate([r, z, nn], axis=1))
+    r, z, nn = saved[:, :H], saved[:, H:2 * H], saved[:, 2 * H:]
+    dM = torch.full((E, n, H), float("nan"), device="cuda", dtype=torch_dt(dt))
+    da_prev = torch.full((H, n), float("nan"), device="cuda", dtype=torch_dt(dt))
+    dh_prev = torch.full((n, H), float("nan"), device="cuda")
+    ghat = torch.full((n, 3 * H), float("nan"), device="cuda", dtype=torch_dt(dt))
+    capi.ggnn_step_bits_gru_bwd(dt, n, B, H, E, bits_t, dev(da.T, dt), dev(W, dt), dev(dX_in), dM, n, dev(Wi, dt),
+                                dev(U, dt), dev(h_prev, dt), dev(saved, dt), da_prev, dh_prev, ghat)
+    s, d, e, _, _ = O.kept_edges(src, dst, et, B)
+    want_dM = O.aggregate_transpose(n, s, d, e, da, E)
+    g, _, _ = O.msg_transform_backward(np.zeros((n, H)), W, want_dM)
+    wda, wdh, wdWi, _, wdb = O.gru_backward(dX_in + g, a_prev, h_prev, r, z, nn, Wi, U)
+    assert relerr(host(dM), want_dM) <= TOL[dt]
+    assert relerr(host(da_prev).T, wda) <= TOL[dt]
+    assert relerr(host(dh_prev), wdh) <= TOL[dt]
+    gh = host(ghat)
+    assert relerr(gh.sum(axis=0), wdb) <= TOL[dt]
+    assert relerr(a_prev.T @ gh, wdWi) <= TOL[dt]
+
+
 def test_device_errors_are_reported():
     n, H = 128, 64
     ws_n = capi.ggnn_gru_update_bwd_workspace_bytes("bf16", n, H)

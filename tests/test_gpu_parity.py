@@ -199,3 +199,28 @@ def test_batch_100k_workload_sampled():
 
 def test_stress_1m_workload_sampled():
     _sampled_batch(CONFIGS[4], picks=[0, 70, 139])
+
+
+@pytest.mark.parametrize("band_format", ["bits", "dense"])
+def test_graph_replay_equals_eager(band_format):
+    """The step captured as a HIP graph: every replay (with eager work and
+    synchronizations between replays) gives the eager step's results bit for
+    bit, and they match the oracle."""
+    dt, n, B, E, H, T = "bf16", 1500, 128, 4, 64, 3
+    say(f"graph replay band={band_format}")
+    g = scramble_graph(61, 0, backbone_graph(61, 0, n, E, span_mean=6.0, max_span=B))[0]
+    m, res, out = _run_full([g], B, E, H, T, dt, 61, reorder=True, with_bias=True, band_format=band_format)
+    _compare(res, out, dt)
+    m.capture()
+    for rep in range(3):
+        m.replay()
+        torch.cuda.synchronize()
+        got = m.results()
+        for k in res:
+            assert np.array_equal(got[k], res[k]), (rep, k)
+        # eager work between the replays: an eager step on the same buffers
+        m.step()
+        torch.cuda.synchronize()
+        again = m.results()
+        for k in res:
+            assert np.array_equal(again[k], res[k]), (rep, k)
