@@ -98,12 +98,22 @@ template <typename S, int H>
 __device__ __forceinline__ frag_t<S> load_frag(const S* v, int kk, int m, int lane) {
   return load_fragi<S>(v, kk * (H / 16) + m, lane);
 }
-// Stage nodes [n0, n0 + KC) of a node-major [n][H] array into LDS in
-// fragment order.  Each thread moves a pair of consecutive nodes for eight
-// features and writes 2-element words.
-template <typename S, int H, int KC, int NT>
+// Staging of a chunk of KC nodes x H features for the streamed (large-H)
+// forms, in one of two LDS layouts: fragment order (frag_off) or feature
+// rows dst[h * VP + c].  The fragment order makes every fragment read a
+// single pass, but its writes from node-major rows conflict; feature rows
+// are written without conflicts and read in two passes.  Measured on the
+// two streamed shapes: fragment order wins at H = 128, feature rows at
+// H = 256 (each chunk there is read by fewer waves per byte written).
+//
+// Nodes [n0, n0 + KC) of a node-major [n][H] array: each thread moves a pair
+// of consecutive nodes for eight features and writes 2-element words.
+template <typename S, int H, int KC, int VP, int NT, bool ROWS>
 __device__ __forceinline__ void stage_nodes_T(S* dst, const S* src, int n0, int tid) {
   constexpr int PAIRS = KC / 2;
+  auto at = [&](int h, int c) __attribute__((always_inline)) {
+    return ROWS ? h * VP + c : frag_off<S, H, KC>(h, c);
+  };
   for (int lin = tid; lin < PAIRS * (H / 8); lin += NT) {
     const int cp = lin % PAIRS, f0 = (lin / PAIRS) * 8;
     const S* p0 = src + (size_t)(n0 + 2 * cp) * H + f0;
@@ -112,27 +122,30 @@ __device__ __forceinline__ void stage_nodes_T(S* dst, const S* src, int n0, int 
       u32x4 x1 = *reinterpret_cast<const u32x4*>(p0 + H);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        store_pair(&dst[frag_off<S, H, KC>(f0 + 2 * i, 2 * cp)], x0[i] & 0xFFFFu, x1[i] & 0xFFFFu);
-        store_pair(&dst[frag_off<S, H, KC>(f0 + 2 * i + 1, 2 * cp)], x0[i] >> 16, x1[i] >> 16);
+        store_pair(&dst[at(f0 + 2 * i, 2 * cp)], x0[i] & 0xFFFFu, x1[i] & 0xFFFFu);
+        store_pair(&dst[at(f0 + 2 * i + 1, 2 * cp)], x0[i] >> 16, x1[i] >> 16);
       }
     } else {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         typedef float f32x2 __attribute__((ext_vector_type(2)));
-        *reinterpret_cast<f32x2*>(&dst[frag_off<S, H, KC>(f0 + i, 2 * cp)]) = f32x2{p0[i], p0[H + i]};
+        *reinterpret_cast<f32x2*>(&dst[at(f0 + i, 2 * cp)]) = f32x2{p0[i], p0[H + i]};
       }
     }
   }
 }
 
-// Stage columns [n0, n0 + KC) of a feature-major [H][n_pad] array into LDS
-// in fragment order (16-byte copies: a unit is one fragment vector).
-template <typename S, int H, int KC, int NT>
+// Columns [n0, n0 + KC) of a feature-major [H][n_pad] array (16-byte
+// copies: a unit is one fragment vector).  In fragment order the feature
+// runs fastest over the threads, so the 16 lanes of one LDS pass write 16
+// different fragment rows (distinct banks).
+template <typename S, int H, int KC, int VP, int NT, bool ROWS>
 __device__ __forceinline__ void stage_cols(S* dst, const S* src, int n_pad, int n0, int tid) {
   constexpr int V = 16 / sizeof(S);
   for (int lin = tid; lin < H * (KC / V); lin += NT) {
-    const int h = lin / (KC / V), c = (lin % (KC / V)) * V;
-    *reinterpret_cast<u32x4*>(&dst[frag_off<S, H, KC>(h, c)]) =
+    const int h = ROWS ? lin / (KC / V) : lin % H;
+    const int c = ROWS ? (lin % (KC / V)) * V : (lin / H) * V;
+    *reinterpret_cast<u32x4*>(&dst[ROWS ? h * VP + c : frag_off<S, H, KC>(h, c)]) =
         *reinterpret_cast<const u32x4*>(src + (size_t)h * n_pad + n0 + c);
   }
 }
@@ -146,6 +159,7 @@ struct BitsCfg {
   static constexpr int KC = ALL ? B : (B < 64 ? B : 64);
   static constexpr int NBUF = ALL ? 3 : 1;
   static constexpr int VP = KC + V;
+  static constexpr bool ROWS = !ALL && H >= 256;   // streamed chunks kept as feature rows
   static constexpr int RB = KC / 32;        // bit-row bytes per lane per chunk (= k steps per chunk)
   static constexpr int RPW = H >= 256 ? 16 : 32;   // rows per wave
   static constexpr int NTW = RPW / 16;      // 16-row tiles per wave
@@ -471,9 +485,9 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         if constexpr (!C::ALL) {
           __syncthreads();
           if constexpr (REV) {
-            stage_cols<S, H, KC, NT>(vt[0], X, n_pad, (k - 1 + s) * B + c0, tid);
+            stage_cols<S, H, KC, VP, NT, C::ROWS>(vt[0], X, n_pad, (k - 1 + s) * B + c0, tid);
           } else {
-            stage_nodes_T<S, H, KC, NT>(vt[0], X, (k - 1 + s) * B + c0, tid);
+            stage_nodes_T<S, H, KC, VP, NT, C::ROWS>(vt[0], X, (k - 1 + s) * B + c0, tid);
           }
           __syncthreads();
         }
@@ -495,7 +509,8 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
           for (int n = 0; n < NTW; ++n) bf[n] = bits_frag<S>(rb[n].byte(kk));
 #pragma unroll
           for (int m = 0; m < MT; ++m) {
-            const frag_t<S> af = load_frag<S, H>(v, kk, m, lane);
+            const frag_t<S> af = C::ROWS ? load8(&v[(16 * m + q) * VP + g * (KC / 4) + 8 * kk])
+                                         : load_frag<S, H>(v, kk, m, lane);
 #pragma unroll
             for (int n = 0; n < NTW; ++n) mma(pre[n][m], af, bf[n]);
           }
@@ -844,7 +859,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
       for (int c0 = 0; c0 < B; c0 += KC) {
         if constexpr (!C::ALL) {
           __syncthreads();
-          stage_cols<S, H, KC, NT>(vt[0], da, n_pad, (j - 1 + s) * B + c0, tid);
+          stage_cols<S, H, KC, VP, NT, C::ROWS>(vt[0], da, n_pad, (j - 1 + s) * B + c0, tid);
           __syncthreads();
         }
         const S* v = vt[C::ALL ? s : 0];
@@ -864,7 +879,8 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
           for (int m = 0; m < NTW; ++m) af[m] = bits_frag<S>(rb[m].byte(kk));
 #pragma unroll
           for (int n = 0; n < NTL; ++n) {
-            const frag_t<S> bf = load_frag<S, H>(v, kk, n, lane);
+            const frag_t<S> bf = C::ROWS ? load8(&v[(16 * n + q) * VP + g * (KC / 4) + 8 * kk])
+                                         : load_frag<S, H>(v, kk, n, lane);
 #pragma unroll
             for (int m = 0; m < NTW; ++m) mma(acc[m][n], af[m], bf);
           }
