@@ -211,6 +211,168 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
 }
 
 // ---------------------------------------------------------------------------
+// Backward for large H (bf16, H >= 128), the same arithmetic as
+// gru_bwd_wave, with the weights shared through LDS: a workgroup of 8 waves
+// (16 nodes each) streams the weights once per 128 nodes, in blocks of 16
+// input features (rows of Wi and U) kept in fragment order and double
+// buffered (the next block's loads are in flight during the current one).
+//   pass 1: q' = n^ U_n^T, block m gives q' for input features 16m..16m+15,
+//           hence r^ and the q' r term of dh for them;
+//   pass 2: block n gives da for input features 16n..16n+15 (G^ Wi^T, all
+//           three gates) and finishes dh for them (r^ U_r^T + z^ U_z^T).
+// ---------------------------------------------------------------------------
+template <typename S, int H>
+__global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restrict__ gin, const S* __restrict__ h,
+                                                          const S* __restrict__ saved, const S* __restrict__ Wi,
+                                                          const S* __restrict__ U, S* __restrict__ daT,
+                                                          float* __restrict__ dh, S* __restrict__ ghat, int n_pad) {
+  static_assert(sizeof(S) == 2, "bf16 only");
+  constexpr int NT = 512, V = 8;
+  constexpr int KS = H / 32, MTL = H / 16;
+  // LDS per buffer: pass 1 the n-gate part of a U block; pass 2 a Wi block
+  // (three gates) and the r, z part of a U block, both in fragment order
+  // (index gate * KS + kk within the block).
+  constexpr int BLK_W = 3 * KS * 64 * 8, BLK_U = 2 * KS * 64 * 8;   // elements
+  __shared__ __attribute__((aligned(16))) S lw[2][BLK_W + BLK_U];
+
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int q = lane % 16, g = lane / 16;
+  const int n0 = xcd_swizzle(blockIdx.x, gridDim.x) * 128 + 16 * wave;
+  const bool valid = n0 < n_pad;
+  const int node = n0 + q;
+
+  // Staging of weight block m (rows 16m .. 16m + 15) into buffer b:
+  // pass 1: U columns of gate 2; pass 2: Wi all gates, U gates 0, 1.
+  constexpr int U1 = 16 * (H / V);                 // 16-byte units, pass 1
+  constexpr int U2 = 16 * (3 * H / V) + 16 * (2 * H / V);
+  constexpr int R1 = (U1 + NT - 1) / NT, R2 = (U2 + NT - 1) / NT;
+  u32x4 rr[R2];
+  auto load_blk = [&](int pass, int m) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < R2; ++u) {
+      const int lin = u * NT + tid;
+      if (pass == 1) {
+        if (u < R1 && lin < U1) {
+          const int r = lin / (H / V), c = 2 * H + (lin % (H / V)) * V;
+          rr[u] = *reinterpret_cast<const u32x4*>(U + (size_t)(16 * m + r) * 3 * H + c);
+        }
+      } else if (lin < U2) {
+        const bool isw = lin < 16 * (3 * H / V);
+        const int l2 = isw ? lin : lin - 16 * (3 * H / V);
+        const int per = isw ? 3 * H / V : 2 * H / V;
+        const int r = l2 / per, c = (l2 % per) * V;
+        rr[u] = *reinterpret_cast<const u32x4*>((isw ? Wi : U) + (size_t)(16 * m + r) * 3 * H + c);
+      }
+    }
+  };
+  auto store_blk = [&](int pass, int b) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < R2; ++u) {
+      const int lin = u * NT + tid;
+      const S* pw = reinterpret_cast<const S*>(&rr[u]);
+      if (pass == 1) {
+        if (u < R1 && lin < U1) {
+          const int r = lin / (H / V), c = (lin % (H / V)) * V;   // column within gate 2
+#pragma unroll
+          for (int i = 0; i < V; i += 4) put4<S>(lw[b], (c + i) / 32, r, (c + i) % 32, pw + i);
+        }
+      } else if (lin < U2) {
+        const bool isw = lin < 16 * (3 * H / V);
+        const int l2 = isw ? lin : lin - 16 * (3 * H / V);
+        const int per = isw ? 3 * H / V : 2 * H / V;
+        const int r = l2 / per, c = (l2 % per) * V;              // gate column (0 .. 3H or 2H)
+        S* base = isw ? lw[b] : lw[b] + BLK_W;
+#pragma unroll
+        for (int i = 0; i < V; i += 4)
+          put4<S>(base, ((c + i) / H) * KS + ((c + i) % H) / 32, r, (c + i) % 32, pw + i);
+      }
+    }
+  };
+
+  // Phase 1 (elementwise, registers): n^, z^ as operand fragments, the
+  // g' z term of dh, and G^'s z, n columns.
+  frag_t<S> gf[3][KS];
+  f32x4 dacc[MTL];
+  const S* sv = saved + (size_t)node * 3 * H;
+  S* gh = ghat + (size_t)node * 3 * H;
+  if (valid) {
+    float zv[8], nv[8];
+#pragma unroll
+    for (int m = 0; m < MTL; ++m) {
+      const int f = 16 * m + 4 * g;
+      const f32x4 gg = *reinterpret_cast<const f32x4*>(gin + (size_t)node * H + f);
+      const f32x4 z4 = load4f(sv + H + f), n4 = load4f(sv + 2 * H + f);
+      const f32x4 h4 = load4f(h + (size_t)node * H + f);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float dn = gg[j] * (1.f - z4[j]);
+        const float dz = gg[j] * (h4[j] - n4[j]);
+        dacc[m][j] = gg[j] * z4[j];
+        nv[4 * (m % 2) + j] = dn * (1.f - n4[j] * n4[j]);
+        zv[4 * (m % 2) + j] = dz * z4[j] * (1.f - z4[j]);
+      }
+      if (m % 2 == 1) {
+        gf[2][m / 2] = pack8<S>(nv);
+        gf[1][m / 2] = pack8<S>(zv);
+      }
+      store4(gh + H + f, zv[4 * (m % 2)], zv[4 * (m % 2) + 1], zv[4 * (m % 2) + 2], zv[4 * (m % 2) + 3]);
+      store4(gh + 2 * H + f, nv[4 * (m % 2)], nv[4 * (m % 2) + 1], nv[4 * (m % 2) + 2], nv[4 * (m % 2) + 3]);
+    }
+  }
+
+  // Pass 1: blocks m = 0 .. MTL-1 of U_n (unrolled: static register indices).
+  load_blk(1, 0);
+  float rv[8];
+#pragma unroll
+  for (int m = 0; m < MTL; ++m) {
+    const int b = m & 1;
+    store_blk(1, b);
+    __syncthreads();
+    if (m + 1 < MTL) load_blk(1, m + 1);
+    else load_blk(2, 0);
+    if (valid) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) mma(acc, load_fragi<S>(lw[b], kk, lane), gf[2][kk]);
+      const int f = 16 * m + 4 * g;
+      const f32x4 r4 = load4f(sv + f), h4 = load4f(h + (size_t)node * H + f);
+      float rloc[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        rloc[j] = acc[j] * h4[j] * r4[j] * (1.f - r4[j]);
+        dacc[m][j] += acc[j] * r4[j];
+      }
+      store4(gh + f, rloc[0], rloc[1], rloc[2], rloc[3]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) rv[4 * (m % 2) + j] = rloc[j];
+      if (m % 2 == 1) gf[0][m / 2] = pack8<S>(rv);
+    }
+  }
+  // Pass 2: blocks n = 0 .. MTL-1 of Wi (da) and U_r, U_z (dh).
+#pragma unroll
+  for (int n = 0; n < MTL; ++n) {
+    const int b = (MTL + n) & 1;
+    store_blk(2, b);
+    __syncthreads();
+    if (n + 1 < MTL) load_blk(2, n + 1);
+    if (valid) {
+      f32x4 da = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int gate = 0; gate < 3; ++gate)
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) mma(da, gf[gate][kk], load_fragi<S>(lw[b], gate * KS + kk, lane));
+      store4(daT + (size_t)(16 * n + q) * n_pad + n0 + 4 * g, da[0], da[1], da[2], da[3]);
+      f32x4 d = dacc[n];
+#pragma unroll
+      for (int gate = 0; gate < 2; ++gate)
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) mma(d, load_fragi<S>(lw[b] + BLK_W, gate * KS + kk, lane), gf[gate][kk]);
+      store4(dh + (size_t)node * H + 16 * n + 4 * g, d[0], d[1], d[2], d[3]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Weight gradients of the GRU over one split of the rows k:
 //   P[split][0][i][c] = sum_k a[k][i] G^[k][c]          (dWi)
 //   P[split][1][i][c] = sum_k x_c[k][i] G^[k][c]        (dU)
@@ -429,6 +591,12 @@ hipError_t gru_fwd_h(int n_pad, const float* a, const void* h, const void* Wi, c
 template <typename S, int H>
 hipError_t gru_bwd_nodes_h(int n_pad, const float* dh_out, const void* h, const void* saved, const void* Wi,
                            const void* U, void* da, float* dh, void* ghat, hipStream_t st) {
+  if constexpr (sizeof(S) == 2 && H >= 128) {
+    hipLaunchKernelGGL((dev::gru_bwd_big_kernel<S, H>), dim3((n_pad + 127) / 128), dim3(512), 0, st, dh_out,
+                       static_cast<const S*>(h), static_cast<const S*>(saved), static_cast<const S*>(Wi),
+                       static_cast<const S*>(U), static_cast<S*>(da), dh, static_cast<S*>(ghat), n_pad);
+    return hipGetLastError();
+  }
   constexpr int WAVES = 4;
   hipLaunchKernelGGL((dev::gru_bwd_kernel<S, H, WAVES>), dim3((n_pad + 16 * WAVES - 1) / (16 * WAVES)),
                      dim3(WAVES * 64), 0, st, dh_out, static_cast<const S*>(h), static_cast<const S*>(saved),
