@@ -211,6 +211,154 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
 }
 
 // ---------------------------------------------------------------------------
+// Forward for large H (bf16, H >= 128), the arithmetic of gru_fwd_kernel
+// with the weights shared through LDS: a workgroup of 8 waves (16 nodes
+// each) streams Wi and U once per 128 nodes, one 16-column gate tile at a
+// time, transposed into fragment order (8 x 8 register tiles) and double
+// buffered.  Pass 1 (tiles of the r gate) forms r and keeps r*h as operand
+// fragments; pass 2 (tiles of z and n) finishes the state.
+// ---------------------------------------------------------------------------
+template <typename S, int H>
+__global__ __launch_bounds__(512) void gru_fwd_big_kernel(const float* __restrict__ a, const S* __restrict__ h,
+                                                          const S* __restrict__ Wi, const S* __restrict__ U,
+                                                          const float* __restrict__ b, S* __restrict__ h_out,
+                                                          S* __restrict__ saved, int n_pad) {
+  static_assert(sizeof(S) == 2, "bf16 only");
+  constexpr int NT = 512, V = 8;
+  constexpr int KS = H / 32, NC = H / 16;
+  constexpr int FR = KS * 64 * 8;                  // elements of one (matrix, 16-column tile) block
+  __shared__ __attribute__((aligned(16))) S lw[2][4 * FR];   // up to four blocks per stage
+
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int q = lane % 16, g = lane / 16;
+  const int n0 = xcd_swizzle(blockIdx.x, gridDim.x) * 128 + 16 * wave;
+  const bool valid = n0 < n_pad;
+  const int node = n0 + q;
+
+  // Stage s of 2 NC: s < NC is pass 1, tile s (Wi, U columns of gate r);
+  // s >= NC is pass 2, tile s - NC (Wi, U columns of gates z and n).  A
+  // block is 16 columns x H rows of one matrix; an 8 x 8 tile (8 input
+  // rows, 8 columns) per unit.
+  constexpr int TPB = (H / V) * 2;                 // 8 x 8 tiles per block
+  constexpr int RMAX = (4 * TPB + NT - 1) / NT;
+  u32x4 rr[RMAX][V];
+  auto block_src = [&](int s, int blk, int& col) __attribute__((always_inline)) {
+    // blk: pass 1 {Wi_r, U_r}, pass 2 {Wi_z, U_z, Wi_n, U_n}
+    const int t16 = s < NC ? s : s - NC;
+    const int gate = s < NC ? 0 : 1 + blk / 2;
+    col = gate * H + 16 * t16;
+    return (blk % 2) ? U : Wi;
+  };
+  auto load_stage = [&](int s) __attribute__((always_inline)) {
+    const int nblk = s < NC ? 2 : 4;
+#pragma unroll
+    for (int u = 0; u < RMAX; ++u) {
+      const int lin = u * NT + tid;
+      if (lin < nblk * TPB) {
+        const int blk = lin / TPB, rem = lin % TPB;
+        const int hq = rem / 2, cq = rem % 2;
+        int col;
+        const S* src = block_src(s, blk, col);
+        tile_load<S>(rr[u], src + (size_t)(V * hq) * 3 * H + col + V * cq, 3 * H);
+      }
+    }
+  };
+  auto store_stage = [&](int s, int bf) __attribute__((always_inline)) {
+    const int nblk = s < NC ? 2 : 4;
+#pragma unroll
+    for (int u = 0; u < RMAX; ++u) {
+      const int lin = u * NT + tid;
+      if (lin < nblk * TPB) {
+        const int blk = lin / TPB, rem = lin % TPB;
+        const int hq = rem / 2, cq = rem % 2;
+#pragma unroll
+        for (int x = 0; x < V; ++x) {
+          // row x of the transposed tile: column 8cq + x of the block,
+          // input rows 8hq .. 8hq + 7
+          const u32x4 o = tile_row_T<S>(rr[u], x);
+          const S* po = reinterpret_cast<const S*>(&o);
+#pragma unroll
+          for (int i = 0; i < V; i += 4)
+            put4<S>(lw[bf] + blk * FR, (V * hq + i) / 32, V * cq + x, (V * hq + i) % 32, po + i);
+        }
+      }
+    }
+  };
+
+  // Operand fragments of the 16 nodes (accumulator-compatible k order):
+  // a as hi + lo, h, and later r*h.
+  frag_t<S> af[2][KS], hf[KS], rh[KS];
+  if (valid) {
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const float* row = a + (size_t)node * H;
+      const f32x4 x = *reinterpret_cast<const f32x4*>(row + 32 * kk + 4 * g);
+      const f32x4 y = *reinterpret_cast<const f32x4*>(row + 32 * kk + 16 + 4 * g);
+      const float v[8] = {x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
+      split8(v, af[0][kk], af[1][kk]);
+      hf[kk] = rowfrag<S>(h + (size_t)node * H, kk, g);
+    }
+  }
+  float rhv[8];
+  load_stage(0);
+#pragma unroll
+  for (int s = 0; s < 2 * NC; ++s) {
+    const int bf = s & 1;
+    store_stage(s, bf);
+    __syncthreads();
+    if (s + 1 < 2 * NC) load_stage(s + 1);
+    if (!valid) continue;
+    const S* L = lw[bf];
+    if (s < NC) {
+      f32x4 ar = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        const frag_t<S> w0 = load_fragi<S>(L, kk, lane);
+        mma(ar, w0, af[0][kk]);
+        mma(ar, w0, af[1][kk]);
+        mma(ar, load_fragi<S>(L + FR, kk, lane), hf[kk]);
+      }
+      const int f = 16 * s + 4 * g;
+      float r[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        r[j] = sigmoidf_(ar[j] + b[f + j]);
+        rhv[4 * (s % 2) + j] = r[j] * static_cast<float>(hf[s / 2][4 * (s % 2) + j]);
+      }
+      if (saved) store4(saved + (size_t)node * 3 * H + f, r[0], r[1], r[2], r[3]);
+      if (s % 2 == 1) rh[s / 2] = pack8<S>(rhv);
+    } else {
+      const int t16 = s - NC;
+      f32x4 az = {0.f, 0.f, 0.f, 0.f}, an = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        const frag_t<S> wz = load_fragi<S>(L, kk, lane), wn = load_fragi<S>(L + 2 * FR, kk, lane);
+        mma(az, wz, af[0][kk]);
+        mma(az, wz, af[1][kk]);
+        mma(an, wn, af[0][kk]);
+        mma(an, wn, af[1][kk]);
+        mma(az, load_fragi<S>(L + FR, kk, lane), hf[kk]);
+        mma(an, load_fragi<S>(L + 3 * FR, kk, lane), rh[kk]);
+      }
+      const int f = 16 * t16 + 4 * g;
+      float z[4], nn[4], o[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        z[j] = sigmoidf_(az[j] + b[H + f + j]);
+        nn[j] = tanhf_(an[j] + b[2 * H + f + j]);
+        const float hv = static_cast<float>(hf[t16 / 2][4 * (t16 % 2) + j]);
+        o[j] = z[j] * hv + (1.f - z[j]) * nn[j];
+      }
+      store4(h_out + (size_t)node * H + f, o[0], o[1], o[2], o[3]);
+      if (saved) {
+        store4(saved + (size_t)node * 3 * H + H + f, z[0], z[1], z[2], z[3]);
+        store4(saved + (size_t)node * 3 * H + 2 * H + f, nn[0], nn[1], nn[2], nn[3]);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Backward for large H (bf16, H >= 128), the same arithmetic as
 // gru_bwd_wave, with the weights shared through LDS: a workgroup of 8 waves
 // (16 nodes each) streams the weights once per 128 nodes, in blocks of 16
@@ -581,6 +729,12 @@ Split gru_split(long K, int H) {
 template <typename S, int H>
 hipError_t gru_fwd_h(int n_pad, const float* a, const void* h, const void* Wi, const void* U, const float* b,
                      void* h_out, void* saved, hipStream_t st) {
+  if constexpr (sizeof(S) == 2 && H >= 128) {
+    hipLaunchKernelGGL((dev::gru_fwd_big_kernel<S, H>), dim3((n_pad + 127) / 128), dim3(512), 0, st, a,
+                       static_cast<const S*>(h), static_cast<const S*>(Wi), static_cast<const S*>(U), b,
+                       static_cast<S*>(h_out), static_cast<S*>(saved), n_pad);
+    return hipGetLastError();
+  }
   constexpr int WAVES = 4;
   hipLaunchKernelGGL((dev::gru_fwd_kernel<S, H, WAVES>), dim3((n_pad + 16 * WAVES - 1) / (16 * WAVES)),
                      dim3(WAVES * 64), 0, st, a, static_cast<const S*>(h), static_cast<const S*>(Wi),
