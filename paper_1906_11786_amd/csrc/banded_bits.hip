@@ -947,6 +947,12 @@ hipError_t bits_launch(const BitsArgs& A, hipStream_t st) {
   const int nb = A.n_pad / B;
   const bool fused = A.mode != 2;
   int waves = B / C::RPW < 4 ? B / C::RPW : 4;
+  // Streamed blocks at H = 256, forward: eight waves (128 rows) share each
+  // staged chunk, halving the staging per row (the reverse step's
+  // eight-wave form would spill registers).
+  if constexpr (!C::ALL && H >= 256) {
+    if (A.mode == 0) waves = B / C::RPW < 8 ? B / C::RPW : 8;
+  }
   const long min_blocks = fused ? GGNN_BITS_FWD_MIN_BLOCKS : GGNN_BITS_BWD_MIN_BLOCKS;
   while (waves > C::MINW && (long)nb * (B / (C::RPW * waves)) < min_blocks) waves /= 2;
   const int tiles = nb * (B / (C::RPW * waves));
@@ -981,25 +987,30 @@ hipError_t bits_launch(const BitsArgs& A, hipStream_t st) {
                      static_cast<S*>(A.rh_da), A.rh_dh, static_cast<S*>(A.rh_ghat))
 #define GGNN_BITS_CASE(WV)                                                                                   \
   case WV:                                                                                                   \
-    if constexpr (B / C::RPW >= WV && WV >= C::MINW) {                                                       \
+    if constexpr (B / C::RPW >= WV && WV >= C::MINW && (WV <= 4 || (!C::ALL && H >= 256))) {         \
       if (A.mode == 0 && gru)                                                                                \
         GGNN_STEP(WV, (C::WDIR ? 2 : 1), false, C::WDIR);                                                    \
       else if (A.mode == 0 && tg2)                                                                           \
         GGNN_STEP(WV, (C::WDIR ? 2 : 1), false, false);                                                      \
       else if (A.mode == 0)                                                                                  \
         GGNN_STEP(WV, 1, false, false);                                                                      \
-      else if (A.mode == 1 && rgru)                                                                          \
-        GGNN_STEP(WV, (C::WDIR ? 2 : 1), true, C::WDIR);                                                     \
-      else if (A.mode == 1 && tg2)                                                                           \
-        GGNN_STEP(WV, (C::WDIR ? 2 : 1), true, false);                                                       \
-      else if (A.mode == 1)                                                                                  \
-        GGNN_STEP(WV, 1, true, false);                                                                       \
-      else                                                                                                   \
-        hipLaunchKernelGGL((dev::bits_bwd_kernel<S, H, B, WV>), dim3(blocks), dim3(WV * 64), 0, st, bp, vp,  \
-                           static_cast<S*>(A.out), A.n_pad, A.E, groups, A.ldm);                             \
+      else {                                                                                                 \
+        if constexpr (WV <= 4) { /* eight-wave forms: forward only */                                       \
+          if (A.mode == 1 && rgru)                                                                           \
+            GGNN_STEP(WV, (C::WDIR ? 2 : 1), true, C::WDIR);                                                 \
+          else if (A.mode == 1 && tg2)                                                                       \
+            GGNN_STEP(WV, (C::WDIR ? 2 : 1), true, false);                                                   \
+          else if (A.mode == 1)                                                                              \
+            GGNN_STEP(WV, 1, true, false);                                                                   \
+          else                                                                                               \
+            hipLaunchKernelGGL((dev::bits_bwd_kernel<S, H, B, WV>), dim3(blocks), dim3(WV * 64), 0, st, bp,  \
+                               vp, static_cast<S*>(A.out), A.n_pad, A.E, groups, A.ldm);                     \
+        }                                                                                                    \
+      }                                                                                                      \
     }                                                                                                        \
     break;
   switch (waves) {
+    GGNN_BITS_CASE(8)
     GGNN_BITS_CASE(4)
     GGNN_BITS_CASE(2)
     GGNN_BITS_CASE(1)
