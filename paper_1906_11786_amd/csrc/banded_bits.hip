@@ -98,6 +98,19 @@ template <typename S, int H>
 __device__ __forceinline__ frag_t<S> load_frag(const S* v, int kk, int m, int lane) {
   return load_fragi<S>(v, kk * (H / 16) + m, lane);
 }
+
+// Reverse step: the da window is staged with its features permuted so that
+// tile m, row i of the aggregation holds feature
+//   32 (m / 2) + 8 (i / 4) + 4 (m % 2) + i % 4.
+// A lane's accumulators of tiles 2kk and 2kk + 1 then hold eight
+// consecutive features, 32kk + 8g .. 32kk + 8g + 7, of its node: dM_e is
+// stored with one 16-byte write per pair of tiles, and the transform reads
+// eight consecutive elements of a row of W_e per fragment.  rev_row(h) is
+// the (tile, row) slot of feature h, as 16 * tile + row.
+__device__ __forceinline__ int rev_row(int h) {
+  const int w = h % 32;
+  return 16 * (2 * (h / 32) + (w % 8) / 4) + 4 * (w / 8) + w % 4;
+}
 // Staging of a chunk of KC nodes x H features for the streamed (large-H)
 // forms, in one of two LDS layouts: fragment order (frag_off) or feature
 // rows dst[h * VP + c].  The fragment order makes every fragment read a
@@ -139,13 +152,15 @@ __device__ __forceinline__ void stage_nodes_T(S* dst, const S* src, int n0, int 
 // copies: a unit is one fragment vector).  In fragment order the feature
 // runs fastest over the threads, so the 16 lanes of one LDS pass write 16
 // different fragment rows (distinct banks).
-template <typename S, int H, int KC, int VP, int NT, bool ROWS>
+// PERM: feature h goes to the (tile, row) slot rev_row(h) (reverse step).
+template <typename S, int H, int KC, int VP, int NT, bool ROWS, bool PERM>
 __device__ __forceinline__ void stage_cols(S* dst, const S* src, int n_pad, int n0, int tid) {
   constexpr int V = 16 / sizeof(S);
   for (int lin = tid; lin < H * (KC / V); lin += NT) {
     const int h = ROWS ? lin / (KC / V) : lin % H;
     const int c = ROWS ? (lin % (KC / V)) * V : (lin / H) * V;
-    *reinterpret_cast<u32x4*>(&dst[ROWS ? h * VP + c : frag_off<S, H, KC>(h, c)]) =
+    const int hs = PERM ? rev_row(h) : h;
+    *reinterpret_cast<u32x4*>(&dst[ROWS ? hs * VP + c : frag_off<S, H, KC>(hs, c)]) =
         *reinterpret_cast<const u32x4*>(src + (size_t)h * n_pad + n0 + c);
   }
 }
@@ -352,7 +367,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
           if (lin < nx) {
             const int slot = s_lo + lin / UPB, rem = lin % UPB;
             const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
-            *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(h, c)]) = r[u];
+            *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(rev_row(h), c)]) = r[u];
           } else if (lin < total) {
             const int w = lin - nx, m = w / UPW, rem = w % UPW;
             const int h = rem / (3 * H / V), c = (rem % (3 * H / V)) * V;
@@ -388,8 +403,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
 #pragma unroll
         for (int kk = 0; kk < HK; ++kk) {
           if constexpr (REV) {
-            const S* p = we + (size_t)(16 * mo + q) * H + 32 * kk + 4 * g;
-            wf[mo][kk] = load4x2(p, p + 16);
+            wf[mo][kk] = load8(we + (size_t)(16 * mo + q) * H + 32 * kk + 8 * g);   // features 32kk + 8g + 0..7
           } else {
             const S* p = we + (size_t)(32 * kk + 4 * g) * H + 16 * mo + q;
             if constexpr (sizeof(S) == 2) {
@@ -485,7 +499,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         if constexpr (!C::ALL) {
           __syncthreads();
           if constexpr (REV) {
-            stage_cols<S, H, KC, VP, NT, C::ROWS>(vt[0], X, n_pad, (k - 1 + s) * B + c0, tid);
+            stage_cols<S, H, KC, VP, NT, C::ROWS, true>(vt[0], X, n_pad, (k - 1 + s) * B + c0, tid);
           } else {
             stage_nodes_T<S, H, KC, VP, NT, C::ROWS>(vt[0], X, (k - 1 + s) * B + c0, tid);
           }
@@ -537,20 +551,18 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
       }
     if constexpr (REV) {
       // dM_e rows of this wave's nodes (node-major, rows of type e start at
-      // row e * ldm): features 32kk + 4g + {0..3} and 32kk + 16 + 4g + {0..3}.
+      // row e * ldm): features 32kk + 8g .. 32kk + 8g + 7 (rev_row order).
 #pragma unroll
       for (int n = 0; n < NTW; ++n) {
         S* row = dM + ((size_t)e * ldm + k * B + rw + 16 * n + q) * H + 4 * g;
 #pragma unroll
         for (int kk = 0; kk < HK; ++kk) {
           if constexpr (sizeof(S) == 2) {
-            const u32x4 w = __builtin_bit_cast(u32x4, pf[0][n][kk]);
-            *reinterpret_cast<u32x2*>(row + 32 * kk) = u32x2{w[0], w[1]};
-            *reinterpret_cast<u32x2*>(row + 32 * kk + 16) = u32x2{w[2], w[3]};
+            *reinterpret_cast<u32x4*>(row + 32 * kk + 4 * g) = __builtin_bit_cast(u32x4, pf[0][n][kk]);
           } else {
             const f32x8 w = pf[0][n][kk];
-            *reinterpret_cast<f32x4*>(row + 32 * kk) = f32x4{w[0], w[1], w[2], w[3]};
-            *reinterpret_cast<f32x4*>(row + 32 * kk + 16) = f32x4{w[4], w[5], w[6], w[7]};
+            *reinterpret_cast<f32x4*>(row + 32 * kk + 4 * g) = f32x4{w[0], w[1], w[2], w[3]};
+            *reinterpret_cast<f32x4*>(row + 32 * kk + 4 * g + 4) = f32x4{w[4], w[5], w[6], w[7]};
           }
         }
       }
@@ -574,8 +586,8 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         for (int mo = 0; mo < WC / 16; ++mo)
 #pragma unroll
           for (int kk = 0; kk < HK; ++kk) {
-            const S* wr = &wt[(16 * mo + q) * WP + 32 * kk + 4 * g];
-            const frag_t<S> af = load4x2(wr, wr + 16);
+            const S* wr = &wt[(16 * mo + q) * WP + 32 * kk + (REV ? 8 : 4) * g];
+            const frag_t<S> af = REV ? load8(wr) : load4x2(wr, wr + 16);
 #pragma unroll
             for (int n = 0; n < NTW; ++n)
 #pragma unroll
@@ -859,7 +871,7 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
       for (int c0 = 0; c0 < B; c0 += KC) {
         if constexpr (!C::ALL) {
           __syncthreads();
-          stage_cols<S, H, KC, VP, NT, C::ROWS>(vt[0], da, n_pad, (j - 1 + s) * B + c0, tid);
+          stage_cols<S, H, KC, VP, NT, C::ROWS, false>(vt[0], da, n_pad, (j - 1 + s) * B + c0, tid);
           __syncthreads();
         }
         const S* v = vt[C::ALL ? s : 0];
