@@ -312,7 +312,7 @@ def main():
         dh_prev = torch.empty_like(m.dh)
         ghat = torch.empty((n_pad, 3 * H), dtype=td, device="cuda")
         fns = {"step_bits_gru": lambda: capi.ggnn_step_bits_gru(spec.dtype, n_pad, B, H, E, m.band, m.X[0], m.W,
-                                                                m.bias, m.Wi, m.U, m.b, m.a[0], m.X[1],
+                                                                m.Wt, m.bias, m.Wi, m.U, m.b, m.a[0], m.X[1],
                                                                 m.saved[0]),
                "step_bits_gru_bwd": lambda: capi.ggnn_step_bits_gru_bwd(
                    spec.dtype, n_pad, B, H, E, m.band_t, m.da, m.W, m.dh, m.dM, spec.T * n_pad, m.Wi, m.U,

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define GGNN_ABI_VERSION 5
+#define GGNN_ABI_VERSION 6
 
 typedef enum {
   GGNN_OK = 0,
@@ -235,11 +235,17 @@ ggnn_status ggnn_banded_step_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, i
  * those two calls:
  *   a      [n_pad][H] float (written: the aggregate, kept for the reverse pass)
  *   h_out  [n_pad][H] dt (written: the next state);  saved [n_pad][3H] dt (r | z | n)
- * Wi, U [H][3H] dt; b [3H] float.  X and h_out must not overlap. */
+ * Wi, U [H][3H] dt; b [3H] float.  X and h_out must not overlap.  Wt: W_e^T (ggnn_transpose_weights)
+ * or NULL; the result does not depend on it. */
 ggnn_status ggnn_step_bits_gru(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
-                               const void* bits, const void* X, const void* W, const float* bias,
-                               const void* Wi, const void* U, const float* b, float* a, void* h_out,
-                               void* saved, void* stream);
+                               const void* bits, const void* X, const void* W, const void* Wt,
+                               const float* bias, const void* Wi, const void* U, const float* b, float* a,
+                               void* h_out, void* saved, void* stream);
+
+/* W_e^T for every edge type: Wt[e][o][h] = W[e][h][o] (both [E][H][H] dt, 16-byte aligned, not
+ * overlapping).  The transposed weights are an optional operand of the forward steps (Wt of
+ * ggnn_step_bits_gru and of ggnn_model). */
+ggnn_status ggnn_transpose_weights(ggnn_dtype dt, int32_t H, int32_t E, const void* W, void* Wt, void* stream);
 
 /* One reverse step on a 1-bit band, the form ggnn_backward runs for t > 0:
  * the reverse of step t's propagation (ggnn_banded_step_bits_bwd: dM_e =
@@ -314,6 +320,9 @@ typedef struct ggnn_model {
   const float* b;       /* [3H] */
   int32_t band_format;  /* ggnn_band_format */
   const void* band_t;   /* bits: the transposed bit band (bits_t); dense: unused */
+  const void* Wt;       /* [E][H][H] dt, W_e^T (Wt[e][o][h] = W[e][h][o], ggnn_transpose_weights), or NULL.
+                           Optional: lets the bit-band forward read its weight fragments as rows; the
+                           caller refreshes it whenever W changes. */
 } ggnn_model;
 
 typedef struct ggnn_activations {

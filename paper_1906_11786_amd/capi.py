@@ -30,7 +30,7 @@ EXPORTS = [
     "ggnn_abi_version", "ggnn_last_error", "ggnn_status_string",
     "ggnn_rcm_order", "ggnn_bandwidth", "ggnn_band_bytes", "ggnn_banded_pack",
     "ggnn_band_bits_bytes", "ggnn_banded_pack_bits", "ggnn_banded_step_bits", "ggnn_banded_propagate_bits_bwd",
-    "ggnn_banded_step_bits_bwd", "ggnn_step_bits_gru", "ggnn_step_bits_gru_bwd",
+    "ggnn_banded_step_bits_bwd", "ggnn_step_bits_gru", "ggnn_step_bits_gru_bwd", "ggnn_transpose_weights",
     "ggnn_msg_transform", "ggnn_banded_propagate", "ggnn_gru_update",
     "ggnn_gru_update_bwd_workspace_bytes", "ggnn_gru_update_bwd",
     "ggnn_banded_propagate_bwd", "ggnn_msg_transform_bwd_workspace_bytes", "ggnn_msg_transform_bwd",
@@ -49,7 +49,7 @@ class ggnn_model(C.Structure):
     _fields_ = [("dtype", C.c_int32), ("n_pad", C.c_int32), ("B", C.c_int32), ("H", C.c_int32),
                 ("E", C.c_int32), ("T", C.c_int32), ("band", C.c_void_p), ("W", C.c_void_p),
                 ("bias", C.c_void_p), ("Wi", C.c_void_p), ("U", C.c_void_p), ("b", C.c_void_p),
-                ("band_format", C.c_int32), ("band_t", C.c_void_p)]
+                ("band_format", C.c_int32), ("band_t", C.c_void_p), ("Wt", C.c_void_p)]
 
 
 class ggnn_activations(C.Structure):
@@ -80,7 +80,8 @@ _SIGS = {
     "ggnn_banded_step_bits": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]),
     "ggnn_banded_propagate_bits_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp]),
     "ggnn_banded_step_bits_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i64, vp]),
-    "ggnn_step_bits_gru": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+    "ggnn_step_bits_gru": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+    "ggnn_transpose_weights": (C.c_int, [C.c_int, i32, i32, vp, vp, vp]),
     "ggnn_step_bits_gru_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp,
                                          vp, vp, vp]),
     "ggnn_msg_transform": (C.c_int, [C.c_int, i32, i32, i32, vp, vp, vp, vp, vp]),
@@ -238,10 +239,15 @@ def ggnn_banded_step_bits_bwd(dt, n_pad, B, H, E, bits_t, da, W, dX_in, dX_out, 
         _stream(stream)))
 
 
-def ggnn_step_bits_gru(dt, n_pad, B, H, E, bits, X, W, bias, Wi, U, b, a, h_out, saved, stream=None):
+def ggnn_step_bits_gru(dt, n_pad, B, H, E, bits, X, W, Wt, bias, Wi, U, b, a, h_out, saved, stream=None):
     _check("ggnn_step_bits_gru", lib().ggnn_step_bits_gru(
-        _dt(dt), n_pad, B, H, E, _ptr(bits), _ptr(X), _ptr(W), _ptr(bias), _ptr(Wi), _ptr(U), _ptr(b), _ptr(a),
-        _ptr(h_out), _ptr(saved), _stream(stream)))
+        _dt(dt), n_pad, B, H, E, _ptr(bits), _ptr(X), _ptr(W), _ptr(Wt), _ptr(bias), _ptr(Wi), _ptr(U), _ptr(b),
+        _ptr(a), _ptr(h_out), _ptr(saved), _stream(stream)))
+
+
+def ggnn_transpose_weights(dt, H, E, W, Wt, stream=None):
+    _check("ggnn_transpose_weights", lib().ggnn_transpose_weights(_dt(dt), H, E, _ptr(W), _ptr(Wt),
+                                                                    _stream(stream)))
 
 
 def ggnn_step_bits_gru_bwd(dt, n_pad, B, H, E, bits_t, da, W, dX_in, dM, ldm, Wi, U, h_prev, saved_prev, da_prev,

@@ -99,15 +99,17 @@ __device__ __forceinline__ frag_t<S> load_frag(const S* v, int kk, int m, int la
   return load_fragi<S>(v, kk * (H / 16) + m, lane);
 }
 
-// Reverse step: the da window is staged with its features permuted so that
-// tile m, row i of the aggregation holds feature
+// Fused steps: the staged window (X forward, da reverse) has its features
+// permuted so that tile m, row i of the aggregation holds feature
 //   32 (m / 2) + 8 (i / 4) + 4 (m % 2) + i % 4.
 // A lane's accumulators of tiles 2kk and 2kk + 1 then hold eight
-// consecutive features, 32kk + 8g .. 32kk + 8g + 7, of its node: dM_e is
-// stored with one 16-byte write per pair of tiles, and the transform reads
-// eight consecutive elements of a row of W_e per fragment.  rev_row(h) is
-// the (tile, row) slot of feature h, as 16 * tile + row.
-__device__ __forceinline__ int rev_row(int h) {
+// consecutive features, 32kk + 8g .. 32kk + 8g + 7, of its node, so the
+// aggregate enters the transform as fragments whose weight operand is eight
+// consecutive elements of a row of W_e (reverse) or of W_e^T (forward, when
+// the transposed weights are given), one 16-byte load, and the reverse
+// stores dM_e with one 16-byte write per pair of tiles.  perm_row(h) is the
+// (tile, row) slot of feature h, as 16 * tile + row.
+__device__ __forceinline__ int perm_row(int h) {
   const int w = h % 32;
   return 16 * (2 * (h / 32) + (w % 8) / 4) + 4 * (w / 8) + w % 4;
 }
@@ -124,8 +126,8 @@ __device__ __forceinline__ int rev_row(int h) {
 template <typename S, int H, int KC, int VP, int NT, bool ROWS>
 __device__ __forceinline__ void stage_nodes_T(S* dst, const S* src, int n0, int tid) {
   constexpr int PAIRS = KC / 2;
-  auto at = [&](int h, int c) __attribute__((always_inline)) {
-    return ROWS ? h * VP + c : frag_off<S, H, KC>(h, c);
+  auto at = [&](int h, int c) __attribute__((always_inline)) {   // feature h goes to slot perm_row(h)
+    return ROWS ? perm_row(h) * VP + c : frag_off<S, H, KC>(perm_row(h), c);
   };
   for (int lin = tid; lin < PAIRS * (H / 8); lin += NT) {
     const int cp = lin % PAIRS, f0 = (lin / PAIRS) * 8;
@@ -152,14 +154,14 @@ __device__ __forceinline__ void stage_nodes_T(S* dst, const S* src, int n0, int 
 // copies: a unit is one fragment vector).  In fragment order the feature
 // runs fastest over the threads, so the 16 lanes of one LDS pass write 16
 // different fragment rows (distinct banks).
-// PERM: feature h goes to the (tile, row) slot rev_row(h) (reverse step).
+// PERM: feature h goes to the (tile, row) slot perm_row(h) (reverse step).
 template <typename S, int H, int KC, int VP, int NT, bool ROWS, bool PERM>
 __device__ __forceinline__ void stage_cols(S* dst, const S* src, int n_pad, int n0, int tid) {
   constexpr int V = 16 / sizeof(S);
   for (int lin = tid; lin < H * (KC / V); lin += NT) {
     const int h = ROWS ? lin / (KC / V) : lin % H;
     const int c = ROWS ? (lin % (KC / V)) * V : (lin / H) * V;
-    const int hs = PERM ? rev_row(h) : h;
+    const int hs = PERM ? perm_row(h) : h;
     *reinterpret_cast<u32x4*>(&dst[ROWS ? hs * VP + c : frag_off<S, H, KC>(hs, c)]) =
         *reinterpret_cast<const u32x4*>(src + (size_t)h * n_pad + n0 + c);
   }
@@ -230,7 +232,8 @@ struct BitsCfg {
 // ---------------------------------------------------------------------------
 template <typename S, int H, int B, int WAVES, bool WDIR, int TG, bool REV, bool GRU>
 __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
-    const uint8_t* __restrict__ bits, const S* __restrict__ X, const S* __restrict__ W, const float* __restrict__ bias,
+    const uint8_t* __restrict__ bits, const S* __restrict__ X, const S* __restrict__ W, const S* __restrict__ Wt,
+    const float* __restrict__ bias,
     float* out, int n_pad, int E, const float* dX_in, S* __restrict__ dM, long ldm, const S* __restrict__ Wi,
     const S* __restrict__ U, const float* __restrict__ bg, S* __restrict__ h_out, S* __restrict__ saved,
     const S* __restrict__ rh_h, const S* __restrict__ rh_saved, S* __restrict__ rh_da, float* __restrict__ rh_dh,
@@ -321,7 +324,8 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
             const int cq = rem % (KC / V), fq = rem / (KC / V);
 #pragma unroll
             for (int x = 0; x < V; ++x)
-              *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(V * fq + x, V * cq)]) = tile_row_T<S>(r[u], x);
+              *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(perm_row(V * fq + x), V * cq)]) =
+                  tile_row_T<S>(r[u], x);
           } else if (lin < total) {
             const int w = lin - nx, m = w / GT, rem = w % GT;
             const int hq = rem % (H / V), cq = rem / (H / V);
@@ -367,7 +371,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
           if (lin < nx) {
             const int slot = s_lo + lin / UPB, rem = lin % UPB;
             const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
-            *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(rev_row(h), c)]) = r[u];
+            *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(perm_row(h), c)]) = r[u];
           } else if (lin < total) {
             const int w = lin - nx, m = w / UPW, rem = w % UPW;
             const int h = rem / (3 * H / V), c = (rem % (3 * H / V)) * V;
@@ -404,20 +408,22 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         for (int kk = 0; kk < HK; ++kk) {
           if constexpr (REV) {
             wf[mo][kk] = load8(we + (size_t)(16 * mo + q) * H + 32 * kk + 8 * g);   // features 32kk + 8g + 0..7
+          } else if (Wt != nullptr) {
+            // W_e^T row 16mo + q: features 32kk + 8g + 0..7
+            wf[mo][kk] = load8(Wt + (size_t)e * H * H + (size_t)(16 * mo + q) * H + 32 * kk + 8 * g);
           } else {
-            const S* p = we + (size_t)(32 * kk + 4 * g) * H + 16 * mo + q;
+            // column 16mo + q of W_e, rows 32kk + 8g + 0..7 (2-byte gathers)
+            const S* p = we + (size_t)(32 * kk + 8 * g) * H + 16 * mo + q;
             if constexpr (sizeof(S) == 2) {
               u32x4 w;
 #pragma unroll
-              for (int d = 0; d < 4; ++d) {
-                const int h0 = (d < 2 ? 0 : 16) + 2 * (d % 2);
-                w[d] = static_cast<uint32_t>(p[(size_t)h0 * H]) |
-                       (static_cast<uint32_t>(p[(size_t)(h0 + 1) * H]) << 16);
-              }
+              for (int d = 0; d < 4; ++d)
+                w[d] = static_cast<uint32_t>(p[(size_t)(2 * d) * H]) |
+                       (static_cast<uint32_t>(p[(size_t)(2 * d + 1) * H]) << 16);
               wf[mo][kk] = __builtin_bit_cast(bf16x8, w);
             } else {
 #pragma unroll
-              for (int x = 0; x < 8; ++x) wf[mo][kk][x] = p[(size_t)((x < 4 ? 0 : 16) + x % 4) * H];
+              for (int x = 0; x < 8; ++x) wf[mo][kk][x] = p[(size_t)x * H];
             }
           }
         }
@@ -586,8 +592,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         for (int mo = 0; mo < WC / 16; ++mo)
 #pragma unroll
           for (int kk = 0; kk < HK; ++kk) {
-            const S* wr = &wt[(16 * mo + q) * WP + 32 * kk + (REV ? 8 : 4) * g];
-            const frag_t<S> af = REV ? load8(wr) : load4x2(wr, wr + 16);
+            const frag_t<S> af = load8(&wt[(16 * mo + q) * WP + 32 * kk + 8 * g]);
 #pragma unroll
             for (int n = 0; n < NTW; ++n)
 #pragma unroll
@@ -908,6 +913,23 @@ __global__ __launch_bounds__(WAVES * kWave) void bits_bwd_kernel(const uint8_t* 
   }
 }
 
+// W_e^T from W_e for every edge type: Wt[e][o][h] = W[e][h][o], 8 x 8 tiles
+// transposed in registers (16-byte loads and stores).
+template <typename S>
+__global__ void transpose_weights_kernel(const S* __restrict__ W, S* __restrict__ Wt, int H, int E) {
+  constexpr int V = 16 / sizeof(S);
+  const int tiles = (H / V) * (H / V);
+  const long lin = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (lin >= (long)E * tiles) return;
+  const int e = (int)(lin / tiles), rem = (int)(lin % tiles);
+  const int hq = rem / (H / V), oq = rem % (H / V);
+  u32x4 r[V];
+  tile_load<S>(r, W + (size_t)e * H * H + (size_t)(V * hq) * H + V * oq, H);
+#pragma unroll
+  for (int x = 0; x < V; ++x)
+    *reinterpret_cast<u32x4*>(Wt + (size_t)e * H * H + (size_t)(V * oq + x) * H + V * hq) = tile_row_T<S>(r, x);
+}
+
 }  // namespace dev
 
 // Workgroup size: the largest (up to four waves, never more rows than a block
@@ -939,6 +961,7 @@ struct BitsArgs {
   void* dM;             // mode 1
   long ldm;
   int n_pad, E;
+  const void* Wt = nullptr;   // mode 0: W_e^T [E][H][H] (optional; used by the direct-weight forms)
   const void* Wi = nullptr;   // mode 0 with the GRU epilogue (when non-NULL and supported)
   const void* U = nullptr;
   const float* bg = nullptr;
@@ -993,7 +1016,8 @@ hipError_t bits_launch(const BitsArgs& A, hipStream_t st) {
   if (rgru) op = nullptr;   // dX goes straight into the GRU reverse
 #define GGNN_STEP(WV, TGN, REVB, GRUB)                                                                        \
   hipLaunchKernelGGL((dev::step_bits_kernel<S, H, B, WV, C::WDIR, TGN, REVB, GRUB>), dim3(blocks),            \
-                     dim3(TGN * WV * 64), 0, st, bp, vp, wp, A.bias, op, A.n_pad, A.E, A.dX_in, dmp, A.ldm,     \
+                     dim3(TGN * WV * 64), 0, st, bp, vp, wp, static_cast<const S*>(A.Wt), A.bias, op, A.n_pad,  \
+                     A.E, A.dX_in, dmp, A.ldm,                                                                  \
                      static_cast<const S*>(A.Wi), static_cast<const S*>(A.U), A.bg, static_cast<S*>(A.h_out),  \
                      static_cast<S*>(A.saved), static_cast<const S*>(A.rh_h), static_cast<const S*>(A.rh_saved), \
                      static_cast<S*>(A.rh_da), A.rh_dh, static_cast<S*>(A.rh_ghat))
@@ -1063,9 +1087,10 @@ hipError_t launch_step_fwd_bits(int n_pad, int B, int H, int E, const void* bits
 }
 
 hipError_t launch_step_fwd_bits_gru(int n_pad, int B, int H, int E, const void* bits, const void* X, const void* W,
-                                    const float* bias, float* a, const void* Wi, const void* U, const float* bg,
-                                    void* h_out, void* saved, bool* fused, hipStream_t st) {
+                                    const void* Wt, const float* bias, float* a, const void* Wi, const void* U,
+                                    const float* bg, void* h_out, void* saved, bool* fused, hipStream_t st) {
   BitsArgs A{0, bits, X, W, bias, a, nullptr, nullptr, 0, n_pad, E};
+  A.Wt = Wt;
   A.Wi = Wi;
   A.U = U;
   A.bg = bg;
@@ -1073,6 +1098,15 @@ hipError_t launch_step_fwd_bits_gru(int n_pad, int B, int H, int E, const void* 
   A.saved = saved;
   A.fused_gru = fused;
   return bits_t<dev::dt_t>(H, B, A, st);
+}
+
+hipError_t launch_transpose_weights(int H, int E, const void* W, void* Wt, hipStream_t st) {
+  using S = dev::dt_t;
+  constexpr int V = 16 / sizeof(S);
+  const long n = (long)E * (H / V) * (H / V);
+  hipLaunchKernelGGL((dev::transpose_weights_kernel<S>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+                     static_cast<const S*>(W), static_cast<S*>(Wt), H, E);
+  return hipGetLastError();
 }
 
 hipError_t launch_step_bwd_bits(int n_pad, int B, int H, int E, const void* bits_t_, const void* da, const void* W,

@@ -204,9 +204,20 @@ ggnn_status ggnn_banded_step_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, i
       "banded_step_bits_bwd");
 }
 
+ggnn_status ggnn_transpose_weights(ggnn_dtype dt, int32_t H, int32_t E, const void* W, void* Wt, void* stream) {
+  clear_error();
+  GGNN_CHECK_ARG(supported_dtype(dt), "unknown dtype %d", dt);
+  GGNN_CHECK_ARG(supported_H(H), "H=%d must be one of 32, 64, 128, 256", H);
+  GGNN_CHECK_ARG(E >= 1 && E <= 64, "E=%d must be in [1, 64]", E);
+  CHECK_PTR(W, "W");
+  CHECK_PTR(Wt, "Wt");
+  GGNN_CHECK_ARG(W != Wt, "Wt must not overlap W");
+  return device_status(launch_transpose_weights(dt, H, E, W, Wt, as_stream(stream)), "transpose_weights");
+}
+
 ggnn_status ggnn_step_bits_gru(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E, const void* bits,
-                               const void* X, const void* W, const float* bias, const void* Wi, const void* U,
-                               const float* b, float* a, void* h_out, void* saved, void* stream) {
+                               const void* X, const void* W, const void* Wt, const float* bias, const void* Wi,
+                               const void* U, const float* b, float* a, void* h_out, void* saved, void* stream) {
   clear_error();
   ggnn_status st = check_banded(dt, n_pad, B, H, E);
   if (st != GGNN_OK) return st;
@@ -222,7 +233,9 @@ ggnn_status ggnn_step_bits_gru(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t 
   CHECK_PTR(saved, "saved");
   hipStream_t s = as_stream(stream);
   bool fused = false;
-  hipError_t err = launch_step_fwd_bits_gru(dt, n_pad, B, H, E, bits, X, W, bias, a, Wi, U, b, h_out, saved, &fused, s);
+  CHECK_OPT_PTR(Wt, "Wt");
+  hipError_t err =
+      launch_step_fwd_bits_gru(dt, n_pad, B, H, E, bits, X, W, Wt, bias, a, Wi, U, b, h_out, saved, &fused, s);
   if (err == hipSuccess && !fused) err = launch_gru_fwd(dt, n_pad, H, a, X, Wi, U, b, h_out, saved, s);
   return device_status(err, "step_bits_gru");
 }
@@ -308,6 +321,7 @@ static ggnn_status check_model(const ggnn_model* m) {
   GGNN_CHECK_ARG(m->band_format == GGNN_BAND_DENSE || m->band_format == GGNN_BAND_BITS,
                  "unknown band_format %d", m->band_format);
   if (m->band_format == GGNN_BAND_BITS) CHECK_PTR(m->band_t, "model.band_t");
+  CHECK_OPT_PTR(m->Wt, "model.Wt");
   return GGNN_OK;
 }
 
@@ -346,8 +360,8 @@ ggnn_status ggnn_forward(const ggnn_model* m, const ggnn_activations* act, void*
     hipError_t err;
     bool fused = false;   // the bit-band step also ran the GRU update
     if (m->band_format == GGNN_BAND_BITS) {
-      err = launch_step_fwd_bits_gru(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, Xt, m->W, m->bias, at, m->Wi,
-                                     m->U, m->b, Xn, sv, &fused, s);
+      err = launch_step_fwd_bits_gru(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, Xt, m->W, m->Wt, m->bias, at,
+                                     m->Wi, m->U, m->b, Xn, sv, &fused, s);
     } else {
       err = launch_transform_fwd(m->dtype, m->n_pad, m->H, m->E, Xt, m->W, m->bias, act->M, s);
       if (err == hipSuccess) err = launch_banded_fwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, act->M, at, s);

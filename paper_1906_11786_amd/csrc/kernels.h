@@ -25,8 +25,10 @@ namespace ggnn {
   hipError_t launch_banded_bwd_bits(int n_pad, int B, int H, int E, const void* bits_t, const void* da, void* dM, \
                                     long ldm, hipStream_t st);                                                    \
   hipError_t launch_step_fwd_bits_gru(int n_pad, int B, int H, int E, const void* bits, const void* X,           \
-                                      const void* W, const float* bias, float* a, const void* Wi, const void* U,  \
-                                      const float* bg, void* h_out, void* saved, bool* fused, hipStream_t st);    \
+                                      const void* W, const void* Wt, const float* bias, float* a, const void* Wi, \
+                                      const void* U, const float* bg, void* h_out, void* saved, bool* fused,      \
+                                      hipStream_t st);                                                            \
+  hipError_t launch_transpose_weights(int H, int E, const void* W, void* Wt, hipStream_t st);                    \
   hipError_t launch_step_bwd_bits_gru(int n_pad, int B, int H, int E, const void* bits_t, const void* da,         \
                                       const void* W, const float* dX_in, float* dX_out, void* dM, long ldm,       \
                                       const void* Wi, const void* U, const void* h_prev, const void* saved_prev,  \
@@ -89,11 +91,18 @@ inline hipError_t launch_banded_bwd_bits(int dt, int n_pad, int B, int H, int E,
 }
 // Forward step with the GRU update fused in where the shape allows (sets
 // *fused; otherwise only `a` is written and the caller runs the GRU).
+// Wt (W_e^T, optional) lets the direct-weight forms read their weight
+// fragments as 16-byte rows instead of 2-byte column gathers.
 inline hipError_t launch_step_fwd_bits_gru(int dt, int n_pad, int B, int H, int E, const void* bits, const void* X,
-                                           const void* W, const float* bias, float* a, const void* Wi, const void* U,
-                                           const float* bg, void* h_out, void* saved, bool* fused, hipStream_t st) {
-  return GGNN_DT_PICK(launch_step_fwd_bits_gru, n_pad, B, H, E, bits, X, W, bias, a, Wi, U, bg, h_out, saved, fused,
-                      st);
+                                           const void* W, const void* Wt, const float* bias, float* a,
+                                           const void* Wi, const void* U, const float* bg, void* h_out, void* saved,
+                                           bool* fused, hipStream_t st) {
+  return GGNN_DT_PICK(launch_step_fwd_bits_gru, n_pad, B, H, E, bits, X, W, Wt, bias, a, Wi, U, bg, h_out, saved,
+                      fused, st);
+}
+// Wt[e][o][h] = W[e][h][o].
+inline hipError_t launch_transpose_weights(int dt, int H, int E, const void* W, void* Wt, hipStream_t st) {
+  return GGNN_DT_PICK(launch_transpose_weights, H, E, W, Wt, st);
 }
 // Reverse step that continues, where the shape allows (sets *fused), with
 // the previous step's GRU reverse on the completed dX: writes da_prev

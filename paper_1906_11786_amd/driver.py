@@ -111,6 +111,9 @@ class BandedGGNN:
             self.band = band_to_device(band, dt, device)
             del band
         self.W = to_device(params.W, dt, device)
+        # W_e^T, an optional operand of the bit-band forward (row reads of its
+        # weight fragments); refreshed from W by refresh_weights().
+        self.Wt = torch.empty_like(self.W)
         self.bias = None if params.bias is None else torch.from_numpy(params.bias.astype(np.float32)).to(device)
         self.Wi = to_device(params.Wi, dt, device)
         self.U = to_device(params.U, dt, device)
@@ -143,7 +146,8 @@ class BandedGGNN:
             dtype=capi.DTYPES[dt], n_pad=n_pad, B=B, H=H, E=E, T=T, band=self.band.data_ptr(),
             W=self.W.data_ptr(), bias=None if self.bias is None else self.bias.data_ptr(), Wi=self.Wi.data_ptr(),
             U=self.U.data_ptr(), b=self.b.data_ptr(), band_format=capi.BAND_FORMATS[band_format],
-            band_t=None if self.band_t is None else self.band_t.data_ptr())
+            band_t=None if self.band_t is None else self.band_t.data_ptr(), Wt=self.Wt.data_ptr())
+        self.refresh_weights()
         ws = capi.ggnn_backward_workspace_bytes(self.model)
         self.workspace = torch.empty((max(ws, 16),), dtype=torch.uint8, device=device)
         self.act = capi.ggnn_activations(X=self.X.data_ptr(), a=self.a.data_ptr(), saved=self.saved.data_ptr(),
@@ -153,6 +157,10 @@ class BandedGGNN:
             dU=self.dU.data_ptr(), db=self.db.data_ptr(), da=self.da.data_ptr(), dM=self.dM.data_ptr(),
             dh=self.dh.data_ptr(), workspace=self.workspace.data_ptr(), workspace_bytes=self.workspace.numel())
         comp.stats["upload_seconds"] = time.perf_counter() - t0
+
+    def refresh_weights(self, stream=None):
+        """Recompute W_e^T after W changes."""
+        capi.ggnn_transpose_weights(self.dt, self.H, self.comp.E, self.W, self.Wt, stream)
 
     def forward(self, stream=None):
         capi.ggnn_forward(self.model, self.act, stream)

@@ -327,8 +327,19 @@ def test_step_bits_gru(dt, B, H, E, nb):
     a = torch.full((n, H), float("nan"), device="cuda")
     h_out = torch.full((n, H), float("nan"), device="cuda", dtype=torch_dt(dt))
     saved = torch.full((n, 3 * H), float("nan"), device="cuda", dtype=torch_dt(dt))
-    capi.ggnn_step_bits_gru(dt, n, B, H, E, bits, dev(X, dt), dev(W, dt), dev(bias), dev(Wi, dt), dev(U, dt),
+    Wd = dev(W, dt)
+    Wt = torch.empty_like(Wd)
+    capi.ggnn_transpose_weights(dt, H, E, Wd, Wt)
+    assert torch.equal(Wt.float().cpu(), Wd.float().cpu().transpose(1, 2))
+    capi.ggnn_step_bits_gru(dt, n, B, H, E, bits, dev(X, dt), Wd, Wt, dev(bias), dev(Wi, dt), dev(U, dt),
                             dev(b), a, h_out, saved)
+    # without the transposed weights (column gathers): the same bits
+    a2 = torch.full((n, H), float("nan"), device="cuda")
+    h2 = torch.full((n, H), float("nan"), device="cuda", dtype=torch_dt(dt))
+    s2 = torch.full((n, 3 * H), float("nan"), device="cuda", dtype=torch_dt(dt))
+    capi.ggnn_step_bits_gru(dt, n, B, H, E, bits, dev(X, dt), Wd, None, dev(bias), dev(Wi, dt), dev(U, dt),
+                            dev(b), a2, h2, s2)
+    assert torch.equal(a, a2) and torch.equal(h_out, h2) and torch.equal(saved, s2)
     s, d, e, _, _ = O.kept_edges(src, dst, et, B)
     wa = O.aggregate(n, s, d, e, O.msg_transform(X, W, bias))
     assert relerr(host(a), wa) <= 1e-4

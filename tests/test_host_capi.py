@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
     for name in declared:
         assert hasattr(L, name), name
     assert set(declared) == set(capi.EXPORTS)
-    assert capi.ggnn_abi_version() == 5
+    assert capi.ggnn_abi_version() == 6
     assert capi.ggnn_status_string(3) == "GGNN_ERR_OUT_OF_BAND"
 
 
