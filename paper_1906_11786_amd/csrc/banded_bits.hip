@@ -292,25 +292,28 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   // node (k-1+s)*B + c, feature f.  Forward: V x V tiles of node-major X,
   // transposed in registers (loads of whole 128-byte lines), one 16-byte
   // store per tile row.  Reverse: plain 16-byte copies of feature-major da.
-  // Each thread issues the loads of up to PB units before its writes.
-  if constexpr (C::ALL) {
-    if constexpr (!REV) {
-      // With GRU, the tiles of Wi and U follow (fragment order, gru_fwd_idx).
-      constexpr int XT = (KC / V) * (H / V);       // tiles per block
-      constexpr int GT = (H / V) * (3 * H / V);    // tiles per GRU weight
+  // With the GRU fused, Wi and U follow as further units (fragment order);
+  // they are only read by the epilogue, so they are staged after the type
+  // loop, while the waves of the other type group are still busy.  Each
+  // thread issues the loads of up to PB units before its writes.
+  constexpr int XT = !REV ? (KC / V) * (H / V) : H * (KC / V);   // units per block: tiles / 16-byte copies
+  constexpr int GT = !REV ? (H / V) * (3 * H / V) : H * (3 * H / V);   // units per GRU weight
+  const int nx = (s_hi - s_lo + 1) * XT;
+  const int total = nx + (GRU ? 2 * GT : 0);
+  auto stage_units = [&](int lo, int hi) __attribute__((always_inline)) {
+    if constexpr (C::ALL && !REV) {
       constexpr int PB = 2;
-      const int nx = (s_hi - s_lo + 1) * XT;
-      const int total = nx + (GRU ? 2 * GT : 0);
-      for (int base = 0; base < total; base += PB * NT) {
+      for (int base = lo; base < hi; base += PB * NT) {
         u32x4 r[PB][V];
 #pragma unroll
         for (int u = 0; u < PB; ++u) {
           const int lin = base + u * NT + tid;
-          if (lin < nx) {
+          if (lin >= hi) {
+          } else if (lin < nx) {
             const int slot = s_lo + lin / XT, rem = lin % XT;
             const int cq = rem % (KC / V), fq = rem / (KC / V);
             tile_load<S>(r[u], X + (size_t)((k - 1 + slot) * B + V * cq) * H + V * fq, H);
-          } else if (lin < total) {
+          } else {
             const int w = lin - nx, m = w / GT, rem = w % GT;
             const int hq = rem % (H / V), cq = rem / (H / V);
             tile_load<S>(r[u], (m ? U : Wi) + (size_t)(V * hq) * 3 * H + V * cq, 3 * H);
@@ -319,14 +322,15 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
 #pragma unroll
         for (int u = 0; u < PB; ++u) {
           const int lin = base + u * NT + tid;
-          if (lin < nx) {
+          if (lin >= hi) {
+          } else if (lin < nx) {
             const int slot = s_lo + lin / XT, rem = lin % XT;
             const int cq = rem % (KC / V), fq = rem / (KC / V);
 #pragma unroll
             for (int x = 0; x < V; ++x)
               *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(perm_row(V * fq + x), V * cq)]) =
                   tile_row_T<S>(r[u], x);
-          } else if (lin < total) {
+          } else {
             const int w = lin - nx, m = w / GT, rem = w % GT;
             const int hq = rem % (H / V), cq = rem / (H / V);
             // row x of the transposed tile: gate column V*cq + x, input
@@ -343,24 +347,20 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
           }
         }
       }
-    } else {
-      // With GRU, Wi and U follow (fragment order, gru_rev_idx).
-      constexpr int UPB = H * (KC / V);            // 16-byte units per block
-      constexpr int UPW = H * (3 * H / V);         // 16-byte units per GRU weight
-      constexpr int PB = 4;
-      const int nx = (s_hi - s_lo + 1) * UPB;
-      const int total = nx + (GRU ? 2 * UPW : 0);
-      for (int base = 0; base < total; base += PB * NT) {
+    } else if constexpr (C::ALL) {
+      constexpr int PB = 8;
+      for (int base = lo; base < hi; base += PB * NT) {
         u32x4 r[PB];
 #pragma unroll
         for (int u = 0; u < PB; ++u) {
           const int lin = base + u * NT + tid;
-          if (lin < nx) {
-            const int slot = s_lo + lin / UPB, rem = lin % UPB;
+          if (lin >= hi) {
+          } else if (lin < nx) {
+            const int slot = s_lo + lin / XT, rem = lin % XT;
             const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
             r[u] = *reinterpret_cast<const u32x4*>(X + (size_t)h * n_pad + (k - 1 + slot) * B + c);
-          } else if (lin < total) {
-            const int w = lin - nx, m = w / UPW, rem = w % UPW;
+          } else {
+            const int w = lin - nx, m = w / GT, rem = w % GT;
             const int h = rem / (3 * H / V), c = (rem % (3 * H / V)) * V;
             r[u] = *reinterpret_cast<const u32x4*>((m ? U : Wi) + (size_t)h * 3 * H + c);
           }
@@ -368,12 +368,13 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
 #pragma unroll
         for (int u = 0; u < PB; ++u) {
           const int lin = base + u * NT + tid;
-          if (lin < nx) {
-            const int slot = s_lo + lin / UPB, rem = lin % UPB;
+          if (lin >= hi) {
+          } else if (lin < nx) {
+            const int slot = s_lo + lin / XT, rem = lin % XT;
             const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
             *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(perm_row(h), c)]) = r[u];
-          } else if (lin < total) {
-            const int w = lin - nx, m = w / UPW, rem = w % UPW;
+          } else {
+            const int w = lin - nx, m = w / GT, rem = w % GT;
             const int h = rem / (3 * H / V), c = (rem % (3 * H / V)) * V;
             // input feature h, gate columns c .. c + V - 1 (runs of four)
             const S* po = reinterpret_cast<const S*>(&r[u]);
@@ -385,6 +386,9 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         }
       }
     }
+  };
+  if constexpr (C::ALL) {
+    stage_units(0, nx);
     __syncthreads();
   }
 
@@ -617,6 +621,21 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   // Row tiles this wave completes: all of them, or with two groups and two
   // tiles per wave, tile tg.
   constexpr bool SPLIT = (TG == 2 && NTW == 2);
+  // GRU weights for the epilogue (read after the barriers below).
+  if constexpr (C::ALL && GRU) stage_units(nx, total);
+  // Epilogue operands of this wave's tile requested now, in flight across
+  // the barriers: h (forward) or the gates of the previous step (reverse).
+  frag_t<S> hf_pre[(GRU && !REV && SPLIT) ? H / 32 : 1];
+  GruBwdIn<S, H> gin_pre;
+  if constexpr (GRU && SPLIT) {
+    const int node = k * B + rw + 16 * tg + q;
+    if constexpr (!REV) {
+#pragma unroll
+      for (int kk = 0; kk < H / 32; ++kk) hf_pre[kk] = rowfrag<S>(X + (size_t)node * H, kk, g);
+    } else {
+      gin_pre.load(rh_saved, rh_h, node, g);
+    }
+  }
   if constexpr (TG > 1) {
     f32x4* red = reinterpret_cast<f32x4*>(&vt[0][0]);
     __syncthreads();   // every wave is done reading the staged blocks
@@ -682,8 +701,8 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
       auto wl = [&](int which, int row, int gate, int kk) __attribute__((always_inline)) {
         return load_fragi<S>(gw, gru_rev_idx<S, H>(which, row / 16, gate, kk), lane);
       };
-      gru_bwd_wave<S, H>(gg, k * B + rw + 16 * n, q, g, rh_h, rh_saved, wl, rh_da, n_pad, rh_dh,
-                             rh_ghat);
+      if constexpr (!SPLIT) gin_pre.load(rh_saved, rh_h, k * B + rw + 16 * n + q, g);
+      gru_bwd_wave<S, H>(gg, k * B + rw + 16 * n, q, g, gin_pre, wl, rh_da, n_pad, rh_dh, rh_ghat);
     }
     if constexpr (GRU && !REV) {
       // GRU of Eq. 1 (Cho et al. 2014 form) for this tile's 16 nodes, as in
@@ -705,7 +724,11 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         } else {
           af[0][kk] = pack8<S>(v8);
         }
-        hf[kk] = load4x2(X + (size_t)node * H + 32 * kk + 4 * g, X + (size_t)node * H + 32 * kk + 16 + 4 * g);
+        if constexpr (SPLIT) {
+          hf[kk] = hf_pre[kk];
+        } else {
+          hf[kk] = rowfrag<S>(X + (size_t)node * H, kk, g);
+        }
       }
       // Weight fragments of gate columns 16*t16 .. 16*t16 + 15 (fragment order).
       auto gfrag = [&](int mat, int t16, int kk) __attribute__((always_inline)) {

@@ -197,16 +197,18 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
   f32x4 gg[MTL];
 #pragma unroll
   for (int m = 0; m < MTL; ++m) gg[m] = *reinterpret_cast<const f32x4*>(gin + (size_t)node * H + 16 * m + 4 * g);
+  GruBwdIn<S, H> in;
+  in.load(saved, h, node, g);
   if constexpr (LDSW) {
     auto wf = [&](int which, int row, int gate, int kk) __attribute__((always_inline)) {
       return load_fragi<S>(wl, gru_rev_idx<S, H>(which, row / 16, gate, kk), lane);
     };
-    gru_bwd_wave<S, H>(gg, n0, q, g, h, saved, wf, daT, n_pad, dh, ghat);
+    gru_bwd_wave<S, H>(gg, n0, q, g, in, wf, daT, n_pad, dh, ghat);
   } else {
     auto wf = [&](int which, int row, int gate, int kk) __attribute__((always_inline)) {
       return rowfrag<S>((which ? U : Wi) + (size_t)row * 3 * H + gate * H, kk, g);
     };
-    gru_bwd_wave<S, H>(gg, n0, q, g, h, saved, wf, daT, n_pad, dh, ghat);
+    gru_bwd_wave<S, H>(gg, n0, q, g, in, wf, daT, n_pad, dh, ghat);
   }
 }
 

@@ -24,15 +24,36 @@ __device__ __forceinline__ frag_t<S> rowfrag(const S* row, int kk, int g) {
   return load4x2(row + 32 * kk + 4 * g, row + 32 * kk + 16 + 4 * g);
 }
 
-// gg[m]: dL/dh' for features 16m + 4g + {0..3} of node n0 + q.
+// The per-node inputs of the GRU reverse, for features 16m + 4g + {0..3}
+// of one node: the saved gates r, z, n and the state h (loaded ahead of
+// use by the fused reverse step, where the loads cross a barrier).
+template <typename S, int H>
+struct GruBwdIn {
+  f32x4 r[H / 16], z[H / 16], n[H / 16], h[H / 16];
+  __device__ __forceinline__ void load(const S* saved, const S* hs, int node, int g) {
+    const S* sv = saved + (size_t)node * 3 * H;
+#pragma unroll
+    for (int m = 0; m < H / 16; ++m) {
+      const int f = 16 * m + 4 * g;
+      r[m] = load4f(sv + f);
+      z[m] = load4f(sv + H + f);
+      n[m] = load4f(sv + 2 * H + f);
+      h[m] = load4f(hs + (size_t)node * H + f);
+    }
+  }
+};
+
+// gg[m]: dL/dh' for features 16m + 4g + {0..3} of node n0 + q; in: the
+// gates and state of that node (GruBwdIn::load).
 // wfrag(which, row, gate, kk): the weight fragment of input feature `row`
 // (row % 16 == q) and gate columns gate*H + 32kk + (accumulator-compatible
 // order) of Wi (which = 0) or U (which = 1), from LDS or global memory.
 // Writes daT[f][n0 + 4g + j] (feature-major, row pitch ld), dh[node][.]
 // (node-major, float) and ghat[node][.] (node-major, 3H).
 template <typename S, int H, typename WF>
-__device__ __forceinline__ void gru_bwd_wave(const f32x4 (&gg)[H / 16], int n0, int q, int g, const S* h,
-                                             const S* saved, WF wfrag, S* daT, long ld, float* dh, S* ghat) {
+__device__ __forceinline__ void gru_bwd_wave(const f32x4 (&gg)[H / 16], int n0, int q, int g,
+                                             const GruBwdIn<S, H>& in, WF wfrag, S* daT, long ld, float* dh,
+                                             S* ghat) {
   constexpr int KS = H / 32;
   constexpr int MTL = H / 16;
   const int node = n0 + q;
@@ -40,13 +61,11 @@ __device__ __forceinline__ void gru_bwd_wave(const f32x4 (&gg)[H / 16], int n0, 
   frag_t<S> gf[3][KS];          // r^, z^, n^ as operand fragments
   f32x4 dacc[MTL];              // dh accumulator (D layout: features 16m + 4g + j)
   float zv[8], nv[8];
-  const S* sv = saved + (size_t)node * 3 * H;
   S* gh = ghat + (size_t)node * 3 * H;
 #pragma unroll
   for (int m = 0; m < MTL; ++m) {
     const int f = 16 * m + 4 * g;
-    const f32x4 z4 = load4f(sv + H + f), n4 = load4f(sv + 2 * H + f);
-    const f32x4 h4 = load4f(h + (size_t)node * H + f);
+    const f32x4 z4 = in.z[m], n4 = in.n[m], h4 = in.h[m];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const float dn = gg[m][j] * (1.f - z4[j]);
@@ -76,7 +95,7 @@ __device__ __forceinline__ void gru_bwd_wave(const f32x4 (&gg)[H / 16], int n0, 
     for (int m = 0; m < MTL; ++m) {
       const f32x4 acc = qacc[m];
       const int f = 16 * m + 4 * g;
-      const f32x4 r4 = load4f(sv + f), h4 = load4f(h + (size_t)node * H + f);
+      const f32x4 r4 = in.r[m], h4 = in.h[m];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         rv[4 * (m % 2) + j] = acc[j] * h4[j] * r4[j] * (1.f - r4[j]);
