@@ -51,7 +51,11 @@ namespace ggnn {
                                   const void* Wi, const void* U, void* da, float* dh, void* ghat,                 \
                                   hipStream_t st);                                                                \
   hipError_t launch_gru_wgrad(long K, int H, const float* a, const void* h, const void* saved, const void* ghat,  \
-                              float* dWi, float* dU, float* db, void* ws, hipStream_t st);
+                              float* dWi, float* dU, float* db, void* ws, hipStream_t st);                       \
+  bool step_wide_applies(int B, int H);                                                                           \
+  hipError_t launch_step_wide(bool rev, int n_pad, int B, int H, int E, const void* bits, const void* V,          \
+                              const void* Wsrc, const float* bias, float* out, const float* dX_in, void* dM,      \
+                              long ldm, hipStream_t st);
 
 namespace impl_bf16 {
 GGNN_DT_LAUNCHERS
@@ -93,10 +97,19 @@ inline hipError_t launch_banded_bwd_bits(int dt, int n_pad, int B, int H, int E,
 // *fused; otherwise only `a` is written and the caller runs the GRU).
 // Wt (W_e^T, optional) lets the direct-weight forms read their weight
 // fragments as 16-byte rows instead of 2-byte column gathers.
+//
+// Wide shapes (bf16, H = 128 or 256, B = 128..512) run the sliced wide step
+// kernel instead (forward: only when Wt is given); the GRU then runs in its
+// own kernel.
+inline bool step_wide(int dt, int B, int H) { return dt == GGNN_BF16 && impl_bf16::step_wide_applies(B, H); }
 inline hipError_t launch_step_fwd_bits_gru(int dt, int n_pad, int B, int H, int E, const void* bits, const void* X,
                                            const void* W, const void* Wt, const float* bias, float* a,
                                            const void* Wi, const void* U, const float* bg, void* h_out, void* saved,
                                            bool* fused, hipStream_t st) {
+  if (Wt != nullptr && step_wide(dt, B, H)) {
+    if (fused) *fused = false;
+    return impl_bf16::launch_step_wide(false, n_pad, B, H, E, bits, X, Wt, bias, a, nullptr, nullptr, 0, st);
+  }
   return GGNN_DT_PICK(launch_step_fwd_bits_gru, n_pad, B, H, E, bits, X, W, Wt, bias, a, Wi, U, bg, h_out, saved,
                       fused, st);
 }
@@ -113,6 +126,10 @@ inline hipError_t launch_step_bwd_bits_gru(int dt, int n_pad, int B, int H, int 
                                            const void* Wi, const void* U, const void* h_prev, const void* saved_prev,
                                            void* da_prev, float* dh_prev, void* ghat_prev, bool* fused,
                                            hipStream_t st) {
+  if (dX_out != nullptr && step_wide(dt, B, H)) {
+    if (fused) *fused = false;
+    return impl_bf16::launch_step_wide(true, n_pad, B, H, E, bits_t, da, W, nullptr, dX_out, dX_in, dM, ldm, st);
+  }
   return GGNN_DT_PICK(launch_step_bwd_bits_gru, n_pad, B, H, E, bits_t, da, W, dX_in, dX_out, dM, ldm, Wi, U, h_prev,
                       saved_prev, da_prev, dh_prev, ghat_prev, fused, st);
 }
@@ -121,6 +138,8 @@ inline hipError_t launch_step_bwd_bits_gru(int dt, int n_pad, int B, int H, int 
 inline hipError_t launch_step_bwd_bits(int dt, int n_pad, int B, int H, int E, const void* bits_t, const void* da,
                                        const void* W, const float* dX_in, float* dX_out, void* dM, long ldm,
                                        hipStream_t st) {
+  if (step_wide(dt, B, H))
+    return impl_bf16::launch_step_wide(true, n_pad, B, H, E, bits_t, da, W, nullptr, dX_out, dX_in, dM, ldm, st);
   return GGNN_DT_PICK(launch_step_bwd_bits, n_pad, B, H, E, bits_t, da, W, dX_in, dX_out, dM, ldm, st);
 }
 

@@ -309,6 +309,86 @@ def test_banded_step_bits_bwd_real_values(dt, B, H, E, nb):
 STEP_GRU_CASES = [(128, 64, 10, 5), (64, 128, 2, 6), (32, 32, 4, 9), (256, 256, 2, 3)]
 
 
+def _wide(dt, B, H):
+    """Shapes served by the sliced wide step kernel (bf16, H of 128 or 256,
+    B of 128 to 512; the forward only when W_e^T is given)."""
+    return dt == "bf16" and H in (128, 256) and B in (128, 256, 512)
+
+
+# Wide-kernel shapes: E = 1 stages most of each next feature slice after the
+# slice's last type, B = 512 keeps a single node-slice buffer, nb = 1 has no
+# neighbouring blocks, nb >= 3 has interior block rows.
+WIDE_CASES = [(128, 128, 2, 3), (256, 128, 1, 3), (512, 128, 2, 2), (128, 256, 3, 3), (256, 256, 1, 2),
+              (256, 256, 4, 1), (256, 256, 3, 3), (512, 256, 2, 2)]
+
+
+@pytest.mark.parametrize("B,H,E,nb", WIDE_CASES)
+@pytest.mark.parametrize("with_bias", [False, True])
+def test_step_wide_forward_integer_exact(B, H, E, nb, with_bias):
+    """a = sum_e (A_e X) W_e (+ deg_e b_e) through the wide forward step
+    (bf16, W_e^T given), small integers: every partial sum exact."""
+    dt = "bf16"
+    say(f"step_wide fwd int B={B} H={H} E={E} nb={nb} bias={with_bias}")
+    rng = np.random.default_rng(B * 29 + H + E + nb)
+    n = B * nb
+    src, dst, et = _edges(rng, n, 6 * n, E, 2 * B + 5)
+    bits, _, _ = _bits(n, E, B, src, dst, et)
+    X = rng.integers(-2, 3, (n, H)).astype(np.float64)
+    W = rng.integers(-1, 2, (E, H, H)).astype(np.float64)
+    bias = rng.integers(-2, 3, (E, H)).astype(np.float64) if with_bias else None
+    _, _, Wi, U, b = _gru_inputs(dt, rng, n, H)
+    Wd = dev(W, dt)
+    Wt = torch.empty_like(Wd)
+    capi.ggnn_transpose_weights(dt, H, E, Wd, Wt)
+    a = torch.full((n, H), float("nan"), device="cuda")
+    h_out = torch.full((n, H), float("nan"), device="cuda", dtype=torch_dt(dt))
+    saved = torch.full((n, 3 * H), float("nan"), device="cuda", dtype=torch_dt(dt))
+    capi.ggnn_step_bits_gru(dt, n, B, H, E, bits, dev(X, dt), Wd, Wt, None if bias is None else dev(bias),
+                            dev(Wi, dt), dev(U, dt), dev(b), a, h_out, saved)
+    s, d, e, _, _ = O.kept_edges(src, dst, et, B)
+    np.testing.assert_array_equal(host(a), O.aggregate(n, s, d, e, O.msg_transform(X, W, bias)))
+
+
+@pytest.mark.parametrize("B,H,E,nb", WIDE_CASES)
+def test_step_wide_reverse_integer_exact(B, H, E, nb):
+    """dM_e = A_e^T da and dX = dX_in + sum_e dM_e W_e^T through the wide
+    reverse step, small integers: exact (rows past n_pad untouched)."""
+    test_banded_step_bits_bwd_integer_exact("bf16", B, H, E, nb)
+
+
+@pytest.mark.parametrize("B,H,nb", [(256, 256, 3), (128, 128, 4), (512, 128, 2)])
+def test_step_wide_real_values(B, H, nb):
+    """Ten edge types, real values, both directions of the wide step against
+    the oracle at the bf16 tolerance (the forward aggregate as hi + lo)."""
+    dt, E = "bf16", 10
+    say(f"step_wide real B={B} H={H} E={E} nb={nb}")
+    rng = np.random.default_rng(B + 13 * H + nb)
+    n = B * nb
+    src, dst, et = _edges(rng, n, 20 * n, E, B + 3)
+    bits, bits_t, _ = _bits(n, E, B, src, dst, et)
+    X = round_to(dt, rng.standard_normal((n, H)))
+    W = round_to(dt, rng.standard_normal((E, H, H)) / np.sqrt(H))
+    _, _, Wi, U, b = _gru_inputs(dt, rng, n, H)
+    Wd = dev(W, dt)
+    Wt = torch.empty_like(Wd)
+    capi.ggnn_transpose_weights(dt, H, E, Wd, Wt)
+    a = torch.empty((n, H), device="cuda")
+    h_out = torch.empty((n, H), device="cuda", dtype=torch_dt(dt))
+    saved = torch.empty((n, 3 * H), device="cuda", dtype=torch_dt(dt))
+    capi.ggnn_step_bits_gru(dt, n, B, H, E, bits, dev(X, dt), Wd, Wt, None, dev(Wi, dt), dev(U, dt), dev(b), a,
+                            h_out, saved)
+    s, d, e, _, _ = O.kept_edges(src, dst, et, B)
+    assert relerr(host(a), O.aggregate(n, s, d, e, O.msg_transform(X, W))) <= 1e-4
+    da = X                                   # any bf16 values serve as the upstream gradient
+    want_dM = O.aggregate_transpose(n, s, d, e, da, E)
+    want_dX, _, _ = O.msg_transform_backward(np.zeros((n, H)), W, want_dM)
+    dM = torch.empty((E, n, H), device="cuda", dtype=torch_dt(dt))
+    dX = torch.empty((n, H), device="cuda")
+    capi.ggnn_banded_step_bits_bwd(dt, n, B, H, E, bits_t, dev(da.T, dt), Wd, None, dX, dM, n)
+    assert relerr(host(dM), want_dM) <= TOL[dt]
+    assert relerr(host(dX), want_dX) <= TOL[dt]
+
+
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("B,H,E,nb", STEP_GRU_CASES)
 def test_step_bits_gru(dt, B, H, E, nb):
@@ -339,7 +419,11 @@ def test_step_bits_gru(dt, B, H, E, nb):
     s2 = torch.full((n, 3 * H), float("nan"), device="cuda", dtype=torch_dt(dt))
     capi.ggnn_step_bits_gru(dt, n, B, H, E, bits, dev(X, dt), Wd, None, dev(bias), dev(Wi, dt), dev(U, dt),
                             dev(b), a2, h2, s2)
-    assert torch.equal(a, a2) and torch.equal(h_out, h2) and torch.equal(saved, s2)
+    if _wide(dt, B, H):
+        # with Wt the sliced wide kernel runs: another summation order
+        assert relerr(host(a2), host(a)) <= 1e-5
+    else:
+        assert torch.equal(a, a2) and torch.equal(h_out, h2) and torch.equal(saved, s2)
     s, d, e, _, _ = O.kept_edges(src, dst, et, B)
     wa = O.aggregate(n, s, d, e, O.msg_transform(X, W, bias))
     assert relerr(host(a), wa) <= 1e-4
