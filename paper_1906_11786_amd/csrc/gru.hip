@@ -538,7 +538,9 @@ __global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restric
 // Wave w: matrix w / 4 (dWi or dU) and a quarter of that matrix's tiles.
 // ---------------------------------------------------------------------------
 template <typename S, int H> struct GruWgradCfg {
-  static constexpr int IT = H >= 128 ? 4096 / H : H;   // input features per workgroup
+  // input features per workgroup: each slice re-reads G^ (3H per row), so
+  // slices are as wide as the accumulators allow
+  static constexpr int IT = (H >= 256 && sizeof(S) == 2) ? 32 : (H >= 128 ? 4096 / H : H);
   static constexpr int NI = IT / 16, NCT = 3 * H / 16;  // tiles: input, gate columns
   static constexpr int KC = (sizeof(S) == 4 || H >= 256) ? 32 : (H >= 128 ? 64 : 128);   // rows per chunk
   static constexpr int IW = H == 32 ? 1 : NI;            // input tiles per wave
@@ -721,8 +723,8 @@ namespace {
 struct Split {
   int nsplit, per;
 };
-Split gru_split(long K, int H) {
-  const long slices = H >= 128 ? H / (4096 / H) : 1;
+Split gru_split(long K, int H, bool f32) {
+  const long slices = (H >= 256 && !f32) ? H / 32 : (H >= 128 ? H / (4096 / H) : 1);
   const long want = 256 / slices > 0 ? 256 / slices : 1;
   long per = ((K + want - 1) / want + 127) / 128 * 128;
   return {(int)((K + per - 1) / per), (int)per};
@@ -764,7 +766,7 @@ hipError_t gru_bwd_nodes_h(int n_pad, const float* dh_out, const void* h, const 
 template <typename S, int H>
 hipError_t gru_wgrad_h(long K, const float* a, const void* h, const void* saved, const void* ghat, float* dWi,
                        float* dU, float* db, void* ws, hipStream_t st) {
-  Split sp = gru_split(K, H);
+  Split sp = gru_split(K, H, sizeof(S) == 4);
   float* P = static_cast<float*>(ws);
   float* Pb = P + (size_t)sp.nsplit * 2 * H * 3 * H;
   const int blocks = sp.nsplit * (H / dev::GruWgradCfg<S, H>::IT);
@@ -815,7 +817,10 @@ size_t ghat_bytes(int dt, long rows, int H) {
 }
 
 size_t gru_wgrad_workspace(long K, int H) {
-  Split sp = gru_split(K, H);
+  // large enough for the split of either dtype
+  Split sp = gru_split(K, H, false);
+  const Split s32 = gru_split(K, H, true);
+  if (s32.nsplit > sp.nsplit) sp = s32;
   return ((size_t)sp.nsplit * 2 * H * 3 * H + (size_t)sp.nsplit * 3 * H) * sizeof(float);
 }
 

@@ -298,9 +298,11 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
 // each over all IT/16 input tiles.
 // ---------------------------------------------------------------------------
 template <typename S, int H> struct WgradNmCfg {
-  static constexpr int IT = H >= 256 ? 64 : H;                  // input features per workgroup
+  // All input features per workgroup: the stored dM (the large operand) is
+  // then read once; the H = 256 fp32 form keeps 64-feature slices.
+  static constexpr int IT = (H >= 256 && sizeof(S) == 4) ? 64 : H;   // input features per workgroup
   static constexpr int TE = H <= 32 ? 10 : (H == 64 ? 4 : (H == 128 && sizeof(S) == 2 ? 2 : 1));   // types per workgroup
-  static constexpr int KC = sizeof(S) == 4 ? 64 : 128;           // rows per chunk
+  static constexpr int KC = (sizeof(S) == 4 || H >= 256) ? 64 : 128;   // rows per chunk
   static constexpr int PX = IT + 16, PD = H + 16;                // LDS row pitches (elements)
   static constexpr int NPAIR = TE * H / 16;                      // (type, output tile) pairs
   static constexpr int PW = (NPAIR + 7) / 8;                     // pairs per wave (at most)
@@ -392,19 +394,45 @@ __global__ __launch_bounds__(512) void transform_wgrad_nm_kernel(const S* __rest
     if (c0 + KC < nhi) load_chunk(c0 + KC);
 #pragma unroll
     for (int k0 = 0; k0 < KC; k0 += 32) {
-      frag_t<S> fa[NI];
+      if constexpr (NI <= 8) {
+        // all X fragments of the k step held, each dM fragment in turn
+        frag_t<S> fa[NI];
 #pragma unroll
-      for (int i = 0; i < NI; ++i) fa[i] = tr_frag(sx[buf], PX, k0, 16 * i, lane);
+        for (int i = 0; i < NI; ++i) fa[i] = tr_frag(sx[buf], PX, k0, 16 * i, lane);
+#pragma unroll
+        for (int p = 0; p < PW; ++p) {
+          const int pr = wave + 8 * p;
+          if (PW * 8 == C::NPAIR || pr < C::NPAIR) {
+            const int te = pr / (H / 16), ot = pr % (H / 16);
+            const frag_t<S> fb = tr_frag(sd[buf] + te * KC * PD, PD, k0, 16 * ot, lane);
+#pragma unroll
+            for (int x = 0; x < 8; ++x) bsum[p] += static_cast<float>(fb[x]);
+#pragma unroll
+            for (int i = 0; i < NI; ++i) mma(acc[p][i], fa[i], fb);
+          }
+        }
+        continue;
+      }
+      // wide slices: the wave's dM fragments first (few), then each X
+      // fragment in turn (holding all X fragments would spill)
+      frag_t<S> fb[PW];
 #pragma unroll
       for (int p = 0; p < PW; ++p) {
         const int pr = wave + 8 * p;
         if (PW * 8 == C::NPAIR || pr < C::NPAIR) {
           const int te = pr / (H / 16), ot = pr % (H / 16);
-          const frag_t<S> fb = tr_frag(sd[buf] + te * KC * PD, PD, k0, 16 * ot, lane);
+          fb[p] = tr_frag(sd[buf] + te * KC * PD, PD, k0, 16 * ot, lane);
 #pragma unroll
-          for (int x = 0; x < 8; ++x) bsum[p] += static_cast<float>(fb[x]);
+          for (int x = 0; x < 8; ++x) bsum[p] += static_cast<float>(fb[p][x]);
+        }
+      }
 #pragma unroll
-          for (int i = 0; i < NI; ++i) mma(acc[p][i], fa[i], fb);
+      for (int i = 0; i < NI; ++i) {
+        const frag_t<S> fa = tr_frag(sx[buf], PX, k0, 16 * i, lane);
+#pragma unroll
+        for (int p = 0; p < PW; ++p) {
+          const int pr = wave + 8 * p;
+          if (PW * 8 == C::NPAIR || pr < C::NPAIR) mma(acc[p][i], fa, fb[p]);
         }
       }
     }
@@ -517,11 +545,11 @@ Split transform_split(long K, int H, int E) {
 }
 
 // Node-major form: about 256 workgroups (one per compute unit, 8 waves
-// each) over splits x type groups x input slices; splits are multiples of
-// 128 rows.
-Split transform_nm_split(long K, int H, int E) {
+// each) over splits x type groups x input slices (fp32 at H = 256 only);
+// splits are multiples of 128 rows.
+Split transform_nm_split(long K, int H, int E, bool f32) {
   const long te = H <= 32 ? 10 : (H == 64 ? 4 : (H == 128 ? 2 : 1));
-  const long per_split = ((E + te - 1) / te) * (H >= 256 ? H / 64 : 1);
+  const long per_split = ((E + te - 1) / te) * (H >= 256 && f32 ? H / 64 : 1);
   const long want = 256 / per_split > 0 ? 256 / per_split : 1;
   long per = ((K + want - 1) / want + 127) / 128 * 128;
   return {(int)((K + per - 1) / per), (int)per};
@@ -571,7 +599,7 @@ hipError_t transform_wgrad_h(long K, int E, const void* X, const void* dM, long 
 template <typename S, int H>
 hipError_t transform_wgrad_nm_h(long K, int E, const void* X, const void* dM, long ldk, float* dW, float* dbias,
                                 void* ws, hipStream_t st) {
-  Split sp = transform_nm_split(K, H, E);
+  Split sp = transform_nm_split(K, H, E, sizeof(S) == 4);
   using C = dev::WgradNmCfg<S, H>;
   float* P = static_cast<float*>(ws);
   float* Pb = dbias ? P + (size_t)sp.nsplit * E * H * H : nullptr;
@@ -635,8 +663,10 @@ hipError_t transform_wgrad_t(long K, int H, int E, const void* X, const void* dM
 #if GGNN_DT_BF16
 size_t transform_wgrad_workspace(long K, int H, int E) {
   // large enough for both forms (feature-major and node-major dM)
-  const Split a = transform_split(K, H, E), b = transform_nm_split(K, H, E);
-  const size_t n = (size_t)(a.nsplit > b.nsplit ? a.nsplit : b.nsplit);
+  const Split a = transform_split(K, H, E), b = transform_nm_split(K, H, E, false),
+              c = transform_nm_split(K, H, E, true);
+  size_t n = (size_t)(a.nsplit > b.nsplit ? a.nsplit : b.nsplit);
+  if ((size_t)c.nsplit > n) n = (size_t)c.nsplit;
   return (n * E * H * H + n * E * H) * sizeof(float);
 }
 #endif
