@@ -7,61 +7,85 @@
 // arranged so that every operand staged in LDS feeds several matrix-core
 // steps and the node blocks are staged once per workgroup, not per edge type.
 //
-// The transform's contraction over features is split into slices of
-// HQ = 32 features:  (A_e X) W_e = sum_q (A_e X[:, q]) W_e[q, :].
+// The transform's contraction over features is split into slices of HQ
+// features (64 or 32, chosen per shape below):
+//   (A_e X) W_e = sum_q (A_e X[:, q]) W_e[q, :].
 // For each slice q the workgroup stages features q of the three node blocks
 // (k-1, k, k+1) once; every edge type then reuses them.  Per type a wave
-// aggregates its 32 rows over the slice (registers, 32 x 32), and multiplies
-// that into its output accumulators (32 rows x H, registers) with rows q of
-// W_e (reverse) or of W_e^T (forward), which the workgroup stages per
-// (slice, type) in LDS in fragment order.  The next (slice, type)'s weights
-// and a share of the next slice's node blocks are loaded at the top of each
-// (slice, type) and written to the other LDS buffer at its end: one barrier
-// per (slice, type), none inside the products.
+// aggregates its 32 rows over the slice (registers, 32 x HQ), then
+// multiplies that into its output accumulators (32 rows x H, registers) with
+// rows q of W_e (reverse) or of W_e^T (forward).  The bit rows expanded to
+// matrix-core fragments (vector ALU work) feed HQ / 16 products each, so the
+// wider slice keeps the matrix cores, not the expansion, the bottleneck.
+// The weights pass through LDS in units of 32 features (H rows, fragment
+// order), shared by all waves: a ring of NH + 1 unit buffers (NH = HQ / 32),
+// the next slice's units loaded while the current ones are used and written
+// after each unit's products, one barrier per unit.  The next slice's node
+// blocks are prefetched over the type loop into a second buffer where LDS
+// allows, otherwise staged at the slice boundary.
 //
-// LDS layouts of a staged block slice (B nodes x 32 features):
-//   forward (X node-major in HBM): node rows of 32 features, the node range
-//     split into four lane-group regions (lane group g owns block columns
-//     [gB/4, (g+1)B/4) in the k order of the aggregation) separated by 32
-//     bytes, so the two 16-lane halves of a transposing read hit disjoint
-//     banks; read with ds_read_b64_tr_b16, which hands a lane eight
-//     consecutive nodes of one feature.  Feature f of the slice sits in
-//     column 16 (f % 8 / 4) + 4 (f / 8) + f % 4: the aggregate's tiles 0 and
-//     1 then give a lane eight consecutive features (the weight fragments are
-//     16-byte rows; the reverse stores dM with one 16-byte write).
+// LDS layouts of a staged block slice (B nodes x HQ features):
+//   forward (X node-major in HBM): node rows of HQ features, read with
+//     ds_read_b64_tr_b16, which hands a lane eight consecutive nodes of one
+//     feature.  Within a 32-feature group, feature f sits in column
+//     16 (f % 8 / 4) + 4 (f / 8) + f % 4, so the aggregate's tiles give a lane
+//     eight consecutive features (the weight fragments are 16-byte rows; the
+//     reverse stores dM with one 16-byte write).  The 16-column groups of a
+//     row are XOR-swizzled by row and lane group so that the four rows one
+//     read touches, and the two lane groups served together, hit disjoint
+//     banks.
 //   reverse (da feature-major in HBM): fragment order (a fragment's 64 lane
-//     vectors contiguous, 16-byte copies), features in the same permuted
-//     order.
+//     vectors contiguous, 16-byte copies), features in the same order.
 #include "device_common.h"
 #include "kernels.h"
 
 namespace ggnn {
 namespace dev {
 
-template <int H, int B>
+template <int H, int B, bool REV>
 struct WideCfg {
-  static constexpr int HQ = 32;                  // features per slice
-  static constexpr int NQ = H / HQ;
-  static constexpr int RPW = 32, NTW = 2;        // rows per wave, 16-row tiles per wave
+  // Features per slice: 64 where the three blocks' slice and the weight ring
+  // fit in LDS and the workgroup fills a compute unit anyway (B >= 256),
+  // except the H = 256 forward (its hi + lo transform already gives each
+  // staged byte more products; measured slower at 64); else 32 (at B = 128
+  // two workgroups then share a compute unit).
+  static constexpr int HQ =
+      (B >= 256 && (REV || H <= 128) && (3 * B * 64 + 3 * H * 32) * 2 <= 160 * 1024) ? 64 : 32;
+  static constexpr int NQ = H / HQ;             // slices
+  static constexpr int NH = HQ / 32;            // 32-feature weight units per slice
+  static constexpr int MQ = HQ / 16;            // aggregation tiles per slice
+  static constexpr int NWB = NH + 1;            // weight-unit buffers
+  static constexpr int RPW = 32, NTW = 2;       // rows per wave, 16-row tiles per wave
   static constexpr int WAVES = B / RPW < 8 ? B / RPW : 8;
-  static constexpr int R = WAVES * RPW;          // rows per workgroup
+  static constexpr int R = WAVES * RPW;         // rows per workgroup
   static constexpr int NT = WAVES * kWave;
-  static constexpr int RB = B / 32;              // bit-row bytes per lane and block
-  static constexpr int GROW = B / 4;             // block columns per lane group
-  static constexpr int PADG = 16;                // elements between lane-group regions (forward)
-  static constexpr int GS = GROW * HQ + PADG;    // elements per lane-group region (forward)
-  static constexpr int XS = B * HQ + 4 * PADG;   // elements per staged block slice
-  static constexpr int WS = (H / 16) * kWave * 8;   // elements per staged weight slice
-  static constexpr int NXB = (2 * 3 * XS + 2 * WS) * 2 <= 160 * 1024 ? 2 : 1;   // block-slice buffers
-  static constexpr int UNITS = 3 * B * HQ / 8;   // 16-byte units of one slice of the three blocks
-  static constexpr int XPT = 2;                  // of which each thread prefetches per (slice, type)
-  static constexpr int WPT = (H * 4 + NT - 1) / NT;   // weight units per thread per (slice, type)
+  static constexpr int RB = B / 32;             // bit-row bytes per lane and block
+  static constexpr int GROW = B / 4;            // block columns per lane group
+  static constexpr int XS = B * HQ;             // elements per staged block slice
+  static constexpr int WS = (H / 16) * kWave * 8;   // elements per weight unit
+  static constexpr int NXB = (2 * 3 * XS + NWB * WS) * 2 <= 160 * 1024 ? 2 : 1;   // block-slice buffers
+  static constexpr int UNITS = 3 * B * HQ / 8;  // 16-byte units of one slice of the three blocks
+  static constexpr int XPT = 2;                 // of which each thread prefetches per (slice, type)
+  static constexpr int WPT = (H * 4 + NT - 1) / NT;   // 16-byte vectors per thread per weight unit
 };
 
-// Feature f (0..31) of a slice -> its column in a forward node row.
-__device__ __forceinline__ int wide_col(int f) { return 16 * ((f % 8) / 4) + 4 * (f / 8) + f % 4; }
-// Feature f of a slice -> its (tile, row) slot, as 16 * tile + row.
-__device__ __forceinline__ int wide_slot(int f) { return wide_col(f); }
+// Feature f of a slice -> its (tile, row) slot, as 16 * tile + row (tile
+// 2j + i of the 32-feature group j holds features 32j + 8r + 4i + {0..3} in
+// rows 4r + {0..3}); also its column in a forward node row, before the
+// swizzle.
+__device__ __forceinline__ int wide_slot(int f) {
+  const int w = f % 32;
+  return 32 * (f / 32) + 16 * ((w % 8) / 4) + 4 * (w / 8) + w % 4;
+}
+// Swizzle of the 16-column groups of forward node row c (block-local).
+template <int HQ, int GROW>
+__device__ __forceinline__ int wide_sw(int c) {
+  if constexpr (HQ == 64) {
+    return ((c >> 1) & 1) | (((c / GROW) & 1) << 1);
+  } else {
+    return (c / GROW) & 1;
+  }
+}
 
 // Transposing fragment read: lane (p, g) addresses a0 (its lane group's row
 // p / 4 at column 4 (p % 4)); the lane receives element (row + j, column p)
@@ -118,19 +142,20 @@ template <int NB> struct WideBits {
 // (reverse, feature-major [H][n_pad]); Wsrc = W_e^T (forward) or W_e
 // (reverse), [E][H][H], row o holding the o-th output feature's weights.
 template <int H, int B, bool REV, bool BIAS>
-__global__ __launch_bounds__((WideCfg<H, B>::NT)) void step_wide_kernel(
+__global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
     const uint8_t* __restrict__ bits, const bf16s* __restrict__ V, const bf16s* __restrict__ Wsrc,
     const float* __restrict__ bias, float* __restrict__ out, int n_pad, int E, const float* __restrict__ dX_in,
     bf16s* __restrict__ dM, long ldm) {
-  using C = WideCfg<H, B>;
-  constexpr int NT = C::NT, HQ = C::HQ, NQ = C::NQ, NTW = C::NTW, RB = C::RB, XS = C::XS, GS = C::GS;
+  using C = WideCfg<H, B, REV>;
+  constexpr int NT = C::NT, HQ = C::HQ, NQ = C::NQ, NH = C::NH, MQ = C::MQ, NWB = C::NWB;
+  constexpr int NTW = C::NTW, RB = C::RB, XS = C::XS, GROW = C::GROW;
   constexpr int MT = H / 16;             // 16-feature output tiles
   constexpr int NP = REV ? 1 : 2;        // forward: the aggregate enters the transform as bf16 hi + lo
   constexpr int ROWB = B / 8;
   constexpr int UB = C::UNITS / 3;       // units per block
   constexpr int TPR = B / C::R;
   __shared__ __attribute__((aligned(16))) bf16s xs[C::NXB][3 * XS];
-  __shared__ __attribute__((aligned(16))) bf16s ws[2][C::WS];
+  __shared__ __attribute__((aligned(16))) bf16s ws[NWB][C::WS];
 
   const int nb = n_pad / B;
   const int t = xcd_swizzle(blockIdx.x, gridDim.x);
@@ -143,10 +168,11 @@ __global__ __launch_bounds__((WideCfg<H, B>::NT)) void step_wide_kernel(
   const int iters = NQ * E;
 
   // ---- staging units ----------------------------------------------------
-  // Unit u of slice qs, block s = u / UB.  Forward: node c = r / 4 of the
-  // block, features qs*HQ + 8G .. 8G + 7 (G = r % 4); reverse: feature
-  // f = 16 (r / (16 B/8)) + r % 16, nodes 8 c8 .. 8 c8 + 7 (c8 = (r / 16) %
-  // (B/8)).  Units of a block outside the matrix are skipped.
+  // Unit u of slice qs, block s = u / UB, r = u % UB.  Forward: node
+  // c = r / (HQ/8) of the block, features qs*HQ + 8G .. 8G + 7 (G = r %
+  // (HQ/8)); reverse: feature f = 16 (r / (16 B/8)) + r % 16 of the slice,
+  // nodes 8 c8 .. 8 c8 + 7 (c8 = (r / 16) % (B/8)).  Units of a block
+  // outside the matrix are skipped.
   auto unit_ok = [&](int u) __attribute__((always_inline)) {
     const int s = u / UB;
     return u < C::UNITS && s >= s_lo && s <= s_hi;
@@ -155,7 +181,7 @@ __global__ __launch_bounds__((WideCfg<H, B>::NT)) void step_wide_kernel(
     const int s = u / UB, r = u % UB;
     const bf16s* p;
     if constexpr (!REV) {
-      p = V + (size_t)((k - 1 + s) * B + r / 4) * H + qs * HQ + 8 * (r % 4);
+      p = V + (size_t)((k - 1 + s) * B + r / (HQ / 8)) * H + qs * HQ + 8 * (r % (HQ / 8));
     } else {
       const int f = 16 * (r / (16 * (B / 8))) + r % 16, c8 = (r / 16) % (B / 8);
       p = V + (size_t)(qs * HQ + f) * n_pad + (k - 1 + s) * B + 8 * c8;
@@ -166,25 +192,28 @@ __global__ __launch_bounds__((WideCfg<H, B>::NT)) void step_wide_kernel(
     const int s = u / UB, r = u % UB;
     bf16s* d = xb + s * XS;
     if constexpr (!REV) {
-      const int c = r / 4, G = r % 4;
-      bf16s* row = d + (c / C::GROW) * GS + (c % C::GROW) * HQ;
-      *reinterpret_cast<u32x2*>(row + 4 * G) = u32x2{v[0], v[1]};        // features 8G .. 8G+3
-      *reinterpret_cast<u32x2*>(row + 16 + 4 * G) = u32x2{v[2], v[3]};   // features 8G+4 .. 8G+7
+      const int c = r / (HQ / 8), G = r % (HQ / 8);
+      const int sw = wide_sw<HQ, GROW>(c);
+      const int m0 = 2 * (G / 4), w0 = 4 * (G % 4);   // tiles m0, m0 + 1 of the 32-group G / 4
+      bf16s* row = d + c * HQ;
+      *reinterpret_cast<u32x2*>(row + 16 * (m0 ^ sw) + w0) = u32x2{v[0], v[1]};         // features 8G .. 8G+3
+      *reinterpret_cast<u32x2*>(row + 16 * ((m0 + 1) ^ sw) + w0) = u32x2{v[2], v[3]};   // features 8G+4 .. 8G+7
     } else {
       const int f = 16 * (r / (16 * (B / 8))) + r % 16, c = 8 * ((r / 16) % (B / 8));
       // fragment (kk, tile) of the block: lane group c / (B/4), k step (c % (B/4)) / 8
-      const int slot = wide_slot(f), gg = c / C::GROW, kk = (c % C::GROW) / 8;
-      *reinterpret_cast<u32x4*>(d + fo<bf16s>(kk * 2 + slot / 16, slot % 16 + 16 * gg, 0)) = v;
+      const int slot = wide_slot(f), gg = c / GROW, kk = (c % GROW) / 8;
+      *reinterpret_cast<u32x4*>(d + fo<bf16s>(kk * MQ + slot / 16, slot % 16 + 16 * gg, 0)) = v;
     }
   };
   auto stage_x = [&](int qs, bf16s* xb, int u0) __attribute__((always_inline)) {
     for (int u = u0 + tid; u < C::UNITS; u += NT)
       if (unit_ok(u)) unit_store(u, xb, unit_load(u, qs));
   };
-  // Weight unit u of (slice qs, type e): output row o = u / 4, slice
-  // features 8G .. 8G + 7 (G = u % 4): one fragment vector.
-  auto w_load = [&](int u, int qs, int e) __attribute__((always_inline)) {
-    return *reinterpret_cast<const u32x4*>(Wsrc + (size_t)e * H * H + (size_t)(u / 4) * H + qs * HQ + 8 * (u % 4));
+  // Weight unit (slice qs, type e, half h2), vector u: output row o = u / 4,
+  // features qs*HQ + 32 h2 + 8G .. + 7 (G = u % 4): one fragment vector.
+  auto w_load = [&](int u, int qs, int e, int h2) __attribute__((always_inline)) {
+    return *reinterpret_cast<const u32x4*>(Wsrc + (size_t)e * H * H + (size_t)(u / 4) * H + qs * HQ + 32 * h2 +
+                                           8 * (u % 4));
   };
   auto w_store = [&](int u, bf16s* wb, const u32x4& v) __attribute__((always_inline)) {
     const int o = u / 4, G = u % 4;
@@ -209,7 +238,9 @@ __global__ __launch_bounds__((WideCfg<H, B>::NT)) void step_wide_kernel(
 
   // ---- prologue: slice 0, type 0 ----------------------------------------
   load_bits(0, cur);
-  for (int u = tid; u < H * 4; u += NT) w_store(u, ws[0], w_load(u, 0, 0));
+#pragma unroll
+  for (int h2 = 0; h2 < NH; ++h2)
+    for (int u = tid; u < H * 4; u += NT) w_store(u, ws[h2], w_load(u, 0, 0, h2));
   stage_x(0, xs[0], 0);
   __syncthreads();
 
@@ -219,19 +250,23 @@ __global__ __launch_bounds__((WideCfg<H, B>::NT)) void step_wide_kernel(
 #pragma unroll
     for (int m = 0; m < MT; ++m) acc[n][m] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  int qs = 0, e = 0;   // slice and edge type of iteration it
+  // Forward tiles: lane (p, g) reads rows 8kk + p/4 (+4) of its group's
+  // region; its swizzle is the same for every k step and both reads.
+  const int swl = wide_sw<HQ, GROW>(g * GROW + q / 4);
+  int qs = 0, e = 0;     // slice and edge type of iteration it
+  int wcur = 0;          // ring buffer of this iteration's first weight unit
   for (int it = 0; it < iters; ++it) {
     const bf16s* xb = xs[C::NXB == 2 ? (qs & 1) : 0];
-    const bf16s* wb = ws[it & 1];
     const bool more = it + 1 < iters;
     const int en = e + 1 < E ? e + 1 : 0, qn = e + 1 < E ? qs : qs + 1;
+
     // Aggregate of this wave's rows over the slice: P[n][m] = D[feature
     // slot 16m + 4g + j][row 16n + q].
-    f32x4 P[NTW][2];
+    f32x4 P[NTW][MQ];
 #pragma unroll
     for (int n = 0; n < NTW; ++n)
 #pragma unroll
-      for (int m = 0; m < 2; ++m) P[n][m] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int m = 0; m < MQ; ++m) P[n][m] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
       if (s < s_lo || s > s_hi) continue;
@@ -242,31 +277,22 @@ __global__ __launch_bounds__((WideCfg<H, B>::NT)) void step_wide_kernel(
 #pragma unroll
         for (int n = 0; n < NTW; ++n) bf[n] = wide_bits_frag(cur[s][n].byte(kk));
 #pragma unroll
-        for (int m = 0; m < 2; ++m) {
+        for (int m = 0; m < MQ; ++m) {
           bf16x8 af;
           if constexpr (!REV) {
-            af = tr_read8(xsb + g * GS + (8 * kk + q / 4) * HQ + 16 * m + 4 * (q % 4), HQ);
+            af = tr_read8(xsb + (g * GROW + 8 * kk + q / 4) * HQ + 16 * (m ^ swl) + 4 * (q % 4), HQ);
           } else {
-            af = load_fragi<bf16s>(xsb, kk * 2 + m, lane);
+            af = load_fragi<bf16s>(xsb, kk * MQ + m, lane);
           }
 #pragma unroll
           for (int n = 0; n < NTW; ++n) mma(P[n][m], af, bf[n]);
         }
       }
     }
-    // Next (slice, type): weights and bit rows; a share of the next slice's
-    // blocks (double-buffered forms).  Requested after the aggregation (its
-    // LDS reads keep many registers in flight), in flight during the
-    // transform.
-    u32x4 wreg[C::WPT];
-    if (more) {
-#pragma unroll
-      for (int i = 0; i < C::WPT; ++i) {
-        const int u = i * NT + tid;
-        if ((H * 4) % NT == 0 || u < H * 4) wreg[i] = w_load(u, qn, en);
-      }
-      load_bits(en, nxt);
-    }
+
+    // A share of the next slice's blocks (double-buffered forms), requested
+    // after the aggregation (its LDS reads keep many registers in flight)
+    // and in flight during the transform.
     const bool pre_x = C::NXB == 2 && qs + 1 < NQ;
     u32x4 xreg[C::XPT];
     if (pre_x) {
@@ -276,9 +302,8 @@ __global__ __launch_bounds__((WideCfg<H, B>::NT)) void step_wide_kernel(
         if (unit_ok(u)) xreg[i] = unit_load(u, qs + 1);
       }
     }
-
     // Per-type bias (forward, once per type): deg_e(row) b_e, added with the
-    // slice-0 transform below.
+    // first unit's products below.
     float fd[NTW];
     if constexpr (BIAS) {
       if (qs == 0) {
@@ -291,63 +316,81 @@ __global__ __launch_bounds__((WideCfg<H, B>::NT)) void step_wide_kernel(
         }
       }
     }
-    // The lane's eight consecutive slice features 8g .. 8g + 7 of row 16n + q.
-    bf16x8 pf[NP][NTW];
+
 #pragma unroll
-    for (int n = 0; n < NTW; ++n) {
-      float v8[8];
+    for (int h2 = 0; h2 < NH; ++h2) {
+      // The next slice's weight unit h2 (and, with the last unit, the next
+      // type's bit rows), in flight during this unit's products.
+      u32x4 wreg[C::WPT];
+      if (more) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        v8[j] = P[n][0][j];
-        v8[4 + j] = P[n][1][j];
+        for (int i = 0; i < C::WPT; ++i) {
+          const int u = i * NT + tid;
+          if ((H * 4) % NT == 0 || u < H * 4) wreg[i] = w_load(u, qn, en, h2);
+        }
+        if (h2 == NH - 1) load_bits(en, nxt);
       }
-      if constexpr (NP == 2) {
-        split8(v8, pf[0][n], pf[NP - 1][n]);
-      } else {
-        pf[0][n] = pack8<bf16s>(v8);
-      }
-    }
-    if constexpr (REV) {
+      // The lane's eight consecutive features 32 h2 + 8g .. + 7 of the slice,
+      // row 16n + q.
+      bf16x8 pf[NP][NTW];
 #pragma unroll
-      for (int n = 0; n < NTW; ++n)
-        *reinterpret_cast<u32x4*>(dM + ((size_t)e * ldm + (size_t)k * B + rw + 16 * n + q) * H + qs * HQ + 8 * g) =
-            __builtin_bit_cast(u32x4, pf[0][n]);
-    }
-    // Transform: acc[n][mo] += W^T rows 16mo.. (slice features) x aggregate.
+      for (int n = 0; n < NTW; ++n) {
+        float v8[8];
 #pragma unroll
-    for (int mo = 0; mo < MT; ++mo) {
-      const bf16x8 wf = load_fragi<bf16s>(wb, mo, lane);
-#pragma unroll
-      for (int n = 0; n < NTW; ++n)
-#pragma unroll
-        for (int part = 0; part < NP; ++part) mma(acc[n][mo], wf, pf[part][n]);
-      if constexpr (BIAS) {
-        if (qs == 0) {
-          const f32x4 b4 = *reinterpret_cast<const f32x4*>(bias + (size_t)e * H + 16 * mo + 4 * g);
-#pragma unroll
-          for (int n = 0; n < NTW; ++n)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) acc[n][mo][j] += fd[n] * b4[j];
+        for (int j = 0; j < 4; ++j) {
+          v8[j] = P[n][2 * h2][j];
+          v8[4 + j] = P[n][2 * h2 + 1][j];
+        }
+        if constexpr (NP == 2) {
+          split8(v8, pf[0][n], pf[NP - 1][n]);
+        } else {
+          pf[0][n] = pack8<bf16s>(v8);
         }
       }
-    }
-
-    // Hand the prefetched operands to the other buffers.
-    if (more) {
+      if constexpr (REV) {
 #pragma unroll
-      for (int i = 0; i < C::WPT; ++i) {
-        const int u = i * NT + tid;
-        if ((H * 4) % NT == 0 || u < H * 4) w_store(u, ws[(it + 1) & 1], wreg[i]);
+        for (int n = 0; n < NTW; ++n)
+          *reinterpret_cast<u32x4*>(dM + ((size_t)e * ldm + (size_t)k * B + rw + 16 * n + q) * H + qs * HQ +
+                                    32 * h2 + 8 * g) = __builtin_bit_cast(u32x4, pf[0][n]);
       }
-    }
-    if (pre_x) {
+      // Transform: acc[n][mo] += (W^T rows 16mo.., features of the unit) x aggregate.
+      const int wb = (wcur + h2) % NWB;
 #pragma unroll
-      for (int i = 0; i < C::XPT; ++i) {
-        const int u = (e * C::XPT + i) * NT + tid;
-        if (unit_ok(u)) unit_store(u, xs[(qs + 1) & 1], xreg[i]);
+      for (int mo = 0; mo < MT; ++mo) {
+        const bf16x8 wf = load_fragi<bf16s>(ws[wb], mo, lane);
+#pragma unroll
+        for (int n = 0; n < NTW; ++n)
+#pragma unroll
+          for (int part = 0; part < NP; ++part) mma(acc[n][mo], wf, pf[part][n]);
+        if constexpr (BIAS) {
+          if (qs == 0 && h2 == 0) {
+            const f32x4 b4 = *reinterpret_cast<const f32x4*>(bias + (size_t)e * H + 16 * mo + 4 * g);
+#pragma unroll
+            for (int n = 0; n < NTW; ++n)
+#pragma unroll
+              for (int j = 0; j < 4; ++j) acc[n][mo][j] += fd[n] * b4[j];
+          }
+        }
       }
+      // The next slice's unit h2 goes to the buffer the previous unit used
+      // (every wave is past that unit's barrier).
+      if (more) {
+        bf16s* wn = ws[(wcur + NH + h2) % NWB];
+#pragma unroll
+        for (int i = 0; i < C::WPT; ++i) {
+          const int u = i * NT + tid;
+          if ((H * 4) % NT == 0 || u < H * 4) w_store(u, wn, wreg[i]);
+        }
+      }
+      if (h2 == NH - 1 && pre_x) {
+#pragma unroll
+        for (int i = 0; i < C::XPT; ++i) {
+          const int u = (e * C::XPT + i) * NT + tid;
+          if (unit_ok(u)) unit_store(u, xs[(qs + 1) & 1], xreg[i]);
+        }
+      }
+      __syncthreads();
     }
-    __syncthreads();
     if (e == E - 1 && qs + 1 < NQ) {
       // Units of the next slice not prefetched above (all of them with a
       // single buffer): staged now that every wave is done with this slice.
@@ -365,6 +408,7 @@ __global__ __launch_bounds__((WideCfg<H, B>::NT)) void step_wide_kernel(
     }
     qs = qn;
     e = en;
+    wcur = (wcur + NH) % NWB;
   }
 
   // Output rows: lane (q, g) holds features 16m + 4g .. + 3 of row 16n + q.
@@ -389,7 +433,7 @@ namespace {
 template <int H, int B>
 hipError_t wide_launch(bool rev, int n_pad, int E, const void* bits, const void* V, const void* Wsrc,
                        const float* bias, float* out, const float* dX_in, void* dM, long ldm, hipStream_t st) {
-  using C = dev::WideCfg<H, B>;
+  using C = dev::WideCfg<H, B, false>;   // R and NT do not depend on the direction
   const int blocks = (n_pad / B) * (B / C::R);
   const uint8_t* bp = static_cast<const uint8_t*>(bits);
   const dev::bf16s* vp = static_cast<const dev::bf16s*>(V);
