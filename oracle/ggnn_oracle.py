@@ -361,3 +361,92 @@ def propagate(n: int, B: int, src, dst, etype, X0, W, Wi, U, b, T: int, G=None, 
         db += db_t
     out.update(dX0=g, dW=dW, dbias=dbias, dWi=dWi, dU=dU, db=db, dX=dXs)
     return out
+
+
+# ----------------------------------------------------------------------------
+# Readout, loss and the parameter update closing one training step
+# ----------------------------------------------------------------------------
+
+def readout_logits(XT, w_out, b_out, cand_node):
+    """Per-candidate logits: a learned linear map R^H -> R applied to the
+    final embeddings of the candidate nodes (Background, "Variable misuse").
+    Returns logits[c] = XT[cand_node[c]] . w_out + b_out."""
+    XT = np.asarray(XT, np.float64)
+    return XT[np.asarray(cand_node, np.int64)] @ np.asarray(w_out, np.float64) + float(b_out)
+
+
+def readout_loss(logits, cand_ptr, target):
+    """Softmax over each graph's candidates (Background, "Variable misuse":
+    the softmax gives the probability of each candidate filling the hole) and
+    the cross-entropy of the correct one.  Graph g owns candidates
+    cand_ptr[g] .. cand_ptr[g+1]-1, target[g] is the index of the correct one
+    within them.  Reading: the training loss is the mean over graphs.
+    Returns (loss per graph [G], mean loss, dlogits = d mean / d logits).
+    A graph without candidates contributes loss 0 and no gradient."""
+    logits = np.asarray(logits, np.float64)
+    ptr = np.asarray(cand_ptr, np.int64)
+    G = len(ptr) - 1
+    loss = np.zeros(G)
+    dlog = np.zeros_like(logits)
+    for g in range(G):
+        lo, hi = ptr[g], ptr[g + 1]
+        if hi == lo:
+            continue
+        z = logits[lo:hi]
+        p = np.exp(z - z.max())
+        p /= p.sum()
+        loss[g] = -np.log(p[target[g]])
+        onehot = np.zeros(hi - lo)
+        onehot[target[g]] = 1.0
+        dlog[lo:hi] = (p - onehot) / G
+    return loss, float(loss.mean()), dlog
+
+
+def readout_backward(XT, w_out, cand_node, dlogits):
+    """Reverse of readout_logits: dXT (zero except candidate rows),
+    dw_out = sum_c dlogits[c] XT[cand_node[c]], db_out = sum_c dlogits[c]."""
+    XT = np.asarray(XT, np.float64)
+    cand = np.asarray(cand_node, np.int64)
+    dl = np.asarray(dlogits, np.float64)
+    dXT = np.zeros_like(XT)
+    np.add.at(dXT, cand, dl[:, None] * np.asarray(w_out, np.float64)[None, :])
+    return dXT, XT[cand].T @ dl, float(dl.sum())
+
+
+def momentum_update(theta, velocity, grad, lr, momentum, weight_decay=0.0, nesterov=False):
+    """One step of the Momentum optimizer (Appendix, "Optimization": momentum,
+    optionally Nesterov, with L2 weight decay):
+        g' = grad + weight_decay * theta
+        v  = momentum * v + g'
+        theta -= lr * (g' + momentum * v)   (Nesterov)   or   lr * v
+    Returns (theta, v)."""
+    theta = np.asarray(theta, np.float64)
+    g = np.asarray(grad, np.float64) + weight_decay * theta
+    v = momentum * np.asarray(velocity, np.float64) + g
+    step = g + momentum * v if nesterov else v
+    return theta - lr * step, v
+
+
+def train_step(n: int, B: int, src, dst, etype, X0, params: dict, velocity: dict, T: int,
+               cand_node, cand_ptr, target, lr, momentum, weight_decay=0.0, nesterov=False):
+    """One training step (Background: propagation, then the readout and the
+    softmax loss; Appendix, "Optimization": the Momentum update of every
+    parameter).  params holds W, bias (or None), Wi, U, b, w_out, b_out;
+    velocity the same keys.  Returns (new params, new velocity, mean loss,
+    gradients)."""
+    bias = params.get("bias")
+    out = propagate(n, B, src, dst, etype, X0, params["W"], params["Wi"], params["U"], params["b"], T, bias=bias)
+    XT = out["X"][T]
+    logits = readout_logits(XT, params["w_out"], params["b_out"], cand_node)
+    _, mean_loss, dlog = readout_loss(logits, cand_ptr, target)
+    dXT, dw_out, db_out = readout_backward(XT, params["w_out"], cand_node, dlog)
+    rev = propagate(n, B, src, dst, etype, X0, params["W"], params["Wi"], params["U"], params["b"], T, G=dXT,
+                    bias=bias)
+    grads = {"W": rev["dW"], "Wi": rev["dWi"], "U": rev["dU"], "b": rev["db"], "w_out": dw_out,
+             "b_out": np.float64(db_out)}
+    if bias is not None:
+        grads["bias"] = rev["dbias"]
+    new_p, new_v = dict(params), dict(velocity)
+    for k, g in grads.items():
+        new_p[k], new_v[k] = momentum_update(params[k], velocity[k], g, lr, momentum, weight_decay, nesterov)
+    return new_p, new_v, mean_loss, grads
