@@ -77,6 +77,8 @@ def parse():
                    help="band storage: 1 bit per entry (aggregate-first fused forward) or dense in the compute dtype")
     p.add_argument("--kernel-reps", type=int, default=50, help="launches per kernel for the roofline timing")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-train", action="store_true",
+                   help="skip the timing of one training step (readout, loss and Momentum update included)")
     p.add_argument("--eager", action="store_true", help="time eager launches only (no HIP graph replay)")
     p.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="summarise two rocprofv3 --pmc counter files (FETCH_SIZE, WRITE_SIZE) of this command "
@@ -299,6 +301,18 @@ def main():
     sec_per_step = graph_s if use_graph else eager_s
     value = comp.n_real * spec.T / sec_per_step
 
+    # One whole training step timed the same way (eager launches): the
+    # propagation step above, then the readout and softmax loss over seeded
+    # candidate sets, the readout's reverse, and the Momentum update of every
+    # parameter.  Reported beside the propagation figure, not as `value`.
+    train_s = None
+    if not args.no_train:
+        from ggnn_synth import draw_candidates, draw_readout
+        cands = draw_candidates(spec.cfg, comp.offsets)
+        w_out, b_out = draw_readout(spec.cfg, spec.H)
+        m.setup_training(cands, w_out, b_out, lr=1e-3, momentum=0.9)
+        train_s = timed(m.train_step)
+
     # Roofline of the banded kernels: each launch timed with HIP events on the
     # stream it runs on, in the same launch shape as inside the step.
     es = 2 if spec.dtype == "bf16" else 4
@@ -373,6 +387,7 @@ def main():
                    "timing": "hip_graph_replay" if use_graph else "eager",
                    "ms_per_step_eager": round(eager_s * 1e3, 4),
                    "ms_per_step_graph": None if graph_s is None else round(graph_s * 1e3, 4),
+                   "ms_per_train_step": None if train_s is None else round(train_s * 1e3, 4),
                    "host_compile_s": round(comp.rcm_seconds + comp.stats.get("pack_seconds", 0.0), 3),
                    "generate_s": round(gen_s, 3)},
         "roofline": roofline,

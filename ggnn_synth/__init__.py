@@ -11,3 +11,4 @@ from .graphs import (  # noqa: F401
 )
 from .params import draw_params, round_bf16, Params  # noqa: F401
 from .configs import CONFIGS, ConfigSpec, make_graphs, sweep_blocks  # noqa: F401
+from .readout import Candidates, draw_candidates, draw_readout, STREAM_CAND  # noqa: F401

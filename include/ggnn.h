@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define GGNN_ABI_VERSION 6
+#define GGNN_ABI_VERSION 7
 
 typedef enum {
   GGNN_OK = 0,
@@ -369,6 +369,60 @@ ggnn_status ggnn_forward(const ggnn_model* model, const ggnn_activations* act, v
  * Needs the activations of a preceding ggnn_forward. */
 ggnn_status ggnn_backward(const ggnn_model* model, const ggnn_activations* act,
                           const ggnn_grads* grads, void* stream);
+
+/* ---- Closing one training step: readout, loss, parameter update ----------
+ *
+ * Readout and loss (Background, "Variable misuse"): a learned linear map
+ * R^H -> R applied to the final embedding of each candidate node gives its
+ * logit; a softmax over each graph's candidates gives the probability of
+ * each filling the hole, and the loss is the cross-entropy of the correct
+ * candidate, averaged over the graphs of the supergraph:
+ *   logits[c] = X[cand_node[c]] . w_out + b_out
+ *   loss[g]   = log sum_{c in g} exp(logits[c]) - logits[cand_ptr[g] + target[g]]
+ *   dlogit[c] = (softmax_g(logits)[c] - [c is the target of g]) / n_graphs
+ * Candidate lists: graph g owns candidates cand_ptr[g] .. cand_ptr[g+1]-1
+ * (cand_ptr [n_graphs + 1] int32, non-decreasing, cand_ptr[n_graphs] =
+ * n_cand), candidate c is node cand_node[c] ([n_cand] int32, < n_pad),
+ * target[g] ([n_graphs] int32) indexes the graph's own list.  A graph without
+ * candidates gets loss 0; a target outside the graph's list gives loss NaN.
+ * All of these arrays are device memory.
+ *   X [n_pad][H] dt (the final states X_T);  w_out [H] float;  b_out [1] float
+ *   logits, dlogit [n_cand] float (written);  loss [n_graphs] float (written) */
+ggnn_status ggnn_readout_loss(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t n_graphs, int32_t n_cand,
+                              const void* X, const float* w_out, const float* b_out, const int32_t* cand_node,
+                              const int32_t* cand_ptr, const int32_t* target, float* logits, float* loss,
+                              float* dlogit, void* stream);
+
+/* Workspace bytes of ggnn_readout_loss_bwd (0 for unsupported sizes). */
+size_t ggnn_readout_loss_bwd_workspace_bytes(int32_t H, int32_t n_cand);
+
+/* Reverse of the readout for the upstream gradients dlogit (of
+ * ggnn_readout_loss):
+ *   dX [n_pad][H] float (written whole: dlogit[c] * w_out on the row of each
+ *      candidate, zero elsewhere) -- the dL/dX_T that ggnn_backward takes
+ *   dw_out [H] float += sum_c dlogit[c] X[cand_node[c]];  db_out [1] float += sum_c dlogit[c]
+ * A node may be the candidate of at most one graph, once (otherwise its dX
+ * row holds one of the contributions).  workspace: 16-byte aligned, at least
+ * ggnn_readout_loss_bwd_workspace_bytes(H, n_cand) bytes (per-block partial
+ * sums, reduced in a fixed order). */
+ggnn_status ggnn_readout_loss_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t n_cand, const void* X,
+                                  const float* w_out, const int32_t* cand_node, const float* dlogit, float* dX,
+                                  float* dw_out, float* db_out, void* workspace, size_t workspace_bytes,
+                                  void* stream);
+
+/* One Momentum-optimizer step (Appendix, "Optimization": Momentum, with
+ * Nesterov momentum and L2 weight decay as options) on count float32 master
+ * parameters, element-wise:
+ *   g = grad + weight_decay * param;  velocity = momentum * velocity + g;
+ *   param -= lr * (nesterov ? g + momentum * velocity : velocity)
+ * param, velocity [count] float (updated in place); grad [count] float.
+ * param_copy: NULL, or a [count] tensor of copy_dtype rewritten from the new
+ * param (round to nearest even for bf16) -- the compute copy that the
+ * propagation reads.  The four buffers must not overlap.  momentum and
+ * weight_decay must be >= 0; all three scalars finite. */
+ggnn_status ggnn_sgd_momentum(int64_t count, float* param, float* velocity, const float* grad, float lr,
+                              float momentum, float weight_decay, int32_t nesterov, ggnn_dtype copy_dtype,
+                              void* param_copy, void* stream);
 
 #ifdef __cplusplus
 }

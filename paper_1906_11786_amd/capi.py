@@ -35,6 +35,7 @@ EXPORTS = [
     "ggnn_gru_update_bwd_workspace_bytes", "ggnn_gru_update_bwd",
     "ggnn_banded_propagate_bwd", "ggnn_msg_transform_bwd_workspace_bytes", "ggnn_msg_transform_bwd",
     "ggnn_backward_workspace_bytes", "ggnn_forward", "ggnn_backward",
+    "ggnn_readout_loss", "ggnn_readout_loss_bwd_workspace_bytes", "ggnn_readout_loss_bwd", "ggnn_sgd_momentum",
 ]
 
 
@@ -95,6 +96,10 @@ _SIGS = {
     "ggnn_backward_workspace_bytes": (sz, [C.POINTER(ggnn_model)]),
     "ggnn_forward": (C.c_int, [C.POINTER(ggnn_model), C.POINTER(ggnn_activations), vp]),
     "ggnn_backward": (C.c_int, [C.POINTER(ggnn_model), C.POINTER(ggnn_activations), C.POINTER(ggnn_grads), vp]),
+    "ggnn_readout_loss": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+    "ggnn_readout_loss_bwd_workspace_bytes": (sz, [i32, i32]),
+    "ggnn_readout_loss_bwd": (C.c_int, [C.c_int, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+    "ggnn_sgd_momentum": (C.c_int, [i64, vp, vp, vp, C.c_float, C.c_float, C.c_float, i32, C.c_int, vp, vp]),
 }
 
 
@@ -309,3 +314,30 @@ def ggnn_forward(model: ggnn_model, act: ggnn_activations, stream=None):
 
 def ggnn_backward(model: ggnn_model, act: ggnn_activations, grads: ggnn_grads, stream=None):
     _check("ggnn_backward", lib().ggnn_backward(C.byref(model), C.byref(act), C.byref(grads), _stream(stream)))
+
+
+# ------------------------------------------- readout, loss, parameter update
+
+def ggnn_readout_loss(dt, n_pad, H, n_graphs, n_cand, X, w_out, b_out, cand_node, cand_ptr, target, logits, loss,
+                      dlogit, stream=None):
+    _check("ggnn_readout_loss", lib().ggnn_readout_loss(
+        _dt(dt), n_pad, H, n_graphs, n_cand, _ptr(X), _ptr(w_out), _ptr(b_out), _ptr(cand_node), _ptr(cand_ptr),
+        _ptr(target), _ptr(logits), _ptr(loss), _ptr(dlogit), _stream(stream)))
+
+
+def ggnn_readout_loss_bwd_workspace_bytes(H, n_cand) -> int:
+    return int(lib().ggnn_readout_loss_bwd_workspace_bytes(H, n_cand))
+
+
+def ggnn_readout_loss_bwd(dt, n_pad, H, n_cand, X, w_out, cand_node, dlogit, dX, dw_out, db_out, workspace,
+                          workspace_bytes, stream=None):
+    _check("ggnn_readout_loss_bwd", lib().ggnn_readout_loss_bwd(
+        _dt(dt), n_pad, H, n_cand, _ptr(X), _ptr(w_out), _ptr(cand_node), _ptr(dlogit), _ptr(dX), _ptr(dw_out),
+        _ptr(db_out), _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def ggnn_sgd_momentum(count, param, velocity, grad, lr, momentum, weight_decay=0.0, nesterov=False,
+                      copy_dtype="f32", param_copy=None, stream=None):
+    _check("ggnn_sgd_momentum", lib().ggnn_sgd_momentum(
+        count, _ptr(param), _ptr(velocity), _ptr(grad), lr, momentum, weight_decay, 1 if nesterov else 0,
+        _dt(copy_dtype), _ptr(param_copy), _stream(stream)))

@@ -3,6 +3,8 @@
 // Eq. 1 (forward with stored activations, then the reverse pass).
 #include <hip/hip_runtime.h>
 
+#include <cmath>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -452,6 +454,86 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
               ? launch_transform_wgrad_nm(m->dtype, K, m->H, m->E, act->X, gr->dM, K, gr->dW, dbias, ws + L.tr_part, s)
               : launch_transform_wgrad(m->dtype, K, m->H, m->E, act->X, gr->dM, K, gr->dW, dbias, ws + L.tr_part, s);
   return device_status(err, "backward");
+}
+
+ggnn_status ggnn_readout_loss(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t n_graphs, int32_t n_cand,
+                              const void* X, const float* w_out, const float* b_out, const int32_t* cand_node,
+                              const int32_t* cand_ptr, const int32_t* target, float* logits, float* loss,
+                              float* dlogit, void* stream) {
+  clear_error();
+  ggnn_status st = check_common(dt, n_pad, H);
+  if (st != GGNN_OK) return st;
+  GGNN_CHECK_ARG(n_graphs >= 1, "n_graphs=%d must be at least 1", n_graphs);
+  GGNN_CHECK_ARG(n_cand >= 0, "n_cand=%d must not be negative", n_cand);
+  CHECK_PTR(X, "X");
+  CHECK_PTR(w_out, "w_out");
+  CHECK_PTR(b_out, "b_out");
+  CHECK_PTR(cand_ptr, "cand_ptr");
+  CHECK_PTR(target, "target");
+  CHECK_PTR(loss, "loss");
+  if (n_cand > 0) {
+    CHECK_PTR(cand_node, "cand_node");
+    CHECK_PTR(logits, "logits");
+    CHECK_PTR(dlogit, "dlogit");
+  }
+  return device_status(launch_readout_loss(dt, H, n_graphs, X, w_out, b_out, cand_node, cand_ptr, target, logits,
+                                           loss, dlogit, as_stream(stream)),
+                       "readout_loss");
+}
+
+size_t ggnn_readout_loss_bwd_workspace_bytes(int32_t H, int32_t n_cand) {
+  if (!supported_H(H) || n_cand < 0) return 0;
+  return readout_bwd_workspace(H, n_cand);
+}
+
+ggnn_status ggnn_readout_loss_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t n_cand, const void* X,
+                                  const float* w_out, const int32_t* cand_node, const float* dlogit, float* dX,
+                                  float* dw_out, float* db_out, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+  clear_error();
+  ggnn_status st = check_common(dt, n_pad, H);
+  if (st != GGNN_OK) return st;
+  GGNN_CHECK_ARG(n_cand >= 0, "n_cand=%d must not be negative", n_cand);
+  CHECK_PTR(X, "X");
+  CHECK_PTR(w_out, "w_out");
+  CHECK_PTR(dX, "dX");
+  CHECK_PTR(dw_out, "dw_out");
+  CHECK_PTR(db_out, "db_out");
+  if (n_cand > 0) {
+    CHECK_PTR(cand_node, "cand_node");
+    CHECK_PTR(dlogit, "dlogit");
+  }
+  const size_t need = readout_bwd_workspace(H, n_cand);
+  if (workspace == nullptr || workspace_bytes < need || !aligned16(workspace))
+    return fail(GGNN_ERR_WORKSPACE, "readout_loss_bwd needs a 16-byte aligned workspace of %zu bytes (got %zu)",
+                need, workspace ? workspace_bytes : (size_t)0);
+  return device_status(launch_readout_bwd(dt, n_pad, H, n_cand, X, w_out, cand_node, dlogit, dX, dw_out, db_out,
+                                          workspace, as_stream(stream)),
+                       "readout_loss_bwd");
+}
+
+ggnn_status ggnn_sgd_momentum(int64_t count, float* param, float* velocity, const float* grad, float lr,
+                              float momentum, float weight_decay, int32_t nesterov, ggnn_dtype copy_dtype,
+                              void* param_copy, void* stream) {
+  clear_error();
+  GGNN_CHECK_ARG(count >= 0, "count=%lld must not be negative", (long long)count);
+  GGNN_CHECK_ARG(std::isfinite(lr) && std::isfinite(momentum) && std::isfinite(weight_decay),
+                 "lr, momentum and weight_decay must be finite");
+  GGNN_CHECK_ARG(momentum >= 0.f && weight_decay >= 0.f, "momentum and weight_decay must not be negative");
+  if (count == 0) return GGNN_OK;
+  CHECK_PTR(param, "param");
+  CHECK_PTR(velocity, "velocity");
+  CHECK_PTR(grad, "grad");
+  CHECK_OPT_PTR(param_copy, "param_copy");
+  if (param_copy != nullptr) {
+    GGNN_CHECK_ARG(supported_dtype(copy_dtype), "unknown copy dtype %d", copy_dtype);
+    GGNN_CHECK_ARG(param_copy != param, "param_copy must not be param");
+  }
+  GGNN_CHECK_ARG(velocity != param && grad != param && grad != velocity,
+                 "param, velocity and grad must be distinct buffers");
+  return device_status(launch_sgd_momentum(count, param, velocity, grad, lr, momentum, weight_decay,
+                                           nesterov != 0, copy_dtype, param_copy, as_stream(stream)),
+                       "sgd_momentum");
 }
 
 }  // extern "C"

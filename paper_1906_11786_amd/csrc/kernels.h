@@ -52,6 +52,12 @@ namespace ggnn {
                                   hipStream_t st);                                                                \
   hipError_t launch_gru_wgrad(long K, int H, const float* a, const void* h, const void* saved, const void* ghat,  \
                               float* dWi, float* dU, float* db, void* ws, hipStream_t st);                       \
+  hipError_t launch_readout_loss(int H, int n_graphs, const void* X, const float* w_out, const float* b_out,      \
+                                 const int32_t* cand_node, const int32_t* cand_ptr, const int32_t* target,       \
+                                 float* logits, float* loss, float* dlogit, hipStream_t st);                     \
+  hipError_t launch_readout_bwd(int n_pad, int H, int n_cand, const void* X, const float* w_out,                 \
+                                const int32_t* cand_node, const float* dlogit, float* dX, float* dw_out,         \
+                                float* db_out, void* ws, hipStream_t st);                                        \
   bool step_wide_applies(int B, int H);                                                                           \
   hipError_t launch_step_wide(bool rev, int n_pad, int B, int H, int E, const void* bits, const void* V,          \
                               const void* Wsrc, const float* bias, float* out, const float* dX_in, void* dM,      \
@@ -190,6 +196,26 @@ size_t gru_bwd_workspace(int dt, int n_pad, int H);
 hipError_t launch_gru_bwd(int dt, int n_pad, int H, const float* dh_out, const float* a, const void* h,
                           const void* saved, const void* Wi, const void* U, void* da, float* dh, float* dWi,
                           float* dU, float* db, void* ws, hipStream_t st);
+
+// Readout and loss (candidate logits, per-graph softmax cross-entropy, mean
+// over graphs) and their reverse: dX (written whole), dw_out and db_out
+// (accumulated; partials in readout_bwd_workspace bytes, fixed order).
+inline hipError_t launch_readout_loss(int dt, int H, int n_graphs, const void* X, const float* w_out,
+                                      const float* b_out, const int32_t* cand_node, const int32_t* cand_ptr,
+                                      const int32_t* target, float* logits, float* loss, float* dlogit,
+                                      hipStream_t st) {
+  return GGNN_DT_PICK(launch_readout_loss, H, n_graphs, X, w_out, b_out, cand_node, cand_ptr, target, logits, loss,
+                      dlogit, st);
+}
+size_t readout_bwd_workspace(int H, int n_cand);
+inline hipError_t launch_readout_bwd(int dt, int n_pad, int H, int n_cand, const void* X, const float* w_out,
+                                     const int32_t* cand_node, const float* dlogit, float* dX, float* dw_out,
+                                     float* db_out, void* ws, hipStream_t st) {
+  return GGNN_DT_PICK(launch_readout_bwd, n_pad, H, n_cand, X, w_out, cand_node, dlogit, dX, dw_out, db_out, ws, st);
+}
+// Momentum update of float32 master parameters (and their compute copy).
+hipError_t launch_sgd_momentum(long count, float* theta, float* vel, const float* grad, float lr, float mu, float wd,
+                               int nesterov, int copy_dt, void* copy, hipStream_t st);
 
 #undef GGNN_DT_PICK
 

@@ -127,8 +127,9 @@ class BandedGGNN:
         self.G = torch.from_numpy(params.G.astype(np.float32)).to(device)
         self.dX = torch.empty((n_pad, H), dtype=torch.float32, device=device)
         # All weight gradients in one buffer (one fill clears them), each
-        # view starting on a 64-float boundary.
-        sizes = [E * H * H, E * H, H * 3 * H, H * 3 * H, 3 * H]
+        # view starting on a 64-float boundary; the last two are the readout's
+        # (w_out, b_out), used by train_step().
+        sizes = [E * H * H, E * H, H * 3 * H, H * 3 * H, 3 * H, H, 1]
         offs = [0]
         for s_ in sizes:
             offs.append(offs[-1] + -(-s_ // 64) * 64)
@@ -139,6 +140,8 @@ class BandedGGNN:
         self.dWi = views[2].view(H, 3 * H)
         self.dU = views[3].view(H, 3 * H)
         self.db = views[4]
+        self.dw_out = views[5]
+        self.db_out = views[6]
         self.da = torch.empty((H, n_pad), dtype=td, device=device)
         self.dM = torch.empty((E, H, T * n_pad), dtype=td, device=device)
         self.dh = torch.empty((n_pad, H), dtype=torch.float32, device=device)
@@ -201,6 +204,70 @@ class BandedGGNN:
     def replay(self):
         """One step() through the captured graph (capture() first)."""
         self.graph.replay()
+
+    # ------------------------------------------------------------ training
+
+    def setup_training(self, cands, w_out, b_out: float, lr: float = 0.01, momentum: float = 0.9,
+                       weight_decay: float = 0.0, nesterov: bool = False):
+        """Readout inputs and optimizer state for train_step(): candidate
+        lists (ggnn_synth.Candidates layout, supergraph node ids), the readout
+        parameters, float32 master copies of the parameters the propagation
+        reads in bf16, and zero velocities."""
+        torch = self.torch
+        dev = self.device
+        self.cand_node = torch.from_numpy(np.ascontiguousarray(cands.node, np.int32)).to(dev)
+        self.cand_ptr = torch.from_numpy(np.ascontiguousarray(cands.ptr, np.int32)).to(dev)
+        self.target = torch.from_numpy(np.ascontiguousarray(cands.target, np.int32)).to(dev)
+        self.n_graphs = len(cands.ptr) - 1
+        self.n_cand = int(cands.ptr[-1])
+        self.w_out = torch.from_numpy(np.asarray(w_out, np.float32)).to(dev)
+        self.b_out = torch.tensor([b_out], dtype=torch.float32, device=dev)
+        self.logits = torch.empty((max(self.n_cand, 1),), dtype=torch.float32, device=dev)
+        self.dlogit = torch.empty_like(self.logits)
+        self.loss = torch.empty((self.n_graphs,), dtype=torch.float32, device=dev)
+        ws = capi.ggnn_readout_loss_bwd_workspace_bytes(self.H, self.n_cand)
+        self.readout_ws = torch.empty((max(ws, 16),), dtype=torch.uint8, device=dev)
+        self.opt = dict(lr=lr, momentum=momentum, weight_decay=weight_decay, nesterov=nesterov)
+        # (master float32, velocity, gradient, compute copy or None)
+        bf = self.dt == "bf16"
+        entries = [(self.W, self.dW), (self.Wi, self.dWi), (self.U, self.dU), (self.b, self.db),
+                   (self.w_out, self.dw_out), (self.b_out, self.db_out)]
+        if self.bias is not None:
+            entries.append((self.bias, self.dbias))
+        self.param_state = []
+        for t, g in entries:
+            copy = t if (bf and t.dtype != torch.float32) else None
+            master = t.float().clone() if copy is not None else t
+            self.param_state.append((master, torch.zeros_like(master), g, copy))
+
+    def readout(self, stream=None):
+        """Logits, per-graph losses and d(mean loss)/d(logits) of X_T."""
+        capi.ggnn_readout_loss(self.dt, self.comp.n_pad, self.H, self.n_graphs, self.n_cand, self.X[self.T],
+                               self.w_out, self.b_out, self.cand_node, self.cand_ptr, self.target, self.logits,
+                               self.loss, self.dlogit, stream)
+
+    def train_step(self, stream=None):
+        """One training step: T forward steps, readout and loss, the reverse
+        pass from dL/dX_T of the readout, and the Momentum update of every
+        parameter (W_e^T refreshed from the updated W)."""
+        self.forward(stream)
+        self.readout(stream)
+        self.grad_buf.zero_()
+        capi.ggnn_readout_loss_bwd(self.dt, self.comp.n_pad, self.H, self.n_cand, self.X[self.T], self.w_out,
+                                   self.cand_node, self.dlogit, self.dX, self.dw_out, self.db_out, self.readout_ws,
+                                   self.readout_ws.numel(), stream)
+        capi.ggnn_backward(self.model, self.act, self.grads, stream)
+        o = self.opt
+        for master, vel, g, copy in self.param_state:
+            capi.ggnn_sgd_momentum(master.numel(), master, vel, g, o["lr"], o["momentum"], o["weight_decay"],
+                                   o["nesterov"], self.dt, copy, stream)
+        self.refresh_weights(stream)
+
+    def parameters(self) -> dict:
+        """Host copies (float64) of the float32 master parameters."""
+        f = (lambda t: t.float().cpu().numpy().astype(np.float64))
+        names = ["W", "Wi", "U", "b", "w_out", "b_out"] + (["bias"] if self.bias is not None else [])
+        return {n: f(st[0]) for n, st in zip(names, self.param_state)}
 
     def results(self) -> dict:
         """Host copies (float64) of the outputs compared against the oracle."""

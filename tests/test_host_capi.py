@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
     for name in declared:
         assert hasattr(L, name), name
     assert set(declared) == set(capi.EXPORTS)
-    assert capi.ggnn_abi_version() == 6
+    assert capi.ggnn_abi_version() == 7
     assert capi.ggnn_status_string(3) == "GGNN_ERR_OUT_OF_BAND"
 
 
@@ -159,6 +159,36 @@ def test_device_entry_points_validate_before_touching_the_gpu():
     assert capi.ggnn_gru_update_bwd_workspace_bytes("bf16", 20096, 64) > 0
     assert capi.ggnn_msg_transform_bwd_workspace_bytes("bf16", 20096, 64, 10) > 0
     assert capi.ggnn_msg_transform_bwd_workspace_bytes("bf16", 20096, 48, 10) == 0
+
+
+def test_training_entry_points_validate_before_touching_the_gpu():
+    """Readout, loss and Momentum update reject bad arguments on the host."""
+    _need_lib()
+    P = 16   # a 16-byte aligned stand-in address; nothing is launched
+    bad_readout = [
+        dict(n_graphs=0), dict(n_cand=-1), dict(H=48), dict(X=None), dict(cand_ptr=None), dict(loss=8),
+    ]
+    for over in bad_readout:
+        kw = dict(dt="bf16", n_pad=128, H=64, n_graphs=2, n_cand=4, X=P, w_out=P, b_out=P, cand_node=P, cand_ptr=P,
+                  target=P, logits=P, loss=P, dlogit=P)
+        kw.update(over)
+        with pytest.raises(capi.GGNNError) as ei:
+            capi.ggnn_readout_loss(**kw, stream=0)
+        assert ei.value.status_name == "GGNN_ERR_INVALID_ARG", over
+    need = capi.ggnn_readout_loss_bwd_workspace_bytes(64, 1000)
+    assert need == 16 * 65 * 4   # one partial row of H + 1 floats per block of 64 candidates
+    assert capi.ggnn_readout_loss_bwd_workspace_bytes(48, 10) == 0
+    with pytest.raises(capi.GGNNError) as ei:
+        capi.ggnn_readout_loss_bwd("bf16", 128, 64, 1000, P, P, P, P, P, P, P, P, need - 4, stream=0)
+    assert ei.value.status_name == "GGNN_ERR_WORKSPACE"
+    for args in [dict(count=-1), dict(momentum=-0.5), dict(weight_decay=-1.0), dict(lr=float("nan")),
+                 dict(param=None), dict(velocity=P, param=P), dict(param_copy=P, param=P)]:
+        kw = dict(count=10, param=P, velocity=32, grad=48, lr=0.1, momentum=0.9)
+        kw.update(args)
+        with pytest.raises(capi.GGNNError) as ei:
+            capi.ggnn_sgd_momentum(**kw, stream=0)
+        assert ei.value.status_name == "GGNN_ERR_INVALID_ARG", args
+    capi.ggnn_sgd_momentum(0, None, None, None, 0.1, 0.9, stream=0)   # nothing to do: OK
 
 
 def _unpack_bits(bits):
