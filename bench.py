@@ -305,13 +305,18 @@ def main():
     # propagation step above, then the readout and softmax loss over seeded
     # candidate sets, the readout's reverse, and the Momentum update of every
     # parameter.  Reported beside the propagation figure, not as `value`.
-    train_s = None
+    train_s = eval_band_s = eval_sparse_s = None
     if not args.no_train:
         from ggnn_synth import draw_candidates, draw_readout
         cands = draw_candidates(spec.cfg, comp.offsets)
         w_out, b_out = draw_readout(spec.cfg, spec.H)
         m.setup_training(cands, w_out, b_out, lr=1e-3, momentum=0.9)
         train_s = timed(m.train_step)
+        # Evaluation of the same parameters: T forward steps and the readout,
+        # on the band, and along every edge through the sparse path.
+        m.setup_sparse(comp.src, comp.dst, comp.etype)
+        eval_band_s = timed(lambda: (m.forward(), m.readout()))
+        eval_sparse_s = timed(m.evaluate_sparse)
 
     # Roofline of the banded kernels: each launch timed with HIP events on the
     # stream it runs on, in the same launch shape as inside the step.
@@ -388,6 +393,8 @@ def main():
                    "ms_per_step_eager": round(eager_s * 1e3, 4),
                    "ms_per_step_graph": None if graph_s is None else round(graph_s * 1e3, 4),
                    "ms_per_train_step": None if train_s is None else round(train_s * 1e3, 4),
+                   "ms_eval_band": None if eval_band_s is None else round(eval_band_s * 1e3, 4),
+                   "ms_eval_sparse_all_edges": None if eval_sparse_s is None else round(eval_sparse_s * 1e3, 4),
                    "host_compile_s": round(comp.rcm_seconds + comp.stats.get("pack_seconds", 0.0), 3),
                    "generate_s": round(gen_s, 3)},
         "roofline": roofline,

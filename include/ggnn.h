@@ -424,6 +424,36 @@ ggnn_status ggnn_sgd_momentum(int64_t count, float* param, float* velocity, cons
                               float momentum, float weight_decay, int32_t nesterov, ggnn_dtype copy_dtype,
                               void* param_copy, void* stream);
 
+/* ---- Evaluation on every edge (the lossy regime) --------------------------
+ *
+ * A model trained on the block band with B smaller than some graphs'
+ * bandwidth drops their out-of-band edges (the coverage remark after Eq. 3);
+ * its parameters are those of the sparse model, which evaluates with
+ * messages passed along all edges (Experiments, "Training time to validation
+ * accuracy").  These two calls are that sparse evaluation path.
+ *
+ * Host, synchronous: receiver-major lists of all edges, deduplicated (A_e has
+ * entries in {0, 1}).  Row r = i * E + e lists the senders j of edges
+ * j -> i of type e, ascending: col[row_ptr[r] .. row_ptr[r+1]-1].
+ *   src, dst, etype [m] int32 (nodes < n_pad, types < E);
+ *   row_ptr [n_pad * E + 1] int32 (written);  col [m] int32 (first *nnz written)
+ *   *nnz = distinct edges; *n_duplicate = m - *nnz (either may be NULL). */
+ggnn_status ggnn_sparse_csr(int32_t n_pad, int32_t E, int64_t m, const int32_t* src, const int32_t* dst,
+                            const int32_t* etype, int32_t* row_ptr, int32_t* col, int64_t* nnz,
+                            int64_t* n_duplicate);
+
+/* Device: one propagation step's aggregate over every listed edge, in the
+ * operand order of Algorithm 1:
+ *   a[i] = sum_e ( sum_{j in col[row i*E+e]} X[j] ) W_e  (+ deg_e(i) bias_e)
+ * row_ptr, col: ggnn_sparse_csr output copied to the device (nnz entries of
+ * col; every col value < n_pad -- device data is not checked);
+ * X [n_pad][H] dt; Wt [E][H][H] dt = W_e^T (ggnn_transpose_weights);
+ * bias [E][H] float or NULL; a [n_pad][H] float (written).  The GRU update
+ * of ggnn_gru_update then completes the step. */
+ggnn_status ggnn_sparse_step(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E, const int32_t* row_ptr,
+                             const int32_t* col, int64_t nnz, const void* X, const void* Wt, const float* bias,
+                             float* a, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

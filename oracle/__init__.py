@@ -11,5 +11,5 @@ from .ggnn_oracle import (  # noqa: F401
     pack_band, unpack_band, banded_apply,
     msg_transform, aggregate, aggregate_transpose, msg_transform_backward,
     gru_forward, gru_backward, propagate, batch_layout,
-    readout_logits, readout_loss, readout_backward, momentum_update, train_step,
+    readout_logits, readout_loss, readout_backward, momentum_update, train_step, evaluate,
 )

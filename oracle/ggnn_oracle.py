@@ -314,16 +314,23 @@ def gru_backward(g, a, h, r, z, nn, Wi, U):
     return da, dh, dWi, dU, db
 
 
-def propagate(n: int, B: int, src, dst, etype, X0, W, Wi, U, b, T: int, G=None, bias=None):
+def propagate(n: int, B, src, dst, etype, X0, W, Wi, U, b, T: int, G=None, bias=None):
     """T steps of banded GGNN propagation (Eq. 1, Algorithm 1 semantics) on the
     edges the three block diagonals cover, and, when G is given, the reverse
-    pass for the loss L = sum(G * X_T).
+    pass for the loss L = sum(G * X_T).  B = None propagates along every
+    (deduplicated) edge: the sparse model that evaluates the weights of a
+    banded one on all edges (Experiments, "Training time to validation
+    accuracy").
 
     Returns a dict with 'X' (list of X_0..X_T), 'a', 'r', 'z', 'n' (per step),
     'n_dropped', 'n_duplicate', and with G: 'dX0', 'dW', 'dbias', 'dWi', 'dU',
     'db', 'dX' (list of dX_0..dX_T)."""
     E = W.shape[0]
-    s, d, e, ndrop, ndup = kept_edges(src, dst, etype, B)
+    if B is None:
+        s, d, e, ndup = dedupe_edges(src, dst, etype)
+        ndrop = 0
+    else:
+        s, d, e, ndrop, ndup = kept_edges(src, dst, etype, B)
     out = {"X": [np.asarray(X0, np.float64)], "a": [], "r": [], "z": [], "n": [],
            "n_dropped": ndrop, "n_duplicate": ndup}
     for t in range(T):
@@ -425,6 +432,16 @@ def momentum_update(theta, velocity, grad, lr, momentum, weight_decay=0.0, neste
     v = momentum * np.asarray(velocity, np.float64) + g
     step = g + momentum * v if nesterov else v
     return theta - lr * step, v
+
+
+def evaluate(n: int, B, src, dst, etype, X0, params: dict, T: int, cand_node, cand_ptr, target):
+    """Mean readout loss of the parameters after T propagation steps (B = None:
+    along every edge).  Returns (loss per graph, mean loss)."""
+    out = propagate(n, B, src, dst, etype, X0, params["W"], params["Wi"], params["U"], params["b"], T,
+                    bias=params.get("bias"))
+    logits = readout_logits(out["X"][T], params["w_out"], params["b_out"], cand_node)
+    loss, mean, _ = readout_loss(logits, cand_ptr, target)
+    return loss, mean
 
 
 def train_step(n: int, B: int, src, dst, etype, X0, params: dict, velocity: dict, T: int,

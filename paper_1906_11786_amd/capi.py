@@ -36,6 +36,7 @@ EXPORTS = [
     "ggnn_banded_propagate_bwd", "ggnn_msg_transform_bwd_workspace_bytes", "ggnn_msg_transform_bwd",
     "ggnn_backward_workspace_bytes", "ggnn_forward", "ggnn_backward",
     "ggnn_readout_loss", "ggnn_readout_loss_bwd_workspace_bytes", "ggnn_readout_loss_bwd", "ggnn_sgd_momentum",
+    "ggnn_sparse_csr", "ggnn_sparse_step",
 ]
 
 
@@ -100,6 +101,8 @@ _SIGS = {
     "ggnn_readout_loss_bwd_workspace_bytes": (sz, [i32, i32]),
     "ggnn_readout_loss_bwd": (C.c_int, [C.c_int, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
     "ggnn_sgd_momentum": (C.c_int, [i64, vp, vp, vp, C.c_float, C.c_float, C.c_float, i32, C.c_int, vp, vp]),
+    "ggnn_sparse_csr": (C.c_int, [i32, i32, i64, vp, vp, vp, vp, vp, vp, vp]),
+    "ggnn_sparse_step": (C.c_int, [C.c_int, i32, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp]),
 }
 
 
@@ -341,3 +344,23 @@ def ggnn_sgd_momentum(count, param, velocity, grad, lr, momentum, weight_decay=0
     _check("ggnn_sgd_momentum", lib().ggnn_sgd_momentum(
         count, _ptr(param), _ptr(velocity), _ptr(grad), lr, momentum, weight_decay, 1 if nesterov else 0,
         _dt(copy_dtype), _ptr(param_copy), _stream(stream)))
+
+
+# ------------------------------------------------ evaluation on every edge
+
+def ggnn_sparse_csr(n_pad, E, src, dst, etype):
+    """Receiver-major lists of all edges (host).  Returns (row_ptr, col,
+    n_duplicate) as int32 arrays (col holds exactly the distinct edges)."""
+    s, d, t = _i32(src), _i32(dst), _i32(etype)
+    m = len(s)
+    row_ptr = np.empty(n_pad * E + 1, dtype=np.int32)
+    col = np.empty(max(m, 1), dtype=np.int32)
+    nnz, dup = C.c_int64(0), C.c_int64(0)
+    _check("ggnn_sparse_csr", lib().ggnn_sparse_csr(n_pad, E, m, _ptr(s), _ptr(d), _ptr(t), _ptr(row_ptr),
+                                                    _ptr(col), C.byref(nnz), C.byref(dup)))
+    return row_ptr, col[:nnz.value].copy(), int(dup.value)
+
+
+def ggnn_sparse_step(dt, n_pad, H, E, row_ptr, col, nnz, X, Wt, bias, a, stream=None):
+    _check("ggnn_sparse_step", lib().ggnn_sparse_step(_dt(dt), n_pad, H, E, _ptr(row_ptr), _ptr(col), nnz, _ptr(X),
+                                                      _ptr(Wt), _ptr(bias), _ptr(a), _stream(stream)))

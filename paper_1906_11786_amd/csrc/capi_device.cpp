@@ -536,4 +536,22 @@ ggnn_status ggnn_sgd_momentum(int64_t count, float* param, float* velocity, cons
                        "sgd_momentum");
 }
 
+ggnn_status ggnn_sparse_step(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E, const int32_t* row_ptr,
+                             const int32_t* col, int64_t nnz, const void* X, const void* Wt, const float* bias,
+                             float* a, void* stream) {
+  clear_error();
+  ggnn_status st = check_common(dt, n_pad, H);
+  if (st != GGNN_OK) return st;
+  GGNN_CHECK_ARG(E >= 1 && E <= 64, "E=%d must be in [1, 64]", E);
+  GGNN_CHECK_ARG(nnz >= 0 && nnz < ((int64_t)1 << 31), "nnz=%lld must be in [0, 2^31)", (long long)nnz);
+  CHECK_PTR(row_ptr, "row_ptr");
+  if (nnz > 0) CHECK_PTR(col, "col");
+  CHECK_PTR(X, "X");
+  CHECK_PTR(Wt, "Wt");
+  CHECK_OPT_PTR(bias, "bias");
+  CHECK_PTR(a, "a");
+  return device_status(launch_sparse_step(dt, n_pad, H, E, row_ptr, col, X, Wt, bias, a, as_stream(stream)),
+                       "sparse_step");
+}
+
 }  // extern "C"

@@ -357,4 +357,47 @@ ggnn_status ggnn_banded_pack_bits(int32_t n_pad, int32_t E, int32_t B, int64_t m
   return GGNN_OK;
 }
 
+// Receiver-major lists of all edges, deduplicated (A_e has entries in
+// {0, 1}): the sparse form of sum_e A_e X used to evaluate on every edge.
+ggnn_status ggnn_sparse_csr(int32_t n_pad, int32_t E, int64_t m, const int32_t* src, const int32_t* dst,
+                            const int32_t* etype, int32_t* row_ptr, int32_t* col, int64_t* nnz,
+                            int64_t* n_duplicate) {
+  clear_error();
+  GGNN_CHECK_ARG(n_pad > 0, "n_pad=%d must be positive", n_pad);
+  GGNN_CHECK_ARG(E >= 1 && E <= 64, "E=%d must be in [1, 64]", E);
+  GGNN_CHECK_ARG(m >= 0 && m < ((int64_t)1 << 31), "m=%lld must be in [0, 2^31)", (long long)m);
+  GGNN_CHECK_ARG(m == 0 || (src && dst && etype), "src/dst/etype is NULL");
+  GGNN_CHECK_ARG(row_ptr != nullptr && (m == 0 || col != nullptr), "row_ptr/col is NULL");
+  GGNN_CHECK_ARG((int64_t)n_pad * E < ((int64_t)1 << 31), "n_pad*E exceeds 2^31");
+  for (int64_t k = 0; k < m; ++k) {
+    GGNN_CHECK_ARG(src[k] >= 0 && src[k] < n_pad && dst[k] >= 0 && dst[k] < n_pad,
+                   "edge %lld (%d -> %d) out of range [0,%d)", (long long)k, src[k], dst[k], n_pad);
+    GGNN_CHECK_ARG(etype[k] >= 0 && etype[k] < E, "edge %lld has type %d outside [0,%d)", (long long)k, etype[k],
+                   E);
+  }
+  // (receiver, type, sender) keys, sorted and made unique
+  std::vector<int64_t> key;
+  try {
+    key.resize(static_cast<size_t>(m));
+  } catch (const std::bad_alloc&) {
+    return fail(GGNN_ERR_HOST_ALLOC, "temporary allocation failed");
+  }
+  for (int64_t k = 0; k < m; ++k)
+    key[k] = ((static_cast<int64_t>(dst[k]) * E + etype[k]) << 31) | static_cast<int64_t>(src[k]);
+  std::sort(key.begin(), key.end());
+  const int64_t uniq = static_cast<int64_t>(std::unique(key.begin(), key.end()) - key.begin());
+  const int64_t rows = static_cast<int64_t>(n_pad) * E;
+  int64_t r = 0;
+  row_ptr[0] = 0;
+  for (int64_t k = 0; k < uniq; ++k) {
+    const int64_t row = key[k] >> 31;
+    while (r < row) row_ptr[++r] = static_cast<int32_t>(k);
+    col[k] = static_cast<int32_t>(key[k] & 0x7FFFFFFF);
+  }
+  while (r < rows) row_ptr[++r] = static_cast<int32_t>(uniq);
+  if (nnz) *nnz = uniq;
+  if (n_duplicate) *n_duplicate = m - uniq;
+  return GGNN_OK;
+}
+
 }  // extern "C"

@@ -58,6 +58,8 @@ namespace ggnn {
   hipError_t launch_readout_bwd(int n_pad, int H, int n_cand, const void* X, const float* w_out,                 \
                                 const int32_t* cand_node, const float* dlogit, float* dX, float* dw_out,         \
                                 float* db_out, void* ws, hipStream_t st);                                        \
+  hipError_t launch_sparse_step(int n_pad, int H, int E, const int32_t* row_ptr, const int32_t* col,            \
+                                const void* X, const void* Wt, const float* bias, float* a, hipStream_t st);   \
   bool step_wide_applies(int B, int H);                                                                           \
   hipError_t launch_step_wide(bool rev, int n_pad, int B, int H, int E, const void* bits, const void* V,          \
                               const void* Wsrc, const float* bias, float* out, const float* dX_in, void* dM,      \
@@ -212,6 +214,12 @@ inline hipError_t launch_readout_bwd(int dt, int n_pad, int H, int n_cand, const
                                      const int32_t* cand_node, const float* dlogit, float* dX, float* dw_out,
                                      float* db_out, void* ws, hipStream_t st) {
   return GGNN_DT_PICK(launch_readout_bwd, n_pad, H, n_cand, X, w_out, cand_node, dlogit, dX, dw_out, db_out, ws, st);
+}
+// Sparse aggregate-first step over receiver-major edge lists (every edge):
+// a = sum_e (A_e X) W_e (+ deg_e b_e), W_e given transposed.
+inline hipError_t launch_sparse_step(int dt, int n_pad, int H, int E, const int32_t* row_ptr, const int32_t* col,
+                                     const void* X, const void* Wt, const float* bias, float* a, hipStream_t st) {
+  return GGNN_DT_PICK(launch_sparse_step, n_pad, H, E, row_ptr, col, X, Wt, bias, a, st);
 }
 // Momentum update of float32 master parameters (and their compute copy).
 hipError_t launch_sgd_momentum(long count, float* theta, float* vel, const float* grad, float lr, float mu, float wd,

@@ -263,6 +263,36 @@ class BandedGGNN:
                                    o["nesterov"], self.dt, copy, stream)
         self.refresh_weights(stream)
 
+    # --------------------------------------------- evaluation on every edge
+
+    def setup_sparse(self, src, dst, etype):
+        """Receiver-major lists of every edge (final labels; may include edges
+        the band drops) for evaluate_sparse()."""
+        torch = self.torch
+        row_ptr, col, dup = capi.ggnn_sparse_csr(self.comp.n_pad, self.comp.E, src, dst, etype)
+        self.sp_row_ptr = torch.from_numpy(row_ptr).to(self.device)
+        self.sp_col = torch.from_numpy(col if len(col) else np.zeros(1, np.int32)).to(self.device)
+        self.sp_nnz = len(col)
+        self.sp_duplicates = dup
+        self.sp_X = torch.empty((2, self.comp.n_pad, self.H), dtype=self.X.dtype, device=self.device)
+
+    def evaluate_sparse(self, stream=None):
+        """T propagation steps from X_0 along every edge (ggnn_sparse_step,
+        then ggnn_gru_update) with the current parameters, then the readout and
+        loss (per-graph losses in self.loss).  Training state is untouched
+        except the readout outputs."""
+        n_pad, H, E = self.comp.n_pad, self.H, self.comp.E
+        x = self.X[0]
+        for t in range(self.T):
+            nxt = self.sp_X[t % 2]
+            capi.ggnn_sparse_step(self.dt, n_pad, H, E, self.sp_row_ptr, self.sp_col, self.sp_nnz, x, self.Wt,
+                                  self.bias, self.a[0], stream)
+            capi.ggnn_gru_update(self.dt, n_pad, H, self.a[0], x, self.Wi, self.U, self.b, nxt, None, stream)
+            x = nxt
+        capi.ggnn_readout_loss(self.dt, n_pad, H, self.n_graphs, self.n_cand, x, self.w_out, self.b_out,
+                               self.cand_node, self.cand_ptr, self.target, self.logits, self.loss, self.dlogit,
+                               stream)
+
     def parameters(self) -> dict:
         """Host copies (float64) of the float32 master parameters."""
         f = (lambda t: t.float().cpu().numpy().astype(np.float64))

@@ -239,3 +239,29 @@ def test_pack_bits_strict_and_errors():
     assert ei.value.status_name == "GGNN_ERR_INVALID_ARG"
     bits, bits_t, *_ = capi.ggnn_banded_pack_bits(128, 1, 32, src, dst, et, with_transpose=False)
     assert bits_t is None and int(np.unpackbits(bits).sum()) == 1
+
+
+def test_sparse_csr_bit_exact_against_oracle_dedupe():
+    """Receiver-major lists of every edge: rows (receiver, type), senders
+    ascending, duplicates merged -- the oracle's deduplicated edge set."""
+    _need_lib()
+    rng = np.random.default_rng(11)
+    n, E, m = 300, 5, 4000
+    src = rng.integers(0, n, m)
+    dst = rng.integers(0, n, m)
+    et = rng.integers(0, E, m)
+    src[:50], dst[:50], et[:50] = src[50:100], dst[50:100], et[50:100]      # planted duplicates
+    row_ptr, col, dup = capi.ggnn_sparse_csr(n, E, src, dst, et)
+    s, d, e, ndup = O.dedupe_edges(src, dst, et)
+    assert dup == ndup and len(col) == len(s)
+    order = np.lexsort((s, e, d))
+    np.testing.assert_array_equal(col, s[order])
+    want_ptr = np.concatenate([[0], np.cumsum(np.bincount(d * E + e, minlength=n * E))])
+    np.testing.assert_array_equal(row_ptr, want_ptr)
+    # empty edge list, and errors
+    rp, c, dup = capi.ggnn_sparse_csr(64, 2, [], [], [])
+    assert (rp == 0).all() and len(c) == 0 and dup == 0
+    with pytest.raises(capi.GGNNError):
+        capi.ggnn_sparse_csr(64, 2, [0], [64], [0])      # node out of range
+    with pytest.raises(capi.GGNNError):
+        capi.ggnn_sparse_csr(64, 2, [0], [1], [2])       # type out of range

@@ -155,3 +155,23 @@ def test_train_step_gradients_match_finite_differences(seed):
         assert abs(fd - an) <= 1e-7 * max(1.0, abs(fd)), key
         np.testing.assert_allclose(newp[key], p[key] - 0.1 * grads[key], rtol=1e-14, atol=1e-16)
         np.testing.assert_allclose(newv[key], grads[key], rtol=1e-14, atol=1e-16)
+
+
+def test_all_edge_propagation_equals_a_band_wide_enough():
+    """B = None (every edge) agrees with a band wide enough to drop nothing,
+    and differs from a narrow band that drops edges."""
+    rng = np.random.default_rng(5)
+    n, E, H, T = 48, 2, 3, 2
+    src = rng.integers(0, n, 150)
+    dst = rng.integers(0, n, 150)            # spans up to n-1: outside any narrow band
+    et = rng.integers(0, E, 150)
+    k = 1 / np.sqrt(H)
+    W = rng.standard_normal((E, H, H)) / np.sqrt(H)
+    Wi, U, b = rng.uniform(-k, k, (H, 3 * H)), rng.uniform(-k, k, (H, 3 * H)), rng.uniform(-k, k, 3 * H)
+    X0 = rng.standard_normal((n, H))
+    full = O.propagate(n, None, src, dst, et, X0, W, Wi, U, b, T)
+    wide = O.propagate(n, 64, src, dst, et, X0, W, Wi, U, b, T)      # one block: nothing dropped
+    narrow = O.propagate(n, 4, src, dst, et, X0, W, Wi, U, b, T)
+    assert wide["n_dropped"] == 0 and narrow["n_dropped"] > 0 and full["n_dropped"] == 0
+    np.testing.assert_allclose(full["X"][T], wide["X"][T], rtol=1e-13, atol=1e-13)
+    assert np.abs(full["X"][T] - narrow["X"][T]).max() > 1e-3
