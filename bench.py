@@ -80,6 +80,9 @@ def parse():
     p.add_argument("--no-train", action="store_true",
                    help="skip the timing of one training step (readout, loss and Momentum update included)")
     p.add_argument("--eager", action="store_true", help="time eager launches only (no HIP graph replay)")
+    p.add_argument("--drops", action="store_true",
+                   help="host only: print the edges each block size keeps and drops on the workload's graphs "
+                        "(with and without reordering, and with long-span variants of the graphs), then exit")
     p.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="summarise two rocprofv3 --pmc counter files (FETCH_SIZE, WRITE_SIZE) of this command "
                         "and exit")
@@ -242,8 +245,34 @@ def cpu_baseline(spec, graphs, comp, params):
                       f"{dt:.1f} s"}
 
 
+def drops_table(spec_name: str) -> str:
+    """Dropped-edge fraction against the block size (the coverage remark
+    after Eq. 3) on the workload's graphs: host reordering and packing only.
+    The long-span variant redraws every graph with parent distances of mean
+    30 and at most 512 (wider than the program-graph backbone), the regime
+    where a block size below the bandwidth loses edges."""
+    from ggnn_synth import make_graphs, backbone_graph, scramble_graph
+    from paper_1906_11786_amd.driver import dropped_edges
+    spec = spec_for(spec_name)
+    graphs = make_graphs(spec)
+    wide = [scramble_graph(spec.cfg, gi, backbone_graph(spec.cfg, gi, g.n, spec.E, span_mean=30.0, max_span=512))[0]
+            for gi, g in enumerate(graphs)]
+    rows = ["| graphs | reordering | B | bandwidth (max over graphs) | edges | dropped | dropped fraction |",
+            "|---|---|---:|---:|---:|---:|---:|"]
+    for label, gs in (("workload", graphs), ("long-span variant", wide)):
+        for reorder in (True, False):
+            for B in (32, 64, 128, 256, 512):
+                r = dropped_edges(gs, B, spec.E, reorder=reorder)
+                rows.append(f"| {label} | {'RCM' if reorder else 'none (scrambled)'} | {B} | {r['bandwidth']} | "
+                            f"{r['edges']} | {r['dropped']} | {r['dropped_fraction']:.4f} |")
+    return "\n".join(rows)
+
+
 def main():
     args = parse()
+    if args.drops:
+        print(drops_table(args.workload))
+        return
     if args.traffic_from:
         lines, (kf, kw), recs = traffic_summary(*args.traffic_from, " ".join(sys.argv))
         print("\n".join(lines))

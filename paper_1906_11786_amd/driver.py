@@ -58,6 +58,18 @@ def compile_graphs(graphs: Sequence, B: int, E: int, reorder: bool = True) -> Co
                     np.asarray(offs, np.int64), bw, time.perf_counter() - t0)
 
 
+def dropped_edges(graphs: Sequence, B: int, E: int, reorder: bool = True) -> dict:
+    """Edges the three block diagonals keep and drop when the graphs are
+    packed with block size B (the coverage remark after Eq. 3): host
+    reordering and packing only, no device work."""
+    comp = compile_graphs(graphs, B, E, reorder=reorder)
+    _, _, packed, dropped, dup = capi.ggnn_banded_pack_bits(comp.n_pad, E, B, comp.src, comp.dst, comp.etype,
+                                                            with_transpose=False, strict=False)
+    total = packed + dropped
+    return {"B": B, "reorder": reorder, "bandwidth": comp.bandwidth, "edges": total, "kept": packed,
+            "dropped": dropped, "duplicates": dup, "dropped_fraction": dropped / total if total else 0.0}
+
+
 def torch_dtype(dt: str):
     import torch
     return torch.bfloat16 if dt == "bf16" else torch.float32

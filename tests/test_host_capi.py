@@ -265,3 +265,24 @@ def test_sparse_csr_bit_exact_against_oracle_dedupe():
         capi.ggnn_sparse_csr(64, 2, [0], [64], [0])      # node out of range
     with pytest.raises(capi.GGNNError):
         capi.ggnn_sparse_csr(64, 2, [0], [1], [2])       # type out of range
+
+
+def test_dropped_edges_counts_against_oracle():
+    """The host measurement of dropped edges equals the oracle's coverage
+    rule on the same (oracle-reordered) labels; nothing drops when B exceeds
+    the bandwidth."""
+    _need_lib()
+    from paper_1906_11786_amd.driver import dropped_edges
+    graphs = [scramble_graph(9, gi, backbone_graph(9, gi, sz, 3, span_mean=20.0, max_span=200))[0]
+              for gi, sz in enumerate([400, 250])]
+    parts = []
+    for g in graphs:
+        _, rank = O.rcm_order(g.n, g.src, g.dst)
+        parts.append((g.n, *O.relabel(rank, g.src, g.dst), g.etype))
+    _, _, s, d, e, _ = O.batch_layout(parts, 32)
+    for B in (32, 64, 128, 512):
+        r = dropped_edges(graphs, B, 3)
+        ks, kd, ke, ndrop, ndup = O.kept_edges(s, d, e, B)
+        assert (r["dropped"], r["kept"], r["duplicates"]) == (ndrop, len(ks), ndup), B
+        if r["bandwidth"] < B:
+            assert r["dropped"] == 0
