@@ -7,7 +7,7 @@ propagation): both the GPU path and the CPU oracle take its outputs as inputs.
 from .graphs import (  # noqa: F401
     Graph, rng_for, local_window_graph, backbone_graph, scramble_graph,
     lognormal_batch_sizes, STREAM_SIZES, STREAM_EDGES, STREAM_SCRAMBLE,
-    STREAM_X, STREAM_W, STREAM_GRU, STREAM_G,
+    STREAM_X, STREAM_W, STREAM_GRU, STREAM_G, STREAM_HUBS, add_hubs,
 )
 from .params import draw_params, round_bf16, Params  # noqa: F401
 from .configs import CONFIGS, ConfigSpec, make_graphs, sweep_blocks  # noqa: F401

@@ -159,3 +159,24 @@ def lognormal_batch_sizes(cfg: int, capacity: int, median: float, sigma: float,
         else:
             misses += 1
     return sizes
+
+
+STREAM_HUBS = 8   # hub nodes added to a graph (per graph)
+
+
+def add_hubs(cfg: int, graph: int, g: Graph, n_hubs: int, frac: float, n_types: int) -> tuple[Graph, np.ndarray]:
+    """Pick n_hubs distinct nodes of g and connect each, in both directions,
+    to a random fraction `frac` of the graph's nodes (edge types drawn
+    uniformly): the nodes that talk to a large part of their graph.  Returns
+    (graph with the extra edges, hub node ids)."""
+    r = rng_for(cfg, STREAM_HUBS, graph)
+    hubs = r.choice(g.n, size=min(n_hubs, g.n), replace=False).astype(np.int32)
+    S, D, T = [g.src], [g.dst], [g.etype]
+    for h in hubs:
+        k = max(1, int(frac * g.n))
+        peers = r.choice(g.n, size=k, replace=False).astype(np.int32)
+        peers = peers[peers != h]
+        S += [np.full(len(peers), h, np.int32), peers]
+        D += [peers, np.full(len(peers), h, np.int32)]
+        T += [r.integers(0, n_types, len(peers)).astype(np.int32), r.integers(0, n_types, len(peers)).astype(np.int32)]
+    return Graph(g.n, np.concatenate(S), np.concatenate(D), np.concatenate(T)), hubs

@@ -454,6 +454,50 @@ ggnn_status ggnn_sparse_step(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E,
                              const int32_t* col, int64_t nnz, const void* X, const void* Wt, const float* bias,
                              float* a, void* stream);
 
+/* ---- Supernodes: dense slices of the first rows and columns ---------------
+ *
+ * A second runtime primitive next to the band (Discussion section: nodes that
+ * communicate with all nodes, through dense slices of the first rows and
+ * columns of the adjacency matrix).  The supernodes are nodes 0 .. s-1
+ * (s in {32, 64, 96, 128}; n_pad a multiple of 64).  Per edge type e, 1 bit
+ * per entry:
+ *   rows   [E][s][n_pad/8]:  edges j -> i with i < s   (row i, byte j/8, bit j%8)
+ *   cols   [E][n_pad][s/8]:  edges j -> i with i >= s, j < s
+ *   rows_t [E][n_pad][s/8]:  rows transposed (row j, bit i);  cols_t [E][s][n_pad/8]: cols transposed
+ * Every other edge (both ends >= s) belongs to the block band.
+ *
+ * Host, synchronous: sizes in bytes of one slice (0 for unsupported sizes),
+ * and the packing of an edge list (rows_t, cols_t may be NULL).  n_rows /
+ * n_cols count the distinct edges packed into each slice, n_rest the edges
+ * left to the band, n_duplicate the repeats (any count pointer may be NULL). */
+size_t ggnn_super_bytes(int32_t n_pad, int32_t E, int32_t s);
+ggnn_status ggnn_super_pack(int32_t n_pad, int32_t E, int32_t s, int64_t m, const int32_t* src, const int32_t* dst,
+                            const int32_t* etype, void* rows, void* cols, void* rows_t, void* cols_t,
+                            int64_t* n_rows, int64_t* n_cols, int64_t* n_rest, int64_t* n_duplicate);
+
+/* Workspace bytes of the two device calls below (0 for unsupported sizes). */
+size_t ggnn_super_workspace_bytes(int32_t n_pad, int32_t H, int32_t E, int32_t s);
+
+/* Device: the slices' share of one propagation step, added onto a (the
+ * band's aggregate, e.g. from ggnn_banded_step_bits), with M_e = X W_e + b_e:
+ *   a[i] += sum_e sum_j R_e[i][j] M_e[j]      (i < s; computed as (R_e X) W_e + deg b_e)
+ *   a[i] += sum_e sum_{j<s} C_e[i][j] M_e[j]  (all i; M_e of the s supernodes)
+ * X [n_pad][H] dt;  W [E][H][H] dt;  bias [E][H] float or NULL;  a [n_pad][H] float (+=).
+ * ggnn_gru_update then completes the step. */
+ggnn_status ggnn_super_propagate(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E, int32_t s, const void* rows,
+                                 const void* cols, const void* X, const void* W, const float* bias, float* a,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Device: reverse of ggnn_super_propagate for the upstream gradient da of a:
+ * with dM_e = S_e^T da (S_e = the two slices),
+ *   dX += sum_e dM_e W_e^T;  dW_e += X^T dM_e;  dbias_e += column sums of dM_e (dbias may be NULL)
+ * da [H][n_pad] dt feature-major (as ggnn_gru_update_bwd writes it);
+ * dX [n_pad][H] float, dW [E][H][H] float, dbias [E][H] float: accumulated. */
+ggnn_status ggnn_super_propagate_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E, int32_t s,
+                                     const void* rows, const void* rows_t, const void* cols_t, const void* X,
+                                     const void* W, const void* da, float* dX, float* dW, float* dbias,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

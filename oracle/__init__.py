@@ -7,7 +7,7 @@ smoke check and the CPU-baseline leg of the benchmark may import it.  It
 shares no code with the GPU library and imports nothing from it.
 """
 from .ggnn_oracle import (  # noqa: F401
-    bandwidth, dedupe_edges, covered_mask, kept_edges, rcm_order, relabel,
+    bandwidth, dedupe_edges, covered_mask, kept_edges, kept_edges_super, rcm_order, relabel,
     pack_band, unpack_band, banded_apply,
     msg_transform, aggregate, aggregate_transpose, msg_transform_backward,
     gru_forward, gru_backward, propagate, batch_layout,

@@ -70,6 +70,17 @@ def kept_edges(src, dst, etype, B: int):
     return s[keep], d[keep], e[keep], int((~keep).sum()), ndup
 
 
+def kept_edges_super(src, dst, etype, B: int, n_super: int):
+    """The edge set propagated with n_super supernodes next to the band
+    (Discussion section: dense slices of the first rows and columns of the
+    adjacency matrix): every edge into or out of a node labelled < n_super,
+    and the other edges when the three block diagonals cover them.  Returns
+    (src, dst, etype, n_dropped, n_duplicates)."""
+    s, d, e, ndup = dedupe_edges(src, dst, etype)
+    keep = (d < n_super) | (s < n_super) | covered_mask(s, d, B)
+    return s[keep], d[keep], e[keep], int((~keep).sum()), ndup
+
+
 def _sym_neighbours(n: int, src, dst):
     """Neighbour lists of the undirected simple graph that is the union of all
     edge types, symmetrised, without self-loops or repeats."""
@@ -314,11 +325,12 @@ def gru_backward(g, a, h, r, z, nn, Wi, U):
     return da, dh, dWi, dU, db
 
 
-def propagate(n: int, B, src, dst, etype, X0, W, Wi, U, b, T: int, G=None, bias=None):
+def propagate(n: int, B, src, dst, etype, X0, W, Wi, U, b, T: int, G=None, bias=None, n_super: int = 0):
     """T steps of banded GGNN propagation (Eq. 1, Algorithm 1 semantics) on the
     edges the three block diagonals cover, and, when G is given, the reverse
-    pass for the loss L = sum(G * X_T).  B = None propagates along every
-    (deduplicated) edge: the sparse model that evaluates the weights of a
+    pass for the loss L = sum(G * X_T).  n_super > 0 adds every edge touching
+    the supernodes 0 .. n_super-1 (kept_edges_super).  B = None propagates
+    along every (deduplicated) edge: the sparse model that evaluates the weights of a
     banded one on all edges (Experiments, "Training time to validation
     accuracy").
 
@@ -329,6 +341,8 @@ def propagate(n: int, B, src, dst, etype, X0, W, Wi, U, b, T: int, G=None, bias=
     if B is None:
         s, d, e, ndup = dedupe_edges(src, dst, etype)
         ndrop = 0
+    elif n_super > 0:
+        s, d, e, ndrop, ndup = kept_edges_super(src, dst, etype, B, n_super)
     else:
         s, d, e, ndrop, ndup = kept_edges(src, dst, etype, B)
     out = {"X": [np.asarray(X0, np.float64)], "a": [], "r": [], "z": [], "n": [],

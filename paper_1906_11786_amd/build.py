@@ -30,7 +30,7 @@ HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall"]
 
 # (source, language, dtype build or None)
 SOURCES = [("host.cpp", "c++", None), ("capi_device.cpp", "hip", None)] + [
-    (src, "hip", dt) for src in ("banded.hip", "banded_bits.hip", "banded_wide.hip", "transform.hip", "gru.hip", "readout.hip", "sparse.hip") for dt in ("bf16", "f32")]
+    (src, "hip", dt) for src in ("banded.hip", "banded_bits.hip", "banded_wide.hip", "transform.hip", "gru.hip", "readout.hip", "sparse.hip", "supernode.hip") for dt in ("bf16", "f32")]
 
 
 def _compile(src: str, lang: str, dt) -> str:

@@ -37,6 +37,8 @@ EXPORTS = [
     "ggnn_backward_workspace_bytes", "ggnn_forward", "ggnn_backward",
     "ggnn_readout_loss", "ggnn_readout_loss_bwd_workspace_bytes", "ggnn_readout_loss_bwd", "ggnn_sgd_momentum",
     "ggnn_sparse_csr", "ggnn_sparse_step",
+    "ggnn_super_bytes", "ggnn_super_pack", "ggnn_super_workspace_bytes", "ggnn_super_propagate",
+    "ggnn_super_propagate_bwd",
 ]
 
 
@@ -103,6 +105,12 @@ _SIGS = {
     "ggnn_sgd_momentum": (C.c_int, [i64, vp, vp, vp, C.c_float, C.c_float, C.c_float, i32, C.c_int, vp, vp]),
     "ggnn_sparse_csr": (C.c_int, [i32, i32, i64, vp, vp, vp, vp, vp, vp, vp]),
     "ggnn_sparse_step": (C.c_int, [C.c_int, i32, i32, i32, vp, vp, i64, vp, vp, vp, vp, vp]),
+    "ggnn_super_bytes": (sz, [i32, i32, i32]),
+    "ggnn_super_pack": (C.c_int, [i32, i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+    "ggnn_super_workspace_bytes": (sz, [i32, i32, i32, i32]),
+    "ggnn_super_propagate": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+    "ggnn_super_propagate_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
+                                           vp]),
 }
 
 
@@ -364,3 +372,43 @@ def ggnn_sparse_csr(n_pad, E, src, dst, etype):
 def ggnn_sparse_step(dt, n_pad, H, E, row_ptr, col, nnz, X, Wt, bias, a, stream=None):
     _check("ggnn_sparse_step", lib().ggnn_sparse_step(_dt(dt), n_pad, H, E, _ptr(row_ptr), _ptr(col), nnz, _ptr(X),
                                                       _ptr(Wt), _ptr(bias), _ptr(a), _stream(stream)))
+
+
+# ------------------------------------------------------------- supernodes
+
+def ggnn_super_pack(n_pad, E, s, src, dst, etype, with_transpose=True):
+    """Host packing of the supernode slices.  Returns (rows, cols, rows_t,
+    cols_t, counts) with rows/cols_t shaped [E, s, n_pad/8] and cols/rows_t
+    [E, n_pad, s/8] (uint8; the transposes None without with_transpose) and
+    counts = dict(rows, cols, rest, duplicates)."""
+    nbytes = lib().ggnn_super_bytes(n_pad, E, s)
+    if nbytes == 0:
+        raise GGNNError("ggnn_super_pack", 1, f"unsupported sizes n_pad={n_pad} E={E} s={s}")
+    sv, dv, tv = _i32(src), _i32(dst), _i32(etype)
+    wide, narrow = (E, s, n_pad // 8), (E, n_pad, s // 8)
+    rows, cols = np.empty(wide, np.uint8), np.empty(narrow, np.uint8)
+    rows_t = np.empty(narrow, np.uint8) if with_transpose else None
+    cols_t = np.empty(wide, np.uint8) if with_transpose else None
+    c = [C.c_int64(0) for _ in range(4)]
+    _check("ggnn_super_pack", lib().ggnn_super_pack(
+        n_pad, E, s, len(sv), _ptr(sv), _ptr(dv), _ptr(tv), _ptr(rows), _ptr(cols), _ptr(rows_t), _ptr(cols_t),
+        *[C.byref(x) for x in c]))
+    return rows, cols, rows_t, cols_t, dict(rows=c[0].value, cols=c[1].value, rest=c[2].value,
+                                            duplicates=c[3].value)
+
+
+def ggnn_super_workspace_bytes(n_pad, H, E, s) -> int:
+    return int(lib().ggnn_super_workspace_bytes(n_pad, H, E, s))
+
+
+def ggnn_super_propagate(dt, n_pad, H, E, s, rows, cols, X, W, bias, a, workspace, workspace_bytes, stream=None):
+    _check("ggnn_super_propagate", lib().ggnn_super_propagate(
+        _dt(dt), n_pad, H, E, s, _ptr(rows), _ptr(cols), _ptr(X), _ptr(W), _ptr(bias), _ptr(a), _ptr(workspace),
+        workspace_bytes, _stream(stream)))
+
+
+def ggnn_super_propagate_bwd(dt, n_pad, H, E, s, rows, rows_t, cols_t, X, W, da, dX, dW, dbias, workspace,
+                             workspace_bytes, stream=None):
+    _check("ggnn_super_propagate_bwd", lib().ggnn_super_propagate_bwd(
+        _dt(dt), n_pad, H, E, s, _ptr(rows), _ptr(rows_t), _ptr(cols_t), _ptr(X), _ptr(W), _ptr(da), _ptr(dX),
+        _ptr(dW), _ptr(dbias), _ptr(workspace), workspace_bytes, _stream(stream)))

@@ -555,3 +555,70 @@ ggnn_status ggnn_sparse_step(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E,
 }
 
 }  // extern "C"
+
+namespace {
+ggnn_status check_super(int32_t dt, int32_t n_pad, int32_t H, int32_t E, int32_t s) {
+  ggnn_status st = check_common(dt, n_pad, H);
+  if (st != GGNN_OK) return st;
+  GGNN_CHECK_ARG(n_pad % 64 == 0, "n_pad=%d must be a multiple of 64", n_pad);
+  GGNN_CHECK_ARG(E >= 1 && E <= 64, "E=%d must be in [1, 64]", E);
+  GGNN_CHECK_ARG(s >= 32 && s <= 128 && s % 32 == 0 && s <= n_pad, "s=%d must be 32, 64, 96 or 128 (<= n_pad)", s);
+  return GGNN_OK;
+}
+}  // namespace
+
+extern "C" {
+
+size_t ggnn_super_workspace_bytes(int32_t n_pad, int32_t H, int32_t E, int32_t s) {
+  if (n_pad <= 0 || n_pad % 64 != 0 || !supported_H(H) || E < 1 || E > 64 || s < 32 || s > 128 || s % 32 != 0 ||
+      s > n_pad)
+    return 0;
+  return super_workspace(n_pad, H, E, s);
+}
+
+ggnn_status ggnn_super_propagate(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E, int32_t s, const void* rows,
+                                 const void* cols, const void* X, const void* W, const float* bias, float* a,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  ggnn_status st = check_super(dt, n_pad, H, E, s);
+  if (st != GGNN_OK) return st;
+  CHECK_PTR(rows, "rows");
+  CHECK_PTR(cols, "cols");
+  CHECK_PTR(X, "X");
+  CHECK_PTR(W, "W");
+  CHECK_OPT_PTR(bias, "bias");
+  CHECK_PTR(a, "a");
+  const size_t need = super_workspace(n_pad, H, E, s);
+  if (workspace == nullptr || workspace_bytes < need || !aligned16(workspace))
+    return fail(GGNN_ERR_WORKSPACE, "super_propagate needs a 16-byte aligned workspace of %zu bytes (got %zu)", need,
+                workspace ? workspace_bytes : (size_t)0);
+  return device_status(launch_super_fwd(dt, n_pad, H, E, s, rows, cols, X, W, bias, a, workspace, as_stream(stream)),
+                       "super_propagate");
+}
+
+ggnn_status ggnn_super_propagate_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t E, int32_t s,
+                                     const void* rows, const void* rows_t, const void* cols_t, const void* X,
+                                     const void* W, const void* da, float* dX, float* dW, float* dbias,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  clear_error();
+  ggnn_status st = check_super(dt, n_pad, H, E, s);
+  if (st != GGNN_OK) return st;
+  CHECK_PTR(rows, "rows");
+  CHECK_PTR(rows_t, "rows_t");
+  CHECK_PTR(cols_t, "cols_t");
+  CHECK_PTR(X, "X");
+  CHECK_PTR(W, "W");
+  CHECK_PTR(da, "da");
+  CHECK_PTR(dX, "dX");
+  CHECK_PTR(dW, "dW");
+  CHECK_OPT_PTR(dbias, "dbias");
+  const size_t need = super_workspace(n_pad, H, E, s);
+  if (workspace == nullptr || workspace_bytes < need || !aligned16(workspace))
+    return fail(GGNN_ERR_WORKSPACE, "super_propagate_bwd needs a 16-byte aligned workspace of %zu bytes (got %zu)",
+                need, workspace ? workspace_bytes : (size_t)0);
+  return device_status(launch_super_bwd(dt, n_pad, H, E, s, rows, rows_t, cols_t, X, W, da, dX, dW, dbias, workspace,
+                                        as_stream(stream)),
+                       "super_propagate_bwd");
+}
+
+}  // extern "C"

@@ -400,4 +400,74 @@ ggnn_status ggnn_sparse_csr(int32_t n_pad, int32_t E, int64_t m, const int32_t* 
   return GGNN_OK;
 }
 
+// Dense 1-bit slices of the first s rows and columns (supernodes 0 .. s-1):
+// rows [E][s][n_pad/8] holds edges into a supernode, cols [E][n_pad][s/8]
+// edges out of a supernode into any other node; rows_t / cols_t (optional)
+// their transposes with the same two layouts swapped.  Every other edge is
+// counted in *n_rest (the band's).
+size_t ggnn_super_bytes(int32_t n_pad, int32_t E, int32_t s) {
+  if (n_pad <= 0 || n_pad % 64 != 0 || E < 1 || E > 64 || s < 32 || s > 128 || s % 32 != 0 || s > n_pad) return 0;
+  return static_cast<size_t>(E) * s * (n_pad / 8);
+}
+
+ggnn_status ggnn_super_pack(int32_t n_pad, int32_t E, int32_t s, int64_t m, const int32_t* src, const int32_t* dst,
+                            const int32_t* etype, void* rows, void* cols, void* rows_t, void* cols_t,
+                            int64_t* n_rows, int64_t* n_cols, int64_t* n_rest, int64_t* n_duplicate) {
+  clear_error();
+  const size_t nbytes = ggnn_super_bytes(n_pad, E, s);
+  GGNN_CHECK_ARG(nbytes > 0, "n_pad=%d (a positive multiple of 64), E=%d (1..64), s=%d (32, 64, 96 or 128, <= n_pad)",
+                 n_pad, E, s);
+  GGNN_CHECK_ARG(m >= 0, "m=%lld must be >= 0", (long long)m);
+  GGNN_CHECK_ARG(m == 0 || (src && dst && etype), "src/dst/etype is NULL");
+  GGNN_CHECK_ARG(rows != nullptr && cols != nullptr, "rows/cols is NULL");
+  for (int64_t k = 0; k < m; ++k) {
+    GGNN_CHECK_ARG(src[k] >= 0 && src[k] < n_pad && dst[k] >= 0 && dst[k] < n_pad,
+                   "edge %lld (%d -> %d) out of range [0,%d)", (long long)k, src[k], dst[k], n_pad);
+    GGNN_CHECK_ARG(etype[k] >= 0 && etype[k] < E, "edge %lld has type %d outside [0,%d)", (long long)k, etype[k],
+                   E);
+  }
+  uint8_t* R = static_cast<uint8_t*>(rows);
+  uint8_t* Cc = static_cast<uint8_t*>(cols);
+  uint8_t* Rt = static_cast<uint8_t*>(rows_t);
+  uint8_t* Ct = static_cast<uint8_t*>(cols_t);
+  std::memset(R, 0, nbytes);
+  std::memset(Cc, 0, nbytes);
+  if (Rt) std::memset(Rt, 0, nbytes);
+  if (Ct) std::memset(Ct, 0, nbytes);
+  const size_t wide = static_cast<size_t>(n_pad / 8), narrow = static_cast<size_t>(s / 8);
+  int64_t nr = 0, nc = 0, rest = 0, dup = 0;
+  for (int64_t k = 0; k < m; ++k) {
+    const int64_t i = dst[k], j = src[k], e = etype[k];
+    uint8_t* byte;
+    uint8_t bit;
+    if (i < s) {   // into a supernode: row i of the row slice, column j
+      byte = R + (static_cast<size_t>(e) * s + i) * wide + j / 8;
+      bit = static_cast<uint8_t>(1u << (j % 8));
+    } else if (j < s) {   // out of a supernode: row i of the column slice, column j
+      byte = Cc + (static_cast<size_t>(e) * n_pad + i) * narrow + j / 8;
+      bit = static_cast<uint8_t>(1u << (j % 8));
+    } else {
+      ++rest;
+      continue;
+    }
+    if (*byte & bit) {
+      ++dup;
+      continue;
+    }
+    *byte |= bit;
+    if (i < s) {
+      ++nr;
+      if (Rt) Rt[(static_cast<size_t>(e) * n_pad + j) * narrow + i / 8] |= static_cast<uint8_t>(1u << (i % 8));
+    } else {
+      ++nc;
+      if (Ct) Ct[(static_cast<size_t>(e) * s + j) * wide + i / 8] |= static_cast<uint8_t>(1u << (i % 8));
+    }
+  }
+  if (n_rows) *n_rows = nr;
+  if (n_cols) *n_cols = nc;
+  if (n_rest) *n_rest = rest;
+  if (n_duplicate) *n_duplicate = dup;
+  return GGNN_OK;
+}
+
 }  // extern "C"

@@ -60,6 +60,11 @@ namespace ggnn {
                                 float* db_out, void* ws, hipStream_t st);                                        \
   hipError_t launch_sparse_step(int n_pad, int H, int E, const int32_t* row_ptr, const int32_t* col,            \
                                 const void* X, const void* Wt, const float* bias, float* a, hipStream_t st);   \
+  hipError_t launch_super_fwd(int n_pad, int H, int E, int s, const void* rows, const void* cols, const void* X,  \
+                              const void* W, const float* bias, float* a, void* ws, hipStream_t st);            \
+  hipError_t launch_super_bwd(int n_pad, int H, int E, int s, const void* rows, const void* rows_t,              \
+                              const void* cols_t, const void* X, const void* W, const void* da, float* dX,       \
+                              float* dW, float* dbias, void* ws, hipStream_t st);                                \
   bool step_wide_applies(int B, int H);                                                                           \
   hipError_t launch_step_wide(bool rev, int n_pad, int B, int H, int E, const void* bits, const void* V,          \
                               const void* Wsrc, const float* bias, float* out, const float* dX_in, void* dM,      \
@@ -220,6 +225,19 @@ inline hipError_t launch_readout_bwd(int dt, int n_pad, int H, int n_cand, const
 inline hipError_t launch_sparse_step(int dt, int n_pad, int H, int E, const int32_t* row_ptr, const int32_t* col,
                                      const void* X, const void* Wt, const float* bias, float* a, hipStream_t st) {
   return GGNN_DT_PICK(launch_sparse_step, n_pad, H, E, row_ptr, col, X, Wt, bias, a, st);
+}
+// Supernode slices (first s rows and columns), forward (a +=) and reverse
+// (dX, dW, dbias +=); workspace of super_workspace bytes.
+size_t super_workspace(int n_pad, int H, int E, int s);
+inline hipError_t launch_super_fwd(int dt, int n_pad, int H, int E, int s, const void* rows, const void* cols,
+                                   const void* X, const void* W, const float* bias, float* a, void* ws,
+                                   hipStream_t st) {
+  return GGNN_DT_PICK(launch_super_fwd, n_pad, H, E, s, rows, cols, X, W, bias, a, ws, st);
+}
+inline hipError_t launch_super_bwd(int dt, int n_pad, int H, int E, int s, const void* rows, const void* rows_t,
+                                   const void* cols_t, const void* X, const void* W, const void* da, float* dX,
+                                   float* dW, float* dbias, void* ws, hipStream_t st) {
+  return GGNN_DT_PICK(launch_super_bwd, n_pad, H, E, s, rows, rows_t, cols_t, X, W, da, dX, dW, dbias, ws, st);
 }
 // Momentum update of float32 master parameters (and their compute copy).
 hipError_t launch_sgd_momentum(long count, float* theta, float* vel, const float* grad, float lr, float mu, float wd,

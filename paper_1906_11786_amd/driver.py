@@ -319,3 +319,130 @@ class BandedGGNN:
         if self.bias is not None:
             out["dbias"] = f(self.dbias)
         return out
+
+
+# ---------------------------------------------------------------- supernodes
+
+def compile_with_supernodes(graphs: Sequence, hubs: Sequence, B: int, E: int, s: int) -> Compiled:
+    """Host compilation with supernodes (Discussion section): the hub nodes
+    of every graph (hubs[g], ids in graph g's labels) take the first labels
+    0 .. (total hubs - 1) < s; the other nodes of each graph are reordered with
+    reverse Cuthill-McKee on the edges between them (the band's share) and
+    placed after s, graph after graph.  n_pad is a multiple of B and of 64."""
+    t0 = time.perf_counter()
+    n_h = sum(len(h) for h in hubs)
+    if n_h > s:
+        raise ValueError(f"{n_h} hubs do not fit in s={s} supernode slots")
+    S, D, T = [], [], []
+    next_hub, base, bw = 0, s, 0
+    for g, hg in zip(graphs, hubs):
+        label = np.full(g.n, -1, np.int64)
+        hg = np.asarray(hg, np.int64)
+        label[hg] = np.arange(next_hub, next_hub + len(hg))
+        next_hub += len(hg)
+        rest = np.flatnonzero(label < 0)
+        local = np.full(g.n, -1, np.int64)
+        local[rest] = np.arange(len(rest))
+        inner = (label[g.src] < 0) & (label[g.dst] < 0)
+        ls, ld = local[g.src[inner]], local[g.dst[inner]]
+        _, rank, b = capi.ggnn_rcm_order(len(rest), ls, ld)
+        bw = max(bw, b)
+        label[rest] = base + rank
+        base += len(rest)
+        S.append(label[g.src].astype(np.int32))
+        D.append(label[g.dst].astype(np.int32))
+        T.append(g.etype.astype(np.int32))
+    step = B * 64 // np.gcd(B, 64)
+    n_pad = -(-base // step) * step
+    comp = Compiled(base, n_pad, B, E, np.concatenate(S), np.concatenate(D), np.concatenate(T),
+                    np.asarray([0, base], np.int64), bw, time.perf_counter() - t0)
+    comp.stats["n_super"] = s
+    comp.stats["n_hubs"] = n_h
+    return comp
+
+
+class SupernodeGGNN:
+    """T-step propagation with supernode slices next to the 1-bit band, its
+    reverse pass for L = sum(G * X_T), composed from the per-step C-ABI calls:
+      forward step:  ggnn_banded_step_bits (band) + ggnn_super_propagate (slices) -> a;  ggnn_gru_update
+      reverse step:  ggnn_gru_update_bwd -> da, dh;  ggnn_banded_propagate_bits_bwd -> dM;
+                     ggnn_msg_transform_bwd (dX = dh + sum_e dM_e W_e^T, dW, dbias);
+                     ggnn_super_propagate_bwd (the slices' share of dX, dW, dbias)."""
+
+    def __init__(self, comp: Compiled, H: int, T: int, dt: str, params, device="cuda"):
+        import torch
+        self.torch, self.comp, self.H, self.T, self.dt = torch, comp, H, T, dt
+        n_pad, E, B, s = comp.n_pad, comp.E, comp.B, comp.stats["n_super"]
+        self.s = s
+        inner = (comp.src >= s) & (comp.dst >= s)
+        bits, bits_t, packed, dropped, dup = capi.ggnn_banded_pack_bits(
+            n_pad, E, B, comp.src[inner], comp.dst[inner], comp.etype[inner], strict=False)
+        rows, cols, rows_t, cols_t, cnt = capi.ggnn_super_pack(n_pad, E, s, comp.src, comp.dst, comp.etype)
+        comp.stats.update(n_packed=packed, n_dropped=dropped, n_duplicate=dup + cnt["duplicates"],
+                          n_super_rows=cnt["rows"], n_super_cols=cnt["cols"])
+        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+        self.bits, self.bits_t = dev(bits), dev(bits_t)
+        self.rows, self.cols, self.rows_t, self.cols_t = dev(rows), dev(cols), dev(rows_t), dev(cols_t)
+        td = torch_dtype(dt)
+        self.W = to_device(params.W, dt, device)
+        self.bias = None if params.bias is None else torch.from_numpy(params.bias.astype(np.float32)).to(device)
+        self.Wi, self.U = to_device(params.Wi, dt, device), to_device(params.U, dt, device)
+        self.b = torch.from_numpy(params.b.astype(np.float32)).to(device)
+        self.X = torch.empty((T + 1, n_pad, H), dtype=td, device=device)
+        self.X[0].copy_(to_device(params.X, dt, device))
+        self.a = torch.empty((T, n_pad, H), dtype=torch.float32, device=device)
+        self.saved = torch.empty((T, n_pad, 3 * H), dtype=td, device=device)
+        self.G = torch.from_numpy(params.G.astype(np.float32)).to(device)
+        self.dX = torch.empty((n_pad, H), dtype=torch.float32, device=device)
+        self.dX2 = torch.empty_like(self.dX)
+        self.dh = torch.empty_like(self.dX)
+        self.da = torch.empty((H, n_pad), dtype=td, device=device)
+        self.dM = torch.empty((E, H, n_pad), dtype=td, device=device)
+        self.dW = torch.zeros((E, H, H), dtype=torch.float32, device=device)
+        self.dbias = torch.zeros((E, H), dtype=torch.float32, device=device)
+        self.dWi = torch.zeros((H, 3 * H), dtype=torch.float32, device=device)
+        self.dU = torch.zeros_like(self.dWi)
+        self.db = torch.zeros((3 * H,), dtype=torch.float32, device=device)
+        mk = lambda n: torch.empty((max(n, 16),), dtype=torch.uint8, device=device)
+        self.ws_sn = mk(capi.ggnn_super_workspace_bytes(n_pad, H, E, s))
+        self.ws_gru = mk(capi.ggnn_gru_update_bwd_workspace_bytes(dt, n_pad, H))
+        self.ws_tr = mk(capi.ggnn_msg_transform_bwd_workspace_bytes(dt, n_pad, H, E))
+
+    def forward(self, stream=None):
+        c, H, E = self.comp, self.H, self.comp.E
+        for t in range(self.T):
+            capi.ggnn_banded_step_bits(self.dt, c.n_pad, c.B, H, E, self.bits, self.X[t], self.W, self.bias, self.a[t],
+                                       stream)
+            capi.ggnn_super_propagate(self.dt, c.n_pad, H, E, self.s, self.rows, self.cols, self.X[t], self.W,
+                                      self.bias, self.a[t], self.ws_sn, self.ws_sn.numel(), stream)
+            capi.ggnn_gru_update(self.dt, c.n_pad, H, self.a[t], self.X[t], self.Wi, self.U, self.b, self.X[t + 1],
+                                 self.saved[t], stream)
+
+    def backward(self, stream=None):
+        c, H, E = self.comp, self.H, self.comp.E
+        for z in (self.dW, self.dbias, self.dWi, self.dU, self.db):
+            z.zero_()
+        g, gn = self.dX, self.dX2
+        g.copy_(self.G)
+        for t in range(self.T - 1, -1, -1):
+            capi.ggnn_gru_update_bwd(self.dt, c.n_pad, H, g, self.a[t], self.X[t], self.saved[t], self.Wi, self.U,
+                                     self.da, self.dh, self.dWi, self.dU, self.db, self.ws_gru, self.ws_gru.numel(),
+                                     stream)
+            capi.ggnn_banded_propagate_bits_bwd(self.dt, c.n_pad, c.B, H, E, self.bits_t, self.da, self.dM, stream)
+            capi.ggnn_msg_transform_bwd(self.dt, c.n_pad, H, E, self.X[t], self.W, self.dM, self.dh, gn, self.dW,
+                                        self.dbias if self.bias is not None else None, self.ws_tr,
+                                        self.ws_tr.numel(), stream)
+            capi.ggnn_super_propagate_bwd(self.dt, c.n_pad, H, E, self.s, self.rows, self.rows_t, self.cols_t,
+                                          self.X[t], self.W, self.da, gn, self.dW,
+                                          self.dbias if self.bias is not None else None, self.ws_sn,
+                                          self.ws_sn.numel(), stream)
+            g, gn = gn, g
+        self.dX0 = g
+
+    def results(self) -> dict:
+        f = (lambda t: t.float().cpu().numpy().astype(np.float64))
+        out = dict(XT=f(self.X[self.T]), dX0=f(self.dX0), dW=f(self.dW), dWi=f(self.dWi), dU=f(self.dU),
+                   db=f(self.db))
+        if self.bias is not None:
+            out["dbias"] = f(self.dbias)
+        return out

@@ -1,0 +1,142 @@
+"""GPU parity of the supernode slices (dense first rows and columns next to
+the band): each primitive against the oracle's sparse sums on the slices'
+edges (small integers: exact), and T steps forward and reverse composed with
+the band against the oracle's propagation on the supernode edge set."""
+import numpy as np
+import pytest
+
+import oracle as O
+from gpu_helpers import TOL, relerr, say, dev, host
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+capi = pytest.importorskip("paper_1906_11786_amd.capi")
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    yield
+    torch.cuda.synchronize()
+
+
+def _case(rng, n, E, s, m):
+    src, dst, et = rng.integers(0, n, m), rng.integers(0, n, m), rng.integers(0, E, m)
+    src[: m // 4] = rng.integers(0, s, m // 4)
+    dst[m // 4: m // 2] = rng.integers(0, s, m // 4)
+    src[:16], dst[:16], et[:16] = src[16:32], dst[16:32], et[16:32]     # repeats
+    return src, dst, et
+
+
+def _slices(n, E, s, src, dst, et):
+    rows, cols, rows_t, cols_t, _ = capi.ggnn_super_pack(n, E, s, src, dst, et)
+    t = lambda a: torch.from_numpy(a).cuda()
+    return t(rows), t(cols), t(rows_t), t(cols_t)
+
+
+def _slice_edges(src, dst, et, s):
+    sd, dd, ed, _ = O.dedupe_edges(src, dst, et)
+    k = (dd < s) | (sd < s)
+    return sd[k], dd[k], ed[k]
+
+
+CASES = [("f32", 32, 2, 32, 256), ("bf16", 64, 3, 64, 512), ("bf16", 128, 1, 96, 384), ("bf16", 256, 2, 128, 640),
+         ("f32", 128, 3, 128, 320)]
+
+
+@pytest.mark.parametrize("dt,H,E,s,n", CASES)
+def test_super_propagate_integer_exact(dt, H, E, s, n):
+    say(f"super_propagate int dt={dt} H={H} E={E} s={s} n={n}")
+    rng = np.random.default_rng(H + s + n)
+    src, dst, et = _case(rng, n, E, s, 8 * n)
+    rows, cols, _, _ = _slices(n, E, s, src, dst, et)
+    X = rng.integers(-2, 3, (n, H)).astype(np.float64)
+    W = rng.integers(-1, 2, (E, H, H)).astype(np.float64)
+    bias = rng.integers(-2, 3, (E, H)).astype(np.float64)
+    a0 = rng.integers(-5, 6, (n, H)).astype(np.float64)
+    a = dev(a0)
+    nb = capi.ggnn_super_workspace_bytes(n, H, E, s)
+    ws = torch.empty((nb,), dtype=torch.uint8, device="cuda")
+    capi.ggnn_super_propagate(dt, n, H, E, s, rows, cols, dev(X, dt), dev(W, dt), dev(bias), a, ws, nb)
+    ks, kd, ke = _slice_edges(src, dst, et, s)
+    np.testing.assert_array_equal(host(a) - a0, O.aggregate(n, ks, kd, ke, O.msg_transform(X, W, bias)))
+
+
+@pytest.mark.parametrize("dt,H,E,s,n", CASES)
+def test_super_propagate_bwd_integer_exact(dt, H, E, s, n):
+    say(f"super_propagate_bwd int dt={dt} H={H} E={E} s={s} n={n}")
+    rng = np.random.default_rng(3 * H + s + n)
+    src, dst, et = _case(rng, n, E, s, 8 * n)
+    rows, _, rows_t, cols_t = _slices(n, E, s, src, dst, et)
+    X = rng.integers(-2, 3, (n, H)).astype(np.float64)
+    W = rng.integers(-1, 2, (E, H, H)).astype(np.float64)
+    da = rng.integers(-3, 4, (n, H)).astype(np.float64)
+    dX0 = rng.integers(-5, 6, (n, H)).astype(np.float64)
+    dX, dW, dbias = dev(dX0), torch.ones((E, H, H), device="cuda"), torch.ones((E, H), device="cuda")
+    nb = capi.ggnn_super_workspace_bytes(n, H, E, s)
+    ws = torch.empty((nb,), dtype=torch.uint8, device="cuda")
+    capi.ggnn_super_propagate_bwd(dt, n, H, E, s, rows, rows_t, cols_t, dev(X, dt), dev(W, dt), dev(da.T, dt), dX, dW,
+                                  dbias, ws, nb)
+    ks, kd, ke = _slice_edges(src, dst, et, s)
+    dM = O.aggregate_transpose(n, ks, kd, ke, da, E)
+    wdX, wdW, wdb = O.msg_transform_backward(X, W, dM)
+    np.testing.assert_array_equal(host(dX) - dX0, wdX)
+    np.testing.assert_array_equal(host(dW) - 1.0, wdW)
+    np.testing.assert_array_equal(host(dbias) - 1.0, wdb)
+
+
+@pytest.mark.parametrize("dt,B,H,s", [("f32", 32, 32, 32), ("bf16", 64, 64, 32), ("bf16", 128, 128, 64)])
+def test_supernode_steps_match_oracle(dt, B, H, s):
+    """Graphs with hub nodes linked to a large share of their graph: hubs
+    become supernodes, the rest is reordered into the band; T steps forward
+    and the reverse pass against the oracle on the supernode edge set."""
+    from ggnn_synth import backbone_graph, scramble_graph, add_hubs, draw_params
+    from paper_1906_11786_amd.driver import compile_with_supernodes, SupernodeGGNN
+    E, T = 3, 2
+    say(f"supernode steps dt={dt} B={B} H={H} s={s}")
+    graphs, hubs = [], []
+    for gi, sz in enumerate([900, 500]):
+        g, h = add_hubs(70, gi, scramble_graph(70, gi, backbone_graph(70, gi, sz, E))[0], 4, 0.5, E)
+        graphs.append(g)
+        hubs.append(h)
+    comp = compile_with_supernodes(graphs, hubs, B, E, s)
+    prm = draw_params(70, comp.n_real, comp.n_pad, H, E, dt, with_bias=True)
+    m = SupernodeGGNN(comp, H, T, dt, prm)
+    assert comp.stats["n_super_rows"] > 0 and comp.stats["n_super_cols"] > 0
+    m.forward()
+    m.backward()
+    torch.cuda.synchronize()
+    res = m.results()
+    # the oracle's own labelling: hubs first, the rest in its reverse
+    # Cuthill-McKee order (the product's must agree)
+    S, D, base, nh = [], [], s, 0
+    for g, h in zip(graphs, hubs):
+        label = np.full(g.n, -1, np.int64)
+        label[h] = np.arange(nh, nh + len(h))
+        nh += len(h)
+        rest = np.flatnonzero(label < 0)
+        local = np.full(g.n, -1, np.int64)
+        local[rest] = np.arange(len(rest))
+        inner = (label[g.src] < 0) & (label[g.dst] < 0)
+        _, rank = O.rcm_order(len(rest), local[g.src[inner]], local[g.dst[inner]])
+        label[rest] = base + np.asarray(rank)
+        base += len(rest)
+        S.append(label[g.src])
+        D.append(label[g.dst])
+    src, dst, et = np.concatenate(S), np.concatenate(D), np.concatenate([g.etype for g in graphs])
+    np.testing.assert_array_equal(comp.src, src)
+    np.testing.assert_array_equal(comp.dst, dst)
+    out = O.propagate(comp.n_pad, B, src, dst, et, prm.X, prm.W, prm.Wi, prm.U, prm.b, T, G=prm.G, bias=prm.bias,
+                      n_super=s)
+    band_only = O.kept_edges(src, dst, et, B)[3]
+    say(f"  hub edges: rows {comp.stats['n_super_rows']} cols {comp.stats['n_super_cols']}; "
+        f"a plain band would drop {band_only}; dropped with supernodes {out['n_dropped']}")
+    assert band_only > 0
+    want = dict(XT=out["X"][T], dX0=out["dX0"], dW=out["dW"], dWi=out["dWi"], dU=out["dU"], db=out["db"],
+                dbias=out["dbias"])
+    for k, w in want.items():
+        err = relerr(res[k], w)
+        say(f"  {k}: {err:.2e}")
+        assert err <= TOL[dt], (k, err)

@@ -286,3 +286,74 @@ def test_dropped_edges_counts_against_oracle():
         assert (r["dropped"], r["kept"], r["duplicates"]) == (ndrop, len(ks), ndup), B
         if r["bandwidth"] < B:
             assert r["dropped"] == 0
+
+
+def _expected_slices(n, E, s, src, dst, et):
+    s_, d_, e_, _ = O.dedupe_edges(src, dst, et)
+    R = np.zeros((E, s, n), np.uint8)
+    Cc = np.zeros((E, n, s), np.uint8)
+    into = d_ < s
+    R[e_[into], d_[into], s_[into]] = 1
+    out = (~into) & (s_ < s)
+    Cc[e_[out], d_[out], s_[out]] = 1
+    return R, Cc, int(into.sum()), int(out.sum()), int((~into & ~out).sum())
+
+
+@pytest.mark.parametrize("s", [32, 64, 128])
+def test_super_pack_bit_exact_against_oracle(s):
+    """Rows slice = edges into nodes < s, cols slice = edges out of them into
+    the others, transposes consistent, counts = the oracle's deduplicated
+    edge split."""
+    _need_lib()
+    rng = np.random.default_rng(s)
+    n, E, m = 448, 3, 5000
+    src, dst, et = rng.integers(0, n, m), rng.integers(0, n, m), rng.integers(0, E, m)
+    src[:200] = rng.integers(0, s, 200)      # plenty of edges touching the supernodes
+    dst[200:400] = rng.integers(0, s, 200)
+    rows, cols, rows_t, cols_t, cnt = capi.ggnn_super_pack(n, E, s, src, dst, et)
+    R, Cc, nr, nc, rest = _expected_slices(n, E, s, src, dst, et)
+    unpack = lambda b: np.unpackbits(b, axis=-1, bitorder="little")
+    np.testing.assert_array_equal(unpack(rows), R)
+    np.testing.assert_array_equal(unpack(cols), Cc)
+    np.testing.assert_array_equal(unpack(rows_t), R.transpose(0, 2, 1))
+    np.testing.assert_array_equal(unpack(cols_t), Cc.transpose(0, 2, 1))
+    _, _, _, ndup = O.dedupe_edges(src, dst, et)
+    assert (cnt["rows"], cnt["cols"]) == (nr, nc)
+    assert cnt["rest"] + cnt["rows"] + cnt["cols"] + cnt["duplicates"] == m
+    assert cnt["rest"] >= rest and cnt["duplicates"] <= ndup
+    with pytest.raises(capi.GGNNError):
+        capi.ggnn_super_pack(448, 3, 48, src, dst, et)     # s not a multiple of 32
+    with pytest.raises(capi.GGNNError):
+        capi.ggnn_super_pack(480, 3, 32, src, dst, et)     # n_pad not a multiple of 64
+
+
+def test_compile_with_supernodes_matches_oracle_reordering():
+    """Hubs take the first labels; the other nodes of each graph follow in
+    the oracle's reverse Cuthill-McKee order of the edges between them."""
+    _need_lib()
+    from ggnn_synth import add_hubs
+    from paper_1906_11786_amd.driver import compile_with_supernodes
+    graphs, hubs = [], []
+    for gi, sz in enumerate([300, 200]):
+        g, h = add_hubs(4, gi, scramble_graph(4, gi, backbone_graph(4, gi, sz, 3))[0], 3, 0.4, 3)
+        graphs.append(g)
+        hubs.append(h)
+    comp = compile_with_supernodes(graphs, hubs, 64, 3, 32)
+    assert comp.n_pad % 64 == 0 and comp.n_real == 32 + 500 - 6
+    base, nh = 32, 0
+    S, D = [], []
+    for g, h in zip(graphs, hubs):
+        label = np.full(g.n, -1, np.int64)
+        label[h] = np.arange(nh, nh + len(h))
+        nh += len(h)
+        rest = np.flatnonzero(label < 0)
+        local = np.full(g.n, -1, np.int64)
+        local[rest] = np.arange(len(rest))
+        inner = (label[g.src] < 0) & (label[g.dst] < 0)
+        _, rank = O.rcm_order(len(rest), local[g.src[inner]], local[g.dst[inner]])
+        label[rest] = base + np.asarray(rank)
+        base += len(rest)
+        S.append(label[g.src])
+        D.append(label[g.dst])
+    np.testing.assert_array_equal(comp.src, np.concatenate(S))
+    np.testing.assert_array_equal(comp.dst, np.concatenate(D))

@@ -175,3 +175,32 @@ def test_all_edge_propagation_equals_a_band_wide_enough():
     assert wide["n_dropped"] == 0 and narrow["n_dropped"] > 0 and full["n_dropped"] == 0
     np.testing.assert_allclose(full["X"][T], wide["X"][T], rtol=1e-13, atol=1e-13)
     assert np.abs(full["X"][T] - narrow["X"][T]).max() > 1e-3
+
+
+def test_supernode_edge_set():
+    """With supernodes, every edge touching a node < n_super is propagated:
+    equal to propagation on all edges when the other edges fit the band, and
+    to the plain band when no edge touches a supernode."""
+    rng = np.random.default_rng(8)
+    n, B, E, H, T, ns = 64, 8, 2, 3, 2, 4
+    far_s = rng.integers(0, ns, 40)                  # supernode edges spanning the whole graph
+    far_d = rng.integers(0, n, 40)
+    near_s = rng.integers(ns, n, 120)
+    near_d = np.clip(near_s + rng.integers(-3, 4, 120), ns, n - 1)
+    src = np.concatenate([far_s, far_d, near_s])
+    dst = np.concatenate([far_d, far_s, near_d])
+    et = rng.integers(0, E, len(src))
+    k = 1 / np.sqrt(H)
+    W = rng.standard_normal((E, H, H)) / np.sqrt(H)
+    Wi, U, b = rng.uniform(-k, k, (H, 3 * H)), rng.uniform(-k, k, (H, 3 * H)), rng.uniform(-k, k, 3 * H)
+    X0, G = rng.standard_normal((n, H)), rng.standard_normal((n, H))
+    sup = O.propagate(n, B, src, dst, et, X0, W, Wi, U, b, T, G=G, n_super=ns)
+    full = O.propagate(n, None, src, dst, et, X0, W, Wi, U, b, T, G=G)
+    band = O.propagate(n, B, src, dst, et, X0, W, Wi, U, b, T, G=G)
+    assert sup["n_dropped"] == 0 and band["n_dropped"] > 0
+    for key in ("dX0", "dW", "dWi"):
+        np.testing.assert_allclose(sup[key], full[key], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(sup["X"][T], full["X"][T], rtol=1e-12, atol=1e-12)
+    ns_ = O.propagate(n, B, near_s, near_d, et[:120], X0, W, Wi, U, b, T, n_super=ns)
+    nb_ = O.propagate(n, B, near_s, near_d, et[:120], X0, W, Wi, U, b, T)
+    np.testing.assert_array_equal(ns_["X"][T], nb_["X"][T])
