@@ -80,6 +80,10 @@ def parse():
     p.add_argument("--no-train", action="store_true",
                    help="skip the timing of one training step (readout, loss and Momentum update included)")
     p.add_argument("--eager", action="store_true", help="time eager launches only (no HIP graph replay)")
+    p.add_argument("--supernodes", type=int, default=0, metavar="S",
+                   help="also time T steps forward and reverse with S supernode slots next to the band, on the "
+                        "workload's graphs with added hub nodes (two per graph linked to 10%% of it); reported in "
+                        "config.supernodes")
     p.add_argument("--drops", action="store_true",
                    help="host only: print the edges each block size keeps and drops on the workload's graphs "
                         "(with and without reordering, and with long-span variants of the graphs), then exit")
@@ -245,6 +249,42 @@ def cpu_baseline(spec, graphs, comp, params):
                       f"{dt:.1f} s"}
 
 
+def time_supernodes(spec, graphs, s, timed, torch):
+    """T steps forward and reverse with supernode slices next to the band
+    (SupernodeGGNN: per-step calls), on the workload's graphs with two hub
+    nodes per graph linked both ways to 10% of it; the slices' own calls
+    timed alone."""
+    from ggnn_synth import add_hubs, draw_params
+    from paper_1906_11786_amd import capi
+    from paper_1906_11786_amd.driver import compile_with_supernodes, SupernodeGGNN
+    hubbed, hubs = [], []
+    budget = s
+    for gi, g in enumerate(graphs):
+        k = 2 if budget >= 2 else 0
+        budget -= k
+        g2, h = add_hubs(spec.cfg, gi, g, k, 0.1, spec.E) if k else (g, np.zeros(0, np.int32))
+        hubbed.append(g2)
+        hubs.append(h)
+    comp = compile_with_supernodes(hubbed, hubs, spec.B, spec.E, s)
+    params = draw_params(spec.cfg, comp.n_real, comp.n_pad, spec.H, spec.E, spec.dtype)
+    m = SupernodeGGNN(comp, spec.H, spec.T, spec.dtype, params)
+    step_s = timed(lambda: (m.forward(), m.backward()))
+    n_pad, H, E = comp.n_pad, spec.H, spec.E
+    fwd_s = timed(lambda: capi.ggnn_super_propagate(spec.dtype, n_pad, H, E, s, m.rows, m.cols, m.X[0], m.W, m.bias,
+                                                    m.a[0], m.ws_sn, m.ws_sn.numel()))
+    bwd_s = timed(lambda: capi.ggnn_super_propagate_bwd(spec.dtype, n_pad, H, E, s, m.rows, m.rows_t, m.cols_t,
+                                                        m.X[0], m.W, m.da, m.dX, m.dW, m.bias, m.ws_sn,
+                                                        m.ws_sn.numel()))
+    st = comp.stats
+    out = {"n_super": s, "hubs": st["n_hubs"], "hub_edges_rows": st["n_super_rows"],
+           "hub_edges_cols": st["n_super_cols"], "band_edges": st["n_packed"], "dropped": st["n_dropped"],
+           "ms_per_step_composed": round(step_s * 1e3, 4), "ms_super_propagate": round(fwd_s * 1e3, 4),
+           "ms_super_propagate_bwd": round(bwd_s * 1e3, 4)}
+    del m
+    torch.cuda.empty_cache()
+    return out
+
+
 def drops_table(spec_name: str) -> str:
     """Dropped-edge fraction against the block size (the coverage remark
     after Eq. 3) on the workload's graphs: host reordering and packing only.
@@ -347,6 +387,10 @@ def main():
         eval_band_s = timed(lambda: (m.forward(), m.readout()))
         eval_sparse_s = timed(m.evaluate_sparse)
 
+    supernodes = None
+    if args.supernodes:
+        supernodes = time_supernodes(spec, graphs, args.supernodes, timed, torch)
+
     # Roofline of the banded kernels: each launch timed with HIP events on the
     # stream it runs on, in the same launch shape as inside the step.
     es = 2 if spec.dtype == "bf16" else 4
@@ -424,6 +468,7 @@ def main():
                    "ms_per_train_step": None if train_s is None else round(train_s * 1e3, 4),
                    "ms_eval_band": None if eval_band_s is None else round(eval_band_s * 1e3, 4),
                    "ms_eval_sparse_all_edges": None if eval_sparse_s is None else round(eval_sparse_s * 1e3, 4),
+                   "supernodes": supernodes,
                    "host_compile_s": round(comp.rcm_seconds + comp.stats.get("pack_seconds", 0.0), 3),
                    "generate_s": round(gen_s, 3)},
         "roofline": roofline,
