@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define GGNN_ABI_VERSION 7
+#define GGNN_ABI_VERSION 8
 
 typedef enum {
   GGNN_OK = 0,
@@ -247,6 +247,22 @@ ggnn_status ggnn_step_bits_gru(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t 
  * ggnn_step_bits_gru and of ggnn_model). */
 ggnn_status ggnn_transpose_weights(ggnn_dtype dt, int32_t H, int32_t E, const void* W, void* Wt, void* stream);
 
+/* GRU weights repacked for the large-width GRU kernels (bf16, H = 128 or 256):
+ * those kernels stream Wi and U through on-chip memory in stages, and the
+ * packed copy holds every stage's 16-byte pieces in the order they are
+ * staged, so staging becomes contiguous loads.  The packing is a pure
+ * reordering of the elements of Wi and U (the GRU of Eq. 1 is unchanged):
+ * results with and without it are bitwise identical.  An optional operand of
+ * ggnn_model (gru_packed).
+ * ggnn_gru_pack_bytes: bytes of the packed copy, 12 H^2 elements of dt; 0 where
+ *   no kernel reads it (float32, or H < 128), and then ggnn_gru_pack_weights
+ *   does nothing and `packed` may be NULL.
+ * ggnn_gru_pack_weights: Wi, U [H][3H] dt (device); packed: device memory of
+ *   ggnn_gru_pack_bytes bytes, 16-byte aligned, overlapping neither. */
+size_t ggnn_gru_pack_bytes(ggnn_dtype dt, int32_t H);
+ggnn_status ggnn_gru_pack_weights(ggnn_dtype dt, int32_t H, const void* Wi, const void* U, void* packed,
+                                  void* stream);
+
 /* One reverse step on a 1-bit band, the form ggnn_backward runs for t > 0:
  * the reverse of step t's propagation (ggnn_banded_step_bits_bwd: dM_e =
  * A_e^T da and g = dX_in + sum_e dM_e W_e^T), then the reverse of step t-1's
@@ -323,6 +339,8 @@ typedef struct ggnn_model {
   const void* Wt;       /* [E][H][H] dt, W_e^T (Wt[e][o][h] = W[e][h][o], ggnn_transpose_weights), or NULL.
                            Optional: lets the bit-band forward read its weight fragments as rows; the
                            caller refreshes it whenever W changes. */
+  const void* gru_packed; /* Wi, U as ggnn_gru_pack_weights lays them out, or NULL (optional, used where
+                             ggnn_gru_pack_bytes > 0; the caller refreshes it whenever Wi or U change). */
 } ggnn_model;
 
 typedef struct ggnn_activations {

@@ -31,6 +31,7 @@ EXPORTS = [
     "ggnn_rcm_order", "ggnn_bandwidth", "ggnn_band_bytes", "ggnn_banded_pack",
     "ggnn_band_bits_bytes", "ggnn_banded_pack_bits", "ggnn_banded_step_bits", "ggnn_banded_propagate_bits_bwd",
     "ggnn_banded_step_bits_bwd", "ggnn_step_bits_gru", "ggnn_step_bits_gru_bwd", "ggnn_transpose_weights",
+    "ggnn_gru_pack_bytes", "ggnn_gru_pack_weights",
     "ggnn_msg_transform", "ggnn_banded_propagate", "ggnn_gru_update",
     "ggnn_gru_update_bwd_workspace_bytes", "ggnn_gru_update_bwd",
     "ggnn_banded_propagate_bwd", "ggnn_msg_transform_bwd_workspace_bytes", "ggnn_msg_transform_bwd",
@@ -53,7 +54,8 @@ class ggnn_model(C.Structure):
     _fields_ = [("dtype", C.c_int32), ("n_pad", C.c_int32), ("B", C.c_int32), ("H", C.c_int32),
                 ("E", C.c_int32), ("T", C.c_int32), ("band", C.c_void_p), ("W", C.c_void_p),
                 ("bias", C.c_void_p), ("Wi", C.c_void_p), ("U", C.c_void_p), ("b", C.c_void_p),
-                ("band_format", C.c_int32), ("band_t", C.c_void_p), ("Wt", C.c_void_p)]
+                ("band_format", C.c_int32), ("band_t", C.c_void_p), ("Wt", C.c_void_p),
+                ("gru_packed", C.c_void_p)]
 
 
 class ggnn_activations(C.Structure):
@@ -86,6 +88,8 @@ _SIGS = {
     "ggnn_banded_step_bits_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, i64, vp]),
     "ggnn_step_bits_gru": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
     "ggnn_transpose_weights": (C.c_int, [C.c_int, i32, i32, vp, vp, vp]),
+    "ggnn_gru_pack_bytes": (sz, [C.c_int, i32]),
+    "ggnn_gru_pack_weights": (C.c_int, [C.c_int, i32, vp, vp, vp, vp]),
     "ggnn_step_bits_gru_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp,
                                          vp, vp, vp]),
     "ggnn_msg_transform": (C.c_int, [C.c_int, i32, i32, i32, vp, vp, vp, vp, vp]),
@@ -162,6 +166,11 @@ def _i32(a) -> np.ndarray:
 
 
 # ---------------------------------------------------------------- host calls
+
+# Interface version this binding is written against (GGNN_ABI_VERSION of
+# include/ggnn.h); the library must report the same number.
+ABI_VERSION = 8
+
 
 def ggnn_abi_version() -> int:
     return lib().ggnn_abi_version()
@@ -264,6 +273,15 @@ def ggnn_step_bits_gru(dt, n_pad, B, H, E, bits, X, W, Wt, bias, Wi, U, b, a, h_
 def ggnn_transpose_weights(dt, H, E, W, Wt, stream=None):
     _check("ggnn_transpose_weights", lib().ggnn_transpose_weights(_dt(dt), H, E, _ptr(W), _ptr(Wt),
                                                                     _stream(stream)))
+
+
+def ggnn_gru_pack_bytes(dt, H) -> int:
+    return int(lib().ggnn_gru_pack_bytes(_dt(dt), H))
+
+
+def ggnn_gru_pack_weights(dt, H, Wi, U, packed, stream=None):
+    _check("ggnn_gru_pack_weights", lib().ggnn_gru_pack_weights(_dt(dt), H, _ptr(Wi), _ptr(U), _ptr(packed),
+                                                                  _stream(stream)))
 
 
 def ggnn_step_bits_gru_bwd(dt, n_pad, B, H, E, bits_t, da, W, dX_in, dM, ldm, Wi, U, h_prev, saved_prev, da_prev,

@@ -217,6 +217,31 @@ ggnn_status ggnn_transpose_weights(ggnn_dtype dt, int32_t H, int32_t E, const vo
   return device_status(launch_transpose_weights(dt, H, E, W, Wt, as_stream(stream)), "transpose_weights");
 }
 
+size_t ggnn_gru_pack_bytes(ggnn_dtype dt, int32_t H) {
+  if (!supported_dtype(dt) || !supported_H(H)) return 0;
+  return gru_pack_bytes(dt, H);
+}
+
+ggnn_status ggnn_gru_pack_weights(ggnn_dtype dt, int32_t H, const void* Wi, const void* U, void* packed,
+                                  void* stream) {
+  clear_error();
+  GGNN_CHECK_ARG(supported_dtype(dt), "unknown dtype %d", dt);
+  GGNN_CHECK_ARG(supported_H(H), "H=%d must be one of 32, 64, 128, 256", H);
+  const size_t bytes = gru_pack_bytes(dt, H);
+  if (bytes == 0) return GGNN_OK;   // no kernel reads the packed form
+  CHECK_PTR(Wi, "Wi");
+  CHECK_PTR(U, "U");
+  CHECK_PTR(packed, "packed");
+  const size_t wb = (size_t)H * 3 * H * dtype_bytes(dt);
+  auto disjoint = [](const void* p, size_t pb, const void* q, size_t qb) {
+    const char *a = static_cast<const char*>(p), *c = static_cast<const char*>(q);
+    return a + pb <= c || c + qb <= a;
+  };
+  GGNN_CHECK_ARG(disjoint(packed, bytes, Wi, wb) && disjoint(packed, bytes, U, wb),
+                 "packed must not overlap Wi or U");
+  return device_status(launch_gru_pack(dt, H, Wi, U, packed, as_stream(stream)), "gru_pack_weights");
+}
+
 ggnn_status ggnn_step_bits_gru(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E, const void* bits,
                                const void* X, const void* W, const void* Wt, const float* bias, const void* Wi,
                                const void* U, const float* b, float* a, void* h_out, void* saved, void* stream) {
@@ -324,6 +349,7 @@ static ggnn_status check_model(const ggnn_model* m) {
                  "unknown band_format %d", m->band_format);
   if (m->band_format == GGNN_BAND_BITS) CHECK_PTR(m->band_t, "model.band_t");
   CHECK_OPT_PTR(m->Wt, "model.Wt");
+  CHECK_OPT_PTR(m->gru_packed, "model.gru_packed");
   return GGNN_OK;
 }
 
@@ -354,6 +380,7 @@ ggnn_status ggnn_forward(const ggnn_model* m, const ggnn_activations* act, void*
   const size_t es = dtype_bytes(m->dtype);
   const size_t xs = (size_t)m->n_pad * m->H;
   hipStream_t s = as_stream(stream);
+  const void* gru_pk = gru_pack_bytes(m->dtype, m->H) ? m->gru_packed : nullptr;
   for (int t = 0; t < m->T; ++t) {
     const char* Xt = static_cast<const char*>(act->X) + t * xs * es;
     char* Xn = static_cast<char*>(act->X) + (t + 1) * xs * es;
@@ -369,7 +396,7 @@ ggnn_status ggnn_forward(const ggnn_model* m, const ggnn_activations* act, void*
       if (err == hipSuccess) err = launch_banded_fwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, act->M, at, s);
     }
     if (err == hipSuccess && !fused)
-      err = launch_gru_fwd(m->dtype, m->n_pad, m->H, at, Xt, m->Wi, m->U, m->b, Xn, sv, s);
+      err = launch_gru_fwd(m->dtype, m->n_pad, m->H, at, Xt, m->Wi, m->U, m->b, Xn, sv, s, gru_pk);
     if (err != hipSuccess) return device_status(err, "forward");
   }
   return GGNN_OK;
@@ -400,6 +427,7 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
   const long K = (long)m->T * m->n_pad;   // rows of the weight-gradient contractions; also the dM row length
   hipStream_t s = as_stream(stream);
   float* dbias = m->bias ? gr->dbias : nullptr;
+  const void* gru_pk = gru_pack_bytes(m->dtype, m->H) ? m->gru_packed : nullptr;
   char* ws = static_cast<char*>(gr->workspace);
   char* ghat = ws + L.ghat;
   // Node passes, t = T-1..0.  The weight gradients are sums over steps and
@@ -417,7 +445,7 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
     float* dh_b[2] = {gr->dh, reinterpret_cast<float*>(ws + L.dh2)};
     int cur = 0;
     hipError_t err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xs(m->T - 1), Ss(m->T - 1), m->Wi, m->U,
-                                          da_b[0], dh_b[0], Gs(m->T - 1), s);
+                                          da_b[0], dh_b[0], Gs(m->T - 1), s, gru_pk);
     if (err != hipSuccess) return device_status(err, "backward");
     for (int t = m->T - 1; t >= 0; --t) {
       char* dMr = static_cast<char*>(gr->dM) + (size_t)t * m->n_pad * m->H * es;   // node-major rows of step t
@@ -428,7 +456,7 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
                                        dh_b[1 - cur], Gs(t - 1), &fused, s);
         if (err == hipSuccess && !fused)
           err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xs(t - 1), Ss(t - 1), m->Wi, m->U,
-                                     da_b[1 - cur], dh_b[1 - cur], Gs(t - 1), s);
+                                     da_b[1 - cur], dh_b[1 - cur], Gs(t - 1), s, gru_pk);
       } else {
         err = launch_step_bwd_bits(m->dtype, m->n_pad, m->B, m->H, m->E, m->band_t, da_b[cur], m->W, dh_b[cur],
                                    gr->dX, dMr, K, s);
@@ -440,19 +468,24 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
     for (int t = m->T - 1; t >= 0; --t) {
       char* dMt = static_cast<char*>(gr->dM) + (size_t)t * m->n_pad * es;   // feature-major columns of step t
       hipError_t err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xs(t), Ss(t), m->Wi, m->U, gr->da,
-                                            gr->dh, Gs(t), s);
+                                            gr->dh, Gs(t), s, gru_pk);
       if (err == hipSuccess) err = launch_banded_bwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, gr->da, dMt, K, s);
       if (err == hipSuccess)
         err = launch_transform_bwd_dx(m->dtype, m->n_pad, m->H, m->E, m->W, dMt, K, gr->dh, gr->dX, s);
       if (err != hipSuccess) return device_status(err, "backward");
     }
   }
+  // The weight-gradient contractions leave per-split partials; their
+  // fixed-order reductions then run as one launch.
+  ReduceList red;
   hipError_t err = launch_gru_wgrad(m->dtype, K, m->H, act->a, act->X, act->saved, ghat, gr->dWi, gr->dU, gr->db,
-                                    ws + L.gru_part, s);
+                                    ws + L.gru_part, s, &red);
   if (err == hipSuccess)
     err = m->band_format == GGNN_BAND_BITS
-              ? launch_transform_wgrad_nm(m->dtype, K, m->H, m->E, act->X, gr->dM, K, gr->dW, dbias, ws + L.tr_part, s)
+              ? launch_transform_wgrad_nm(m->dtype, K, m->H, m->E, act->X, gr->dM, K, gr->dW, dbias, ws + L.tr_part, s,
+                                          &red)
               : launch_transform_wgrad(m->dtype, K, m->H, m->E, act->X, gr->dM, K, gr->dW, dbias, ws + L.tr_part, s);
+  if (err == hipSuccess) err = launch_reduce_multi(red, s);
   return device_status(err, "backward");
 }
 

@@ -213,6 +213,119 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
 }
 
 // ---------------------------------------------------------------------------
+// Weight staging of the large-H kernels.  Both stream Wi and U through LDS in
+// stages kept in fragment order; a staging unit is one lane vector (eight
+// elements, 16 bytes) of one fragment, and unit `lin` of a stage lands at
+// element 8 lin of the stage buffer.  The units are gathered from the
+// row-major weights, or copied from a packed array that holds every stage's
+// units back to back (GruPack), which turns staging into contiguous 16-byte
+// loads.
+//   forward stage s < NC:  16 columns 16s.. of gate r, blocks {Wi, U};
+//   forward stage s >= NC: 16 columns of gates z and n, {Wi_z, U_z, Wi_n, U_n};
+//     block unit (kk, lane (qq, gg)): column qq of the tile at input rows
+//     32kk + 4gg + {0..3}, 32kk + 16 + 4gg + {0..3};
+//   reverse pass 1, block m: U rows 16m.., gate n, fragments kk;
+//   reverse pass 2, block m: Wi rows 16m.., gates r, z, n, then U gates r, z;
+//     unit (gate, kk, lane (qq, gg)): row 16m + qq at gate columns
+//     32kk + 4gg + {0..3}, 32kk + 16 + 4gg + {0..3}.
+// ---------------------------------------------------------------------------
+template <int H>
+struct GruPack {
+  static constexpr int KS = H / 32, NC = H / 16, FRU = KS * 64;   // units per 16-wide block
+  static constexpr int UNITS = 6 * NC * FRU;                      // units per region (6 H^2 / 8)
+  // first unit of forward stage s / reverse block m of pass p
+  __host__ __device__ static constexpr int fwd_stage(int s) {
+    return s < NC ? 2 * s * FRU : 2 * NC * FRU + 4 * (s - NC) * FRU;
+  }
+  __host__ __device__ static constexpr int rev_stage(int p, int m) {
+    return p == 1 ? m * FRU : NC * FRU + 5 * m * FRU;
+  }
+};
+
+template <typename S, int H>
+__device__ __forceinline__ u32x4 gru_fwd_unit(const S* __restrict__ Wi, const S* __restrict__ U, int s, int lin) {
+  constexpr int NC = H / 16, UPB = GruPack<H>::FRU;
+  const int blk = lin / UPB, rem = lin % UPB;
+  const int kk = rem / 64, l = rem % 64, qq = l % 16, gg = l / 16;
+  const int t16 = s < NC ? s : s - NC;
+  const int gate = s < NC ? 0 : 1 + blk / 2;
+  const S* src = ((blk % 2) ? U : Wi) + gate * H + 16 * t16 + qq;
+  const int r0 = 32 * kk + 4 * gg;
+  uint32_t w[4];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    w[j] = static_cast<uint32_t>(src[(size_t)(r0 + 2 * j) * 3 * H]) |
+           (static_cast<uint32_t>(src[(size_t)(r0 + 2 * j + 1) * 3 * H]) << 16);
+    w[2 + j] = static_cast<uint32_t>(src[(size_t)(r0 + 16 + 2 * j) * 3 * H]) |
+               (static_cast<uint32_t>(src[(size_t)(r0 + 16 + 2 * j + 1) * 3 * H]) << 16);
+  }
+  return u32x4{w[0], w[1], w[2], w[3]};
+}
+
+template <typename S, int H>
+__device__ __forceinline__ u32x4 gru_rev_unit(const S* __restrict__ Wi, const S* __restrict__ U, int pass, int m,
+                                              int lin) {
+  constexpr int KS = H / 32;
+  const int frag = lin / 64, l = lin % 64, qq = l % 16, gg = l / 16;
+  const S* mat;
+  int gate, kk;
+  if (pass == 1) {
+    mat = U;
+    gate = 2;
+    kk = frag;
+  } else if (frag < 3 * KS) {
+    mat = Wi;
+    gate = frag / KS;
+    kk = frag % KS;
+  } else {
+    mat = U;
+    gate = (frag - 3 * KS) / KS;
+    kk = (frag - 3 * KS) % KS;
+  }
+  const S* p = mat + (size_t)(16 * m + qq) * 3 * H + gate * H + 32 * kk + 4 * gg;
+  const u32x2 a = *reinterpret_cast<const u32x2*>(p);
+  const u32x2 b = *reinterpret_cast<const u32x2*>(p + 16);
+  return u32x4{a[0], a[1], b[0], b[1]};
+}
+
+// One thread per unit: forward region, then reverse region.
+template <typename S, int H>
+__global__ __launch_bounds__(256) void gru_pack_kernel(const S* __restrict__ Wi, const S* __restrict__ U,
+                                                       S* __restrict__ out) {
+  using P = GruPack<H>;
+  const int u = blockIdx.x * 256 + threadIdx.x;
+  if (u >= 2 * P::UNITS) return;
+  u32x4 v;
+  if (u < P::UNITS) {
+    int s, lin;
+    if (u < 2 * P::NC * P::FRU) {
+      s = u / (2 * P::FRU);
+      lin = u % (2 * P::FRU);
+    } else {
+      const int x = u - 2 * P::NC * P::FRU;
+      s = P::NC + x / (4 * P::FRU);
+      lin = x % (4 * P::FRU);
+    }
+    v = gru_fwd_unit<S, H>(Wi, U, s, lin);
+  } else {
+    const int x = u - P::UNITS;
+    int pass, m, lin;
+    if (x < P::NC * P::FRU) {
+      pass = 1;
+      m = x / P::FRU;
+      lin = x % P::FRU;
+    } else {
+      const int y = x - P::NC * P::FRU;
+      pass = 2;
+      m = y / (5 * P::FRU);
+      lin = y % (5 * P::FRU);
+    }
+    v = gru_rev_unit<S, H>(Wi, U, pass, m, lin);
+  }
+  *reinterpret_cast<u32x4*>(out + (size_t)u * 8) = v;
+}
+
+// ---------------------------------------------------------------------------
 // Forward for large H (bf16, H >= 128), the arithmetic of gru_fwd_kernel
 // with the weights shared through LDS: a workgroup of 8 waves (16 nodes
 // each) streams Wi and U once per 128 nodes, one 16-column gate tile at a
@@ -220,11 +333,11 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
 // buffered.  Pass 1 (tiles of the r gate) forms r and keeps r*h as operand
 // fragments; pass 2 (tiles of z and n) finishes the state.
 // ---------------------------------------------------------------------------
-template <typename S, int H>
+template <typename S, int H, bool PK>
 __global__ __launch_bounds__(512) void gru_fwd_big_kernel(const float* __restrict__ a, const S* __restrict__ h,
                                                           const S* __restrict__ Wi, const S* __restrict__ U,
-                                                          const float* __restrict__ b, S* __restrict__ h_out,
-                                                          S* __restrict__ saved, int n_pad) {
+                                                          const S* __restrict__ pk, const float* __restrict__ b,
+                                                          S* __restrict__ h_out, S* __restrict__ saved, int n_pad) {
   static_assert(sizeof(S) == 2, "bf16 only");
   constexpr int NT = 512, V = 8;
   constexpr int KS = H / 32, NC = H / 16;
@@ -238,30 +351,21 @@ __global__ __launch_bounds__(512) void gru_fwd_big_kernel(const float* __restric
   const int node = n0 + q;
 
   // Stage s of 2 NC: s < NC is pass 1, tile s (Wi, U columns of gate r);
-  // s >= NC is pass 2, tile s - NC (Wi, U columns of gates z and n).  A
-  // block is 16 columns x H rows of one matrix; an 8 x 8 tile (8 input
-  // rows, 8 columns) per unit.
-  constexpr int TPB = (H / V) * 2;                 // 8 x 8 tiles per block
-  constexpr int RMAX = (4 * TPB + NT - 1) / NT;
-  u32x4 rr[RMAX][V];
-  auto block_src = [&](int s, int blk, int& col) __attribute__((always_inline)) {
-    // blk: pass 1 {Wi_r, U_r}, pass 2 {Wi_z, U_z, Wi_n, U_n}
-    const int t16 = s < NC ? s : s - NC;
-    const int gate = s < NC ? 0 : 1 + blk / 2;
-    col = gate * H + 16 * t16;
-    return (blk % 2) ? U : Wi;
-  };
+  // s >= NC is pass 2, tile s - NC (Wi, U columns of gates z and n); units
+  // as gru_fwd_unit, from the packed forward region when PK.
+  constexpr int UPB = KS * 64;                     // units per block
+  constexpr int RMAX = (4 * UPB + NT - 1) / NT;
+  u32x4 rr[RMAX];
   auto load_stage = [&](int s) __attribute__((always_inline)) {
     const int nblk = s < NC ? 2 : 4;
 #pragma unroll
     for (int u = 0; u < RMAX; ++u) {
       const int lin = u * NT + tid;
-      if (lin < nblk * TPB) {
-        const int blk = lin / TPB, rem = lin % TPB;
-        const int hq = rem / 2, cq = rem % 2;
-        int col;
-        const S* src = block_src(s, blk, col);
-        tile_load<S>(rr[u], src + (size_t)(V * hq) * 3 * H + col + V * cq, 3 * H);
+      if (lin < nblk * UPB) {
+        if constexpr (PK)
+          rr[u] = *reinterpret_cast<const u32x4*>(pk + ((size_t)GruPack<H>::fwd_stage(s) + lin) * 8);
+        else
+          rr[u] = gru_fwd_unit<S, H>(Wi, U, s, lin);
       }
     }
   };
@@ -270,20 +374,7 @@ __global__ __launch_bounds__(512) void gru_fwd_big_kernel(const float* __restric
 #pragma unroll
     for (int u = 0; u < RMAX; ++u) {
       const int lin = u * NT + tid;
-      if (lin < nblk * TPB) {
-        const int blk = lin / TPB, rem = lin % TPB;
-        const int hq = rem / 2, cq = rem % 2;
-#pragma unroll
-        for (int x = 0; x < V; ++x) {
-          // row x of the transposed tile: column 8cq + x of the block,
-          // input rows 8hq .. 8hq + 7
-          const u32x4 o = tile_row_T<S>(rr[u], x);
-          const S* po = reinterpret_cast<const S*>(&o);
-#pragma unroll
-          for (int i = 0; i < V; i += 4)
-            put4<S>(lw[bf] + blk * FR, (V * hq + i) / 32, V * cq + x, (V * hq + i) % 32, po + i);
-        }
-      }
+      if (lin < nblk * UPB) *reinterpret_cast<u32x4*>(&lw[bf][lin * 8]) = rr[u];
     }
   };
 
@@ -371,10 +462,11 @@ __global__ __launch_bounds__(512) void gru_fwd_big_kernel(const float* __restric
 //   pass 2: block n gives da for input features 16n..16n+15 (G^ Wi^T, all
 //           three gates) and finishes dh for them (r^ U_r^T + z^ U_z^T).
 // ---------------------------------------------------------------------------
-template <typename S, int H>
+template <typename S, int H, bool PK>
 __global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restrict__ gin, const S* __restrict__ h,
                                                           const S* __restrict__ saved, const S* __restrict__ Wi,
-                                                          const S* __restrict__ U, S* __restrict__ daT,
+                                                          const S* __restrict__ U, const S* __restrict__ pk,
+                                                          S* __restrict__ daT,
                                                           float* __restrict__ dh, S* __restrict__ ghat, int n_pad) {
   static_assert(sizeof(S) == 2, "bf16 only");
   constexpr int NT = 512, V = 8;
@@ -392,26 +484,21 @@ __global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restric
   const int node = n0 + q;
 
   // Staging of weight block m (rows 16m .. 16m + 15) into buffer b:
-  // pass 1: U columns of gate 2; pass 2: Wi all gates, U gates 0, 1.
-  constexpr int U1 = 16 * (H / V);                 // 16-byte units, pass 1
-  constexpr int U2 = 16 * (3 * H / V) + 16 * (2 * H / V);
-  constexpr int R1 = (U1 + NT - 1) / NT, R2 = (U2 + NT - 1) / NT;
+  // pass 1: U columns of gate n; pass 2: Wi all gates, U gates r, z; units as
+  // gru_rev_unit, from the packed reverse region when PK.
+  constexpr int U1 = KS * 64;                      // units, pass 1
+  constexpr int U2 = 5 * KS * 64;                  // pass 2: 3 KS fragments of Wi, 2 KS of U
+  constexpr int R2 = (U2 + NT - 1) / NT;
   u32x4 rr[R2];
   auto load_blk = [&](int pass, int m) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < R2; ++u) {
       const int lin = u * NT + tid;
-      if (pass == 1) {
-        if (u < R1 && lin < U1) {
-          const int r = lin / (H / V), c = 2 * H + (lin % (H / V)) * V;
-          rr[u] = *reinterpret_cast<const u32x4*>(U + (size_t)(16 * m + r) * 3 * H + c);
-        }
-      } else if (lin < U2) {
-        const bool isw = lin < 16 * (3 * H / V);
-        const int l2 = isw ? lin : lin - 16 * (3 * H / V);
-        const int per = isw ? 3 * H / V : 2 * H / V;
-        const int r = l2 / per, c = (l2 % per) * V;
-        rr[u] = *reinterpret_cast<const u32x4*>((isw ? Wi : U) + (size_t)(16 * m + r) * 3 * H + c);
+      if (lin < (pass == 1 ? U1 : U2)) {
+        if constexpr (PK)
+          rr[u] = *reinterpret_cast<const u32x4*>(pk + ((size_t)GruPack<H>::rev_stage(pass, m) + lin) * 8);
+        else
+          rr[u] = gru_rev_unit<S, H>(Wi, U, pass, m, lin);
       }
     }
   };
@@ -419,23 +506,7 @@ __global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restric
 #pragma unroll
     for (int u = 0; u < R2; ++u) {
       const int lin = u * NT + tid;
-      const S* pw = reinterpret_cast<const S*>(&rr[u]);
-      if (pass == 1) {
-        if (u < R1 && lin < U1) {
-          const int r = lin / (H / V), c = (lin % (H / V)) * V;   // column within gate 2
-#pragma unroll
-          for (int i = 0; i < V; i += 4) put4<S>(lw[b], (c + i) / 32, r, (c + i) % 32, pw + i);
-        }
-      } else if (lin < U2) {
-        const bool isw = lin < 16 * (3 * H / V);
-        const int l2 = isw ? lin : lin - 16 * (3 * H / V);
-        const int per = isw ? 3 * H / V : 2 * H / V;
-        const int r = l2 / per, c = (l2 % per) * V;              // gate column (0 .. 3H or 2H)
-        S* base = isw ? lw[b] : lw[b] + BLK_W;
-#pragma unroll
-        for (int i = 0; i < V; i += 4)
-          put4<S>(base, ((c + i) / H) * KS + ((c + i) % H) / 32, r, (c + i) % 32, pw + i);
-      }
+      if (lin < (pass == 1 ? U1 : U2)) *reinterpret_cast<u32x4*>(&lw[b][lin * 8]) = rr[u];
     }
   };
 
@@ -731,12 +802,35 @@ Split gru_split(long K, int H, bool f32) {
 }
 
 template <typename S, int H>
+constexpr bool gru_big() {
+  return sizeof(S) == 2 && H >= 128;
+}
+
+template <typename S, int H>
+hipError_t gru_pack_h(const void* Wi, const void* U, void* packed, hipStream_t st) {
+  if constexpr (gru_big<S, H>()) {
+    const int units = 2 * dev::GruPack<H>::UNITS;
+    hipLaunchKernelGGL((dev::gru_pack_kernel<S, H>), dim3((units + 255) / 256), dim3(256), 0, st,
+                       static_cast<const S*>(Wi), static_cast<const S*>(U), static_cast<S*>(packed));
+    return hipGetLastError();
+  }
+  return hipSuccess;   // no kernel reads the packed form
+}
+
+template <typename S, int H>
 hipError_t gru_fwd_h(int n_pad, const float* a, const void* h, const void* Wi, const void* U, const float* b,
-                     void* h_out, void* saved, hipStream_t st) {
-  if constexpr (sizeof(S) == 2 && H >= 128) {
-    hipLaunchKernelGGL((dev::gru_fwd_big_kernel<S, H>), dim3((n_pad + 127) / 128), dim3(512), 0, st, a,
-                       static_cast<const S*>(h), static_cast<const S*>(Wi), static_cast<const S*>(U), b,
-                       static_cast<S*>(h_out), static_cast<S*>(saved), n_pad);
+                     void* h_out, void* saved, const void* packed, hipStream_t st) {
+  if constexpr (gru_big<S, H>()) {
+    const S* pk = static_cast<const S*>(packed);
+#define GGNN_GRU_FWD_BIG(PK)                                                                                   \
+  hipLaunchKernelGGL((dev::gru_fwd_big_kernel<S, H, PK>), dim3((n_pad + 127) / 128), dim3(512), 0, st, a,      \
+                     static_cast<const S*>(h), static_cast<const S*>(Wi), static_cast<const S*>(U), pk, b,      \
+                     static_cast<S*>(h_out), static_cast<S*>(saved), n_pad)
+    if (pk != nullptr)
+      GGNN_GRU_FWD_BIG(true);
+    else
+      GGNN_GRU_FWD_BIG(false);
+#undef GGNN_GRU_FWD_BIG
     return hipGetLastError();
   }
   constexpr int WAVES = 4;
@@ -748,11 +842,19 @@ hipError_t gru_fwd_h(int n_pad, const float* a, const void* h, const void* Wi, c
 
 template <typename S, int H>
 hipError_t gru_bwd_nodes_h(int n_pad, const float* dh_out, const void* h, const void* saved, const void* Wi,
-                           const void* U, void* da, float* dh, void* ghat, hipStream_t st) {
-  if constexpr (sizeof(S) == 2 && H >= 128) {
-    hipLaunchKernelGGL((dev::gru_bwd_big_kernel<S, H>), dim3((n_pad + 127) / 128), dim3(512), 0, st, dh_out,
-                       static_cast<const S*>(h), static_cast<const S*>(saved), static_cast<const S*>(Wi),
-                       static_cast<const S*>(U), static_cast<S*>(da), dh, static_cast<S*>(ghat), n_pad);
+                           const void* U, void* da, float* dh, void* ghat, const void* packed, hipStream_t st) {
+  if constexpr (gru_big<S, H>()) {
+    // the reverse region follows the forward one
+    const S* pk = packed ? static_cast<const S*>(packed) + (size_t)dev::GruPack<H>::UNITS * 8 : nullptr;
+#define GGNN_GRU_BWD_BIG(PK)                                                                                   \
+  hipLaunchKernelGGL((dev::gru_bwd_big_kernel<S, H, PK>), dim3((n_pad + 127) / 128), dim3(512), 0, st, dh_out, \
+                     static_cast<const S*>(h), static_cast<const S*>(saved), static_cast<const S*>(Wi),         \
+                     static_cast<const S*>(U), pk, static_cast<S*>(da), dh, static_cast<S*>(ghat), n_pad)
+    if (pk != nullptr)
+      GGNN_GRU_BWD_BIG(true);
+    else
+      GGNN_GRU_BWD_BIG(false);
+#undef GGNN_GRU_BWD_BIG
     return hipGetLastError();
   }
   constexpr int WAVES = 4;
@@ -765,7 +867,7 @@ hipError_t gru_bwd_nodes_h(int n_pad, const float* dh_out, const void* h, const 
 
 template <typename S, int H>
 hipError_t gru_wgrad_h(long K, const float* a, const void* h, const void* saved, const void* ghat, float* dWi,
-                       float* dU, float* db, void* ws, hipStream_t st) {
+                       float* dU, float* db, void* ws, ReduceList* defer, hipStream_t st) {
   Split sp = gru_split(K, H, sizeof(S) == 4);
   float* P = static_cast<float*>(ws);
   float* Pb = P + (size_t)sp.nsplit * 2 * H * 3 * H;
@@ -776,11 +878,11 @@ hipError_t gru_wgrad_h(long K, const float* a, const void* h, const void* saved,
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const long slice = 2L * H * 3 * H;  // partials are [split][which][H][3H]
-  err = launch_reduce_partials(P, dWi, sp.nsplit, H * 3 * H, slice, st);
+  err = reduce_or_defer(P, dWi, sp.nsplit, H * 3 * H, slice, defer, st);
   if (err != hipSuccess) return err;
-  err = launch_reduce_partials(P + (size_t)H * 3 * H, dU, sp.nsplit, H * 3 * H, slice, st);
+  err = reduce_or_defer(P + (size_t)H * 3 * H, dU, sp.nsplit, H * 3 * H, slice, defer, st);
   if (err != hipSuccess) return err;
-  return launch_reduce_partials(Pb, db, sp.nsplit, 3 * H, 3L * H, st);
+  return reduce_or_defer(Pb, db, sp.nsplit, 3 * H, 3L * H, defer, st);
 }
 
 #define GGNN_GRU_SWITCH(CALL)                  \
@@ -793,19 +895,23 @@ hipError_t gru_wgrad_h(long K, const float* a, const void* h, const void* saved,
   return hipErrorInvalidValue;
 
 template <typename S>
+hipError_t gru_pack_t(int H, const void* Wi, const void* U, void* packed, hipStream_t st) {
+  GGNN_GRU_SWITCH(return (gru_pack_h<S, HH>(Wi, U, packed, st)))
+}
+template <typename S>
 hipError_t gru_fwd_t(int n_pad, int H, const float* a, const void* h, const void* Wi, const void* U, const float* b,
-                     void* h_out, void* saved, hipStream_t st) {
-  GGNN_GRU_SWITCH(return (gru_fwd_h<S, HH>(n_pad, a, h, Wi, U, b, h_out, saved, st)))
+                     void* h_out, void* saved, const void* packed, hipStream_t st) {
+  GGNN_GRU_SWITCH(return (gru_fwd_h<S, HH>(n_pad, a, h, Wi, U, b, h_out, saved, packed, st)))
 }
 template <typename S>
 hipError_t gru_bwd_nodes_t(int n_pad, int H, const float* dh_out, const void* h, const void* saved, const void* Wi,
-                           const void* U, void* da, float* dh, void* ghat, hipStream_t st) {
-  GGNN_GRU_SWITCH(return (gru_bwd_nodes_h<S, HH>(n_pad, dh_out, h, saved, Wi, U, da, dh, ghat, st)))
+                           const void* U, void* da, float* dh, void* ghat, const void* packed, hipStream_t st) {
+  GGNN_GRU_SWITCH(return (gru_bwd_nodes_h<S, HH>(n_pad, dh_out, h, saved, Wi, U, da, dh, ghat, packed, st)))
 }
 template <typename S>
 hipError_t gru_wgrad_t(long K, int H, const float* a, const void* h, const void* saved, const void* ghat, float* dWi,
-                       float* dU, float* db, void* ws, hipStream_t st) {
-  GGNN_GRU_SWITCH(return (gru_wgrad_h<S, HH>(K, a, h, saved, ghat, dWi, dU, db, ws, st)))
+                       float* dU, float* db, void* ws, ReduceList* defer, hipStream_t st) {
+  GGNN_GRU_SWITCH(return (gru_wgrad_h<S, HH>(K, a, h, saved, ghat, dWi, dU, db, ws, defer, st)))
 }
 #undef GGNN_GRU_SWITCH
 }  // namespace
@@ -824,6 +930,10 @@ size_t gru_wgrad_workspace(long K, int H) {
   return ((size_t)sp.nsplit * 2 * H * 3 * H + (size_t)sp.nsplit * 3 * H) * sizeof(float);
 }
 
+size_t gru_pack_bytes(int dt, int H) {
+  return dt == GGNN_BF16 && H >= 128 ? (size_t)12 * H * H * 2 : 0;
+}
+
 size_t gru_bwd_workspace(int dt, int n_pad, int H) {
   return ghat_bytes(dt, n_pad, H) + gru_wgrad_workspace(n_pad, H);
 }
@@ -840,19 +950,24 @@ hipError_t launch_gru_bwd(int dt, int n_pad, int H, const float* dh_out, const f
 #endif
 
 namespace GGNN_IMPL_NS {
+hipError_t launch_gru_pack(int H, const void* Wi, const void* U, void* packed, hipStream_t st) {
+  return gru_pack_t<dev::dt_t>(H, Wi, U, packed, st);
+}
+
 hipError_t launch_gru_fwd(int n_pad, int H, const float* a, const void* h, const void* Wi, const void* U,
-                          const float* b, void* h_out, void* saved, hipStream_t st) {
-  return gru_fwd_t<dev::dt_t>(n_pad, H, a, h, Wi, U, b, h_out, saved, st);
+                          const float* b, void* h_out, void* saved, const void* packed, hipStream_t st) {
+  return gru_fwd_t<dev::dt_t>(n_pad, H, a, h, Wi, U, b, h_out, saved, packed, st);
 }
 
 hipError_t launch_gru_bwd_nodes(int n_pad, int H, const float* dh_out, const void* h, const void* saved,
-                                const void* Wi, const void* U, void* da, float* dh, void* ghat, hipStream_t st) {
-  return gru_bwd_nodes_t<dev::dt_t>(n_pad, H, dh_out, h, saved, Wi, U, da, dh, ghat, st);
+                                const void* Wi, const void* U, void* da, float* dh, void* ghat, const void* packed,
+                                hipStream_t st) {
+  return gru_bwd_nodes_t<dev::dt_t>(n_pad, H, dh_out, h, saved, Wi, U, da, dh, ghat, packed, st);
 }
 
 hipError_t launch_gru_wgrad(long K, int H, const float* a, const void* h, const void* saved, const void* ghat,
-                            float* dWi, float* dU, float* db, void* ws, hipStream_t st) {
-  return gru_wgrad_t<dev::dt_t>(K, H, a, h, saved, ghat, dWi, dU, db, ws, st);
+                            float* dWi, float* dU, float* db, void* ws, ReduceList* defer, hipStream_t st) {
+  return gru_wgrad_t<dev::dt_t>(K, H, a, h, saved, ghat, dWi, dU, db, ws, defer, st);
 }
 }  // namespace GGNN_IMPL_NS
 

@@ -15,6 +15,24 @@
 
 namespace ggnn {
 
+// Partial-sum reductions that a caller can collect and launch together
+// (launch_reduce_multi): out[i] += sum_{s < nsplit} part[s * stride + i].
+struct ReduceSeg {
+  const float* part;
+  float* out;
+  int nsplit, count;
+  long stride;
+};
+struct ReduceList {
+  static constexpr int kMax = 8;
+  ReduceSeg seg[kMax];
+  int n = 0;
+};
+hipError_t launch_reduce_multi(const ReduceList& l, hipStream_t st);
+// Appends to *defer (when non-NULL and not full), else launches the reduction.
+hipError_t reduce_or_defer(const float* part, float* out, int nsplit, int count, long stride, ReduceList* defer,
+                           hipStream_t st);
+
 #define GGNN_DT_LAUNCHERS                                                                                         \
   hipError_t launch_banded_fwd(int n_pad, int B, int H, int E, const void* band, const float* M, float* a,        \
                                hipStream_t st);                                                                   \
@@ -44,14 +62,15 @@ namespace ggnn {
   hipError_t launch_transform_wgrad(long K, int H, int E, const void* X, const void* dM, long ld, float* dW,      \
                                     float* dbias, void* ws, hipStream_t st);                                      \
   hipError_t launch_transform_wgrad_nm(long K, int H, int E, const void* X, const void* dM, long ldk, float* dW,  \
-                                       float* dbias, void* ws, hipStream_t st);                                   \
+                                       float* dbias, void* ws, ReduceList* defer, hipStream_t st);                \
   hipError_t launch_gru_fwd(int n_pad, int H, const float* a, const void* h, const void* Wi, const void* U,       \
-                            const float* b, void* h_out, void* saved, hipStream_t st);                            \
+                            const float* b, void* h_out, void* saved, const void* packed, hipStream_t st);        \
   hipError_t launch_gru_bwd_nodes(int n_pad, int H, const float* dh_out, const void* h, const void* saved,        \
                                   const void* Wi, const void* U, void* da, float* dh, void* ghat,                 \
-                                  hipStream_t st);                                                                \
+                                  const void* packed, hipStream_t st);                                            \
+  hipError_t launch_gru_pack(int H, const void* Wi, const void* U, void* packed, hipStream_t st);               \
   hipError_t launch_gru_wgrad(long K, int H, const float* a, const void* h, const void* saved, const void* ghat,  \
-                              float* dWi, float* dU, float* db, void* ws, hipStream_t st);                       \
+                              float* dWi, float* dU, float* db, void* ws, ReduceList* defer, hipStream_t st);    \
   hipError_t launch_readout_loss(int H, int n_graphs, const void* X, const float* w_out, const float* b_out,      \
                                  const int32_t* cand_node, const int32_t* cand_ptr, const int32_t* target,       \
                                  float* logits, float* loss, float* dlogit, hipStream_t st);                     \
@@ -175,28 +194,40 @@ inline hipError_t launch_transform_wgrad(int dt, long K, int H, int E, const voi
   return GGNN_DT_PICK(launch_transform_wgrad, K, H, E, X, dM, ld, dW, dbias, ws, st);
 }
 // The same with node-major dM: row k of type e at dM + (e * ldk + k) * H.
+// With defer non-NULL the partial-sum reductions are appended to it instead
+// of launched (launch_reduce_multi runs them together).
 inline hipError_t launch_transform_wgrad_nm(int dt, long K, int H, int E, const void* X, const void* dM, long ldk,
-                                            float* dW, float* dbias, void* ws, hipStream_t st) {
-  return GGNN_DT_PICK(launch_transform_wgrad_nm, K, H, E, X, dM, ldk, dW, dbias, ws, st);
+                                            float* dW, float* dbias, void* ws, hipStream_t st,
+                                            ReduceList* defer = nullptr) {
+  return GGNN_DT_PICK(launch_transform_wgrad_nm, K, H, E, X, dM, ldk, dW, dbias, ws, defer, st);
 }
 
+// GRU weights packed in the staging order of the large-H kernels (bf16,
+// H >= 128): gru_pack_bytes is 0 where no kernel reads the packed form, and
+// `packed` (NULL allowed) is then ignored by the launchers below.
+size_t gru_pack_bytes(int dt, int H);
+inline hipError_t launch_gru_pack(int dt, int H, const void* Wi, const void* U, void* packed, hipStream_t st) {
+  return GGNN_DT_PICK(launch_gru_pack, H, Wi, U, packed, st);
+}
 inline hipError_t launch_gru_fwd(int dt, int n_pad, int H, const float* a, const void* h, const void* Wi,
-                                 const void* U, const float* b, void* h_out, void* saved, hipStream_t st) {
-  return GGNN_DT_PICK(launch_gru_fwd, n_pad, H, a, h, Wi, U, b, h_out, saved, st);
+                                 const void* U, const float* b, void* h_out, void* saved, hipStream_t st,
+                                 const void* packed = nullptr) {
+  return GGNN_DT_PICK(launch_gru_fwd, n_pad, H, a, h, Wi, U, b, h_out, saved, packed, st);
 }
 // Node pass of the GRU reverse: da, dh and the gate gradients G^ [n_pad][3H].
 inline hipError_t launch_gru_bwd_nodes(int dt, int n_pad, int H, const float* dh_out, const void* h,
                                        const void* saved, const void* Wi, const void* U, void* da, float* dh,
-                                       void* ghat, hipStream_t st) {
-  return GGNN_DT_PICK(launch_gru_bwd_nodes, n_pad, H, dh_out, h, saved, Wi, U, da, dh, ghat, st);
+                                       void* ghat, hipStream_t st, const void* packed = nullptr) {
+  return GGNN_DT_PICK(launch_gru_bwd_nodes, n_pad, H, dh_out, h, saved, Wi, U, da, dh, ghat, packed, st);
 }
 size_t ghat_bytes(int dt, long rows, int H);
 // GRU weight gradients over K rows of (a, h, saved, G^) stacked node-major:
 // dWi, dU, db += (partials in ws of gru_wgrad_workspace bytes, fixed order).
 size_t gru_wgrad_workspace(long K, int H);
 inline hipError_t launch_gru_wgrad(int dt, long K, int H, const float* a, const void* h, const void* saved,
-                                   const void* ghat, float* dWi, float* dU, float* db, void* ws, hipStream_t st) {
-  return GGNN_DT_PICK(launch_gru_wgrad, K, H, a, h, saved, ghat, dWi, dU, db, ws, st);
+                                   const void* ghat, float* dWi, float* dU, float* db, void* ws, hipStream_t st,
+                                   ReduceList* defer = nullptr) {
+  return GGNN_DT_PICK(launch_gru_wgrad, K, H, a, h, saved, ghat, dWi, dU, db, ws, defer, st);
 }
 // One step: node pass with G^ in ws, then the weight gradients over n_pad rows.
 size_t gru_bwd_workspace(int dt, int n_pad, int H);

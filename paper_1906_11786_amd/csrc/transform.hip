@@ -467,13 +467,12 @@ __global__ __launch_bounds__(512) void transform_wgrad_nm_kernel(const S* __rest
 // loads in flight), then thread (x, 0) adds the RW sums in order y = 0..RW-1.
 // The order depends only on nsplit, so results do not depend on scheduling.
 constexpr int kReduceRW = 16;
-__global__ __launch_bounds__(64 * kReduceRW) void reduce_partials_kernel(const float* __restrict__ part,
-                                                                         float* __restrict__ out, int nsplit,
-                                                                         int count, long stride) {
+__device__ __forceinline__ void reduce_block(const float* __restrict__ part, float* __restrict__ out, int nsplit,
+                                             int count, long stride, int blk) {
   constexpr int RW = kReduceRW;
   __shared__ float red[RW][64];
   const int x = threadIdx.x % 64, y = threadIdx.x / 64;
-  const int i = blockIdx.x * 64 + x;
+  const int i = blk * 64 + x;
   float s = 0.f;
   if (i < count) {
     int k = y;
@@ -494,6 +493,50 @@ __global__ __launch_bounds__(64 * kReduceRW) void reduce_partials_kernel(const f
     for (int w = 0; w < RW; ++w) t += red[w][x];
     out[i] += t;
   }
+}
+
+__global__ __launch_bounds__(64 * kReduceRW) void reduce_partials_kernel(const float* __restrict__ part,
+                                                                         float* __restrict__ out, int nsplit,
+                                                                         int count, long stride) {
+  reduce_block(part, out, nsplit, count, stride, blockIdx.x);
+}
+
+// Several reductions in one launch (the weight-gradient partials of one
+// reverse pass): block b works for the segment whose block range holds it.
+struct ReduceMulti {
+  ReduceSeg seg[ReduceList::kMax];
+  int first[ReduceList::kMax + 1];
+  int n;
+};
+__global__ __launch_bounds__(64 * kReduceRW) void reduce_multi_kernel(ReduceMulti m) {
+  const int b = blockIdx.x;
+  int si = 0;
+  while (si + 1 < m.n && b >= m.first[si + 1]) ++si;
+  const ReduceSeg sg = m.seg[si];
+  reduce_block(sg.part, sg.out, sg.nsplit, sg.count, sg.stride, b - m.first[si]);
+}
+
+hipError_t launch_reduce_multi(const ReduceList& l, hipStream_t st) {
+  if (l.n == 0) return hipSuccess;
+  ReduceMulti m{};
+  m.n = l.n;
+  m.first[0] = 0;
+  for (int i = 0; i < l.n; ++i) {
+    m.seg[i] = l.seg[i];
+    m.first[i + 1] = m.first[i] + (l.seg[i].count + 63) / 64;
+  }
+  hipLaunchKernelGGL(reduce_multi_kernel, dim3(m.first[l.n]), dim3(64 * kReduceRW), 0, st, m);
+  return hipGetLastError();
+}
+
+hipError_t reduce_or_defer(const float* part, float* out, int nsplit, int count, long stride, ReduceList* defer,
+                           hipStream_t st) {
+  if (count <= 0) return hipSuccess;
+  if (defer != nullptr && defer->n < ReduceList::kMax) {
+    defer->seg[defer->n++] = ReduceSeg{part, out, nsplit, count, stride};
+    return hipSuccess;
+  }
+  return launch_reduce_partials(part, out, nsplit, count, stride, st);
 }
 
 // Zero-fill with a kernel (not hipMemsetAsync, so the launch can sit inside a
@@ -598,7 +641,7 @@ hipError_t transform_wgrad_h(long K, int E, const void* X, const void* dM, long 
 
 template <typename S, int H>
 hipError_t transform_wgrad_nm_h(long K, int E, const void* X, const void* dM, long ldk, float* dW, float* dbias,
-                                void* ws, hipStream_t st) {
+                                void* ws, ReduceList* defer, hipStream_t st) {
   Split sp = transform_nm_split(K, H, E, sizeof(S) == 4);
   using C = dev::WgradNmCfg<S, H>;
   float* P = static_cast<float*>(ws);
@@ -608,19 +651,19 @@ hipError_t transform_wgrad_nm_h(long K, int E, const void* X, const void* dM, lo
                      static_cast<const S*>(X), static_cast<const S*>(dM), ldk, P, Pb, K, E, sp.per);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  err = launch_reduce_partials(P, dW, sp.nsplit, E * H * H, (long)E * H * H, st);
+  err = reduce_or_defer(P, dW, sp.nsplit, E * H * H, (long)E * H * H, defer, st);
   if (err != hipSuccess || !dbias) return err;
-  return launch_reduce_partials(Pb, dbias, sp.nsplit, E * H, (long)E * H, st);
+  return reduce_or_defer(Pb, dbias, sp.nsplit, E * H, (long)E * H, defer, st);
 }
 
 template <typename S>
 hipError_t transform_wgrad_nm_t(long K, int H, int E, const void* X, const void* dM, long ldk, float* dW,
-                                float* dbias, void* ws, hipStream_t st) {
+                                float* dbias, void* ws, ReduceList* defer, hipStream_t st) {
   switch (H) {
-    case 32: return transform_wgrad_nm_h<S, 32>(K, E, X, dM, ldk, dW, dbias, ws, st);
-    case 64: return transform_wgrad_nm_h<S, 64>(K, E, X, dM, ldk, dW, dbias, ws, st);
-    case 128: return transform_wgrad_nm_h<S, 128>(K, E, X, dM, ldk, dW, dbias, ws, st);
-    case 256: return transform_wgrad_nm_h<S, 256>(K, E, X, dM, ldk, dW, dbias, ws, st);
+    case 32: return transform_wgrad_nm_h<S, 32>(K, E, X, dM, ldk, dW, dbias, ws, defer, st);
+    case 64: return transform_wgrad_nm_h<S, 64>(K, E, X, dM, ldk, dW, dbias, ws, defer, st);
+    case 128: return transform_wgrad_nm_h<S, 128>(K, E, X, dM, ldk, dW, dbias, ws, defer, st);
+    case 256: return transform_wgrad_nm_h<S, 256>(K, E, X, dM, ldk, dW, dbias, ws, defer, st);
   }
   return hipErrorInvalidValue;
 }
@@ -688,8 +731,8 @@ hipError_t launch_transform_wgrad(long K, int H, int E, const void* X, const voi
 }
 
 hipError_t launch_transform_wgrad_nm(long K, int H, int E, const void* X, const void* dM, long ldk, float* dW,
-                                     float* dbias, void* ws, hipStream_t st) {
-  return transform_wgrad_nm_t<dev::dt_t>(K, H, E, X, dM, ldk, dW, dbias, ws, st);
+                                     float* dbias, void* ws, ReduceList* defer, hipStream_t st) {
+  return transform_wgrad_nm_t<dev::dt_t>(K, H, E, X, dM, ldk, dW, dbias, ws, defer, st);
 }
 }  // namespace GGNN_IMPL_NS
 

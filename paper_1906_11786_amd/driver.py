@@ -93,10 +93,11 @@ class BandedGGNN:
     gradients and workspace, sized for T steps."""
 
     def __init__(self, comp: Compiled, H: int, T: int, dt: str, params, device="cuda", strict: bool = True,
-                 band_format: str = "bits"):
+                 band_format: str = "bits", gru_pack: bool = True):
         """band_format: "bits" (1 bit per band entry; aggregate-first fused
         forward) or "dense" (band entries in the compute dtype; transform-first
-        forward)."""
+        forward).  gru_pack: hand the GRU kernels Wi, U in their staging order
+        (used at H >= 128 in bf16; results are identical either way)."""
         import torch
         self.torch = torch
         self.comp, self.H, self.T, self.dt, self.device = comp, H, T, dt, device
@@ -130,6 +131,10 @@ class BandedGGNN:
         self.Wi = to_device(params.Wi, dt, device)
         self.U = to_device(params.U, dt, device)
         self.b = torch.from_numpy(params.b.astype(np.float32)).to(device)
+        # Wi, U in the staging order of the large-width GRU kernels, refreshed
+        # with Wt; absent where no kernel reads it.
+        pk = capi.ggnn_gru_pack_bytes(dt, H) if gru_pack else 0
+        self.gru_packed = torch.empty((pk,), dtype=torch.uint8, device=device) if pk else None
         self.X = torch.empty((T + 1, n_pad, H), dtype=td, device=device)
         self.X[0].copy_(to_device(params.X, dt, device))
         self.a = torch.empty((T, n_pad, H), dtype=torch.float32, device=device)
@@ -161,7 +166,8 @@ class BandedGGNN:
             dtype=capi.DTYPES[dt], n_pad=n_pad, B=B, H=H, E=E, T=T, band=self.band.data_ptr(),
             W=self.W.data_ptr(), bias=None if self.bias is None else self.bias.data_ptr(), Wi=self.Wi.data_ptr(),
             U=self.U.data_ptr(), b=self.b.data_ptr(), band_format=capi.BAND_FORMATS[band_format],
-            band_t=None if self.band_t is None else self.band_t.data_ptr(), Wt=self.Wt.data_ptr())
+            band_t=None if self.band_t is None else self.band_t.data_ptr(), Wt=self.Wt.data_ptr(),
+            gru_packed=None if self.gru_packed is None else self.gru_packed.data_ptr())
         self.refresh_weights()
         ws = capi.ggnn_backward_workspace_bytes(self.model)
         self.workspace = torch.empty((max(ws, 16),), dtype=torch.uint8, device=device)
@@ -174,8 +180,10 @@ class BandedGGNN:
         comp.stats["upload_seconds"] = time.perf_counter() - t0
 
     def refresh_weights(self, stream=None):
-        """Recompute W_e^T after W changes."""
+        """Recompute W_e^T and the packed GRU weights after W, Wi or U change."""
         capi.ggnn_transpose_weights(self.dt, self.H, self.comp.E, self.W, self.Wt, stream)
+        if self.gru_packed is not None:
+            capi.ggnn_gru_pack_weights(self.dt, self.H, self.Wi, self.U, self.gru_packed, stream)
 
     def forward(self, stream=None):
         capi.ggnn_forward(self.model, self.act, stream)

@@ -202,6 +202,37 @@ def test_stress_1m_workload_sampled():
 
 
 @pytest.mark.parametrize("band_format", ["bits", "dense"])
+@pytest.mark.parametrize("n,B,E,H,T", [(1500, 128, 3, 128, 3), (1300, 256, 2, 256, 2)])
+def test_gru_packed_weights_equal_gathered(n, B, E, H, T, band_format):
+    """The large-width GRU kernels staging Wi, U from the packed copy give the
+    same forward and reverse results, bit for bit, as staging them straight
+    from the row-major weights; the packed copy holds every element of Wi
+    and U once in each of its two regions."""
+    dt = "bf16"
+    say(f"gru packed vs gathered n={n} B={B} E={E} H={H} T={T} band={band_format}")
+    g = scramble_graph(70 + H, 0, backbone_graph(70 + H, 0, n, E, span_mean=6.0, max_span=B))[0]
+    comp = drv.compile_graphs([g], B, E, reorder=True)
+    params = draw_params(70 + H, comp.n_real, comp.n_pad, H, E, dt, with_bias=True)
+    res = {}
+    for pack in (True, False):
+        m = drv.BandedGGNN(comp, H, T, dt, params, band_format=band_format, gru_pack=pack)
+        assert (m.gru_packed is not None) == pack
+        m.step()
+        torch.cuda.synchronize()
+        res[pack] = m.results()
+        if pack:
+            pk = m.gru_packed.view(torch.int16).cpu().numpy().reshape(2, -1)
+            w = np.concatenate([m.Wi.view(torch.int16).cpu().numpy().ravel(),
+                                m.U.view(torch.int16).cpu().numpy().ravel()])
+            for region in pk:
+                np.testing.assert_array_equal(np.sort(region), np.sort(w))
+        del m
+    assert res[True].keys() == res[False].keys()
+    for k in res[True]:
+        assert np.array_equal(res[True][k], res[False][k]), k
+
+
+@pytest.mark.parametrize("band_format", ["bits", "dense"])
 def test_graph_replay_equals_eager(band_format):
     """The step captured as a HIP graph: every replay (with eager work and
     synchronizations between replays) gives the eager step's results bit for

@@ -33,7 +33,9 @@ def test_library_exports_every_declared_symbol():
     for name in declared:
         assert hasattr(L, name), name
     assert set(declared) == set(capi.EXPORTS)
-    assert capi.ggnn_abi_version() == 7
+    header = open(os.path.join(ROOT, "include", "ggnn.h")).read()
+    declared_abi = int(re.search(r"#define GGNN_ABI_VERSION (\d+)", header).group(1))
+    assert capi.ggnn_abi_version() == capi.ABI_VERSION == declared_abi
     assert capi.ggnn_status_string(3) == "GGNN_ERR_OUT_OF_BAND"
 
 
@@ -189,6 +191,30 @@ def test_training_entry_points_validate_before_touching_the_gpu():
             capi.ggnn_sgd_momentum(**kw, stream=0)
         assert ei.value.status_name == "GGNN_ERR_INVALID_ARG", args
     capi.ggnn_sgd_momentum(0, None, None, None, 0.1, 0.9, stream=0)   # nothing to do: OK
+
+
+def test_gru_pack_sizes_and_validation_before_touching_the_gpu():
+    """Packed GRU weights: 12 H^2 bf16 elements where the large-width kernels
+    read them, nothing elsewhere (the call is then a no-op); bad pointers and
+    overlaps are rejected on the host."""
+    _need_lib()
+    assert capi.ggnn_gru_pack_bytes("bf16", 128) == 12 * 128 * 128 * 2
+    assert capi.ggnn_gru_pack_bytes("bf16", 256) == 12 * 256 * 256 * 2
+    for dt, H in [("bf16", 32), ("bf16", 64), ("f32", 128), ("f32", 256), ("bf16", 48)]:
+        assert capi.ggnn_gru_pack_bytes(dt, H) == 0, (dt, H)
+    capi.ggnn_gru_pack_weights("f32", 128, None, None, None, stream=0)   # nothing to pack: OK
+    capi.ggnn_gru_pack_weights("bf16", 64, None, None, None, stream=0)
+    H = 128
+    wb = H * 3 * H * 2
+    Wi, U, pk = 1 << 20, 2 << 20, 4 << 20   # 16-byte aligned stand-in addresses; nothing is launched
+    for args in [(None, U, pk), (Wi, U, None), (Wi + 8, U, pk), (Wi, U, Wi + wb - 16), (Wi, U, U - 16),
+                 (Wi, U, Wi - capi.ggnn_gru_pack_bytes("bf16", H) + 16)]:
+        with pytest.raises(capi.GGNNError) as ei:
+            capi.ggnn_gru_pack_weights("bf16", H, *args, stream=0)
+        assert ei.value.status_name == "GGNN_ERR_INVALID_ARG", args
+    with pytest.raises(capi.GGNNError) as ei:
+        capi.ggnn_gru_pack_weights("bf16", 48, Wi, U, pk, stream=0)
+    assert ei.value.status_name == "GGNN_ERR_INVALID_ARG"
 
 
 def _unpack_bits(bits):
