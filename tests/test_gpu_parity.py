@@ -201,6 +201,45 @@ def test_stress_1m_workload_sampled():
     _sampled_batch(CONFIGS[4], picks=[0, 70, 139])
 
 
+def _no_edges(n):
+    z = np.zeros(0, np.int32)
+    return Graph(n=n, src=z, dst=z, etype=z)
+
+
+def _one_type(seed, n, E, keep):
+    g = scramble_graph(seed, 0, backbone_graph(seed, 0, n, E, span_mean=5.0, max_span=32))[0]
+    m = g.etype == keep
+    return Graph(n=g.n, src=g.src[m], dst=g.dst[m], etype=g.etype[m])
+
+
+DEGENERATE = {  # name: (graphs, B, E, H, T, dt, bias)
+    "no_edges": (lambda: [_no_edges(200)], 64, 3, 64, 2, "bf16", True),
+    "one_node": (lambda: [_no_edges(1)], 32, 2, 32, 3, "f32", True),
+    "batch_of_edgeless_graphs": (lambda: [_no_edges(1), _no_edges(150), _no_edges(1)], 64, 2, 128, 2, "bf16", False),
+    "one_edge_type_of_four": (lambda: [_one_type(83, 700, 4, 2)], 64, 4, 64, 2, "bf16", True),
+    "mixed_with_empty": (lambda: [_no_edges(40), _one_type(84, 500, 3, 0), _no_edges(1)], 128, 3, 256, 2, "bf16",
+                         True),
+}
+
+
+@pytest.mark.parametrize("band_format", ["bits", "dense"])
+@pytest.mark.parametrize("case", list(DEGENERATE))
+def test_degenerate_graphs(case, band_format):
+    """Edgeless graphs (the aggregate is zero, only the GRU acts), a single
+    node, a batch mixing edgeless graphs with one that has edges of a single
+    type: the whole forward and reverse pass against the oracle."""
+    make, B, E, H, T, dt, bias = DEGENERATE[case]
+    say(f"degenerate {case} B={B} E={E} H={H} T={T} dt={dt} band={band_format}")
+    _, res, out = _run_full(make(), B, E, H, T, dt, 90, reorder=True, with_bias=bias, band_format=band_format)
+    assert out["n_dropped"] == 0
+    _compare(res, out, dt)
+    if case.startswith("no_edges") or case.startswith("one_node") or case.startswith("batch_of"):
+        # no messages: the weight gradients of the transform are exactly zero
+        assert not np.any(res["dW"]), case
+        if "dbias" in res:
+            assert not np.any(res["dbias"]), case
+
+
 @pytest.mark.parametrize("band_format", ["bits", "dense"])
 @pytest.mark.parametrize("n,B,E,H,T", [(1500, 128, 3, 128, 3), (1300, 256, 2, 256, 2)])
 def test_gru_packed_weights_equal_gathered(n, B, E, H, T, band_format):
