@@ -38,7 +38,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint16_t bf16s;  // bf16 storage word
 #if GGNN_DT_BF16
-typedef bf16s dt_t;      // storage type of this build
+typedef bf16s dt_t;      // storage type of the bf16 object (GGNN_DT_BF16)
 #else
 typedef float dt_t;
 #endif
