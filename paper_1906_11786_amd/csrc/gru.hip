@@ -328,10 +328,10 @@ __global__ __launch_bounds__(256) void gru_pack_kernel(const S* __restrict__ Wi,
 // ---------------------------------------------------------------------------
 // Forward for large H (bf16, H >= 128), the arithmetic of gru_fwd_kernel
 // with the weights shared through LDS: a workgroup of 8 waves (16 nodes
-// each) streams Wi and U once per 128 nodes, one 16-column gate tile at a
-// time, transposed into fragment order (8 x 8 register tiles) and double
-// buffered.  Pass 1 (tiles of the r gate) forms r and keeps r*h as operand
-// fragments; pass 2 (tiles of z and n) finishes the state.
+// each) streams Wi and U once per 128 nodes in stages of one 16-column gate
+// tile, kept in fragment order, two stages per barrier and double buffered.
+// Pass 1 (tiles of the r gate) forms r and keeps r*h as operand fragments;
+// pass 2 (tiles of z and n) finishes the state.
 // ---------------------------------------------------------------------------
 template <typename S, int H, bool PK>
 __global__ __launch_bounds__(512) void gru_fwd_big_kernel(const float* __restrict__ a, const S* __restrict__ h,
@@ -339,10 +339,13 @@ __global__ __launch_bounds__(512) void gru_fwd_big_kernel(const float* __restric
                                                           const S* __restrict__ pk, const float* __restrict__ b,
                                                           S* __restrict__ h_out, S* __restrict__ saved, int n_pad) {
   static_assert(sizeof(S) == 2, "bf16 only");
-  constexpr int NT = 512, V = 8;
+  constexpr int NT = 512;
   constexpr int KS = H / 32, NC = H / 16;
   constexpr int FR = KS * 64 * 8;                  // elements of one (matrix, 16-column tile) block
-  __shared__ __attribute__((aligned(16))) S lw[2][4 * FR];   // up to four blocks per stage
+  // Stages are staged in pairs (one barrier per two stages; NC is even, so a
+  // pair never spans the two passes), double buffered: four stage buffers.
+  constexpr int SS = 2;
+  __shared__ __attribute__((aligned(16))) S lw[2 * SS][4 * FR];   // up to four blocks per stage
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int q = lane % 16, g = lane / 16;
@@ -355,26 +358,26 @@ __global__ __launch_bounds__(512) void gru_fwd_big_kernel(const float* __restric
   // as gru_fwd_unit, from the packed forward region when PK.
   constexpr int UPB = KS * 64;                     // units per block
   constexpr int RMAX = (4 * UPB + NT - 1) / NT;
-  u32x4 rr[RMAX];
-  auto load_stage = [&](int s) __attribute__((always_inline)) {
+  u32x4 rr[SS][RMAX];
+  auto load_stage = [&](int s, int j) __attribute__((always_inline)) {
     const int nblk = s < NC ? 2 : 4;
 #pragma unroll
     for (int u = 0; u < RMAX; ++u) {
       const int lin = u * NT + tid;
       if (lin < nblk * UPB) {
         if constexpr (PK)
-          rr[u] = *reinterpret_cast<const u32x4*>(pk + ((size_t)GruPack<H>::fwd_stage(s) + lin) * 8);
+          rr[j][u] = *reinterpret_cast<const u32x4*>(pk + ((size_t)GruPack<H>::fwd_stage(s) + lin) * 8);
         else
-          rr[u] = gru_fwd_unit<S, H>(Wi, U, s, lin);
+          rr[j][u] = gru_fwd_unit<S, H>(Wi, U, s, lin);
       }
     }
   };
-  auto store_stage = [&](int s, int bf) __attribute__((always_inline)) {
+  auto store_stage = [&](int s, int j, int bf) __attribute__((always_inline)) {
     const int nblk = s < NC ? 2 : 4;
 #pragma unroll
     for (int u = 0; u < RMAX; ++u) {
       const int lin = u * NT + tid;
-      if (lin < nblk * UPB) *reinterpret_cast<u32x4*>(&lw[bf][lin * 8]) = rr[u];
+      if (lin < nblk * UPB) *reinterpret_cast<u32x4*>(&lw[bf][lin * 8]) = rr[j][u];
     }
   };
 
@@ -393,15 +396,10 @@ __global__ __launch_bounds__(512) void gru_fwd_big_kernel(const float* __restric
     }
   }
   float rhv[8];
-  load_stage(0);
+  static_assert(NC % SS == 0, "stage pairs must not span the two passes");
 #pragma unroll
-  for (int s = 0; s < 2 * NC; ++s) {
-    const int bf = s & 1;
-    store_stage(s, bf);
-    __syncthreads();
-    if (s + 1 < 2 * NC) load_stage(s + 1);
-    if (!valid) continue;
-    const S* L = lw[bf];
+  for (int j = 0; j < SS; ++j) load_stage(j, j);
+  auto compute = [&](int s, const S* L) __attribute__((always_inline)) {
     if (s < NC) {
       f32x4 ar = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -448,6 +446,20 @@ __global__ __launch_bounds__(512) void gru_fwd_big_kernel(const float* __restric
         store4(saved + (size_t)node * 3 * H + 2 * H + f, nn[0], nn[1], nn[2], nn[3]);
       }
     }
+  };
+#pragma unroll
+  for (int s0 = 0; s0 < 2 * NC; s0 += SS) {
+    const int bf = ((s0 / SS) & 1) * SS;
+#pragma unroll
+    for (int j = 0; j < SS; ++j) store_stage(s0 + j, j, bf + j);
+    __syncthreads();
+    if (s0 + SS < 2 * NC) {
+#pragma unroll
+      for (int j = 0; j < SS; ++j) load_stage(s0 + SS + j, j);
+    }
+    if (!valid) continue;
+#pragma unroll
+    for (int j = 0; j < SS; ++j) compute(s0 + j, lw[bf + j]);
   }
 }
 
