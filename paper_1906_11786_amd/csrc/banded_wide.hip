@@ -108,6 +108,10 @@ __device__ __forceinline__ bf16x8 wide_bits_frag(uint32_t byte) {
   return __builtin_bit_cast(bf16x8, w);
 }
 
+// Whether any lane of the wave holds a nonzero x (the same answer in every
+// lane, so a branch on it is taken by the whole wave).
+__device__ __forceinline__ bool wide_any(uint32_t x) { return __builtin_amdgcn_ballot_w64(x != 0u) != 0; }
+
 template <int NB> struct WideBits {
   static constexpr int NW = NB / 4;
   uint32_t w[NW];
@@ -270,6 +274,17 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
       if (s < s_lo || s > s_hi) continue;
+      // Forward: a neighbour block with no edge of this type into the
+      // wave's rows adds exact zeros, so its expansion and products are
+      // skipped (one wave-uniform test per block).
+      if constexpr (!REV) {
+        uint32_t any_bits = 0;
+#pragma unroll
+        for (int n = 0; n < NTW; ++n)
+#pragma unroll
+          for (int i = 0; i < WideBits<RB>::NW; ++i) any_bits |= cur[s][n].w[i];
+        if (!wide_any(any_bits)) continue;
+      }
       const bf16s* xsb = xb + s * XS;
 #pragma unroll
       for (int kk = 0; kk < RB; ++kk) {
