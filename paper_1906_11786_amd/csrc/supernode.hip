@@ -222,25 +222,37 @@ struct SmallGemm {
   const float* bias;
   const float* scale;
 };
+// kSgG threads per output, thread t summing k = t, t + kSgG, ... of every
+// batch in order (the bias of batch bb on thread 0 after its terms); the kSgG
+// partial sums are combined by a fixed butterfly, so the result does not
+// depend on scheduling.
+constexpr int kSgG = 8;
 template <typename TA, typename TB>
 __global__ __launch_bounds__(256) void small_gemm_kernel(SmallGemm p) {
-  const long idx = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long idx = ((long)blockIdx.x * blockDim.x + threadIdx.x) / kSgG;
+  const int t = threadIdx.x % kSgG;
   const long outs = (long)(p.reduce ? 1 : p.nb) * p.M * p.N;
-  if (idx >= outs) return;
+  const bool active = idx < outs;   // the same for the kSgG threads of an output
   const int n = (int)(idx % p.N), m = (int)((idx / p.N) % p.M), b = (int)(idx / ((long)p.N * p.M));
   const TA* A = static_cast<const TA*>(p.A);
   const TB* B = static_cast<const TB*>(p.B);
   float s = 0.f;
-  const int b_lo = p.reduce ? 0 : b, b_hi = p.reduce ? p.nb : b + 1;
-  for (int bb = b_lo; bb < b_hi; ++bb) {
-    for (int k = 0; k < p.K; ++k) {
-      const float a = A ? to_f<TA>(A[bb * p.a_b + m * p.a_m + k * p.a_k]) : 1.f;
-      s += a * to_f<TB>(B[bb * p.b_b + k * p.b_k + n * p.b_n]);
+  if (active) {
+    const int b_lo = p.reduce ? 0 : b, b_hi = p.reduce ? p.nb : b + 1;
+    for (int bb = b_lo; bb < b_hi; ++bb) {
+      for (int k = t; k < p.K; k += kSgG) {
+        const float a = A ? to_f<TA>(A[bb * p.a_b + m * p.a_m + k * p.a_k]) : 1.f;
+        s += a * to_f<TB>(B[bb * p.b_b + k * p.b_k + n * p.b_n]);
+      }
+      if (p.bias && t == 0) s += (p.scale ? p.scale[(long)bb * p.M + m] : 1.f) * p.bias[(long)bb * p.N + n];
     }
-    if (p.bias) s += (p.scale ? p.scale[(long)bb * p.M + m] : 1.f) * p.bias[(long)bb * p.N + n];
   }
-  float* c = p.C + b * p.c_b + m * p.c_m + n * p.c_n;
-  *c = p.accumulate ? *c + s : s;
+#pragma unroll
+  for (int d = kSgG / 2; d > 0; d /= 2) s += __shfl_xor(s, d);
+  if (active && t == 0) {
+    float* c = p.C + b * p.c_b + m * p.c_m + n * p.c_n;
+    *c = p.accumulate ? *c + s : s;
+  }
 }
 
 }  // namespace dev
@@ -251,7 +263,8 @@ using dev::SmallGemm;
 template <typename TA, typename TB>
 hipError_t small_gemm(const SmallGemm& p, hipStream_t st) {
   const long outs = (long)(p.reduce ? 1 : p.nb) * p.M * p.N;
-  hipLaunchKernelGGL((dev::small_gemm_kernel<TA, TB>), dim3((unsigned)((outs + 255) / 256)), dim3(256), 0, st, p);
+  const long threads = outs * dev::kSgG;
+  hipLaunchKernelGGL((dev::small_gemm_kernel<TA, TB>), dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, p);
   return hipGetLastError();
 }
 
