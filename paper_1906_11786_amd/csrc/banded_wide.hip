@@ -1,6 +1,8 @@
-// Wide fused step on a 1-bit block band (bf16 storage, H >= 128, blocks too
-// large to stage whole): the products of the fused step of Eq. 3 in the
-// operand order of Algorithm 1,
+// Wide fused step on a 1-bit block band (bf16 storage, H >= 128, where the
+// three node blocks with all features are too large to stage whole; B from
+// 32 to 512, one workgroup per block row of up to 256 rows, B / 32 waves
+// below that): the products of the fused step of Eq. 3 in the operand order
+// of Algorithm 1,
 //   forward:  a[k]    = sum_e (sum_s bits[e][k][s] X[k-1+s]) W_e   (+ deg_e b_e)
 //   reverse:  dM_e[k] = sum_s bits_t[e][k][s] da[k-1+s]            (stored)
 //             dX[k]   = dX_in[k] + sum_e dM_e[k] W_e^T
@@ -113,10 +115,14 @@ __device__ __forceinline__ bf16x8 wide_bits_frag(uint32_t byte) {
 __device__ __forceinline__ bool wide_any(uint32_t x) { return __builtin_amdgcn_ballot_w64(x != 0u) != 0; }
 
 template <int NB> struct WideBits {
-  static constexpr int NW = NB / 4;
+  static constexpr int NW = NB < 4 ? 1 : NB / 4;
   uint32_t w[NW];
   __device__ __forceinline__ void load(const uint8_t* p) {
-    if constexpr (NB == 4) {
+    if constexpr (NB == 1) {
+      w[0] = *p;
+    } else if constexpr (NB == 2) {
+      w[0] = *reinterpret_cast<const uint16_t*>(p);
+    } else if constexpr (NB == 4) {
       w[0] = *reinterpret_cast<const uint32_t*>(p);
     } else if constexpr (NB == 8) {
       const u32x2 v = *reinterpret_cast<const u32x2*>(p);
@@ -470,6 +476,8 @@ template <int H>
 hipError_t wide_h(bool rev, int n_pad, int B, int E, const void* bits, const void* V, const void* Wsrc,
                   const float* bias, float* out, const float* dX_in, void* dM, long ldm, hipStream_t st) {
   switch (B) {
+    case 32: return wide_launch<H, 32>(rev, n_pad, E, bits, V, Wsrc, bias, out, dX_in, dM, ldm, st);
+    case 64: return wide_launch<H, 64>(rev, n_pad, E, bits, V, Wsrc, bias, out, dX_in, dM, ldm, st);
     case 128: return wide_launch<H, 128>(rev, n_pad, E, bits, V, Wsrc, bias, out, dX_in, dM, ldm, st);
     case 256: return wide_launch<H, 256>(rev, n_pad, E, bits, V, Wsrc, bias, out, dX_in, dM, ldm, st);
     case 512: return wide_launch<H, 512>(rev, n_pad, E, bits, V, Wsrc, bias, out, dX_in, dM, ldm, st);
@@ -481,7 +489,7 @@ hipError_t wide_h(bool rev, int n_pad, int B, int E, const void* bits, const voi
 namespace GGNN_IMPL_NS {
 bool step_wide_applies(int B, int H) {
 #if GGNN_DT_BF16
-  return (H == 128 || H == 256) && (B == 128 || B == 256 || B == 512);
+  return (H == 128 || H == 256) && (B == 32 || B == 64 || B == 128 || B == 256 || B == 512);
 #else
   (void)B;
   (void)H;

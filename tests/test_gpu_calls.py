@@ -311,15 +311,16 @@ STEP_GRU_CASES = [(128, 64, 10, 5), (64, 128, 2, 6), (32, 32, 4, 9), (256, 256, 
 
 def _wide(dt, B, H):
     """Shapes served by the sliced wide step kernel (bf16, H of 128 or 256,
-    B of 128 to 512; the forward only when W_e^T is given)."""
-    return dt == "bf16" and H in (128, 256) and B in (128, 256, 512)
+    B of 32 to 512; the forward only when W_e^T is given)."""
+    return dt == "bf16" and H in (128, 256) and B in (32, 64, 128, 256, 512)
 
 
 # Wide-kernel shapes: E = 1 stages most of each next feature slice after the
 # slice's last type, B = 512 keeps a single node-slice buffer, nb = 1 has no
 # neighbouring blocks, nb >= 3 has interior block rows.
 WIDE_CASES = [(128, 128, 2, 3), (256, 128, 1, 3), (512, 128, 2, 2), (128, 256, 3, 3), (256, 256, 1, 2),
-              (256, 256, 4, 1), (256, 256, 3, 3), (512, 256, 2, 2)]
+              (256, 256, 4, 1), (256, 256, 3, 3), (512, 256, 2, 2), (64, 128, 3, 5), (32, 128, 2, 7),
+              (64, 256, 1, 4), (32, 256, 3, 1)]
 
 
 @pytest.mark.parametrize("B,H,E,nb", WIDE_CASES)
