@@ -272,12 +272,15 @@ def test_gru_packed_weights_equal_gathered(n, B, E, H, T, band_format):
 
 
 @pytest.mark.parametrize("band_format", ["bits", "dense"])
-def test_graph_replay_equals_eager(band_format):
+@pytest.mark.parametrize("B,H", [(128, 64), (128, 128), (64, 256)])
+def test_graph_replay_equals_eager(band_format, B, H):
     """The step captured as a HIP graph: every replay (with eager work and
     synchronizations between replays) gives the eager step's results bit for
-    bit, and they match the oracle."""
-    dt, n, B, E, H, T = "bf16", 1500, 128, 4, 64, 3
-    say(f"graph replay band={band_format}")
+    bit, and they match the oracle.  H = 64 runs the fused step kernels,
+    H >= 128 the wide step kernels and the large-width GRU kernels (weights
+    from their packed copy)."""
+    dt, n, E, T = "bf16", 1500, 4, 3
+    say(f"graph replay band={band_format} B={B} H={H}")
     g = scramble_graph(61, 0, backbone_graph(61, 0, n, E, span_mean=6.0, max_span=B))[0]
     m, res, out = _run_full([g], B, E, H, T, dt, 61, reorder=True, with_bias=True, band_format=band_format)
     _compare(res, out, dt)
