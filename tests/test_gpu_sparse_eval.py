@@ -71,7 +71,7 @@ def test_sparse_step_real_values(dt, H):
     assert relerr(host(a), O.aggregate(n, s, d, e, O.msg_transform(X, W))) <= 1e-4
 
 
-@pytest.mark.parametrize("dt,B,H", [("f32", 32, 32), ("bf16", 32, 64), ("bf16", 64, 128)])
+@pytest.mark.parametrize("dt,B,H", [("f32", 32, 32), ("bf16", 32, 64), ("bf16", 64, 128), ("bf16", 64, 256)])
 def test_lossy_training_then_sparse_evaluation(dt, B, H):
     """A batch whose bandwidth after reordering exceeds B: one banded training
     step drops the out-of-band edges; the updated weights are then evaluated

@@ -87,7 +87,8 @@ def test_super_propagate_bwd_integer_exact(dt, H, E, s, n):
     np.testing.assert_array_equal(host(dbias) - 1.0, wdb)
 
 
-@pytest.mark.parametrize("dt,B,H,s", [("f32", 32, 32, 32), ("bf16", 64, 64, 32), ("bf16", 128, 128, 64)])
+@pytest.mark.parametrize("dt,B,H,s", [("f32", 32, 32, 32), ("bf16", 64, 64, 32), ("bf16", 128, 128, 64),
+                                      ("bf16", 64, 256, 32)])
 def test_supernode_steps_match_oracle(dt, B, H, s):
     """Graphs with hub nodes linked to a large share of their graph: hubs
     become supernodes, the rest is reordered into the band; T steps forward

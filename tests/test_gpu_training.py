@@ -94,7 +94,7 @@ def test_sgd_momentum(nesterov, copy_dt):
 
 
 @pytest.mark.parametrize("dt,n,B,E,H,T", [("f32", 700, 64, 3, 32, 2), ("bf16", 1500, 128, 4, 64, 3),
-                                          ("bf16", 900, 128, 2, 128, 2)])
+                                          ("bf16", 900, 128, 2, 128, 2), ("bf16", 700, 64, 2, 256, 2)])
 @pytest.mark.parametrize("band_format", ["bits", "dense"])
 def test_train_step_matches_oracle(dt, n, B, E, H, T, band_format):
     """Two training steps (propagation, readout, loss, reverse pass, Momentum
