@@ -93,6 +93,7 @@ SMALL = [  # (dt, n_nodes, B, E, H, T, bias)
     ("bf16", 1300, 256, 2, 256, 2, True),
     ("bf16", 2000, 512, 2, 128, 2, False),
     ("bf16", 1100, 64, 5, 128, 3, True),
+    ("f32", 600, 64, 2, 256, 2, True),
 ]
 
 
