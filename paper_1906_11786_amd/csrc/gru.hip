@@ -620,18 +620,24 @@ __global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restric
 // LDS reads; the next chunk's loads are in flight during the products.
 // Wave w: matrix w / 4 (dWi or dU) and a quarter of that matrix's tiles.
 // ---------------------------------------------------------------------------
+#ifndef GGNN_GRU_WGRAD_KC64
+#define GGNN_GRU_WGRAD_KC64 128
+#endif
+#ifndef GGNN_GRU_WGRAD_MAXBUF
+#define GGNN_GRU_WGRAD_MAXBUF 2
+#endif
 template <typename S, int H> struct GruWgradCfg {
   // input features per workgroup: each slice re-reads G^ (3H per row), so
   // slices are as wide as the accumulators allow
   static constexpr int IT = (H >= 256 && sizeof(S) == 2) ? 32 : (H >= 128 ? 4096 / H : H);
   static constexpr int NI = IT / 16, NCT = 3 * H / 16;  // tiles: input, gate columns
-  static constexpr int KC = (sizeof(S) == 4 || H >= 256) ? 32 : (H >= 128 ? 64 : 128);   // rows per chunk
+  static constexpr int KC = (sizeof(S) == 4 || H >= 256) ? 32 : (H >= 128 ? 64 : (H == 64 ? GGNN_GRU_WGRAD_KC64 : 128));   // rows per chunk
   static constexpr int IW = H == 32 ? 1 : NI;            // input tiles per wave
   static constexpr int CW = H == 32 ? 3 : NCT / 4;       // gate-column tiles per wave
   static constexpr int PA = IT + 16, PG = 3 * H + 16;    // LDS row pitches (elements)
   // LDS buffers: two (the next chunk is written while the current one is
   // read) when they fit in 160 KB.
-  static constexpr int NBUF = 2 * KC * (3 * PA + PG) * (int)sizeof(S) <= 160 * 1024 ? 2 : 1;
+  static constexpr int NBUF = GGNN_GRU_WGRAD_MAXBUF >= 2 && 2 * KC * (3 * PA + PG) * (int)sizeof(S) <= 160 * 1024 ? 2 : 1;
 };
 
 template <typename S, int H>
@@ -806,9 +812,12 @@ namespace {
 struct Split {
   int nsplit, per;
 };
+#ifndef GGNN_GRU_WGRAD_WGS
+#define GGNN_GRU_WGRAD_WGS 256
+#endif
 Split gru_split(long K, int H, bool f32) {
   const long slices = (H >= 256 && !f32) ? H / 32 : (H >= 128 ? H / (4096 / H) : 1);
-  const long want = 256 / slices > 0 ? 256 / slices : 1;
+  const long want = GGNN_GRU_WGRAD_WGS / slices > 0 ? GGNN_GRU_WGRAD_WGS / slices : 1;
   long per = ((K + want - 1) / want + 127) / 128 * 128;
   return {(int)((K + per - 1) / per), (int)per};
 }

@@ -297,11 +297,18 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
 // Wave w owns the (type, output tile) pairs w, w + 8, ... of its workgroup,
 // each over all IT/16 input tiles.
 // ---------------------------------------------------------------------------
+#ifndef GGNN_WGRAD_TE64
+#define GGNN_WGRAD_TE64 4
+#endif
+// Edge types per workgroup of the node-major form.
+constexpr int wgrad_nm_types(int H, bool f32) {
+  return H <= 32 ? 10 : (H == 64 ? GGNN_WGRAD_TE64 : (H == 128 && !f32 ? 2 : 1));
+}
 template <typename S, int H> struct WgradNmCfg {
   // All input features per workgroup: the stored dM (the large operand) is
   // then read once; the H = 256 fp32 form keeps 64-feature slices.
   static constexpr int IT = (H >= 256 && sizeof(S) == 4) ? 64 : H;   // input features per workgroup
-  static constexpr int TE = H <= 32 ? 10 : (H == 64 ? 4 : (H == 128 && sizeof(S) == 2 ? 2 : 1));   // types per workgroup
+  static constexpr int TE = wgrad_nm_types(H, sizeof(S) == 4);   // types per workgroup
   static constexpr int KC = (sizeof(S) == 4 || H >= 256) ? 64 : 128;   // rows per chunk
   static constexpr int PX = IT + 16, PD = H + 16;                // LDS row pitches (elements)
   static constexpr int NPAIR = TE * H / 16;                      // (type, output tile) pairs
@@ -590,10 +597,12 @@ Split transform_split(long K, int H, int E) {
 // Node-major form: about 256 workgroups (one per compute unit, 8 waves
 // each) over splits x type groups x input slices (fp32 at H = 256 only);
 // splits are multiples of 128 rows.
-Split transform_nm_split(long K, int H, int E, bool f32) {
-  const long te = H <= 32 ? 10 : (H == 64 ? 4 : (H == 128 ? 2 : 1));
+#ifndef GGNN_WGRAD_NM_WGS
+#define GGNN_WGRAD_NM_WGS 256
+#endif
+Split transform_nm_split(long K, int H, int E, int te, bool f32) {
   const long per_split = ((E + te - 1) / te) * (H >= 256 && f32 ? H / 64 : 1);
-  const long want = 256 / per_split > 0 ? 256 / per_split : 1;
+  const long want = GGNN_WGRAD_NM_WGS / per_split > 0 ? GGNN_WGRAD_NM_WGS / per_split : 1;
   long per = ((K + want - 1) / want + 127) / 128 * 128;
   return {(int)((K + per - 1) / per), (int)per};
 }
@@ -642,8 +651,8 @@ hipError_t transform_wgrad_h(long K, int E, const void* X, const void* dM, long 
 template <typename S, int H>
 hipError_t transform_wgrad_nm_h(long K, int E, const void* X, const void* dM, long ldk, float* dW, float* dbias,
                                 void* ws, ReduceList* defer, hipStream_t st) {
-  Split sp = transform_nm_split(K, H, E, sizeof(S) == 4);
   using C = dev::WgradNmCfg<S, H>;
+  Split sp = transform_nm_split(K, H, E, C::TE, sizeof(S) == 4);
   float* P = static_cast<float*>(ws);
   float* Pb = dbias ? P + (size_t)sp.nsplit * E * H * H : nullptr;
   const int blocks = sp.nsplit * ((E + C::TE - 1) / C::TE) * (H / C::IT);
@@ -706,8 +715,8 @@ hipError_t transform_wgrad_t(long K, int H, int E, const void* X, const void* dM
 #if GGNN_DT_BF16
 size_t transform_wgrad_workspace(long K, int H, int E) {
   // large enough for both forms (feature-major and node-major dM)
-  const Split a = transform_split(K, H, E), b = transform_nm_split(K, H, E, false),
-              c = transform_nm_split(K, H, E, true);
+  const Split a = transform_split(K, H, E), b = transform_nm_split(K, H, E, dev::wgrad_nm_types(H, false), false),
+              c = transform_nm_split(K, H, E, dev::wgrad_nm_types(H, true), true);
   size_t n = (size_t)(a.nsplit > b.nsplit ? a.nsplit : b.nsplit);
   if ((size_t)c.nsplit > n) n = (size_t)c.nsplit;
   return (n * E * H * H + n * E * H) * sizeof(float);
