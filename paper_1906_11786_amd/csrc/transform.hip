@@ -300,6 +300,9 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
 #ifndef GGNN_WGRAD_TE64
 #define GGNN_WGRAD_TE64 4
 #endif
+#ifndef GGNN_WGRAD_KC64
+#define GGNN_WGRAD_KC64 128
+#endif
 // Edge types per workgroup of the node-major form.
 constexpr int wgrad_nm_types(int H, bool f32) {
   return H <= 32 ? 10 : (H == 64 ? GGNN_WGRAD_TE64 : (H == 128 && !f32 ? 2 : 1));
@@ -309,7 +312,7 @@ template <typename S, int H> struct WgradNmCfg {
   // then read once; the H = 256 fp32 form keeps 64-feature slices.
   static constexpr int IT = (H >= 256 && sizeof(S) == 4) ? 64 : H;   // input features per workgroup
   static constexpr int TE = wgrad_nm_types(H, sizeof(S) == 4);   // types per workgroup
-  static constexpr int KC = (sizeof(S) == 4 || H >= 256) ? 64 : 128;   // rows per chunk
+  static constexpr int KC = (sizeof(S) == 4 || H >= 256) ? 64 : (H == 64 ? GGNN_WGRAD_KC64 : 128);   // rows per chunk
   static constexpr int PX = IT + 16, PD = H + 16;                // LDS row pitches (elements)
   static constexpr int NPAIR = TE * H / 16;                      // (type, output tile) pairs
   static constexpr int PW = (NPAIR + 7) / 8;                     // pairs per wave (at most)
