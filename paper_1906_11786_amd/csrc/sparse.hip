@@ -20,24 +20,28 @@
 namespace ggnn {
 namespace dev {
 
-// The waves of a workgroup share 16 receivers and split the edge types among
-// them (wave w takes types w, w + NW, ...), which multiplies the waves in
-// flight by NW and shortens each wave's chain of dependent loads (list
-// bounds, column index, sender row) by the same factor. Their partial results
-// are added through LDS in wave order, so the output does not depend on
-// timing. NW = 8 up to H = 64, 4 above (the partials take NW * H * 64 bytes
-// of LDS).
+// On small graphs (few groups of 16 receivers) the waves of a workgroup share
+// 16 receivers and split the edge types among them (wave w takes types w,
+// w + NW, ...), which multiplies the waves in flight by NW and shortens each
+// wave's chain of dependent loads (list bounds, column index, sender row) by
+// the same factor. Their partial results are added through LDS in wave
+// order, so the output does not depend on timing. NW = 8 up to H = 64, 4
+// above (the partials take NW * H * 64 bytes of LDS). Larger graphs give
+// every SIMD several waves already: there NW = 1 (one wave walks all types).
 template <int H>
 constexpr int sparse_waves() { return H <= 64 ? 8 : 4; }
+#ifndef GGNN_SPARSE_SPLIT_MAX_GROUPS
+#define GGNN_SPARSE_SPLIT_MAX_GROUPS 2048
+#endif
 
-template <typename S, int H, int NW = sparse_waves<H>()>
+template <typename S, int H, int NW>
 __global__ __launch_bounds__(NW * kWave) void sparse_step_kernel(
     const int32_t* __restrict__ row_ptr, const int32_t* __restrict__ col, const S* __restrict__ X,
     const S* __restrict__ Wt, const float* __restrict__ bias, float* __restrict__ out, int n_pad, int E) {
   constexpr int HK = H / 32, MT = H / 16;
   constexpr int NP = sizeof(S) == 2 ? 2 : 1;
   // partial results: red[wave][mo][lane], one f32x4 per lane and output tile
-  __shared__ f32x4 red[NW][MT][kWave];
+  __shared__ f32x4 red[NW > 1 ? NW : 1][NW > 1 ? MT : 1][kWave];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int q = lane % 16, g = lane / 16;
   const int n0 = blockIdx.x * 16;
@@ -51,8 +55,8 @@ __global__ __launch_bounds__(NW * kWave) void sparse_step_kernel(
   // Up to two of the wave's edge types per pass: their gathers are
   // independent, so both lists' loads are in flight together. Each list is
   // still walked in order, so every type's sum is formed as with one type at
-  // a time. Above H = 128 a second set of partial sums would cost occupancy.
-  constexpr int NE = H <= 128 ? 2 : 1;
+  // a time. Above H = 64 a second set of partial sums costs occupancy.
+  constexpr int NE = H <= 64 ? 2 : 1;
   for (int k0 = 0; wave + NW * k0 < E; k0 += NE) {
     // List bounds of the pass's types; a type index past E is clamped to the
     // node's last bound and so gets an empty list.
@@ -133,6 +137,13 @@ __global__ __launch_bounds__(NW * kWave) void sparse_step_kernel(
       }
     }
   }
+  if constexpr (NW == 1) {
+    // acc[mo] = D[feature 16mo + 4g + j][receiver q]
+#pragma unroll
+    for (int mo = 0; mo < MT; ++mo)
+      *reinterpret_cast<f32x4*>(out + (size_t)node * H + 16 * mo + 4 * g) = acc[mo];
+    return;
+  }
 #pragma unroll
   for (int mo = 0; mo < MT; ++mo) red[wave][mo][lane] = acc[mo];
   __syncthreads();
@@ -157,9 +168,16 @@ hipError_t launch_sparse_step(int n_pad, int H, int E, const int32_t* row_ptr, c
                               const void* Wt, const float* bias, float* a, hipStream_t st) {
   using S = dev::dt_t;
   const int blocks = n_pad / 16;   // n_pad is a multiple of 32 (checked by the caller)
-#define GGNN_SPARSE(HH)                                                                                          \
-  hipLaunchKernelGGL((dev::sparse_step_kernel<S, HH>), dim3(blocks), dim3(dev::sparse_waves<HH>() * 64), 0, st,    \
-                     row_ptr, col, static_cast<const S*>(X), static_cast<const S*>(Wt), bias, a, n_pad, E)
+  const bool split = blocks <= GGNN_SPARSE_SPLIT_MAX_GROUPS;
+#define GGNN_SPARSE_NW(HH, NWV)                                                                               \
+  hipLaunchKernelGGL((dev::sparse_step_kernel<S, HH, NWV>), dim3(blocks), dim3((NWV) * 64), 0, st, row_ptr, col, \
+                     static_cast<const S*>(X), static_cast<const S*>(Wt), bias, a, n_pad, E)
+#define GGNN_SPARSE(HH)                                  \
+  if (split) {                                           \
+    GGNN_SPARSE_NW(HH, dev::sparse_waves<HH>());         \
+  } else {                                               \
+    GGNN_SPARSE_NW(HH, 1);                               \
+  }
   switch (H) {
     case 32: GGNN_SPARSE(32); break;
     case 64: GGNN_SPARSE(64); break;
@@ -168,6 +186,7 @@ hipError_t launch_sparse_step(int n_pad, int H, int E, const int32_t* row_ptr, c
     default: return hipErrorInvalidValue;
   }
 #undef GGNN_SPARSE
+#undef GGNN_SPARSE_NW
   return hipGetLastError();
 }
 }  // namespace GGNN_IMPL_NS

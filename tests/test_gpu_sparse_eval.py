@@ -35,7 +35,8 @@ def _wt(W, dt):
 
 
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
-@pytest.mark.parametrize("H,E,n", [(32, 3, 160), (64, 10, 512), (128, 2, 96), (256, 4, 224), (64, 1, 64), (128, 7, 128)])
+@pytest.mark.parametrize("H,E,n", [(32, 3, 160), (64, 10, 512), (128, 2, 96), (256, 4, 224), (64, 1, 64), (128, 7, 128),
+                                   (64, 10, 33280), (128, 3, 33280)])
 def test_sparse_step_integer_exact(dt, H, E, n):
     """Random edges anywhere in the graph (no band), repeated edges, nodes
     without incoming edges, a bias: small integers, exact."""
