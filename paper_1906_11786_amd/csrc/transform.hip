@@ -7,6 +7,8 @@
 #include "device_common.h"
 #include "kernels.h"
 
+#include <type_traits>
+
 namespace ggnn {
 namespace dev {
 
@@ -472,43 +474,48 @@ __global__ __launch_bounds__(512) void transform_wgrad_nm_kernel(const S* __rest
 
 #if GGNN_DT_BF16   // dtype-independent kernels: built once
 // out[i] += sum_{s < nsplit} part[s * stride + i] for i < count.  A
-// workgroup of 64 x RW threads owns 64 consecutive outputs: thread (x, y)
-// sums the splits s = y, y + RW, y + 2RW, ... in increasing order (eight
-// loads in flight), then thread (x, 0) adds the RW sums in order y = 0..RW-1.
-// The order depends only on nsplit, so results do not depend on scheduling.
+// workgroup of 64 x RW threads owns 64 V consecutive outputs: thread (x, y)
+// sums, for its V outputs, the splits s = y, y + RW, y + 2RW, ... in
+// increasing order (eight loads in flight), then thread (x, 0) adds the RW
+// sums in order y = 0..RW-1.  The order depends only on nsplit, so results do
+// not depend on scheduling, and V = 4 (16-byte loads; count, stride and both
+// pointers must be multiples of four floats) gives the same bits as V = 1.
 constexpr int kReduceRW = 16;
+template <int V>
 __device__ __forceinline__ void reduce_block(const float* __restrict__ part, float* __restrict__ out, int nsplit,
                                              int count, long stride, int blk) {
+  using T = std::conditional_t<V == 4, dev::f32x4, float>;
   constexpr int RW = kReduceRW;
-  __shared__ float red[RW][64];
+  __shared__ T red[RW][64];
   const int x = threadIdx.x % 64, y = threadIdx.x / 64;
-  const int i = blk * 64 + x;
-  float s = 0.f;
+  const int i = (blk * 64 + x) * V;
+  T s = {};
   if (i < count) {
     int k = y;
     for (; k + 7 * RW < nsplit; k += 8 * RW) {
-      float v[8];
+      T v[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = part[(size_t)(k + j * RW) * stride + i];
+      for (int j = 0; j < 8; ++j) v[j] = *reinterpret_cast<const T*>(part + (size_t)(k + j * RW) * stride + i);
 #pragma unroll
       for (int j = 0; j < 8; ++j) s += v[j];
     }
-    for (; k < nsplit; k += RW) s += part[(size_t)k * stride + i];
+    for (; k < nsplit; k += RW) s += *reinterpret_cast<const T*>(part + (size_t)k * stride + i);
   }
   red[y][x] = s;
   __syncthreads();
   if (y == 0 && i < count) {
-    float t = 0.f;
+    T t = {};
 #pragma unroll
     for (int w = 0; w < RW; ++w) t += red[w][x];
-    out[i] += t;
+    T* o = reinterpret_cast<T*>(out + i);
+    *o = *o + t;
   }
 }
 
 __global__ __launch_bounds__(64 * kReduceRW) void reduce_partials_kernel(const float* __restrict__ part,
                                                                          float* __restrict__ out, int nsplit,
                                                                          int count, long stride) {
-  reduce_block(part, out, nsplit, count, stride, blockIdx.x);
+  reduce_block<1>(part, out, nsplit, count, stride, blockIdx.x);
 }
 
 // Several reductions in one launch (the weight-gradient partials of one
@@ -516,6 +523,7 @@ __global__ __launch_bounds__(64 * kReduceRW) void reduce_partials_kernel(const f
 struct ReduceMulti {
   ReduceSeg seg[ReduceList::kMax];
   int first[ReduceList::kMax + 1];
+  int vec[ReduceList::kMax];   // 4: the segment meets the 16-byte conditions of reduce_block<4>
   int n;
 };
 __global__ __launch_bounds__(64 * kReduceRW) void reduce_multi_kernel(ReduceMulti m) {
@@ -523,7 +531,11 @@ __global__ __launch_bounds__(64 * kReduceRW) void reduce_multi_kernel(ReduceMult
   int si = 0;
   while (si + 1 < m.n && b >= m.first[si + 1]) ++si;
   const ReduceSeg sg = m.seg[si];
-  reduce_block(sg.part, sg.out, sg.nsplit, sg.count, sg.stride, b - m.first[si]);
+  if (m.vec[si] == 4) {
+    reduce_block<4>(sg.part, sg.out, sg.nsplit, sg.count, sg.stride, b - m.first[si]);
+  } else {
+    reduce_block<1>(sg.part, sg.out, sg.nsplit, sg.count, sg.stride, b - m.first[si]);
+  }
 }
 
 hipError_t launch_reduce_multi(const ReduceList& l, hipStream_t st) {
@@ -532,8 +544,12 @@ hipError_t launch_reduce_multi(const ReduceList& l, hipStream_t st) {
   m.n = l.n;
   m.first[0] = 0;
   for (int i = 0; i < l.n; ++i) {
-    m.seg[i] = l.seg[i];
-    m.first[i + 1] = m.first[i] + (l.seg[i].count + 63) / 64;
+    const ReduceSeg& sg = l.seg[i];
+    m.seg[i] = sg;
+    const bool v4 = sg.count % 4 == 0 && sg.stride % 4 == 0 && reinterpret_cast<uintptr_t>(sg.part) % 16 == 0 &&
+                    reinterpret_cast<uintptr_t>(sg.out) % 16 == 0;
+    m.vec[i] = v4 ? 4 : 1;
+    m.first[i + 1] = m.first[i] + (sg.count + 64 * m.vec[i] - 1) / (64 * m.vec[i]);
   }
   hipLaunchKernelGGL(reduce_multi_kernel, dim3(m.first[l.n]), dim3(64 * kReduceRW), 0, st, m);
   return hipGetLastError();
