@@ -621,7 +621,7 @@ __global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restric
 // Wave w: matrix w / 4 (dWi or dU) and a quarter of that matrix's tiles.
 // ---------------------------------------------------------------------------
 #ifndef GGNN_GRU_WGRAD_KC64
-#define GGNN_GRU_WGRAD_KC64 128
+#define GGNN_GRU_WGRAD_KC64 64
 #endif
 #ifndef GGNN_GRU_WGRAD_MAXBUF
 #define GGNN_GRU_WGRAD_MAXBUF 2
