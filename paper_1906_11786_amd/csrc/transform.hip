@@ -291,12 +291,12 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
 // step writes dM_e rows node by node): one split of the rows,
 //   P[split][e][h_in][h_out] = sum_k X[k][h_in] * dM[e][k][h_out],
 //   Pb[split][e][h_out]      = sum_k dM[e][k][h_out],
-// rows k of type e at dM + (e * ldk + k) * H.  A workgroup (8 waves) owns one
+// rows k of type e at dM + (e * ldk + k) * H.  A workgroup (NWV waves) owns one
 // split of the rows, a group of TE edge types and a slice of IT input
 // features: per chunk of KC rows it stages X and the group's dM rows
 // node-major in LDS (plain 16-byte copies) and reads them as matrix-core
 // fragments with transposing LDS reads, the next chunk's loads in flight.
-// Wave w owns the (type, output tile) pairs w, w + 8, ... of its workgroup,
+// Wave w owns the (type, output tile) pairs w, w + NWV, ... of its workgroup,
 // each over all IT/16 input tiles.
 // ---------------------------------------------------------------------------
 #ifndef GGNN_WGRAD_TE64
@@ -304,6 +304,9 @@ __global__ __launch_bounds__((H < 64 ? H : 64) / 16 * kWave) void transform_wgra
 #endif
 #ifndef GGNN_WGRAD_KC64
 #define GGNN_WGRAD_KC64 128
+#endif
+#ifndef GGNN_WGRAD_WAVES64
+#define GGNN_WGRAD_WAVES64 8
 #endif
 // Edge types per workgroup of the node-major form.
 constexpr int wgrad_nm_types(int H, bool f32) {
@@ -317,18 +320,19 @@ template <typename S, int H> struct WgradNmCfg {
   static constexpr int KC = (sizeof(S) == 4 || H >= 256) ? 64 : (H == 64 ? GGNN_WGRAD_KC64 : 128);   // rows per chunk
   static constexpr int PX = IT + 16, PD = H + 16;                // LDS row pitches (elements)
   static constexpr int NPAIR = TE * H / 16;                      // (type, output tile) pairs
-  static constexpr int PW = (NPAIR + 7) / 8;                     // pairs per wave (at most)
+  static constexpr int NWV = (H == 64 && sizeof(S) == 2) ? GGNN_WGRAD_WAVES64 : 8;   // waves per workgroup
+  static constexpr int PW = (NPAIR + NWV - 1) / NWV;             // pairs per wave (at most)
   static constexpr int NBUF = 2 * KC * (PX + TE * PD) * (int)sizeof(S) <= 160 * 1024 ? 2 : 1;
 };
 
 template <typename S, int H>
-__global__ __launch_bounds__(512) void transform_wgrad_nm_kernel(const S* __restrict__ X, const S* __restrict__ dM,
+__global__ __launch_bounds__(64 * (WgradNmCfg<S, H>::NWV)) void transform_wgrad_nm_kernel(const S* __restrict__ X, const S* __restrict__ dM,
                                                                  long ldk, float* __restrict__ P,
                                                                  float* __restrict__ Pb, long K, int E,
                                                                  int rows_per_split) {
   using C = WgradNmCfg<S, H>;
   constexpr int IT = C::IT, TE = C::TE, KC = C::KC, PX = C::PX, PD = C::PD, PW = C::PW, NBUF = C::NBUF;
-  constexpr int NT = 512, NI = IT / 16;
+  constexpr int NWV = C::NWV, NT = 64 * NWV, NI = IT / 16;
   constexpr int V = 16 / sizeof(S);
   constexpr int NX = KC * IT / V, ND = TE * KC * H / V;   // 16-byte units per chunk
   constexpr int UX = (NX + NT - 1) / NT, UD = (ND + NT - 1) / NT;
@@ -413,8 +417,8 @@ __global__ __launch_bounds__(512) void transform_wgrad_nm_kernel(const S* __rest
         for (int i = 0; i < NI; ++i) fa[i] = tr_frag(sx[buf], PX, k0, 16 * i, lane);
 #pragma unroll
         for (int p = 0; p < PW; ++p) {
-          const int pr = wave + 8 * p;
-          if (PW * 8 == C::NPAIR || pr < C::NPAIR) {
+          const int pr = wave + NWV * p;
+          if (PW * NWV == C::NPAIR || pr < C::NPAIR) {
             const int te = pr / (H / 16), ot = pr % (H / 16);
             const frag_t<S> fb = tr_frag(sd[buf] + te * KC * PD, PD, k0, 16 * ot, lane);
 #pragma unroll
@@ -430,8 +434,8 @@ __global__ __launch_bounds__(512) void transform_wgrad_nm_kernel(const S* __rest
       frag_t<S> fb[PW];
 #pragma unroll
       for (int p = 0; p < PW; ++p) {
-        const int pr = wave + 8 * p;
-        if (PW * 8 == C::NPAIR || pr < C::NPAIR) {
+        const int pr = wave + NWV * p;
+        if (PW * NWV == C::NPAIR || pr < C::NPAIR) {
           const int te = pr / (H / 16), ot = pr % (H / 16);
           fb[p] = tr_frag(sd[buf] + te * KC * PD, PD, k0, 16 * ot, lane);
 #pragma unroll
@@ -443,8 +447,8 @@ __global__ __launch_bounds__(512) void transform_wgrad_nm_kernel(const S* __rest
         const frag_t<S> fa = tr_frag(sx[buf], PX, k0, 16 * i, lane);
 #pragma unroll
         for (int p = 0; p < PW; ++p) {
-          const int pr = wave + 8 * p;
-          if (PW * 8 == C::NPAIR || pr < C::NPAIR) mma(acc[p][i], fa, fb[p]);
+          const int pr = wave + NWV * p;
+          if (PW * NWV == C::NPAIR || pr < C::NPAIR) mma(acc[p][i], fa, fb[p]);
         }
       }
     }
@@ -452,8 +456,8 @@ __global__ __launch_bounds__(512) void transform_wgrad_nm_kernel(const S* __rest
   // D[h_in = i0 + 16 i + 4g + j][h_out = 16 ot + q] of type e0 + te
 #pragma unroll
   for (int p = 0; p < PW; ++p) {
-    const int pr = wave + 8 * p;
-    if (!(PW * 8 == C::NPAIR || pr < C::NPAIR)) continue;
+    const int pr = wave + NWV * p;
+    if (!(PW * NWV == C::NPAIR || pr < C::NPAIR)) continue;
     const int te = pr / (H / 16), ot = pr % (H / 16);
     if (te >= ne) continue;
     float* out = P + ((size_t)split * E + e0 + te) * H * H;
@@ -675,7 +679,7 @@ hipError_t transform_wgrad_nm_h(long K, int E, const void* X, const void* dM, lo
   float* P = static_cast<float*>(ws);
   float* Pb = dbias ? P + (size_t)sp.nsplit * E * H * H : nullptr;
   const int blocks = sp.nsplit * ((E + C::TE - 1) / C::TE) * (H / C::IT);
-  hipLaunchKernelGGL((dev::transform_wgrad_nm_kernel<S, H>), dim3(blocks), dim3(512), 0, st,
+  hipLaunchKernelGGL((dev::transform_wgrad_nm_kernel<S, H>), dim3(blocks), dim3(64 * C::NWV), 0, st,
                      static_cast<const S*>(X), static_cast<const S*>(dM), ldk, P, Pb, K, E, sp.per);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
