@@ -87,6 +87,10 @@ def parse():
     p.add_argument("--drops", action="store_true",
                    help="host only: print the edges each block size keeps and drops on the workload's graphs "
                         "(with and without reordering, and with long-span variants of the graphs), then exit")
+    p.add_argument("--stream-probe", action="store_true",
+                   help="print the streaming rates of torch's own kernels on this GPU (sums over 1 GiB fp32 and "
+                        "512 MiB bf16: reads only; a 1 GiB copy: read + write), the practical reference for an "
+                        "HBM-bound kernel next to the 8 TB/s peak, and exit")
     p.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="summarise two rocprofv3 --pmc counter files (FETCH_SIZE, WRITE_SIZE) of this command "
                         "and exit")
@@ -308,8 +312,35 @@ def drops_table(spec_name: str) -> str:
     return "\n".join(rows)
 
 
+def stream_probe(reps=10):
+    """Streaming rates of library kernels (HIP events around `reps` launches
+    after one warm-up), in bytes moved per second."""
+    import torch
+    x = torch.empty(256 << 20, dtype=torch.float32, device="cuda").uniform_()
+    y = torch.empty_like(x)
+    xb = torch.empty(256 << 20, dtype=torch.bfloat16, device="cuda").uniform_()
+    out = {}
+    for name, f, nbytes in [("sum_fp32_1GiB_read", lambda: x.sum(), x.numel() * 4),
+                            ("sum_bf16_512MiB_read", lambda: xb.sum(), xb.numel() * 2),
+                            ("copy_fp32_1GiB_read_write", lambda: y.copy_(x), 2 * x.numel() * 4)]:
+        f()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            f()
+        b.record()
+        torch.cuda.synchronize()
+        sec = a.elapsed_time(b) / reps * 1e-3
+        out[name] = {"us": round(sec * 1e6, 1), "TB_per_s": round(nbytes / sec / 1e12, 3)}
+    return out
+
+
 def main():
     args = parse()
+    if args.stream_probe:
+        print(json.dumps({"stream_probe": stream_probe(), "hbm_peak_TB_per_s": HBM_PEAK_GBS / 1000}))
+        return
     if args.drops:
         print(drops_table(args.workload))
         return
