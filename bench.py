@@ -44,7 +44,6 @@ HBM_PEAK_GBS = 8000.0       # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix cores
 FP32_PEAK_TFLOPS = 157.3    # MI355X fp32 matrix cores
 
-WORKLOADS = {"program_graph": 1, "tiny": 0, "batch_100k": 2, "stress_1m": 4}
 
 # C-ABI entry point -> (device kernel name fragments, sources that define it)
 KERNELS = {
@@ -169,9 +168,9 @@ def traffic_summary(fetch_csv, write_csv, cmd_line):
 
 
 def spec_for(name):
-    from ggnn_synth import CONFIGS, sweep_blocks
+    from ggnn_synth import WORKLOADS, sweep_blocks
     if name in WORKLOADS:
-        return CONFIGS[WORKLOADS[name]]
+        return WORKLOADS[name]
     if name.startswith("sweep_B"):
         B = int(name[len("sweep_B"):])
         for s in sweep_blocks():

@@ -10,5 +10,6 @@ from .graphs import (  # noqa: F401
     STREAM_X, STREAM_W, STREAM_GRU, STREAM_G, STREAM_HUBS, add_hubs,
 )
 from .params import draw_params, round_bf16, Params  # noqa: F401
-from .configs import CONFIGS, ConfigSpec, make_graphs, sweep_blocks  # noqa: F401
+from .configs import (CONFIGS, WORKLOADS, TINY, PROGRAM_GRAPH, BATCH_100K, STRESS_1M, ConfigSpec,  # noqa: F401
+                      make_graphs, sweep_blocks)
 from .readout import Candidates, draw_candidates, draw_readout, STREAM_CAND  # noqa: F401

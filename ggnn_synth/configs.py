@@ -62,6 +62,14 @@ CONFIGS = {
 }
 
 
+# The workloads by name.
+TINY = CONFIGS[0]
+PROGRAM_GRAPH = CONFIGS[1]
+BATCH_100K = CONFIGS[2]
+STRESS_1M = CONFIGS[4]
+WORKLOADS = {"tiny": TINY, "program_graph": PROGRAM_GRAPH, "batch_100k": BATCH_100K, "stress_1m": STRESS_1M}
+
+
 def sweep_blocks() -> list[ConfigSpec]:
     return [_c3(B) for B in SWEEP_BLOCKS]
 

@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 
 import oracle as O
-from ggnn_synth import CONFIGS, make_graphs, sweep_blocks, draw_params, backbone_graph, scramble_graph, Graph
+from ggnn_synth import BATCH_100K, PROGRAM_GRAPH, STRESS_1M, TINY, make_graphs, sweep_blocks, draw_params, backbone_graph, scramble_graph, Graph
 from gpu_helpers import TOL, relerr, say
 
 pytestmark = pytest.mark.gpu
@@ -75,7 +75,7 @@ def _run_full(graphs, spec_B, E, H, T, dt, cfg, reorder, with_bias=False, band_f
 
 @pytest.mark.parametrize("band_format", ["bits", "dense"])
 def test_tiny_fp32_workload(band_format):
-    spec = CONFIGS[0]
+    spec = TINY
     say(f"workload {spec.name} band={band_format}")
     g = make_graphs(spec)
     _, res, out = _run_full(g, spec.B, spec.E, spec.H, spec.T, spec.dtype, spec.cfg, reorder=False,
@@ -125,7 +125,7 @@ def test_small_lossy_band(band_format):
 
 @pytest.mark.parametrize("band_format", ["bits", "dense"])
 def test_program_graph_workload(band_format):
-    spec = CONFIGS[1]
+    spec = PROGRAM_GRAPH
     say(f"workload {spec.name} band={band_format}")
     g = make_graphs(spec)
     m, res, out = _run_full(g, spec.B, spec.E, spec.H, spec.T, spec.dtype, spec.cfg, reorder=True,
@@ -195,11 +195,11 @@ def _sampled_batch(spec, picks):
 
 
 def test_batch_100k_workload_sampled():
-    _sampled_batch(CONFIGS[2], picks=[0, 7, 19])
+    _sampled_batch(BATCH_100K, picks=[0, 7, 19])
 
 
 def test_stress_1m_workload_sampled():
-    _sampled_batch(CONFIGS[4], picks=[0, 70, 139])
+    _sampled_batch(STRESS_1M, picks=[0, 70, 139])
 
 
 def _no_edges(n):

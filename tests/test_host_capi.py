@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 import oracle as O
-from ggnn_synth import CONFIGS, make_graphs, backbone_graph, scramble_graph, local_window_graph
+from ggnn_synth import PROGRAM_GRAPH, make_graphs, backbone_graph, scramble_graph, local_window_graph
 
 capi = pytest.importorskip("paper_1906_11786_amd.capi")
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -73,11 +73,11 @@ def test_rcm_bit_exact_against_oracle():
 
 def test_rcm_bit_exact_on_program_graph_workload():
     _need_lib()
-    g = make_graphs(CONFIGS[1])[0]
+    g = make_graphs(PROGRAM_GRAPH)[0]
     order, rank, bw = capi.ggnn_rcm_order(g.n, g.src, g.dst)
     o_order, _ = O.rcm_order(g.n, g.src, g.dst)
     np.testing.assert_array_equal(order, o_order)
-    assert bw <= CONFIGS[1].B - 1
+    assert bw <= PROGRAM_GRAPH.B - 1
 
 
 @pytest.mark.parametrize("dt", ["f32", "bf16"])

@@ -14,7 +14,7 @@ import scipy.sparse as sp
 from scipy.sparse.csgraph import reverse_cuthill_mckee, connected_components, breadth_first_order
 
 import oracle as O
-from ggnn_synth import CONFIGS, make_graphs, backbone_graph, scramble_graph, local_window_graph
+from ggnn_synth import BATCH_100K, TINY, make_graphs, backbone_graph, scramble_graph, local_window_graph
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
@@ -454,9 +454,9 @@ def test_supergraph_components_do_not_interact():
 def test_workload_graphs_fit_the_band_after_reordering():
     """The bf16 workloads are built so that reordering brings every edge into
     the 128 band (zero drops)."""
-    for gi, g in enumerate(make_graphs(CONFIGS[2], max_graphs=3)):
+    for gi, g in enumerate(make_graphs(BATCH_100K, max_graphs=3)):
         order, rank = O.rcm_order(g.n, g.src, g.dst)
         s, d = O.relabel(rank, g.src, g.dst)
-        assert O.bandwidth(s, d) <= CONFIGS[2].B - 1, gi
-    g = make_graphs(CONFIGS[0])[0]
-    assert O.bandwidth(g.src, g.dst) <= CONFIGS[0].B - 1
+        assert O.bandwidth(s, d) <= BATCH_100K.B - 1, gi
+    g = make_graphs(TINY)[0]
+    assert O.bandwidth(g.src, g.dst) <= TINY.B - 1

@@ -2,13 +2,13 @@
 import numpy as np
 import pytest
 
-from ggnn_synth import (CONFIGS, make_graphs, sweep_blocks, draw_params, round_bf16, lognormal_batch_sizes,
+from ggnn_synth import (PROGRAM_GRAPH, TINY, make_graphs, sweep_blocks, draw_params, round_bf16, lognormal_batch_sizes,
                         backbone_graph, local_window_graph)
 
 
 def test_generators_are_reproducible():
-    a = make_graphs(CONFIGS[1])[0]
-    b = make_graphs(CONFIGS[1])[0]
+    a = make_graphs(PROGRAM_GRAPH)[0]
+    b = make_graphs(PROGRAM_GRAPH)[0]
     assert np.array_equal(a.src, b.src) and np.array_equal(a.dst, b.dst) and np.array_equal(a.etype, b.etype)
     p1 = draw_params(1, 100, 128, 64, 10, "bf16")
     p2 = draw_params(1, 100, 128, 64, 10, "bf16")
@@ -16,7 +16,7 @@ def test_generators_are_reproducible():
 
 
 def test_tiny_config_edges():
-    spec = CONFIGS[0]
+    spec = TINY
     g = make_graphs(spec)[0]
     assert g.n == 512 and set(np.unique(g.etype)) == {0, 1}
     span = np.abs(g.src - g.dst)
@@ -27,7 +27,7 @@ def test_tiny_config_edges():
 
 
 def test_program_graph_config_edges():
-    g = make_graphs(CONFIGS[1])[0]
+    g = make_graphs(PROGRAM_GRAPH)[0]
     assert g.n == 20000 and g.m == 2 * 19999 * 10
 
 
