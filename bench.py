@@ -14,8 +14,17 @@ skips the graph).
 Prints one JSON line.  `--gpus N` with N > 1 is refused: the path runs on
 one GPU.
 
-The roofline entry times the dominant banded kernel live (HIP events on its
-stream).  Its `traffic` field is the HBM traffic per launch measured with the
+The default workload is the largest single-GPU one: 1,048,576 nodes in 141
+log-normal graphs, B = 256, E = 10, H = 256, T = 8, bf16 (`--workload`
+picks another; the 20k-node program graph is measured after it and reported
+under `config.secondary`).
+
+The roofline entry covers the kernel that takes the most device time in the
+step.  Its launches are timed inside the eager timed steps: the library's
+launch profiler (ggnn_profile_*) brackets every kernel launch of
+ggnn_forward / ggnn_backward with HIP events on the launch's stream, and the
+average over those launches is the duration the fraction uses (the same
+kernel relaunched back to back is reported beside it).  Its `traffic` field is the HBM traffic per launch measured with the
 FETCH_SIZE and WRITE_SIZE counters of two rocprofv3 --pmc runs of this same
 command, each scaled by what the counter reads for a plain copy of known size
 (the calibration copy every run makes after the timed region);
@@ -45,8 +54,10 @@ BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix cores
 FP32_PEAK_TFLOPS = 157.3    # MI355X fp32 matrix cores
 
 
-# C-ABI entry point -> (device kernel name fragments, sources that define it)
+# Roofline key -> (device kernel name fragments, sources that define it)
 KERNELS = {
+    "step_wide_fwd": (("step_wide_kernel", ", false, false>("), ["banded_wide.hip", "device_common.h"]),
+    "step_wide_rev": (("step_wide_kernel", ", true, false>("), ["banded_wide.hip", "device_common.h"]),
     "step_bits_gru": (("step_bits_kernel", ", false, true>("), ["banded_bits.hip", "device_common.h"]),
     "step_bits_gru_bwd": (("step_bits_kernel", ", true, true>("),
                           ["banded_bits.hip", "device_common.h", "gru_wave.h"]),
@@ -56,7 +67,8 @@ KERNELS = {
     "banded_propagate_bwd": (("banded_bwd_kernel",), ["banded.hip", "device_common.h"]),
 }
 # Other kernels of the step, listed in the traffic summary.
-OTHER_KERNELS = [("gru_fwd_kernel",), ("gru_bwd_kernel",), ("gru_wgrad_kernel",), ("transform_bwd_dx_kernel",),
+OTHER_KERNELS = [("gru_fwd_kernel",), ("gru_bwd_kernel",), ("gru_fwd_big_kernel",), ("gru_bwd_big_kernel",),
+                 ("gru_wgrad_kernel",), ("transform_bwd_dx_kernel",),
                  ("transform_wgrad_kernel",), ("transform_wgrad_nm_kernel",), ("transform_fwd_kernel",),
                  ("reduce_partials_kernel",), ("reduce_multi_kernel",)]
 CAL_ELEMS = 64 << 20            # calibration copy: 64 Mi fp32 read, 64 Mi fp32 written
@@ -70,8 +82,14 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=3)
-    p.add_argument("--workload", default="program_graph",
-                   help="program_graph (default), tiny, batch_100k, stress_1m, or sweep_B<block>")
+    p.add_argument("--workload", default="stress_1m",
+                   help="stress_1m (default), program_graph, tiny, batch_100k, or sweep_B<block>")
+    p.add_argument("--secondary", default=None,
+                   help="a second workload measured after the first and reported under config.secondary "
+                        "(default: program_graph after stress_1m, none otherwise; 'none' disables)")
+    p.add_argument("--cpu-nodes", type=int, default=32768,
+                   help="node budget of the CPU oracle sample: whole graphs in draw order up to this many nodes "
+                        "(at least one graph)")
     p.add_argument("--band", choices=["bits", "dense"], default="bits",
                    help="band storage: 1 bit per entry (aggregate-first fused forward) or dense in the compute dtype")
     p.add_argument("--kernel-reps", type=int, default=50, help="launches per kernel for the roofline timing")
@@ -205,10 +223,27 @@ def kernel_costs(fmt, n_pad, B, E, H, es):
         bwd_gru = (agg_flops + tr_flops + gru_flops, band + nh * es + E * H * H * es + E * nh * es + nh * 4 + gru_w
                    + nh * es + 3 * nh * es + nh * es + nh * 4 + 3 * nh * es)
         return {"banded_step_bits": fwd, "banded_step_bits_bwd": bwd, "step_bits_gru": fwd_gru,
-                "step_bits_gru_bwd": bwd_gru}
+                "step_bits_gru_bwd": bwd_gru, "step_wide_fwd": fwd, "step_wide_rev": bwd}
     band = blocks * B * B * es
     return {"banded_propagate": (agg_flops, band + E * H * n_pad * 4 + n_pad * H * 4),
             "banded_propagate_bwd": (agg_flops, band + H * n_pad * es + E * H * n_pad * es)}
+
+
+def node_costs(n_pad, E, H, T, es):
+    """Algorithmic flops and HBM bytes of one launch of the GRU kernels and of
+    the weight-gradient contractions (over all T * n_pad rows)."""
+    nh, K = n_pad * H, T * n_pad
+    gru_w = 6 * H * H * es + 3 * H * 4
+    return {
+        # a (fp32) and h read; h' and the saved gates (r, z, n) written
+        "gru_fwd": (12.0 * nh * H, nh * 4 + nh * es + nh * es + 3 * nh * es + gru_w),
+        # dh_out (fp32), h, saved read; da, dh (fp32), G^ written
+        "gru_rev": (12.0 * nh * H, nh * 4 + nh * es + 3 * nh * es + nh * es + nh * 4 + 3 * nh * es + gru_w),
+        # per row: a (fp32), h, r, G^ read; dWi, dU (fp32) partials written once per split
+        "wgrad_gru": (12.0 * K * H * H, K * (4 * H + es * H + es * H + 3 * es * H)),
+        # per row: X and dM of every type read
+        "wgrad_transform": (2.0 * K * E * H * H, K * (es * H + E * es * H)),
+    }
 
 
 def time_kernel(fn, reps, torch):
@@ -225,17 +260,33 @@ def time_kernel(fn, reps, torch):
     return s.elapsed_time(e) / 1e3 / reps
 
 
-def cpu_baseline(spec, graphs, comp, params):
-    """The fp64 oracle (as it stands) on one full step of the same workload:
-    T forward and T reverse steps over the same graph and parameters."""
+def oracle_sample(spec, graphs, node_budget):
+    """The graphs the CPU baseline runs on: whole graphs in draw order while
+    their node count stays within the budget (at least the first)."""
+    out, total = [], 0
+    for g in graphs:
+        if out and total + g.n > node_budget:
+            break
+        out.append(g)
+        total += g.n
+    return out
+
+
+def cpu_baseline(spec, graphs, params_for, node_budget):
+    """The fp64 oracle (as it stands) on one full step (T forward and T
+    reverse steps) of a sample of the workload's graphs: whole graphs in draw
+    order up to `node_budget` nodes, reordered and batched as the GPU run
+    does, with parameters drawn the same way for that sample.  node-steps/s
+    is the sample's real nodes * T over the oracle's wall time."""
     import oracle as O
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        threads = 1
+        blas = None
+    sample = oracle_sample(spec, graphs, node_budget)
     parts = []
-    for g in graphs:
+    for g in sample:
         if spec.reorder:
             _, rank = O.rcm_order(g.n, g.src, g.dst)
             s, d = O.relabel(rank, g.src, g.dst)
@@ -243,13 +294,18 @@ def cpu_baseline(spec, graphs, comp, params):
             s, d = g.src, g.dst
         parts.append((g.n, s, d, g.etype))
     n_real, n_pad, s, d, e, _ = O.batch_layout(parts, spec.B)
+    params = params_for(n_real, n_pad)
     t0 = time.perf_counter()
     O.propagate(n_pad, spec.B, s, d, e, params.X, params.W, params.Wi, params.U, params.b, spec.T, G=params.G,
                 bias=params.bias)
     dt = time.perf_counter() - t0
-    return {"value": n_real * spec.T / dt, "unit": "node-steps/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"one full step (T={spec.T} forward + T reverse) of the same workload, {n_real} nodes, "
-                      f"{dt:.1f} s"}
+    whole = len(sample) == len(graphs)
+    what = ("the whole workload" if whole else
+            f"{len(sample)} of its {len(graphs)} graphs ({n_real} of {sum(g.n for g in graphs)} nodes, the first "
+            f"in draw order)")
+    return {"value": n_real * spec.T / dt, "unit": "node-steps/s", "cores": len(os.sched_getaffinity(0)),
+            "kind": "oracle", "blas_threads": blas,
+            "sample": f"one full step (T={spec.T} forward + T reverse, fp64) on {what}; {dt:.1f} s"}
 
 
 def time_supernodes(spec, graphs, s, timed, torch):
@@ -335,6 +391,176 @@ def stream_probe(reps=10):
     return out
 
 
+# Launch kinds of the library's profiler -> roofline key, per path.
+def roofline_key(kind, band, wide):
+    if band == "dense":
+        return {"banded_fwd": "banded_propagate", "banded_rev": "banded_propagate_bwd"}.get(kind, kind)
+    if wide:
+        return {"step_fwd": "step_wide_fwd", "step_rev": "step_wide_rev"}.get(kind, kind)
+    return {"step_fwd_gru": "step_bits_gru", "step_rev_gru": "step_bits_gru_bwd", "step_fwd": "banded_step_bits",
+            "step_rev": "banded_step_bits_bwd"}.get(kind, kind)
+
+
+def roofline_entry(key, dur, flops, nbytes, dtype):
+    """Achieved rate of one launch against the roofline it is bound by (the
+    longer of bytes / HBM peak and flops / matrix-core peak)."""
+    mfma_peak = BF16_PEAK_TFLOPS if dtype == "bf16" else FP32_PEAK_TFLOPS
+    hbm_bound = nbytes / (HBM_PEAK_GBS * 1e9) >= flops / (mfma_peak * 1e12)
+    gbs, tfs = nbytes / dur / 1e9, flops / dur / 1e12
+    if hbm_bound:
+        r = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+             "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    else:
+        r = {"bound": "mfma", "achieved": round(tfs, 2), "peak": mfma_peak, "unit": "TFLOP/s",
+             "frac": round(tfs / mfma_peak, 4)}
+    r.update({"kernel": key, "avg_launch_us": round(dur * 1e6, 2), "algorithmic_bytes": int(nbytes),
+              "algorithmic_flops": flops, "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+              "mfma_frac_effective": round(tfs / mfma_peak, 4)})
+    return r
+
+
+def measure(spec, args, torch, with_extras=True):
+    """Build the workload on the GPU, time the step (eager with the launch
+    profiler on, then as a replayed HIP graph) and derive the roofline of the
+    kernel that takes the most device time.  Returns (result dict, graphs)."""
+    from ggnn_synth import make_graphs, draw_params
+    from paper_1906_11786_amd import capi
+    from paper_1906_11786_amd.driver import compile_graphs, BandedGGNN
+
+    t0 = time.perf_counter()
+    graphs = make_graphs(spec)
+    gen_s = time.perf_counter() - t0
+    comp = compile_graphs(graphs, spec.B, spec.E, reorder=spec.reorder)
+    params = draw_params(spec.cfg, comp.n_real, comp.n_pad, spec.H, spec.E, spec.dtype)
+    m = BandedGGNN(comp, spec.H, spec.T, spec.dtype, params, band_format=args.band)
+    del params
+    torch.cuda.synchronize()
+
+    def timed(fn, profile=False):
+        """Seconds per step over args.steps calls after args.warmup, the larger
+        of the host clock and the device events around the timed calls; with
+        `profile`, the launch profiler records every kernel of those calls."""
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        if profile:
+            capi.ggnn_profile_start(args.steps * (5 * spec.T + 8) + 16)
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        start.record()
+        for _ in range(args.steps):
+            fn()
+        end.record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        if profile:
+            capi.ggnn_profile_stop()
+        return max(wall, start.elapsed_time(end) / 1e3) / args.steps
+
+    eager_s = timed(m.step, profile=True)
+    records = [capi.ggnn_profile_read(i) for i in range(capi.ggnn_profile_count())]
+    capi.ggnn_profile_start(0)
+    graph_s = None
+    if not args.eager:
+        # The same step recorded once as a HIP graph and replayed: no host
+        # launch overhead between the kernels.
+        m.capture()
+        graph_s = timed(m.replay)
+    use_graph = graph_s is not None and graph_s < eager_s
+    sec_per_step = graph_s if use_graph else eager_s
+
+    # One whole training step timed the same way (eager launches): the
+    # propagation step above, then the readout and softmax loss over seeded
+    # candidate sets, the readout's reverse, and the Momentum update of every
+    # parameter.  Reported beside the propagation figure, not as `value`.
+    train_s = eval_band_s = eval_sparse_s = None
+    if with_extras and not args.no_train:
+        from ggnn_synth import draw_candidates, draw_readout
+        cands = draw_candidates(spec.cfg, comp.offsets)
+        w_out, b_out = draw_readout(spec.cfg, spec.H)
+        m.setup_training(cands, w_out, b_out, lr=1e-3, momentum=0.9)
+        train_s = timed(m.train_step)
+        # Evaluation of the same parameters: T forward steps and the readout,
+        # on the band, and along every edge through the sparse path.
+        m.setup_sparse(comp.src, comp.dst, comp.etype)
+        eval_band_s = timed(lambda: (m.forward(), m.readout()))
+        eval_sparse_s = timed(m.evaluate_sparse)
+
+    supernodes = None
+    if with_extras and args.supernodes:
+        supernodes = time_supernodes(spec, graphs, args.supernodes, timed, torch)
+
+    # Device time per step of every launch kind, from the eager timed steps.
+    es = 2 if spec.dtype == "bf16" else 4
+    n_pad, B, E, H, T = comp.n_pad, spec.B, spec.E, spec.H, spec.T
+    wide = args.band == "bits" and spec.dtype == "bf16" and H in (128, 256)
+    costs = kernel_costs(args.band, n_pad, B, E, H, es)
+    costs.update(node_costs(n_pad, E, H, T, es))
+    per_kind = {}
+    for kind, ms in records:
+        per_kind.setdefault(kind, []).append(ms)
+    kinds = {}
+    for kind, v in per_kind.items():
+        key = roofline_key(kind, args.band, wide)
+        kinds[key] = {"launches_per_step": round(len(v) / args.steps, 2), "avg_us": round(1e3 * sum(v) / len(v), 2),
+                      "ms_per_step": round(sum(v) / args.steps, 4)}
+    dom = max((k for k in kinds if k in costs), key=lambda k: kinds[k]["ms_per_step"])
+    flops, nbytes = costs[dom]
+    dur = kinds[dom]["avg_us"] * 1e-6
+    roofline = roofline_entry(dom, dur, flops, nbytes, spec.dtype)
+    roofline["timing"] = "in-step: HIP events around each launch of the eager timed steps (launch profiler)"
+    # The same kernel relaunched back to back in the step's launch shape, where
+    # an entry point launches it alone.
+    td = m.X.dtype
+    da_prev, dh_prev = torch.empty_like(m.da), torch.empty_like(m.dh)
+    ghat = torch.empty((n_pad, 3 * H), dtype=td, device="cuda")
+    b2b = {
+        "step_wide_rev": lambda: capi.ggnn_banded_step_bits_bwd(spec.dtype, n_pad, B, H, E, m.band_t, m.da, m.W, m.dh,
+                                                                m.dX, m.dM, T * n_pad),
+        "banded_step_bits_bwd": lambda: capi.ggnn_banded_step_bits_bwd(spec.dtype, n_pad, B, H, E, m.band_t, m.da,
+                                                                       m.W, m.dh, m.dX, m.dM, T * n_pad),
+        "step_bits_gru": lambda: capi.ggnn_step_bits_gru(spec.dtype, n_pad, B, H, E, m.band, m.X[0], m.W, m.Wt,
+                                                         m.bias, m.Wi, m.U, m.b, m.a[0], m.X[1], m.saved[0]),
+        "step_bits_gru_bwd": lambda: capi.ggnn_step_bits_gru_bwd(
+            spec.dtype, n_pad, B, H, E, m.band_t, m.da, m.W, m.dh, m.dM, T * n_pad, m.Wi, m.U, m.X[0], m.saved[0],
+            da_prev, dh_prev, ghat),
+        "banded_propagate": lambda: capi.ggnn_banded_propagate(spec.dtype, n_pad, B, H, E, m.band, m.M, m.a[0]),
+        "banded_propagate_bwd": lambda: capi.ggnn_banded_propagate_bwd(spec.dtype, n_pad, B, H, E, m.band, m.da,
+                                                                       m.dM),
+    }.get(dom)
+    roofline["avg_launch_us_back_to_back"] = (None if b2b is None else
+                                              round(time_kernel(b2b, args.kernel_reps, torch) * 1e6, 2))
+    traffic, traffic_src = recorded_traffic(dom, spec.name, args.band) if dom in KERNELS else (None, None)
+    roofline["traffic"] = traffic
+    roofline["traffic_source"] = traffic_src
+    roofline["launch_kinds"] = kinds
+    del da_prev, dh_prev, ghat
+
+    res = {
+        "value": comp.n_real * T / sec_per_step,
+        "ms_per_step": sec_per_step * 1e3,
+        "config": {"workload": spec.name, "band": args.band, "n_nodes": comp.n_real, "n_pad": comp.n_pad,
+                   "graphs": len(graphs), "B": B, "E": E, "H": H, "T": T,
+                   "bandwidth_after_reordering": comp.bandwidth,
+                   "edges_packed": comp.stats.get("n_packed"), "edges_dropped": comp.stats.get("n_dropped"),
+                   "node_steps_per_s_padded": round(comp.n_pad * T / sec_per_step, 1),
+                   "timing": "hip_graph_replay" if use_graph else "eager",
+                   "ms_per_step_eager": round(eager_s * 1e3, 4),
+                   "ms_per_step_graph": None if graph_s is None else round(graph_s * 1e3, 4),
+                   "ms_per_train_step": None if train_s is None else round(train_s * 1e3, 4),
+                   "ms_eval_band": None if eval_band_s is None else round(eval_band_s * 1e3, 4),
+                   "ms_eval_sparse_all_edges": None if eval_sparse_s is None else round(eval_sparse_s * 1e3, 4),
+                   "supernodes": supernodes,
+                   "host_compile_s": round(comp.rcm_seconds + comp.stats.get("pack_seconds", 0.0), 3),
+                   "generate_s": round(gen_s, 3)},
+        "roofline": roofline,
+    }
+    del m
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res, graphs
+
+
 def main():
     args = parse()
     if args.stream_probe:
@@ -357,112 +583,29 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     import torch
-    from ggnn_synth import make_graphs, draw_params
+    from ggnn_synth import draw_params
     from paper_1906_11786_amd import capi
-    from paper_1906_11786_amd.driver import compile_graphs, BandedGGNN
 
     capi.lib()
     if not torch.cuda.is_available():
         raise SystemExit("no GPU visible")
     spec = spec_for(args.workload)
-    t0 = time.perf_counter()
-    graphs = make_graphs(spec)
-    gen_s = time.perf_counter() - t0
-    comp = compile_graphs(graphs, spec.B, spec.E, reorder=spec.reorder)
-    params = draw_params(spec.cfg, comp.n_real, comp.n_pad, spec.H, spec.E, spec.dtype)
-    m = BandedGGNN(comp, spec.H, spec.T, spec.dtype, params, band_format=args.band)
-    torch.cuda.synchronize()
+    res, graphs = measure(spec, args, torch)
+    print(f"# {spec.name}: {res['ms_per_step']:.3f} ms per step, {res['value'] / 1e6:.2f} M node-steps/s",
+          file=sys.stderr, flush=True)
 
-    def timed(fn):
-        """Seconds per step over args.steps calls after args.warmup, the larger
-        of the host clock and the device events around the timed calls."""
-        for _ in range(args.warmup):
-            fn()
-        torch.cuda.synchronize()
-        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        t0 = time.perf_counter()
-        start.record()
-        for _ in range(args.steps):
-            fn()
-        end.record()
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-        return max(wall, start.elapsed_time(end) / 1e3) / args.steps
-
-    eager_s = timed(m.step)
-    graph_s = None
-    if not args.eager:
-        # The same step recorded once as a HIP graph and replayed: no host
-        # launch overhead between the kernels.
-        m.capture()
-        graph_s = timed(m.replay)
-    use_graph = graph_s is not None and graph_s < eager_s
-    sec_per_step = graph_s if use_graph else eager_s
-    value = comp.n_real * spec.T / sec_per_step
-
-    # One whole training step timed the same way (eager launches): the
-    # propagation step above, then the readout and softmax loss over seeded
-    # candidate sets, the readout's reverse, and the Momentum update of every
-    # parameter.  Reported beside the propagation figure, not as `value`.
-    train_s = eval_band_s = eval_sparse_s = None
-    if not args.no_train:
-        from ggnn_synth import draw_candidates, draw_readout
-        cands = draw_candidates(spec.cfg, comp.offsets)
-        w_out, b_out = draw_readout(spec.cfg, spec.H)
-        m.setup_training(cands, w_out, b_out, lr=1e-3, momentum=0.9)
-        train_s = timed(m.train_step)
-        # Evaluation of the same parameters: T forward steps and the readout,
-        # on the band, and along every edge through the sparse path.
-        m.setup_sparse(comp.src, comp.dst, comp.etype)
-        eval_band_s = timed(lambda: (m.forward(), m.readout()))
-        eval_sparse_s = timed(m.evaluate_sparse)
-
-    supernodes = None
-    if args.supernodes:
-        supernodes = time_supernodes(spec, graphs, args.supernodes, timed, torch)
-
-    # Roofline of the banded kernels: each launch timed with HIP events on the
-    # stream it runs on, in the same launch shape as inside the step.
-    es = 2 if spec.dtype == "bf16" else 4
-    n_pad, B, E, H = comp.n_pad, spec.B, spec.E, spec.H
-    if args.band == "bits":
-        # The two launches a step is made of (ggnn_forward runs the first T
-        # times, ggnn_backward the second for t = T-1..1), with the step's own
-        # buffers: state 0 -> 1 and the reverse of step 1 into step 0.
-        td = m.X.dtype
-        da_prev = torch.empty_like(m.da)
-        dh_prev = torch.empty_like(m.dh)
-        ghat = torch.empty((n_pad, 3 * H), dtype=td, device="cuda")
-        fns = {"step_bits_gru": lambda: capi.ggnn_step_bits_gru(spec.dtype, n_pad, B, H, E, m.band, m.X[0], m.W,
-                                                                m.Wt, m.bias, m.Wi, m.U, m.b, m.a[0], m.X[1],
-                                                                m.saved[0]),
-               "step_bits_gru_bwd": lambda: capi.ggnn_step_bits_gru_bwd(
-                   spec.dtype, n_pad, B, H, E, m.band_t, m.da, m.W, m.dh, m.dM, spec.T * n_pad, m.Wi, m.U,
-                   m.X[0], m.saved[0], da_prev, dh_prev, ghat)}
-    else:
-        fns = {"banded_propagate": lambda: capi.ggnn_banded_propagate(spec.dtype, n_pad, B, H, E, m.band, m.M,
-                                                                      m.a[0]),
-               "banded_propagate_bwd": lambda: capi.ggnn_banded_propagate_bwd(spec.dtype, n_pad, B, H, E, m.band,
-                                                                              m.da, m.dM)}
-    costs = kernel_costs(args.band, n_pad, B, E, H, es)
-    times = {k: time_kernel(f, args.kernel_reps, torch) for k, f in fns.items()}
-    dom = max(times, key=times.get)
-    dur = times[dom]
-    flops, nbytes = costs[dom]
-    mfma_peak = BF16_PEAK_TFLOPS if spec.dtype == "bf16" else FP32_PEAK_TFLOPS
-    hbm_bound = nbytes / (HBM_PEAK_GBS * 1e9) >= flops / (mfma_peak * 1e12)
-    gbs, tfs = nbytes / dur / 1e9, flops / dur / 1e12
-    if hbm_bound:
-        roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(gbs / HBM_PEAK_GBS, 4)}
-    else:
-        roofline = {"bound": "mfma", "achieved": round(tfs, 2), "peak": mfma_peak, "unit": "TFLOP/s",
-                    "frac": round(tfs / mfma_peak, 4)}
-    traffic, traffic_src = recorded_traffic(dom, spec.name, args.band)
-    roofline.update({"traffic": traffic, "traffic_source": traffic_src, "kernel": dom, "avg_launch_us": round(dur * 1e6, 2),
-                     "algorithmic_bytes": int(nbytes), "algorithmic_flops": flops,
-                     "hbm_frac": round(gbs / HBM_PEAK_GBS, 4), "mfma_frac": round(tfs / mfma_peak, 4),
-                     "other_kernels_us": {k: round(v * 1e6, 2) for k, v in times.items() if k != dom}})
+    secondary = args.secondary
+    if secondary is None:
+        secondary = "program_graph" if args.workload == "stress_1m" else "none"
+    sec = None
+    if secondary != "none":
+        s_res, _ = measure(spec_for(secondary), args, torch, with_extras=False)
+        r = s_res["roofline"]
+        sec = {"workload": s_res["config"]["workload"], "value": round(s_res["value"], 1),
+               "unit": "node-steps/s", "ms_per_step": round(s_res["ms_per_step"], 4),
+               "timing": s_res["config"]["timing"],
+               "roofline": {k: r[k] for k in ("bound", "achieved", "peak", "unit", "frac", "kernel", "avg_launch_us",
+                                              "avg_launch_us_back_to_back", "traffic", "traffic_source")}}
 
     # Calibration copy for the traffic counters (outside every timed region).
     cal_src = torch.ones(CAL_ELEMS, dtype=torch.float32, device="cuda")
@@ -473,35 +616,26 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(spec, graphs, comp, params)
+        cpu = cpu_baseline(spec, graphs, lambda n_real, n_pad: draw_params(spec.cfg, n_real, n_pad, spec.H, spec.E,
+                                                                           spec.dtype), args.cpu_nodes)
 
+    config = res["config"]
+    config["secondary"] = sec
     line = {
         "metric": "GGNN propagation node-steps/sec (fwd+bwd) at 1 GPU; % bf16 MFMA peak",
-        "value": round(value, 1),
+        "value": round(res["value"], 1),
         "unit": "node-steps/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(sec_per_step * 1e3, 4),
+        "ms_per_step": round(res["ms_per_step"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": spec.dtype,
         "data": "synthetic",
-        "config": {"workload": spec.name, "band": args.band, "n_nodes": comp.n_real, "n_pad": comp.n_pad, "graphs": len(graphs),
-                   "B": B, "E": E, "H": H, "T": spec.T, "bandwidth_after_reordering": comp.bandwidth,
-                   "edges_packed": comp.stats.get("n_packed"), "edges_dropped": comp.stats.get("n_dropped"),
-                   "node_steps_per_s_padded": round(comp.n_pad * spec.T / sec_per_step, 1),
-                   "timing": "hip_graph_replay" if use_graph else "eager",
-                   "ms_per_step_eager": round(eager_s * 1e3, 4),
-                   "ms_per_step_graph": None if graph_s is None else round(graph_s * 1e3, 4),
-                   "ms_per_train_step": None if train_s is None else round(train_s * 1e3, 4),
-                   "ms_eval_band": None if eval_band_s is None else round(eval_band_s * 1e3, 4),
-                   "ms_eval_sparse_all_edges": None if eval_sparse_s is None else round(eval_sparse_s * 1e3, 4),
-                   "supernodes": supernodes,
-                   "host_compile_s": round(comp.rcm_seconds + comp.stats.get("pack_seconds", 0.0), 3),
-                   "generate_s": round(gen_s, 3)},
-        "roofline": roofline,
+        "config": config,
+        "roofline": res["roofline"],
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

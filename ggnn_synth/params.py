@@ -16,14 +16,24 @@ from .graphs import rng_for, STREAM_X, STREAM_W, STREAM_GRU, STREAM_G
 
 
 def round_bf16(x: np.ndarray) -> np.ndarray:
-    """Round to the nearest bf16 value (ties to even); returns float64."""
+    """Round to the nearest bf16 value (ties to even); returns float64.
+
+    Works on the float32 bit patterns in chunks (32-bit integer arithmetic:
+    add 0x7FFF plus the lowest kept bit, clear the low half); NaNs stay NaN."""
     f = np.ascontiguousarray(x, dtype=np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    nan = np.isnan(f)
-    lsb = (u >> 16) & 1
-    r = ((u + 0x7FFF + lsb) >> 16) << 16
-    out = r.astype(np.uint32).view(np.float32).astype(np.float64)
-    out[nan] = np.nan
+    out = np.empty(f.shape, dtype=np.float64)
+    fu, o = f.reshape(-1).view(np.uint32), out.reshape(-1)
+    step = 1 << 22
+    with np.errstate(invalid="ignore"):
+        for s in range(0, fu.size, step):
+            u = fu[s:s + step].copy()
+            nan = (u & np.uint32(0x7FFFFFFF)) > np.uint32(0x7F800000)
+            u += np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+            u &= np.uint32(0xFFFF0000)
+            r = u.view(np.float32).astype(np.float64)
+            if nan.any():
+                r[nan] = np.nan
+            o[s:s + step] = r
     return out
 
 

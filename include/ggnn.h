@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define GGNN_ABI_VERSION 8
+#define GGNN_ABI_VERSION 9
 
 typedef enum {
   GGNN_OK = 0,
@@ -387,6 +387,35 @@ ggnn_status ggnn_forward(const ggnn_model* model, const ggnn_activations* act, v
  * Needs the activations of a preceding ggnn_forward. */
 ggnn_status ggnn_backward(const ggnn_model* model, const ggnn_activations* act,
                           const ggnn_grads* grads, void* stream);
+
+/* ---- Launch profiler (device time of every kernel of a real pass) --------
+ *
+ * While enabled, ggnn_forward and ggnn_backward bracket each kernel launch
+ * they enqueue with two HIP events on the launch's stream and tag the pair
+ * with the launch kind (ggnn_profile_name: "step_fwd", "step_fwd_gru",
+ * "gru_fwd", "transform_fwd", "banded_fwd", "gru_rev", "step_rev",
+ * "step_rev_gru", "banded_rev", "transform_rev_dx", "wgrad_gru",
+ * "wgrad_transform", "reduce"; the "_gru" forms are band steps with the GRU
+ * or GRU reverse fused into the same kernel).  Launches made while the stream
+ * is being captured into a HIP graph, and launches beyond `capacity`, are not
+ * recorded.  The state is process-wide and meant for one driving host thread;
+ * the events are host-side objects (no device memory is allocated).
+ *
+ * ggnn_profile_start(capacity): releases earlier records, creates `capacity`
+ *   event pairs and enables recording (capacity 0: release and disable).
+ *   Errors: capacity outside [0, 2^20] -> INVALID_ARG; event creation
+ *   failure -> DEVICE.
+ * ggnn_profile_stop(): disables recording; the records stay readable.
+ * ggnn_profile_count(): records taken since the last start.
+ * ggnn_profile_read(i, &id, &ms): waits for record i's stop event and returns
+ *   its launch kind and elapsed device time in milliseconds.  Errors: i out
+ *   of range or NULL outputs -> INVALID_ARG; HIP error -> DEVICE.
+ * ggnn_profile_name(id): name of a launch kind ("" when out of range). */
+ggnn_status ggnn_profile_start(int32_t capacity);
+ggnn_status ggnn_profile_stop(void);
+int32_t ggnn_profile_count(void);
+ggnn_status ggnn_profile_read(int32_t i, int32_t* id, float* ms);
+const char* ggnn_profile_name(int32_t id);
 
 /* ---- Closing one training step: readout, loss, parameter update ----------
  *

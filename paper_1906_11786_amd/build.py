@@ -29,7 +29,7 @@ DT_FLAGS = {"bf16": ["-DGGNN_DT_BF16=1", "-mllvm", "-amdgpu-mfma-vgpr-form"], "f
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall"]
 
 # (source, language, dtype build or None)
-SOURCES = [("host.cpp", "c++", None), ("capi_device.cpp", "hip", None)] + [
+SOURCES = [("host.cpp", "c++", None), ("capi_device.cpp", "hip", None), ("profile.cpp", "hip", None)] + [
     (src, "hip", dt) for src in ("banded.hip", "banded_bits.hip", "banded_wide.hip", "transform.hip", "gru.hip", "readout.hip", "sparse.hip", "supernode.hip") for dt in ("bf16", "f32")]
 
 

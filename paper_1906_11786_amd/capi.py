@@ -40,6 +40,7 @@ EXPORTS = [
     "ggnn_sparse_csr", "ggnn_sparse_step",
     "ggnn_super_bytes", "ggnn_super_pack", "ggnn_super_workspace_bytes", "ggnn_super_propagate",
     "ggnn_super_propagate_bwd",
+    "ggnn_profile_start", "ggnn_profile_stop", "ggnn_profile_count", "ggnn_profile_read", "ggnn_profile_name",
 ]
 
 
@@ -115,6 +116,11 @@ _SIGS = {
     "ggnn_super_propagate": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
     "ggnn_super_propagate_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                            vp]),
+    "ggnn_profile_start": (C.c_int, [i32]),
+    "ggnn_profile_stop": (C.c_int, []),
+    "ggnn_profile_count": (i32, []),
+    "ggnn_profile_read": (C.c_int, [i32, vp, vp]),
+    "ggnn_profile_name": (C.c_char_p, [i32]),
 }
 
 
@@ -169,7 +175,7 @@ def _i32(a) -> np.ndarray:
 
 # Interface version this binding is written against (GGNN_ABI_VERSION of
 # include/ggnn.h); the library must report the same number.
-ABI_VERSION = 8
+ABI_VERSION = 9
 
 
 def ggnn_abi_version() -> int:
@@ -430,3 +436,28 @@ def ggnn_super_propagate_bwd(dt, n_pad, H, E, s, rows, rows_t, cols_t, X, W, da,
     _check("ggnn_super_propagate_bwd", lib().ggnn_super_propagate_bwd(
         _dt(dt), n_pad, H, E, s, _ptr(rows), _ptr(rows_t), _ptr(cols_t), _ptr(X), _ptr(W), _ptr(da), _ptr(dX),
         _ptr(dW), _ptr(dbias), _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+# ------------------------------------------------------------ launch profiler
+
+def ggnn_profile_start(capacity: int):
+    _check("ggnn_profile_start", lib().ggnn_profile_start(capacity))
+
+
+def ggnn_profile_stop():
+    _check("ggnn_profile_stop", lib().ggnn_profile_stop())
+
+
+def ggnn_profile_count() -> int:
+    return int(lib().ggnn_profile_count())
+
+
+def ggnn_profile_read(i: int):
+    """Returns (launch kind name, milliseconds) of record i."""
+    kid, ms = C.c_int32(0), C.c_float(0.0)
+    _check("ggnn_profile_read", lib().ggnn_profile_read(i, C.addressof(kid), C.addressof(ms)))
+    return lib().ggnn_profile_name(kid.value).decode(), float(ms.value)
+
+
+def ggnn_profile_name(kind: int) -> str:
+    return lib().ggnn_profile_name(kind).decode()

@@ -7,6 +7,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "profile.h"
 
 using namespace ggnn;
 
@@ -389,14 +390,25 @@ ggnn_status ggnn_forward(const ggnn_model* m, const ggnn_activations* act, void*
     hipError_t err;
     bool fused = false;   // the bit-band step also ran the GRU update
     if (m->band_format == GGNN_BAND_BITS) {
+      prof_begin(s);
       err = launch_step_fwd_bits_gru(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, Xt, m->W, m->Wt, m->bias, at,
                                      m->Wi, m->U, m->b, Xn, sv, &fused, s);
+      prof_end(s, fused ? PROF_STEP_FWD_GRU : PROF_STEP_FWD);
     } else {
+      prof_begin(s);
       err = launch_transform_fwd(m->dtype, m->n_pad, m->H, m->E, Xt, m->W, m->bias, act->M, s);
-      if (err == hipSuccess) err = launch_banded_fwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, act->M, at, s);
+      prof_end(s, PROF_TRANSFORM_FWD);
+      if (err == hipSuccess) {
+        prof_begin(s);
+        err = launch_banded_fwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, act->M, at, s);
+        prof_end(s, PROF_BANDED_FWD);
+      }
     }
-    if (err == hipSuccess && !fused)
+    if (err == hipSuccess && !fused) {
+      prof_begin(s);
       err = launch_gru_fwd(m->dtype, m->n_pad, m->H, at, Xt, m->Wi, m->U, m->b, Xn, sv, s, gru_pk);
+      prof_end(s, PROF_GRU_FWD);
+    }
     if (err != hipSuccess) return device_status(err, "forward");
   }
   return GGNN_OK;
@@ -444,22 +456,31 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
     void* da_b[2] = {gr->da, ws + L.da2};
     float* dh_b[2] = {gr->dh, reinterpret_cast<float*>(ws + L.dh2)};
     int cur = 0;
+    prof_begin(s);
     hipError_t err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xs(m->T - 1), Ss(m->T - 1), m->Wi, m->U,
                                           da_b[0], dh_b[0], Gs(m->T - 1), s, gru_pk);
+    prof_end(s, PROF_GRU_REV);
     if (err != hipSuccess) return device_status(err, "backward");
     for (int t = m->T - 1; t >= 0; --t) {
       char* dMr = static_cast<char*>(gr->dM) + (size_t)t * m->n_pad * m->H * es;   // node-major rows of step t
       if (t > 0) {
         bool fused = false;
+        prof_begin(s);
         err = launch_step_bwd_bits_gru(m->dtype, m->n_pad, m->B, m->H, m->E, m->band_t, da_b[cur], m->W, dh_b[cur],
                                        gr->dX, dMr, K, m->Wi, m->U, Xs(t - 1), Ss(t - 1), da_b[1 - cur],
                                        dh_b[1 - cur], Gs(t - 1), &fused, s);
-        if (err == hipSuccess && !fused)
+        prof_end(s, fused ? PROF_STEP_REV_GRU : PROF_STEP_REV);
+        if (err == hipSuccess && !fused) {
+          prof_begin(s);
           err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xs(t - 1), Ss(t - 1), m->Wi, m->U,
                                      da_b[1 - cur], dh_b[1 - cur], Gs(t - 1), s, gru_pk);
+          prof_end(s, PROF_GRU_REV);
+        }
       } else {
+        prof_begin(s);
         err = launch_step_bwd_bits(m->dtype, m->n_pad, m->B, m->H, m->E, m->band_t, da_b[cur], m->W, dh_b[cur],
                                    gr->dX, dMr, K, s);
+        prof_end(s, PROF_STEP_REV);
       }
       if (err != hipSuccess) return device_status(err, "backward");
       cur ^= 1;
@@ -467,25 +488,43 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
   } else {
     for (int t = m->T - 1; t >= 0; --t) {
       char* dMt = static_cast<char*>(gr->dM) + (size_t)t * m->n_pad * es;   // feature-major columns of step t
+      prof_begin(s);
       hipError_t err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xs(t), Ss(t), m->Wi, m->U, gr->da,
                                             gr->dh, Gs(t), s, gru_pk);
-      if (err == hipSuccess) err = launch_banded_bwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, gr->da, dMt, K, s);
-      if (err == hipSuccess)
+      prof_end(s, PROF_GRU_REV);
+      if (err == hipSuccess) {
+        prof_begin(s);
+        err = launch_banded_bwd(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, gr->da, dMt, K, s);
+        prof_end(s, PROF_BANDED_REV);
+      }
+      if (err == hipSuccess) {
+        prof_begin(s);
         err = launch_transform_bwd_dx(m->dtype, m->n_pad, m->H, m->E, m->W, dMt, K, gr->dh, gr->dX, s);
+        prof_end(s, PROF_TRANSFORM_REV_DX);
+      }
       if (err != hipSuccess) return device_status(err, "backward");
     }
   }
   // The weight-gradient contractions leave per-split partials; their
   // fixed-order reductions then run as one launch.
   ReduceList red;
+  prof_begin(s);
   hipError_t err = launch_gru_wgrad(m->dtype, K, m->H, act->a, act->X, act->saved, ghat, gr->dWi, gr->dU, gr->db,
                                     ws + L.gru_part, s, &red);
-  if (err == hipSuccess)
+  prof_end(s, PROF_WGRAD_GRU);
+  if (err == hipSuccess) {
+    prof_begin(s);
     err = m->band_format == GGNN_BAND_BITS
               ? launch_transform_wgrad_nm(m->dtype, K, m->H, m->E, act->X, gr->dM, K, gr->dW, dbias, ws + L.tr_part, s,
                                           &red)
               : launch_transform_wgrad(m->dtype, K, m->H, m->E, act->X, gr->dM, K, gr->dW, dbias, ws + L.tr_part, s);
-  if (err == hipSuccess) err = launch_reduce_multi(red, s);
+    prof_end(s, PROF_WGRAD_TRANSFORM);
+  }
+  if (err == hipSuccess) {
+    prof_begin(s);
+    err = launch_reduce_multi(red, s);
+    prof_end(s, PROF_REDUCE);
+  }
   return device_status(err, "backward");
 }
 
