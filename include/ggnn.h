@@ -235,8 +235,9 @@ ggnn_status ggnn_banded_step_bits_bwd(ggnn_dtype dt, int32_t n_pad, int32_t B, i
  * those two calls:
  *   a      [n_pad][H] float (written: the aggregate, kept for the reverse pass)
  *   h_out  [n_pad][H] dt (written: the next state);  saved [n_pad][3H] dt (r | z | n)
- * Wi, U [H][3H] dt; b [3H] float.  X and h_out must not overlap.  Wt: W_e^T (ggnn_transpose_weights)
- * or NULL; the result does not depend on it. */
+ * Wi, U [H][3H] dt; b [3H] float.  X and h_out must not share a byte (INVALID_ARG otherwise: workgroups
+ * read the neighbour rows of X that others' rows of h_out would overwrite).  Wt: W_e^T
+ * (ggnn_transpose_weights) or NULL; the result does not depend on it. */
 ggnn_status ggnn_step_bits_gru(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E,
                                const void* bits, const void* X, const void* W, const void* Wt,
                                const float* bias, const void* Wi, const void* U, const float* b, float* a,

@@ -49,6 +49,12 @@ ggnn_status check_banded(int32_t dt, int32_t n_pad, int32_t B, int32_t H, int32_
 
 inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
+// Whether the byte ranges [p, p + pb) and [q, q + qb) share no byte.
+bool disjoint(const void* p, size_t pb, const void* q, size_t qb) {
+  const char *a = static_cast<const char*>(p), *c = static_cast<const char*>(q);
+  return a + pb <= c || c + qb <= a;
+}
+
 }  // namespace
 
 // Reverse-pass workspace: the gate gradients G^ of every step ([T][n_pad][3H],
@@ -234,10 +240,6 @@ ggnn_status ggnn_gru_pack_weights(ggnn_dtype dt, int32_t H, const void* Wi, cons
   CHECK_PTR(U, "U");
   CHECK_PTR(packed, "packed");
   const size_t wb = (size_t)H * 3 * H * dtype_bytes(dt);
-  auto disjoint = [](const void* p, size_t pb, const void* q, size_t qb) {
-    const char *a = static_cast<const char*>(p), *c = static_cast<const char*>(q);
-    return a + pb <= c || c + qb <= a;
-  };
   GGNN_CHECK_ARG(disjoint(packed, bytes, Wi, wb) && disjoint(packed, bytes, U, wb),
                  "packed must not overlap Wi or U");
   return device_status(launch_gru_pack(dt, H, Wi, U, packed, as_stream(stream)), "gru_pack_weights");
@@ -259,6 +261,10 @@ ggnn_status ggnn_step_bits_gru(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t 
   CHECK_PTR(a, "a");
   CHECK_PTR(h_out, "h_out");
   CHECK_PTR(saved, "saved");
+  // Workgroups read neighbour-block rows of X that other workgroups' rows of
+  // h_out would overwrite: the two must not share bytes.
+  const size_t xb = (size_t)n_pad * H * dtype_bytes(dt);
+  GGNN_CHECK_ARG(disjoint(X, xb, h_out, xb), "X and h_out must not overlap");
   hipStream_t s = as_stream(stream);
   bool fused = false;
   CHECK_OPT_PTR(Wt, "Wt");

@@ -70,6 +70,27 @@ def dropped_edges(graphs: Sequence, B: int, E: int, reorder: bool = True) -> dic
             "dropped": dropped, "duplicates": dup, "dropped_fraction": dropped / total if total else 0.0}
 
 
+def check_candidates(cands, n_pad: int) -> None:
+    """The readout's reverse (ggnn_readout_loss_bwd) writes each candidate's
+    row of dL/dX_T once, so a node may be a candidate of at most one list
+    entry; ids must lie in [0, n_pad), lists must be well formed and each
+    target inside its graph's list.  Raises ValueError otherwise."""
+    node = np.asarray(cands.node, np.int64)
+    ptr = np.asarray(cands.ptr, np.int64)
+    tgt = np.asarray(cands.target, np.int64)
+    if ptr.ndim != 1 or len(ptr) < 2 or ptr[0] != 0 or np.any(np.diff(ptr) < 0) or ptr[-1] != len(node):
+        raise ValueError("candidate list offsets must start at 0, not decrease and end at the candidate count")
+    if len(tgt) != len(ptr) - 1:
+        raise ValueError("one target per graph is required")
+    if len(node) and (node.min() < 0 or node.max() >= n_pad):
+        raise ValueError(f"candidate node ids must lie in [0, {n_pad})")
+    k = np.diff(ptr)
+    if np.any((k > 0) & ((tgt < 0) | (tgt >= np.maximum(k, 1)))):
+        raise ValueError("a target lies outside its graph's candidate list")
+    if len(np.unique(node)) != len(node):
+        raise ValueError("a node appears more than once among the candidates")
+
+
 def torch_dtype(dt: str):
     import torch
     return torch.bfloat16 if dt == "bf16" else torch.float32
@@ -235,6 +256,7 @@ class BandedGGNN:
         reads in bf16, and zero velocities."""
         torch = self.torch
         dev = self.device
+        check_candidates(cands, self.comp.n_pad)
         self.cand_node = torch.from_numpy(np.ascontiguousarray(cands.node, np.int32)).to(dev)
         self.cand_ptr = torch.from_numpy(np.ascontiguousarray(cands.ptr, np.int32)).to(dev)
         self.target = torch.from_numpy(np.ascontiguousarray(cands.target, np.int32)).to(dev)

@@ -217,6 +217,43 @@ def test_gru_pack_sizes_and_validation_before_touching_the_gpu():
     assert ei.value.status_name == "GGNN_ERR_INVALID_ARG"
 
 
+def test_step_bits_gru_rejects_overlapping_state_buffers():
+    """The fused forward step reads neighbour rows of X while writing h_out:
+    any shared byte is rejected on the host (nothing is launched)."""
+    _need_lib()
+    n_pad, B, H, E = 256, 64, 64, 2
+    xb = n_pad * H * 2
+    X = 1 << 24
+    P = 1 << 28   # 16-byte aligned stand-in addresses for the other operands
+    for h_out in (X, X + xb - 16, X - xb + 16):
+        with pytest.raises(capi.GGNNError) as ei:
+            capi.ggnn_step_bits_gru("bf16", n_pad, B, H, E, P, X, P, None, None, P, P, P, P, h_out, P, stream=0)
+        assert ei.value.status_name == "GGNN_ERR_INVALID_ARG", h_out
+        assert "overlap" in capi.ggnn_last_error()
+
+
+def test_candidate_lists_are_checked_on_the_host():
+    """The readout's reverse writes each candidate's dX row once: repeated
+    nodes, ids outside the supergraph, malformed offsets and targets outside
+    a list are refused before anything reaches the device."""
+    from ggnn_synth.readout import Candidates, draw_candidates
+    from paper_1906_11786_amd.driver import check_candidates
+    good = draw_candidates(1, np.array([0, 50, 120, 121, 400]))
+    check_candidates(good, 512)
+    i32 = lambda *v: np.array(v, np.int32)
+    bad = [
+        Candidates(i32(3, 7, 3), i32(0, 3), i32(0)),            # node 3 twice in one graph
+        Candidates(i32(3, 7, 9, 7), i32(0, 2, 4), i32(0, 1)),   # node 7 in two graphs
+        Candidates(i32(3, 600), i32(0, 2), i32(0)),             # id beyond n_pad
+        Candidates(i32(3, 4), i32(0, 3), i32(0)),               # offsets do not end at the count
+        Candidates(i32(3, 4), i32(0, 2), i32(2)),               # target outside the list
+        Candidates(i32(3, 4), i32(0, 2), i32(0, 0)),            # one target per graph
+    ]
+    for c in bad:
+        with pytest.raises(ValueError):
+            check_candidates(c, 512)
+
+
 def _unpack_bits(bits):
     return np.unpackbits(bits, axis=-1, bitorder="little").astype(np.float64)
 
