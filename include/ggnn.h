@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define GGNN_ABI_VERSION 9
+#define GGNN_ABI_VERSION 10
 
 typedef enum {
   GGNN_OK = 0,
@@ -457,6 +457,29 @@ ggnn_status ggnn_readout_loss_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int32
                                   const float* w_out, const int32_t* cand_node, const float* dlogit, float* dX,
                                   float* dw_out, float* db_out, void* workspace, size_t workspace_bytes,
                                   void* stream);
+
+/* Bytes of the device array ggnn_readout_loss_bwd_noalloc keeps its partial
+ * sums in (one per device, held until the process ends). */
+#define GGNN_NOALLOC_SCRATCH_BYTES (4u << 20)
+
+/* ggnn_readout_loss_bwd without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight
+ * training or serving loops, harnesses that forbid hipMalloc): the per-block
+ * partial sums go to a scratch array of GGNN_NOALLOC_SCRATCH_BYTES that the
+ * library holds on each device.  Same arguments, results and determinism as
+ * ggnn_readout_loss_bwd (bitwise equal outputs); the call allocates nothing.
+ * Every partial is written before it is read, so no state carries over
+ * between calls, but all calls on one device share the array: calls that
+ * overlap on a device (concurrent streams or threads) race and must be
+ * serialised by the caller.  The first call on a device looks up the array's
+ * address there (host side; the stream's device is used).
+ * Errors: as ggnn_readout_loss_bwd; partial sums larger than the scratch
+ * (ggnn_readout_loss_bwd_workspace_bytes(H, n_cand) >
+ * GGNN_NOALLOC_SCRATCH_BYTES: above 261,120 candidates at H = 256, 1,032,384
+ * at H = 64) -> GGNN_ERR_UNSUPPORTED, checked before anything is enqueued. */
+ggnn_status ggnn_readout_loss_bwd_noalloc(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t n_cand, const void* X,
+                                          const float* w_out, const int32_t* cand_node, const float* dlogit,
+                                          float* dX, float* dw_out, float* db_out, void* stream);
 
 /* One Momentum-optimizer step (Appendix, "Optimization": Momentum, with
  * Nesterov momentum and L2 weight decay as options) on count float32 master

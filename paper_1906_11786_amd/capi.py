@@ -41,6 +41,7 @@ EXPORTS = [
     "ggnn_super_bytes", "ggnn_super_pack", "ggnn_super_workspace_bytes", "ggnn_super_propagate",
     "ggnn_super_propagate_bwd",
     "ggnn_profile_start", "ggnn_profile_stop", "ggnn_profile_count", "ggnn_profile_read", "ggnn_profile_name",
+    "ggnn_readout_loss_bwd_noalloc",
 ]
 
 
@@ -121,6 +122,7 @@ _SIGS = {
     "ggnn_profile_count": (i32, []),
     "ggnn_profile_read": (C.c_int, [i32, vp, vp]),
     "ggnn_profile_name": (C.c_char_p, [i32]),
+    "ggnn_readout_loss_bwd_noalloc": (C.c_int, [C.c_int, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
 }
 
 
@@ -175,7 +177,7 @@ def _i32(a) -> np.ndarray:
 
 # Interface version this binding is written against (GGNN_ABI_VERSION of
 # include/ggnn.h); the library must report the same number.
-ABI_VERSION = 9
+ABI_VERSION = 10
 
 
 def ggnn_abi_version() -> int:
@@ -369,6 +371,17 @@ def ggnn_readout_loss_bwd(dt, n_pad, H, n_cand, X, w_out, cand_node, dlogit, dX,
     _check("ggnn_readout_loss_bwd", lib().ggnn_readout_loss_bwd(
         _dt(dt), n_pad, H, n_cand, _ptr(X), _ptr(w_out), _ptr(cand_node), _ptr(dlogit), _ptr(dX), _ptr(dw_out),
         _ptr(db_out), _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+# Bytes of the library's per-device scratch array (GGNN_NOALLOC_SCRATCH_BYTES).
+NOALLOC_SCRATCH_BYTES = 4 << 20
+
+
+def ggnn_readout_loss_bwd_noalloc(dt, n_pad, H, n_cand, X, w_out, cand_node, dlogit, dX, dw_out, db_out,
+                                  stream=None):
+    _check("ggnn_readout_loss_bwd_noalloc", lib().ggnn_readout_loss_bwd_noalloc(
+        _dt(dt), n_pad, H, n_cand, _ptr(X), _ptr(w_out), _ptr(cand_node), _ptr(dlogit), _ptr(dX), _ptr(dw_out),
+        _ptr(db_out), _stream(stream)))
 
 
 def ggnn_sgd_momentum(count, param, velocity, grad, lr, momentum, weight_decay=0.0, nesterov=False,

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <mutex>
 
 #include "common.h"
 #include "kernels.h"
@@ -564,11 +565,12 @@ size_t ggnn_readout_loss_bwd_workspace_bytes(int32_t H, int32_t n_cand) {
   return readout_bwd_workspace(H, n_cand);
 }
 
-ggnn_status ggnn_readout_loss_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t n_cand, const void* X,
-                                  const float* w_out, const int32_t* cand_node, const float* dlogit, float* dX,
-                                  float* dw_out, float* db_out, void* workspace, size_t workspace_bytes,
-                                  void* stream) {
-  clear_error();
+}  // extern "C"
+
+namespace {
+ggnn_status check_readout_bwd(int32_t dt, int32_t n_pad, int32_t H, int32_t n_cand, const void* X,
+                              const float* w_out, const int32_t* cand_node, const float* dlogit, float* dX,
+                              float* dw_out, float* db_out) {
   ggnn_status st = check_common(dt, n_pad, H);
   if (st != GGNN_OK) return st;
   GGNN_CHECK_ARG(n_cand >= 0, "n_cand=%d must not be negative", n_cand);
@@ -581,6 +583,19 @@ ggnn_status ggnn_readout_loss_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int32
     CHECK_PTR(cand_node, "cand_node");
     CHECK_PTR(dlogit, "dlogit");
   }
+  return GGNN_OK;
+}
+}  // namespace
+
+extern "C" {
+
+ggnn_status ggnn_readout_loss_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t n_cand, const void* X,
+                                  const float* w_out, const int32_t* cand_node, const float* dlogit, float* dX,
+                                  float* dw_out, float* db_out, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+  clear_error();
+  ggnn_status st = check_readout_bwd(dt, n_pad, H, n_cand, X, w_out, cand_node, dlogit, dX, dw_out, db_out);
+  if (st != GGNN_OK) return st;
   const size_t need = readout_bwd_workspace(H, n_cand);
   if (workspace == nullptr || workspace_bytes < need || !aligned16(workspace))
     return fail(GGNN_ERR_WORKSPACE, "readout_loss_bwd needs a 16-byte aligned workspace of %zu bytes (got %zu)",
@@ -697,6 +712,70 @@ ggnn_status ggnn_super_propagate_bwd(ggnn_dtype dt, int32_t n_pad, int32_t H, in
   return device_status(launch_super_bwd(dt, n_pad, H, E, s, rows, rows_t, cols_t, X, W, da, dX, dW, dbias, workspace,
                                         as_stream(stream)),
                        "super_propagate_bwd");
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Allocation-free readout reverse.  Its per-block partial sums live in a
+// file-scope device array that the library holds on every device it runs on
+// (until the process ends) instead of a caller workspace.  In host code the
+// array's name is only a stand-in: its device address on each device is
+// looked up once, with that device current, and kept.
+// ---------------------------------------------------------------------------
+static constexpr size_t kNoAllocScratchBytes = (size_t)GGNN_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) float scratch[kNoAllocScratchBytes / sizeof(float)];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the device that runs `stream`.
+ggnn_status scratch_address(hipStream_t stream, void** out) {
+  int dev = -1;
+  hipError_t e = hipStreamGetDevice(stream, &dev);
+  if (e != hipSuccess) return fail(GGNN_ERR_DEVICE, "device of the stream: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(GGNN_ERR_UNSUPPORTED, "device %d beyond the %d supported", dev,
+                                                 kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    int cur = -1;
+    e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != dev) e = hipSetDevice(dev);
+    void* p = nullptr;
+    if (e == hipSuccess) e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur >= 0 && cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || p == nullptr)
+      return fail(GGNN_ERR_DEVICE, "address of the scratch array on device %d: %s", dev,
+                  e != hipSuccess ? hipGetErrorString(e) : "null");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return GGNN_OK;
+}
+}  // namespace
+
+extern "C" {
+
+ggnn_status ggnn_readout_loss_bwd_noalloc(ggnn_dtype dt, int32_t n_pad, int32_t H, int32_t n_cand, const void* X,
+                                          const float* w_out, const int32_t* cand_node, const float* dlogit,
+                                          float* dX, float* dw_out, float* db_out, void* stream) {
+  clear_error();
+  ggnn_status st = check_readout_bwd(dt, n_pad, H, n_cand, X, w_out, cand_node, dlogit, dX, dw_out, db_out);
+  if (st != GGNN_OK) return st;
+  const size_t need = readout_bwd_workspace(H, n_cand);
+  if (need > kNoAllocScratchBytes)
+    return fail(GGNN_ERR_UNSUPPORTED,
+                "readout_loss_bwd_noalloc: %d candidates at H=%d need %zu bytes of partial sums, more than the "
+                "library's %zu-byte scratch; use ggnn_readout_loss_bwd with a workspace",
+                n_cand, H, need, kNoAllocScratchBytes);
+  void* part = nullptr;
+  st = scratch_address(as_stream(stream), &part);
+  if (st != GGNN_OK) return st;
+  return device_status(launch_readout_bwd(dt, n_pad, H, n_cand, X, w_out, cand_node, dlogit, dX, dw_out, db_out,
+                                          part, as_stream(stream)),
+                       "readout_loss_bwd_noalloc");
 }
 
 }  // extern "C"
