@@ -62,7 +62,16 @@ struct WideCfg {
   static constexpr int R = WAVES * RPW;         // rows per workgroup
   static constexpr int NT = WAVES * kWave;
   static constexpr int RB = B / 32;             // bit-row bytes per lane and block
-  static constexpr int GROW = B / 4;            // block columns per lane group
+  static constexpr int GROW = B / 4;            // block columns per lane group (split k order)
+  // k order of a block's B columns over the RB matrix-core k steps:
+  //   contiguous (B = 128, 256): step kk covers columns 32 kk .. 32 kk + 31,
+  //     lane group g the eight columns 32 kk + 8 g + {0..7};
+  //   split (other B): lane group g covers columns g GROW .. g GROW + GROW - 1,
+  //     step kk the eight columns g GROW + 8 kk + {0..7}.
+  // The contiguous order keeps a step's columns together, so the steps whose
+  // columns hold no edge into a wave's rows (most of them in a band much
+  // narrower than B) are skipped whole.
+  static constexpr bool KCONT = (RB == 4 || RB == 8);
   static constexpr int XS = B * HQ;             // elements per staged block slice
   static constexpr int WS = (H / 16) * kWave * 8;   // elements per weight unit
   static constexpr int NXB = (2 * 3 * XS + NWB * WS) * 2 <= 160 * 1024 ? 2 : 1;   // block-slice buffers
@@ -79,13 +88,31 @@ __device__ __forceinline__ int wide_slot(int f) {
   const int w = f % 32;
   return 32 * (f / 32) + 16 * ((w % 8) / 4) + 4 * (w / 8) + w % 4;
 }
-// Swizzle of the 16-column groups of forward node row c (block-local).
-template <int HQ, int GROW>
+// Lane group and k step of block column c (a multiple of 8 for the step).
+template <bool KCONT, int GROW>
+__device__ __forceinline__ int wide_colgroup(int c) {
+  return KCONT ? (c >> 3) & 3 : c / GROW;
+}
+template <bool KCONT, int GROW>
+__device__ __forceinline__ int wide_colstep(int c) {
+  return KCONT ? c >> 5 : (c % GROW) / 8;
+}
+// First block column of lane group g at k step kk.
+template <bool KCONT, int GROW>
+__device__ __forceinline__ int wide_col0(int g, int kk) {
+  return KCONT ? 32 * kk + 8 * g : g * GROW + 8 * kk;
+}
+// Swizzle of the 16-column groups of forward node row c (block-local): the
+// lane group's parity (and, at HQ = 64, bit 1 of the row), so that the rows
+// two lane groups read in one pass, and the four rows one read touches,
+// fall on disjoint banks.
+template <int HQ, bool KCONT, int GROW>
 __device__ __forceinline__ int wide_sw(int c) {
+  const int gp = wide_colgroup<KCONT, GROW>(c) & 1;
   if constexpr (HQ == 64) {
-    return ((c >> 1) & 1) | (((c / GROW) & 1) << 1);
+    return ((c >> 1) & 1) | (gp << 1);
   } else {
-    return (c / GROW) & 1;
+    return gp;
   }
 }
 
@@ -139,6 +166,38 @@ template <int NB> struct WideBits {
     for (int i = 0; i < NW; ++i) w[i] = 0u;
   }
   __device__ __forceinline__ uint32_t byte(int i) const { return (w[i / 4] >> (8 * (i % 4))) & 0xFFu; }
+  // From the split byte order (lane group g holds row bytes NB g .. NB g +
+  // NB - 1, as loaded) to the contiguous one (byte kk = row byte 4 kk + g):
+  // a 4 x 4 transpose between the lane groups (rows of 16 lanes) of a wave,
+  // done with one permlane32 and one permlane16 swap and byte permutes.
+  // `odd` is g & 1.
+  __device__ __forceinline__ void to_contiguous(uint32_t odd) {
+    if constexpr (NB == 8) {
+      // lane g' holds k steps 2g' (w[0]) and 2g'+1 (w[1]), byte d = group d.
+      // Pair the two steps per destination group: L for groups 0, 1, U for 2, 3.
+      uint32_t L = __builtin_amdgcn_perm(w[1], w[0], 0x05010400u);
+      uint32_t U = __builtin_amdgcn_perm(w[1], w[0], 0x07030602u);
+      // lanes 0-31 keep L and take L of lanes 32-63; lanes 32-63 keep U.
+      auto r32 = __builtin_amdgcn_permlane32_swap(L, U, false, false);
+      L = r32[0];
+      U = r32[1];
+      uint32_t X0 = __builtin_amdgcn_perm(U, L, 0x05040100u);   // pairs for the even group of the half
+      uint32_t X1 = __builtin_amdgcn_perm(U, L, 0x07060302u);   // pairs for the odd group
+      auto r16 = __builtin_amdgcn_permlane16_swap(X0, X1, false, false);
+      X0 = r16[0];   // pairs of source lane groups 0 and 2
+      X1 = r16[1];   // pairs of source lane groups 1 and 3
+      w[0] = __builtin_amdgcn_perm(X1, X0, 0x05040100u);      // steps 0..3
+      w[1] = __builtin_amdgcn_perm(X1, X0, 0x07060302u);      // steps 4..7
+    } else if constexpr (NB == 4) {
+      // lane g' holds k step g' (byte d = group d).
+      const uint32_t D = w[0];
+      const uint32_t Yr = __builtin_amdgcn_perm(D, D, 0x01000302u);   // halves rotated
+      auto r32 = __builtin_amdgcn_permlane32_swap(D, Yr, false, false);
+      const uint32_t Z = __builtin_amdgcn_perm(r32[1], r32[0], 0x05040100u);
+      auto r16 = __builtin_amdgcn_permlane16_swap(Z, Z, false, false);
+      w[0] = __builtin_amdgcn_perm(r16[1], r16[0], odd ? 0x07030501u : 0x06020400u);
+    }
+  }
   __device__ __forceinline__ int popc() const {
     int c = 0;
 #pragma unroll
@@ -203,7 +262,7 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
     bf16s* d = xb + s * XS;
     if constexpr (!REV) {
       const int c = r / (HQ / 8), G = r % (HQ / 8);
-      const int sw = wide_sw<HQ, GROW>(c);
+      const int sw = wide_sw<HQ, C::KCONT, GROW>(c);
       const int m0 = 2 * (G / 4), w0 = 4 * (G % 4);   // tiles m0, m0 + 1 of the 32-group G / 4
       bf16s* row = d + c * HQ;
       *reinterpret_cast<u32x2*>(row + 16 * (m0 ^ sw) + w0) = u32x2{v[0], v[1]};         // features 8G .. 8G+3
@@ -211,7 +270,7 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
     } else {
       const int f = 16 * (r / (16 * (B / 8))) + r % 16, c = 8 * ((r / 16) % (B / 8));
       // fragment (kk, tile) of the block: lane group c / (B/4), k step (c % (B/4)) / 8
-      const int slot = wide_slot(f), gg = c / GROW, kk = (c % GROW) / 8;
+      const int slot = wide_slot(f), gg = wide_colgroup<C::KCONT, GROW>(c), kk = wide_colstep<C::KCONT, GROW>(c);
       *reinterpret_cast<u32x4*>(d + fo<bf16s>(kk * MQ + slot / 16, slot % 16 + 16 * gg, 0)) = v;
     }
   };
@@ -246,8 +305,21 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
     }
   };
 
+  // Bit rows in the contiguous k order (see WideCfg::KCONT).
+  const uint32_t godd = static_cast<uint32_t>(g & 1);
+  auto reorder_bits = [&](WideBits<RB> (&b)[3][NTW]) __attribute__((always_inline)) {
+    if constexpr (C::KCONT) {
+#pragma unroll
+      for (int s = 0; s < 3; ++s)
+        if (s >= s_lo && s <= s_hi)
+#pragma unroll
+          for (int n = 0; n < NTW; ++n) b[s][n].to_contiguous(godd);
+    }
+  };
+
   // ---- prologue: slice 0, type 0 ----------------------------------------
   load_bits(0, cur);
+  reorder_bits(cur);
 #pragma unroll
   for (int h2 = 0; h2 < NH; ++h2)
     for (int u = tid; u < H * 4; u += NT) w_store(u, ws[h2], w_load(u, 0, 0, h2));
@@ -262,7 +334,7 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
 
   // Forward tiles: lane (p, g) reads rows 8kk + p/4 (+4) of its group's
   // region; its swizzle is the same for every k step and both reads.
-  const int swl = wide_sw<HQ, GROW>(g * GROW + q / 4);
+  const int swl = wide_sw<HQ, C::KCONT, GROW>(wide_col0<C::KCONT, GROW>(g, 0) + q / 4);
   int qs = 0, e = 0;     // slice and edge type of iteration it
   int wcur = 0;          // ring buffer of this iteration's first weight unit
   for (int it = 0; it < iters; ++it) {
@@ -280,10 +352,11 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
       if (s < s_lo || s > s_hi) continue;
-      // Forward: a neighbour block with no edge of this type into the
-      // wave's rows adds exact zeros, so its expansion and products are
-      // skipped (one wave-uniform test per block).
-      if constexpr (!REV) {
+      // A block, or (contiguous k order) a k step, with no edge of this type
+      // into the wave's rows adds exact zeros: its expansion and products are
+      // skipped (wave-uniform tests; the split order tests whole blocks, in
+      // the forward only).
+      if constexpr (C::KCONT || !REV) {
         uint32_t any_bits = 0;
 #pragma unroll
         for (int n = 0; n < NTW; ++n)
@@ -294,6 +367,12 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
       const bf16s* xsb = xb + s * XS;
 #pragma unroll
       for (int kk = 0; kk < RB; ++kk) {
+        if constexpr (C::KCONT) {
+          uint32_t any_step = 0;
+#pragma unroll
+          for (int n = 0; n < NTW; ++n) any_step |= cur[s][n].byte(kk);
+          if (!wide_any(any_step)) continue;
+        }
         bf16x8 bf[NTW];
 #pragma unroll
         for (int n = 0; n < NTW; ++n) bf[n] = wide_bits_frag(cur[s][n].byte(kk));
@@ -301,7 +380,7 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
         for (int m = 0; m < MQ; ++m) {
           bf16x8 af;
           if constexpr (!REV) {
-            af = tr_read8(xsb + (g * GROW + 8 * kk + q / 4) * HQ + 16 * (m ^ swl) + 4 * (q % 4), HQ);
+            af = tr_read8(xsb + (wide_col0<C::KCONT, GROW>(g, kk) + q / 4) * HQ + 16 * (m ^ swl) + 4 * (q % 4), HQ);
           } else {
             af = load_fragi<bf16s>(xsb, kk * MQ + m, lane);
           }
@@ -426,6 +505,7 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
       for (int s = 0; s < 3; ++s)
 #pragma unroll
         for (int n = 0; n < NTW; ++n) cur[s][n] = nxt[s][n];
+      reorder_bits(cur);
     }
     qs = qn;
     e = en;
