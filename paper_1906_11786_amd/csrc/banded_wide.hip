@@ -44,15 +44,22 @@
 namespace ggnn {
 namespace dev {
 
-template <int H, int B, bool REV>
+#ifndef GGNN_WIDE_FWD_HQ64
+#define GGNN_WIDE_FWD_HQ64 1
+#endif
+template <int H, int B, bool REV, bool BIAS = false>
 struct WideCfg {
   // Features per slice: 64 where the three blocks' slice and the weight ring
   // fit in LDS and the workgroup fills a compute unit anyway (B >= 256),
-  // except the H = 256 forward (its hi + lo transform already gives each
-  // staged byte more products; measured slower at 64); else 32 (at B = 128
-  // two workgroups then share a compute unit).
+  // except the forward with a message bias at H = 256 (its registers spill
+  // at 64); else 32 (at B = 128 two workgroups then share a compute unit).
+  // With empty k steps skipped, fewer, wider slices halve the per-slice
+  // fixed work (bit loads and re-ordering, skip tests, barriers): the
+  // H = 256 forward on the 1M-node workload went 4.26 -> 3.54 ms at 64.
   static constexpr int HQ =
-      (B >= 256 && (REV || H <= 128) && (3 * B * 64 + 3 * H * 32) * 2 <= 160 * 1024) ? 64 : 32;
+      (B >= 256 && (REV || H <= 128 || (GGNN_WIDE_FWD_HQ64 && !BIAS)) && (3 * B * 64 + 3 * H * 32) * 2 <= 160 * 1024)
+          ? 64
+          : 32;
   static constexpr int NQ = H / HQ;             // slices
   static constexpr int NH = HQ / 32;            // 32-feature weight units per slice
   static constexpr int MQ = HQ / 16;            // aggregation tiles per slice
@@ -215,7 +222,7 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
     const uint8_t* __restrict__ bits, const bf16s* __restrict__ V, const bf16s* __restrict__ Wsrc,
     const float* __restrict__ bias, float* __restrict__ out, int n_pad, int E, const float* __restrict__ dX_in,
     bf16s* __restrict__ dM, long ldm) {
-  using C = WideCfg<H, B, REV>;
+  using C = WideCfg<H, B, REV, BIAS>;
   constexpr int NT = C::NT, HQ = C::HQ, NQ = C::NQ, NH = C::NH, MQ = C::MQ, NWB = C::NWB;
   constexpr int NTW = C::NTW, RB = C::RB, XS = C::XS, GROW = C::GROW;
   constexpr int MT = H / 16;             // 16-feature output tiles
@@ -291,7 +298,19 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
 
   // ---- bit rows ---------------------------------------------------------
   WideBits<RB> cur[3][NTW], nxt[3][NTW];
+  // Byte offset of the lane's part of row 16n + q of block s within one edge
+  // type's band (below 2^32: nb * 3 * B * B / 8 bytes per type), and that
+  // type's first byte (wave-uniform), so that each load is a uniform base
+  // plus a loop-invariant lane offset.
+  uint32_t boff[3][NTW];
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+#pragma unroll
+    for (int n = 0; n < NTW; ++n)
+      boff[s][n] = (uint32_t)(((k * 3 + s) * B + rw + 16 * n + q) * ROWB + g * RB);
+  const size_t type_bytes = (size_t)nb * 3 * B * ROWB;
   auto load_bits = [&](int e, WideBits<RB> (&dst)[3][NTW]) __attribute__((always_inline)) {
+    const uint8_t* tb = bits + (size_t)e * type_bytes;
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
 #pragma unroll
@@ -299,7 +318,7 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
         if (s < s_lo || s > s_hi) {
           dst[s][n].zero();
         } else {
-          dst[s][n].load(bits + ((((size_t)e * nb + k) * 3 + s) * B + rw + 16 * n + q) * ROWB + g * RB);
+          dst[s][n].load(tb + boff[s][n]);
         }
       }
     }
@@ -307,13 +326,21 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
 
   // Bit rows in the contiguous k order (see WideCfg::KCONT).
   const uint32_t godd = static_cast<uint32_t>(g & 1);
+  // Blocks with no edge into the wave's rows stay all zero and are skipped.
   auto reorder_bits = [&](WideBits<RB> (&b)[3][NTW]) __attribute__((always_inline)) {
     if constexpr (C::KCONT) {
 #pragma unroll
-      for (int s = 0; s < 3; ++s)
-        if (s >= s_lo && s <= s_hi)
+      for (int s = 0; s < 3; ++s) {
+        if (s < s_lo || s > s_hi) continue;
+        uint32_t any_bits = 0;
 #pragma unroll
-          for (int n = 0; n < NTW; ++n) b[s][n].to_contiguous(godd);
+        for (int n = 0; n < NTW; ++n)
+#pragma unroll
+          for (int i = 0; i < WideBits<RB>::NW; ++i) any_bits |= b[s][n].w[i];
+        if (!wide_any(any_bits)) continue;
+#pragma unroll
+        for (int n = 0; n < NTW; ++n) b[s][n].to_contiguous(godd);
+      }
     }
   };
 
@@ -341,6 +368,8 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
     const bf16s* xb = xs[C::NXB == 2 ? (qs & 1) : 0];
     const bool more = it + 1 < iters;
     const int en = e + 1 < E ? e + 1 : 0, qn = e + 1 < E ? qs : qs + 1;
+    // The next type's bit rows (HBM reads), in flight over this iteration.
+    if (more) load_bits(en, nxt);
 
     // Aggregate of this wave's rows over the slice: P[n][m] = D[feature
     // slot 16m + 4g + j][row 16n + q].
@@ -419,8 +448,8 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
 
 #pragma unroll
     for (int h2 = 0; h2 < NH; ++h2) {
-      // The next slice's weight unit h2 (and, with the last unit, the next
-      // type's bit rows), in flight during this unit's products.
+      // The next slice's weight unit h2, in flight during this unit's
+      // products.
       u32x4 wreg[C::WPT];
       if (more) {
 #pragma unroll
@@ -428,7 +457,6 @@ __global__ __launch_bounds__((WideCfg<H, B, REV>::NT)) void step_wide_kernel(
           const int u = i * NT + tid;
           if ((H * 4) % NT == 0 || u < H * 4) wreg[i] = w_load(u, qn, en, h2);
         }
-        if (h2 == NH - 1) load_bits(en, nxt);
       }
       // The lane's eight consecutive features 32 h2 + 8g .. + 7 of the slice,
       // row 16n + q.
