@@ -99,8 +99,9 @@ ggnn_status ggnn_rcm_order(int32_t n, int64_t m, const int32_t* src, const int32
 
 /* Bandwidth of an edge list (Background: the smallest b with a_ij = 0 for
  * |i - j| > b) under an optional relabelling rank[v] (nullable: identity).
- *   n          number of nodes; src, dst [m] ids in [0, n); rank [n] or NULL
- *   bandwidth  out (0 for m == 0) */
+ *   n          number of nodes; src, dst [m] ids in [0, n); rank [n] with values in [0, n), or NULL
+ *   bandwidth  out (0 for m == 0)
+ * Errors: ids or rank values out of range, NULL pointers -> INVALID_ARG. */
 ggnn_status ggnn_bandwidth(int32_t n, int64_t m, const int32_t* src, const int32_t* dst,
                            const int32_t* rank, int32_t* bandwidth);
 

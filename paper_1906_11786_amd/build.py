@@ -63,6 +63,32 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# Host compilation code (reordering, packing, CSR, supernode slices) built on
+# its own with the address and undefined-behaviour sanitizers, for the CPU
+# tests that run its index arithmetic under them.  g++ only, no device code.
+SAN_CXX = os.environ.get("CXX_SAN", "g++")
+SAN_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+             "-fno-sanitize-recover=undefined", "-shared", "-fPIC", "-std=c++17", "-Wall"]
+SAN_LIB = os.path.join(BUILD, "libggnn_host_san.so")
+
+
+def build_host_sanitized() -> str:
+    """Compile csrc/host.cpp into _build/libggnn_host_san.so (rebuilt when the
+    source or its headers are newer); returns the library path."""
+    os.makedirs(BUILD, exist_ok=True)
+    deps = [os.path.join(CSRC, f) for f in ("host.cpp", "common.h")] + [
+        os.path.join(HERE, "..", "include", "ggnn.h")]
+    if os.path.exists(SAN_LIB) and os.path.getmtime(SAN_LIB) >= max(os.path.getmtime(d) for d in deps):
+        return SAN_LIB
+    tmp = SAN_LIB + ".tmp"
+    cmd = [SAN_CXX, *SAN_FLAGS, os.path.join(CSRC, "host.cpp"), "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"sanitized host build failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, SAN_LIB)
+    return SAN_LIB
+
+
 if __name__ == "__main__":
     build(verbose=True)
     sys.exit(0)

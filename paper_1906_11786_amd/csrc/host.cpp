@@ -130,6 +130,9 @@ ggnn_status ggnn_bandwidth(int32_t n, int64_t m, const int32_t* src, const int32
   GGNN_CHECK_ARG(n >= 0 && m >= 0, "n=%d m=%lld must be >= 0", n, (long long)m);
   GGNN_CHECK_ARG(bandwidth != nullptr, "bandwidth is NULL");
   GGNN_CHECK_ARG(m == 0 || (src && dst), "src/dst is NULL");
+  if (rank != nullptr)
+    for (int32_t v = 0; v < n; ++v)
+      GGNN_CHECK_ARG(rank[v] >= 0 && rank[v] < n, "rank[%d]=%d out of range [0,%d)", v, rank[v], n);
   int32_t bw = 0;
   for (int64_t k = 0; k < m; ++k) {
     int32_t s = src[k], d = dst[k];
