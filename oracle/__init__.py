@@ -10,6 +10,6 @@ from .ggnn_oracle import (  # noqa: F401
     bandwidth, dedupe_edges, covered_mask, kept_edges, kept_edges_super, rcm_order, relabel,
     pack_band, unpack_band, banded_apply,
     msg_transform, aggregate, aggregate_transpose, msg_transform_backward,
-    gru_forward, gru_backward, propagate, batch_layout,
+    gru_forward, gru_gate_gradients, gru_backward, propagate, batch_layout,
     readout_logits, readout_loss, readout_backward, momentum_update, train_step, evaluate,
 )

@@ -303,20 +303,27 @@ def gru_forward(a, h, Wi, U, b):
     return z * h + (1.0 - z) * nn, r, z, nn
 
 
+def gru_gate_gradients(g, h, r, z, nn, U):
+    """Gradients of the three gate pre-activations of gru_forward (the sums
+    inside sigma, sigma and tanh, bias included) for the upstream gradient g
+    of h': the [n, 3H] matrix [r^, z^, n^] that the reverse pass multiplies
+    by Wi^T and U^T and that the weight gradients contract with a and h."""
+    H = h.shape[1]
+    gn = g * (1.0 - z) * (1.0 - nn * nn)  # d/d(pre-activation of n)
+    gz = g * (h - nn) * z * (1.0 - z)     # d/d(pre-activation of z)
+    q = gn @ U[:, 2 * H:].T               # d/d(r * h)
+    gr = q * h * r * (1.0 - r)            # d/d(pre-activation of r)
+    return np.concatenate([gr, gz, gn], axis=1)
+
+
 def gru_backward(g, a, h, r, z, nn, Wi, U):
     """Reverse-mode derivative of gru_forward for the upstream gradient g of
     h'.  Returns (da, dh, dWi, dU, db)."""
     H = h.shape[1]
-    dn = g * (1.0 - z)
-    dz = g * (h - nn)
-    dh = g * z
-    gn = dn * (1.0 - nn * nn)             # d/d(pre-activation of n)
-    gz = dz * z * (1.0 - z)               # d/d(pre-activation of z)
+    ghat = gru_gate_gradients(g, h, r, z, nn, U)
+    gr, gz, gn = ghat[:, :H], ghat[:, H:2 * H], ghat[:, 2 * H:]
     q = gn @ U[:, 2 * H:].T               # d/d(r * h)
-    dr = q * h
-    dh = dh + q * r
-    gr = dr * r * (1.0 - r)               # d/d(pre-activation of r)
-    ghat = np.concatenate([gr, gz, gn], axis=1)
+    dh = g * z + q * r
     da = ghat @ Wi.T
     dh = dh + gr @ U[:, :H].T + gz @ U[:, H:2 * H].T
     dWi = a.T @ ghat

@@ -16,6 +16,27 @@ def relerr(got, want) -> float:
     return float(np.max(np.abs(got - want)) / scale)
 
 
+def elemerr(got, want) -> float:
+    """Elementwise relative error max |got - want| / (|want| + 1e-3 max|want|):
+    the worst element against its own size, floored at a thousandth of the
+    tensor's largest magnitude (reported next to the normwise figure)."""
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    scale = np.max(np.abs(want)) if want.size else 0.0
+    if scale == 0:
+        return float(np.max(np.abs(got))) if got.size else 0.0
+    return float(np.max(np.abs(got - want) / (np.abs(want) + 1e-3 * scale)))
+
+
+# (test, tensor, normwise, elementwise) of every whole-path comparison in this
+# session, printed as a table at the end of the run (tests/conftest.py).
+PARITY_LOG = []
+
+
+def record(test: str, tensor: str, normwise: float, elementwise: float):
+    PARITY_LOG.append((test, tensor, normwise, elementwise))
+
+
 def say(*a):
     """Print and flush, so a GPU run that dies still names its case."""
     print(*a, flush=True)

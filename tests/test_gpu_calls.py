@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import oracle as O
-from gpu_helpers import TOL, relerr, say, dev, host, round_to, torch_dt
+from gpu_helpers import elemerr, TOL, relerr, say, dev, host, round_to, torch_dt
 
 pytestmark = pytest.mark.gpu
 
@@ -467,6 +467,14 @@ def test_step_bits_gru_bwd(dt, B, H, E, nb):
     gh = host(ghat)
     assert relerr(gh.sum(axis=0), wdb) <= TOL[dt]
     assert relerr(a_prev.T @ gh, wdWi) <= TOL[dt]
+    # the gate gradients themselves, element by element against the oracle's
+    # (stored in the compute dtype: bf16 rounding of each element, 2^-8
+    # relative, on top of the dX and dM roundings upstream of them)
+    want_gh = O.gru_gate_gradients(dX_in + g, h_prev, r, z, nn, U)
+    assert relerr(gh, want_gh) <= TOL[dt]
+    ew = elemerr(gh, want_gh)
+    say(f"  G^ normwise {relerr(gh, want_gh):.2e} elementwise {ew:.2e}")
+    assert ew <= (1e-4 if dt == "f32" else 5e-2), ew
 
 
 def test_device_errors_are_reported():

@@ -5,12 +5,14 @@ tails.  Large batches are checked on sampled graphs: graphs in a supergraph
 do not interact, so the oracle runs on a few of them alone, and a second
 reverse pass with the upstream gradient restricted to those graphs gives
 weight gradients comparable with the oracle's."""
+import os
+
 import numpy as np
 import pytest
 
 import oracle as O
 from ggnn_synth import BATCH_100K, PROGRAM_GRAPH, STRESS_1M, TINY, make_graphs, sweep_blocks, draw_params, backbone_graph, scramble_graph, Graph
-from gpu_helpers import TOL, relerr, say
+from gpu_helpers import TOL, relerr, elemerr, record, say
 
 pytestmark = pytest.mark.gpu
 
@@ -45,12 +47,15 @@ def _compare(res, out, dt, keys=("XT", "dX0", "dW", "dWi", "dU", "db"), rows=Non
     if "dbias" in res:
         want["dbias"] = out["dbias"]
         keys = tuple(keys) + ("dbias",)
-    errs = {}
+    errs, elem = {}, {}
+    test = os.environ.get("PYTEST_CURRENT_TEST", "?").split(" ")[0]
     for k in keys:
         g = res[k] if rows is None or k not in ("XT", "dX0") else res[k][rows]
         w = want[k]
         errs[k] = relerr(g, w)
-    say("  errors:", {k: f"{v:.2e}" for k, v in errs.items()})
+        elem[k] = elemerr(g, w)
+        record(test, k, errs[k], elem[k])
+    say("  errors (normwise / elementwise):", {k: f"{errs[k]:.2e} / {elem[k]:.2e}" for k in errs})
     for k, v in errs.items():
         assert v <= TOL[dt], (k, v)
     return errs
@@ -171,6 +176,7 @@ def _sampled_batch(spec, picks):
     torch.cuda.synchronize()
     masked = m.results()
     acc = {}
+    test = os.environ.get("PYTEST_CURRENT_TEST", "?").split(" ")[0]
     for gi in picks:
         g = graphs[gi]
         o = slice(int(comp.offsets[gi]), int(comp.offsets[gi + 1]))
@@ -184,22 +190,31 @@ def _sampled_batch(spec, picks):
         rows = slice(o.start, o.stop)
         e1 = relerr(full["XT"][rows], out["X"][-1])
         e2 = relerr(full["dX0"][rows], out["dX0"])
-        say(f"  graph {gi} n={g.n}: XT {e1:.2e} dX0 {e2:.2e}")
+        x1, x2 = elemerr(full["XT"][rows], out["X"][-1]), elemerr(full["dX0"][rows], out["dX0"])
+        record(test, f"XT[graph {gi}]", e1, x1)
+        record(test, f"dX0[graph {gi}]", e2, x2)
+        say(f"  graph {gi} n={g.n}: XT {e1:.2e} / {x1:.2e}, dX0 {e2:.2e} / {x2:.2e} (normwise / elementwise)")
         assert e1 <= TOL[spec.dtype] and e2 <= TOL[spec.dtype]
         for k in ("dW", "dWi", "dU", "db"):
             acc[k] = acc.get(k, 0) + out[k]
     for k in ("dW", "dWi", "dU", "db"):
-        e = relerr(masked[k], acc[k])
-        say(f"  {k} (sampled graphs) {e:.2e}")
+        e, x = relerr(masked[k], acc[k]), elemerr(masked[k], acc[k])
+        record(test, f"{k} (sampled graphs)", e, x)
+        say(f"  {k} (sampled graphs) {e:.2e} / {x:.2e}")
         assert e <= TOL[spec.dtype], k
 
 
-def test_batch_100k_workload_sampled():
-    _sampled_batch(BATCH_100K, picks=[0, 7, 19])
+def test_batch_100k_workload_every_graph():
+    """All 34 graphs of the 100k-node batch, each against the oracle run on
+    it alone, and the weight gradients against the sum over all of them."""
+    _sampled_batch(BATCH_100K, picks=list(range(34)))
 
 
 def test_stress_1m_workload_sampled():
-    _sampled_batch(STRESS_1M, picks=[0, 70, 139])
+    """Eight of the 141 graphs of the 1M-node batch: the first two, the last
+    two (148 and 372 nodes), and four between them, one of the largest size
+    (20,000 nodes)."""
+    _sampled_batch(STRESS_1M, picks=[0, 1, 20, 50, 70, 100, 139, 140])
 
 
 def _no_edges(n):

@@ -378,6 +378,34 @@ def test_gradients_match_central_finite_differences(seed):
             assert abs(fd - gr.reshape(-1)[f]) <= 1e-6 * max(1.0, abs(fd)), (name, f)
 
 
+def test_gru_gate_gradients_are_derivatives_in_the_gate_biases():
+    """The gate gradients [r^, z^, n^] are dL/d(pre-activation): giving every
+    node its own copy of the gate bias (b as an [n, 3H] matrix) makes row i
+    of the bias gradient exactly row i of them; central differences of
+    L = sum(g * h') in each such per-node bias entry must agree."""
+    rng = np.random.default_rng(31)
+    n, H = 6, 3
+    a = rng.standard_normal((n, H)); h = rng.standard_normal((n, H))
+    Wi = rng.standard_normal((H, 3 * H)) * 0.5; U = rng.standard_normal((H, 3 * H)) * 0.5
+    b = rng.standard_normal((n, 3 * H)) * 0.3
+    g = rng.standard_normal((n, H))
+    _, r, z, nn = O.gru_forward(a, h, Wi, U, b)
+    ghat = O.gru_gate_gradients(g, h, r, z, nn, U)
+    assert ghat.shape == (n, 3 * H)
+    eps = 1e-6
+    for i in range(n):
+        for c in range(3 * H):
+            bp, bm = b.copy(), b.copy()
+            bp[i, c] += eps
+            bm[i, c] -= eps
+            fd = (np.sum(g * O.gru_forward(a, h, Wi, U, bp)[0]) - np.sum(g * O.gru_forward(a, h, Wi, U, bm)[0])) / (2 * eps)
+            assert abs(fd - ghat[i, c]) <= 1e-7 * max(1.0, abs(fd)), (i, c, fd, ghat[i, c])
+    # and the reverse pass built on them: db is their column sum, dWi = a^T ghat
+    _, _, dWi, _, db = O.gru_backward(g, a, h, r, z, nn, Wi, U)
+    np.testing.assert_allclose(db, ghat.sum(axis=0), atol=1e-13)
+    np.testing.assert_allclose(dWi, a.T @ ghat, atol=1e-13)
+
+
 def test_gradients_match_torch_autograd():
     torch = pytest.importorskip("torch")
     c = _small_case(5, n=32, B=8, E=3, H=5, m=200, T=3)
