@@ -444,7 +444,7 @@ def measure(spec, args, torch, with_extras=True):
             fn()
         torch.cuda.synchronize()
         if profile:
-            capi.ggnn_profile_start(args.steps * (5 * spec.T + 8) + 16)
+            capi.ggnn_profile_start(args.steps * (6 * spec.T + 8) + 16)
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t0 = time.perf_counter()
         start.record()

@@ -487,7 +487,12 @@ __global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restric
   // (three gates) and the r, z part of a U block, both in fragment order
   // (index gate * KS + kk within the block).
   constexpr int BLK_W = 3 * KS * 64 * 8, BLK_U = 2 * KS * 64 * 8;   // elements
-  __shared__ __attribute__((aligned(16))) S lw[2][BLK_W + BLK_U];
+  // Pass 1 reads all of U_n (MTL blocks) from one staging, without barriers
+  // between blocks; pass 2's two block buffers then reuse the same LDS.
+  constexpr int P1E = MTL * KS * 64 * 8;                               // elements of U_n's blocks
+  constexpr int LDSE = P1E > 2 * (BLK_W + BLK_U) ? P1E : 2 * (BLK_W + BLK_U);
+  __shared__ __attribute__((aligned(16))) S lds_all[LDSE];
+  S (*lw)[BLK_W + BLK_U] = reinterpret_cast<S (*)[BLK_W + BLK_U]>(lds_all);
 
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int q = lane % 16, g = lane / 16;
@@ -522,6 +527,31 @@ __global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restric
     }
   };
 
+  // Pass 1's weights (all blocks of U_n, gate n), staged in rounds of R2
+  // units per thread; the first round's loads are in flight during phase 1.
+  constexpr int P1U = MTL * U1;
+  constexpr int P1R = (P1U + R2 * NT - 1) / (R2 * NT);
+  auto load_p1 = [&](int round) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < R2; ++u) {
+      const int lin = (round * R2 + u) * NT + tid;
+      if (lin < P1U) {
+        if constexpr (PK)
+          rr[u] = *reinterpret_cast<const u32x4*>(pk + ((size_t)GruPack<H>::rev_stage(1, 0) + lin) * 8);
+        else
+          rr[u] = gru_rev_unit<S, H>(Wi, U, 1, lin / U1, lin % U1);
+      }
+    }
+  };
+  auto store_p1 = [&](int round) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < R2; ++u) {
+      const int lin = (round * R2 + u) * NT + tid;
+      if (lin < P1U) *reinterpret_cast<u32x4*>(&lds_all[lin * 8]) = rr[u];
+    }
+  };
+  load_p1(0);
+
   // Phase 1 (elementwise, registers): n^, z^ as operand fragments, the
   // g' z term of dh, and G^'s z, n columns.
   frag_t<S> gf[3][KS];
@@ -553,20 +583,23 @@ __global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restric
     }
   }
 
+#pragma unroll
+  for (int round = 0; round < P1R; ++round) {
+    store_p1(round);
+    if (round + 1 < P1R) load_p1(round + 1);
+  }
+  __syncthreads();
+  // Pass 2's first block, in flight during pass 1.
+  load_blk(2, 0);
+
   // Pass 1: blocks m = 0 .. MTL-1 of U_n (unrolled: static register indices).
-  load_blk(1, 0);
   float rv[8];
 #pragma unroll
   for (int m = 0; m < MTL; ++m) {
-    const int b = m & 1;
-    store_blk(1, b);
-    __syncthreads();
-    if (m + 1 < MTL) load_blk(1, m + 1);
-    else load_blk(2, 0);
     if (valid) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) mma(acc, load_fragi<S>(lw[b], kk, lane), gf[2][kk]);
+      for (int kk = 0; kk < KS; ++kk) mma(acc, load_fragi<S>(lds_all + m * U1 * 8, kk, lane), gf[2][kk]);
       const int f = 16 * m + 4 * g;
       const f32x4 r4 = load4f(sv + f), h4 = load4f(h + (size_t)node * H + f);
       float rloc[4];
@@ -581,10 +614,12 @@ __global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restric
       if (m % 2 == 1) gf[0][m / 2] = pack8<S>(rv);
     }
   }
+  // Every wave is done with U_n before pass 2's buffers overwrite it.
+  __syncthreads();
   // Pass 2: blocks n = 0 .. MTL-1 of Wi (da) and U_r, U_z (dh).
 #pragma unroll
   for (int n = 0; n < MTL; ++n) {
-    const int b = (MTL + n) & 1;
+    const int b = n & 1;
     store_blk(2, b);
     __syncthreads();
     if (n + 1 < MTL) load_blk(2, n + 1);
