@@ -25,12 +25,16 @@ HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17", "-Wall", "-W
 # and spends a VALU move per element on every round trip).  The fp32 build
 # keeps the default assignment: its large-H forms do not compile in VGPR-only
 # mode with this toolchain.
-DT_FLAGS = {"bf16": ["-DGGNN_DT_BF16=1", "-mllvm", "-amdgpu-mfma-vgpr-form"], "f32": ["-DGGNN_DT_BF16=0"]}
+# "bf16acc": bf16 kernels whose matrix-core accumulators are read once, at
+# the end (they may live in AGPRs, which frees VGPRs for loads in flight).
+DT_FLAGS = {"bf16": ["-DGGNN_DT_BF16=1", "-mllvm", "-amdgpu-mfma-vgpr-form"], "f32": ["-DGGNN_DT_BF16=0"],
+            "bf16acc": ["-DGGNN_DT_BF16=1"]}
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall"]
 
 # (source, language, dtype build or None)
 SOURCES = [("host.cpp", "c++", None), ("capi_device.cpp", "hip", None), ("profile.cpp", "hip", None)] + [
-    (src, "hip", dt) for src in ("banded.hip", "banded_bits.hip", "banded_wide.hip", "transform.hip", "gru.hip", "readout.hip", "sparse.hip", "supernode.hip") for dt in ("bf16", "f32")]
+    (src, "hip", dt) for src in ("banded.hip", "banded_bits.hip", "banded_wide.hip", "transform.hip", "gru.hip", "readout.hip", "sparse.hip", "supernode.hip") for dt in ("bf16", "f32")] + [
+    ("wgrad_wide.hip", "hip", "bf16acc")]
 
 
 def _compile(src: str, lang: str, dt) -> str:

@@ -30,6 +30,11 @@ struct ReduceList {
 };
 hipError_t launch_reduce_multi(const ReduceList& l, hipStream_t st);
 // Appends to *defer (when non-NULL and not full), else launches the reduction.
+// Message-transform weight gradient at H = 256 in bf16 with node-major dM
+// (csrc/wgrad_wide.hip): per-split partials P [nsplit][E][256][256] and, when
+// Pb is not NULL, Pb [nsplit][E][256]; splits of rows_per_split rows.
+hipError_t launch_transform_wgrad_nm256(int nsplit, int rows_per_split, long K, int E, const void* X, const void* dM,
+                                        long ldk, float* P, float* Pb, hipStream_t st);
 hipError_t reduce_or_defer(const float* part, float* out, int nsplit, int count, long stride, ReduceList* defer,
                            hipStream_t st);
 

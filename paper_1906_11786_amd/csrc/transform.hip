@@ -671,6 +671,9 @@ hipError_t transform_wgrad_h(long K, int E, const void* X, const void* dM, long 
   return launch_reduce_partials(Pb, dbias, sp.nsplit, E * H, (long)E * H, st);
 }
 
+#ifndef GGNN_WGRAD256_WIDE
+#define GGNN_WGRAD256_WIDE 1
+#endif
 template <typename S, int H>
 hipError_t transform_wgrad_nm_h(long K, int E, const void* X, const void* dM, long ldk, float* dW, float* dbias,
                                 void* ws, ReduceList* defer, hipStream_t st) {
@@ -678,10 +681,15 @@ hipError_t transform_wgrad_nm_h(long K, int E, const void* X, const void* dM, lo
   Split sp = transform_nm_split(K, H, E, C::TE, sizeof(S) == 4);
   float* P = static_cast<float*>(ws);
   float* Pb = dbias ? P + (size_t)sp.nsplit * E * H * H : nullptr;
-  const int blocks = sp.nsplit * ((E + C::TE - 1) / C::TE) * (H / C::IT);
-  hipLaunchKernelGGL((dev::transform_wgrad_nm_kernel<S, H>), dim3(blocks), dim3(64 * C::NWV), 0, st,
-                     static_cast<const S*>(X), static_cast<const S*>(dM), ldk, P, Pb, K, E, sp.per);
-  hipError_t err = hipGetLastError();
+  hipError_t err;
+  if (GGNN_WGRAD256_WIDE && H == 256 && sizeof(S) == 2 && C::TE == 1) {
+    err = launch_transform_wgrad_nm256(sp.nsplit, sp.per, K, E, X, dM, ldk, P, Pb, st);   // same split
+  } else {
+    const int blocks = sp.nsplit * ((E + C::TE - 1) / C::TE) * (H / C::IT);
+    hipLaunchKernelGGL((dev::transform_wgrad_nm_kernel<S, H>), dim3(blocks), dim3(64 * C::NWV), 0, st,
+                       static_cast<const S*>(X), static_cast<const S*>(dM), ldk, P, Pb, K, E, sp.per);
+    err = hipGetLastError();
+  }
   if (err != hipSuccess) return err;
   err = reduce_or_defer(P, dW, sp.nsplit, E * H * H, (long)E * H * H, defer, st);
   if (err != hipSuccess || !dbias) return err;

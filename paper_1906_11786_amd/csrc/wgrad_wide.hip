@@ -1,0 +1,199 @@
+// Weight gradient of the message transform at H = 256 (bf16), the largest
+// single contraction of the reverse pass: over all T * n_pad rows k,
+//   P[split][e][h_in][h_out] = sum_k X[k][h_in] dM[e][k][h_out],
+//   Pb[split][e][h_out]      = sum_k dM[e][k][h_out]
+// (partials per row split, summed later in a fixed order), with dM stored
+// node-major by the reverse step kernels (row k of type e at (e ldk + k) H).
+//
+// It streams 47 GB at the 1M-node workload: what bounds it is how many bytes
+// each compute unit keeps in flight.  Loads that pass through registers are
+// limited by the registers left next to the accumulators (one chunk at a
+// time); here the rows go from global memory straight to LDS
+// (global_load_lds_dwordx4: each lane's 16 bytes land at the wave's LDS base
+// + 16 lane), three chunks ahead of the one being multiplied, in a ring of
+// four LDS slots.  The loads are issued from inline assembly, so that the
+// compiler does not wait for all of them before every LDS read; the kernel
+// waits for exactly the chunk it needs (s_waitcnt vmcnt counts these loads in
+// issue order) and then meets the other waves at a barrier.
+//
+// Workgroup: 8 waves, one row split, one edge type, all 256 input features
+// (dM, the large operand, read once).  Wave (wi, wo) of a 2 x 4 grid owns
+// input tiles 8 wi .. 8 wi + 7 and output tiles 4 wo .. 4 wo + 3.  A chunk
+// is 32 rows of X and of dM_e, node-major, unpadded; the 16-element groups of
+// chunk row r are XOR-permuted by sw(r) = (r & 3) | ((r >> 3) & 1) << 2 (the
+// permutation is applied to each lane's source address, the LDS writes being
+// contiguous), so that the rows of one transposing read fall on disjoint
+// banks.  Splits are multiples of 128 rows and K = T n_pad a multiple of 32,
+// so every chunk is whole.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace ggnn {
+namespace dev {
+namespace wgw {
+
+constexpr int H = 256, KC = 32, WI = 2, WO = 4, NWV = WI * WO, NT = 64 * NWV;
+constexpr int TI = 16 / WI, TO = 16 / WO;   // input / output tiles per wave
+constexpr int SLOT = 2 * KC * H;            // elements of one slot: X rows, then dM rows
+constexpr int NSLOT = 4;
+constexpr int IPW = KC * H * 2 / 1024 / NWV;   // 1 KB loads per wave per operand and chunk (2)
+
+__device__ __forceinline__ int sw(int r) { return (r & 3) | (((r >> 3) & 1) << 2); }
+
+// Fragment of a swizzled k-major [KC][256] tile: lane (q, g) receives
+// elements (k0 + 8g + j, n0 + q), j = 0..7 (n0 a multiple of 16); two
+// transposing reads, four rows apart (rows r and r + 4 share the swizzle).
+__device__ __forceinline__ bf16x8 frag(const bf16s* base, int k0, int n0, int lane) {
+  const int p = lane % 16, g = lane / 16;
+  const int row = k0 + 8 * g + p / 4;
+  const bf16s* a0 = base + row * H + ((n0 ^ (sw(row) << 4)) + 4 * (p % 4));
+  const tr_v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_tr_v4i16*)(const_cast<bf16s*>(a0)));
+  const tr_v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_tr_v4i16*)(const_cast<bf16s*>(a0) + 4 * H));
+  typedef short v8i16 __attribute__((ext_vector_type(8)));
+  const v8i16 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// One wave-wide 1 KB copy: lane l's 16 bytes at gsrc go to LDS byte address
+// lds + 16 l (lds wave-uniform).  M0 holds the LDS base; one wait state
+// between writing M0 and the load that uses it.
+__device__ __forceinline__ void dma16(const void* gsrc, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(gsrc)
+               : "memory", "m0");
+}
+// Wait until at most N of this wave's copies are outstanding (vmcnt only).
+template <int N>
+__device__ __forceinline__ void wait_copies() {
+  static_assert(N >= 0 && N < 16, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt(0xF70 | N);
+}
+
+__global__ __launch_bounds__(NT) void transform_wgrad_nm256_kernel(const bf16s* __restrict__ X,
+                                                                   const bf16s* __restrict__ dM, long ldk,
+                                                                   float* __restrict__ P, float* __restrict__ Pb,
+                                                                   long K, int E, int rows_per_split) {
+  __shared__ __attribute__((aligned(1024))) bf16s ring[NSLOT * SLOT];
+
+  const int tid = threadIdx.x, lane = tid % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int q = lane % 16, g = lane / 16;
+  const int wi = wave % WI, wo = wave / WI;
+  const int bid = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int e = bid % E;
+  const int split = bid / E;
+  const long nlo = (long)split * rows_per_split;
+  const long nhi = min(K, nlo + rows_per_split);
+  const int nchunks = nlo < nhi ? (int)((nhi - nlo) / KC) : 0;
+  const bf16s* dMe = dM + (size_t)e * ldk * H;
+  const uint32_t ring_lds = (uint32_t)(uintptr_t)ring;
+
+  // This lane's part of a chunk: copy j of the wave covers chunk rows
+  // r = 2 (IPW wave + j) + lane / 32, 16-byte unit lane % 32 of the row, whose
+  // source is the unit of column (8 (lane % 32)) ^ (16 sw(r)).
+  int src_off[IPW];   // element offset within the chunk's first row
+#pragma unroll
+  for (int j = 0; j < IPW; ++j) {
+    const int r = 2 * (IPW * wave + j) + lane / 32;
+    src_off[j] = r * H + ((8 * (lane % 32)) ^ (sw(r) << 4));
+  }
+  auto issue = [&](int chunk, int slot) __attribute__((always_inline)) {
+    const size_t row0 = (size_t)(nlo + (long)chunk * KC) * H;
+    const uint32_t base = ring_lds + (uint32_t)(slot * SLOT) * 2u;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const uint32_t at = base + (uint32_t)(2 * (IPW * wave + j)) * H * 2u;
+      dma16(X + row0 + src_off[j], at);
+      dma16(dMe + row0 + src_off[j], at + (uint32_t)KC * H * 2u);
+    }
+  };
+
+  f32x4 acc[TI][TO];
+  float bsum[TO];
+#pragma unroll
+  for (int o = 0; o < TO; ++o) {
+    bsum[o] = 0.f;
+#pragma unroll
+    for (int i = 0; i < TI; ++i) acc[i][o] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  auto compute = [&](int slot) __attribute__((always_inline)) {
+    const bf16s* sx = ring + slot * SLOT;
+    const bf16s* sd = sx + KC * H;
+#pragma unroll
+    for (int k0 = 0; k0 < KC; k0 += 32) {
+      bf16x8 fb[TO];
+#pragma unroll
+      for (int o = 0; o < TO; ++o) {
+        fb[o] = frag(sd, k0, 16 * (wo * TO + o), lane);
+        if (wi == 0) {
+#pragma unroll
+          for (int x = 0; x < 8; ++x) bsum[o] += static_cast<float>(fb[o][x]);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < TI; ++i) {
+        const bf16x8 fa = frag(sx, k0, 16 * (wi * TI + i), lane);
+#pragma unroll
+        for (int o = 0; o < TO; ++o) mma(acc[i][o], fa, fb[o]);
+      }
+    }
+  };
+  // Chunk c in slot c % 4; before multiplying it, wait for this wave's copies
+  // of it (the chunks after it that were issued may stay in flight), meet the
+  // other waves, and issue chunk c + 3 into the slot chunk c - 1 used (every
+  // wave is past its products).
+  constexpr int PER = 2 * IPW;   // copies per wave and chunk
+  auto stage = [&](int c, int slot) __attribute__((always_inline)) {
+    const int later = nchunks - 1 - c;   // chunks after c already issued (at most 2)
+    if (later >= 2) wait_copies<2 * PER>();
+    else if (later == 1) wait_copies<PER>();
+    else wait_copies<0>();
+    __syncthreads();
+    if (c + 3 < nchunks) issue(c + 3, (slot + 3) % NSLOT);
+    compute(slot);
+  };
+#pragma unroll
+  for (int c = 0; c < 3; ++c)
+    if (c < nchunks) issue(c, c);
+  for (int c = 0; c < nchunks; c += NSLOT) {
+    stage(c, 0);
+    if (c + 1 >= nchunks) break;
+    stage(c + 1, 1);
+    if (c + 2 >= nchunks) break;
+    stage(c + 2, 2);
+    if (c + 3 >= nchunks) break;
+    stage(c + 3, 3);
+  }
+
+  // D[h_in = 16 (wi TI + i) + 4g + j][h_out = 16 (wo TO + o) + q]
+  float* out = P + ((size_t)split * E + e) * H * H;
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int o = 0; o < TO; ++o)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        out[(size_t)(16 * (wi * TI + i) + 4 * g + j) * H + 16 * (wo * TO + o) + q] = acc[i][o][j];
+  if (Pb != nullptr && wi == 0) {
+#pragma unroll
+    for (int o = 0; o < TO; ++o) {
+      float v = bsum[o];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (g == 0) Pb[((size_t)split * E + e) * H + 16 * (wo * TO + o) + q] = v;
+    }
+  }
+}
+
+}  // namespace wgw
+}  // namespace dev
+
+hipError_t launch_transform_wgrad_nm256(int nsplit, int rows_per_split, long K, int E, const void* X, const void* dM,
+                                        long ldk, float* P, float* Pb, hipStream_t st) {
+  if (rows_per_split % dev::wgw::KC != 0 || K % dev::wgw::KC != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(dev::wgw::transform_wgrad_nm256_kernel, dim3(nsplit * E), dim3(dev::wgw::NT), 0, st,
+                     static_cast<const dev::bf16s*>(X), static_cast<const dev::bf16s*>(dM), ldk, P, Pb, K, E,
+                     rows_per_split);
+  return hipGetLastError();
+}
+
+}  // namespace ggnn
