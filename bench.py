@@ -70,7 +70,7 @@ KERNELS = {
 OTHER_KERNELS = [("gru_fwd_kernel",), ("gru_bwd_kernel",), ("gru_fwd_big_kernel",), ("gru_bwd_big_kernel",),
                  ("gru_wgrad_kernel",), ("transform_bwd_dx_kernel",),
                  ("transform_wgrad_kernel",), ("transform_wgrad_nm_kernel",), ("transform_fwd_kernel",),
-                 ("reduce_partials_kernel",), ("reduce_multi_kernel",)]
+                 ("transform_wgrad_nm256_kernel",), ("reduce_partials_kernel",), ("reduce_multi_kernel",)]
 CAL_ELEMS = 64 << 20            # calibration copy: 64 Mi fp32 read, 64 Mi fp32 written
 CAL_BYTES = CAL_ELEMS * 4
 CAL_NAME = "neg_kernel"         # torch's elementwise negation: one read and one write per element
