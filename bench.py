@@ -30,7 +30,12 @@ command, each scaled by what the counter reads for a plain copy of known size
 (the calibration copy every run makes after the timed region);
 `--traffic-from FETCH.csv WRITE.csv` turns those two counter files into the
 summary kept under profiles/.  The figure is used only while the kernel's
-sources hash to the value recorded with it.
+sources hash to the value recorded with it.  The roofline's fractions are
+effective rates (work counted on the paper's dense blocks, some of which the
+kernels skip); `mfma_busy_counters` beside them is the fraction of cycles the
+matrix cores were busy in a rocprofv3 --pmc run of this command
+(SQ_VALU_MFMA_BUSY_CYCLES and SQ_BUSY_CYCLES, summarised by `--busy-from`),
+under the same source-hash rule.
 """
 from __future__ import annotations
 
@@ -111,6 +116,9 @@ def parse():
     p.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="summarise two rocprofv3 --pmc counter files (FETCH_SIZE, WRITE_SIZE) of this command "
                         "and exit")
+    p.add_argument("--busy-from", metavar="SQ_CSV",
+                   help="summarise a rocprofv3 --pmc counter file holding SQ_VALU_MFMA_BUSY_CYCLES and "
+                        "SQ_BUSY_CYCLES of this command (matrix-core busy fraction per kernel) and exit")
     return p.parse_args()
 
 
@@ -136,6 +144,39 @@ def recorded_traffic(kernel, workload, band):
                     if rec.get("source_hash") == want:
                         return rec["bytes_per_launch"], os.path.relpath(path, ROOT)
     return None, None
+
+
+def recorded_busy(kernel, workload, band):
+    """Counter-measured matrix-core busy fraction recorded under profiles/
+    for this kernel, workload and band, if its sources are unchanged since."""
+    want = source_hash(KERNELS[kernel][1])
+    for path in sorted(glob.glob(os.path.join(PROFILES, "*.md"))):
+        with open(path) as f:
+            for line in f:
+                if not line.startswith("mfma-busy-record: "):
+                    continue
+                rec = json.loads(line[len("mfma-busy-record: "):])
+                if (rec.get("kernel"), rec.get("workload"), rec.get("band")) == (kernel, workload, band):
+                    if rec.get("source_hash") == want:
+                        return rec["mfma_busy"], os.path.relpath(path, ROOT)
+    return None, None
+
+
+def busy_summary(sq_csv):
+    """Matrix-core busy fraction per launch, SQ_VALU_MFMA_BUSY_CYCLES /
+    (1024 SIMDs x SQ_BUSY_CYCLES / 32 shader engines), median per kernel."""
+    mfma, busy = _counter_rows(sq_csv, "SQ_VALU_MFMA_BUSY_CYCLES"), _counter_rows(sq_csv, "SQ_BUSY_CYCLES")
+    lines = ["| kernel | launches | matrix cores busy (median) |", "|---|---:|---:|"]
+    recs = []
+    for key, (frag, srcs) in KERNELS.items():
+        vals = [v / (1024.0 * busy[d][1] / 32.0) for d, (name, v) in mfma.items()
+                if d in busy and busy[d][1] > 0 and all(f in name for f in frag)]
+        if not vals:
+            continue
+        m = statistics.median(vals)
+        lines.append(f"| `{' '.join(frag)}` | {len(vals)} | {m:.3f} |")
+        recs.append((key, m, srcs))
+    return lines, recs
 
 
 def _counter_rows(path, counter):
@@ -533,6 +574,9 @@ def measure(spec, args, torch, with_extras=True):
     traffic, traffic_src = recorded_traffic(dom, spec.name, args.band) if dom in KERNELS else (None, None)
     roofline["traffic"] = traffic
     roofline["traffic_source"] = traffic_src
+    busy, busy_src = recorded_busy(dom, spec.name, args.band) if dom in KERNELS else (None, None)
+    roofline["mfma_busy_counters"] = busy
+    roofline["mfma_busy_source"] = busy_src
     roofline["launch_kinds"] = kinds
     del da_prev, dh_prev, ghat
 
@@ -578,6 +622,14 @@ def main():
                    "source_hash": source_hash(srcs), "sources": srcs}
             print("traffic-record: " + json.dumps(rec))
         return
+    if args.busy_from:
+        lines, recs = busy_summary(args.busy_from)
+        print("\n".join(lines) + "\n")
+        for k, m, srcs in recs:
+            rec = {"kernel": k, "workload": spec_for(args.workload).name, "band": args.band,
+                   "mfma_busy": round(m, 4), "source_hash": source_hash(srcs), "sources": srcs}
+            print("mfma-busy-record: " + json.dumps(rec))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the path is measured on a single GPU",
               file=sys.stderr)
@@ -605,7 +657,8 @@ def main():
                "unit": "node-steps/s", "ms_per_step": round(s_res["ms_per_step"], 4),
                "timing": s_res["config"]["timing"],
                "roofline": {k: r[k] for k in ("bound", "achieved", "peak", "unit", "frac", "kernel", "avg_launch_us",
-                                              "avg_launch_us_back_to_back", "traffic", "traffic_source")}}
+                                              "avg_launch_us_back_to_back", "traffic", "traffic_source",
+                                              "mfma_busy_counters")}}
 
     # Calibration copy for the traffic counters (outside every timed region).
     cal_src = torch.ones(CAL_ELEMS, dtype=torch.float32, device="cuda")
