@@ -349,11 +349,13 @@ def cpu_baseline(spec, graphs, params_for, node_budget):
             "sample": f"one full step (T={spec.T} forward + T reverse, fp64) on {what}; {dt:.1f} s"}
 
 
-def time_supernodes(spec, graphs, s, timed, torch):
+def time_supernodes(spec, graphs, s, timed, torch, eager_only):
     """T steps forward and reverse with supernode slices next to the band
-    (SupernodeGGNN: per-step calls), on the workload's graphs with two hub
-    nodes per graph linked both ways to 10% of it; the slices' own calls
-    timed alone."""
+    (SupernodeGGNN: the slices inside ggnn_forward / ggnn_backward), on the
+    workload's graphs with two hub nodes per graph linked both ways to 10% of
+    it, timed like the band-only step (eager and as a replayed HIP graph);
+    the stand-alone slice calls timed alone; device time per launch kind of
+    the eager steps from the launch profiler."""
     from ggnn_synth import add_hubs, draw_params
     from paper_1906_11786_amd import capi
     from paper_1906_11786_amd.driver import compile_with_supernodes, SupernodeGGNN
@@ -368,18 +370,32 @@ def time_supernodes(spec, graphs, s, timed, torch):
     comp = compile_with_supernodes(hubbed, hubs, spec.B, spec.E, s)
     params = draw_params(spec.cfg, comp.n_real, comp.n_pad, spec.H, spec.E, spec.dtype)
     m = SupernodeGGNN(comp, spec.H, spec.T, spec.dtype, params)
-    step_s = timed(lambda: (m.forward(), m.backward()))
+    eager_s = timed(m.step, profile=True)
+    records = [capi.ggnn_profile_read(i) for i in range(capi.ggnn_profile_count())]
+    capi.ggnn_profile_start(0)
+    graph_s = None
+    if not eager_only:
+        m.capture()
+        graph_s = timed(m.replay)
+    kinds = {}
+    for kind, ms in records:
+        kinds.setdefault(kind, []).append(ms)
     n_pad, H, E = comp.n_pad, spec.H, spec.E
-    fwd_s = timed(lambda: capi.ggnn_super_propagate(spec.dtype, n_pad, H, E, s, m.rows, m.cols, m.X[0], m.W, m.bias,
-                                                    m.a[0], m.ws_sn, m.ws_sn.numel()))
-    bwd_s = timed(lambda: capi.ggnn_super_propagate_bwd(spec.dtype, n_pad, H, E, s, m.rows, m.rows_t, m.cols_t,
-                                                        m.X[0], m.W, m.da, m.dX, m.dW, m.bias, m.ws_sn,
-                                                        m.ws_sn.numel()))
+    rows, cols, rows_t, cols_t = m.super_slices
+    fwd_s = timed(lambda: capi.ggnn_super_propagate(spec.dtype, n_pad, H, E, s, rows, cols, m.X[0], m.W, m.bias,
+                                                    m.a[0], m.super_ws, m.super_ws.numel()))
+    bwd_s = timed(lambda: capi.ggnn_super_propagate_bwd(spec.dtype, n_pad, H, E, s, rows, rows_t, cols_t,
+                                                        m.X[0], m.W, m.da, m.dX, m.dW, m.bias, m.super_ws,
+                                                        m.super_ws.numel()))
     st = comp.stats
-    out = {"n_super": s, "hubs": st["n_hubs"], "hub_edges_rows": st["n_super_rows"],
+    best = min(x for x in (eager_s, graph_s) if x is not None)
+    out = {"n_super": s, "hubs": st["n_hubs"], "n_super_active": st["n_super_active"],
+           "fused_in_step_kernels": bool(m.super_fused), "hub_edges_rows": st["n_super_rows"],
            "hub_edges_cols": st["n_super_cols"], "band_edges": st["n_packed"], "dropped": st["n_dropped"],
-           "ms_per_step_composed": round(step_s * 1e3, 4), "ms_super_propagate": round(fwd_s * 1e3, 4),
-           "ms_super_propagate_bwd": round(bwd_s * 1e3, 4)}
+           "ms_per_step": round(best * 1e3, 4), "ms_per_step_eager": round(eager_s * 1e3, 4),
+           "ms_per_step_graph": None if graph_s is None else round(graph_s * 1e3, 4),
+           "launch_kinds_us": {k: round(1e3 * sum(v) / len(v), 2) for k, v in kinds.items()},
+           "ms_super_propagate": round(fwd_s * 1e3, 4), "ms_super_propagate_bwd": round(bwd_s * 1e3, 4)}
     del m
     torch.cuda.empty_cache()
     return out
@@ -529,7 +545,8 @@ def measure(spec, args, torch, with_extras=True):
 
     supernodes = None
     if with_extras and args.supernodes:
-        supernodes = time_supernodes(spec, graphs, args.supernodes, timed, torch)
+        supernodes = time_supernodes(spec, graphs, args.supernodes, timed, torch, args.eager)
+        supernodes["ratio_to_band_only"] = round(supernodes["ms_per_step"] / (sec_per_step * 1e3), 3)
 
     # Device time per step of every launch kind, from the eager timed steps.
     es = 2 if spec.dtype == "bf16" else 4

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define GGNN_ABI_VERSION 10
+#define GGNN_ABI_VERSION 11
 
 typedef enum {
   GGNN_OK = 0,
@@ -343,6 +343,20 @@ typedef struct ggnn_model {
                            caller refreshes it whenever W changes. */
   const void* gru_packed; /* Wi, U as ggnn_gru_pack_weights lays them out, or NULL (optional, used where
                              ggnn_gru_pack_bytes > 0; the caller refreshes it whenever Wi or U change). */
+  /* Supernodes next to the band (Discussion section; optional, bit band only): n_super = 0 for none.
+   * Otherwise nodes 0 .. n_super-1 are supernode slots and the four slices of ggnn_super_pack hold every
+   * edge that touches one (the band holds the others).  n_super_active: 0 when the slices hold no edge,
+   * else a multiple of 16, at most n_super, with no slice edge at a supernode index at or above it
+   * (ggnn_super_active computes it from the packed slices); the slices' rows and columns at or beyond it
+   * are never read.  super_ws: device scratch of ggnn_super_model_workspace_bytes(model) bytes, 16-byte
+   * aligned, used by ggnn_forward and ggnn_backward (neither keeps anything in it between calls). */
+  int32_t n_super, n_super_active;
+  const void* super_rows;    /* [E][n_super][n_pad/8] */
+  const void* super_cols;    /* [E][n_pad][n_super/8] */
+  const void* super_rows_t;  /* [E][n_pad][n_super/8] */
+  const void* super_cols_t;  /* [E][n_super][n_pad/8] */
+  void* super_ws;
+  size_t super_ws_bytes;
 } ggnn_model;
 
 typedef struct ggnn_activations {
@@ -372,14 +386,26 @@ typedef struct ggnn_grads {
 /* Workspace bytes needed by ggnn_backward for this model. */
 size_t ggnn_backward_workspace_bytes(const ggnn_model* model);
 
+/* Workspace bytes of the supernode slices for this model (model->super_ws); 0 without supernodes. */
+size_t ggnn_super_model_workspace_bytes(const ggnn_model* model);
+
 /* Forward over T steps: for t = 0..T-1,
  *   dense band: M = msg_transform(X[t]); a[t] = banded_propagate(M);
  *   bit band:   a[t] = banded_step_bits(X[t]);
- *   then X[t+1], saved[t] = gru_update(a[t], X[t]). */
+ *   with supernodes (bit band): a[t] += the slices' share (ggnn_super_propagate);
+ *   then X[t+1], saved[t] = gru_update(a[t], X[t]).
+ * With supernodes, in bf16 at H <= 64 with n_super_active <= 32 and a grid small enough for the
+ * two-group fused steps (ggnn_super_fusable), the slices run inside the fused step kernels: the
+ * column slice as a fourth block next to the three of Eq. 3 (the 32 supernodes' states staged once per
+ * workgroup), and the supernode rows' aggregate R_e X from one long contraction per step; otherwise the
+ * slice kernels of ggnn_super_propagate run between the band step and the GRU. */
 ggnn_status ggnn_forward(const ggnn_model* model, const ggnn_activations* act, void* stream);
 
 /* Reverse pass for L with dL/dX_T given in grads->dX: for t = T-1..0,
  *   da, dh, G^_t = gru_update_bwd node pass(dX);
+ *   with supernodes: the slices' reverse (fused as in ggnn_forward: the transposed row slice as a fourth
+ *   block, the supernode rows' message gradients C_e^T da from one long contraction per step, all of it
+ *   in dM; otherwise ggnn_super_propagate_bwd adds its share to dh, dW and dbias first);
  *   dense band: dM_t = banded_propagate_bwd(da); dX = dh + sum_e dM_t,e W_e^T;
  *   bit band:   dM_t, dX = banded_step_bits_bwd(da, dX_in = dh) (one kernel);
  * then the weight gradients as single contractions over all T * n_pad rows:
@@ -397,7 +423,9 @@ ggnn_status ggnn_backward(const ggnn_model* model, const ggnn_activations* act,
  * with the launch kind (ggnn_profile_name: "step_fwd", "step_fwd_gru",
  * "gru_fwd", "transform_fwd", "banded_fwd", "gru_rev", "step_rev",
  * "step_rev_gru", "banded_rev", "transform_rev_dx", "wgrad_gru",
- * "wgrad_transform", "reduce"; the "_gru" forms are band steps with the GRU
+ * "wgrad_transform", "reduce", "super_long" (the supernode rows' long contraction of a fused
+ * supernode step, with its reduction), "super" (the stand-alone slice kernels of one step's share);
+ * the "_gru" forms are band steps with the GRU
  * or GRU reverse fused into the same kernel).  Launches made while the stream
  * is being captured into a HIP graph, and launches beyond `capacity`, are not
  * recorded.  The state is process-wide and meant for one driving host thread;
@@ -549,6 +577,15 @@ ggnn_status ggnn_super_pack(int32_t n_pad, int32_t E, int32_t s, int64_t m, cons
 
 /* Workspace bytes of the two device calls below (0 for unsupported sizes). */
 size_t ggnn_super_workspace_bytes(int32_t n_pad, int32_t H, int32_t E, int32_t s);
+
+/* Host: the smallest multiple of 16 above every supernode index that has an edge in the slices (0 when
+ * they hold none): rows i of rows [E][s][n_pad/8] with a bit set, columns j of cols [E][n_pad][s/8] with
+ * a bit set.  Returns -1 (message via ggnn_last_error) for a NULL slice or unsupported sizes. */
+int32_t ggnn_super_active(int32_t n_pad, int32_t E, int32_t s, const void* rows, const void* cols);
+
+/* Whether ggnn_forward / ggnn_backward run the slices inside the fused step kernels for this shape
+ * (bf16, H <= 64, two-group fused forms at this n_pad, B; and n_super_active = 16 or 32). */
+int32_t ggnn_super_fusable(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E, int32_t n_super_active);
 
 /* Device: the slices' share of one propagation step, added onto a (the
  * band's aggregate, e.g. from ggnn_banded_step_bits), with M_e = X W_e + b_e:

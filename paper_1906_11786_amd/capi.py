@@ -39,7 +39,7 @@ EXPORTS = [
     "ggnn_readout_loss", "ggnn_readout_loss_bwd_workspace_bytes", "ggnn_readout_loss_bwd", "ggnn_sgd_momentum",
     "ggnn_sparse_csr", "ggnn_sparse_step",
     "ggnn_super_bytes", "ggnn_super_pack", "ggnn_super_workspace_bytes", "ggnn_super_propagate",
-    "ggnn_super_propagate_bwd",
+    "ggnn_super_propagate_bwd", "ggnn_super_active", "ggnn_super_fusable", "ggnn_super_model_workspace_bytes",
     "ggnn_profile_start", "ggnn_profile_stop", "ggnn_profile_count", "ggnn_profile_read", "ggnn_profile_name",
     "ggnn_readout_loss_bwd_noalloc",
 ]
@@ -57,7 +57,9 @@ class ggnn_model(C.Structure):
                 ("E", C.c_int32), ("T", C.c_int32), ("band", C.c_void_p), ("W", C.c_void_p),
                 ("bias", C.c_void_p), ("Wi", C.c_void_p), ("U", C.c_void_p), ("b", C.c_void_p),
                 ("band_format", C.c_int32), ("band_t", C.c_void_p), ("Wt", C.c_void_p),
-                ("gru_packed", C.c_void_p)]
+                ("gru_packed", C.c_void_p), ("n_super", C.c_int32), ("n_super_active", C.c_int32),
+                ("super_rows", C.c_void_p), ("super_cols", C.c_void_p), ("super_rows_t", C.c_void_p),
+                ("super_cols_t", C.c_void_p), ("super_ws", C.c_void_p), ("super_ws_bytes", C.c_size_t)]
 
 
 class ggnn_activations(C.Structure):
@@ -114,6 +116,9 @@ _SIGS = {
     "ggnn_super_bytes": (sz, [i32, i32, i32]),
     "ggnn_super_pack": (C.c_int, [i32, i32, i32, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
     "ggnn_super_workspace_bytes": (sz, [i32, i32, i32, i32]),
+    "ggnn_super_active": (i32, [i32, i32, i32, vp, vp]),
+    "ggnn_super_fusable": (i32, [C.c_int, i32, i32, i32, i32, i32]),
+    "ggnn_super_model_workspace_bytes": (sz, [C.POINTER(ggnn_model)]),
     "ggnn_super_propagate": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
     "ggnn_super_propagate_bwd": (C.c_int, [C.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz,
                                            vp]),
@@ -177,7 +182,7 @@ def _i32(a) -> np.ndarray:
 
 # Interface version this binding is written against (GGNN_ABI_VERSION of
 # include/ggnn.h); the library must report the same number.
-ABI_VERSION = 10
+ABI_VERSION = 11
 
 
 def ggnn_abi_version() -> int:
@@ -436,6 +441,25 @@ def ggnn_super_pack(n_pad, E, s, src, dst, etype, with_transpose=True):
 
 def ggnn_super_workspace_bytes(n_pad, H, E, s) -> int:
     return int(lib().ggnn_super_workspace_bytes(n_pad, H, E, s))
+
+
+def ggnn_super_active(n_pad, E, s, rows, cols) -> int:
+    """Active supernode count (a multiple of 16, 0 for empty slices) of the
+    host slices `rows`, `cols` (numpy uint8 arrays of ggnn_super_pack)."""
+    r = np.ascontiguousarray(rows, np.uint8)
+    c = np.ascontiguousarray(cols, np.uint8)
+    v = int(lib().ggnn_super_active(n_pad, E, s, r.ctypes.data, c.ctypes.data))
+    if v < 0:
+        raise GGNNError("ggnn_super_active", 1, ggnn_last_error())
+    return v
+
+
+def ggnn_super_fusable(dt, n_pad, B, H, E, n_super_active) -> bool:
+    return bool(lib().ggnn_super_fusable(_dt(dt), n_pad, B, H, E, n_super_active))
+
+
+def ggnn_super_model_workspace_bytes(model: ggnn_model) -> int:
+    return int(lib().ggnn_super_model_workspace_bytes(C.byref(model)))
 
 
 def ggnn_super_propagate(dt, n_pad, H, E, s, rows, cols, X, W, bias, a, workspace, workspace_bytes, stream=None):

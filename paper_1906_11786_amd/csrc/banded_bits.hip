@@ -21,6 +21,7 @@
 #include "device_common.h"
 #include "gru_wave.h"
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace ggnn {
 namespace dev {
@@ -224,20 +225,34 @@ struct BitsCfg {
 // here.  Wi^T and U^T are staged in LDS with the blocks; the GRU products
 // take a (hi + lo in bf16 mode), h and r*h as operand fragments straight
 // from registers (accumulator-compatible order).
+// SN (supernodes next to the band, bf16 direct-weight forms): the first 32
+// nodes are supernodes.  Per edge type the aggregation gets a fourth block,
+// the supernode window (nodes 0..31 of X forward, of da reverse; staged once)
+// against the slice bits of each row ([E][n_pad][sn_s/8]: forward the
+// column slice, edges from a supernode into this row; reverse the
+// transposed row slice, edges from this node into a supernode).  The rows of
+// the supernodes themselves get their whole per-type aggregate from the
+// record sn_rec = [P_e (sn_sr x H) | deg_e (sn_sr)] of the long contraction over
+// all nodes (forward R_e X, reverse C_e^T da): the wave holding rows 0..31
+// copies P_e of its rows into LDS (global -> LDS, issued at the top of the
+// type, waited for after the aggregation) and adds it to the aggregate (the
+// record's first sn_sr rows, 16 or 32: the supernodes with edges).
 // GRU, reverse (WDIR): the completed dX of these nodes is dL/dh' of the
 // previous step's GRU, whose reverse (gru_bwd_wave) runs right here: it
 // writes that step's da (feature-major), dh and G^, so one launch covers a
 // whole reverse step.  Wi and U are staged in LDS (plain copies) with the
 // blocks; dX itself is written only when `out` is not NULL.
 // ---------------------------------------------------------------------------
-template <typename S, int H, int B, int WAVES, bool WDIR, int TG, bool REV, bool GRU>
+constexpr int kSnFused = 32;   // supernodes handled inside the fused step kernels
+template <typename S, int H, int B, int WAVES, bool WDIR, int TG, bool REV, bool GRU, bool SN = false>
 __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
     const uint8_t* __restrict__ bits, const S* __restrict__ X, const S* __restrict__ W, const S* __restrict__ Wt,
     const float* __restrict__ bias,
     float* out, int n_pad, int E, const float* dX_in, S* __restrict__ dM, long ldm, const S* __restrict__ Wi,
     const S* __restrict__ U, const float* __restrict__ bg, S* __restrict__ h_out, S* __restrict__ saved,
     const S* __restrict__ rh_h, const S* __restrict__ rh_saved, S* __restrict__ rh_da, float* __restrict__ rh_dh,
-    S* __restrict__ rh_ghat) {
+    S* __restrict__ rh_ghat, const uint8_t* __restrict__ sn_bits, const float* __restrict__ sn_rec, int sn_s,
+    int sn_sr) {
   using C = BitsCfg<S, H, B>;
   constexpr int NT = TG * WAVES * kWave;
   constexpr int V = C::V, KC = C::KC, VP = C::VP, RB = C::RB, NTW = C::NTW, WP = C::WP;
@@ -250,10 +265,16 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   static_assert(TG == 1 || (TG - 1) * WAVES * kWave * NTW * MT * 16 <= (int)(C::NBUF * H * VP * sizeof(S)),
                 "partial sums must fit in the staged-block space");
   static_assert(!GRU || WDIR, "the GRU epilogues are direct-weight forms");
+  static_assert(!SN || (WDIR && sizeof(S) == 2 && C::RPW == kSnFused), "supernodes: bf16 direct-weight forms");
   constexpr int GWN = !GRU ? 8 : 2 * 3 * H * H;   // Wi and U in fragment order
   __shared__ __attribute__((aligned(16))) S vt[C::NBUF][H * VP];
   __shared__ __attribute__((aligned(16))) S wt[WDIR ? 8 : WC * WP];
   __shared__ __attribute__((aligned(16))) S gw[GWN];
+  // SN: supernode window (fragment order, features permuted as the blocks)
+  // and, per type group, the record rows of the wave holding nodes 0..31
+  // (NTW x MT 1 KB copies, one 16-byte unit per lane each).
+  __shared__ __attribute__((aligned(16))) S hubw[SN ? kSnFused * H : 8];
+  __shared__ __attribute__((aligned(1024))) float recb[SN ? TG * NTW * MT * 256 : 4];
 
   const int nb = n_pad / B;
   constexpr int NW = C::RPW * WAVES;
@@ -387,8 +408,53 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
       }
     }
   };
+  // SN: the supernode window (nodes 0..31) in the layout of a staged block
+  // chunk of 32 nodes; its loads are issued before the blocks' staging and
+  // written after it.  Forward unit: two nodes x eight features of
+  // node-major X; reverse unit: 16 bytes (V nodes) of one feature row of da.
+  constexpr int HU = SN ? (!REV ? (kSnFused / 2) * (H / 8) : H * (kSnFused / V)) : 1;
+  constexpr int HPT = (HU + NT - 1) / NT;
+  u32x4 hx[SN ? HPT : 1][SN && !REV ? 2 : 1];
+  if constexpr (SN) {
+#pragma unroll
+    for (int u = 0; u < HPT; ++u) {
+      const int lin = u * NT + tid;
+      if (lin < HU) {
+        if constexpr (!REV) {
+          const int cp = lin % (kSnFused / 2), f0 = (lin / (kSnFused / 2)) * 8;
+          hx[u][0] = *reinterpret_cast<const u32x4*>(X + (size_t)(2 * cp) * H + f0);
+          hx[u][!REV ? 1 : 0] = *reinterpret_cast<const u32x4*>(X + (size_t)(2 * cp + 1) * H + f0);
+        } else {
+          const int h = lin % H, c = (lin / H) * V;
+          hx[u][0] = *reinterpret_cast<const u32x4*>(X + (size_t)h * n_pad + c);
+        }
+      }
+    }
+  }
   if constexpr (C::ALL) {
     stage_units(0, nx);
+    if constexpr (SN) {
+#pragma unroll
+      for (int u = 0; u < HPT; ++u) {
+        const int lin = u * NT + tid;
+        if (lin < HU) {
+          if constexpr (!REV) {
+            const int cp = lin % (kSnFused / 2), f0 = (lin / (kSnFused / 2)) * 8;
+            const u32x4 x0 = hx[u][0], x1 = hx[u][!REV ? 1 : 0];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              store_pair(&hubw[frag_off<S, H, kSnFused>(perm_row(f0 + 2 * i), 2 * cp)], x0[i] & 0xFFFFu,
+                         x1[i] & 0xFFFFu);
+              store_pair(&hubw[frag_off<S, H, kSnFused>(perm_row(f0 + 2 * i + 1), 2 * cp)], x0[i] >> 16,
+                         x1[i] >> 16);
+            }
+          } else {
+            const int h = lin % H, c = (lin / H) * V;
+            *reinterpret_cast<u32x4*>(&hubw[frag_off<S, H, kSnFused>(perm_row(h), c)]) = hx[u][0];
+          }
+        }
+      }
+    }
     __syncthreads();
   }
 
@@ -501,6 +567,35 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         if (e + 1 < e_hi) load_type(e + 1, nx1);
       }
     }
+    // SN: the slice bytes of this wave's rows (window columns 8g .. 8g + 7)
+    // and, in the wave holding nodes 0..31, P_e of its rows (into LDS) and
+    // their degrees; all in flight during the aggregation below.
+    uint32_t hb[SN ? NTW : 1];
+    float hdeg[SN ? NTW : 1];
+    const bool hub_wave = SN && k * B + rw < kSnFused;   // wave-uniform
+    if constexpr (SN) {
+#pragma unroll
+      for (int n = 0; n < NTW; ++n) {
+        hb[n] = sn_bits[((size_t)e * n_pad + k * B + rw + 16 * n + q) * (size_t)(sn_s / 8) + g];
+        hdeg[n] = 0.f;
+      }
+      if (hub_wave) {
+        const uint32_t base = (uint32_t)(uintptr_t)recb + (uint32_t)(__builtin_amdgcn_readfirstlane(tg) * NTW * MT * 1024);
+#pragma unroll
+        for (int n = 0; n < NTW; ++n) {
+          if (16 * n >= sn_sr) continue;
+#pragma unroll
+          for (int m = 0; m < MT; ++m)
+            dma16(sn_rec + ((size_t)e * sn_sr + 16 * n + q) * H + 32 * (m / 2) + 8 * g + 4 * (m % 2),
+                  base + (uint32_t)((n * MT + m) * 1024));
+        }
+        if (!REV && bias) {
+#pragma unroll
+          for (int n = 0; n < NTW; ++n)
+            if (16 * n < sn_sr) hdeg[n] = sn_rec[(size_t)E * sn_sr * H + (size_t)e * sn_sr + 16 * n + q];
+        }
+      }
+    }
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
       if (s < s_lo || s > s_hi) continue;
@@ -537,6 +632,41 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
                                          : load_frag<S, H>(v, kk, m, lane);
 #pragma unroll
             for (int n = 0; n < NTW; ++n) mma(pre[n][m], af, bf[n]);
+          }
+        }
+      }
+    }
+    if constexpr (SN) {
+      // the supernode block, and the record of the supernode rows
+      uint32_t any = 0u;
+#pragma unroll
+      for (int n = 0; n < NTW; ++n) any |= hb[n];
+      if (__builtin_amdgcn_ballot_w64(any != 0u) != 0) {
+        frag_t<S> bf[NTW];
+#pragma unroll
+        for (int n = 0; n < NTW; ++n) {
+          bf[n] = bits_frag<S>(hb[n]);
+          if (!REV && bias) deg[n] += __popc(hb[n]);
+        }
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+          const frag_t<S> af = load_frag<S, H>(hubw, 0, m, lane);
+#pragma unroll
+          for (int n = 0; n < NTW; ++n) mma(pre[n][m], af, bf[n]);
+        }
+      }
+      if (hub_wave) {
+        wait_copies<0>();
+        asm volatile("" ::: "memory");
+        const float* rbuf = recb + tg * NTW * MT * 256;
+#pragma unroll
+        for (int n = 0; n < NTW; ++n) {
+          if (16 * n >= sn_sr) continue;
+#pragma unroll
+          for (int m = 0; m < MT; ++m) {
+            const f32x4 r = *reinterpret_cast<const f32x4*>(rbuf + ((n * MT + m) * 64 + lane) * 4);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) pre[n][m][j] += r[j];
           }
         }
       }
@@ -610,7 +740,8 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         int d = deg[n];
         d += __shfl_xor(d, 16);
         d += __shfl_xor(d, 32);
-        const float fd = static_cast<float>(d);
+        float fd = static_cast<float>(d);
+        if constexpr (SN) fd += hdeg[n];
 #pragma unroll
         for (int m = 0; m < MT; ++m)
 #pragma unroll
@@ -997,19 +1128,25 @@ struct BitsArgs {
   void* rh_da = nullptr;
   float* rh_dh = nullptr;
   void* rh_ghat = nullptr;
+  const SnStep* sn = nullptr;   // fused supernode share (bf16 direct-weight forms with the GRU or the t = 0 reverse)
 };
 
+// Launch shape of a bit-band kernel (mode as in BitsArgs).
+struct BitsPlan {
+  int waves, groups, blocks;
+  bool tg2;
+};
 template <typename S, int H, int B>
-hipError_t bits_launch(const BitsArgs& A, hipStream_t st) {
+BitsPlan bits_plan(int mode, int n_pad, int E) {
   using C = dev::BitsCfg<S, H, B>;
-  const int nb = A.n_pad / B;
-  const bool fused = A.mode != 2;
+  const int nb = n_pad / B;
+  const bool fused = mode != 2;
   int waves = B / C::RPW < 4 ? B / C::RPW : 4;
   // Streamed blocks at H = 256, forward: eight waves (128 rows) share each
   // staged chunk, halving the staging per row (the reverse step's
   // eight-wave form would spill registers).
   if constexpr (!C::ALL && H >= 256) {
-    if (A.mode == 0) waves = B / C::RPW < 8 ? B / C::RPW : 8;
+    if (mode == 0) waves = B / C::RPW < 8 ? B / C::RPW : 8;
   }
   const long min_blocks = fused ? GGNN_BITS_FWD_MIN_BLOCKS : GGNN_BITS_BWD_MIN_BLOCKS;
   while (waves > C::MINW && (long)nb * (B / (C::RPW * waves)) < min_blocks) waves /= 2;
@@ -1020,12 +1157,20 @@ hipError_t bits_launch(const BitsArgs& A, hipStream_t st) {
   int groups = 1;
   if (!fused) {
     const long want = (GGNN_BITS_BWD_WAVES + (long)tiles * waves - 1) / ((long)tiles * waves);
-    groups = (int)(want < 1 ? 1 : (want > A.E ? A.E : want));
+    groups = (int)(want < 1 ? 1 : (want > E ? E : want));
   }
   const int blocks = tiles * groups;
   // Fused steps: two type groups per workgroup (two waves per SIMD) when the
   // grid alone does not give every SIMD several waves.
-  const bool tg2 = C::WDIR && blocks <= GGNN_BITS_TG2_MAX_BLOCKS;
+  return BitsPlan{waves, groups, blocks, C::WDIR && blocks <= GGNN_BITS_TG2_MAX_BLOCKS};
+}
+
+template <typename S, int H, int B>
+hipError_t bits_launch(const BitsArgs& A, hipStream_t st) {
+  using C = dev::BitsCfg<S, H, B>;
+  const BitsPlan plan = bits_plan<S, H, B>(A.mode, A.n_pad, A.E);
+  const int waves = plan.waves, groups = plan.groups, blocks = plan.blocks;
+  const bool tg2 = plan.tg2;
   const uint8_t* bp = static_cast<const uint8_t*>(A.bits);
   const S* vp = static_cast<const S*>(A.V);
   const S* wp = static_cast<const S*>(A.W);
@@ -1037,13 +1182,31 @@ hipError_t bits_launch(const BitsArgs& A, hipStream_t st) {
   const bool rgru = A.mode == 1 && A.rh_da != nullptr && C::WDIR && tg2;
   if (A.fused_gru) *A.fused_gru = gru || rgru;
   if (rgru) op = nullptr;   // dX goes straight into the GRU reverse
-#define GGNN_STEP(WV, TGN, REVB, GRUB)                                                                        \
-  hipLaunchKernelGGL((dev::step_bits_kernel<S, H, B, WV, C::WDIR, TGN, REVB, GRUB>), dim3(blocks),            \
+  // Supernodes ride along only in the two-group direct-weight forms: the
+  // forward with its GRU, the reverse with or without it.
+  const bool sn = A.sn != nullptr;
+  if (sn && !(sizeof(S) == 2 && C::WDIR && C::RPW == dev::kSnFused && tg2 && (A.mode == 1 || gru)))
+    return hipErrorNotSupported;
+  const uint8_t* snb = sn ? static_cast<const uint8_t*>(A.sn->bits) : nullptr;
+  const float* snrec = sn ? A.sn->rec : nullptr;
+  const int sns = sn ? A.sn->s : 0, snr = sn ? A.sn->sr : 0;
+#define GGNN_STEP_SN(WV, TGN, REVB, GRUB, SNB)                                                                \
+  hipLaunchKernelGGL((dev::step_bits_kernel<S, H, B, WV, C::WDIR, TGN, REVB, GRUB, SNB>), dim3(blocks),       \
                      dim3(TGN * WV * 64), 0, st, bp, vp, wp, static_cast<const S*>(A.Wt), A.bias, op, A.n_pad,  \
                      A.E, A.dX_in, dmp, A.ldm,                                                                  \
                      static_cast<const S*>(A.Wi), static_cast<const S*>(A.U), A.bg, static_cast<S*>(A.h_out),  \
                      static_cast<S*>(A.saved), static_cast<const S*>(A.rh_h), static_cast<const S*>(A.rh_saved), \
-                     static_cast<S*>(A.rh_da), A.rh_dh, static_cast<S*>(A.rh_ghat))
+                     static_cast<S*>(A.rh_da), A.rh_dh, static_cast<S*>(A.rh_ghat), snb, snrec, sns, snr)
+#define GGNN_STEP(WV, TGN, REVB, GRUB)                                                                        \
+  do {                                                                                                        \
+    if constexpr (sizeof(S) == 2 && C::WDIR && C::RPW == dev::kSnFused && TGN == 2 && (REVB || GRUB)) {       \
+      if (sn) {                                                                                               \
+        GGNN_STEP_SN(WV, TGN, REVB, GRUB, true);                                                              \
+        break;                                                                                                \
+      }                                                                                                       \
+    }                                                                                                         \
+    GGNN_STEP_SN(WV, TGN, REVB, GRUB, false);                                                                 \
+  } while (0)
 #define GGNN_BITS_CASE(WV)                                                                                   \
   case WV:                                                                                                   \
     if constexpr (B / C::RPW >= WV && WV >= C::MINW && (WV <= 4 || (!C::ALL && H >= 256))) {         \
@@ -1076,6 +1239,7 @@ hipError_t bits_launch(const BitsArgs& A, hipStream_t st) {
   }
 #undef GGNN_BITS_CASE
 #undef GGNN_STEP
+#undef GGNN_STEP_SN
   return hipGetLastError();
 }
 
@@ -1158,6 +1322,69 @@ hipError_t launch_banded_bwd_bits(int n_pad, int B, int H, int E, const void* bi
   return bits_t<dev::dt_t>(H, B, BitsArgs{2, bits_t_, da, nullptr, nullptr, dM, nullptr, nullptr, ldm, n_pad, E},
                            st);
 }
+
+#if GGNN_DT_BF16
+namespace {
+template <int H, int B>
+bool sn_fusable_hb(int n_pad, int E) {
+  using C = dev::BitsCfg<dev::bf16s, H, B>;
+  if constexpr (!C::WDIR || C::RPW != dev::kSnFused) {
+    return false;
+  } else {
+    return bits_plan<dev::bf16s, H, B>(0, n_pad, E).tg2 && bits_plan<dev::bf16s, H, B>(1, n_pad, E).tg2;
+  }
+}
+template <int H>
+bool sn_fusable_h(int B, int n_pad, int E) {
+  switch (B) {
+    case 32: return sn_fusable_hb<H, 32>(n_pad, E);
+    case 64: return sn_fusable_hb<H, 64>(n_pad, E);
+    case 128: return sn_fusable_hb<H, 128>(n_pad, E);
+    case 256: return sn_fusable_hb<H, 256>(n_pad, E);
+    case 512: return sn_fusable_hb<H, 512>(n_pad, E);
+  }
+  return false;
+}
+}  // namespace
+
+bool step_sn_fusable(int n_pad, int B, int H, int E) {
+  switch (H) {
+    case 32: return sn_fusable_h<32>(B, n_pad, E);
+    case 64: return sn_fusable_h<64>(B, n_pad, E);
+  }
+  return false;
+}
+
+hipError_t launch_step_fwd_bits_gru_sn(int n_pad, int B, int H, int E, const void* bits, const void* X, const void* W,
+                                       const void* Wt, const float* bias, float* a, const void* Wi, const void* U,
+                                       const float* bg, void* h_out, void* saved, const SnStep& sn, hipStream_t st) {
+  BitsArgs A{0, bits, X, W, bias, a, nullptr, nullptr, 0, n_pad, E};
+  A.Wt = Wt;
+  A.Wi = Wi;
+  A.U = U;
+  A.bg = bg;
+  A.h_out = h_out;
+  A.saved = saved;
+  A.sn = &sn;
+  return bits_t<dev::bf16s>(H, B, A, st);
+}
+
+hipError_t launch_step_bwd_bits_sn(int n_pad, int B, int H, int E, const void* bits_t_, const void* da,
+                                   const void* W, const float* dX_in, float* dX_out, void* dM, long ldm,
+                                   const void* Wi, const void* U, const void* h_prev, const void* saved_prev,
+                                   void* da_prev, float* dh_prev, void* ghat_prev, const SnStep& sn, hipStream_t st) {
+  BitsArgs A{1, bits_t_, da, W, nullptr, dX_out, dX_in, dM, ldm, n_pad, E};
+  A.Wi = Wi;
+  A.U = U;
+  A.rh_h = h_prev;
+  A.rh_saved = saved_prev;
+  A.rh_da = da_prev;
+  A.rh_dh = dh_prev;
+  A.rh_ghat = ghat_prev;
+  A.sn = &sn;
+  return bits_t<dev::bf16s>(H, B, A, st);
+}
+#endif
 }  // namespace GGNN_IMPL_NS
 
 }  // namespace ggnn

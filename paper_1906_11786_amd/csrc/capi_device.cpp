@@ -358,6 +358,41 @@ static ggnn_status check_model(const ggnn_model* m) {
   if (m->band_format == GGNN_BAND_BITS) CHECK_PTR(m->band_t, "model.band_t");
   CHECK_OPT_PTR(m->Wt, "model.Wt");
   CHECK_OPT_PTR(m->gru_packed, "model.gru_packed");
+  GGNN_CHECK_ARG(m->n_super >= 0, "n_super=%d must not be negative", m->n_super);
+  if (m->n_super > 0) {
+    GGNN_CHECK_ARG(m->band_format == GGNN_BAND_BITS, "supernodes need the bit band");
+    GGNN_CHECK_ARG(ggnn_super_bytes(m->n_pad, m->E, m->n_super) > 0,
+                   "n_super=%d (32, 64, 96 or 128, at most n_pad; n_pad=%d a multiple of 64)", m->n_super, m->n_pad);
+    GGNN_CHECK_ARG(m->n_super_active >= 0 && m->n_super_active <= m->n_super && m->n_super_active % 16 == 0,
+                   "n_super_active=%d must be a multiple of 16 in [0, n_super=%d]", m->n_super_active, m->n_super);
+    if (m->n_super_active > 0) {
+      CHECK_PTR(m->super_rows, "model.super_rows");
+      CHECK_PTR(m->super_cols, "model.super_cols");
+      CHECK_PTR(m->super_rows_t, "model.super_rows_t");
+      CHECK_PTR(m->super_cols_t, "model.super_cols_t");
+    }
+  }
+  return GGNN_OK;
+}
+
+// Supernode slices run inside the fused step kernels (see ggnn_forward).
+static bool super_fused(const ggnn_model* m) {
+  return m->n_super > 0 && (m->n_super_active == 16 || m->n_super_active == 32) && m->dtype == GGNN_BF16 &&
+         m->H <= 64 && impl_bf16::step_sn_fusable(m->n_pad, m->B, m->H, m->E);
+}
+static size_t super_model_ws(const ggnn_model* m) {
+  if (m->n_super <= 0 || m->n_super_active <= 0) return 0;
+  const size_t a = super_workspace(m->n_pad, m->H, m->E, m->n_super);
+  const size_t b = super_fused(m) ? super_fused_workspace(m->n_pad, m->H, m->E) : 0;
+  return a > b ? a : b;
+}
+// The supernode scratch of a model about to run.
+static ggnn_status check_super_ws(const ggnn_model* m) {
+  const size_t need = super_model_ws(m);
+  if (need == 0) return GGNN_OK;
+  if (m->super_ws == nullptr || m->super_ws_bytes < need || !aligned16(m->super_ws))
+    return fail(GGNN_ERR_WORKSPACE, "supernodes need a 16-byte aligned model.super_ws of %zu bytes (got %zu)", need,
+                m->super_ws ? m->super_ws_bytes : (size_t)0);
   return GGNN_OK;
 }
 
@@ -370,6 +405,25 @@ static ggnn_status check_acts(const ggnn_model* m, const ggnn_activations* act) 
   return GGNN_OK;
 }
 
+
+size_t ggnn_super_model_workspace_bytes(const ggnn_model* m) {
+  if (m == nullptr || check_model(m) != GGNN_OK) {
+    clear_error();
+    return 0;
+  }
+  return super_model_ws(m);
+}
+
+int32_t ggnn_super_fusable(ggnn_dtype dt, int32_t n_pad, int32_t B, int32_t H, int32_t E, int32_t n_super_active) {
+  if (check_banded(dt, n_pad, B, H, E) != GGNN_OK) {
+    clear_error();
+    return 0;
+  }
+  return (n_super_active == 16 || n_super_active == 32) && dt == GGNN_BF16 && H <= 64 &&
+                 impl_bf16::step_sn_fusable(n_pad, B, H, E)
+             ? 1
+             : 0;
+}
 
 size_t ggnn_backward_workspace_bytes(const ggnn_model* m) {
   if (m == nullptr || check_model(m) != GGNN_OK) {
@@ -385,10 +439,16 @@ ggnn_status ggnn_forward(const ggnn_model* m, const ggnn_activations* act, void*
   if (st != GGNN_OK) return st;
   st = check_acts(m, act);
   if (st != GGNN_OK) return st;
+  st = check_super_ws(m);
+  if (st != GGNN_OK) return st;
   const size_t es = dtype_bytes(m->dtype);
   const size_t xs = (size_t)m->n_pad * m->H;
   hipStream_t s = as_stream(stream);
   const void* gru_pk = gru_pack_bytes(m->dtype, m->H) ? m->gru_packed : nullptr;
+  const bool sn = m->n_super > 0 && m->n_super_active > 0;
+  const bool snf = sn && super_fused(m);
+  float* sn_rec = static_cast<float*>(m->super_ws);
+  float* sn_scr = snf ? sn_rec + super_fused_record_floats(m->H, m->E) : nullptr;
   for (int t = 0; t < m->T; ++t) {
     const char* Xt = static_cast<const char*>(act->X) + t * xs * es;
     char* Xn = static_cast<char*>(act->X) + (t + 1) * xs * es;
@@ -396,11 +456,34 @@ ggnn_status ggnn_forward(const ggnn_model* m, const ggnn_activations* act, void*
     char* sv = static_cast<char*>(act->saved) + t * 3 * xs * es;
     hipError_t err;
     bool fused = false;   // the bit-band step also ran the GRU update
-    if (m->band_format == GGNN_BAND_BITS) {
+    if (snf) {
+      // supernode rows: R_e X over all nodes; then the fused step with the
+      // column slice as a fourth block
+      prof_begin(s);
+      err = impl_bf16::launch_super_long_fused(m->n_pad, m->H, m->E, m->n_super, m->n_super_active, m->super_rows,
+                                               Xt, false, sn_scr, sn_rec, s);
+      prof_end(s, PROF_SUPER_LONG);
+      if (err == hipSuccess) {
+        prof_begin(s);
+        err = impl_bf16::launch_step_fwd_bits_gru_sn(m->n_pad, m->B, m->H, m->E, m->band, Xt, m->W, m->Wt, m->bias,
+                                                     at, m->Wi, m->U, m->b, Xn, sv,
+                                                     SnStep{m->super_cols, sn_rec, m->n_super, m->n_super_active},
+                                                     s);
+        prof_end(s, PROF_STEP_FWD_GRU);
+        fused = true;
+      }
+    } else if (m->band_format == GGNN_BAND_BITS) {
+      // with stand-alone supernode slices the GRU waits for their share of a
       prof_begin(s);
       err = launch_step_fwd_bits_gru(m->dtype, m->n_pad, m->B, m->H, m->E, m->band, Xt, m->W, m->Wt, m->bias, at,
-                                     m->Wi, m->U, m->b, Xn, sv, &fused, s);
+                                     sn ? nullptr : m->Wi, m->U, m->b, Xn, sv, &fused, s);
       prof_end(s, fused ? PROF_STEP_FWD_GRU : PROF_STEP_FWD);
+      if (err == hipSuccess && sn) {
+        prof_begin(s);
+        err = launch_super_fwd(m->dtype, m->n_pad, m->H, m->E, m->n_super, m->super_rows, m->super_cols, Xt, m->W,
+                               m->bias, at, m->super_ws, s);
+        prof_end(s, PROF_SUPER);
+      }
     } else {
       prof_begin(s);
       err = launch_transform_fwd(m->dtype, m->n_pad, m->H, m->E, Xt, m->W, m->bias, act->M, s);
@@ -437,6 +520,8 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
   CHECK_PTR(gr->dM, "grads.dM");
   CHECK_PTR(gr->dh, "grads.dh");
   if (m->bias) CHECK_PTR(gr->dbias, "grads.dbias");
+  st = check_super_ws(m);
+  if (st != GGNN_OK) return st;
   const BwdLayout L = bwd_layout(m);
   if (gr->workspace == nullptr || gr->workspace_bytes < L.total || !aligned16(gr->workspace))
     return fail(GGNN_ERR_WORKSPACE, "backward needs a 16-byte aligned workspace of %zu bytes (got %zu)", L.total,
@@ -463,6 +548,11 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
     void* da_b[2] = {gr->da, ws + L.da2};
     float* dh_b[2] = {gr->dh, reinterpret_cast<float*>(ws + L.dh2)};
     int cur = 0;
+    const bool sn = m->n_super > 0 && m->n_super_active > 0;
+    const bool snf = sn && super_fused(m);
+    float* sn_rec = static_cast<float*>(m->super_ws);
+    float* sn_scr = snf ? sn_rec + super_fused_record_floats(m->H, m->E) : nullptr;
+
     prof_begin(s);
     hipError_t err = launch_gru_bwd_nodes(m->dtype, m->n_pad, m->H, gr->dX, Xs(m->T - 1), Ss(m->T - 1), m->Wi, m->U,
                                           da_b[0], dh_b[0], Gs(m->T - 1), s, gru_pk);
@@ -470,6 +560,36 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
     if (err != hipSuccess) return device_status(err, "backward");
     for (int t = m->T - 1; t >= 0; --t) {
       char* dMr = static_cast<char*>(gr->dM) + (size_t)t * m->n_pad * m->H * es;   // node-major rows of step t
+      if (snf) {
+        // supernode rows: C_e^T da over all nodes; then the fused reverse step
+        // with the transposed row slice as a fourth block
+        prof_begin(s);
+        err = impl_bf16::launch_super_long_fused(m->n_pad, m->H, m->E, m->n_super, m->n_super_active,
+                                                 m->super_cols_t, da_b[cur], true, sn_scr, sn_rec, s);
+        prof_end(s, PROF_SUPER_LONG);
+        if (err == hipSuccess) {
+          const bool prev = t > 0;
+          prof_begin(s);
+          err = impl_bf16::launch_step_bwd_bits_sn(
+              m->n_pad, m->B, m->H, m->E, m->band_t, da_b[cur], m->W, dh_b[cur], gr->dX, dMr, K, m->Wi, m->U,
+              prev ? Xs(t - 1) : nullptr, prev ? Ss(t - 1) : nullptr, prev ? da_b[1 - cur] : nullptr,
+              prev ? dh_b[1 - cur] : nullptr, prev ? Gs(t - 1) : nullptr,
+              SnStep{m->super_rows_t, sn_rec, m->n_super, m->n_super_active}, s);
+          prof_end(s, prev ? PROF_STEP_REV_GRU : PROF_STEP_REV);
+        }
+        if (err != hipSuccess) return device_status(err, "backward");
+        cur ^= 1;
+        continue;
+      }
+      if (sn) {
+        // stand-alone slices: their share of dX goes into dh (the step's
+        // dX_in), of dW and dbias straight into the gradients
+        prof_begin(s);
+        err = launch_super_bwd(m->dtype, m->n_pad, m->H, m->E, m->n_super, m->super_rows, m->super_rows_t,
+                               m->super_cols_t, Xs(t), m->W, da_b[cur], dh_b[cur], gr->dW, dbias, m->super_ws, s);
+        prof_end(s, PROF_SUPER);
+        if (err != hipSuccess) return device_status(err, "backward");
+      }
       if (t > 0) {
         bool fused = false;
         prof_begin(s);

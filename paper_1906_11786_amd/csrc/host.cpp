@@ -473,4 +473,34 @@ ggnn_status ggnn_super_pack(int32_t n_pad, int32_t E, int32_t s, int64_t m, cons
   return GGNN_OK;
 }
 
+int32_t ggnn_super_active(int32_t n_pad, int32_t E, int32_t s, const void* rows, const void* cols) {
+  clear_error();
+  if (ggnn_super_bytes(n_pad, E, s) == 0) {
+    fail(GGNN_ERR_INVALID_ARG, "n_pad=%d (a positive multiple of 64), E=%d (1..64), s=%d (32, 64, 96 or 128, <= n_pad)",
+         n_pad, E, s);
+    return -1;
+  }
+  if (rows == nullptr || cols == nullptr) {
+    fail(GGNN_ERR_INVALID_ARG, "rows/cols is NULL");
+    return -1;
+  }
+  const uint8_t* R = static_cast<const uint8_t*>(rows);
+  const uint8_t* Cc = static_cast<const uint8_t*>(cols);
+  const size_t wide = static_cast<size_t>(n_pad / 8), narrow = static_cast<size_t>(s / 8);
+  int top = -1;   // largest supernode index with an edge
+  for (int e = 0; e < E; ++e)
+    for (int i = s - 1; i > top; --i) {
+      const uint8_t* row = R + (static_cast<size_t>(e) * s + i) * wide;
+      bool any = false;
+      for (size_t b = 0; b < wide && !any; ++b) any = row[b] != 0;
+      if (any) top = i;
+    }
+  uint8_t orb[16] = {0};   // s / 8 <= 16 bytes: the union of every row of the column slice
+  for (size_t r = 0; r < static_cast<size_t>(E) * n_pad; ++r)
+    for (size_t b = 0; b < narrow; ++b) orb[b] |= Cc[r * narrow + b];
+  for (int j = 0; j < s; ++j)
+    if ((orb[j / 8] >> (j % 8)) & 1u) top = j > top ? j : top;
+  return top < 0 ? 0 : (top / 16 + 1) * 16;
+}
+
 }  // extern "C"

@@ -38,6 +38,19 @@ hipError_t launch_transform_wgrad_nm256(int nsplit, int rows_per_split, long K, 
 hipError_t reduce_or_defer(const float* part, float* out, int nsplit, int count, long stride, ReduceList* defer,
                            hipStream_t st);
 
+// Supernode share of a fused bit-band step (the first 32 nodes are
+// supernodes): the slice bits of the step's direction, [E][n_pad][s/8] (the
+// column slice forward, the transposed row slice reverse), and the record
+// [P_e (sr x H) | deg_e (sr)] of the long contraction over all nodes that
+// gives the first sr supernode rows their per-type aggregate
+// (launch_super_long_fused).
+struct SnStep {
+  const void* bits;
+  const float* rec;
+  int s;
+  int sr;   // record rows: the supernodes with edges are among the first sr (16 or 32)
+};
+
 #define GGNN_DT_LAUNCHERS                                                                                         \
   hipError_t launch_banded_fwd(int n_pad, int B, int H, int E, const void* band, const float* M, float* a,        \
                                hipStream_t st);                                                                   \
@@ -96,6 +109,23 @@ hipError_t reduce_or_defer(const float* part, float* out, int nsplit, int count,
 
 namespace impl_bf16 {
 GGNN_DT_LAUNCHERS
+// Fused supernode steps (bf16, H <= 64, grids small enough for the
+// two-group forms): whether both fused steps take the supernode share at
+// this size, and the forward step (with its GRU) and reverse step (with the
+// previous step's GRU reverse when da_prev is not NULL) carrying it.
+bool step_sn_fusable(int n_pad, int B, int H, int E);
+// The long contraction of the fused supernode steps: rec = [P_e (sr x H) |
+// deg_e (sr)], P_e = bits_e Z over all nodes for the first sr slice rows
+// (zfm: Z feature-major); ws holds the per-chunk partials.
+hipError_t launch_super_long_fused(int n_pad, int H, int E, int s, int sr, const void* bits, const void* Z, bool zfm,
+                                   float* ws, float* rec, hipStream_t st);
+hipError_t launch_step_fwd_bits_gru_sn(int n_pad, int B, int H, int E, const void* bits, const void* X, const void* W,
+                                       const void* Wt, const float* bias, float* a, const void* Wi, const void* U,
+                                       const float* bg, void* h_out, void* saved, const SnStep& sn, hipStream_t st);
+hipError_t launch_step_bwd_bits_sn(int n_pad, int B, int H, int E, const void* bits_t, const void* da,
+                                   const void* W, const float* dX_in, float* dX_out, void* dM, long ldm,
+                                   const void* Wi, const void* U, const void* h_prev, const void* saved_prev,
+                                   void* da_prev, float* dh_prev, void* ghat_prev, const SnStep& sn, hipStream_t st);
 }
 namespace impl_f32 {
 GGNN_DT_LAUNCHERS
@@ -265,6 +295,11 @@ inline hipError_t launch_sparse_step(int dt, int n_pad, int H, int E, const int3
 // Supernode slices (first s rows and columns), forward (a +=) and reverse
 // (dX, dW, dbias +=); workspace of super_workspace bytes.
 size_t super_workspace(int n_pad, int H, int E, int s);
+// Workspace of the fused supernode steps (bf16, H = 32 or 64): the record
+// (super_fused_record_floats floats, room for [P_e (32 x H) | deg_e (32)]),
+// then the scratch of launch_super_long_fused (the per-chunk partials).
+size_t super_fused_workspace(int n_pad, int H, int E);
+size_t super_fused_record_floats(int H, int E);
 inline hipError_t launch_super_fwd(int dt, int n_pad, int H, int E, int s, const void* rows, const void* cols,
                                    const void* X, const void* W, const float* bias, float* a, void* ws,
                                    hipStream_t st) {

@@ -40,85 +40,170 @@ template <> __device__ __forceinline__ f32x8 sn_bits_frag<float>(uint32_t byte) 
   return r;
 }
 
-constexpr int kSnKC = 64;   // nodes staged per sub-chunk of the long contraction
-
 // LDS row pitch (elements) of node-major staging read with transposing
 // reads: 2P bytes = 160 mod 256 puts the four rows of one read on disjoint
 // banks.
 template <typename S, int H> constexpr int sn_pitch() {
   return sizeof(S) == 2 ? H + ((80 - H) % 128 + 128) % 128 : H + 4;
 }
+// Nodes per chunk of the long contraction: the whole chunk of Z is staged in
+// LDS at once (at most 96 KB), a multiple of 64 nodes.
+template <typename S, int H, bool ZFM> constexpr int sn_chunk_nodes() {
+  constexpr int per = ZFM ? 98304 / (H * (int)sizeof(S)) - 16 : 98304 / (sn_pitch<S, H>() * (int)sizeof(S));
+  constexpr int c = per / 64 * 64;
+  return c > 576 ? 576 : c;
+}
 
-// Long contraction over the nodes of one chunk:
-//   part[c][e][i][h] = sum_{j in chunk c} bits[e][i][j] Z(j, h),  i < s.
+// Long contraction over the nodes of one chunk, for the active supernode
+// rows i < sa and the edge types of one group:
+//   part[c][e][i][h] = sum_{j in chunk c} bits[e][i][j] Z(j, h)
+//   part[c][E sa H + e sa + i] = number of those bits set (row degree)
 // bits [E][s][n_pad/8] (row i, bit j).  Z node-major [n_pad][H] (ZFM =
 // false) or feature-major [H][n_pad] (ZFM = true), storage type S.
-// Workgroup (4 waves): one chunk and one edge type; wave w owns the row
-// tiles w, w + 4 (s <= 128) and every feature tile.
+// Workgroup (4 waves): chunk c, types [e0, e1); the chunk of Z is staged in
+// LDS once (all of a thread's loads issued before its writes, one memory
+// latency), then every (type, 16-row tile) pair of the group goes to a wave;
+// a wave loads its rows' bit bytes for the whole chunk in one go (the first
+// pair's before the staging) and skips every 32-node k step where none of
+// its 16 rows has an edge (wave-uniform test).
 template <typename S, int H, bool ZFM>
-__global__ __launch_bounds__(256) void super_rows_kernel(const uint8_t* __restrict__ bits, const S* __restrict__ Z,
-                                                         float* __restrict__ part, int n_pad, int E, int s,
-                                                         int chunk) {
-  constexpr int MT = H / 16, P = sn_pitch<S, H>(), PF = kSnKC + 16 / (int)sizeof(S);
-  constexpr int V = 16 / sizeof(S);
-  __shared__ __attribute__((aligned(16))) S zs[ZFM ? H * PF : kSnKC * P];
-  const int c = blockIdx.x / E, e = blockIdx.x % E;
+__global__ __launch_bounds__(256) void super_long_kernel(const uint8_t* __restrict__ bits, const S* __restrict__ Z,
+                                                         float* __restrict__ part, long pstride, int n_pad, int E,
+                                                         int s, int sa, int chunk, int tpg) {
+  constexpr int MT = H / 16, CN = sn_chunk_nodes<S, H, ZFM>(), V = 16 / (int)sizeof(S);
+  constexpr int P = sn_pitch<S, H>(), PF = CN + 16 / (int)sizeof(S);
+  constexpr int NKS = CN / 32;   // k steps (and bit dwords per row) of a full chunk
+  __shared__ __attribute__((aligned(16))) S zs[ZFM ? H * PF : CN * P];
+  const int ntg = (E + tpg - 1) / tpg;
+  // the type groups of one chunk on one XCD (they stage the same rows)
+  const int lid = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int c = lid / ntg, tgi = lid % ntg;
+  const int e0 = tgi * tpg, e1 = min(E, e0 + tpg);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int q = lane % 16, g = lane / 16;
-  const int nrt = s / 16;
-  const int j_lo = c * chunk, j_hi = min(n_pad, j_lo + chunk);
+  const int j_lo = c * chunk, len = min(n_pad - j_lo, chunk);   // a multiple of 64
+  const int nks = len / 32;
   const size_t rowb = (size_t)n_pad / 8;
-  f32x4 acc[2][MT];
+  const int nrt = sa / 16;
+  const int npairs = (e1 - e0) * nrt;
+  // this lane's bit row of pair pr, whole chunk: dword ks holds the bytes of
+  // k step ks for the four lane groups (byte g: nodes 32 ks + 8 g .. + 7)
+  uint32_t bw[NKS];
+  auto load_bits = [&](int pr) __attribute__((always_inline)) {
+    const int e = e0 + pr / nrt, rt = pr % nrt;
+    const uint8_t* brow = bits + ((size_t)e * s + 16 * rt + q) * rowb + j_lo / 8;
 #pragma unroll
-  for (int r = 0; r < 2; ++r)
-#pragma unroll
-    for (int m = 0; m < MT; ++m) acc[r][m] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int j0 = j_lo; j0 < j_hi; j0 += kSnKC) {
-    __syncthreads();   // the previous sub-chunk is fully read
-    if constexpr (!ZFM) {
-      for (int u = tid; u < kSnKC * (H / V); u += 256) {
-        const int k = u / (H / V), h = (u % (H / V)) * V;
-        *reinterpret_cast<u32x4*>(&zs[k * P + h]) = *reinterpret_cast<const u32x4*>(Z + (size_t)(j0 + k) * H + h);
-      }
-    } else {
-      for (int u = tid; u < H * (kSnKC / V); u += 256) {
-        const int h = u / (kSnKC / V), k = (u % (kSnKC / V)) * V;
-        *reinterpret_cast<u32x4*>(&zs[h * PF + k]) = *reinterpret_cast<const u32x4*>(Z + (size_t)h * n_pad + j0 + k);
+    for (int d = 0; d < NKS; d += 2) {
+      if (d < nks) {
+        const u32x2 v = *reinterpret_cast<const u32x2*>(brow + 4 * d);
+        bw[d] = v[0];
+        bw[d + 1] = v[1];
+      } else {
+        bw[d] = 0u;
+        bw[d + 1] = 0u;
       }
     }
-    __syncthreads();
+  };
+  if (wave < npairs) load_bits(wave);
+  // stage the chunk: every 16-byte unit of a thread in flight at once
+  {
+    constexpr int UPT = ((ZFM ? H * (CN / V) : CN * (H / V)) + 255) / 256;
+    const int units = ZFM ? H * (len / V) : len * (H / V);
+    u32x4 r[UPT];
 #pragma unroll
-    for (int kk = 0; kk < kSnKC / 32; ++kk) {
-      frag_t<S> bf[2];
-#pragma unroll
-      for (int r = 0; r < 2; ++r) {
-        const int rt = wave + 4 * r;
-        const uint32_t byte =
-            rt < nrt ? bits[((size_t)e * s + 16 * rt + q) * rowb + (j0 + 32 * kk) / 8 + g] : 0u;
-        bf[r] = sn_bits_frag<S>(byte);
+    for (int u = 0; u < UPT; ++u) {
+      const int lin = u * 256 + tid;
+      if (lin < units) {
+        if constexpr (ZFM) {
+          const int h = lin / (len / V), k = (lin % (len / V)) * V;
+          r[u] = *reinterpret_cast<const u32x4*>(Z + (size_t)h * n_pad + j_lo + k);
+        } else {
+          const int k = lin / (H / V), h = (lin % (H / V)) * V;
+          r[u] = *reinterpret_cast<const u32x4*>(Z + (size_t)(j_lo + k) * H + h);
+        }
       }
+    }
+#pragma unroll
+    for (int u = 0; u < UPT; ++u) {
+      const int lin = u * 256 + tid;
+      if (lin < units) {
+        if constexpr (ZFM) {
+          const int h = lin / (len / V), k = (lin % (len / V)) * V;
+          *reinterpret_cast<u32x4*>(&zs[h * PF + k]) = r[u];
+        } else {
+          const int k = lin / (H / V), h = (lin % (H / V)) * V;
+          *reinterpret_cast<u32x4*>(&zs[k * P + h]) = r[u];
+        }
+      }
+    }
+  }
+  __syncthreads();
+  for (int pr = wave; pr < npairs; pr += 4) {
+    const int e = e0 + pr / nrt, rt = pr % nrt;
+    if (pr != wave) load_bits(pr);
+    f32x4 acc[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+    int deg = 0;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) {
+      const uint32_t byte = (bw[ks] >> (8 * g)) & 0xFFu;
+      if (__builtin_amdgcn_ballot_w64(byte != 0u) == 0) continue;
+      deg += __popc(byte);
+      const frag_t<S> bf = sn_bits_frag<S>(byte);
 #pragma unroll
       for (int m = 0; m < MT; ++m) {
         frag_t<S> af;
         if constexpr (!ZFM) {
-          af = tr_frag(zs, P, 32 * kk, 16 * m, lane);
+          af = tr_frag(zs, P, 32 * ks, 16 * m, lane);
         } else {
-          af = load8(&zs[(16 * m + q) * PF + 32 * kk + 8 * g]);
+          af = load8(&zs[(16 * m + q) * PF + 32 * ks + 8 * g]);
         }
-#pragma unroll
-        for (int r = 0; r < 2; ++r)
-          if (wave + 4 * r < nrt) mma(acc[r][m], af, bf[r]);
+        mma(acc[m], af, bf);
       }
     }
+    // D[feature 16m + 4g + j][row 16 rt + q]
+    float* o = part + (size_t)c * pstride + ((size_t)e * sa + 16 * rt + q) * H + 4 * g;
+#pragma unroll
+    for (int m = 0; m < MT; ++m) *reinterpret_cast<f32x4*>(o + 16 * m) = acc[m];
+    deg += __shfl_xor(deg, 16);
+    deg += __shfl_xor(deg, 32);
+    if (g == 0) part[(size_t)c * pstride + (size_t)E * sa * H + (size_t)e * sa + 16 * rt + q] = static_cast<float>(deg);
   }
-  // D[feature 16m + 4g + j][row 16 rt + q]
+}
+
+// out[i] = sum_{c < nch} part[c * stride + i] for i < count (a multiple of
+// four).  A workgroup of 64 x 16 threads owns 256 consecutive outputs:
+// thread (x, y) sums, for its four outputs, the chunks c = y, y + 16, ... in
+// increasing order (all its loads in flight), then thread (x, 0) adds the 16
+// sums in order y = 0..15.  The order depends only on nch: results do not
+// depend on scheduling.
+constexpr int kSnRW = 16;
+static __global__ __launch_bounds__(64 * kSnRW) void sn_reduce_kernel(const float* __restrict__ part,
+                                                                      float* __restrict__ out, int nch, int count,
+                                                                      long stride) {
+  __shared__ f32x4 red[kSnRW][64];
+  const int x = threadIdx.x % 64, y = threadIdx.x / 64;
+  const int i = 4 * (blockIdx.x * 64 + x);
+  f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (i < count) {
+    int c = y;
+    for (; c + 3 * kSnRW < nch; c += 4 * kSnRW) {
+      f32x4 v[4];
 #pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    const int rt = wave + 4 * r;
-    if (rt >= nrt) continue;
-    float* o = part + (((size_t)c * E + e) * s + 16 * rt + q) * H + 4 * g;
+      for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const f32x4*>(part + (size_t)(c + u * kSnRW) * stride + i);
 #pragma unroll
-    for (int m = 0; m < MT; ++m) *reinterpret_cast<f32x4*>(o + 16 * m) = acc[r][m];
+      for (int u = 0; u < 4; ++u) s += v[u];
+    }
+    for (; c < nch; c += kSnRW) s += *reinterpret_cast<const f32x4*>(part + (size_t)c * stride + i);
+  }
+  red[y][x] = s;
+  __syncthreads();
+  if (y == 0 && i < count) {
+    f32x4 t = red[0][x];
+#pragma unroll
+    for (int w = 1; w < kSnRW; ++w) t += red[w][x];
+    *reinterpret_cast<f32x4*>(out + i) = t;
   }
 }
 
@@ -182,26 +267,6 @@ __global__ __launch_bounds__(256) void super_cols_kernel(const uint8_t* __restri
     const f32x4 b = *reinterpret_cast<const f32x4*>(o);
     *reinterpret_cast<f32x4*>(o) = f32x4{b[0] + acc[m][0], b[1] + acc[m][1], b[2] + acc[m][2], b[3] + acc[m][3]};
   }
-}
-
-// Row degrees of the row slice: deg[e][i] = number of bits set in row i
-// (one instance per storage-type build).
-template <typename S>
-__global__ __launch_bounds__(256) void super_deg_kernel(const uint8_t* __restrict__ bits, float* __restrict__ deg,
-                                                        int n_pad, int rows) {
-  const int r = blockIdx.x;
-  const size_t rowb = (size_t)n_pad / 8;
-  int c = 0;
-  for (size_t w = threadIdx.x; w < rowb / 4; w += 256)
-    c += __popc(reinterpret_cast<const uint32_t*>(bits + (size_t)r * rowb)[w]);
-  __shared__ int red[256];
-  red[threadIdx.x] = c;
-  __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) {
-    if ((int)threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0 && r < rows) deg[r] = static_cast<float>(red[0]);
 }
 
 // Small dense products on the vector ALUs, one thread per output element:
@@ -268,62 +333,83 @@ hipError_t small_gemm(const SmallGemm& p, hipStream_t st) {
   return hipGetLastError();
 }
 
-// Row-slice chunking: about 256 workgroups over chunks x types, chunks a
-// multiple of the staging sub-chunk.
-int sn_chunk(int n_pad, int E) {
-  const long want = (256 + E - 1) / E;
-  long ch = ((n_pad + want - 1) / want + dev::kSnKC - 1) / dev::kSnKC * dev::kSnKC;
-  return (int)(ch < dev::kSnKC ? dev::kSnKC : ch);
+// Long contraction plan: chunks of the LDS capacity, and edge-type groups so
+// that the grid has about 256 workgroups.  Partial and result records hold
+// E sa H products then E sa row degrees.
+struct SnLong {
+  int chunk, nch, tpg;
+  long pstride;   // floats per record (a multiple of 64)
+  int count;      // floats used per record
+};
+template <typename S, int H, bool ZFM>
+SnLong sn_long_plan(int n_pad, int E, int sa) {
+  constexpr int CN = dev::sn_chunk_nodes<S, H, ZFM>();
+  SnLong p;
+  p.chunk = CN;
+  p.nch = (n_pad + CN - 1) / CN;
+  // type groups: about 256 workgroups, and at least one (type, row tile)
+  // pair for each of the four waves where the types allow
+  const int want = (256 + p.nch - 1) / p.nch;
+  int ntg = want < 1 ? 1 : (want > E ? E : want);
+  const int nrt = sa / 16, tpg4 = (4 + nrt - 1) / nrt;
+  if ((E + ntg - 1) / ntg < tpg4) ntg = (E + tpg4 - 1) / tpg4;
+  p.tpg = (E + ntg - 1) / ntg;
+  p.count = E * sa * (H + 1);
+  p.pstride = ((long)p.count + 63) / 64 * 64;
+  return p;
+}
+// Partial records needed by either long contraction (node-major or
+// feature-major Z) of this size.
+template <typename S, int H>
+size_t sn_long_part_floats(int n_pad, int E, int sa) {
+  const SnLong a = sn_long_plan<S, H, false>(n_pad, E, sa), b = sn_long_plan<S, H, true>(n_pad, E, sa);
+  const int nch = a.nch > b.nch ? a.nch : b.nch;
+  return nch > 1 ? (size_t)nch * a.pstride : 0;
 }
 
-// Workspace (floats): row-slice partials [nch][E][s][H], then three [E][s][H]
-// buffers (P, the second product, the third) and deg [E][s].
+// out = [P_e (sa x H) for every e | deg_e (sa) for every e], P_e = (bits_e Z)
+// over all nodes, for the first sa rows of the slice.
+template <typename S, int H, bool ZFM>
+hipError_t super_long(const uint8_t* bits, const S* Z, float* part, float* out, int n_pad, int E, int s, int sa,
+                      hipStream_t st) {
+  const SnLong p = sn_long_plan<S, H, ZFM>(n_pad, E, sa);
+  const int ntg = (E + p.tpg - 1) / p.tpg;
+  float* dst = p.nch == 1 ? out : part;
+  hipLaunchKernelGGL((dev::super_long_kernel<S, H, ZFM>), dim3(p.nch * ntg), dim3(256), 0, st, bits, Z, dst,
+                     p.pstride, n_pad, E, s, sa, p.chunk, p.tpg);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || p.nch == 1) return err;
+  hipLaunchKernelGGL(dev::sn_reduce_kernel, dim3((p.count / 4 + 63) / 64), dim3(64 * dev::kSnRW), 0, st, part, out,
+                     p.nch, p.count, p.pstride);
+  return hipGetLastError();
+}
+
+// Workspace (floats) of the stand-alone slice calls: long-contraction
+// partials, then the records P (R_e X, deg_R), dP (E s H) and dM_s (C_e^T da).
 struct SnLayout {
-  size_t part, p0, p1, p2, deg, total;
-  int nch, chunk;
+  size_t part, p0, p1, p2, total;
 };
-SnLayout sn_layout(int n_pad, int H, int E, int s) {
+template <typename S, int H>
+SnLayout sn_layout(int n_pad, int E, int s) {
   auto up = [](size_t x) { return (x + 63) / 64 * 64; };
   SnLayout l;
-  l.chunk = sn_chunk(n_pad, E);
-  l.nch = (n_pad + l.chunk - 1) / l.chunk;
-  const size_t esh = (size_t)E * s * H;
+  const size_t rec = (size_t)sn_long_plan<S, H, false>(n_pad, E, s).pstride;
   l.part = 0;
-  l.p0 = up((size_t)l.nch * esh);
-  l.p1 = l.p0 + up(esh);
-  l.p2 = l.p1 + up(esh);
-  l.deg = l.p2 + up(esh);
-  l.total = (l.deg + up((size_t)E * s)) * sizeof(float);
+  l.p0 = up(sn_long_part_floats<S, H>(n_pad, E, s));
+  l.p1 = l.p0 + rec;
+  l.p2 = l.p1 + up((size_t)E * s * H);
+  l.total = (l.p2 + rec) * sizeof(float);
   return l;
-}
-
-template <typename S, int H>
-hipError_t rows_product(const uint8_t* bits, const S* Z, bool zfm, float* out, float* part, const SnLayout& L,
-                        int n_pad, int E, int s, hipStream_t st) {
-  if (zfm)
-    hipLaunchKernelGGL((dev::super_rows_kernel<S, H, true>), dim3(L.nch * E), dim3(256), 0, st, bits, Z, part, n_pad,
-                       E, s, L.chunk);
-  else
-    hipLaunchKernelGGL((dev::super_rows_kernel<S, H, false>), dim3(L.nch * E), dim3(256), 0, st, bits, Z, part,
-                       n_pad, E, s, L.chunk);
-  hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
-  const long cnt = (long)E * s * H;
-  err = launch_fill_zero(out, (size_t)cnt, st);
-  if (err != hipSuccess) return err;
-  return launch_reduce_partials(part, out, L.nch, (int)cnt, cnt, st);
 }
 
 template <typename S, int H>
 hipError_t super_fwd_h(int n_pad, int E, int s, const uint8_t* rows, const uint8_t* cols, const S* X, const S* W,
                        const float* bias, float* a, float* ws, hipStream_t st) {
-  const SnLayout L = sn_layout(n_pad, H, E, s);
-  float *P = ws + L.p0, *Ms = ws + L.p1, *deg = ws + L.deg;
+  const SnLayout L = sn_layout<S, H>(n_pad, E, s);
+  float *P = ws + L.p0, *Ms = ws + L.p1, *deg = P + (size_t)E * s * H;
   // P_e = R_e X, deg_R
-  hipError_t err = rows_product<S, H>(rows, X, false, P, ws + L.part, L, n_pad, E, s, st);
+  hipError_t err = super_long<S, H, false>(rows, X, ws + L.part, P, n_pad, E, s, s, st);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL((dev::super_deg_kernel<S>), dim3(E * s), dim3(256), 0, st, rows, deg, n_pad, E * s);
-  if ((err = hipGetLastError()) != hipSuccess) return err;
   // a[0:s] += sum_e P_e W_e + deg_R,e b_e
   SmallGemm g1{s, H, H, E, 1, 1, P, (long)s * H, H, 1, W, (long)H * H, H, 1, a, 0, H, 1, bias, deg};
   if ((err = small_gemm<float, S>(g1, st)) != hipSuccess) return err;
@@ -338,15 +424,13 @@ template <typename S, int H>
 hipError_t super_bwd_h(int n_pad, int E, int s, const uint8_t* rows, const uint8_t* rows_t, const uint8_t* cols_t,
                        const S* X, const S* W, const S* da, float* dX, float* dW, float* dbias, float* ws,
                        hipStream_t st) {
-  const SnLayout L = sn_layout(n_pad, H, E, s);
-  float *P = ws + L.p0, *dP = ws + L.p1, *dMs = ws + L.p2, *deg = ws + L.deg;
+  const SnLayout L = sn_layout<S, H>(n_pad, E, s);
+  float *P = ws + L.p0, *dP = ws + L.p1, *dMs = ws + L.p2, *deg = P + (size_t)E * s * H;
   const long np = n_pad;
   // recompute P_e = R_e X and deg_R; dM_s,e = C_e^T da
-  hipError_t err = rows_product<S, H>(rows, X, false, P, ws + L.part, L, n_pad, E, s, st);
+  hipError_t err = super_long<S, H, false>(rows, X, ws + L.part, P, n_pad, E, s, s, st);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL((dev::super_deg_kernel<S>), dim3(E * s), dim3(256), 0, st, rows, deg, n_pad, E * s);
-  if ((err = hipGetLastError()) != hipSuccess) return err;
-  if ((err = rows_product<S, H>(cols_t, da, true, dMs, ws + L.part, L, n_pad, E, s, st)) != hipSuccess) return err;
+  if ((err = super_long<S, H, true>(cols_t, da, ws + L.part, dMs, n_pad, E, s, s, st)) != hipSuccess) return err;
   // dP_e = da_s W_e^T  (da feature-major: element (i, h) at h * n_pad + i)
   SmallGemm g1{s, H, H, E, 0, 0, da, 0, 1, np, W, (long)H * H, 1, H, dP, (long)s * H, H, 1, nullptr, nullptr};
   if ((err = small_gemm<S, S>(g1, st)) != hipSuccess) return err;
@@ -386,6 +470,26 @@ hipError_t launch_super_fwd(int n_pad, int H, int E, int s, const void* rows, co
   return hipErrorInvalidValue;
 }
 
+#if GGNN_DT_BF16
+// The long contraction of the fused supernode steps (bf16, H = 32 or 64):
+// rec = [P_e (sr x H) | deg_e (sr)] for the first sr rows of the slice, the
+// per-chunk partials in ws.
+hipError_t launch_super_long_fused(int n_pad, int H, int E, int s, int sr, const void* bits, const void* Z, bool zfm,
+                                   float* ws, float* rec, hipStream_t st) {
+  if (sr != 16 && sr != 32) return hipErrorInvalidValue;
+  const uint8_t* b = static_cast<const uint8_t*>(bits);
+  const dev::bf16s* z = static_cast<const dev::bf16s*>(Z);
+  using S = dev::bf16s;
+  if (H == 32)
+    return zfm ? super_long<S, 32, true>(b, z, ws, rec, n_pad, E, s, sr, st)
+               : super_long<S, 32, false>(b, z, ws, rec, n_pad, E, s, sr, st);
+  if (H == 64)
+    return zfm ? super_long<S, 64, true>(b, z, ws, rec, n_pad, E, s, sr, st)
+               : super_long<S, 64, false>(b, z, ws, rec, n_pad, E, s, sr, st);
+  return hipErrorInvalidValue;
+}
+#endif
+
 hipError_t launch_super_bwd(int n_pad, int H, int E, int s, const void* rows, const void* rows_t,
                             const void* cols_t, const void* X, const void* W, const void* da, float* dX, float* dW,
                             float* dbias, void* ws, hipStream_t st) {
@@ -405,7 +509,38 @@ hipError_t launch_super_bwd(int n_pad, int H, int E, int s, const void* rows, co
 }  // namespace GGNN_IMPL_NS
 
 #if GGNN_DT_BF16
-size_t super_workspace(int n_pad, int H, int E, int s) { return sn_layout(n_pad, H, E, s).total; }
+namespace {
+template <int H>
+size_t super_ws_h(int n_pad, int E, int s) {
+  const size_t a = sn_layout<dev::bf16s, H>(n_pad, E, s).total, b = sn_layout<float, H>(n_pad, E, s).total;
+  return a > b ? a : b;
+}
+// Fused form: the record (super_fused_record_floats, room for 32 rows a
+// type), then the long contraction's partials.
+template <int H>
+size_t super_fused_ws_h(int n_pad, int E) {
+  return (((size_t)E * 32 * (H + 1) + 63) / 64 * 64 + sn_long_part_floats<dev::bf16s, H>(n_pad, E, 32)) *
+         sizeof(float);
+}
+}  // namespace
+
+size_t super_workspace(int n_pad, int H, int E, int s) {
+  switch (H) {
+    case 32: return super_ws_h<32>(n_pad, E, s);
+    case 64: return super_ws_h<64>(n_pad, E, s);
+    case 128: return super_ws_h<128>(n_pad, E, s);
+    case 256: return super_ws_h<256>(n_pad, E, s);
+  }
+  return 0;
+}
+size_t super_fused_record_floats(int H, int E) { return ((size_t)E * 32 * (H + 1) + 63) / 64 * 64; }
+size_t super_fused_workspace(int n_pad, int H, int E) {
+  switch (H) {
+    case 32: return super_fused_ws_h<32>(n_pad, E);
+    case 64: return super_fused_ws_h<64>(n_pad, E);
+  }
+  return 0;
+}
 #endif
 
 }  // namespace ggnn

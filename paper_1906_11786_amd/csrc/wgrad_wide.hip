@@ -27,6 +27,7 @@
 // so every chunk is whole.
 #include "device_common.h"
 #include "kernels.h"
+#include "lds_dma.h"
 
 namespace ggnn {
 namespace dev {
@@ -52,20 +53,6 @@ __device__ __forceinline__ bf16x8 frag(const bf16s* base, int k0, int n0, int la
   typedef short v8i16 __attribute__((ext_vector_type(8)));
   const v8i16 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   return __builtin_bit_cast(bf16x8, v);
-}
-
-// One wave-wide 1 KB copy: lane l's 16 bytes at gsrc go to LDS byte address
-// lds + 16 l (lds wave-uniform).  M0 holds the LDS base; one wait state
-// between writing M0 and the load that uses it.
-__device__ __forceinline__ void dma16(const void* gsrc, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(gsrc)
-               : "memory", "m0");
-}
-// Wait until at most N of this wave's copies are outstanding (vmcnt only).
-template <int N>
-__device__ __forceinline__ void wait_copies() {
-  static_assert(N >= 0 && N < 16, "vmcnt field");
-  __builtin_amdgcn_s_waitcnt(0xF70 | N);
 }
 
 __global__ __launch_bounds__(NT) void transform_wgrad_nm256_kernel(const bf16s* __restrict__ X,

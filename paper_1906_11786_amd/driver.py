@@ -127,11 +127,27 @@ class BandedGGNN:
         td = torch_dtype(dt)
         t0 = time.perf_counter()
         self.band_t = None
+        # Supernodes (compile_with_supernodes): edges touching nodes 0..s-1
+        # go to the dense slices, the others to the band.
+        s_sn = int(comp.stats.get("n_super", 0))
+        self.n_super, self.n_super_active = s_sn, 0
+        if s_sn and band_format != "bits":
+            raise ValueError("supernodes need the bit band")
         if band_format == "bits":
-            bits, bits_t, packed, dropped, dup = capi.ggnn_banded_pack_bits(n_pad, E, B, comp.src, comp.dst,
-                                                                            comp.etype, strict=strict)
+            keep = slice(None) if not s_sn else (comp.src >= s_sn) & (comp.dst >= s_sn)
+            bits, bits_t, packed, dropped, dup = capi.ggnn_banded_pack_bits(n_pad, E, B, comp.src[keep],
+                                                                            comp.dst[keep], comp.etype[keep],
+                                                                            strict=strict)
             comp.stats.update(n_packed=packed, n_dropped=dropped, n_duplicate=dup,
                               pack_seconds=time.perf_counter() - t0)
+            if s_sn:
+                rows, cols, rows_t, cols_t, cnt = capi.ggnn_super_pack(n_pad, E, s_sn, comp.src, comp.dst,
+                                                                       comp.etype)
+                self.n_super_active = capi.ggnn_super_active(n_pad, E, s_sn, rows, cols)
+                comp.stats.update(n_duplicate=dup + cnt["duplicates"], n_super_rows=cnt["rows"],
+                                  n_super_cols=cnt["cols"], n_super_active=self.n_super_active)
+                self.super_slices = [torch.from_numpy(np.ascontiguousarray(x)).to(device)
+                                     for x in (rows, cols, rows_t, cols_t)]
             t0 = time.perf_counter()
             self.band = torch.from_numpy(bits).to(device)
             self.band_t = torch.from_numpy(bits_t).to(device)
@@ -189,6 +205,14 @@ class BandedGGNN:
             U=self.U.data_ptr(), b=self.b.data_ptr(), band_format=capi.BAND_FORMATS[band_format],
             band_t=None if self.band_t is None else self.band_t.data_ptr(), Wt=self.Wt.data_ptr(),
             gru_packed=None if self.gru_packed is None else self.gru_packed.data_ptr())
+        if s_sn:
+            m = self.model
+            m.n_super, m.n_super_active = s_sn, self.n_super_active
+            m.super_rows, m.super_cols, m.super_rows_t, m.super_cols_t = (x.data_ptr() for x in self.super_slices)
+            nws = capi.ggnn_super_model_workspace_bytes(m)
+            self.super_ws = torch.empty((max(nws, 16),), dtype=torch.uint8, device=device)
+            m.super_ws, m.super_ws_bytes = self.super_ws.data_ptr(), self.super_ws.numel()
+            self.super_fused = capi.ggnn_super_fusable(dt, n_pad, B, H, E, self.n_super_active)
         self.refresh_weights()
         ws = capi.ggnn_backward_workspace_bytes(self.model)
         self.workspace = torch.empty((max(ws, 16),), dtype=torch.uint8, device=device)
@@ -391,88 +415,17 @@ def compile_with_supernodes(graphs: Sequence, hubs: Sequence, B: int, E: int, s:
     return comp
 
 
-class SupernodeGGNN:
-    """T-step propagation with supernode slices next to the 1-bit band, its
-    reverse pass for L = sum(G * X_T), composed from the per-step C-ABI calls:
-      forward step:  ggnn_banded_step_bits (band) + ggnn_super_propagate (slices) -> a;  ggnn_gru_update
-      reverse step:  ggnn_gru_update_bwd -> da, dh;  ggnn_banded_propagate_bits_bwd -> dM;
-                     ggnn_msg_transform_bwd (dX = dh + sum_e dM_e W_e^T, dW, dbias);
-                     ggnn_super_propagate_bwd (the slices' share of dX, dW, dbias)."""
+class SupernodeGGNN(BandedGGNN):
+    """T-step propagation with supernode slices next to the 1-bit band and its
+    reverse pass for L = sum(G * X_T), run by ggnn_forward / ggnn_backward
+    with the slices in the model: inside the fused step kernels where the
+    shape allows (bf16, H <= 64, at most 32 supernodes with edges; a long
+    contraction per step for the supernode rows), else with the stand-alone
+    slice kernels between the band step and the GRU.  Edges the band cannot
+    hold are dropped and counted (strict=False)."""
 
     def __init__(self, comp: Compiled, H: int, T: int, dt: str, params, device="cuda"):
-        import torch
-        self.torch, self.comp, self.H, self.T, self.dt = torch, comp, H, T, dt
-        n_pad, E, B, s = comp.n_pad, comp.E, comp.B, comp.stats["n_super"]
-        self.s = s
-        inner = (comp.src >= s) & (comp.dst >= s)
-        bits, bits_t, packed, dropped, dup = capi.ggnn_banded_pack_bits(
-            n_pad, E, B, comp.src[inner], comp.dst[inner], comp.etype[inner], strict=False)
-        rows, cols, rows_t, cols_t, cnt = capi.ggnn_super_pack(n_pad, E, s, comp.src, comp.dst, comp.etype)
-        comp.stats.update(n_packed=packed, n_dropped=dropped, n_duplicate=dup + cnt["duplicates"],
-                          n_super_rows=cnt["rows"], n_super_cols=cnt["cols"])
-        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
-        self.bits, self.bits_t = dev(bits), dev(bits_t)
-        self.rows, self.cols, self.rows_t, self.cols_t = dev(rows), dev(cols), dev(rows_t), dev(cols_t)
-        td = torch_dtype(dt)
-        self.W = to_device(params.W, dt, device)
-        self.bias = None if params.bias is None else torch.from_numpy(params.bias.astype(np.float32)).to(device)
-        self.Wi, self.U = to_device(params.Wi, dt, device), to_device(params.U, dt, device)
-        self.b = torch.from_numpy(params.b.astype(np.float32)).to(device)
-        self.X = torch.empty((T + 1, n_pad, H), dtype=td, device=device)
-        self.X[0].copy_(to_device(params.X, dt, device))
-        self.a = torch.empty((T, n_pad, H), dtype=torch.float32, device=device)
-        self.saved = torch.empty((T, n_pad, 3 * H), dtype=td, device=device)
-        self.G = torch.from_numpy(params.G.astype(np.float32)).to(device)
-        self.dX = torch.empty((n_pad, H), dtype=torch.float32, device=device)
-        self.dX2 = torch.empty_like(self.dX)
-        self.dh = torch.empty_like(self.dX)
-        self.da = torch.empty((H, n_pad), dtype=td, device=device)
-        self.dM = torch.empty((E, H, n_pad), dtype=td, device=device)
-        self.dW = torch.zeros((E, H, H), dtype=torch.float32, device=device)
-        self.dbias = torch.zeros((E, H), dtype=torch.float32, device=device)
-        self.dWi = torch.zeros((H, 3 * H), dtype=torch.float32, device=device)
-        self.dU = torch.zeros_like(self.dWi)
-        self.db = torch.zeros((3 * H,), dtype=torch.float32, device=device)
-        mk = lambda n: torch.empty((max(n, 16),), dtype=torch.uint8, device=device)
-        self.ws_sn = mk(capi.ggnn_super_workspace_bytes(n_pad, H, E, s))
-        self.ws_gru = mk(capi.ggnn_gru_update_bwd_workspace_bytes(dt, n_pad, H))
-        self.ws_tr = mk(capi.ggnn_msg_transform_bwd_workspace_bytes(dt, n_pad, H, E))
-
-    def forward(self, stream=None):
-        c, H, E = self.comp, self.H, self.comp.E
-        for t in range(self.T):
-            capi.ggnn_banded_step_bits(self.dt, c.n_pad, c.B, H, E, self.bits, self.X[t], self.W, self.bias, self.a[t],
-                                       stream)
-            capi.ggnn_super_propagate(self.dt, c.n_pad, H, E, self.s, self.rows, self.cols, self.X[t], self.W,
-                                      self.bias, self.a[t], self.ws_sn, self.ws_sn.numel(), stream)
-            capi.ggnn_gru_update(self.dt, c.n_pad, H, self.a[t], self.X[t], self.Wi, self.U, self.b, self.X[t + 1],
-                                 self.saved[t], stream)
-
-    def backward(self, stream=None):
-        c, H, E = self.comp, self.H, self.comp.E
-        for z in (self.dW, self.dbias, self.dWi, self.dU, self.db):
-            z.zero_()
-        g, gn = self.dX, self.dX2
-        g.copy_(self.G)
-        for t in range(self.T - 1, -1, -1):
-            capi.ggnn_gru_update_bwd(self.dt, c.n_pad, H, g, self.a[t], self.X[t], self.saved[t], self.Wi, self.U,
-                                     self.da, self.dh, self.dWi, self.dU, self.db, self.ws_gru, self.ws_gru.numel(),
-                                     stream)
-            capi.ggnn_banded_propagate_bits_bwd(self.dt, c.n_pad, c.B, H, E, self.bits_t, self.da, self.dM, stream)
-            capi.ggnn_msg_transform_bwd(self.dt, c.n_pad, H, E, self.X[t], self.W, self.dM, self.dh, gn, self.dW,
-                                        self.dbias if self.bias is not None else None, self.ws_tr,
-                                        self.ws_tr.numel(), stream)
-            capi.ggnn_super_propagate_bwd(self.dt, c.n_pad, H, E, self.s, self.rows, self.rows_t, self.cols_t,
-                                          self.X[t], self.W, self.da, gn, self.dW,
-                                          self.dbias if self.bias is not None else None, self.ws_sn,
-                                          self.ws_sn.numel(), stream)
-            g, gn = gn, g
-        self.dX0 = g
-
-    def results(self) -> dict:
-        f = (lambda t: t.float().cpu().numpy().astype(np.float64))
-        out = dict(XT=f(self.X[self.T]), dX0=f(self.dX0), dW=f(self.dW), dWi=f(self.dWi), dU=f(self.dU),
-                   db=f(self.db))
-        if self.bias is not None:
-            out["dbias"] = f(self.dbias)
-        return out
+        if not comp.stats.get("n_super"):
+            raise ValueError("compile_with_supernodes() output expected")
+        super().__init__(comp, H, T, dt, params, device=device, strict=False)
+        self.s = self.n_super

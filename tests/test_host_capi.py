@@ -390,6 +390,33 @@ def test_super_pack_bit_exact_against_oracle(s):
         capi.ggnn_super_pack(480, 3, 32, src, dst, et)     # n_pad not a multiple of 64
 
 
+@pytest.mark.parametrize("s", [32, 64, 128])
+def test_super_active_is_the_highest_supernode_with_an_edge(s):
+    """ggnn_super_active: the smallest multiple of 16 above every supernode
+    index that has an edge into it (row slice) or out of it into another node
+    (column slice); 0 for empty slices; edges among the other nodes do not
+    count."""
+    _need_lib()
+    n, E = 448, 3
+    rng = np.random.default_rng(s + 1)
+    src = rng.integers(s, n, 300)
+    dst = rng.integers(s, n, 300)
+    et = rng.integers(0, E, 300)
+    rows, cols, _, _, _ = capi.ggnn_super_pack(n, E, s, src, dst, et)
+    assert capi.ggnn_super_active(n, E, s, rows, cols) == 0
+    for top, into in [(0, True), (5, False), (15, True), (16, False), (31, True), (32, False), (s - 1, True),
+                      (s - 1, False)]:
+        if top >= s:
+            continue
+        a = np.append(src, s + 3 if into else top)
+        b = np.append(dst, top if into else s + 7)
+        c = np.append(et, E - 1)
+        rows, cols, _, _, _ = capi.ggnn_super_pack(n, E, s, a, b, c)
+        assert capi.ggnn_super_active(n, E, s, rows, cols) == (top // 16 + 1) * 16, (top, into)
+    with pytest.raises(capi.GGNNError):
+        capi.ggnn_super_active(n, E, 48, rows, cols)
+
+
 def test_compile_with_supernodes_matches_oracle_reordering():
     """Hubs take the first labels; the other nodes of each graph follow in
     the oracle's reverse Cuthill-McKee order of the edges between them."""
