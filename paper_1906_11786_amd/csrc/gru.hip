@@ -850,7 +850,19 @@ struct Split {
 #ifndef GGNN_GRU_WGRAD_WGS
 #define GGNN_GRU_WGRAD_WGS 256
 #endif
+// At H = 256 in bf16 the contraction of csrc/wgrad_wide.hip runs instead:
+// six output tiles per split, 144 KB of LDS per workgroup (one per compute
+// unit), so 42 splits (252 workgroups) of a multiple of 32 rows.
+#ifndef GGNN_GRU_WGRAD256_LDS
+#define GGNN_GRU_WGRAD256_LDS 1
+#endif
+bool gru_wgrad256(long K, int H, bool f32) { return GGNN_GRU_WGRAD256_LDS && H == 256 && !f32 && K % 32 == 0; }
 Split gru_split(long K, int H, bool f32) {
+  if (gru_wgrad256(K, H, f32)) {
+    const long want = GGNN_GRU_WGRAD_WGS / 6;
+    const long per = std::max(32L, ((K + want - 1) / want + 31) / 32 * 32);
+    return {(int)((K + per - 1) / per), (int)per};
+  }
   const long slices = (H >= 256 && !f32) ? H / 32 : (H >= 128 ? H / (4096 / H) : 1);
   const long want = GGNN_GRU_WGRAD_WGS / slices > 0 ? GGNN_GRU_WGRAD_WGS / slices : 1;
   long per = ((K + want - 1) / want + 127) / 128 * 128;
@@ -927,11 +939,16 @@ hipError_t gru_wgrad_h(long K, const float* a, const void* h, const void* saved,
   Split sp = gru_split(K, H, sizeof(S) == 4);
   float* P = static_cast<float*>(ws);
   float* Pb = P + (size_t)sp.nsplit * 2 * H * 3 * H;
-  const int blocks = sp.nsplit * (H / dev::GruWgradCfg<S, H>::IT);
-  hipLaunchKernelGGL((dev::gru_wgrad_kernel<S, H>), dim3(blocks), dim3(512), 0, st, a,
-                     static_cast<const S*>(h), static_cast<const S*>(saved), static_cast<const S*>(ghat), P, Pb, K,
-                     sp.per);
-  hipError_t err = hipGetLastError();
+  hipError_t err;
+  if (sizeof(S) == 2 && H == 256 && gru_wgrad256(K, H, false)) {
+    err = launch_gru_wgrad256(sp.nsplit, sp.per, K, a, h, saved, ghat, P, Pb, st);
+  } else {
+    const int blocks = sp.nsplit * (H / dev::GruWgradCfg<S, H>::IT);
+    hipLaunchKernelGGL((dev::gru_wgrad_kernel<S, H>), dim3(blocks), dim3(512), 0, st, a,
+                       static_cast<const S*>(h), static_cast<const S*>(saved), static_cast<const S*>(ghat), P, Pb,
+                       K, sp.per);
+    err = hipGetLastError();
+  }
   if (err != hipSuccess) return err;
   const long slice = 2L * H * 3 * H;  // partials are [split][which][H][3H]
   err = reduce_or_defer(P, dWi, sp.nsplit, H * 3 * H, slice, defer, st);

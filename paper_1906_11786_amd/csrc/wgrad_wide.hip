@@ -172,6 +172,217 @@ __global__ __launch_bounds__(NT) void transform_wgrad_nm256_kernel(const bf16s* 
 }
 
 }  // namespace wgw
+
+// ---------------------------------------------------------------------------
+// Weight gradients of the GRU at H = 256 (bf16) over all T * n_pad rows k
+// (a, h, saved and G^ stacked over t):
+//   P[split][0][i][c] = sum_k a[k][i] G^[k][c]          (dWi)
+//   P[split][1][i][c] = sum_k x_c[k][i] G^[k][c]        (dU)
+//   Pb[split][c]      = sum_k G^[k][c]                  (db)
+// with x_c = h for the first 2H gate columns and r*h for the last H (r the
+// first H values of the saved gates); a enters rounded to bf16 and r*h is
+// formed in fp32 and rounded to bf16, as at the other widths.
+//
+// The contraction streams 3.6 KB per row (a in fp32, h, r, G^) over 8.4 M
+// rows at the 1M-node workload.  Loads staged through registers leave one
+// chunk in flight per workgroup, which then waits on memory at every chunk;
+// here each workgroup owns one row split and one of the six 256 x 256 output
+// tiles (matrix m in {dWi, dU} x gate block gb), reads G^'s 256-column block
+// and one input operand (a, h, or h and r), and copies the rows from global
+// memory straight to LDS (global_load_lds_dwordx4) two 32-row chunks ahead of
+// the one being multiplied, in a ring of three 48 KB slots.  The six tiles of
+// a split are neighbouring workgroups (one XCD, shared L2).  (Pairing both
+// matrices of one input half and gate block in a workgroup instead, so that
+// the workgroups sharing a G^ block do equal work, fetched more: over a
+// split's thousands of chunks independent workgroups drift apart whatever
+// their balance, and the L2 serves few of the shared rows either way.)
+//
+// Slot layouts (32 rows each): dWi: a as fp32 [32][256] (32 KB) then the G^
+// block [32][256] bf16; dU on the r and z blocks: h, G^ block; dU on the n
+// block: h, r, G^ block.  bf16 tiles are XOR-permuted by sw(r) as above; in
+// the fp32 tile, the 4-column units of row r are XOR-permuted by
+// 16 ((r >> 3) & 3), so that the four 8-row groups of one strided fragment
+// read fall on disjoint banks.  Waves form a 2 x 4 grid as above.
+// ---------------------------------------------------------------------------
+namespace gwg {
+
+constexpr int H = 256, G3 = 3 * H, KC = 32, WI = 2, WO = 4, NWV = WI * WO, NT = 64 * NWV;
+constexpr int TI = 16 / WI, TO = 16 / WO;
+constexpr int TILE16 = KC * H * 2;          // bytes of a bf16 [32][256] tile
+constexpr int SLOT = 3 * TILE16;            // bytes of one slot (48 KB)
+constexpr int NSLOT = 3;
+constexpr int NTILE = 6;                    // output tiles per split
+
+// Fragment of the fp32 a tile, rounded to bf16: lane (q, g) receives
+// a(8g + j, n0 + q), j = 0..7.
+__device__ __forceinline__ bf16x8 frag_f32(const float* base, int n0, int lane) {
+  const int q = lane % 16, g = lane / 16;
+  float v[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int row = 8 * g + j;
+    v[j] = base[row * H + ((n0 ^ (((row >> 3) & 3) << 4)) + q)];
+  }
+  return pack8<bf16s>(v);
+}
+
+// KIND 0: dWi (operand a), 1: dU on the r or z block (h), 2: dU on the n
+// block (r * h).
+template <int KIND>
+__device__ __forceinline__ void gru_wgrad256_body(const float* __restrict__ a, const bf16s* __restrict__ h,
+                                                  const bf16s* __restrict__ saved, const bf16s* __restrict__ ghat,
+                                                  float* __restrict__ P, float* __restrict__ Pb, long K,
+                                                  int rows_per_split, int split, int m, int gb, int wave, int lane,
+                                                  unsigned char* ring) {
+  const int q = lane % 16, g = lane / 16;
+  const int wi = wave % WI, wo = wave / WI;
+  const long nlo = (long)split * rows_per_split;
+  const long nhi = min(K, nlo + rows_per_split);
+  const int nchunks = nlo < nhi ? (int)((nhi - nlo) / KC) : 0;
+  const uint32_t ring_lds = (uint32_t)(uintptr_t)ring;
+  // byte offsets of the operand tiles within a slot
+  constexpr int OFF_G = KIND == 1 ? TILE16 : 2 * TILE16;
+  constexpr int OFF_R = TILE16;   // KIND 2 only
+  constexpr int PER = KIND == 1 ? 4 : 6;   // copies per wave and chunk
+
+  // This lane's element offsets relative to the chunk's first row.  bf16
+  // tiles: copy j (0, 1) of the wave covers chunk rows r = 2 (2 wave + j) +
+  // lane / 32, 8-element unit lane % 32 of the row.  fp32 a: copy j (0..3)
+  // covers row 4 wave + j, 4-element unit lane.
+  int off_h[2], off_g[2], off_a[4];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int r = 2 * (2 * wave + j) + lane / 32;
+    const int u = (8 * (lane % 32)) ^ (wgw::sw(r) << 4);
+    off_h[j] = r * H + u;
+    off_g[j] = r * G3 + gb * H + u;
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int r = 4 * wave + j;
+    off_a[j] = r * H + ((4 * lane) ^ (((r >> 3) & 3) << 4));
+  }
+  auto issue = [&](int chunk, int slot) __attribute__((always_inline)) {
+    const size_t row0 = (size_t)(nlo + (long)chunk * KC);
+    const uint32_t base = ring_lds + (uint32_t)(slot * SLOT);
+    if constexpr (KIND == 0) {
+      const float* ac = a + row0 * H;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) dma16(ac + off_a[j], base + (uint32_t)((4 * wave + j) * H * 4));
+    } else {
+      const bf16s* hc = h + row0 * H;
+      const bf16s* rc = saved + row0 * G3;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const uint32_t at = base + (uint32_t)(2 * (2 * wave + j) * H * 2);
+        dma16(hc + off_h[j], at);
+        if constexpr (KIND == 2) dma16(rc + (off_g[j] - gb * H), at + OFF_R);
+      }
+    }
+    const bf16s* gc = ghat + row0 * G3;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) dma16(gc + off_g[j], base + (uint32_t)(OFF_G + 2 * (2 * wave + j) * H * 2));
+  };
+
+  f32x4 acc[TI][TO];
+  float bsum[TO];
+#pragma unroll
+  for (int o = 0; o < TO; ++o) {
+    bsum[o] = 0.f;
+#pragma unroll
+    for (int i = 0; i < TI; ++i) acc[i][o] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const bool do_bias = KIND == 0 && wi == 0;
+  auto compute = [&](int slot) __attribute__((always_inline)) {
+    const unsigned char* sb = ring + slot * SLOT;
+    const bf16s* sg = reinterpret_cast<const bf16s*>(sb + OFF_G);
+    bf16x8 fb[TO];
+#pragma unroll
+    for (int o = 0; o < TO; ++o) {
+      fb[o] = wgw::frag(sg, 0, 16 * (wo * TO + o), lane);
+      if (do_bias) {
+#pragma unroll
+        for (int x = 0; x < 8; ++x) bsum[o] += static_cast<float>(fb[o][x]);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < TI; ++i) {
+      const int n0 = 16 * (wi * TI + i);
+      bf16x8 fa;
+      if constexpr (KIND == 0) {
+        fa = frag_f32(reinterpret_cast<const float*>(sb), n0, lane);
+      } else if constexpr (KIND == 1) {
+        fa = wgw::frag(reinterpret_cast<const bf16s*>(sb), 0, n0, lane);
+      } else {
+        const bf16x8 fh = wgw::frag(reinterpret_cast<const bf16s*>(sb), 0, n0, lane);
+        const bf16x8 fr = wgw::frag(reinterpret_cast<const bf16s*>(sb + OFF_R), 0, n0, lane);
+        float v[8];
+#pragma unroll
+        for (int x = 0; x < 8; ++x) v[x] = static_cast<float>(fh[x]) * static_cast<float>(fr[x]);
+        fa = pack8<bf16s>(v);
+      }
+#pragma unroll
+      for (int o = 0; o < TO; ++o) mma(acc[i][o], fa, fb[o]);
+    }
+  };
+  // Chunk c in slot c % 3: wait for this wave's copies of it (chunk c + 1's
+  // may stay in flight), meet the other waves, issue chunk c + 2 into the
+  // slot chunk c - 1 used (every wave is past its products), multiply.  The
+  // slot is a run-time value: with the loop unrolled over the three slots the
+  // compiler keeps every slot's fragment addresses in registers and spills.
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+    if (c < nchunks) issue(c, c);
+  int slot = 0;
+#pragma clang loop unroll(disable)
+  for (int c = 0; c < nchunks; ++c) {
+    if (c + 1 < nchunks) wait_copies<PER>();
+    else wait_copies<0>();
+    __syncthreads();
+    if (c + 2 < nchunks) issue(c + 2, slot == 0 ? 2 : slot - 1);
+    compute(slot);
+    slot = slot == 2 ? 0 : slot + 1;
+  }
+
+  // D[i = 16 (wi TI + i) + 4g + j][c = gb H + 16 (wo TO + o) + q]
+  float* out = P + ((size_t)split * 2 + m) * H * G3 + gb * H;
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int o = 0; o < TO; ++o)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        out[(size_t)(16 * (wi * TI + i) + 4 * g + j) * G3 + 16 * (wo * TO + o) + q] = acc[i][o][j];
+  if (do_bias) {
+#pragma unroll
+    for (int o = 0; o < TO; ++o) {
+      float v = bsum[o];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (g == 0) Pb[(size_t)split * G3 + gb * H + 16 * (wo * TO + o) + q] = v;
+    }
+  }
+}
+
+__global__ __launch_bounds__(NT) void gru_wgrad256_kernel(const float* __restrict__ a, const bf16s* __restrict__ h,
+                                                          const bf16s* __restrict__ saved,
+                                                          const bf16s* __restrict__ ghat, float* __restrict__ P,
+                                                          float* __restrict__ Pb, long K, int rows_per_split) {
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[NSLOT * SLOT];
+  const int tid = threadIdx.x, lane = tid % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int bid = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int tile = bid % NTILE, split = bid / NTILE;
+  const int m = tile / 3, gb = tile % 3;
+  if (m == 0)
+    gru_wgrad256_body<0>(a, h, saved, ghat, P, Pb, K, rows_per_split, split, m, gb, wave, lane, ring);
+  else if (gb < 2)
+    gru_wgrad256_body<1>(a, h, saved, ghat, P, Pb, K, rows_per_split, split, m, gb, wave, lane, ring);
+  else
+    gru_wgrad256_body<2>(a, h, saved, ghat, P, Pb, K, rows_per_split, split, m, gb, wave, lane, ring);
+}
+
+}  // namespace gwg
 }  // namespace dev
 
 hipError_t launch_transform_wgrad_nm256(int nsplit, int rows_per_split, long K, int E, const void* X, const void* dM,
@@ -180,6 +391,15 @@ hipError_t launch_transform_wgrad_nm256(int nsplit, int rows_per_split, long K, 
   hipLaunchKernelGGL(dev::wgw::transform_wgrad_nm256_kernel, dim3(nsplit * E), dim3(dev::wgw::NT), 0, st,
                      static_cast<const dev::bf16s*>(X), static_cast<const dev::bf16s*>(dM), ldk, P, Pb, K, E,
                      rows_per_split);
+  return hipGetLastError();
+}
+
+hipError_t launch_gru_wgrad256(int nsplit, int rows_per_split, long K, const float* a, const void* h,
+                               const void* saved, const void* ghat, float* P, float* Pb, hipStream_t st) {
+  if (rows_per_split % dev::gwg::KC != 0 || K % dev::gwg::KC != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(dev::gwg::gru_wgrad256_kernel, dim3(nsplit * dev::gwg::NTILE), dim3(dev::gwg::NT), 0, st, a,
+                     static_cast<const dev::bf16s*>(h), static_cast<const dev::bf16s*>(saved),
+                     static_cast<const dev::bf16s*>(ghat), P, Pb, K, rows_per_split);
   return hipGetLastError();
 }
 
