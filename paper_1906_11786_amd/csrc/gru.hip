@@ -856,6 +856,9 @@ struct Split {
 #ifndef GGNN_GRU_WGRAD256_LDS
 #define GGNN_GRU_WGRAD256_LDS 1
 #endif
+#ifndef GGNN_GRU_WGRAD_PACE
+#define GGNN_GRU_WGRAD_PACE 1
+#endif
 bool gru_wgrad256(long K, int H, bool f32) { return GGNN_GRU_WGRAD256_LDS && H == 256 && !f32 && K % 32 == 0; }
 Split gru_split(long K, int H, bool f32) {
   if (gru_wgrad256(K, H, f32)) {
@@ -941,7 +944,9 @@ hipError_t gru_wgrad_h(long K, const float* a, const void* h, const void* saved,
   float* Pb = P + (size_t)sp.nsplit * 2 * H * 3 * H;
   hipError_t err;
   if (sizeof(S) == 2 && H == 256 && gru_wgrad256(K, H, false)) {
-    err = launch_gru_wgrad256(sp.nsplit, sp.per, K, a, h, saved, ghat, P, Pb, st);
+    int* prog = reinterpret_cast<int*>(Pb + (size_t)sp.nsplit * 3 * H);   // pacing counters
+    err = launch_gru_wgrad256(sp.nsplit, sp.per, K, a, h, saved, ghat, P, Pb, GGNN_GRU_WGRAD_PACE ? prog : nullptr,
+                              st);
   } else {
     const int blocks = sp.nsplit * (H / dev::GruWgradCfg<S, H>::IT);
     hipLaunchKernelGGL((dev::gru_wgrad_kernel<S, H>), dim3(blocks), dim3(512), 0, st, a,
@@ -1000,7 +1005,8 @@ size_t gru_wgrad_workspace(long K, int H) {
   Split sp = gru_split(K, H, false);
   const Split s32 = gru_split(K, H, true);
   if (s32.nsplit > sp.nsplit) sp = s32;
-  return ((size_t)sp.nsplit * 2 * H * 3 * H + (size_t)sp.nsplit * 3 * H) * sizeof(float);
+  // partials, bias partials, then 8 pacing counters per split (H = 256 bf16)
+  return ((size_t)sp.nsplit * 2 * H * 3 * H + (size_t)sp.nsplit * 3 * H + (size_t)sp.nsplit * 8) * sizeof(float);
 }
 
 size_t gru_pack_bytes(int dt, int H) {

@@ -37,9 +37,10 @@ hipError_t launch_transform_wgrad_nm256(int nsplit, int rows_per_split, long K, 
                                         long ldk, float* P, float* Pb, hipStream_t st);
 // GRU weight gradients at H = 256 in bf16 (csrc/wgrad_wide.hip): partials
 // P [nsplit][2][256][768] (dWi, dU) and Pb [nsplit][768]; splits of
-// rows_per_split rows (a multiple of 32, as K).
+// rows_per_split rows (a multiple of 32, as K); prog: nsplit x 8 ints of
+// pacing counters (any contents; NULL turns pacing off).
 hipError_t launch_gru_wgrad256(int nsplit, int rows_per_split, long K, const float* a, const void* h,
-                               const void* saved, const void* ghat, float* P, float* Pb, hipStream_t st);
+                               const void* saved, const void* ghat, float* P, float* Pb, int* prog, hipStream_t st);
 hipError_t reduce_or_defer(const float* part, float* out, int nsplit, int count, long stride, ReduceList* defer,
                            hipStream_t st);
 

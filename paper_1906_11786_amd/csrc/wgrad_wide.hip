@@ -199,12 +199,70 @@ __global__ __launch_bounds__(NT) void transform_wgrad_nm256_kernel(const bf16s* 
 //
 // Slot layouts (32 rows each): dWi: a as fp32 [32][256] (32 KB) then the G^
 // block [32][256] bf16; dU on the r and z blocks: h, G^ block; dU on the n
-// block: h, r, G^ block.  bf16 tiles are XOR-permuted by sw(r) as above; in
+// block: h, r (then r * h), G^ block.  bf16 tiles are XOR-permuted by sw(r) as above; in
 // the fp32 tile, the 4-column units of row r are XOR-permuted by
 // 16 ((r >> 3) & 3), so that the four 8-row groups of one strided fragment
 // read fall on disjoint banks.  Waves form a 2 x 4 grid as above.
 // ---------------------------------------------------------------------------
 namespace gwg {
+
+// XCD of logical workgroup lb (the inverse of xcd_swizzle's grouping).
+__device__ __forceinline__ int xcd_of(int lb, int nblocks) {
+  const int per = nblocks / 8, rem = nblocks % 8;
+  return lb < rem * (per + 1) ? lb / (per + 1) : rem + (lb - rem * (per + 1)) / per;
+}
+
+// Pacing of the workgroups of one row split (up to 8; wave 0 of each,
+// before the stage's barrier).  The output tiles of a split read shared rows
+// of their operands but do unequal work per chunk; left alone they drift
+// apart by many chunks over a split and each fetches the shared rows from
+// memory itself (49 GB per launch at the 1M-node workload, against 29.5 GB
+// of operands).  Each publishes the chunk it has reached in counters[tile]
+// (a vector store); every PACE_EVERY chunks it reads the split's 8 counters
+// (one scalar load that bypasses the scalar cache, so that these waits do
+// not mix with the copies' vmcnt) and, while a sibling on its XCD (bit t of
+// sibs) is more than PACE_SLACK chunks behind, sleeps and reads again
+// (32.6 GB fetched, 11.5 -> 10.2 ms; the poll interval and slack made no
+// difference between 1 and 8 chunks).  Only the timing depends on this:
+// every workgroup reads its own operands and writes its own partials.
+// After PACE_TRIES reads without the laggard catching up, pacing stops for
+// the rest of the launch (a sibling that is not resident, or counters left
+// by an earlier launch, cost one bounded wait).
+#ifndef GGNN_PACE_EVERY
+#define GGNN_PACE_EVERY 4
+#endif
+#ifndef GGNN_PACE_SLACK
+#define GGNN_PACE_SLACK 3
+#endif
+constexpr int PACE_EVERY = GGNN_PACE_EVERY, PACE_SLACK = GGNN_PACE_SLACK, PACE_TRIES = 64;
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ bool pace_split(int* counters, int tile, uint32_t sibs, int c, int lane, bool on) {
+  if (lane == 0) __hip_atomic_store(counters + tile, c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (!on || c % PACE_EVERY != 0 || c < PACE_SLACK) return on;
+  for (int tries = 0; tries < PACE_TRIES; ++tries) {
+    i32x8 v;
+    asm volatile("s_load_dwordx8 %0, %1, 0x0 glc\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(counters) : "memory");
+    int lag = 0x7fffffff;
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      if ((sibs >> t) & 1u) lag = min(lag, v[t]);
+    if (lag >= c - PACE_SLACK) return true;
+    __builtin_amdgcn_s_sleep(4);
+  }
+  return false;
+}
+
+// Siblings of tile `tile` among the ntile workgroups of split `split`
+// (logical ids split * ntile + t) that run on the same XCD as logical
+// workgroup bid.
+__device__ __forceinline__ uint32_t pace_siblings(int bid, int split, int tile, int ntile, int nblocks) {
+  uint32_t sibs = 0u;
+  const int mine = xcd_of(bid, nblocks);
+  for (int t = 0; t < ntile; ++t)
+    if (t != tile && xcd_of(split * ntile + t, nblocks) == mine) sibs |= 1u << t;
+  return sibs;
+}
+
 
 constexpr int H = 256, G3 = 3 * H, KC = 32, WI = 2, WO = 4, NWV = WI * WO, NT = 64 * NWV;
 constexpr int TI = 16 / WI, TO = 16 / WO;
@@ -233,7 +291,8 @@ __device__ __forceinline__ void gru_wgrad256_body(const float* __restrict__ a, c
                                                   const bf16s* __restrict__ saved, const bf16s* __restrict__ ghat,
                                                   float* __restrict__ P, float* __restrict__ Pb, long K,
                                                   int rows_per_split, int split, int m, int gb, int wave, int lane,
-                                                  unsigned char* ring) {
+                                                  unsigned char* ring, int* __restrict__ prog, int tile,
+                                                  uint32_t sibs) {
   const int q = lane % 16, g = lane / 16;
   const int wi = wave % WI, wo = wave / WI;
   const long nlo = (long)split * rows_per_split;
@@ -311,15 +370,8 @@ __device__ __forceinline__ void gru_wgrad256_body(const float* __restrict__ a, c
       bf16x8 fa;
       if constexpr (KIND == 0) {
         fa = frag_f32(reinterpret_cast<const float*>(sb), n0, lane);
-      } else if constexpr (KIND == 1) {
-        fa = wgw::frag(reinterpret_cast<const bf16s*>(sb), 0, n0, lane);
-      } else {
-        const bf16x8 fh = wgw::frag(reinterpret_cast<const bf16s*>(sb), 0, n0, lane);
-        const bf16x8 fr = wgw::frag(reinterpret_cast<const bf16s*>(sb + OFF_R), 0, n0, lane);
-        float v[8];
-#pragma unroll
-        for (int x = 0; x < 8; ++x) v[x] = static_cast<float>(fh[x]) * static_cast<float>(fr[x]);
-        fa = pack8<bf16s>(v);
+      } else {   // h, or r * h (formed over the r tile below)
+        fa = wgw::frag(reinterpret_cast<const bf16s*>(sb + (KIND == 2 ? OFF_R : 0)), 0, n0, lane);
       }
 #pragma unroll
       for (int o = 0; o < TO; ++o) mma(acc[i][o], fa, fb[o]);
@@ -334,12 +386,30 @@ __device__ __forceinline__ void gru_wgrad256_body(const float* __restrict__ a, c
   for (int c = 0; c < 2; ++c)
     if (c < nchunks) issue(c, c);
   int slot = 0;
+  bool pace = sibs != 0u;
 #pragma clang loop unroll(disable)
   for (int c = 0; c < nchunks; ++c) {
     if (c + 1 < nchunks) wait_copies<PER>();
     else wait_copies<0>();
+    if (wave == 0) pace = pace_split(prog + split * 8, tile, sibs, c, lane, pace);
     __syncthreads();
     if (c + 2 < nchunks) issue(c + 2, slot == 0 ? 2 : slot - 1);
+    if constexpr (KIND == 2) {
+      // r * h of the chunk, formed once (in fp32, rounded to bf16) and
+      // written over the r tile (h and r share one layout); formed per
+      // fragment instead, every element was formed by four waves, and the
+      // vector ALU work bound these tiles.
+      unsigned char* sb = ring + slot * SLOT;
+#pragma unroll
+      for (int u = 64 * wave + lane; u < KC * H / 8; u += NT) {
+        const u32x4 hv = *reinterpret_cast<const u32x4*>(sb + 16 * u);
+        u32x4 rv = *reinterpret_cast<const u32x4*>(sb + OFF_R + 16 * u);
+#pragma unroll
+        for (int x = 0; x < 4; ++x) rv[x] = pk2(lo_f(hv[x]) * lo_f(rv[x]), hi_f(hv[x]) * hi_f(rv[x]));
+        *reinterpret_cast<u32x4*>(sb + OFF_R + 16 * u) = rv;
+      }
+      __syncthreads();
+    }
     compute(slot);
     slot = slot == 2 ? 0 : slot + 1;
   }
@@ -367,19 +437,22 @@ __device__ __forceinline__ void gru_wgrad256_body(const float* __restrict__ a, c
 __global__ __launch_bounds__(NT) void gru_wgrad256_kernel(const float* __restrict__ a, const bf16s* __restrict__ h,
                                                           const bf16s* __restrict__ saved,
                                                           const bf16s* __restrict__ ghat, float* __restrict__ P,
-                                                          float* __restrict__ Pb, long K, int rows_per_split) {
+                                                          float* __restrict__ Pb, long K, int rows_per_split,
+                                                          int* __restrict__ prog) {
   __shared__ __attribute__((aligned(1024))) unsigned char ring[NSLOT * SLOT];
   const int tid = threadIdx.x, lane = tid % kWave;
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int bid = xcd_swizzle(blockIdx.x, gridDim.x);
   const int tile = bid % NTILE, split = bid / NTILE;
   const int m = tile / 3, gb = tile % 3;
+  // siblings: the other tiles of this split that run on this workgroup's XCD
+  const uint32_t sibs = prog != nullptr ? pace_siblings(bid, split, tile, NTILE, gridDim.x) : 0u;
   if (m == 0)
-    gru_wgrad256_body<0>(a, h, saved, ghat, P, Pb, K, rows_per_split, split, m, gb, wave, lane, ring);
+    gru_wgrad256_body<0>(a, h, saved, ghat, P, Pb, K, rows_per_split, split, m, gb, wave, lane, ring, prog, tile, sibs);
   else if (gb < 2)
-    gru_wgrad256_body<1>(a, h, saved, ghat, P, Pb, K, rows_per_split, split, m, gb, wave, lane, ring);
+    gru_wgrad256_body<1>(a, h, saved, ghat, P, Pb, K, rows_per_split, split, m, gb, wave, lane, ring, prog, tile, sibs);
   else
-    gru_wgrad256_body<2>(a, h, saved, ghat, P, Pb, K, rows_per_split, split, m, gb, wave, lane, ring);
+    gru_wgrad256_body<2>(a, h, saved, ghat, P, Pb, K, rows_per_split, split, m, gb, wave, lane, ring, prog, tile, sibs);
 }
 
 }  // namespace gwg
@@ -395,11 +468,11 @@ hipError_t launch_transform_wgrad_nm256(int nsplit, int rows_per_split, long K, 
 }
 
 hipError_t launch_gru_wgrad256(int nsplit, int rows_per_split, long K, const float* a, const void* h,
-                               const void* saved, const void* ghat, float* P, float* Pb, hipStream_t st) {
+                               const void* saved, const void* ghat, float* P, float* Pb, int* prog, hipStream_t st) {
   if (rows_per_split % dev::gwg::KC != 0 || K % dev::gwg::KC != 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL(dev::gwg::gru_wgrad256_kernel, dim3(nsplit * dev::gwg::NTILE), dim3(dev::gwg::NT), 0, st, a,
                      static_cast<const dev::bf16s*>(h), static_cast<const dev::bf16s*>(saved),
-                     static_cast<const dev::bf16s*>(ghat), P, Pb, K, rows_per_split);
+                     static_cast<const dev::bf16s*>(ghat), P, Pb, K, rows_per_split, prog);
   return hipGetLastError();
 }
 
