@@ -73,7 +73,7 @@ KERNELS = {
 }
 # Other kernels of the step, listed in the traffic summary.
 OTHER_KERNELS = [("gru_fwd_kernel",), ("gru_bwd_kernel",), ("gru_fwd_big_kernel",), ("gru_bwd_big_kernel",),
-                 ("gru_wgrad_kernel",), ("transform_bwd_dx_kernel",),
+                 ("gru_wgrad_kernel",), ("gru_wgrad256_kernel",), ("transform_bwd_dx_kernel",),
                  ("transform_wgrad_kernel",), ("transform_wgrad_nm_kernel",), ("transform_fwd_kernel",),
                  ("transform_wgrad_nm256_kernel",), ("reduce_partials_kernel",), ("reduce_multi_kernel",)]
 CAL_ELEMS = 64 << 20            # calibration copy: 64 Mi fp32 read, 64 Mi fp32 written
