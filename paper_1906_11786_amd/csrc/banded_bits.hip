@@ -89,10 +89,13 @@ __device__ __forceinline__ void store_pair(bf16s* p, uint32_t lo16, uint32_t hi1
 // four-byte banks, so a fragment read (16 consecutive lanes on 256
 // consecutive bytes) never conflicts; reading feature rows at a padded
 // pitch instead took two passes per read.
-// Staged node chunk: fragment (kk, feature tile h/16).
-template <typename S, int H, int KC>
+// Staged node chunk: fragment (kk, feature tile h/16).  Split k order: lane
+// group g holds nodes g KC/4 + 8 kk + 0..7 of the chunk; contiguous order
+// (KCONT): nodes 32 kk + 8 g + 0..7, so that a k step covers 32 consecutive
+// nodes.
+template <typename S, int H, int KC, bool KCONT = false>
 __device__ __forceinline__ int frag_off(int h, int c) {
-  const int g = c / (KC / 4), kk = (c % (KC / 4)) / 8;
+  const int g = KCONT ? (c / 8) % 4 : c / (KC / 4), kk = KCONT ? c / 32 : (c % (KC / 4)) / 8;
   return fo<S>(kk * (H / 16) + h / 16, h % 16 + 16 * g, c % 8);
 }
 template <typename S, int H>
@@ -179,6 +182,12 @@ struct BitsCfg {
   static constexpr int VP = KC + V;
   static constexpr bool ROWS = !ALL && H >= 256;   // streamed chunks kept as feature rows
   static constexpr int RB = KC / 32;        // bit-row bytes per lane per chunk (= k steps per chunk)
+  // k order of the staged blocks (ALL): contiguous at RB = 4, 8 (B = 128,
+  // 256), the bit bytes re-ordered in registers after each type's load; a
+  // k step then covers 32 consecutive block columns, and in a band much
+  // narrower than B most steps hold no edge into a wave's rows and are
+  // skipped whole.  Split otherwise (a lane's bytes as loaded).
+  static constexpr bool KCONT = ALL && (RB == 4 || RB == 8);
   static constexpr int RPW = H >= 256 ? 16 : 32;   // rows per wave
   static constexpr int NTW = RPW / 16;      // 16-row tiles per wave
   // Smallest workgroup (waves) launched; the fp32 forms with H >= 128 and
@@ -349,7 +358,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
             const int cq = rem % (KC / V), fq = rem / (KC / V);
 #pragma unroll
             for (int x = 0; x < V; ++x)
-              *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(perm_row(V * fq + x), V * cq)]) =
+              *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC, C::KCONT>(perm_row(V * fq + x), V * cq)]) =
                   tile_row_T<S>(r[u], x);
           } else {
             const int w = lin - nx, m = w / GT, rem = w % GT;
@@ -393,7 +402,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
           } else if (lin < nx) {
             const int slot = s_lo + lin / XT, rem = lin % XT;
             const int h = rem / (KC / V), c = (rem % (KC / V)) * V;
-            *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC>(perm_row(h), c)]) = r[u];
+            *reinterpret_cast<u32x4*>(&vt[slot][frag_off<S, H, KC, C::KCONT>(perm_row(h), c)]) = r[u];
           } else {
             const int w = lin - nx, m = w / GT, rem = w % GT;
             const int h = rem / (3 * H / V), c = (rem % (3 * H / V)) * V;
@@ -566,6 +575,23 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
       } else {
         if (e + 1 < e_hi) load_type(e + 1, nx1);
       }
+      if constexpr (C::KCONT) {
+        // contiguous k order; a block with no edge into the wave's rows
+        // stays all zero (and is skipped below)
+        const uint32_t godd = static_cast<uint32_t>(g & 1);
+#pragma unroll
+        for (int s = 0; s < 3; ++s) {
+          if (s < s_lo || s > s_hi) continue;
+          uint32_t any = 0u;
+#pragma unroll
+          for (int n = 0; n < NTW; ++n)
+#pragma unroll
+            for (int i = 0; i < RowBytes<RB>::NW; ++i) any |= cur[s][n].w[i];
+          if (__builtin_amdgcn_ballot_w64(any != 0u) == 0) continue;
+#pragma unroll
+          for (int n = 0; n < NTW; ++n) bytes_to_contiguous<RB>(cur[s][n].w, godd);
+        }
+      }
     }
     // SN: the slice bytes of this wave's rows (window columns 8g .. 8g + 7)
     // and, in the wave holding nodes 0..31, P_e of its rows (into LDS) and
@@ -623,6 +649,13 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         }
 #pragma unroll
         for (int kk = 0; kk < RB; ++kk) {
+          if constexpr (C::KCONT) {
+            // a k step with no edge into the wave's rows adds exact zeros
+            uint32_t any_step = 0u;
+#pragma unroll
+            for (int n = 0; n < NTW; ++n) any_step |= rb[n].byte(kk);
+            if (__builtin_amdgcn_ballot_w64(any_step != 0u) == 0) continue;
+          }
           frag_t<S> bf[NTW];
 #pragma unroll
           for (int n = 0; n < NTW; ++n) bf[n] = bits_frag<S>(rb[n].byte(kk));

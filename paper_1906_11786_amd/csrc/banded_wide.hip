@@ -173,38 +173,9 @@ template <int NB> struct WideBits {
     for (int i = 0; i < NW; ++i) w[i] = 0u;
   }
   __device__ __forceinline__ uint32_t byte(int i) const { return (w[i / 4] >> (8 * (i % 4))) & 0xFFu; }
-  // From the split byte order (lane group g holds row bytes NB g .. NB g +
-  // NB - 1, as loaded) to the contiguous one (byte kk = row byte 4 kk + g):
-  // a 4 x 4 transpose between the lane groups (rows of 16 lanes) of a wave,
-  // done with one permlane32 and one permlane16 swap and byte permutes.
-  // `odd` is g & 1.
-  __device__ __forceinline__ void to_contiguous(uint32_t odd) {
-    if constexpr (NB == 8) {
-      // lane g' holds k steps 2g' (w[0]) and 2g'+1 (w[1]), byte d = group d.
-      // Pair the two steps per destination group: L for groups 0, 1, U for 2, 3.
-      uint32_t L = __builtin_amdgcn_perm(w[1], w[0], 0x05010400u);
-      uint32_t U = __builtin_amdgcn_perm(w[1], w[0], 0x07030602u);
-      // lanes 0-31 keep L and take L of lanes 32-63; lanes 32-63 keep U.
-      auto r32 = __builtin_amdgcn_permlane32_swap(L, U, false, false);
-      L = r32[0];
-      U = r32[1];
-      uint32_t X0 = __builtin_amdgcn_perm(U, L, 0x05040100u);   // pairs for the even group of the half
-      uint32_t X1 = __builtin_amdgcn_perm(U, L, 0x07060302u);   // pairs for the odd group
-      auto r16 = __builtin_amdgcn_permlane16_swap(X0, X1, false, false);
-      X0 = r16[0];   // pairs of source lane groups 0 and 2
-      X1 = r16[1];   // pairs of source lane groups 1 and 3
-      w[0] = __builtin_amdgcn_perm(X1, X0, 0x05040100u);      // steps 0..3
-      w[1] = __builtin_amdgcn_perm(X1, X0, 0x07060302u);      // steps 4..7
-    } else if constexpr (NB == 4) {
-      // lane g' holds k step g' (byte d = group d).
-      const uint32_t D = w[0];
-      const uint32_t Yr = __builtin_amdgcn_perm(D, D, 0x01000302u);   // halves rotated
-      auto r32 = __builtin_amdgcn_permlane32_swap(D, Yr, false, false);
-      const uint32_t Z = __builtin_amdgcn_perm(r32[1], r32[0], 0x05040100u);
-      auto r16 = __builtin_amdgcn_permlane16_swap(Z, Z, false, false);
-      w[0] = __builtin_amdgcn_perm(r16[1], r16[0], odd ? 0x07030501u : 0x06020400u);
-    }
-  }
+  // From the split byte order to the contiguous one (see
+  // bytes_to_contiguous).  `odd` is g & 1.
+  __device__ __forceinline__ void to_contiguous(uint32_t odd) { bytes_to_contiguous<NB>(w, odd); }
   __device__ __forceinline__ int popc() const {
     int c = 0;
 #pragma unroll

@@ -297,6 +297,44 @@ __device__ __forceinline__ float tanhf_(float x) {
   return 1.0f - 2.0f * __builtin_amdgcn_rcpf(__expf(2.0f * x) + 1.0f);
 }
 
+// A lane's NB bit-row bytes (NB = 4 or 8) from the split order to the
+// contiguous one.  Split: lane group g (lanes 16g .. 16g + 15) holds row
+// bytes NB g .. NB g + NB - 1, as a 32-bit load per 4 bytes delivers them;
+// contiguous: byte kk of lane group g is row byte 4 kk + g, so that one
+// matrix-core k step covers 32 consecutive block columns.  A 4 x 4
+// transpose between the lane groups of a wave: one permlane32 and one
+// permlane16 swap and byte permutes.  `odd` is g & 1.
+template <int NB>
+__device__ __forceinline__ void bytes_to_contiguous(uint32_t* w, uint32_t odd) {
+  static_assert(NB == 4 || NB == 8, "contiguous order for 4- or 8-byte rows");
+  if constexpr (NB == 8) {
+    // lane g' holds k steps 2g' (w[0]) and 2g'+1 (w[1]), byte d = group d.
+    // Pair the two steps per destination group: L for groups 0, 1, U for 2, 3.
+    uint32_t L = __builtin_amdgcn_perm(w[1], w[0], 0x05010400u);
+    uint32_t U = __builtin_amdgcn_perm(w[1], w[0], 0x07030602u);
+    // lanes 0-31 keep L and take L of lanes 32-63; lanes 32-63 keep U.
+    auto r32 = __builtin_amdgcn_permlane32_swap(L, U, false, false);
+    L = r32[0];
+    U = r32[1];
+    uint32_t X0 = __builtin_amdgcn_perm(U, L, 0x05040100u);   // pairs for the even group of the half
+    uint32_t X1 = __builtin_amdgcn_perm(U, L, 0x07060302u);   // pairs for the odd group
+    auto r16 = __builtin_amdgcn_permlane16_swap(X0, X1, false, false);
+    X0 = r16[0];   // pairs of source lane groups 0 and 2
+    X1 = r16[1];   // pairs of source lane groups 1 and 3
+    w[0] = __builtin_amdgcn_perm(X1, X0, 0x05040100u);      // steps 0..3
+    w[1] = __builtin_amdgcn_perm(X1, X0, 0x07060302u);      // steps 4..7
+    (void)odd;
+  } else {
+    // lane g' holds k step g' (byte d = group d).
+    const uint32_t D = w[0];
+    const uint32_t Yr = __builtin_amdgcn_perm(D, D, 0x01000302u);   // halves rotated
+    auto r32 = __builtin_amdgcn_permlane32_swap(D, Yr, false, false);
+    const uint32_t Z = __builtin_amdgcn_perm(r32[1], r32[0], 0x05040100u);
+    auto r16 = __builtin_amdgcn_permlane16_swap(Z, Z, false, false);
+    w[0] = __builtin_amdgcn_perm(r16[1], r16[0], odd ? 0x07030501u : 0x06020400u);
+  }
+}
+
 // Logical workgroup index spread so that consecutive logical tiles land on the
 // same XCD (workgroups are dispatched round-robin over the 8 XCDs, each with
 // its own L2): neighbouring tiles then share operand data in one L2.
