@@ -252,6 +252,15 @@ struct BitsCfg {
 // whole reverse step.  Wi and U are staged in LDS (plain copies) with the
 // blocks; dX itself is written only when `out` is not NULL.
 // ---------------------------------------------------------------------------
+#ifndef GGNN_BITS_TG0_PCT_REV
+#define GGNN_BITS_TG0_PCT_REV 50
+#endif
+#ifndef GGNN_BITS_GW_TG0
+#define GGNN_BITS_GW_TG0 0
+#endif
+#ifndef GGNN_BITS_DM_LDS
+#define GGNN_BITS_DM_LDS 1
+#endif
 constexpr int kSnFused = 32;   // supernodes handled inside the fused step kernels
 template <typename S, int H, int B, int WAVES, bool WDIR, int TG, bool REV, bool GRU, bool SN = false>
 __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
@@ -283,6 +292,11 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   // and, per type group, the record rows of the wave holding nodes 0..31
   // (NTW x MT 1 KB copies, one 16-byte unit per lane each).
   __shared__ __attribute__((aligned(16))) S hubw[SN ? kSnFused * H : 8];
+  // reverse, bf16 with the blocks staged: each wave's dM tile (RPW rows,
+  // pitch DMP), for row-ordered stores
+  constexpr bool DMS = REV && C::ALL && sizeof(S) == 2 && GGNN_BITS_DM_LDS;
+  constexpr int DMP = H + 8;
+  __shared__ __attribute__((aligned(16))) S dms[DMS ? TG * WAVES * C::RPW * DMP : 8];
   __shared__ __attribute__((aligned(1024))) float recb[SN ? TG * NTW * MT * 256 : 4];
 
   const int nb = n_pad / B;
@@ -296,7 +310,11 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   const int rw = (t % tiles_per_row) * NW + C::RPW * wave;   // first row of this wave
   const int s_lo = (k == 0) ? 1 : 0;
   const int s_hi = (k == nb - 1) ? 1 : 2;
-  const int e_lo = tg * E / TG, e_hi = (tg + 1) * E / TG;     // this wave's types
+  // this wave's types: group 0 takes the first TG0_PCT percent in the
+  // reverse with two groups, else an even split
+  const int e_mid = (REV && TG == 2 && GGNN_BITS_TG0_PCT_REV != 50) ? (E * GGNN_BITS_TG0_PCT_REV + 50) / 100 : E / 2;
+  const int e_lo = TG == 2 ? (tg == 0 ? 0 : e_mid) : tg * E / TG;
+  const int e_hi = TG == 2 ? (tg == 0 ? e_mid : E) : (tg + 1) * E / TG;
 
   // The bit rows of the first types are requested before the staging, so
   // their latency overlaps it; later types' rows are loaded while the current
@@ -330,14 +348,14 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   constexpr int GT = !REV ? (H / V) * (3 * H / V) : H * (3 * H / V);   // units per GRU weight
   const int nx = (s_hi - s_lo + 1) * XT;
   const int total = nx + (GRU ? 2 * GT : 0);
-  auto stage_units = [&](int lo, int hi) __attribute__((always_inline)) {
+  auto stage_units = [&](int lo, int hi, int nthr, int thr) __attribute__((always_inline)) {
     if constexpr (C::ALL && !REV) {
       constexpr int PB = 2;
-      for (int base = lo; base < hi; base += PB * NT) {
+      for (int base = lo; base < hi; base += PB * nthr) {
         u32x4 r[PB][V];
 #pragma unroll
         for (int u = 0; u < PB; ++u) {
-          const int lin = base + u * NT + tid;
+          const int lin = base + u * nthr + thr;
           if (lin >= hi) {
           } else if (lin < nx) {
             const int slot = s_lo + lin / XT, rem = lin % XT;
@@ -351,7 +369,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         }
 #pragma unroll
         for (int u = 0; u < PB; ++u) {
-          const int lin = base + u * NT + tid;
+          const int lin = base + u * nthr + thr;
           if (lin >= hi) {
           } else if (lin < nx) {
             const int slot = s_lo + lin / XT, rem = lin % XT;
@@ -379,11 +397,11 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
       }
     } else if constexpr (C::ALL) {
       constexpr int PB = 8;
-      for (int base = lo; base < hi; base += PB * NT) {
+      for (int base = lo; base < hi; base += PB * nthr) {
         u32x4 r[PB];
 #pragma unroll
         for (int u = 0; u < PB; ++u) {
-          const int lin = base + u * NT + tid;
+          const int lin = base + u * nthr + thr;
           if (lin >= hi) {
           } else if (lin < nx) {
             const int slot = s_lo + lin / XT, rem = lin % XT;
@@ -397,7 +415,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         }
 #pragma unroll
         for (int u = 0; u < PB; ++u) {
-          const int lin = base + u * NT + tid;
+          const int lin = base + u * nthr + thr;
           if (lin >= hi) {
           } else if (lin < nx) {
             const int slot = s_lo + lin / XT, rem = lin % XT;
@@ -441,7 +459,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
     }
   }
   if constexpr (C::ALL) {
-    stage_units(0, nx);
+    stage_units(0, nx, NT, tid);
     if constexpr (SN) {
 #pragma unroll
       for (int u = 0; u < HPT; ++u) {
@@ -722,7 +740,26 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
           pf[0][n][kk] = pack8<S>(v8);
         }
       }
-    if constexpr (REV) {
+    if constexpr (REV && DMS) {
+      // dM_e rows of this wave's nodes through the wave's LDS tile: written
+      // as the lanes hold them (node 16n + q, features 32kk + 8g .. + 7),
+      // read back in row order, so that each store covers 1 KB of
+      // consecutive rows (stored from the lanes, every store touched 16 rows
+      // for 64 bytes each).  Wave-private, so no barrier.
+      S* dt = dms + (tg * WAVES + wave) * (C::RPW * DMP);
+#pragma unroll
+      for (int n = 0; n < NTW; ++n)
+#pragma unroll
+        for (int kk = 0; kk < HK; ++kk)
+          *reinterpret_cast<u32x4*>(dt + (16 * n + q) * DMP + 32 * kk + 8 * g) = __builtin_bit_cast(u32x4, pf[0][n][kk]);
+      S* rows0 = dM + ((size_t)e * ldm + k * B + rw) * H;
+#pragma unroll
+      for (int i = 0; i < C::RPW * H / 8 / kWave; ++i) {
+        const int u = i * kWave + lane;   // 16-byte unit u of the wave's rows: row u / (H / 8)
+        const int r = u / (H / 8), c = (u % (H / 8)) * 8;
+        *reinterpret_cast<u32x4*>(rows0 + (size_t)r * H + c) = *reinterpret_cast<const u32x4*>(dt + r * DMP + c);
+      }
+    } else if constexpr (REV) {
       // dM_e rows of this wave's nodes (node-major, rows of type e start at
       // row e * ldm): features 32kk + 8g .. 32kk + 8g + 7 (rev_row order).
 #pragma unroll
@@ -786,7 +823,13 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   // tiles per wave, tile tg.
   constexpr bool SPLIT = (TG == 2 && NTW == 2);
   // GRU weights for the epilogue (read after the barriers below).
-  if constexpr (C::ALL && GRU) stage_units(nx, total);
+  if constexpr (C::ALL && GRU) {
+    if (GGNN_BITS_GW_TG0 && TG == 2) {
+      if (tg == 0) stage_units(nx, total, WAVES * kWave, tid);   // the group that finishes first
+    } else {
+      stage_units(nx, total, NT, tid);
+    }
+  }
   // Epilogue operands of this wave's tile requested now, in flight across
   // the barriers: h (forward) or the gates of the previous step (reverse).
   frag_t<S> hf_pre[(GRU && !REV && SPLIT) ? H / 32 : 1];
