@@ -320,6 +320,104 @@ __global__ __launch_bounds__(256) void small_gemm_kernel(SmallGemm p) {
   }
 }
 
+
+#if GGNN_DT_BF16
+// The supernode rows' per-type aggregate for the fused forward step, as a gather:
+//   rec[e][i][h] = sum_{j : bits[e][i] has bit j} X[j][h],   rec[E sr H + e sr + i] = that count
+// for the first sr rows of the row slice R_e (X node-major [n_pad][H]).  The slice rows are sparse
+// (hub edges), so rather than a contraction over all n_pad nodes, a workgroup (e, i) lists the row's
+// set bits and sums the listed nodes' states: each of its sixteen waves takes a sixteenth of the row
+// (at the 20k-node workload one dword per lane, so a call is three dependent memory rounds: bits,
+// list, rows), compacts the set bits of 2048 columns at a time into an LDS list in column order (a
+// prefix count over the lanes), and adds the listed rows in that order in fp32, lane (r, c) taking 8
+// features of entries r, r + R, ... (R rows per load instruction); the waves' partial sums are then
+// combined in wave order, so the result depends only on the row (no float atomics).  The reverse
+// record (C_e^T da, da feature-major) stays on the long contraction: gathered, each listed node costs
+// one scattered element per feature row, and every layout of those loads tried (one node of all
+// features per instruction, 16 nodes of 4 features, the row split over 8 workgroups) ran slower than
+// the contraction's contiguous staging.
+constexpr int kSnGatherWaves = 16;
+template <int H>
+__global__ __launch_bounds__(64 * kSnGatherWaves) void super_gather_kernel(const uint8_t* __restrict__ bits,
+                                                                           const bf16s* __restrict__ X,
+                                                                           float* __restrict__ rec, int n_pad, int E,
+                                                                           int s, int sr) {
+  constexpr int NW = kSnGatherWaves, SLAB = 64 * 32;
+  __shared__ int lst[NW][SLAB];
+  __shared__ float part[NW][H + 1];
+  const int e = blockIdx.x / sr, i = blockIdx.x % sr;
+  const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+  const uint32_t* row = reinterpret_cast<const uint32_t*>(bits + ((size_t)e * s + i) * (size_t)(n_pad / 8));
+  const int ndw = n_pad / 32;
+  const int d0 = w * ndw / NW, d1 = (w + 1) * ndw / NW;
+  constexpr int CPR = H / 8;      // lanes per listed row
+  constexpr int R = 64 / CPR;     // listed rows per load instruction
+  constexpr int UB = 8;           // load instructions in flight
+  const int r = lane / CPR, c = lane % CPR;
+  float acc[8];
+#pragma unroll
+  for (int x = 0; x < 8; ++x) acc[x] = 0.f;
+  int deg = 0;
+  for (int base = d0; base < d1; base += kWave) {
+    const int d = base + lane;
+    uint32_t wd = d < d1 ? row[d] : 0u;
+    const int cnt = __popc(wd);
+    int incl = cnt;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int v = __shfl_up(incl, off);
+      if (lane >= off) incl += v;
+    }
+    const int total = __shfl(incl, kWave - 1);
+    int pos = incl - cnt;
+    while (wd != 0u) {
+      const int b = __ffs(wd) - 1;
+      wd &= wd - 1u;
+      lst[w][pos++] = d * 32 + b;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    deg += total;
+    for (int k0 = 0; k0 < total; k0 += R * UB) {
+      u32x4 v[UB];
+#pragma unroll
+      for (int u = 0; u < UB; ++u) {
+        const int k = k0 + u * R + r;
+        v[u] = k < total ? *reinterpret_cast<const u32x4*>(X + (size_t)lst[w][k] * H + 8 * c) : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int u = 0; u < UB; ++u)
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          acc[2 * x] += lo_f(v[u][x]);
+          acc[2 * x + 1] += hi_f(v[u][x]);
+        }
+    }
+    __builtin_amdgcn_wave_barrier();   // this slab's list is read before the next one is written
+  }
+  // entries r = 0 .. R-1 of the wave, then the waves in order
+#pragma unroll
+  for (int x = 0; x < 8; ++x)
+#pragma unroll
+    for (int off = CPR; off < kWave; off <<= 1) acc[x] += __shfl_xor(acc[x], off);
+  if (r == 0) {
+#pragma unroll
+    for (int x = 0; x < 8; ++x) part[w][8 * c + x] = acc[x];
+  }
+  if (lane == 0) part[w][H] = static_cast<float>(deg);
+  __syncthreads();
+  if (tid <= H) {
+    float t = part[0][tid];
+#pragma unroll
+    for (int ww = 1; ww < NW; ++ww) t += part[ww][tid];
+    if (tid < H)
+      rec[((size_t)e * sr + i) * H + tid] = t;
+    else
+      rec[(size_t)E * sr * H + (size_t)e * sr + i] = t;
+  }
+}
+#endif
 }  // namespace dev
 
 namespace {
@@ -474,12 +572,26 @@ hipError_t launch_super_fwd(int n_pad, int H, int E, int s, const void* rows, co
 // The long contraction of the fused supernode steps (bf16, H = 32 or 64):
 // rec = [P_e (sr x H) | deg_e (sr)] for the first sr rows of the slice, the
 // per-chunk partials in ws.
+
+#ifndef GGNN_SUPER_GATHER
+#define GGNN_SUPER_GATHER 1
+#endif
 hipError_t launch_super_long_fused(int n_pad, int H, int E, int s, int sr, const void* bits, const void* Z, bool zfm,
                                    float* ws, float* rec, hipStream_t st) {
   if (sr != 16 && sr != 32) return hipErrorInvalidValue;
   const uint8_t* b = static_cast<const uint8_t*>(bits);
   const dev::bf16s* z = static_cast<const dev::bf16s*>(Z);
   using S = dev::bf16s;
+  if (GGNN_SUPER_GATHER && !zfm && (H == 32 || H == 64) && n_pad % 64 == 0) {
+    // forward: the row slice's sums as a gather (one workgroup of 16 waves per row)
+    if (H == 32)
+      hipLaunchKernelGGL((dev::super_gather_kernel<32>), dim3(E * sr), dim3(64 * dev::kSnGatherWaves), 0, st, b, z,
+                         rec, n_pad, E, s, sr);
+    else
+      hipLaunchKernelGGL((dev::super_gather_kernel<64>), dim3(E * sr), dim3(64 * dev::kSnGatherWaves), 0, st, b, z,
+                         rec, n_pad, E, s, sr);
+    return hipGetLastError();
+  }
   if (H == 32)
     return zfm ? super_long<S, 32, true>(b, z, ws, rec, n_pad, E, s, sr, st)
                : super_long<S, 32, false>(b, z, ws, rec, n_pad, E, s, sr, st);
