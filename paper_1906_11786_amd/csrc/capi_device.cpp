@@ -564,8 +564,12 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
         // supernode rows: C_e^T da over all nodes; then the fused reverse step
         // with the transposed row slice as a fourth block
         prof_begin(s);
-        err = impl_bf16::launch_super_long_fused(m->n_pad, m->H, m->E, m->n_super, m->n_super_active,
-                                                 m->super_cols_t, da_b[cur], true, sn_scr, sn_rec, s);
+        if (impl_bf16::super_gather_rev_applies(m->n_pad, m->H))
+          err = impl_bf16::launch_super_gather_rev(m->n_pad, m->H, m->E, m->n_super, m->n_super_active,
+                                                   m->super_cols_t, Gs(t), m->Wi, sn_rec, s);
+        else
+          err = impl_bf16::launch_super_long_fused(m->n_pad, m->H, m->E, m->n_super, m->n_super_active,
+                                                   m->super_cols_t, da_b[cur], true, sn_scr, sn_rec, s);
         prof_end(s, PROF_SUPER_LONG);
         if (err == hipSuccess) {
           const bool prev = t > 0;

@@ -125,6 +125,11 @@ bool step_sn_fusable(int n_pad, int B, int H, int E);
 // (zfm: Z feature-major); ws holds the per-chunk partials.
 hipError_t launch_super_long_fused(int n_pad, int H, int E, int s, int sr, const void* bits, const void* Z, bool zfm,
                                    float* ws, float* rec, hipStream_t st);
+// The fused reverse step's supernode record from the step's gate gradients G^ (node-major [n_pad][3H])
+// and Wi: (sum over the listed out-edges of G^ rows) Wi^T (bf16, H = 32 or 64).
+bool super_gather_rev_applies(int n_pad, int H);
+hipError_t launch_super_gather_rev(int n_pad, int H, int E, int s, int sr, const void* bits, const void* ghat,
+                                   const void* Wi, float* rec, hipStream_t st);
 hipError_t launch_step_fwd_bits_gru_sn(int n_pad, int B, int H, int E, const void* bits, const void* X, const void* W,
                                        const void* Wt, const float* bias, float* a, const void* Wi, const void* U,
                                        const float* bg, void* h_out, void* saved, const SnStep& sn, hipStream_t st);

@@ -417,6 +417,108 @@ __global__ __launch_bounds__(64 * kSnGatherWaves) void super_gather_kernel(const
       rec[(size_t)E * sr * H + (size_t)e * sr + i] = t;
   }
 }
+
+// The supernode rows' record of the fused reverse step from the GRU reverse's gate gradients: the
+// message gradient of supernode j is sum_i C_e[i][j] da[i] over its out-edges, and da = G^ Wi^T row
+// by row, so the record is (sum_i C_e[i][j] G^[i]) Wi^T: the listed rows of G^ (node-major [n][3H],
+// contiguous 3H-element rows, where da is stored feature-major and its gathers touch one line per
+// feature) are summed in fp32 in column order as above, then multiplied by Wi once per (e, j).  The
+// sum skips da's bf16 rounding; it is otherwise the same linear map.  Lane (r, c) adds 8 gate columns
+// of entries r, r + R, ... (R = 64 / (3H/8) rows per load); the partial sums of all lanes and waves
+// meet in LDS and are added in (wave, r) order.
+template <int H>
+__global__ __launch_bounds__(64 * kSnGatherWaves) void super_gather_rev_kernel(const uint8_t* __restrict__ bits,
+                                                                               const bf16s* __restrict__ ghat,
+                                                                               const bf16s* __restrict__ Wi,
+                                                                               float* __restrict__ rec, int n_pad,
+                                                                               int E, int s, int sr) {
+  constexpr int NW = kSnGatherWaves, SLAB = 64 * 32, G3 = 3 * H;
+  constexpr int CPR = G3 / 8, R = 64 / CPR;   // lanes per listed row, rows per load instruction
+  constexpr int UB = 8;
+  __shared__ int lst[NW][SLAB];
+  __shared__ float part[NW][R][G3];
+  __shared__ float gsum[G3];
+  __shared__ int degs[NW];
+  const int e = blockIdx.x / sr, j = blockIdx.x % sr;
+  const int tid = threadIdx.x, w = tid / kWave, lane = tid % kWave;
+  const uint32_t* row = reinterpret_cast<const uint32_t*>(bits + ((size_t)e * s + j) * (size_t)(n_pad / 8));
+  const int ndw = n_pad / 32;
+  const int d0 = w * ndw / NW, d1 = (w + 1) * ndw / NW;
+  const int r = lane / CPR, c = lane % CPR;
+  const bool active = r < R;
+  float acc[8];
+#pragma unroll
+  for (int x = 0; x < 8; ++x) acc[x] = 0.f;
+  int deg = 0;
+  for (int base = d0; base < d1; base += kWave) {
+    const int d = base + lane;
+    uint32_t wd = d < d1 ? row[d] : 0u;
+    const int cnt = __popc(wd);
+    int incl = cnt;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int v = __shfl_up(incl, off);
+      if (lane >= off) incl += v;
+    }
+    const int total = __shfl(incl, kWave - 1);
+    int pos = incl - cnt;
+    while (wd != 0u) {
+      const int b = __ffs(wd) - 1;
+      wd &= wd - 1u;
+      lst[w][pos++] = d * 32 + b;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    deg += total;
+    for (int k0 = 0; k0 < total; k0 += R * UB) {
+      u32x4 v[UB];
+#pragma unroll
+      for (int u = 0; u < UB; ++u) {
+        const int k = k0 + u * R + r;
+        v[u] = active && k < total ? *reinterpret_cast<const u32x4*>(ghat + (size_t)lst[w][k] * G3 + 8 * c)
+                                   : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int u = 0; u < UB; ++u)
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          acc[2 * x] += lo_f(v[u][x]);
+          acc[2 * x + 1] += hi_f(v[u][x]);
+        }
+    }
+    __builtin_amdgcn_wave_barrier();   // this slab's list is read before the next one is written
+  }
+  if (active) {
+#pragma unroll
+    for (int x = 0; x < 8; ++x) part[w][r][8 * c + x] = acc[x];
+  }
+  if (lane == 0) degs[w] = deg;
+  __syncthreads();
+  for (int col = tid; col < G3; col += 64 * NW) {
+    float t = 0.f;
+    for (int ww = 0; ww < NW; ++ww)
+#pragma unroll
+      for (int rr = 0; rr < R; ++rr) t += part[ww][rr][col];
+    gsum[col] = t;
+  }
+  __syncthreads();
+  if (tid < H) {
+    // da feature tid of the summed rows: sum over the gate columns of G^ sum x Wi[tid][.]
+    const bf16s* wr = Wi + (size_t)tid * G3;
+    float t = 0.f;
+    for (int col = 0; col < G3; col += 8) {
+      const u32x4 wv = *reinterpret_cast<const u32x4*>(wr + col);
+#pragma unroll
+      for (int x = 0; x < 4; ++x) t += gsum[col + 2 * x] * lo_f(wv[x]) + gsum[col + 2 * x + 1] * hi_f(wv[x]);
+    }
+    rec[((size_t)e * sr + j) * H + tid] = t;
+  } else if (tid == H) {
+    int dsum = 0;
+    for (int ww = 0; ww < NW; ++ww) dsum += degs[ww];
+    rec[(size_t)E * sr * H + (size_t)e * sr + j] = static_cast<float>(dsum);
+  }
+}
 #endif
 }  // namespace dev
 
@@ -599,6 +701,23 @@ hipError_t launch_super_long_fused(int n_pad, int H, int E, int s, int sr, const
     return zfm ? super_long<S, 64, true>(b, z, ws, rec, n_pad, E, s, sr, st)
                : super_long<S, 64, false>(b, z, ws, rec, n_pad, E, s, sr, st);
   return hipErrorInvalidValue;
+}
+bool super_gather_rev_applies(int n_pad, int H) {
+  return GGNN_SUPER_GATHER && (H == 32 || H == 64) && n_pad % 64 == 0;
+}
+hipError_t launch_super_gather_rev(int n_pad, int H, int E, int s, int sr, const void* bits, const void* ghat,
+                                   const void* Wi, float* rec, hipStream_t st) {
+  if ((sr != 16 && sr != 32) || !super_gather_rev_applies(n_pad, H)) return hipErrorInvalidValue;
+  const uint8_t* b = static_cast<const uint8_t*>(bits);
+  const dev::bf16s* g = static_cast<const dev::bf16s*>(ghat);
+  const dev::bf16s* w = static_cast<const dev::bf16s*>(Wi);
+  if (H == 32)
+    hipLaunchKernelGGL((dev::super_gather_rev_kernel<32>), dim3(E * sr), dim3(64 * dev::kSnGatherWaves), 0, st, b, g,
+                       w, rec, n_pad, E, s, sr);
+  else
+    hipLaunchKernelGGL((dev::super_gather_rev_kernel<64>), dim3(E * sr), dim3(64 * dev::kSnGatherWaves), 0, st, b, g,
+                       w, rec, n_pad, E, s, sr);
+  return hipGetLastError();
 }
 #endif
 
