@@ -423,8 +423,8 @@ ggnn_status ggnn_backward(const ggnn_model* model, const ggnn_activations* act,
  * with the launch kind (ggnn_profile_name: "step_fwd", "step_fwd_gru",
  * "gru_fwd", "transform_fwd", "banded_fwd", "gru_rev", "step_rev",
  * "step_rev_gru", "banded_rev", "transform_rev_dx", "wgrad_gru",
- * "wgrad_transform", "reduce", "super_long" (the supernode rows' long contraction of a fused
- * supernode step, with its reduction), "super" (the stand-alone slice kernels of one step's share);
+ * "wgrad_transform", "reduce", "super_record" (the supernode rows' record of a fused supernode
+ * step: their per-type sums over all nodes), "super" (the stand-alone slice kernels of one step's share);
  * the "_gru" forms are band steps with the GRU
  * or GRU reverse fused into the same kernel).  Launches made while the stream
  * is being captured into a HIP graph, and launches beyond `capacity`, are not

@@ -462,7 +462,7 @@ ggnn_status ggnn_forward(const ggnn_model* m, const ggnn_activations* act, void*
       prof_begin(s);
       err = impl_bf16::launch_super_long_fused(m->n_pad, m->H, m->E, m->n_super, m->n_super_active, m->super_rows,
                                                Xt, false, sn_scr, sn_rec, s);
-      prof_end(s, PROF_SUPER_LONG);
+      prof_end(s, PROF_SUPER_RECORD);
       if (err == hipSuccess) {
         prof_begin(s);
         err = impl_bf16::launch_step_fwd_bits_gru_sn(m->n_pad, m->B, m->H, m->E, m->band, Xt, m->W, m->Wt, m->bias,
@@ -570,7 +570,7 @@ ggnn_status ggnn_backward(const ggnn_model* m, const ggnn_activations* act, cons
         else
           err = impl_bf16::launch_super_long_fused(m->n_pad, m->H, m->E, m->n_super, m->n_super_active,
                                                    m->super_cols_t, da_b[cur], true, sn_scr, sn_rec, s);
-        prof_end(s, PROF_SUPER_LONG);
+        prof_end(s, PROF_SUPER_RECORD);
         if (err == hipSuccess) {
           const bool prev = t > 0;
           prof_begin(s);

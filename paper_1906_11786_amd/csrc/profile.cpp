@@ -28,7 +28,7 @@ struct State {
 const char* const kNames[PROF_COUNT] = {
     "step_fwd",        "step_fwd_gru",  "gru_fwd",        "transform_fwd", "banded_fwd",
     "gru_rev",         "step_rev",      "step_rev_gru",   "banded_rev",    "transform_rev_dx",
-    "wgrad_gru",       "wgrad_transform", "reduce",      "super_long",    "super"};
+    "wgrad_gru",       "wgrad_transform", "reduce",      "super_record",  "super"};
 
 void release() {
   for (Record& r : g_prof.recs) {

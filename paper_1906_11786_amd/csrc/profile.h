@@ -21,7 +21,7 @@ enum ProfId {
   PROF_WGRAD_GRU,         // GRU weight-gradient contraction
   PROF_WGRAD_TRANSFORM,   // message-transform weight-gradient contraction
   PROF_REDUCE,            // fixed-order reduction of weight-gradient partials
-  PROF_SUPER_LONG,        // supernode rows' long contraction (fused supernode steps; with its reduction)
+  PROF_SUPER_RECORD,      // supernode rows' record of a fused supernode step (gather, or long contraction + sum)
   PROF_SUPER,             // stand-alone supernode slice kernels (forward or reverse share of one step)
   PROF_COUNT
 };
