@@ -181,24 +181,43 @@ __global__ __launch_bounds__(WAVES * kWave) void gru_bwd_kernel(const float* __r
   const bool valid = n0 < n_pad;
   const int node = n0 + q;
 
-  if constexpr (LDSW) {
-    for (int lin = tid; lin < 2 * H * (3 * H / V); lin += NT) {
-      const int mat = lin / (H * (3 * H / V)), rem = lin % (H * (3 * H / V));
-      const int r = rem / (3 * H / V), c = (rem % (3 * H / V)) * V;
-      const u32x4 w = *reinterpret_cast<const u32x4*>((mat ? U : Wi) + (size_t)r * 3 * H + c);
-      const S* pw = reinterpret_cast<const S*>(&w);
+  // The node's inputs are loaded first, so that they are in flight while the
+  // weights are staged (all of a thread's weight loads issued before its
+  // LDS writes).
+  f32x4 gg[MTL];
+  GruBwdIn<S, H> in;
+  if (valid) {
 #pragma unroll
-      for (int i = 0; i < V; i += 4)
-        put4<S>(wl, gru_rev_idx<S, H>(mat, r / 16, (c + i) / H, ((c + i) % H) / 32), r % 16, (c + i) % H, pw + i);
+    for (int m = 0; m < MTL; ++m) gg[m] = *reinterpret_cast<const f32x4*>(gin + (size_t)node * H + 16 * m + 4 * g);
+    in.load(saved, h, node, g);
+  }
+  if constexpr (LDSW) {
+    constexpr int UNITS = 2 * H * (3 * H / V), ITS = (UNITS + NT - 1) / NT;
+    u32x4 w[ITS];
+#pragma unroll
+    for (int it = 0; it < ITS; ++it) {
+      const int lin = it * NT + tid;
+      if (lin < UNITS) {
+        const int mat = lin / (H * (3 * H / V)), rem = lin % (H * (3 * H / V));
+        const int r = rem / (3 * H / V), c = (rem % (3 * H / V)) * V;
+        w[it] = *reinterpret_cast<const u32x4*>((mat ? U : Wi) + (size_t)r * 3 * H + c);
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < ITS; ++it) {
+      const int lin = it * NT + tid;
+      if (lin < UNITS) {
+        const int mat = lin / (H * (3 * H / V)), rem = lin % (H * (3 * H / V));
+        const int r = rem / (3 * H / V), c = (rem % (3 * H / V)) * V;
+        const S* pw = reinterpret_cast<const S*>(&w[it]);
+#pragma unroll
+        for (int i = 0; i < V; i += 4)
+          put4<S>(wl, gru_rev_idx<S, H>(mat, r / 16, (c + i) / H, ((c + i) % H) / 32), r % 16, (c + i) % H, pw + i);
+      }
     }
     __syncthreads();
   }
   if (!valid) return;   // no barrier follows
-  f32x4 gg[MTL];
-#pragma unroll
-  for (int m = 0; m < MTL; ++m) gg[m] = *reinterpret_cast<const f32x4*>(gin + (size_t)node * H + 16 * m + 4 * g);
-  GruBwdIn<S, H> in;
-  in.load(saved, h, node, g);
   if constexpr (LDSW) {
     auto wf = [&](int which, int row, int gate, int kk) __attribute__((always_inline)) {
       return load_fragi<S>(wl, gru_rev_idx<S, H>(which, row / 16, gate, kk), lane);
