@@ -424,8 +424,10 @@ __global__ __launch_bounds__(64 * kSnGatherWaves) void super_gather_kernel(const
 // contiguous 3H-element rows, where da is stored feature-major and its gathers touch one line per
 // feature) are summed in fp32 in column order as above, then multiplied by Wi once per (e, j).  The
 // sum skips da's bf16 rounding; it is otherwise the same linear map.  Lane (r, c) adds 8 gate columns
-// of entries r, r + R, ... (R = 64 / (3H/8) rows per load); the partial sums of all lanes and waves
-// meet in LDS and are added in (wave, r) order.
+// of entries r, r + R, ... (R = 64 / (3H/8) rows per load); a wave's R partial sums are added in
+// order, then the waves' sums in a fixed order.  For the product, thread (f, p) of 16 per output
+// feature f holds gate columns 3H/16 p .. of row f of Wi (loaded at the start, in flight during the
+// gathers) and the 16 partial dot products are added by a fixed butterfly over the lanes.
 template <int H>
 __global__ __launch_bounds__(64 * kSnGatherWaves) void super_gather_rev_kernel(const uint8_t* __restrict__ bits,
                                                                                const bf16s* __restrict__ ghat,
@@ -436,7 +438,7 @@ __global__ __launch_bounds__(64 * kSnGatherWaves) void super_gather_rev_kernel(c
   constexpr int CPR = G3 / 8, R = 64 / CPR;   // lanes per listed row, rows per load instruction
   constexpr int UB = 8;
   __shared__ int lst[NW][SLAB];
-  __shared__ float part[NW][R][G3];
+  __shared__ float part[NW][G3];
   __shared__ float gsum[G3];
   __shared__ int degs[NW];
   const int e = blockIdx.x / sr, j = blockIdx.x % sr;
@@ -446,6 +448,15 @@ __global__ __launch_bounds__(64 * kSnGatherWaves) void super_gather_rev_kernel(c
   const int d0 = w * ndw / NW, d1 = (w + 1) * ndw / NW;
   const int r = lane / CPR, c = lane % CPR;
   const bool active = r < R;
+  // Wi row f = tid / 16, gate columns CW p .. CW p + CW - 1 (p = tid % 16), as CW / 2 dwords
+  constexpr int CW = G3 / 16;
+  const int wf = tid / 16, wp = tid % 16;
+  uint32_t wreg[CW / 2];
+  if (wf < H) {
+    const uint32_t* wsrc = reinterpret_cast<const uint32_t*>(Wi + (size_t)wf * G3 + CW * wp);
+#pragma unroll
+    for (int x = 0; x < CW / 2; ++x) wreg[x] = wsrc[x];
+  }
   float acc[8];
 #pragma unroll
   for (int x = 0; x < 8; ++x) acc[x] = 0.f;
@@ -489,31 +500,43 @@ __global__ __launch_bounds__(64 * kSnGatherWaves) void super_gather_rev_kernel(c
     }
     __builtin_amdgcn_wave_barrier();   // this slab's list is read before the next one is written
   }
-  if (active) {
+  // entries r = 0 .. R-1 of the wave (lanes c + CPR r) added in order into the lanes of r = 0, then the
+  // waves' sums in order: four threads per column add four waves each, combined by a fixed butterfly
 #pragma unroll
-    for (int x = 0; x < 8; ++x) part[w][r][8 * c + x] = acc[x];
+  for (int x = 0; x < 8; ++x) {
+    float t = acc[x];
+#pragma unroll
+    for (int rr = 1; rr < R; ++rr) t += __shfl(acc[x], c + CPR * rr);
+    acc[x] = t;
+  }
+  if (r == 0) {
+#pragma unroll
+    for (int x = 0; x < 8; ++x) part[w][8 * c + x] = acc[x];
   }
   if (lane == 0) degs[w] = deg;
   __syncthreads();
-  for (int col = tid; col < G3; col += 64 * NW) {
+  static_assert(NW % 4 == 0 && (4 * G3) % kWave == 0, "whole waves per column group");
+  if (tid < 4 * G3) {
+    const int col = tid / 4, qp = tid % 4;
     float t = 0.f;
-    for (int ww = 0; ww < NW; ++ww)
 #pragma unroll
-      for (int rr = 0; rr < R; ++rr) t += part[ww][rr][col];
-    gsum[col] = t;
+    for (int ww = qp * (NW / 4); ww < (qp + 1) * (NW / 4); ++ww) t += part[ww][col];
+    t += __shfl_xor(t, 1);
+    t += __shfl_xor(t, 2);
+    if (qp == 0) gsum[col] = t;
   }
   __syncthreads();
-  if (tid < H) {
-    // da feature tid of the summed rows: sum over the gate columns of G^ sum x Wi[tid][.]
-    const bf16s* wr = Wi + (size_t)tid * G3;
+  if (wf < H) {
+    // da feature wf of the summed rows: the gate columns of G^'s sum times Wi[wf][.]
     float t = 0.f;
-    for (int col = 0; col < G3; col += 8) {
-      const u32x4 wv = *reinterpret_cast<const u32x4*>(wr + col);
 #pragma unroll
-      for (int x = 0; x < 4; ++x) t += gsum[col + 2 * x] * lo_f(wv[x]) + gsum[col + 2 * x + 1] * hi_f(wv[x]);
-    }
-    rec[((size_t)e * sr + j) * H + tid] = t;
-  } else if (tid == H) {
+    for (int x = 0; x < CW / 2; ++x)
+      t += gsum[CW * wp + 2 * x] * lo_f(wreg[x]) + gsum[CW * wp + 2 * x + 1] * hi_f(wreg[x]);
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) t += __shfl_xor(t, off);
+    if (wp == 0) rec[((size_t)e * sr + j) * H + wf] = t;
+  }
+  if (tid == 0) {
     int dsum = 0;
     for (int ww = 0; ww < NW; ++ww) dsum += degs[ww];
     rec[(size_t)E * sr * H + (size_t)e * sr + j] = static_cast<float>(dsum);
