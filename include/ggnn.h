@@ -397,15 +397,17 @@ size_t ggnn_super_model_workspace_bytes(const ggnn_model* model);
  * With supernodes, in bf16 at H <= 64 with n_super_active <= 32 and a grid small enough for the
  * two-group fused steps (ggnn_super_fusable), the slices run inside the fused step kernels: the
  * column slice as a fourth block next to the three of Eq. 3 (the 32 supernodes' states staged once per
- * workgroup), and the supernode rows' aggregate R_e X from one long contraction per step; otherwise the
- * slice kernels of ggnn_super_propagate run between the band step and the GRU. */
+ * workgroup), and the supernode rows' aggregate R_e X from one launch per step before it (a gather of
+ * the node states each slice row lists); otherwise the slice kernels of ggnn_super_propagate run between
+ * the band step and the GRU. */
 ggnn_status ggnn_forward(const ggnn_model* model, const ggnn_activations* act, void* stream);
 
 /* Reverse pass for L with dL/dX_T given in grads->dX: for t = T-1..0,
  *   da, dh, G^_t = gru_update_bwd node pass(dX);
  *   with supernodes: the slices' reverse (fused as in ggnn_forward: the transposed row slice as a fourth
- *   block, the supernode rows' message gradients C_e^T da from one long contraction per step, all of it
- *   in dM; otherwise ggnn_super_propagate_bwd adds its share to dh, dW and dbias first);
+ *   block, the supernode rows' message gradients C_e^T da from one launch per step before it (the
+ *   listed rows of the step's gate gradients G^ summed, then times Wi^T: da = G^ Wi^T row by row), all
+ *   of it in dM; otherwise ggnn_super_propagate_bwd adds its share to dh, dW and dbias first);
  *   dense band: dM_t = banded_propagate_bwd(da); dX = dh + sum_e dM_t,e W_e^T;
  *   bit band:   dM_t, dX = banded_step_bits_bwd(da, dX_in = dh) (one kernel);
  * then the weight gradients as single contractions over all T * n_pad rows:
