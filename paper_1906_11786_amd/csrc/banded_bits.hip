@@ -241,8 +241,8 @@ struct BitsCfg {
 // column slice, edges from a supernode into this row; reverse the
 // transposed row slice, edges from this node into a supernode).  The rows of
 // the supernodes themselves get their whole per-type aggregate from the
-// record sn_rec = [P_e (sn_sr x H) | deg_e (sn_sr)] of the long contraction over
-// all nodes (forward R_e X, reverse C_e^T da): the wave holding rows 0..31
+// record sn_rec = [P_e (sn_sr x H) | deg_e (sn_sr)], their sums over all nodes
+// (forward R_e X, reverse C_e^T da) from a launch before the step: the wave holding rows 0..31
 // copies P_e of its rows into LDS (global -> LDS, issued at the top of the
 // type, waited for after the aggregation) and adds it to the aggregate (the
 // record's first sn_sr rows, 16 or 32: the supernodes with edges).

@@ -47,9 +47,9 @@ hipError_t reduce_or_defer(const float* part, float* out, int nsplit, int count,
 // Supernode share of a fused bit-band step (the first 32 nodes are
 // supernodes): the slice bits of the step's direction, [E][n_pad][s/8] (the
 // column slice forward, the transposed row slice reverse), and the record
-// [P_e (sr x H) | deg_e (sr)] of the long contraction over all nodes that
-// gives the first sr supernode rows their per-type aggregate
-// (launch_super_long_fused).
+// [P_e (sr x H) | deg_e (sr)], the sums over all nodes that give the first sr
+// supernode rows their per-type aggregate (launch_super_long_fused forward,
+// launch_super_gather_rev or launch_super_long_fused reverse).
 struct SnStep {
   const void* bits;
   const float* rec;
@@ -120,9 +120,10 @@ GGNN_DT_LAUNCHERS
 // this size, and the forward step (with its GRU) and reverse step (with the
 // previous step's GRU reverse when da_prev is not NULL) carrying it.
 bool step_sn_fusable(int n_pad, int B, int H, int E);
-// The long contraction of the fused supernode steps: rec = [P_e (sr x H) |
-// deg_e (sr)], P_e = bits_e Z over all nodes for the first sr slice rows
-// (zfm: Z feature-major); ws holds the per-chunk partials.
+// The record of the fused supernode steps: rec = [P_e (sr x H) | deg_e (sr)],
+// P_e = bits_e Z over all nodes for the first sr slice rows (zfm: Z
+// feature-major), as a gather where Z is node-major (n_pad a multiple of 64),
+// else as the long contraction with its per-chunk partials in ws.
 hipError_t launch_super_long_fused(int n_pad, int H, int E, int s, int sr, const void* bits, const void* Z, bool zfm,
                                    float* ws, float* rec, hipStream_t st);
 // The fused reverse step's supernode record from the step's gate gradients G^ (node-major [n_pad][3H])

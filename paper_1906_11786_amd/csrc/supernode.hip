@@ -332,10 +332,10 @@ __global__ __launch_bounds__(256) void small_gemm_kernel(SmallGemm p) {
 // prefix count over the lanes), and adds the listed rows in that order in fp32, lane (r, c) taking 8
 // features of entries r, r + R, ... (R rows per load instruction); the waves' partial sums are then
 // combined in wave order, so the result depends only on the row (no float atomics).  The reverse
-// record (C_e^T da, da feature-major) stays on the long contraction: gathered, each listed node costs
-// one scattered element per feature row, and every layout of those loads tried (one node of all
-// features per instruction, 16 nodes of 4 features, the row split over 8 workgroups) ran slower than
-// the contraction's contiguous staging.
+// record is gathered from the gate gradients G^ instead of da (super_gather_rev_kernel below): da is
+// feature-major, so a gather of it costs one scattered element per feature row and listed node, and
+// every layout of those loads tried (one node of all features per instruction, 16 nodes of 4
+// features, the row split over 8 workgroups) ran slower than the long contraction's staging.
 constexpr int kSnGatherWaves = 16;
 template <int H>
 __global__ __launch_bounds__(64 * kSnGatherWaves) void super_gather_kernel(const uint8_t* __restrict__ bits,
@@ -694,9 +694,11 @@ hipError_t launch_super_fwd(int n_pad, int H, int E, int s, const void* rows, co
 }
 
 #if GGNN_DT_BF16
-// The long contraction of the fused supernode steps (bf16, H = 32 or 64):
-// rec = [P_e (sr x H) | deg_e (sr)] for the first sr rows of the slice, the
-// per-chunk partials in ws.
+// The record of the fused supernode steps (bf16, H = 32 or 64): rec =
+// [P_e (sr x H) | deg_e (sr)] for the first sr rows of the slice, from the
+// forward gather (Z = X node-major) where it applies, else from the long
+// contraction with its per-chunk partials in ws (the reverse takes
+// launch_super_gather_rev where that applies).
 
 #ifndef GGNN_SUPER_GATHER
 #define GGNN_SUPER_GATHER 1
