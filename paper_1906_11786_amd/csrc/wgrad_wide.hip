@@ -391,25 +391,30 @@ __device__ __forceinline__ void gru_wgrad256_body(const float* __restrict__ a, c
   for (int c = 0; c < nchunks; ++c) {
     if (c + 1 < nchunks) wait_copies<PER>();
     else wait_copies<0>();
+    if constexpr (KIND == 2) {
+      // r * h of the chunk, formed once (in fp32, rounded to bf16) and
+      // written over the r tile (h and r share one layout): each lane forms
+      // the 16-byte units its own copies brought in (the same LDS offsets in
+      // both tiles), so the wait for its own copies is enough and the
+      // products are shared by the barrier below.  (Formed per fragment
+      // instead, every element was formed by four waves and the vector ALU
+      // work bound these tiles; formed after the barrier by any thread, a
+      // second barrier per chunk followed.)
+      asm volatile("" ::: "memory");
+      unsigned char* sb = ring + slot * SLOT;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int off = 2 * (2 * wave + j) * H * 2 + 16 * lane;
+        const u32x4 hv = *reinterpret_cast<const u32x4*>(sb + off);
+        u32x4 rv = *reinterpret_cast<const u32x4*>(sb + OFF_R + off);
+#pragma unroll
+        for (int x = 0; x < 4; ++x) rv[x] = pk2(lo_f(hv[x]) * lo_f(rv[x]), hi_f(hv[x]) * hi_f(rv[x]));
+        *reinterpret_cast<u32x4*>(sb + OFF_R + off) = rv;
+      }
+    }
     if (wave == 0) pace = pace_split(prog + split * 8, tile, sibs, c, lane, pace);
     __syncthreads();
     if (c + 2 < nchunks) issue(c + 2, slot == 0 ? 2 : slot - 1);
-    if constexpr (KIND == 2) {
-      // r * h of the chunk, formed once (in fp32, rounded to bf16) and
-      // written over the r tile (h and r share one layout); formed per
-      // fragment instead, every element was formed by four waves, and the
-      // vector ALU work bound these tiles.
-      unsigned char* sb = ring + slot * SLOT;
-#pragma unroll
-      for (int u = 64 * wave + lane; u < KC * H / 8; u += NT) {
-        const u32x4 hv = *reinterpret_cast<const u32x4*>(sb + 16 * u);
-        u32x4 rv = *reinterpret_cast<const u32x4*>(sb + OFF_R + 16 * u);
-#pragma unroll
-        for (int x = 0; x < 4; ++x) rv[x] = pk2(lo_f(hv[x]) * lo_f(rv[x]), hi_f(hv[x]) * hi_f(rv[x]));
-        *reinterpret_cast<u32x4*>(sb + OFF_R + 16 * u) = rv;
-      }
-      __syncthreads();
-    }
     compute(slot);
     slot = slot == 2 ? 0 : slot + 1;
   }
