@@ -366,6 +366,23 @@ __device__ __forceinline__ void store_tiles16(bf16s* row32, u32x2 t0, u32x2 t1, 
   }
   *reinterpret_cast<u32x4*>(row32 + 8 * g) = u32x4{x[0], x[1], y[0], y[1]};
 }
+// The reverse: one 16-byte load per lane of features 8g .. 8g + 7 of the 32,
+// handed out as store_tiles16 takes them (both swaps are their own inverse):
+// t[0] = features 4g .. 4g + 3 of the first tile, t[1] of the second.
+__device__ __forceinline__ void load_tiles16(const bf16s* row32, int g, u32x2 (&t)[2]) {
+  const u32x4 v = *reinterpret_cast<const u32x4*>(row32 + 8 * g);
+#pragma unroll
+  for (int d = 0; d < 2; ++d) {
+    const auto r16 = __builtin_amdgcn_permlane16_swap(v[d], v[2 + d], false, false);
+    const auto r32 = __builtin_amdgcn_permlane32_swap(r16[0], r16[1], false, false);
+    t[0][d] = r32[0];
+    t[1][d] = r32[1];
+  }
+}
+__device__ __forceinline__ f32x4 unpack4(u32x2 v) {
+  return f32x4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xFFFF0000u), __uint_as_float(v.y << 16),
+               __uint_as_float(v.y & 0xFFFF0000u)};
+}
 
 // ---------------------------------------------------------------------------
 // Forward for large H (bf16, H >= 128), the arithmetic of gru_fwd_kernel
@@ -602,12 +619,18 @@ __global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restric
   S* gh = ghat + (size_t)node * 3 * H;
   if (valid) {
     float zv[8], nv[8];
+    u32x2 zp[2], np[2], hp[2];   // tiles m, m + 1 of z, n, h (16-byte loads, load_tiles16)
 #pragma unroll
     for (int m = 0; m < MTL; ++m) {
       const int f = 16 * m + 4 * g;
       const f32x4 gg = *reinterpret_cast<const f32x4*>(gin + (size_t)node * H + f);
-      const f32x4 z4 = load4f(sv + H + f), n4 = load4f(sv + 2 * H + f);
-      const f32x4 h4 = load4f(h + (size_t)node * H + f);
+      if (m % 2 == 0) {
+        load_tiles16(sv + H + 16 * m, g, zp);
+        load_tiles16(sv + 2 * H + 16 * m, g, np);
+        load_tiles16(h + (size_t)node * H + 16 * m, g, hp);
+      }
+      const f32x4 z4 = unpack4(zp[m % 2]), n4 = unpack4(np[m % 2]);
+      const f32x4 h4 = unpack4(hp[m % 2]);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const float dn = gg[j] * (1.f - z4[j]);
@@ -638,14 +661,19 @@ __global__ __launch_bounds__(512) void gru_bwd_big_kernel(const float* __restric
 
   // Pass 1: blocks m = 0 .. MTL-1 of U_n (unrolled: static register indices).
   float rv[8];
+  u32x2 rp[2], hq[2];   // tiles m, m + 1 of r and h (16-byte loads)
 #pragma unroll
   for (int m = 0; m < MTL; ++m) {
     if (valid) {
+      if (m % 2 == 0) {
+        load_tiles16(sv + 16 * m, g, rp);
+        load_tiles16(h + (size_t)node * H + 16 * m, g, hq);
+      }
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) mma(acc, load_fragi<S>(lds_all + m * U1 * 8, kk, lane), gf[2][kk]);
       const int f = 16 * m + 4 * g;
-      const f32x4 r4 = load4f(sv + f), h4 = load4f(h + (size_t)node * H + f);
+      const f32x4 r4 = unpack4(rp[m % 2]), h4 = unpack4(hq[m % 2]);
       float rloc[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
