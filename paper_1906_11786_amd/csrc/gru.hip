@@ -344,45 +344,6 @@ __global__ __launch_bounds__(256) void gru_pack_kernel(const S* __restrict__ Wi,
   *reinterpret_cast<u32x4*>(out + (size_t)u * 8) = v;
 }
 
-// Node-major stores of two consecutive 16-feature tiles of a wave's 16 nodes
-// (lane (q, g) holds features 4g .. 4g + 3 of each tile, rounded to bf16 and
-// packed: t0 the first tile, t1 the second) as one 16-byte store per lane:
-// after one permlane32 and one permlane16 swap per dword, lane group g holds
-// features 8g .. 8g + 7 of the 32 (groups 0, 1 the first tile's, 2, 3 the
-// second's).  Each node row then gets 64 contiguous bytes per instruction
-// instead of 32 from 8-byte stores, which streams ~20% faster here (the
-// reverse's G^ stores; in the forward, the h', r, z, n stores paired this way
-// measured no gain and cost registers).
-__device__ __forceinline__ void store_tiles16(bf16s* row32, u32x2 t0, u32x2 t1, int g) {
-  uint32_t x[2], y[2];
-#pragma unroll
-  for (int d = 0; d < 2; ++d) {
-    // rows of 16 lanes: (A0 A1 A2 A3), (B0 B1 B2 B3) -> (A0 A1 B0 B1), (A2 A3 B2 B3)
-    const auto r32 = __builtin_amdgcn_permlane32_swap(t0[d], t1[d], false, false);
-    // -> (A0 A2 B0 B2), (A1 A3 B1 B3): lane group g holds (first, second) half of its 8 features
-    const auto r16 = __builtin_amdgcn_permlane16_swap(r32[0], r32[1], false, false);
-    x[d] = r16[0];
-    y[d] = r16[1];
-  }
-  *reinterpret_cast<u32x4*>(row32 + 8 * g) = u32x4{x[0], x[1], y[0], y[1]};
-}
-// The reverse: one 16-byte load per lane of features 8g .. 8g + 7 of the 32,
-// handed out as store_tiles16 takes them (both swaps are their own inverse):
-// t[0] = features 4g .. 4g + 3 of the first tile, t[1] of the second.
-__device__ __forceinline__ void load_tiles16(const bf16s* row32, int g, u32x2 (&t)[2]) {
-  const u32x4 v = *reinterpret_cast<const u32x4*>(row32 + 8 * g);
-#pragma unroll
-  for (int d = 0; d < 2; ++d) {
-    const auto r16 = __builtin_amdgcn_permlane16_swap(v[d], v[2 + d], false, false);
-    const auto r32 = __builtin_amdgcn_permlane32_swap(r16[0], r16[1], false, false);
-    t[0][d] = r32[0];
-    t[1][d] = r32[1];
-  }
-}
-__device__ __forceinline__ f32x4 unpack4(u32x2 v) {
-  return f32x4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xFFFF0000u), __uint_as_float(v.y << 16),
-               __uint_as_float(v.y & 0xFFFF0000u)};
-}
 
 // ---------------------------------------------------------------------------
 // Forward for large H (bf16, H >= 128), the arithmetic of gru_fwd_kernel
