@@ -832,13 +832,22 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
   }
   // Epilogue operands of this wave's tile requested now, in flight across
   // the barriers: h (forward) or the gates of the previous step (reverse).
-  frag_t<S> hf_pre[(GRU && !REV && SPLIT) ? H / 32 : 1];
+  // h as raw 16-byte units in bf16 (features 32kk + 8g.., split at use:
+  // split_tiles16), as fragments in fp32.
+  constexpr bool HRAW = sizeof(S) == 2;
+  frag_t<S> hf_pre[(GRU && !REV && SPLIT && !HRAW) ? H / 32 : 1];
+  u32x4 hraw_pre[(GRU && !REV && SPLIT && HRAW) ? H / 32 : 1];
   GruBwdIn<S, H> gin_pre;
   if constexpr (GRU && SPLIT) {
     const int node = k * B + rw + 16 * tg + q;
     if constexpr (!REV) {
 #pragma unroll
-      for (int kk = 0; kk < H / 32; ++kk) hf_pre[kk] = rowfrag<S>(X + (size_t)node * H, kk, g);
+      for (int kk = 0; kk < H / 32; ++kk) {
+        if constexpr (HRAW)
+          hraw_pre[kk] = *reinterpret_cast<const u32x4*>(X + (size_t)node * H + 32 * kk + 8 * g);
+        else
+          hf_pre[kk] = rowfrag<S>(X + (size_t)node * H, kk, g);
+      }
     } else {
       gin_pre.load(rh_saved, rh_h, node, g);
     }
@@ -931,7 +940,13 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         } else {
           af[0][kk] = pack8<S>(v8);
         }
-        if constexpr (SPLIT) {
+        if constexpr (HRAW) {
+          const u32x4 raw =
+              SPLIT ? hraw_pre[kk] : *reinterpret_cast<const u32x4*>(X + (size_t)node * H + 32 * kk + 8 * g);
+          u32x2 t[2];
+          split_tiles16(raw, t);
+          hf[kk] = __builtin_bit_cast(frag_t<S>, u32x4{t[0][0], t[0][1], t[1][0], t[1][1]});
+        } else if constexpr (SPLIT) {
           hf[kk] = hf_pre[kk];
         } else {
           hf[kk] = rowfrag<S>(X + (size_t)node * H, kk, g);
@@ -958,17 +973,21 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
         }
 #pragma unroll
       for (int c2 = 0; c2 < KS; ++c2) {
-        float rhv[8];
+        float rhv[8], rv[8];
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
           const int f = 32 * c2 + 16 * p + 4 * g;
-          float r[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            r[j] = sigmoidf_(ar[2 * c2 + p][j] + bg[f + j]);
-            rhv[4 * p + j] = r[j] * static_cast<float>(hf[c2][4 * p + j]);
+            rv[4 * p + j] = sigmoidf_(ar[2 * c2 + p][j] + bg[f + j]);
+            rhv[4 * p + j] = rv[4 * p + j] * static_cast<float>(hf[c2][4 * p + j]);
           }
-          store4(saved + (size_t)node * 3 * H + f, r[0], r[1], r[2], r[3]);
+          if constexpr (!HRAW)
+            store4(saved + (size_t)node * 3 * H + f, rv[4 * p], rv[4 * p + 1], rv[4 * p + 2], rv[4 * p + 3]);
+        }
+        if constexpr (HRAW) {   // r of the two tiles as one 16-byte store per lane
+          const u32x4 pr = __builtin_bit_cast(u32x4, pack8<S>(rv));
+          store_tiles16(saved + (size_t)node * 3 * H + 32 * c2, u32x2{pr[0], pr[1]}, u32x2{pr[2], pr[3]}, g);
         }
         rh[c2] = pack8<S>(rhv);
       }
@@ -992,6 +1011,7 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
           mma(az[c], gfrag(1, NC + c, kk), hf[kk]);
           mma(an[c], gfrag(1, 2 * NC + c, kk), rh[kk]);
         }
+      float zk[8], nk[8], ok[8];   // tiles c - 1, c (c odd) for the paired stores
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
         const int f = 16 * c + 4 * g;
@@ -1002,10 +1022,25 @@ __global__ __launch_bounds__(TG * WAVES * kWave) void step_bits_kernel(
           nn[j] = tanhf_(an[c][j] + bg[2 * H + f + j]);
           const float hv = static_cast<float>(hf[c / 2][4 * (c % 2) + j]);
           o[j] = z[j] * hv + (1.f - z[j]) * nn[j];
+          zk[4 * (c % 2) + j] = z[j];
+          nk[4 * (c % 2) + j] = nn[j];
+          ok[4 * (c % 2) + j] = o[j];
         }
-        store4(h_out + (size_t)node * H + f, o[0], o[1], o[2], o[3]);
-        store4(saved + (size_t)node * 3 * H + H + f, z[0], z[1], z[2], z[3]);
-        store4(saved + (size_t)node * 3 * H + 2 * H + f, nn[0], nn[1], nn[2], nn[3]);
+        if constexpr (HRAW) {
+          if (c % 2 == 1) {   // h', z, n of tiles c - 1, c as 16-byte stores
+            const u32x4 po = __builtin_bit_cast(u32x4, pack8<S>(ok)), pz = __builtin_bit_cast(u32x4, pack8<S>(zk)),
+                        pn = __builtin_bit_cast(u32x4, pack8<S>(nk));
+            store_tiles16(h_out + (size_t)node * H + 32 * (c / 2), u32x2{po[0], po[1]}, u32x2{po[2], po[3]}, g);
+            store_tiles16(saved + (size_t)node * 3 * H + H + 32 * (c / 2), u32x2{pz[0], pz[1]}, u32x2{pz[2], pz[3]},
+                          g);
+            store_tiles16(saved + (size_t)node * 3 * H + 2 * H + 32 * (c / 2), u32x2{pn[0], pn[1]},
+                          u32x2{pn[2], pn[3]}, g);
+          }
+        } else {
+          store4(h_out + (size_t)node * H + f, o[0], o[1], o[2], o[3]);
+          store4(saved + (size_t)node * 3 * H + H + f, z[0], z[1], z[2], z[3]);
+          store4(saved + (size_t)node * 3 * H + 2 * H + f, nn[0], nn[1], nn[2], nn[3]);
+        }
       }
     }
   }
