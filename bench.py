@@ -64,11 +64,12 @@ KERNELS = {
     "step_wide_fwd": (("step_wide_kernel", ", false, false>("), ["banded_wide.hip", "device_common.h"]),
     "step_wide_rev": (("step_wide_kernel", ", true, false>("), ["banded_wide.hip", "device_common.h"]),
     # step_bits_kernel<S, H, B, waves, direct weights, type groups, reverse, GRU, supernodes>
-    "step_bits_gru": (("step_bits_kernel", ", false, true, false>("), ["banded_bits.hip", "device_common.h"]),
+    "step_bits_gru": (("step_bits_kernel", ", false, true, false>("),
+                      ["banded_bits.hip", "device_common.h", "gru_wave.h", "lds_dma.h"]),
     "step_bits_gru_bwd": (("step_bits_kernel", ", true, true, false>("),
-                          ["banded_bits.hip", "device_common.h", "gru_wave.h"]),
-    "banded_step_bits": (("step_bits_kernel", ", false, false, false>("), ["banded_bits.hip", "device_common.h"]),
-    "banded_step_bits_bwd": (("step_bits_kernel", ", true, false, false>("), ["banded_bits.hip", "device_common.h"]),
+                          ["banded_bits.hip", "device_common.h", "gru_wave.h", "lds_dma.h"]),
+    "banded_step_bits": (("step_bits_kernel", ", false, false, false>("), ["banded_bits.hip", "device_common.h", "lds_dma.h"]),
+    "banded_step_bits_bwd": (("step_bits_kernel", ", true, false, false>("), ["banded_bits.hip", "device_common.h", "lds_dma.h"]),
     "banded_propagate": (("banded_fwd_kernel",), ["banded.hip", "device_common.h"]),
     "banded_propagate_bwd": (("banded_bwd_kernel",), ["banded.hip", "device_common.h"]),
 }
