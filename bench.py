@@ -68,8 +68,10 @@ KERNELS = {
                       ["banded_bits.hip", "device_common.h", "gru_wave.h", "lds_dma.h"]),
     "step_bits_gru_bwd": (("step_bits_kernel", ", true, true, false>("),
                           ["banded_bits.hip", "device_common.h", "gru_wave.h", "lds_dma.h"]),
-    "banded_step_bits": (("step_bits_kernel", ", false, false, false>("), ["banded_bits.hip", "device_common.h", "lds_dma.h"]),
-    "banded_step_bits_bwd": (("step_bits_kernel", ", true, false, false>("), ["banded_bits.hip", "device_common.h", "lds_dma.h"]),
+    "banded_step_bits": (("step_bits_kernel", ", false, false, false>("),
+                         ["banded_bits.hip", "device_common.h", "gru_wave.h", "lds_dma.h"]),
+    "banded_step_bits_bwd": (("step_bits_kernel", ", true, false, false>("),
+                             ["banded_bits.hip", "device_common.h", "gru_wave.h", "lds_dma.h"]),
     "banded_propagate": (("banded_fwd_kernel",), ["banded.hip", "device_common.h"]),
     "banded_propagate_bwd": (("banded_bwd_kernel",), ["banded.hip", "device_common.h"]),
 }
