@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define GGNN_ABI_VERSION 11
+#define GGNN_ABI_VERSION 12
 
 typedef enum {
   GGNN_OK = 0,
@@ -104,6 +104,27 @@ ggnn_status ggnn_rcm_order(int32_t n, int64_t m, const int32_t* src, const int32
  * Errors: ids or rank values out of range, NULL pointers -> INVALID_ARG. */
 ggnn_status ggnn_bandwidth(int32_t n, int64_t m, const int32_t* src, const int32_t* dst,
                            const int32_t* rank, int32_t* bandwidth);
+
+/* Sparse batching (Background section: a batch of graphs is one graph whose
+ * connected components are the batch's graphs): the graphs' nodes are placed
+ * one after another, graph i at supergraph ids offsets[i] .. offsets[i+1]-1,
+ * each graph's nodes first reordered with reverse Cuthill-McKee (exactly as
+ * ggnn_rcm_order does for that graph alone) when reorder is 1, or kept in
+ * their order when 0.  Edges keep their order (so per-edge arrays such as
+ * the edge types carry over unchanged).
+ *   n_graphs     number of graphs (>= 0)
+ *   node_counts  [n_graphs] nodes of each graph (>= 0; at most 2^31 - 1 in all)
+ *   edge_counts  [n_graphs] edges of each graph (>= 0)
+ *   src, dst     [sum edge_counts] the graphs' edges one graph after another, ids local to their graph
+ *   out_src, out_dst [sum edge_counts] out: the same edges in supergraph ids (may not alias src, dst)
+ *   offsets      [n_graphs + 1] out: first supergraph id of each graph; offsets[n_graphs] = all nodes
+ *   bandwidth    out: the largest bandwidth of a graph after the reordering (the supergraph's, as
+ *                no edge joins two graphs)
+ * Host memory only.  Errors: INVALID_ARG for negative counts, NULL arrays, too many nodes or ids out of
+ * range (the message names the graph); HOST_ALLOC if temporaries cannot be allocated. */
+ggnn_status ggnn_batch_graphs(int32_t n_graphs, const int32_t* node_counts, const int64_t* edge_counts,
+                              const int32_t* src, const int32_t* dst, int32_t reorder, int32_t* out_src,
+                              int32_t* out_dst, int64_t* offsets, int32_t* bandwidth);
 
 /* Bytes of a block band: E * (n_pad / B) * 3 * B * B elements of dtype dt.
  * Returns 0 for invalid arguments. */

@@ -28,7 +28,7 @@ STATUS = {0: "GGNN_OK", 1: "GGNN_ERR_INVALID_ARG", 2: "GGNN_ERR_UNSUPPORTED", 3:
 
 EXPORTS = [
     "ggnn_abi_version", "ggnn_last_error", "ggnn_status_string",
-    "ggnn_rcm_order", "ggnn_bandwidth", "ggnn_band_bytes", "ggnn_banded_pack",
+    "ggnn_rcm_order", "ggnn_bandwidth", "ggnn_batch_graphs", "ggnn_band_bytes", "ggnn_banded_pack",
     "ggnn_band_bits_bytes", "ggnn_banded_pack_bits", "ggnn_banded_step_bits", "ggnn_banded_propagate_bits_bwd",
     "ggnn_banded_step_bits_bwd", "ggnn_step_bits_gru", "ggnn_step_bits_gru_bwd", "ggnn_transpose_weights",
     "ggnn_gru_pack_bytes", "ggnn_gru_pack_weights",
@@ -83,6 +83,7 @@ _SIGS = {
     "ggnn_status_string": (C.c_char_p, [C.c_int]),
     "ggnn_rcm_order": (C.c_int, [i32, i64, vp, vp, vp, vp, vp]),
     "ggnn_bandwidth": (C.c_int, [i32, i64, vp, vp, vp, vp]),
+    "ggnn_batch_graphs": (C.c_int, [i32, vp, vp, vp, vp, i32, vp, vp, vp, vp]),
     "ggnn_band_bytes": (sz, [i32, i32, i32, C.c_int]),
     "ggnn_banded_pack": (C.c_int, [i32, i32, i32, i64, vp, vp, vp, vp, C.c_int, C.c_int, vp, vp, vp, vp]),
     "ggnn_band_bits_bytes": (sz, [i32, i32, i32]),
@@ -182,7 +183,7 @@ def _i32(a) -> np.ndarray:
 
 # Interface version this binding is written against (GGNN_ABI_VERSION of
 # include/ggnn.h); the library must report the same number.
-ABI_VERSION = 11
+ABI_VERSION = 12
 
 
 def ggnn_abi_version() -> int:
@@ -214,6 +215,22 @@ def ggnn_bandwidth(n: int, src, dst, rank=None) -> int:
     bw = C.c_int32(0)
     _check("ggnn_bandwidth", lib().ggnn_bandwidth(n, len(src), _ptr(src), _ptr(dst), _ptr(rk), C.addressof(bw)))
     return int(bw.value)
+
+
+def ggnn_batch_graphs(node_counts, edge_counts, src, dst, reorder: bool = True):
+    """Returns (src, dst, offsets, bandwidth): the edges in supergraph ids
+    (int32 arrays), the int64 offsets [n_graphs + 1] and the largest
+    bandwidth of a graph."""
+    nc = _i32(node_counts)
+    ec = np.ascontiguousarray(edge_counts, dtype=np.int64)
+    src, dst = _i32(src), _i32(dst)
+    out_s, out_d = np.empty_like(src), np.empty_like(dst)
+    offs = np.empty(len(nc) + 1, np.int64)
+    bw = C.c_int32(0)
+    _check("ggnn_batch_graphs", lib().ggnn_batch_graphs(len(nc), _ptr(nc), _ptr(ec), _ptr(src), _ptr(dst),
+                                                        1 if reorder else 0, _ptr(out_s), _ptr(out_d), _ptr(offs),
+                                                        C.addressof(bw)))
+    return out_s, out_d, offs, int(bw.value)
 
 
 def ggnn_band_bytes(n_pad: int, E: int, B: int, dt) -> int:

@@ -214,6 +214,62 @@ ggnn_status ggnn_rcm_order(int32_t n, int64_t m, const int32_t* src, const int32
   return GGNN_OK;
 }
 
+ggnn_status ggnn_batch_graphs(int32_t n_graphs, const int32_t* node_counts, const int64_t* edge_counts,
+                              const int32_t* src, const int32_t* dst, int32_t reorder, int32_t* out_src,
+                              int32_t* out_dst, int64_t* offsets, int32_t* bandwidth) {
+  clear_error();
+  GGNN_CHECK_ARG(n_graphs >= 0, "n_graphs=%d must be >= 0", n_graphs);
+  GGNN_CHECK_ARG(reorder == 0 || reorder == 1, "reorder=%d must be 0 or 1", reorder);
+  GGNN_CHECK_ARG(offsets != nullptr && bandwidth != nullptr, "offsets/bandwidth is NULL");
+  GGNN_CHECK_ARG(n_graphs == 0 || (node_counts && edge_counts), "node_counts/edge_counts is NULL");
+  int64_t total_n = 0, total_m = 0;
+  for (int32_t i = 0; i < n_graphs; ++i) {
+    GGNN_CHECK_ARG(node_counts[i] >= 0 && edge_counts[i] >= 0, "graph %d: node count %d, edge count %lld must be >= 0",
+                   i, node_counts[i], (long long)edge_counts[i]);
+    total_n += node_counts[i];
+    total_m += edge_counts[i];
+    GGNN_CHECK_ARG(total_n < ((int64_t)1 << 31), "more than 2^31 - 1 nodes in all");
+  }
+  GGNN_CHECK_ARG(total_m == 0 || (src && dst && out_src && out_dst), "src/dst/out_src/out_dst is NULL");
+  offsets[0] = 0;
+  int32_t bw = 0;
+  int64_t e0 = 0;
+  try {
+    std::vector<int32_t> order, rank;
+    for (int32_t i = 0; i < n_graphs; ++i) {
+      const int32_t n = node_counts[i];
+      const int64_t m = edge_counts[i];
+      const int32_t* s = src + e0;
+      const int32_t* d = dst + e0;
+      const int32_t off = (int32_t)offsets[i];
+      int32_t b = 0;
+      ggnn_status st;
+      if (reorder) {
+        order.resize(n);
+        rank.resize(n);
+        st = ggnn_rcm_order(n, m, s, d, order.data(), rank.data(), &b);
+      } else {
+        st = ggnn_bandwidth(n, m, s, d, nullptr, &b);
+      }
+      if (st != GGNN_OK) {
+        const std::string why = g_last_error;
+        return fail(st, "graph %d: %s", i, why.c_str());
+      }
+      for (int64_t k = 0; k < m; ++k) {
+        out_src[e0 + k] = (reorder ? rank[s[k]] : s[k]) + off;
+        out_dst[e0 + k] = (reorder ? rank[d[k]] : d[k]) + off;
+      }
+      bw = std::max(bw, b);
+      offsets[i + 1] = offsets[i] + n;
+      e0 += m;
+    }
+  } catch (const std::bad_alloc&) {
+    return fail(GGNN_ERR_HOST_ALLOC, "temporary allocation failed (%d graphs)", n_graphs);
+  }
+  *bandwidth = bw;
+  return GGNN_OK;
+}
+
 size_t ggnn_band_bytes(int32_t n_pad, int32_t E, int32_t B, ggnn_dtype dt) {
   if (n_pad <= 0 || E <= 0 || B <= 0 || n_pad % B != 0 || !supported_dtype(dt)) return 0;
   size_t nb = static_cast<size_t>(n_pad / B);

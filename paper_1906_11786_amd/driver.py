@@ -34,28 +34,18 @@ class Compiled:
 
 
 def compile_graphs(graphs: Sequence, B: int, E: int, reorder: bool = True) -> Compiled:
-    """Reorder every graph with reverse Cuthill-McKee (ggnn_rcm_order), then
-    place the graphs one after another (disjoint components of one
-    supergraph) and pad to a multiple of B."""
+    """Reorder every graph with reverse Cuthill-McKee, place the graphs one
+    after another (disjoint components of one supergraph; both in the host
+    library's ggnn_batch_graphs) and pad to a multiple of B."""
     t0 = time.perf_counter()
-    S, D, T, offs = [], [], [], [0]
-    bw = 0
-    for g in graphs:
-        if reorder:
-            _, rank, b = capi.ggnn_rcm_order(g.n, g.src, g.dst)
-            s, d = rank[g.src], rank[g.dst]
-        else:
-            s, d = g.src, g.dst
-            b = capi.ggnn_bandwidth(g.n, s, d)
-        bw = max(bw, b)
-        S.append(s.astype(np.int32) + offs[-1])
-        D.append(d.astype(np.int32) + offs[-1])
-        T.append(g.etype.astype(np.int32))
-        offs.append(offs[-1] + g.n)
-    n_real = offs[-1]
+    cat = (lambda xs: np.concatenate(xs) if xs else np.zeros(0, np.int32))
+    src, dst, offs, bw = capi.ggnn_batch_graphs([g.n for g in graphs], [len(g.src) for g in graphs],
+                                                cat([g.src for g in graphs]), cat([g.dst for g in graphs]),
+                                                reorder=reorder)
+    etype = cat([np.asarray(g.etype, np.int32) for g in graphs]).astype(np.int32)
+    n_real = int(offs[-1])
     n_pad = -(-n_real // B) * B
-    return Compiled(n_real, n_pad, B, E, np.concatenate(S), np.concatenate(D), np.concatenate(T),
-                    np.asarray(offs, np.int64), bw, time.perf_counter() - t0)
+    return Compiled(n_real, n_pad, B, E, src, dst, etype, offs, bw, time.perf_counter() - t0)
 
 
 def dropped_edges(graphs: Sequence, B: int, E: int, reorder: bool = True) -> dict:

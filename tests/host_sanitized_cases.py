@@ -27,7 +27,7 @@ from paper_1906_11786_amd import capi  # noqa: E402
 
 HOST_FUNCS = ["ggnn_abi_version", "ggnn_last_error", "ggnn_status_string", "ggnn_rcm_order", "ggnn_bandwidth",
               "ggnn_band_bytes", "ggnn_banded_pack", "ggnn_band_bits_bytes", "ggnn_banded_pack_bits",
-              "ggnn_sparse_csr", "ggnn_super_bytes", "ggnn_super_pack"]
+              "ggnn_sparse_csr", "ggnn_super_bytes", "ggnn_super_pack", "ggnn_batch_graphs"]
 
 
 def bind(path):
@@ -84,6 +84,39 @@ def check_rcm():
     expect_error(capi.ggnn_rcm_order, 3, [0, -1], [1, 2])
     expect_error(capi.ggnn_bandwidth, 4, [0, 1], [1, 4])
     expect_error(capi.ggnn_bandwidth, 4, [0, 1], [1, 2], rank=[0, 1, 2, 4])
+
+
+def batch_expected(gs, reorder):
+    """Supergraph edges, offsets and bandwidth from the oracle's RCM, one
+    graph at a time."""
+    S, D, offs, bw = [], [], [0], 0
+    for g in gs:
+        if reorder:
+            s, d = O.relabel(O.rcm_order(g.n, g.src, g.dst)[1], g.src, g.dst)
+        else:
+            s, d = g.src, g.dst
+        bw = max(bw, O.bandwidth(s, d) if len(s) else 0)
+        S.append(np.asarray(s, np.int64) + offs[-1])
+        D.append(np.asarray(d, np.int64) + offs[-1])
+        offs.append(offs[-1] + g.n)
+    cat = (lambda xs: np.concatenate(xs) if xs else np.zeros(0, np.int64))
+    return cat(S), cat(D), np.asarray(offs, np.int64), bw
+
+
+def check_batch():
+    gs = graphs()
+    for reorder in (True, False):
+        for sel in (gs, gs[::-1], gs[2:4], []):
+            cat = (lambda xs: np.concatenate(xs) if xs else np.zeros(0, np.int32))
+            s, d, offs, bw = capi.ggnn_batch_graphs([g.n for g in sel], [len(g.src) for g in sel],
+                                                    cat([g.src for g in sel]), cat([g.dst for g in sel]),
+                                                    reorder=reorder)
+            es, ed, eo, ebw = batch_expected(sel, reorder)
+            assert np.array_equal(s, es) and np.array_equal(d, ed) and np.array_equal(offs, eo) and bw == ebw
+    expect_error(capi.ggnn_batch_graphs, [3, 4], [1, 1], [0, 1], [2, 4])     # graph 1: id 4 of 4 nodes
+    expect_error(capi.ggnn_batch_graphs, [3, -1], [1, 0], [0], [2])
+    expect_error(capi.ggnn_batch_graphs, [3], [-1], [], [])
+    expect_error(capi.ggnn_batch_graphs, [3, 4], [1, 1], [0, -1], [2, 1], reorder=False)
 
 
 def full_band(n, E, B, rng):
@@ -208,7 +241,7 @@ if __name__ == "__main__":
     assert sanitizer_loaded(), "the address / undefined-behaviour sanitizer runtimes are not loaded"
     assert capi.ggnn_abi_version() == capi.ABI_VERSION
     assert capi.ggnn_status_string(3) == "GGNN_ERR_OUT_OF_BAND"
-    for step in (check_rcm, check_pack, check_csr, check_super):
+    for step in (check_rcm, check_batch, check_pack, check_csr, check_super):
         step()
         print(f"{step.__name__} ok", flush=True)
     print("ALL OK", flush=True)

@@ -71,6 +71,19 @@ def test_rcm_bit_exact_against_oracle():
         assert capi.ggnn_bandwidth(g.n, g.src, g.dst) == O.bandwidth(g.src, g.dst)
 
 
+def test_batch_graphs_against_oracle_rcm_per_graph():
+    """Sparse batching in the host library: each graph reordered alone and
+    offset by the nodes before it, edges in order (oracle RCM per graph)."""
+    _need_lib()
+    from host_sanitized_cases import check_batch
+    check_batch()
+    # the composition the driver builds on: the program-graph batch keeps every graph's bandwidth below B
+    gs = make_graphs(PROGRAM_GRAPH)
+    s, d, offs, bw = capi.ggnn_batch_graphs([g.n for g in gs], [len(g.src) for g in gs],
+                                            np.concatenate([g.src for g in gs]), np.concatenate([g.dst for g in gs]))
+    assert offs[-1] == sum(g.n for g in gs) and bw == int(np.abs(s.astype(np.int64) - d).max()) <= PROGRAM_GRAPH.B - 1
+
+
 def test_rcm_bit_exact_on_program_graph_workload():
     _need_lib()
     g = make_graphs(PROGRAM_GRAPH)[0]
