@@ -126,6 +126,25 @@ ggnn_status ggnn_batch_graphs(int32_t n_graphs, const int32_t* node_counts, cons
                               const int32_t* src, const int32_t* dst, int32_t reorder, int32_t* out_src,
                               int32_t* out_dst, int64_t* offsets, int32_t* bandwidth);
 
+/* The same batching with supernodes (Discussion section): the listed hub
+ * nodes of every graph take the first labels, 0 .. (all hubs - 1) < s, graph
+ * after graph in list order; each graph's other nodes are reordered with
+ * reverse Cuthill-McKee on the edges between them (the band's share; as
+ * ggnn_rcm_order on those nodes in their label order) and placed from
+ * label s on, graph after graph.
+ *   hub_counts   [n_graphs] hubs of each graph (0 .. node count)
+ *   hubs         [sum hub_counts] each graph's hubs, ids local to the graph, distinct within it
+ *   s            supernode slots (>= all hubs)
+ *   n_nodes      out: s + the non-hub nodes of all graphs (the labels used)
+ *   bandwidth    out: the largest bandwidth of a graph's non-hub part after the reordering
+ *   the other arguments as ggnn_batch_graphs (no offsets: hubs and graphs interleave)
+ * Host memory only.  Errors: INVALID_ARG for negative counts, NULL arrays, more hubs than s, repeated or
+ * out-of-range hubs or ids (the message names the graph); HOST_ALLOC if temporaries cannot be allocated. */
+ggnn_status ggnn_batch_graphs_super(int32_t n_graphs, const int32_t* node_counts, const int64_t* edge_counts,
+                                    const int32_t* src, const int32_t* dst, const int32_t* hub_counts,
+                                    const int32_t* hubs, int32_t s, int32_t* out_src, int32_t* out_dst,
+                                    int32_t* n_nodes, int32_t* bandwidth);
+
 /* Bytes of a block band: E * (n_pad / B) * 3 * B * B elements of dtype dt.
  * Returns 0 for invalid arguments. */
 size_t ggnn_band_bytes(int32_t n_pad, int32_t E, int32_t B, ggnn_dtype dt);

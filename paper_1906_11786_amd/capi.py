@@ -28,7 +28,7 @@ STATUS = {0: "GGNN_OK", 1: "GGNN_ERR_INVALID_ARG", 2: "GGNN_ERR_UNSUPPORTED", 3:
 
 EXPORTS = [
     "ggnn_abi_version", "ggnn_last_error", "ggnn_status_string",
-    "ggnn_rcm_order", "ggnn_bandwidth", "ggnn_batch_graphs", "ggnn_band_bytes", "ggnn_banded_pack",
+    "ggnn_rcm_order", "ggnn_bandwidth", "ggnn_batch_graphs", "ggnn_batch_graphs_super", "ggnn_band_bytes", "ggnn_banded_pack",
     "ggnn_band_bits_bytes", "ggnn_banded_pack_bits", "ggnn_banded_step_bits", "ggnn_banded_propagate_bits_bwd",
     "ggnn_banded_step_bits_bwd", "ggnn_step_bits_gru", "ggnn_step_bits_gru_bwd", "ggnn_transpose_weights",
     "ggnn_gru_pack_bytes", "ggnn_gru_pack_weights",
@@ -84,6 +84,7 @@ _SIGS = {
     "ggnn_rcm_order": (C.c_int, [i32, i64, vp, vp, vp, vp, vp]),
     "ggnn_bandwidth": (C.c_int, [i32, i64, vp, vp, vp, vp]),
     "ggnn_batch_graphs": (C.c_int, [i32, vp, vp, vp, vp, i32, vp, vp, vp, vp]),
+    "ggnn_batch_graphs_super": (C.c_int, [i32, vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp]),
     "ggnn_band_bytes": (sz, [i32, i32, i32, C.c_int]),
     "ggnn_banded_pack": (C.c_int, [i32, i32, i32, i64, vp, vp, vp, vp, C.c_int, C.c_int, vp, vp, vp, vp]),
     "ggnn_band_bits_bytes": (sz, [i32, i32, i32]),
@@ -231,6 +232,21 @@ def ggnn_batch_graphs(node_counts, edge_counts, src, dst, reorder: bool = True):
                                                         1 if reorder else 0, _ptr(out_s), _ptr(out_d), _ptr(offs),
                                                         C.addressof(bw)))
     return out_s, out_d, offs, int(bw.value)
+
+
+def ggnn_batch_graphs_super(node_counts, edge_counts, src, dst, hub_counts, hubs, s: int):
+    """Returns (src, dst, n_nodes, bandwidth): the edges in supergraph ids
+    (int32 arrays), the labels used (s + non-hub nodes) and the largest
+    bandwidth of a graph's non-hub part."""
+    nc, hc = _i32(node_counts), _i32(hub_counts)
+    ec = np.ascontiguousarray(edge_counts, dtype=np.int64)
+    src, dst, hb = _i32(src), _i32(dst), _i32(hubs)
+    out_s, out_d = np.empty_like(src), np.empty_like(dst)
+    nn, bw = C.c_int32(0), C.c_int32(0)
+    _check("ggnn_batch_graphs_super",
+           lib().ggnn_batch_graphs_super(len(nc), _ptr(nc), _ptr(ec), _ptr(src), _ptr(dst), _ptr(hc), _ptr(hb), s,
+                                         _ptr(out_s), _ptr(out_d), C.addressof(nn), C.addressof(bw)))
+    return out_s, out_d, int(nn.value), int(bw.value)
 
 
 def ggnn_band_bytes(n_pad: int, E: int, B: int, dt) -> int:

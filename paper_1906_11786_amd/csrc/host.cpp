@@ -270,6 +270,85 @@ ggnn_status ggnn_batch_graphs(int32_t n_graphs, const int32_t* node_counts, cons
   return GGNN_OK;
 }
 
+ggnn_status ggnn_batch_graphs_super(int32_t n_graphs, const int32_t* node_counts, const int64_t* edge_counts,
+                                    const int32_t* src, const int32_t* dst, const int32_t* hub_counts,
+                                    const int32_t* hubs, int32_t s, int32_t* out_src, int32_t* out_dst,
+                                    int32_t* n_nodes, int32_t* bandwidth) {
+  clear_error();
+  GGNN_CHECK_ARG(n_graphs >= 0 && s >= 0, "n_graphs=%d and s=%d must be >= 0", n_graphs, s);
+  GGNN_CHECK_ARG(n_nodes != nullptr && bandwidth != nullptr, "n_nodes/bandwidth is NULL");
+  GGNN_CHECK_ARG(n_graphs == 0 || (node_counts && edge_counts && hub_counts), "node/edge/hub counts are NULL");
+  int64_t total_n = s, total_m = 0, total_h = 0;
+  for (int32_t i = 0; i < n_graphs; ++i) {
+    GGNN_CHECK_ARG(node_counts[i] >= 0 && edge_counts[i] >= 0 && hub_counts[i] >= 0 && hub_counts[i] <= node_counts[i],
+                   "graph %d: node count %d, edge count %lld, hub count %d out of range", i, node_counts[i],
+                   (long long)edge_counts[i], hub_counts[i]);
+    total_n += node_counts[i] - hub_counts[i];
+    total_m += edge_counts[i];
+    total_h += hub_counts[i];
+    GGNN_CHECK_ARG(total_n < ((int64_t)1 << 31), "more than 2^31 - 1 nodes in all");
+  }
+  GGNN_CHECK_ARG(total_h <= s, "%lld hubs do not fit in s=%d supernode slots", (long long)total_h, s);
+  GGNN_CHECK_ARG(total_h == 0 || hubs, "hubs is NULL");
+  GGNN_CHECK_ARG(total_m == 0 || (src && dst && out_src && out_dst), "src/dst/out_src/out_dst is NULL");
+  int32_t bw = 0, next_hub = 0, base = s;
+  int64_t e0 = 0, h0 = 0;
+  try {
+    std::vector<int32_t> label, local, is, id, order, rank;
+    for (int32_t i = 0; i < n_graphs; ++i) {
+      const int32_t n = node_counts[i];
+      const int64_t m = edge_counts[i];
+      const int32_t* gs = src + e0;
+      const int32_t* gd = dst + e0;
+      label.assign(n, -1);
+      for (int32_t j = 0; j < hub_counts[i]; ++j) {
+        const int32_t v = hubs[h0 + j];
+        GGNN_CHECK_ARG(v >= 0 && v < n && label[v] < 0, "graph %d: hub %d is out of range [0,%d) or repeated", i, v,
+                       n);
+        label[v] = next_hub++;
+      }
+      for (int64_t k = 0; k < m; ++k)
+        GGNN_CHECK_ARG(gs[k] >= 0 && gs[k] < n && gd[k] >= 0 && gd[k] < n,
+                       "graph %d: edge %lld (%d -> %d) out of range [0,%d)", i, (long long)k, gs[k], gd[k], n);
+      // the other nodes, in label order, and the edges between them (the band's share)
+      local.assign(n, -1);
+      int32_t nr = 0;
+      for (int32_t v = 0; v < n; ++v)
+        if (label[v] < 0) local[v] = nr++;
+      is.clear();
+      id.clear();
+      for (int64_t k = 0; k < m; ++k)
+        if (label[gs[k]] < 0 && label[gd[k]] < 0) {
+          is.push_back(local[gs[k]]);
+          id.push_back(local[gd[k]]);
+        }
+      order.resize(nr);
+      rank.resize(nr);
+      int32_t b = 0;
+      const ggnn_status st = ggnn_rcm_order(nr, (int64_t)is.size(), is.data(), id.data(), order.data(), rank.data(), &b);
+      if (st != GGNN_OK) {
+        const std::string why = g_last_error;
+        return fail(st, "graph %d: %s", i, why.c_str());
+      }
+      for (int32_t v = 0; v < n; ++v)
+        if (label[v] < 0) label[v] = base + rank[local[v]];
+      for (int64_t k = 0; k < m; ++k) {
+        out_src[e0 + k] = label[gs[k]];
+        out_dst[e0 + k] = label[gd[k]];
+      }
+      bw = std::max(bw, b);
+      base += nr;
+      e0 += m;
+      h0 += hub_counts[i];
+    }
+  } catch (const std::bad_alloc&) {
+    return fail(GGNN_ERR_HOST_ALLOC, "temporary allocation failed (%d graphs)", n_graphs);
+  }
+  *n_nodes = base;
+  *bandwidth = bw;
+  return GGNN_OK;
+}
+
 size_t ggnn_band_bytes(int32_t n_pad, int32_t E, int32_t B, ggnn_dtype dt) {
   if (n_pad <= 0 || E <= 0 || B <= 0 || n_pad % B != 0 || !supported_dtype(dt)) return 0;
   size_t nb = static_cast<size_t>(n_pad / B);

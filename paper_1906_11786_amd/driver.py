@@ -372,34 +372,20 @@ def compile_with_supernodes(graphs: Sequence, hubs: Sequence, B: int, E: int, s:
     of every graph (hubs[g], ids in graph g's labels) take the first labels
     0 .. (total hubs - 1) < s; the other nodes of each graph are reordered with
     reverse Cuthill-McKee on the edges between them (the band's share) and
-    placed after s, graph after graph.  n_pad is a multiple of B and of 64."""
+    placed after s, graph after graph (both in the host library's
+    ggnn_batch_graphs_super).  n_pad is a multiple of B and of 64."""
     t0 = time.perf_counter()
     n_h = sum(len(h) for h in hubs)
     if n_h > s:
         raise ValueError(f"{n_h} hubs do not fit in s={s} supernode slots")
-    S, D, T = [], [], []
-    next_hub, base, bw = 0, s, 0
-    for g, hg in zip(graphs, hubs):
-        label = np.full(g.n, -1, np.int64)
-        hg = np.asarray(hg, np.int64)
-        label[hg] = np.arange(next_hub, next_hub + len(hg))
-        next_hub += len(hg)
-        rest = np.flatnonzero(label < 0)
-        local = np.full(g.n, -1, np.int64)
-        local[rest] = np.arange(len(rest))
-        inner = (label[g.src] < 0) & (label[g.dst] < 0)
-        ls, ld = local[g.src[inner]], local[g.dst[inner]]
-        _, rank, b = capi.ggnn_rcm_order(len(rest), ls, ld)
-        bw = max(bw, b)
-        label[rest] = base + rank
-        base += len(rest)
-        S.append(label[g.src].astype(np.int32))
-        D.append(label[g.dst].astype(np.int32))
-        T.append(g.etype.astype(np.int32))
+    cat = (lambda xs: np.concatenate(xs) if xs else np.zeros(0, np.int32))
+    src, dst, base, bw = capi.ggnn_batch_graphs_super(
+        [g.n for g in graphs], [len(g.src) for g in graphs], cat([g.src for g in graphs]),
+        cat([g.dst for g in graphs]), [len(h) for h in hubs], cat([np.asarray(h, np.int32) for h in hubs]), s)
+    etype = cat([np.asarray(g.etype, np.int32) for g in graphs]).astype(np.int32)
     step = B * 64 // np.gcd(B, 64)
     n_pad = -(-base // step) * step
-    comp = Compiled(base, n_pad, B, E, np.concatenate(S), np.concatenate(D), np.concatenate(T),
-                    np.asarray([0, base], np.int64), bw, time.perf_counter() - t0)
+    comp = Compiled(base, n_pad, B, E, src, dst, etype, np.asarray([0, base], np.int64), bw, time.perf_counter() - t0)
     comp.stats["n_super"] = s
     comp.stats["n_hubs"] = n_h
     return comp

@@ -27,7 +27,8 @@ from paper_1906_11786_amd import capi  # noqa: E402
 
 HOST_FUNCS = ["ggnn_abi_version", "ggnn_last_error", "ggnn_status_string", "ggnn_rcm_order", "ggnn_bandwidth",
               "ggnn_band_bytes", "ggnn_banded_pack", "ggnn_band_bits_bytes", "ggnn_banded_pack_bits",
-              "ggnn_sparse_csr", "ggnn_super_bytes", "ggnn_super_pack", "ggnn_batch_graphs"]
+              "ggnn_sparse_csr", "ggnn_super_bytes", "ggnn_super_pack", "ggnn_batch_graphs",
+              "ggnn_batch_graphs_super"]
 
 
 def bind(path):
@@ -117,6 +118,45 @@ def check_batch():
     expect_error(capi.ggnn_batch_graphs, [3, -1], [1, 0], [0], [2])
     expect_error(capi.ggnn_batch_graphs, [3], [-1], [], [])
     expect_error(capi.ggnn_batch_graphs, [3, 4], [1, 1], [0, -1], [2, 1], reorder=False)
+
+
+def check_batch_super():
+    """Hubs first (list order, graph after graph), then each graph's other
+    nodes in the oracle's RCM order of the edges between them, from s on."""
+    gs = [g for g in graphs() if g.n >= 5]
+    rng = np.random.default_rng(3)
+    hubs = [np.sort(rng.choice(g.n, size=min(3, g.n - 2), replace=False)).astype(np.int32) for g in gs]
+    hubs[0] = hubs[0][::-1].copy()      # list order, not id order, decides the labels
+    hubs[1] = np.zeros(0, np.int32)     # a graph without hubs
+    s = 32
+    cat = (lambda xs: np.concatenate(xs) if xs else np.zeros(0, np.int32))
+    out_s, out_d, nn, bw = capi.ggnn_batch_graphs_super([g.n for g in gs], [len(g.src) for g in gs],
+                                                       cat([g.src for g in gs]), cat([g.dst for g in gs]),
+                                                       [len(h) for h in hubs], cat(hubs), s)
+    base, nh, ebw, S, D = s, 0, 0, [], []
+    for g, h in zip(gs, hubs):
+        label = np.full(g.n, -1, np.int64)
+        label[h] = np.arange(nh, nh + len(h))
+        nh += len(h)
+        rest = np.flatnonzero(label < 0)
+        local = np.full(g.n, -1, np.int64)
+        local[rest] = np.arange(len(rest))
+        inner = (label[g.src] < 0) & (label[g.dst] < 0)
+        ls, ld = local[g.src[inner]], local[g.dst[inner]]
+        rank = np.asarray(O.rcm_order(len(rest), ls, ld)[1])
+        if inner.any():
+            ebw = max(ebw, O.bandwidth(*O.relabel(rank, ls, ld)))
+        label[rest] = base + rank
+        base += len(rest)
+        S.append(label[g.src])
+        D.append(label[g.dst])
+    assert np.array_equal(out_s, np.concatenate(S)) and np.array_equal(out_d, np.concatenate(D))
+    assert nn == base and bw == ebw
+    expect_error(capi.ggnn_batch_graphs_super, [4], [1], [0], [1], [3], [0, 1, 2], 2)     # 3 hubs, 2 slots
+    expect_error(capi.ggnn_batch_graphs_super, [4], [1], [0], [1], [2], [1, 1], 4)        # repeated hub
+    expect_error(capi.ggnn_batch_graphs_super, [4], [1], [0], [1], [1], [4], 4)           # hub out of range
+    expect_error(capi.ggnn_batch_graphs_super, [4], [1], [0], [5], [1], [0], 4)           # edge out of range
+    expect_error(capi.ggnn_batch_graphs_super, [2], [0], [], [], [3], [0, 1, 0], 4)       # more hubs than nodes
 
 
 def full_band(n, E, B, rng):
@@ -241,7 +281,7 @@ if __name__ == "__main__":
     assert sanitizer_loaded(), "the address / undefined-behaviour sanitizer runtimes are not loaded"
     assert capi.ggnn_abi_version() == capi.ABI_VERSION
     assert capi.ggnn_status_string(3) == "GGNN_ERR_OUT_OF_BAND"
-    for step in (check_rcm, check_batch, check_pack, check_csr, check_super):
+    for step in (check_rcm, check_batch, check_batch_super, check_pack, check_csr, check_super):
         step()
         print(f"{step.__name__} ok", flush=True)
     print("ALL OK", flush=True)

@@ -460,3 +460,5 @@ def test_compile_with_supernodes_matches_oracle_reordering():
         D.append(label[g.dst])
     np.testing.assert_array_equal(comp.src, np.concatenate(S))
     np.testing.assert_array_equal(comp.dst, np.concatenate(D))
+    from host_sanitized_cases import check_batch_super
+    check_batch_super()
